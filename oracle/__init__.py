@@ -1,0 +1,261 @@
+"""CPU oracle for the bitmask-compressed sparse linear layers.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  The GPU library and
+its Python binding never import, load or call it, and the two share no code.
+
+The arithmetic lives in ``spl_oracle.c`` (plain C, binary64, every step
+written out in the paper's order); this module only marshals numpy arrays
+into it.  Paper: arXiv 2405.03594, section 2.4.1 (bitmask expansion and its
+worked example), section 2.4.2 (the GPU variant: compressed submatrices that
+are decompressed before the matrix units use them), section 3.4 (int8
+weights and activations).
+
+Parity pins for every function here are in ``tests/test_oracle.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spl_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+DTYPES = {"f16": 1, "bf16": 2, "i8": 3}
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (binary64, no contraction of products)."""
+    if not force and os.path.exists(_LIB_PATH) and os.path.getmtime(_LIB_PATH) >= os.path.getmtime(_SRC):
+        return _LIB_PATH
+    tmp = _LIB_PATH + f".tmp{os.getpid()}"
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    build(force=False)
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    I64 = ctypes.c_int64
+    I32 = ctypes.c_int32
+    sig = {
+        "orc_words_per_row": (I64, [I64]),
+        "orc_pack_nnz": (I64, [P, I32, P, I64, I64]),
+        "orc_pack": (None, [P, I32, P, I64, I64, P, P, P]),
+        "orc_unpack": (None, [P, P, P, I32, I64, I64, P]),
+        "orc_linear_f64": (None, [P, I64, I64, I32, P, P, P, I64, P, ctypes.c_int]),
+        "orc_linear_f64_pairs": (None, [P, I64, I64, I32, P, P, P, I64, P, P, I64, P, ctypes.c_int]),
+        "orc_dense_f64": (None, [P, I64, I64, I32, P, I64, P, ctypes.c_int]),
+        "orc_linear_i8": (ctypes.c_int, [P, P, I64, I64, P, P, P, P, I64, P, P, ctypes.c_int]),
+        "orc_dense_i8": (ctypes.c_int, [P, P, I64, I64, P, P, I64, P, P, ctypes.c_int]),
+        "orc_f16_to_f64_array": (None, [P, I64, P]),
+        "orc_bf16_to_f64_array": (None, [P, I64, P]),
+        "orc_f32_to_f16_array": (None, [P, I64, P]),
+        "orc_dequant_f16_array": (None, [P, P, P, I64, P]),
+        "orc_max_threads": (ctypes.c_int, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle inputs must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _code(dtype: str) -> int:
+    return DTYPES[dtype]
+
+
+def max_threads() -> int:
+    return int(_load().orc_max_threads())
+
+
+@dataclass
+class Packed:
+    """The canonical encoding (see spl_oracle.c for the exact bit layout)."""
+
+    bitmask: np.ndarray      # uint32 [N][ceil(K/32)]
+    values: np.ndarray       # uint16 (fp16/bf16 payloads) or int8 [nnz]
+    row_offsets: np.ndarray  # int32 [N+1]
+    N: int
+    K: int
+    dtype: str
+
+    @property
+    def nnz(self) -> int:
+        return int(self.row_offsets[-1])
+
+
+def _payload_dtype(dtype: str):
+    return np.int8 if dtype == "i8" else np.uint16
+
+
+def pack(W: np.ndarray, dtype: str, mask: np.ndarray | None = None) -> Packed:
+    """Bitmask expansion encoder (section 2.4.1): naive column-order walk."""
+    lib = _load()
+    W = np.ascontiguousarray(W)
+    assert W.dtype == _payload_dtype(dtype), (W.dtype, dtype)
+    N, K = W.shape
+    if mask is not None:
+        mask = np.ascontiguousarray(mask, dtype=np.uint8)
+        assert mask.shape == W.shape
+    nnz = int(lib.orc_pack_nnz(_ptr(W), _code(dtype), _ptr(mask), N, K))
+    words = int(lib.orc_words_per_row(K))
+    bitmask = np.zeros((N, words), dtype=np.uint32)
+    values = np.zeros(max(nnz, 1), dtype=_payload_dtype(dtype))
+    row_offsets = np.zeros(N + 1, dtype=np.int32)
+    lib.orc_pack(_ptr(W), _code(dtype), _ptr(mask), N, K, _ptr(bitmask), _ptr(values), _ptr(row_offsets))
+    return Packed(bitmask, values[:nnz], row_offsets, N, K, dtype)
+
+
+def unpack(p: Packed) -> np.ndarray:
+    """Decoder: kept positions take their stored payload, the rest +0."""
+    lib = _load()
+    out = np.zeros((p.N, p.K), dtype=_payload_dtype(p.dtype))
+    vals = p.values if p.values.size else np.zeros(1, dtype=_payload_dtype(p.dtype))
+    lib.orc_unpack(_ptr(p.bitmask), _ptr(np.ascontiguousarray(vals)), _ptr(p.row_offsets), _code(p.dtype),
+                   p.N, p.K, _ptr(out))
+    return out
+
+
+def linear_f64(X: np.ndarray, p: Packed, nthreads: int = 0) -> np.ndarray:
+    """Y = X (W.Mask)^T in binary64 from the packed weight; X is [M][K] fp16/bf16 bits."""
+    lib = _load()
+    X = np.ascontiguousarray(X, dtype=np.uint16)
+    M, K = X.shape
+    assert K == p.K and p.dtype in ("f16", "bf16")
+    Y = np.zeros((M, p.N), dtype=np.float64)
+    vals = p.values if p.values.size else np.zeros(1, dtype=np.uint16)
+    lib.orc_linear_f64(_ptr(X), M, K, _code(p.dtype), _ptr(p.bitmask), _ptr(np.ascontiguousarray(vals)),
+                       _ptr(p.row_offsets), p.N, _ptr(Y), nthreads)
+    return Y
+
+
+def linear_f64_pairs(X: np.ndarray, p: Packed, ms: np.ndarray, ns: np.ndarray, nthreads: int = 0) -> np.ndarray:
+    """The same definition at selected output positions (ms[i], ns[i])."""
+    lib = _load()
+    X = np.ascontiguousarray(X, dtype=np.uint16)
+    M, K = X.shape
+    ms = np.ascontiguousarray(ms, dtype=np.int64)
+    ns = np.ascontiguousarray(ns, dtype=np.int64)
+    assert ms.shape == ns.shape
+    assert (ms >= 0).all() and (ms < M).all() and (ns >= 0).all() and (ns < p.N).all()
+    out = np.zeros(ms.shape, dtype=np.float64)
+    vals = p.values if p.values.size else np.zeros(1, dtype=np.uint16)
+    lib.orc_linear_f64_pairs(_ptr(X), M, K, _code(p.dtype), _ptr(p.bitmask), _ptr(np.ascontiguousarray(vals)),
+                             _ptr(p.row_offsets), p.N, _ptr(ms), _ptr(ns), ms.size, _ptr(out), nthreads)
+    return out
+
+
+def dense_f64(X: np.ndarray, W: np.ndarray, dtype: str, nthreads: int = 0) -> np.ndarray:
+    """Plain dense product in binary64: Y = X W^T, W is [N][K]."""
+    lib = _load()
+    X = np.ascontiguousarray(X, dtype=np.uint16)
+    W = np.ascontiguousarray(W, dtype=np.uint16)
+    M, K = X.shape
+    N, K2 = W.shape
+    assert K == K2
+    Y = np.zeros((M, N), dtype=np.float64)
+    lib.orc_dense_f64(_ptr(X), M, K, _code(dtype), _ptr(W), N, _ptr(Y), nthreads)
+    return Y
+
+
+def linear_i8(Xq: np.ndarray, sx: np.ndarray, p: Packed, sw: np.ndarray, nthreads: int = 0):
+    """Sparse-quantized linear (section 3.4): exact int32 accumulators and fp16 outputs (bits)."""
+    lib = _load()
+    Xq = np.ascontiguousarray(Xq, dtype=np.int8)
+    sx = np.ascontiguousarray(sx, dtype=np.float32)
+    sw = np.ascontiguousarray(sw, dtype=np.float32)
+    M, K = Xq.shape
+    assert K == p.K and p.dtype == "i8" and sx.shape == (M,) and sw.shape == (p.N,)
+    acc = np.zeros((M, p.N), dtype=np.int32)
+    Y = np.zeros((M, p.N), dtype=np.uint16)
+    vals = p.values if p.values.size else np.zeros(1, dtype=np.int8)
+    rc = lib.orc_linear_i8(_ptr(Xq), _ptr(sx), M, K, _ptr(p.bitmask), _ptr(np.ascontiguousarray(vals)),
+                           _ptr(p.row_offsets), _ptr(sw), p.N, _ptr(acc), _ptr(Y), nthreads)
+    if rc != 0:
+        raise OverflowError("int8 accumulator outside the int32 range")
+    return acc, Y
+
+
+def dense_i8(Xq: np.ndarray, sx: np.ndarray, Wq: np.ndarray, sw: np.ndarray, nthreads: int = 0):
+    """Dense int8 reference with the same epilogue."""
+    lib = _load()
+    Xq = np.ascontiguousarray(Xq, dtype=np.int8)
+    Wq = np.ascontiguousarray(Wq, dtype=np.int8)
+    sx = np.ascontiguousarray(sx, dtype=np.float32)
+    sw = np.ascontiguousarray(sw, dtype=np.float32)
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    acc = np.zeros((M, N), dtype=np.int32)
+    Y = np.zeros((M, N), dtype=np.uint16)
+    rc = lib.orc_dense_i8(_ptr(Xq), _ptr(sx), M, K, _ptr(Wq), _ptr(sw), N, _ptr(acc), _ptr(Y), nthreads)
+    if rc != 0:
+        raise OverflowError("int8 accumulator outside the int32 range")
+    return acc, Y
+
+
+def f16_to_f64(bits: np.ndarray) -> np.ndarray:
+    lib = _load()
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.zeros(bits.shape, dtype=np.float64)
+    lib.orc_f16_to_f64_array(_ptr(bits), bits.size, _ptr(out))
+    return out
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    lib = _load()
+    bits = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.zeros(bits.shape, dtype=np.float64)
+    lib.orc_bf16_to_f64_array(_ptr(bits), bits.size, _ptr(out))
+    return out
+
+
+def to_f64(bits: np.ndarray, dtype: str) -> np.ndarray:
+    return f16_to_f64(bits) if dtype == "f16" else bf16_to_f64(bits)
+
+
+def f32_to_f16(x: np.ndarray) -> np.ndarray:
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.zeros(x.shape, dtype=np.uint16)
+    lib.orc_f32_to_f16_array(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def dequant_f16(acc: np.ndarray, sx: np.ndarray, sw: np.ndarray) -> np.ndarray:
+    """Element-wise epilogue on broadcast-compatible arrays; returns fp16 bits."""
+    lib = _load()
+    acc, sx, sw = np.broadcast_arrays(np.asarray(acc, np.int32), np.asarray(sx, np.float32), np.asarray(sw, np.float32))
+    acc = np.ascontiguousarray(acc)
+    sx = np.ascontiguousarray(sx)
+    sw = np.ascontiguousarray(sw)
+    out = np.zeros(acc.shape, dtype=np.uint16)
+    lib.orc_dequant_f16_array(_ptr(acc), _ptr(sx), _ptr(sw), acc.size, _ptr(out))
+    return out
+
+
+def tolerance_ok(y: np.ndarray, ref: np.ndarray, abs_tol: float = 2e-2, rel_tol: float = 1e-2) -> np.ndarray:
+    """Per-element acceptance for fp16/bf16 outputs: |y - ref| <= max(abs_tol, rel_tol * |ref|)."""
+    return np.abs(y - ref) <= np.maximum(abs_tol, rel_tol * np.abs(ref))

@@ -1,0 +1,372 @@
+"""Pins of the CPU oracle to things other than itself (no GPU needed).
+
+Each test checks the oracle against something the paper or the mathematics
+fixes: the paper's worked example of bitmask expansion (section 2.4.1), brute
+force over every mask of tiny blocks, format invariants, NumPy/BLAS and
+NumPy's own fp16 conversion, exact-arithmetic inputs and closed forms.  The
+shapes are rectangular (M != N != K) so that a transposed operand, a swapped
+index or a dropped term fails at least one of them.
+"""
+import itertools
+import os
+
+import numpy as np
+import pytest
+
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_example.txt")
+
+
+def _read_golden():
+    d = {}
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            key, rest = line.split(":", 1)
+            d[key.strip()] = rest.split()
+    return d
+
+
+def _payloads(tokens):
+    """Distinct non-zero 16-bit payloads for the symbolic entries; 0 stays 0."""
+    names = sorted({t for t in tokens if t != "0"})
+    table = {n: 0x1000 + 37 * i for i, n in enumerate(names)}
+    table["0"] = 0
+    return table
+
+
+def _bits_lsb_first(word, n):
+    return "".join("1" if (int(word) >> j) & 1 else "0" for j in range(n))
+
+
+# ------------------------------------------------------------ worked example
+
+def test_worked_example_register_is_vnni_interleave():
+    g = _read_golden()
+    a, b, reg = g["rowA"], g["rowB"], g["register"]
+    assert len(a) == len(b) == 8 and len(reg) == 16
+    # VNNI pairs the two rows along the reduction dimension: A1 B1 A2 B2 ...
+    assert reg == [t for pair in zip(a, b) for t in pair]
+
+
+def test_worked_example_pack(orc):
+    g = _read_golden()
+    reg = g["register"]
+    table = _payloads(reg)
+    W = np.array([[table[t] for t in reg]], dtype=np.uint16)
+    mask = (W != 0).astype(np.uint8)
+    p = orc.pack(W, "f16", mask)
+    assert p.values.tolist() == [table[t] for t in g["values"]]
+    assert _bits_lsb_first(p.bitmask[0, 0], 16) == g["bitmask"][0]
+    assert p.bitmask.shape == (1, 1) and int(p.bitmask[0, 0]) == 0xE94E
+    assert p.row_offsets.tolist() == [0, 9]
+    assert np.array_equal(orc.unpack(p), W)
+
+
+def test_worked_example_row_major(orc):
+    g = _read_golden()
+    table = _payloads(g["rowA"] + g["rowB"])
+    W = np.array([[table[t] for t in g["rowA"]], [table[t] for t in g["rowB"]]], dtype=np.uint16)
+    p = orc.pack(W, "f16", (W != 0).astype(np.uint8))
+    kept_a = [j for j in range(8) if (int(p.bitmask[0, 0]) >> j) & 1]
+    kept_b = [j for j in range(8) if (int(p.bitmask[1, 0]) >> j) & 1]
+    assert kept_a == [1, 3, 4, 7] and kept_b == [0, 1, 5, 6, 7]
+    assert p.values.tolist() == [table[t] for t in ["A2", "A4", "A5", "A8", "B1", "B2", "B6", "B7", "B8"]]
+    assert p.row_offsets.tolist() == [0, 4, 9]
+
+
+# ------------------------------------------------------------ brute force
+
+def _check_pack_against_numpy(orc, W, mask, dtype):
+    p = orc.pack(W, dtype, mask)
+    N, K = W.shape
+    m = mask.astype(bool)
+    # row offsets: exclusive prefix of per-row kept counts
+    assert p.row_offsets[0] == 0
+    assert np.array_equal(np.diff(p.row_offsets.astype(np.int64)), m.sum(axis=1))
+    # bitmask: bit (k % 32) of word k // 32, everything past K zero
+    words = (K + 31) // 32
+    pad = np.zeros((N, words * 32), dtype=bool)
+    pad[:, :K] = m
+    expect = np.zeros((N, words), dtype=np.uint64)
+    for j in range(32):
+        expect |= pad[:, j::32].astype(np.uint64) << np.uint64(j)
+    assert np.array_equal(p.bitmask.astype(np.uint64), expect)
+    # values: kept payloads in row-major order (NumPy boolean indexing order)
+    assert np.array_equal(p.values, W[m])
+    # round trip: decode gives W where kept and +0 elsewhere, bit for bit
+    zero = np.zeros((), dtype=W.dtype)
+    assert np.array_equal(orc.unpack(p), np.where(m, W, zero))
+    return p
+
+
+def test_bruteforce_all_masks_2x8(orc):
+    rng = np.random.default_rng(5)
+    idx = np.arange(1 << 16, dtype=np.uint32)
+    bits = ((idx[:, None] >> np.arange(16, dtype=np.uint32)) & 1).astype(np.uint8)
+    mask = bits.reshape(-1, 8)                      # block i -> rows 2i, 2i+1
+    W = rng.integers(0, 1 << 16, size=mask.shape, dtype=np.uint16)
+    W[::7] = 0                                      # kept zeros and -0.0 payloads stay stored
+    W[1::11] = 0x8000
+    _check_pack_against_numpy(orc, W, mask, "f16")
+
+
+def test_bruteforce_all_masks_small_shapes(orc):
+    rng = np.random.default_rng(11)
+    shapes = [(r, c) for r in range(1, 13) for c in range(1, 13) if r * c <= 12]
+    for (r, c) in shapes:
+        n = r * c
+        W = rng.integers(1, 1 << 16, size=(r, c), dtype=np.uint16)
+        for code in range(1 << n):
+            mask = ((code >> np.arange(n)) & 1).astype(np.uint8).reshape(r, c)
+            p = orc.pack(W, "bf16", mask)
+            assert p.nnz == int(mask.sum())
+            assert np.array_equal(p.values, W[mask.astype(bool)])
+            assert np.array_equal(orc.unpack(p), np.where(mask.astype(bool), W, np.uint16(0)))
+
+
+def test_int8_payloads_and_null_mask(orc):
+    rng = np.random.default_rng(3)
+    W8 = rng.integers(-128, 128, size=(9, 77), dtype=np.int8)
+    W8[W8 % 3 == 0] = 0
+    p = orc.pack(W8, "i8", None)                    # no mask: kept iff non-zero
+    assert np.array_equal(p.values, W8[W8 != 0])
+    assert np.array_equal(orc.unpack(p), W8)
+    W16 = rng.integers(0, 1 << 16, size=(5, 40), dtype=np.uint16)
+    W16[:, ::3] = 0x8000                            # -0.0 is not kept without a mask
+    W16[:, 1::5] = 0
+    p = orc.pack(W16, "bf16", None)
+    keep = (W16 & 0x7FFF) != 0
+    assert np.array_equal(p.values, W16[keep])
+
+
+# ------------------------------------------------------------ invariants
+
+@pytest.mark.parametrize("N,K,s,expect_nnz", [
+    (4096, 4096, 0.7, 5_033_165),
+    (4096, 4096, 0.5, 8_388_608),
+    (300, 100, 0.7, 9_000),
+])
+def test_format_invariants(orc, N, K, s, expect_nnz):
+    W, mask = synth.weight(123, N, K, "bf16", s)
+    p = orc.pack(W, "bf16", mask)
+    numel = N * K
+    assert p.nnz == expect_nnz == numel - int(np.floor(s * numel + 1e-9))
+    pc = np.unpackbits(p.bitmask.view(np.uint8), bitorder="little").reshape(N, -1).sum(axis=1)
+    assert np.array_equal(np.diff(p.row_offsets.astype(np.int64)), pc)
+    assert int(pc.sum()) == p.nnz
+    words = p.bitmask.shape[1]
+    if K % 32:
+        tail = p.bitmask[:, words - 1] >> np.uint32(K % 32)
+        assert not tail.any()
+
+
+# ------------------------------------------------------------ fp linear
+
+def _np_dense(bits, dtype):
+    return synth.bits_to_f32(bits, dtype).astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("M,N,K,s", [(5, 37, 101, 0.5), (3, 64, 96, 0.7), (1, 19, 260, 0.3)])
+def test_linear_matches_blas(orc, dtype, M, N, K, s):
+    W, mask = synth.weight(7 + K, N, K, dtype, s)
+    X = synth.activations(8 + K, M, K, dtype)
+    p = orc.pack(W, dtype, mask)
+    Y = orc.linear_f64(X, p)
+    Wd = np.where(mask.astype(bool), _np_dense(W, dtype), 0.0)
+    Xd = _np_dense(X, dtype)
+    Yref = Xd @ Wd.T
+    scale = np.abs(Xd) @ np.abs(Wd).T
+    assert Y.shape == (M, N)
+    assert np.all(np.abs(Y - Yref) <= 1e-12 * scale + 1e-300)
+
+
+def test_linear_exact_arithmetic(orc):
+    rng = np.random.default_rng(17)
+    M, N, K = 7, 23, 333
+    wi = rng.integers(-15, 16, size=(N, K))          # W = wi / 64, exact in bf16
+    xi = rng.integers(-3, 4, size=(M, K))            # X in {0, +-1, +-2, +-3}
+    W = synth.round_bf16((wi / 64.0).astype(np.float32))
+    X = synth.round_bf16(xi.astype(np.float32))
+    mask = (rng.random((N, K)) < 0.4).astype(np.uint8)
+    p = orc.pack(W, "bf16", mask)
+    Y = orc.linear_f64(X, p)
+    exact = (xi @ (wi * mask).T) / 64.0              # integer arithmetic, one exact scaling
+    assert np.array_equal(Y, exact)
+
+
+def test_identity_activations_give_transpose(orc):
+    N, K = 45, 70
+    W, mask = synth.weight(31, N, K, "f16", 0.6)
+    X = synth.round_f16(np.eye(K, dtype=np.float32))
+    p = orc.pack(W, "f16", mask)
+    Y = orc.linear_f64(X, p)                         # [K][N]
+    expect = np.where(mask.astype(bool), _np_dense(W, "f16"), 0.0).T
+    assert np.array_equal(Y, expect)
+
+
+def test_sparsity_zero_and_one(orc):
+    M, N, K = 4, 33, 50
+    X = synth.activations(1, M, K, "bf16")
+    W, mask0 = synth.weight(2, N, K, "bf16", 0.0)
+    assert mask0.all()
+    p0 = orc.pack(W, "bf16", mask0)
+    assert np.array_equal(orc.linear_f64(X, p0), orc.dense_f64(X, W, "bf16"))
+    _, mask1 = synth.weight(2, N, K, "bf16", 1.0)
+    assert not mask1.any()
+    p1 = orc.pack(W, "bf16", mask1)
+    assert p1.nnz == 0
+    assert not orc.linear_f64(X, p1).any()
+
+
+def test_dense_of_masked_weight_equals_sparse(orc):
+    M, N, K = 6, 29, 131
+    W, mask = synth.weight(41, N, K, "bf16", 0.7)
+    X = synth.activations(42, M, K, "bf16")
+    p = orc.pack(W, "bf16", mask)
+    Wm = np.where(mask.astype(bool), W, np.uint16(0))
+    assert np.array_equal(orc.linear_f64(X, p), orc.dense_f64(X, Wm, "bf16"))
+
+
+def test_pairs_agree_with_full(orc):
+    M, N, K = 9, 40, 75
+    W, mask = synth.weight(51, N, K, "f16", 0.5)
+    X = synth.activations(52, M, K, "f16")
+    p = orc.pack(W, "f16", mask)
+    Y = orc.linear_f64(X, p)
+    rng = np.random.default_rng(0)
+    ms = rng.integers(0, M, 100)
+    ns = rng.integers(0, N, 100)
+    assert np.array_equal(orc.linear_f64_pairs(X, p, ms, ns), Y[ms, ns])
+
+
+# ------------------------------------------------------------ int8 linear
+
+def _np_dequant(acc, sx, sw):
+    y = (acc.astype(np.float32) * sx.astype(np.float32)[:, None]).astype(np.float32)
+    y = (y * sw.astype(np.float32)[None, :]).astype(np.float32)
+    return y.astype(np.float16).view(np.uint16)
+
+
+@pytest.mark.parametrize("M,N,K", [(3, 21, 200), (1, 64, 4096)])
+def test_int8_matches_numpy(orc, M, N, K):
+    Wq, mask, sw = synth.int8_weight(61 + K, N, K, 0.7)
+    Xq, sx = synth.int8_activations(62 + K, M, K)
+    p = orc.pack(Wq, "i8", mask)
+    acc, Y = orc.linear_i8(Xq, sx, p, sw)
+    ref = Xq.astype(np.int64) @ (Wq.astype(np.int64) * mask).T
+    assert np.array_equal(acc.astype(np.int64), ref)
+    assert np.array_equal(Y, _np_dequant(acc, sx, sw))
+    acc_d, Y_d = orc.dense_i8(Xq, sx, np.where(mask.astype(bool), Wq, np.int8(0)), sw)
+    assert np.array_equal(acc_d, acc) and np.array_equal(Y_d, Y)
+
+
+def test_int8_extreme_accumulators(orc):
+    K = 11008
+    Xq = np.full((2, K), 127, dtype=np.int8)
+    Xq[1] = -127
+    Wq = np.full((3, K), 127, dtype=np.int8)
+    Wq[1, ::2] = -127
+    Wq[2, :] = -127
+    mask = np.ones((3, K), dtype=np.uint8)
+    sx = np.array([0.013, 0.0071], dtype=np.float32)
+    sw = np.array([3.1e-4, 2.2e-4, 1.7e-4], dtype=np.float32)
+    p = orc.pack(Wq, "i8", mask)
+    acc, Y = orc.linear_i8(Xq, sx, p, sw)
+    assert int(acc[0, 0]) == 127 * 127 * K == 177_548_032
+    assert int(acc[1, 2]) == 127 * 127 * K
+    assert np.array_equal(Y, _np_dequant(acc, sx, sw))
+
+
+# ------------------------------------------------------------ number formats
+
+def test_f16_decode_exhaustive(orc):
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    mine = orc.f16_to_f64(bits)
+    ref = bits.view(np.float16).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(mine[~nan]), np.signbit(ref[~nan]))
+
+
+def test_bf16_decode_exhaustive(orc):
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    mine = orc.bf16_to_f64(bits)
+    ref = (bits.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+
+
+def test_f16_encode_against_numpy(orc):
+    rng = np.random.default_rng(99)
+    parts = [
+        (rng.standard_normal(200_000) * np.exp2(rng.uniform(-30, 17, 200_000))).astype(np.float32),
+        rng.integers(0, 1 << 32, 200_000, dtype=np.uint64).astype(np.uint32).view(np.float32),
+    ]
+    # exact midpoints between neighbouring fp16 values (ties go to the even neighbour)
+    h = np.arange(0, 0x7C00, dtype=np.uint16)
+    lo = h.view(np.float16).astype(np.float64)
+    hi = (h + 1).view(np.float16).astype(np.float64)
+    mid = ((lo + hi) / 2).astype(np.float32)
+    parts += [mid, -mid, np.nextafter(mid, np.float32(np.inf)), np.nextafter(mid, np.float32(0))]
+    parts.append(np.array([0.0, -0.0, 65504.0, 65519.996, 65520.0, 1e9, -1e9, np.inf, -np.inf,
+                           6.1035156e-05, 5.9604645e-08, 2.9802322e-08, 2.98e-08, 1e-45], dtype=np.float32))
+    x = np.concatenate(parts)
+    mine = orc.f32_to_f16(x)
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float16).view(np.uint16)
+    nan = np.isnan(x)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.all((mine[nan] & 0x7C00) == 0x7C00) and np.all((mine[nan] & 0x3FF) != 0)
+
+
+def test_dequant_matches_numpy_chain(orc):
+    rng = np.random.default_rng(7)
+    acc = rng.integers(-(1 << 28), 1 << 28, 100_000).astype(np.int32)
+    acc[:10] = [0, 1, -1, 16777217, -16777217, 177_548_032, 2**31 - 1, -(2**31), 33554435, 100]
+    sx = (rng.random(100_000) * 0.05).astype(np.float32)
+    sw = (rng.random(100_000) * 1e-3).astype(np.float32)
+    mine = orc.dequant_f16(acc, sx, sw)
+    t = (acc.astype(np.float32) * sx).astype(np.float32)
+    y = (t * sw).astype(np.float32)
+    with np.errstate(over="ignore"):
+        ref = y.astype(np.float16).view(np.uint16)
+    assert np.array_equal(mine, ref)
+
+
+# ------------------------------------------------------------ generator sanity (inputs, not parity)
+
+def test_magnitude_mask_count_and_ties():
+    # all magnitudes equal -> the lowest row-major indices are zeroed
+    bits = np.full((10, 13), 0x3C00, dtype=np.uint16)
+    bits[::2] |= 0x8000
+    m = synth.magnitude_mask(bits, 0.7)
+    z = (130 * 7) // 10
+    assert int((m == 0).sum()) == z
+    assert not m.ravel()[:z].any() and m.ravel()[z:].all()
+    # strictly ordered magnitudes -> exactly the z smallest are zeroed
+    rng = np.random.default_rng(1)
+    vals = rng.permutation(np.arange(1, 1001, dtype=np.uint16)).reshape(20, 50)
+    m = synth.magnitude_mask(vals, 0.5)
+    assert np.array_equal(m.astype(bool), vals > 500)
+
+
+@pytest.mark.parametrize("s,cut", [(0.5, 0.6745), (0.7, 1.0364)])
+def test_magnitude_cut_matches_normal_quantile(s, cut):
+    W, mask = synth.weight(1234, 1024, 1024, "bf16", s)
+    mags = np.abs(synth.bits_to_f32(W, "bf16").astype(np.float64))
+    kept_min = mags[mask.astype(bool)].min()
+    assert abs(kept_min / synth.WEIGHT_STD - cut) < 0.01
+    assert int(mask.sum()) == 1024 * 1024 - int(s * 1024 * 1024)
+
+
+def test_activation_rows_are_prefixes():
+    a = synth.activations(5, 16, 64, "bf16")
+    b = synth.activations(5, 4, 64, "bf16")
+    assert np.array_equal(a[:4], b)
