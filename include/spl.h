@@ -1,0 +1,161 @@
+/*
+ * spl.h - C ABI of the MI355X (gfx950) sparse linear library.
+ *
+ * Dense activations times unstructured-sparse weights held in the bitmask
+ * expansion format of arXiv 2405.03594: section 2.4.1 stores the kept
+ * entries of a block densely in order together with a bitmask that marks
+ * the kept positions; section 2.4.2 applies the same idea to GPU
+ * submatrices that are decompressed right before the matrix units consume
+ * them; section 3.4 adds int8 weights and int8 activations.  The linear
+ * layers computed here are the seven projections of a Llama-2-7B decoder
+ * layer (q, k, v, o, gate, up, down), but any shape is accepted.
+ *
+ * Conventions shared by every entry point
+ *   - W is [N][K] row-major (N output features, K input features), X is
+ *     [M][K] and Y is [M][N], both row-major.  The product is
+ *         Y[m][n] = sum_k X[m][k] * (W . Mask)[n][k].
+ *   - All array arguments are DEVICE pointers (hipMalloc'ed or from a
+ *     framework allocator) unless a comment says "host".  The caller owns
+ *     every buffer; the library allocates no device memory and keeps no
+ *     state between calls.
+ *   - Every call is ordered on `stream` (NULL = the default stream) and
+ *     returns as soon as its kernels are queued, except spl_pack_count,
+ *     which waits for `stream` to return the number of kept entries.
+ *   - Arguments are checked on the host before anything is launched; a
+ *     failed check returns an error code and launches nothing.  Errors
+ *     reported by the HIP runtime at launch map to SPL_ERR_DEVICE.  Nothing
+ *     throws across this interface.
+ *   - Device buffers must be 16-byte aligned.  Kernels may read, but never
+ *     write, up to 15 bytes past the end of `values` inside the same
+ *     aligned 16-byte block.
+ *
+ * The compressed matrix (canonical encoding, lossless)
+ *   bitmask     uint32 [N][ceil(K/32)]; bit j (least significant first) of
+ *               word w of row n is set iff position (n, 32w + j) is kept;
+ *               bits at or past K are 0.
+ *   values      the kept payloads, row by row, ascending column order, as
+ *               raw bit copies (fp16 / bf16: 2 bytes; int8: 1 byte).
+ *   row_offsets int32 [N+1]; row_offsets[n] is the index in `values` of the
+ *               first kept entry of row n, row_offsets[N] = nnz < 2^31.
+ *   Reading of the paper: its worked example packs one 16-lane VNNI register
+ *   (two interleaved rows); here the block is a whole row in column order,
+ *   and the bit order is least-significant-bit first.
+ */
+#ifndef SPL_H
+#define SPL_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPL_OK = 0,
+  SPL_ERR_INVALID_ARG = 1,   /* null pointer, bad size, misaligned buffer, inconsistent view */
+  SPL_ERR_UNSUPPORTED = 2,   /* dtype or algorithm not available for this call */
+  SPL_ERR_OVERFLOW = 3,      /* nnz >= 2^31, or a size product overflows */
+  SPL_ERR_DEVICE = 4         /* the HIP runtime reported an error */
+} spl_status;
+
+typedef enum { SPL_F16 = 1, SPL_BF16 = 2, SPL_I8 = 3 } spl_dtype;
+
+/* Kernel family for spl_sparse_linear_ex / spl_dense_linear_ex.
+ * AUTO picks by batch size M.  DECODE is the small-batch kernel (M <= 32):
+ * compressed rows are decompressed into MFMA operand tiles with the batch
+ * padded to 16 or 32.  PREFILL is the large-batch tiled kernel: compressed
+ * tiles are decompressed into LDS and feed bf16/fp16 MFMA (any M). */
+typedef enum { SPL_ALGO_AUTO = 0, SPL_ALGO_DECODE = 1, SPL_ALGO_PREFILL = 2 } spl_algo;
+
+/* Non-owning view of a compressed matrix (all pointers device pointers).
+ * The arrays must stay alive until work queued with the view completes. */
+typedef struct {
+  int64_t rows;                  /* N */
+  int64_t cols;                  /* K */
+  int32_t dtype;                 /* spl_dtype of `values` */
+  int32_t reserved;              /* must be 0 */
+  int64_t nnz;                   /* == row_offsets[N] */
+  const uint32_t* bitmask;       /* [N][ceil(K/32)] */
+  const void* values;            /* [nnz] payloads */
+  const int32_t* row_offsets;    /* [N+1] */
+} spl_matrix;
+
+/* Library version, (major << 16) | minor. */
+int32_t spl_version(void);
+
+/* Static text for a status code. */
+const char* spl_status_string(spl_status s);
+
+/* Host-only consistency check of a view's scalar fields and pointers
+ * (no device access): non-null arrays (values may be NULL only if nnz == 0),
+ * rows, cols >= 1, dtype known, reserved == 0, 0 <= nnz < 2^31, and 16-byte
+ * alignment of bitmask and values. */
+spl_status spl_check_matrix(const spl_matrix* Wc);
+
+/* Pack, step 1 of 2 (paper section 2.4.1: count the kept entries).
+ *   W           [N][K] payloads of `dtype` (F16, BF16 or I8).
+ *   mask        [N][K] uint8, non-zero = kept; or NULL, then an entry is kept
+ *               iff its payload is non-zero (fp16/bf16: ignoring the sign bit,
+ *               so -0.0 is not kept).
+ *   row_offsets out [N+1], written with the exclusive prefix sum of per-row
+ *               kept counts.
+ *   h_nnz       HOST out: number of kept entries.  This call synchronizes
+ *               `stream` to read it.  Returns SPL_ERR_OVERFLOW if it would
+ *               reach 2^31. */
+spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                          int32_t* row_offsets, int64_t* h_nnz, hipStream_t stream);
+
+/* Pack, step 2 of 2 (paper section 2.4.1: write bitmask and dense values).
+ *   row_offsets from spl_pack_count for the same W and mask.
+ *   bitmask     out [N][ceil(K/32)], fully written (pad bits 0).
+ *   values      out [nnz] payloads of `dtype`. */
+spl_status spl_pack_sparse(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                           const int32_t* row_offsets, uint32_t* bitmask, void* values,
+                           hipStream_t stream);
+
+/* Decompress to a dense [N][K] matrix of the view's dtype: kept positions
+ * receive their payload, every other position +0. */
+spl_status spl_unpack(const spl_matrix* Wc, void* W_dense, hipStream_t stream);
+
+/* Sparse linear layer, fp16 or bf16 (paper section 2.4.2).
+ *   X  [M][K] of Wc->dtype; M >= 0 (M == 0 is a no-op).
+ *   Y  out [M][N] of Wc->dtype, overwritten.  fp32 accumulation, one
+ *      round-to-nearest-even conversion per output.  No bias.
+ *   Requires K % 8 == 0 (rows of X are read in 16-byte pieces). */
+spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, void* Y, hipStream_t stream);
+
+/* As spl_sparse_linear with an explicit kernel family (spl_algo).
+ * DECODE requires M <= 32. */
+spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
+                                hipStream_t stream);
+
+/* Sparse-quantized linear layer (paper section 3.4: int8 weights and
+ * int8 activations).
+ *   Xq        [M][K] int8 activation codes; x_scales [M] float32.
+ *   Wqc       view with dtype SPL_I8; w_scales [N] float32.
+ *   acc       acc[m][n] = sum over kept k of Xq[m][k] * Wq[n][k], exact int32.
+ *   Y         out [M][N] fp16: round-to-nearest-even of
+ *             ((float)acc * x_scales[m]) * w_scales[n], each product rounded
+ *             to float32 (no fused multiply-add).
+ *   acc_out   optional out [M][N] int32 (NULL to skip).
+ *   Requires K % 16 == 0. */
+spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
+                                  const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream);
+
+/* Dense comparators: the same products with a dense W [N][K].
+ * spl_dense_linear: fp16/bf16 (K % 8 == 0); spl_dense_linear_int8: int8
+ * with the epilogue of spl_sparse_linear_int8 (K % 16 == 0). */
+spl_status spl_dense_linear(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                            void* Y, hipStream_t stream);
+spl_status spl_dense_linear_ex(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                               void* Y, int32_t algo, hipStream_t stream);
+spl_status spl_dense_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const int8_t* Wq,
+                                 const float* w_scales, int64_t N, int64_t K, void* Y, int32_t* acc_out,
+                                 hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPL_H */

@@ -1,0 +1,240 @@
+"""Python binding of libspl, the gfx950 sparse linear library (C ABI in ``include/spl.h``).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libspl.so``.  PyTorch supplies device memory and the stream.
+There is no fallback: if the library is missing or a call fails, an
+exception is raised.
+
+Names follow the C ABI without its ``spl_`` prefix:
+
+* ``pack_sparse(W, mask)`` -> :class:`SparseMatrix` (bitmask, packed values,
+  row offsets; paper section 2.4.1);
+* ``sparse_linear(X, Wc)`` -> ``Y = X (W . Mask)^T`` for fp16/bf16 (section 2.4.2);
+* ``sparse_linear_int8(Xq, x_scales, Wqc, w_scales)`` -> fp16 ``Y`` (section 3.4);
+* ``unpack``, ``dense_linear``, ``dense_linear_int8``: decoder and dense comparators.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspl.so")
+
+F16, BF16, I8 = 1, 2, 3
+ALGO = {"auto": 0, "decode": 1, "prefill": 2}
+_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "overflow", 4: "HIP runtime error"}
+_TORCH_DTYPE = {torch.float16: F16, torch.bfloat16: BF16, torch.int8: I8}
+_CODE_DTYPE = {F16: torch.float16, BF16: torch.bfloat16, I8: torch.int8}
+
+
+class SplError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {_STATUS.get(status, status)} (status {status})")
+        self.status = status
+
+
+class _Matrix(ctypes.Structure):
+    _fields_ = [
+        ("rows", ctypes.c_int64),
+        ("cols", ctypes.c_int64),
+        ("dtype", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("nnz", ctypes.c_int64),
+        ("bitmask", ctypes.c_void_p),
+        ("values", ctypes.c_void_p),
+        ("row_offsets", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libspl.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    MP = ctypes.POINTER(_Matrix)
+    sigs = {
+        "spl_version": (I32, []),
+        "spl_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "spl_check_matrix": (ctypes.c_int, [MP]),
+        "spl_pack_count": (ctypes.c_int, [P, I32, P, I64, I64, P, ctypes.POINTER(I64), P]),
+        "spl_pack_sparse": (ctypes.c_int, [P, I32, P, I64, I64, P, P, P, P]),
+        "spl_unpack": (ctypes.c_int, [MP, P, P]),
+        "spl_sparse_linear": (ctypes.c_int, [P, I64, MP, P, P]),
+        "spl_sparse_linear_ex": (ctypes.c_int, [P, I64, MP, P, I32, P]),
+        "spl_sparse_linear_int8": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
+        "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
+        "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
+        "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise SplError(fn, status)
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev_tensor(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+@dataclass
+class SparseMatrix:
+    """A compressed [N][K] matrix: the canonical bitmask-expansion encoding."""
+
+    bitmask: torch.Tensor      # int32 view of uint32 words [N][ceil(K/32)]
+    values: torch.Tensor       # payloads (fp16 / bf16 / int8), length >= nnz
+    row_offsets: torch.Tensor  # int32 [N+1]
+    rows: int
+    cols: int
+    nnz: int
+
+    @property
+    def dtype(self) -> torch.dtype:
+        return self.values.dtype
+
+    def view(self) -> _Matrix:
+        return _Matrix(self.rows, self.cols, _TORCH_DTYPE[self.values.dtype], 0, self.nnz,
+                       self.bitmask.data_ptr(), self.values.data_ptr() if self.nnz > 0 else 0,
+                       self.row_offsets.data_ptr())
+
+    def compressed_bytes(self) -> int:
+        """Bytes of the encoding: payloads + bitmask + row offsets."""
+        return self.nnz * self.values.element_size() + self.bitmask.numel() * 4 + self.row_offsets.numel() * 4
+
+
+def _values_buffer(nnz: int, dtype: torch.dtype, device) -> torch.Tensor:
+    # whole 16-byte blocks, so vector reads of the last payloads stay inside the allocation
+    esz = torch.empty((), dtype=dtype).element_size()
+    n = max(16, ((nnz * esz + 15) // 16) * 16) // esz
+    return torch.zeros(n, dtype=dtype, device=device)
+
+
+def pack_sparse(W: torch.Tensor, mask: torch.Tensor | None = None, stream=None) -> SparseMatrix:
+    """Compress W [N][K] (fp16/bf16/int8) under `mask` (uint8/bool, non-zero = kept;
+    None = keep the non-zero payloads)."""
+    L = lib()
+    _dev_tensor(W, "W")
+    if W.dim() != 2 or W.dtype not in _TORCH_DTYPE:
+        raise ValueError("W must be a 2-D fp16/bf16/int8 tensor")
+    N, K = W.shape
+    if mask is not None:
+        _dev_tensor(mask, "mask")
+        if mask.shape != W.shape:
+            raise ValueError("mask must have W's shape")
+        if mask.dtype == torch.bool:
+            mask = mask.view(torch.uint8)
+        if mask.dtype != torch.uint8:
+            raise ValueError("mask must be uint8 or bool")
+    code = _TORCH_DTYPE[W.dtype]
+    row_offsets = torch.empty(N + 1, dtype=torch.int32, device=W.device)
+    words = (K + 31) // 32
+    bitmask = torch.empty((N, words), dtype=torch.int32, device=W.device)
+    nnz = ctypes.c_int64(0)
+    s = _stream(stream)
+    _check("spl_pack_count", L.spl_pack_count(_ptr(W), code, _ptr(mask), N, K, _ptr(row_offsets),
+                                              ctypes.byref(nnz), s))
+    values = _values_buffer(nnz.value, W.dtype, W.device)
+    _check("spl_pack_sparse", L.spl_pack_sparse(_ptr(W), code, _ptr(mask), N, K, _ptr(row_offsets),
+                                                _ptr(bitmask), _ptr(values), s))
+    return SparseMatrix(bitmask, values, row_offsets, N, K, nnz.value)
+
+
+def unpack(Wc: SparseMatrix, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    L = lib()
+    if out is None:
+        out = torch.empty((Wc.rows, Wc.cols), dtype=Wc.dtype, device=Wc.values.device)
+    view = Wc.view()
+    _check("spl_unpack", L.spl_unpack(ctypes.byref(view), _ptr(out), _stream(stream)))
+    return out
+
+
+def sparse_linear(X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = None, algo: str = "auto",
+                  stream=None) -> torch.Tensor:
+    """Y [M][N] = X [M][K] (W . Mask)^T, fp32 accumulation, output in X's dtype."""
+    L = lib()
+    _dev_tensor(X, "X")
+    M = X.shape[0]
+    if out is None:
+        out = torch.empty((M, Wc.rows), dtype=X.dtype, device=X.device)
+    if X.dtype != Wc.dtype or out.dtype != X.dtype:
+        raise ValueError("X, W and Y must share one fp16/bf16 dtype")
+    view = Wc.view()
+    _check("spl_sparse_linear_ex", L.spl_sparse_linear_ex(_ptr(X), M, ctypes.byref(view), _ptr(out), ALGO[algo],
+                                                          _stream(stream)))
+    return out
+
+
+def sparse_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wqc: SparseMatrix, w_scales: torch.Tensor,
+                       out: torch.Tensor | None = None, acc_out: torch.Tensor | None = None,
+                       stream=None) -> torch.Tensor:
+    """fp16 Y = dequant(int32 Xq (Wq . Mask)^T) with per-token and per-channel scales."""
+    L = lib()
+    for t, nm in ((Xq, "Xq"), (x_scales, "x_scales"), (w_scales, "w_scales")):
+        _dev_tensor(t, nm)
+    M = Xq.shape[0]
+    if out is None:
+        out = torch.empty((M, Wqc.rows), dtype=torch.float16, device=Xq.device)
+    view = Wqc.view()
+    _check("spl_sparse_linear_int8", L.spl_sparse_linear_int8(_ptr(Xq), _ptr(x_scales), M, ctypes.byref(view),
+                                                              _ptr(w_scales), _ptr(out), _ptr(acc_out),
+                                                              _stream(stream)))
+    return out
+
+
+def dense_linear(X: torch.Tensor, W: torch.Tensor, out: torch.Tensor | None = None, algo: str = "auto",
+                 stream=None) -> torch.Tensor:
+    """Dense comparator: Y = X W^T with the same kernel families."""
+    L = lib()
+    _dev_tensor(X, "X")
+    _dev_tensor(W, "W")
+    M, K = X.shape
+    N = W.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=X.dtype, device=X.device)
+    _check("spl_dense_linear_ex", L.spl_dense_linear_ex(_ptr(X), M, _ptr(W), _TORCH_DTYPE[W.dtype], N, K,
+                                                        _ptr(out), ALGO[algo], _stream(stream)))
+    return out
+
+
+def dense_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wq: torch.Tensor, w_scales: torch.Tensor,
+                      out: torch.Tensor | None = None, acc_out: torch.Tensor | None = None,
+                      stream=None) -> torch.Tensor:
+    L = lib()
+    M, K = Xq.shape
+    N = Wq.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    _check("spl_dense_linear_int8", L.spl_dense_linear_int8(_ptr(Xq), _ptr(x_scales), M, _ptr(Wq),
+                                                            _ptr(w_scales), N, K, _ptr(out), _ptr(acc_out),
+                                                            _stream(stream)))
+    return out

@@ -1,0 +1,168 @@
+// Bitmask-expansion encoder and decoder on gfx950 (paper section 2.4.1).
+//
+// pack_count : one wave per row counts kept entries, then one workgroup turns
+//              the counts into exclusive row offsets (int64 running sums; an
+//              overflow past 2^31 is flagged as row_offsets[N] = -1).
+// pack_scatter: one wave per row walks the row in 64-column steps; a ballot of
+//              the keep predicate is the row's next two bitmask words, and each
+//              kept lane's rank among them (v_mbcnt) is its slot in `values`.
+// unpack     : the inverse walk; a lane whose bit is set takes the value at its
+//              rank, every other lane writes +0.
+#include "spl_common.h"
+
+namespace spl {
+namespace {
+
+template <int EB>
+__device__ __forceinline__ bool payload_nonzero(const void* W, int64_t idx) {
+  if constexpr (EB == 1) {
+    return static_cast<const int8_t*>(W)[idx] != 0;
+  } else {
+    return (static_cast<const uint16_t*>(W)[idx] & 0x7fffu) != 0;   // -0.0 counts as zero
+  }
+}
+
+template <int EB>
+__device__ __forceinline__ bool is_kept(const void* W, const uint8_t* mask, int64_t idx) {
+  return mask ? (mask[idx] != 0) : payload_nonzero<EB>(W, idx);
+}
+
+template <int EB>
+__global__ void __launch_bounds__(256) k_row_count(const void* W, const uint8_t* mask, int64_t N, int64_t K,
+                                                   int32_t* counts) {
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const uint32_t lane = threadIdx.x & 63u;
+  const int64_t base = n * K;
+  uint32_t c = 0;
+  for (int64_t k = lane; k < K; k += kWave) c += is_kept<EB>(W, mask, base + k) ? 1u : 0u;
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+  if (lane == 0) counts[n] = (int32_t)c;
+}
+
+// In place: row_offsets[0..N) hold per-row counts on entry, exclusive prefix
+// sums on exit; row_offsets[N] = nnz, or -1 if nnz >= 2^31 (then the other
+// entries are left unspecified).
+__global__ void __launch_bounds__(1024) k_scan_offsets(int32_t* row_offsets, int64_t N) {
+  __shared__ int64_t part[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (N + 1023) / 1024;
+  const int64_t lo = (int64_t)t * per;
+  const int64_t hi = lo + per < N ? lo + per : N;
+  int64_t s = 0;
+  for (int64_t i = lo; i < hi; ++i) s += row_offsets[i];
+  part[t] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int64_t v = t >= off ? part[t - off] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  const int64_t total = part[1023];
+  const bool overflow = total >= (int64_t)2147483648LL;
+  int64_t run = part[t] - s;
+  if (!overflow) {
+    for (int64_t i = lo; i < hi; ++i) {
+      const int32_t c = row_offsets[i];
+      row_offsets[i] = (int32_t)run;
+      run += c;
+    }
+  }
+  if (t == 1023) row_offsets[N] = overflow ? -1 : (int32_t)total;
+}
+
+template <int EB>
+__global__ void __launch_bounds__(256) k_pack_scatter(const void* W, const uint8_t* mask, int64_t N, int64_t K,
+                                                      const int32_t* row_offsets, uint32_t* bitmask,
+                                                      void* values) {
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const uint32_t lane = threadIdx.x & 63u;
+  const int64_t words = words_per_row(K);
+  const int64_t base = n * K;
+  uint32_t* brow = bitmask + n * words;
+  int64_t out = row_offsets[n];
+  for (int64_t k0 = 0; k0 < K; k0 += kWave) {
+    const int64_t k = k0 + lane;
+    const bool keep = k < K && is_kept<EB>(W, mask, base + k);
+    const uint64_t b = __ballot(keep);
+    if (keep) {
+      const int64_t slot = out + mbcnt64(b);
+      if constexpr (EB == 2) {
+        static_cast<uint16_t*>(values)[slot] = static_cast<const uint16_t*>(W)[base + k];
+      } else {
+        static_cast<int8_t*>(values)[slot] = static_cast<const int8_t*>(W)[base + k];
+      }
+    }
+    const int64_t w = k0 >> 5;
+    if (lane == 0) brow[w] = (uint32_t)b;
+    if (lane == 1 && w + 1 < words) brow[w + 1] = (uint32_t)(b >> 32);
+    out += __popcll(b);
+  }
+}
+
+template <int EB>
+__global__ void __launch_bounds__(256) k_unpack(const uint32_t* bitmask, const void* values,
+                                                const int32_t* row_offsets, int64_t N, int64_t K, void* Wd) {
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const uint32_t lane = threadIdx.x & 63u;
+  const int64_t words = words_per_row(K);
+  const uint32_t* brow = bitmask + n * words;
+  int64_t in = row_offsets[n];
+  for (int64_t k0 = 0; k0 < K; k0 += kWave) {
+    const int64_t w = k0 >> 5;
+    const uint64_t b = (uint64_t)brow[w] | (w + 1 < words ? (uint64_t)brow[w + 1] << 32 : 0ull);
+    const int64_t k = k0 + lane;
+    if (k < K) {
+      const bool bit = (b >> lane) & 1ull;
+      const int64_t src = in + mbcnt64(b);
+      if constexpr (EB == 2) {
+        static_cast<uint16_t*>(Wd)[n * K + k] = bit ? static_cast<const uint16_t*>(values)[src] : (uint16_t)0;
+      } else {
+        static_cast<int8_t*>(Wd)[n * K + k] = bit ? static_cast<const int8_t*>(values)[src] : (int8_t)0;
+      }
+    }
+    in += __popcll(b);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                             int32_t* row_offsets, hipStream_t s) {
+  const dim3 grid((unsigned)((N + 3) / 4)), block(256);
+  if (dtype == SPL_I8) {
+    hipLaunchKernelGGL(k_row_count<1>, grid, block, 0, s, W, mask, N, K, row_offsets);
+  } else {
+    hipLaunchKernelGGL(k_row_count<2>, grid, block, 0, s, W, mask, N, K, row_offsets);
+  }
+  hipLaunchKernelGGL(k_scan_offsets, dim3(1), dim3(1024), 0, s, row_offsets, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_scatter(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                               const int32_t* row_offsets, uint32_t* bitmask, void* values, hipStream_t s) {
+  const dim3 grid((unsigned)((N + 3) / 4)), block(256);
+  if (dtype == SPL_I8) {
+    hipLaunchKernelGGL(k_pack_scatter<1>, grid, block, 0, s, W, mask, N, K, row_offsets, bitmask, values);
+  } else {
+    hipLaunchKernelGGL(k_pack_scatter<2>, grid, block, 0, s, W, mask, N, K, row_offsets, bitmask, values);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s) {
+  const dim3 grid((unsigned)((Wc.rows + 3) / 4)), block(256);
+  if (Wc.dtype == SPL_I8) {
+    hipLaunchKernelGGL(k_unpack<1>, grid, block, 0, s, Wc.bitmask, Wc.values, Wc.row_offsets, Wc.rows, Wc.cols,
+                       W_dense);
+  } else {
+    hipLaunchKernelGGL(k_unpack<2>, grid, block, 0, s, Wc.bitmask, Wc.values, Wc.row_offsets, Wc.rows, Wc.cols,
+                       W_dense);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace spl

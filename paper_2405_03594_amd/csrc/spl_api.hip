@@ -1,0 +1,174 @@
+// extern "C" entry points of libspl: argument checks on the host, then
+// launches on the caller's stream.  No entry point allocates device memory.
+#include <stdint.h>
+
+#include "spl.h"
+#include "spl_common.h"
+
+namespace spl {
+int decode_max_k();
+}
+
+namespace {
+
+constexpr int64_t kMaxDim = (int64_t)1 << 31;        // N, K, M < 2^31
+constexpr int64_t kMaxElems = (int64_t)1 << 40;      // N * K, M * K, M * N
+constexpr int64_t kDecodeMaxM = 32;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool dims_ok(int64_t a, int64_t b) {
+  return a >= 1 && b >= 1 && a < kMaxDim && b < kMaxDim && a <= kMaxElems / b;
+}
+
+bool fp_dtype(int32_t d) { return d == SPL_F16 || d == SPL_BF16; }
+bool any_dtype(int32_t d) { return d == SPL_F16 || d == SPL_BF16 || d == SPL_I8; }
+
+spl_status launched(hipError_t e) {
+  if (e == hipSuccess) return SPL_OK;
+  return e == hipErrorNotSupported ? SPL_ERR_UNSUPPORTED : SPL_ERR_DEVICE;
+}
+
+// Shared checks of an activation/output pair for a [M][K] x [N][K]^T product.
+spl_status check_xy(const void* X, int64_t M, int64_t K, int64_t N, const void* Y) {
+  if (M < 0) return SPL_ERR_INVALID_ARG;
+  if (M == 0) return SPL_OK;
+  if (!X || !Y) return SPL_ERR_INVALID_ARG;
+  if (!dims_ok(M, K) || !dims_ok(M, N)) return SPL_ERR_INVALID_ARG;
+  if (!aligned(X, 16) || !aligned(Y, 16)) return SPL_ERR_INVALID_ARG;
+  return SPL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t spl_version(void) { return (1 << 16) | 0; }
+
+const char* spl_status_string(spl_status s) {
+  switch (s) {
+    case SPL_OK: return "ok";
+    case SPL_ERR_INVALID_ARG: return "invalid argument";
+    case SPL_ERR_UNSUPPORTED: return "unsupported";
+    case SPL_ERR_OVERFLOW: return "overflow: nnz >= 2^31";
+    case SPL_ERR_DEVICE: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+spl_status spl_check_matrix(const spl_matrix* Wc) {
+  if (!Wc) return SPL_ERR_INVALID_ARG;
+  if (!dims_ok(Wc->rows, Wc->cols)) return SPL_ERR_INVALID_ARG;
+  if (!any_dtype(Wc->dtype) || Wc->reserved != 0) return SPL_ERR_INVALID_ARG;
+  if (Wc->nnz < 0) return SPL_ERR_INVALID_ARG;
+  if (Wc->nnz >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (Wc->nnz > Wc->rows * Wc->cols) return SPL_ERR_INVALID_ARG;
+  if (!Wc->bitmask || !Wc->row_offsets) return SPL_ERR_INVALID_ARG;
+  if (Wc->nnz > 0 && !Wc->values) return SPL_ERR_INVALID_ARG;
+  if (!aligned(Wc->bitmask, 16) || !aligned(Wc->row_offsets, 4)) return SPL_ERR_INVALID_ARG;
+  if (Wc->values && !aligned(Wc->values, 16)) return SPL_ERR_INVALID_ARG;
+  return SPL_OK;
+}
+
+spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                          int32_t* row_offsets, int64_t* h_nnz, hipStream_t stream) {
+  if (!W || !row_offsets || !h_nnz) return SPL_ERR_INVALID_ARG;
+  if (!any_dtype(dtype) || !dims_ok(N, K)) return SPL_ERR_INVALID_ARG;
+  if (!aligned(W, 16) || !aligned(row_offsets, 4)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  if (spl::launch_pack_count(W, dtype, mask, N, K, row_offsets, stream) != hipSuccess) return SPL_ERR_DEVICE;
+  int32_t total = 0;
+  if (hipMemcpyAsync(&total, row_offsets + N, sizeof(int32_t), hipMemcpyDeviceToHost, stream) != hipSuccess)
+    return SPL_ERR_DEVICE;
+  if (hipStreamSynchronize(stream) != hipSuccess) return SPL_ERR_DEVICE;
+  if (total < 0) return SPL_ERR_OVERFLOW;
+  *h_nnz = total;
+  return SPL_OK;
+}
+
+spl_status spl_pack_sparse(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                           const int32_t* row_offsets, uint32_t* bitmask, void* values, hipStream_t stream) {
+  if (!W || !row_offsets || !bitmask) return SPL_ERR_INVALID_ARG;
+  if (!any_dtype(dtype) || !dims_ok(N, K)) return SPL_ERR_INVALID_ARG;
+  if (!aligned(W, 16) || !aligned(bitmask, 16) || !aligned(row_offsets, 4)) return SPL_ERR_INVALID_ARG;
+  if (values && !aligned(values, 16)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_pack_scatter(W, dtype, mask, N, K, row_offsets, bitmask, values, stream));
+}
+
+spl_status spl_unpack(const spl_matrix* Wc, void* W_dense, hipStream_t stream) {
+  const spl_status st = spl_check_matrix(Wc);
+  if (st != SPL_OK) return st;
+  if (!W_dense || !aligned(W_dense, 16)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_unpack(*Wc, W_dense, stream));
+}
+
+spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
+                                hipStream_t stream) {
+  const spl_status st = spl_check_matrix(Wc);
+  if (st != SPL_OK) return st;
+  if (!fp_dtype(Wc->dtype)) return SPL_ERR_UNSUPPORTED;
+  if (algo < SPL_ALGO_AUTO || algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
+  const spl_status xy = check_xy(X, M, Wc->cols, Wc->rows, Y);
+  if (xy != SPL_OK || M == 0) return xy;
+  if (Wc->cols % 8 != 0) return SPL_ERR_UNSUPPORTED;
+  if (algo == SPL_ALGO_AUTO)
+    algo = (M <= kDecodeMaxM && Wc->cols <= spl::decode_max_k()) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (algo == SPL_ALGO_DECODE && (M > kDecodeMaxM || Wc->cols > spl::decode_max_k())) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  if (algo == SPL_ALGO_DECODE) return launched(spl::launch_sparse_decode(X, M, *Wc, Y, stream));
+  return launched(spl::launch_sparse_prefill(X, M, *Wc, Y, stream));
+}
+
+spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, void* Y, hipStream_t stream) {
+  return spl_sparse_linear_ex(X, M, Wc, Y, SPL_ALGO_AUTO, stream);
+}
+
+spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
+                                  const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream) {
+  const spl_status st = spl_check_matrix(Wqc);
+  if (st != SPL_OK) return st;
+  if (Wqc->dtype != SPL_I8) return SPL_ERR_UNSUPPORTED;
+  const spl_status xy = check_xy(Xq, M, Wqc->cols, Wqc->rows, Y);
+  if (xy != SPL_OK || M == 0) return xy;
+  if (!x_scales || !w_scales || !aligned(x_scales, 4) || !aligned(w_scales, 4)) return SPL_ERR_INVALID_ARG;
+  if (acc_out && !aligned(acc_out, 16)) return SPL_ERR_INVALID_ARG;
+  if (Wqc->cols % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return launched(spl::launch_sparse_int8(Xq, x_scales, M, *Wqc, w_scales, Y, acc_out, stream));
+}
+
+spl_status spl_dense_linear_ex(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                               void* Y, int32_t algo, hipStream_t stream) {
+  if (!W || !fp_dtype(dtype) || !dims_ok(N, K) || !aligned(W, 16)) return SPL_ERR_INVALID_ARG;
+  if (algo < SPL_ALGO_AUTO || algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
+  const spl_status xy = check_xy(X, M, K, N, Y);
+  if (xy != SPL_OK || M == 0) return xy;
+  if (K % 8 != 0) return SPL_ERR_UNSUPPORTED;
+  if (algo == SPL_ALGO_AUTO) algo = M <= kDecodeMaxM ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (algo == SPL_ALGO_DECODE && M > kDecodeMaxM) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  if (algo == SPL_ALGO_DECODE) return launched(spl::launch_dense_decode(X, M, W, dtype, N, K, Y, stream));
+  return launched(spl::launch_dense_prefill(X, M, W, dtype, N, K, Y, stream));
+}
+
+spl_status spl_dense_linear(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                            void* Y, hipStream_t stream) {
+  return spl_dense_linear_ex(X, M, W, dtype, N, K, Y, SPL_ALGO_AUTO, stream);
+}
+
+spl_status spl_dense_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const int8_t* Wq,
+                                 const float* w_scales, int64_t N, int64_t K, void* Y, int32_t* acc_out,
+                                 hipStream_t stream) {
+  if (!Wq || !dims_ok(N, K) || !aligned(Wq, 16)) return SPL_ERR_INVALID_ARG;
+  const spl_status xy = check_xy(Xq, M, K, N, Y);
+  if (xy != SPL_OK || M == 0) return xy;
+  if (!x_scales || !w_scales || !aligned(x_scales, 4) || !aligned(w_scales, 4)) return SPL_ERR_INVALID_ARG;
+  if (acc_out && !aligned(acc_out, 16)) return SPL_ERR_INVALID_ARG;
+  if (K % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return launched(spl::launch_dense_int8(Xq, x_scales, M, Wq, w_scales, N, K, Y, acc_out, stream));
+}
+
+}  // extern "C"

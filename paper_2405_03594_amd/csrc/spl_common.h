@@ -1,0 +1,80 @@
+// Internal helpers shared by the gfx950 kernels of libspl (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "spl.h"
+
+namespace spl {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+// Storage tags: a 16-bit float payload and how to widen / narrow it.
+struct Bf16 {
+  static constexpr int32_t code = SPL_BF16;
+  static __device__ __forceinline__ float to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+  // binary32 -> bfloat16, round to nearest even; NaN stays NaN.
+  static __device__ __forceinline__ uint16_t from_f32(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+  }
+};
+
+struct F16 {
+  static constexpr int32_t code = SPL_F16;
+  static __device__ __forceinline__ float to_f32(uint32_t bits16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+  }
+  static __device__ __forceinline__ uint16_t from_f32(float f) {
+    return __builtin_bit_cast(uint16_t, (_Float16)f);   // v_cvt_f16_f32: round to nearest even
+  }
+};
+
+__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
+
+// Number of set bits of a 64-bit wave mask below this lane.
+__device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Order this wave's LDS writes before its later LDS reads of other lanes' data.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__host__ __device__ __forceinline__ int64_t words_per_row(int64_t K) { return (K + 31) / 32; }
+
+}  // namespace spl
+
+// Launchers implemented in the kernel translation units (host side).
+namespace spl {
+hipError_t launch_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                             int32_t* row_offsets, hipStream_t s);
+hipError_t launch_pack_scatter(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                               const int32_t* row_offsets, uint32_t* bitmask, void* values, hipStream_t s);
+hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s);
+
+hipError_t launch_sparse_decode(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
+hipError_t launch_dense_decode(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                               void* Y, hipStream_t s);
+hipError_t launch_sparse_prefill(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
+hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                                void* Y, hipStream_t s);
+hipError_t launch_sparse_int8(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc,
+                              const float* sw, void* Y, int32_t* acc, hipStream_t s);
+hipError_t launch_dense_int8(const int8_t* Xq, const float* sx, int64_t M, const int8_t* Wq, const float* sw,
+                             int64_t N, int64_t K, void* Y, int32_t* acc, hipStream_t s);
+}  // namespace spl

@@ -1,0 +1,136 @@
+"""The C-ABI library on the host (no GPU): it loads, exports every symbol
+that include/spl.h declares, and rejects bad arguments with status codes
+before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spl.h")
+
+OK, INVALID, UNSUPPORTED, OVERFLOW = 0, 1, 2, 3
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2405_03594_amd import LIB_PATH, build
+
+    if not os.path.exists(LIB_PATH):
+        build.build()
+    import paper_2405_03594_amd as spl
+
+    return spl.lib()
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(spl_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for required in ("spl_pack_count", "spl_pack_sparse", "spl_sparse_linear", "spl_sparse_linear_int8",
+                     "spl_unpack", "spl_dense_linear", "spl_dense_linear_int8"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in _declared():
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for s in range(5):
+        assert L.spl_status_string(s)
+    assert L.spl_version() >> 16 == 1
+
+
+def _mat(**kw):
+    from paper_2405_03594_amd import _Matrix
+
+    d = dict(rows=4, cols=64, dtype=2, reserved=0, nnz=10, bitmask=0x10000, values=0x20000, row_offsets=0x30000)
+    d.update(kw)
+    return _Matrix(**d)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({}, OK),
+    (dict(rows=0), INVALID),
+    (dict(cols=-1), INVALID),
+    (dict(dtype=9), INVALID),
+    (dict(reserved=1), INVALID),
+    (dict(nnz=-1), INVALID),
+    (dict(nnz=257), INVALID),
+    (dict(rows=1 << 20, cols=1 << 20, nnz=1 << 31), OVERFLOW),
+    (dict(bitmask=0), INVALID),
+    (dict(row_offsets=0), INVALID),
+    (dict(values=0), INVALID),
+    (dict(values=0, nnz=0), OK),
+    (dict(bitmask=0x10004), INVALID),
+    (dict(values=0x20008), INVALID),
+    (dict(row_offsets=0x30002), INVALID),
+])
+def test_check_matrix(L, kw, status):
+    m = _mat(**kw)
+    assert L.spl_check_matrix(ctypes.byref(m)) == status
+
+
+def test_null_view(L):
+    assert L.spl_check_matrix(None) == INVALID
+
+
+def test_sparse_linear_argument_checks(L):
+    m = _mat()
+    X, Y = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000)
+    f = L.spl_sparse_linear_ex
+    assert f(None, 2, ctypes.byref(m), Y, 0, None) == INVALID
+    assert f(X, 2, ctypes.byref(m), None, 0, None) == INVALID
+    assert f(X, -1, ctypes.byref(m), Y, 0, None) == INVALID
+    assert f(None, 0, ctypes.byref(m), None, 0, None) == OK            # M = 0 is a no-op
+    assert f(ctypes.c_void_p(0x40002), 2, ctypes.byref(m), Y, 0, None) == INVALID
+    assert f(X, 2, ctypes.byref(m), Y, 7, None) == INVALID            # unknown algorithm
+    assert f(X, 33, ctypes.byref(m), Y, 1, None) == UNSUPPORTED       # decode family is M <= 32
+    m8 = _mat(dtype=3)
+    assert f(X, 2, ctypes.byref(m8), Y, 0, None) == UNSUPPORTED       # int8 view needs the int8 entry
+    mk = _mat(cols=100)
+    assert f(X, 2, ctypes.byref(mk), Y, 0, None) == UNSUPPORTED       # K % 8 != 0
+    assert f(X, 2, None, Y, 0, None) == INVALID
+
+
+def test_int8_argument_checks(L):
+    m = _mat(dtype=3)
+    X, Y, s = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x60000)
+    f = L.spl_sparse_linear_int8
+    assert f(X, None, 2, ctypes.byref(m), s, Y, None, None) == INVALID
+    assert f(X, s, 2, ctypes.byref(m), None, Y, None, None) == INVALID
+    assert f(X, s, 2, ctypes.byref(m), s, Y, ctypes.c_void_p(0x70004), None) == INVALID
+    mk = _mat(dtype=3, cols=40)
+    assert f(X, s, 2, ctypes.byref(mk), s, Y, None, None) == UNSUPPORTED
+    mb = _mat(dtype=2)
+    assert f(X, s, 2, ctypes.byref(mb), s, Y, None, None) == UNSUPPORTED
+    assert f(None, None, 0, ctypes.byref(m), None, None, None, None) == OK
+
+
+def test_pack_argument_checks(L):
+    W, ro = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x20000)
+    nnz = ctypes.c_int64(0)
+    assert L.spl_pack_count(None, 2, None, 4, 4, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 4, 4, ro, None, None) == INVALID
+    assert L.spl_pack_count(W, 5, None, 4, 4, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 0, 4, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 1 << 31, 4, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, ro, None, None, None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, ro, ctypes.c_void_p(0x30004), None, None) == INVALID
+
+
+def test_dense_argument_checks(L):
+    X, Y, W = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x10000)
+    assert L.spl_dense_linear_ex(X, 2, None, 2, 8, 8, Y, 0, None) == INVALID
+    assert L.spl_dense_linear_ex(X, 2, W, 3, 8, 8, Y, 0, None) == INVALID
+    assert L.spl_dense_linear_ex(X, 2, W, 2, 8, 12, Y, 0, None) == UNSUPPORTED
+    assert L.spl_dense_linear_ex(X, 40, W, 2, 8, 8, Y, 1, None) == UNSUPPORTED
+    assert L.spl_dense_linear_int8(X, None, 2, W, X, 8, 16, Y, None, None) == INVALID
+    assert L.spl_dense_linear_int8(X, X, 2, W, X, 8, 24, Y, None, None) == UNSUPPORTED

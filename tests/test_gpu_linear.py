@@ -1,0 +1,142 @@
+"""fp16/bf16 sparse linear layers on the GPU vs the oracle.
+
+Tolerance (fp16/bf16 outputs): |y - y64| <= max(2e-2, 1e-2 |y64|) per element.
+Exact-arithmetic inputs and identity activations are compared bit for bit.
+Both kernel families are forced for every batch size they accept."""
+import numpy as np
+import pytest
+
+import synth
+from tests._helpers import assert_close, from_dev_bits, from_dev_f64, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def spl():
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    return spl
+
+
+def _pack(spl, W, mask, dtype):
+    import torch
+
+    return spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+
+
+DECODE_M = [1, 2, 3, 4, 5, 8, 15, 16, 17, 31, 32]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (15, 64, 0.7), (17, 264, 0.5), (100, 1000, 0.7),
+                                   (48, 2056, 0.0), (33, 512, 1.0)])
+def test_decode_small(orc, spl, dtype, N, K, s):
+    W, mask = synth.weight(200 + N, N, K, dtype, s)
+    X = synth.activations(300 + K, 32, K, dtype)
+    ref_p = orc.pack(W, dtype, mask)
+    Wc = _pack(spl, W, mask, dtype)
+    Xd = to_dev(X, dtype)
+    ref = orc.linear_f64(X, ref_p)
+    for M in DECODE_M:
+        Y = spl.sparse_linear(Xd[:M].contiguous(), Wc, algo="decode")
+        assert_close(from_dev_f64(Y), ref[:M], f"decode {dtype} N={N} K={K} s={s} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_decode_exact_arithmetic(orc, spl, dtype):
+    rng = np.random.default_rng(17)
+    N, K = 70, 1064
+    wi = rng.integers(-15, 16, size=(N, K))
+    xi = rng.integers(-3, 4, size=(32, K))
+    W = synth.round_to((wi / 64.0).astype(np.float32), dtype)
+    X = synth.round_to(xi.astype(np.float32), dtype)
+    mask = (rng.random((N, K)) < 0.35).astype(np.uint8)
+    ref_p = orc.pack(W, dtype, mask)
+    Wc = _pack(spl, W, mask, dtype)
+    ref = orc.linear_f64(X, ref_p)                     # exact: all partial sums are multiples of 2^-6
+    expect = synth.round_to(ref.astype(np.float32), dtype)
+    Xd = to_dev(X, dtype)
+    for M in (1, 4, 16, 17, 32):
+        Y = spl.sparse_linear(Xd[:M].contiguous(), Wc, algo="decode")
+        got = from_dev_bits(Y)
+        norm = lambda a: np.where(a == 0x8000, np.uint16(0), a)   # +0 == -0
+        assert np.array_equal(norm(got), norm(expect[:M])), f"M={M}"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_decode_identity_activations(orc, spl, dtype):
+    N, K = 37, 32                                      # X = I_K (M = K = 32) -> Y = (W . Mask)^T
+    W, mask = synth.weight(77, N, K, dtype, 0.6)
+    X = synth.round_to(np.eye(K, dtype=np.float32), dtype)
+    Wc = _pack(spl, W, mask, dtype)
+    Y = spl.sparse_linear(to_dev(X, dtype), Wc, algo="decode")
+    got = from_dev_bits(Y)
+    expect = np.where(mask.astype(bool), W, np.uint16(0)).T
+    norm = lambda a: np.where(a == 0x8000, 0, a)
+    assert np.array_equal(norm(got), norm(expect))
+
+
+CFG2 = [(name, N, K) for (name, N, K) in synth.LLAMA2_7B_LINEARS]
+
+
+@pytest.mark.parametrize("name,N,K", CFG2[3:])      # o (4096x4096), gate, up, down
+def test_decode_llama_shapes_bf16_70(orc, spl, name, N, K):
+    j = [n for n, _, _ in synth.LLAMA2_7B_LINEARS].index(name)
+    W, mask = synth.weight(synth.weight_seed(0, j), N, K, "bf16", 0.7)
+    X = synth.activations(synth.activation_seed(j), 16, K, "bf16")
+    ref_p = orc.pack(W, "bf16", mask)
+    Wc = _pack(spl, W, mask, "bf16")
+    ref = orc.linear_f64(X, ref_p)
+    Xd = to_dev(X, "bf16")
+    for M in (1, 4, 16):
+        Y = spl.sparse_linear(Xd[:M].contiguous(), Wc)
+        assert_close(from_dev_f64(Y), ref[:M], f"{name} M={M}")
+
+
+def test_decode_cfg1_fp16_50(orc, spl):
+    W, mask = synth.weight(0, 4096, 4096, "f16", 0.5)
+    X = synth.activations(1, 1, 4096, "f16")
+    ref = orc.linear_f64(X, orc.pack(W, "f16", mask))
+    Wc = _pack(spl, W, mask, "f16")
+    Y = spl.sparse_linear(to_dev(X, "f16"), Wc)
+    assert_close(from_dev_f64(Y), ref, "cfg1")
+
+
+def test_decode_deterministic_and_overwrites(orc, spl):
+    import torch
+
+    W, mask = synth.weight(5, 300, 2048, "bf16", 0.7)
+    X = synth.activations(6, 7, 2048, "bf16")
+    Wc = _pack(spl, W, mask, "bf16")
+    Xd = to_dev(X, "bf16")
+    buf = torch.full((7 * 300 + 64,), float("nan"), dtype=torch.bfloat16, device="cuda")
+    Y1 = buf[: 7 * 300].view(7, 300)
+    spl.sparse_linear(Xd, Wc, out=Y1)
+    assert not torch.isnan(Y1).any()                  # every output written
+    assert torch.isnan(buf[7 * 300:]).all()           # nothing written past Y
+    Y2 = spl.sparse_linear(Xd, Wc)
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K", [(16, 64), (100, 1000), (4096, 4096)])
+def test_dense_decode(orc, spl, dtype, N, K):
+    W, _ = synth.weight(900 + N, N, K, dtype, 0.0)
+    X = synth.activations(901, 32, K, dtype)
+    ref = orc.dense_f64(X, W, dtype)
+    Wd = to_dev(W, dtype)
+    Xd = to_dev(X, dtype)
+    for M in (1, 5, 16, 17, 32):
+        Y = spl.dense_linear(Xd[:M].contiguous(), Wd, algo="decode")
+        assert_close(from_dev_f64(Y), ref[:M], f"dense decode {dtype} M={M}")
+
+
+def test_zero_batch_is_noop(spl):
+    import torch
+
+    W, mask = synth.weight(1, 8, 64, "bf16", 0.5)
+    Wc = _pack(spl, W, mask, "bf16")
+    Y = spl.sparse_linear(torch.empty((0, 64), dtype=torch.bfloat16, device="cuda"), Wc)
+    assert Y.shape == (0, 8)
