@@ -48,19 +48,38 @@ def activation_seed(j: int) -> int:
     return 9000 + j
 
 
-def normal_f32(seed: int, shape, std: float = 1.0) -> np.ndarray:
+_CHUNK = 1 << 20
+
+
+def normal_f32(seed: int, shape, std: float = 1.0, out: np.ndarray | None = None) -> np.ndarray:
+    """N(0, std^2) binary32 draws from PCG64(seed), in row-major order.  Filled
+    in chunks from one stream, so a larger draw extends a smaller one."""
+    n = int(np.prod(shape))
+    if out is None:
+        out = np.empty(n, dtype=np.float32)
+    flat = out.reshape(-1)
+    assert flat.size == n and flat.dtype == np.float32
     rng = np.random.Generator(np.random.PCG64(seed))
-    x = rng.standard_normal(size=int(np.prod(shape)), dtype=np.float32)
+    for i in range(0, n, _CHUNK):
+        rng.standard_normal(dtype=np.float32, out=flat[i:i + _CHUNK])
     if std != 1.0:
-        x *= np.float32(std)
-    return x.reshape(shape)
+        flat *= np.float32(std)
+    return out.reshape(shape)
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """binary32 -> bfloat16 bits, round to nearest even (finite inputs)."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.reshape(-1).view(np.uint32)
+    out = np.empty(u.size, dtype=np.uint16)
+    for i in range(0, u.size, _CHUNK):
+        c = u[i:i + _CHUNK]
+        bias = (c >> np.uint32(16)) & np.uint32(1)
+        bias += np.uint32(0x7FFF)
+        bias += c
+        bias >>= np.uint32(16)
+        out[i:i + _CHUNK] = bias
+    return out.reshape(x.shape)
 
 
 def round_f16(x: np.ndarray) -> np.ndarray:
@@ -102,21 +121,31 @@ def magnitude_mask(bits: np.ndarray, sparsity) -> np.ndarray:
     """uint8 keep-mask of a 16-bit float matrix: zero exactly floor(s*numel)
     entries of smallest |w|, ties in ascending row-major order."""
     num, den = parse_sparsity(sparsity)
-    key = (np.ascontiguousarray(bits, dtype=np.uint16) & np.uint16(0x7FFF)).ravel()
-    numel = key.size
+    flat = np.ascontiguousarray(bits, dtype=np.uint16).reshape(-1)
+    numel = flat.size
     z = numel * num // den
-    mask = np.ones(numel, dtype=np.uint8)
     if z <= 0:
-        return mask.reshape(bits.shape)
+        return np.ones(bits.shape, dtype=np.uint8)
     if z >= numel:
         return np.zeros(bits.shape, dtype=np.uint8)
-    counts = np.bincount(key, minlength=0x8000)
+    counts = np.zeros(0x8000, dtype=np.int64)
+    for i in range(0, numel, _CHUNK):
+        counts += np.bincount(flat[i:i + _CHUNK] & np.uint16(0x7FFF), minlength=0x8000)
     cum = np.cumsum(counts)
-    t = int(np.searchsorted(cum, z, side="right"))   # first key value whose cumulative count exceeds z
+    t = int(np.searchsorted(cum, z, side="right"))   # first magnitude key whose cumulative count exceeds z
     below = int(cum[t - 1]) if t > 0 else 0          # entries strictly smaller than t: all zeroed
-    mask[key < t] = 0
-    ties = np.flatnonzero(key == t)
-    mask[ties[: z - below]] = 0
+    tie_zero = z - below                             # entries equal to t zeroed, lowest indices first
+    mask = np.empty(numel, dtype=np.uint8)
+    for i in range(0, numel, _CHUNK):
+        key = flat[i:i + _CHUNK] & np.uint16(0x7FFF)
+        m = mask[i:i + _CHUNK]
+        np.greater(key, t, out=m.view(np.bool_))
+        ties = np.flatnonzero(key == t)
+        if tie_zero >= ties.size:
+            tie_zero -= ties.size                    # all of these ties are zeroed
+        else:
+            m[ties[tie_zero:]] = 1                   # the remaining ties are kept
+            tie_zero = 0
     return mask.reshape(bits.shape)
 
 
