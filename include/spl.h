@@ -25,21 +25,38 @@
  *     failed check returns an error code and launches nothing.  Errors
  *     reported by the HIP runtime at launch map to SPL_ERR_DEVICE.  Nothing
  *     throws across this interface.
- *   - Device buffers must be 16-byte aligned.  Kernels may read, but never
- *     write, up to 15 bytes past the end of `values` inside the same
- *     aligned 16-byte block.
+ *   - Device buffers must be 16-byte aligned.  The `values` array of a
+ *     compressed matrix must be followed by at least 16 readable bytes:
+ *     kernels read (never write) up to 16 bytes past the last payload.
  *
- * The compressed matrix (canonical encoding, lossless)
- *   bitmask     uint32 [N][ceil(K/32)]; bit j (least significant first) of
- *               word w of row n is set iff position (n, 32w + j) is kept;
- *               bits at or past K are 0.
- *   values      the kept payloads, row by row, ascending column order, as
- *               raw bit copies (fp16 / bf16: 2 bytes; int8: 1 byte).
- *   row_offsets int32 [N+1]; row_offsets[n] is the index in `values` of the
- *               first kept entry of row n, row_offsets[N] = nnz < 2^31.
+ * Two lossless encodings of a compressed matrix
+ *
+ *   Row layout (SPL_LAYOUT_ROWS: the interchange format written by the packer;
+ *   paper section 2.4.1, one block per row):
+ *     bitmask     uint32 [N][ceil(K/32)]; bit j (least significant first) of
+ *                 word w of row n is set iff position (n, 32w + j) is kept;
+ *                 bits at or past K are 0.
+ *     values      the kept payloads, row by row, ascending column order, as
+ *                 raw bit copies (fp16 / bf16: 2 bytes; int8: 1 byte).
+ *     row_offsets int32 [N+1]; row_offsets[n] is the index in `values` of the
+ *                 first kept entry of row n, row_offsets[N] = nnz < 2^31.
  *   Reading of the paper: its worked example packs one 16-lane VNNI register
- *   (two interleaved rows); here the block is a whole row in column order,
- *   and the bit order is least-significant-bit first.
+ *   (two interleaved rows); the row layout takes a whole row as the block, in
+ *   column order, with the bit order least-significant-bit first.
+ *
+ *   Tile layout (SPL_LAYOUT_TILE16: the layout the linear kernels read; paper
+ *   section 2.4.2, submatrices sized for the register file, each with its own
+ *   bitmask and dense values).  Tiles are 16 rows x 32 columns, one MFMA
+ *   operand; with B = ceil(N/16) row blocks and S = ceil(K/32) column steps,
+ *   tile (b, s) has index t = b*S + s and
+ *     bitmask      uint32 [B*S][16]: word r of tile t holds row 16b+r,
+ *                  columns 32s..32s+31 (bit j = column 32s+j); rows >= N and
+ *                  columns >= K are 0;
+ *     values       each tile's kept payloads in tile order, inside a tile row
+ *                  by row in ascending column order;
+ *     tile_offsets int32 [B*S + 1]: index in `values` of tile t's first
+ *                  payload; tile_offsets[B*S] = nnz.
+ *   Both layouts hold the same payloads; spl_retile16 converts rows -> tiles.
  */
 #ifndef SPL_H
 #define SPL_H
@@ -68,17 +85,20 @@ typedef enum { SPL_F16 = 1, SPL_BF16 = 2, SPL_I8 = 3 } spl_dtype;
  * tiles are decompressed into LDS and feed bf16/fp16 MFMA (any M). */
 typedef enum { SPL_ALGO_AUTO = 0, SPL_ALGO_DECODE = 1, SPL_ALGO_PREFILL = 2 } spl_algo;
 
+typedef enum { SPL_LAYOUT_ROWS = 0, SPL_LAYOUT_TILE16 = 1 } spl_layout;
+
 /* Non-owning view of a compressed matrix (all pointers device pointers).
  * The arrays must stay alive until work queued with the view completes. */
 typedef struct {
   int64_t rows;                  /* N */
   int64_t cols;                  /* K */
   int32_t dtype;                 /* spl_dtype of `values` */
-  int32_t reserved;              /* must be 0 */
-  int64_t nnz;                   /* == row_offsets[N] */
-  const uint32_t* bitmask;       /* [N][ceil(K/32)] */
+  int32_t layout;                /* spl_layout */
+  int64_t nnz;                   /* number of stored payloads */
+  const uint32_t* bitmask;       /* rows: [N][ceil(K/32)]; tiles: [B*S][16] */
   const void* values;            /* [nnz] payloads */
-  const int32_t* row_offsets;    /* [N+1] */
+  const int32_t* row_offsets;    /* rows: [N+1]; tiles: unused (may be NULL) */
+  const int32_t* tile_offsets;   /* tiles: [B*S + 1]; rows: unused (may be NULL) */
 } spl_matrix;
 
 /* Library version, (major << 16) | minor. */
@@ -88,10 +108,23 @@ int32_t spl_version(void);
 const char* spl_status_string(spl_status s);
 
 /* Host-only consistency check of a view's scalar fields and pointers
- * (no device access): non-null arrays (values may be NULL only if nnz == 0),
- * rows, cols >= 1, dtype known, reserved == 0, 0 <= nnz < 2^31, and 16-byte
- * alignment of bitmask and values. */
+ * (no device access): rows, cols >= 1, dtype and layout known,
+ * 0 <= nnz < 2^31, nnz <= rows*cols, the layout's arrays non-null (values may
+ * be NULL only if nnz == 0), 16-byte alignment of bitmask and values. */
 spl_status spl_check_matrix(const spl_matrix* Wc);
+
+/* Sizes of the tile layout of an N x K matrix: number of tiles B*S (the
+ * bitmask has 16 words per tile, tile_offsets B*S + 1 entries). */
+int64_t spl_tile16_count(int64_t N, int64_t K);
+
+/* Convert a row-layout matrix to the tile layout (a permutation of payloads
+ * and bitmask bits; paper section 2.4.2).
+ *   rows_in       view with layout SPL_LAYOUT_ROWS.
+ *   bitmask_out   out [B*S][16] uint32, fully written.
+ *   values_out    out [nnz] payloads (must not alias rows_in->values).
+ *   tile_offsets_out out [B*S + 1] int32. */
+spl_status spl_retile16(const spl_matrix* rows_in, uint32_t* bitmask_out, void* values_out,
+                        int32_t* tile_offsets_out, hipStream_t stream);
 
 /* Pack, step 1 of 2 (paper section 2.4.1: count the kept entries).
  *   W           [N][K] payloads of `dtype` (F16, BF16 or I8).
@@ -114,11 +147,12 @@ spl_status spl_pack_sparse(const void* W, int32_t dtype, const uint8_t* mask, in
                            const int32_t* row_offsets, uint32_t* bitmask, void* values,
                            hipStream_t stream);
 
-/* Decompress to a dense [N][K] matrix of the view's dtype: kept positions
- * receive their payload, every other position +0. */
+/* Decompress (either layout) to a dense [N][K] matrix of the view's dtype:
+ * kept positions receive their payload, every other position +0. */
 spl_status spl_unpack(const spl_matrix* Wc, void* W_dense, hipStream_t stream);
 
 /* Sparse linear layer, fp16 or bf16 (paper section 2.4.2).
+ *   Wc in the tile layout (SPL_ERR_UNSUPPORTED for the row layout).
  *   X  [M][K] of Wc->dtype; M >= 0 (M == 0 is a no-op).
  *   Y  out [M][N] of Wc->dtype, overwritten.  fp32 accumulation, one
  *      round-to-nearest-even conversion per output.  No bias.
@@ -133,7 +167,7 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
 /* Sparse-quantized linear layer (paper section 3.4: int8 weights and
  * int8 activations).
  *   Xq        [M][K] int8 activation codes; x_scales [M] float32.
- *   Wqc       view with dtype SPL_I8; w_scales [N] float32.
+ *   Wqc       view with dtype SPL_I8 in the tile layout; w_scales [N] float32.
  *   acc       acc[m][n] = sum over kept k of Xq[m][k] * Wq[n][k], exact int32.
  *   Y         out [M][N] fp16: round-to-nearest-even of
  *             ((float)acc * x_scales[m]) * w_scales[n], each product rounded

@@ -62,6 +62,10 @@ def _load():
         "orc_dense_f64": (None, [P, I64, I64, I32, P, I64, P, ctypes.c_int]),
         "orc_linear_i8": (ctypes.c_int, [P, P, I64, I64, P, P, P, P, I64, P, P, ctypes.c_int]),
         "orc_dense_i8": (ctypes.c_int, [P, P, I64, I64, P, P, I64, P, P, ctypes.c_int]),
+        "orc_tile_blocks": (I64, [I64]),
+        "orc_tile_ksteps": (I64, [I64]),
+        "orc_pack_tiled": (None, [P, I32, P, I64, I64, P, P, P]),
+        "orc_unpack_tiled": (None, [P, P, P, I32, I64, I64, P]),
         "orc_f16_to_f64_array": (None, [P, I64, P]),
         "orc_bf16_to_f64_array": (None, [P, I64, P]),
         "orc_f32_to_f16_array": (None, [P, I64, P]),
@@ -127,6 +131,49 @@ def pack(W: np.ndarray, dtype: str, mask: np.ndarray | None = None) -> Packed:
     row_offsets = np.zeros(N + 1, dtype=np.int32)
     lib.orc_pack(_ptr(W), _code(dtype), _ptr(mask), N, K, _ptr(bitmask), _ptr(values), _ptr(row_offsets))
     return Packed(bitmask, values[:nnz], row_offsets, N, K, dtype)
+
+
+@dataclass
+class Tiled:
+    """The GPU tile layout: 16 x 32 submatrices, each with its own 16 bitmask
+    words and its kept values (see spl_oracle.c for the exact definition)."""
+
+    bitmask: np.ndarray       # uint32 [B*S*16]
+    values: np.ndarray        # payloads [nnz]
+    tile_offsets: np.ndarray  # int32 [B*S + 1]
+    N: int
+    K: int
+    dtype: str
+
+    @property
+    def nnz(self) -> int:
+        return int(self.tile_offsets[-1])
+
+
+def pack_tiled(W: np.ndarray, dtype: str, mask: np.ndarray | None = None) -> Tiled:
+    """Submatrix encoder of section 2.4.2 with 16 x 32 tiles."""
+    lib = _load()
+    W = np.ascontiguousarray(W)
+    assert W.dtype == _payload_dtype(dtype)
+    N, K = W.shape
+    if mask is not None:
+        mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    nnz = int(lib.orc_pack_nnz(_ptr(W), _code(dtype), _ptr(mask), N, K))
+    B, S = int(lib.orc_tile_blocks(N)), int(lib.orc_tile_ksteps(K))
+    bitmask = np.zeros(B * S * 16, dtype=np.uint32)
+    values = np.zeros(max(nnz, 1), dtype=_payload_dtype(dtype))
+    offs = np.zeros(B * S + 1, dtype=np.int32)
+    lib.orc_pack_tiled(_ptr(W), _code(dtype), _ptr(mask), N, K, _ptr(bitmask), _ptr(values), _ptr(offs))
+    return Tiled(bitmask, values[:nnz], offs, N, K, dtype)
+
+
+def unpack_tiled(p: Tiled) -> np.ndarray:
+    lib = _load()
+    out = np.zeros((p.N, p.K), dtype=_payload_dtype(p.dtype))
+    vals = p.values if p.values.size else np.zeros(1, dtype=_payload_dtype(p.dtype))
+    lib.orc_unpack_tiled(_ptr(p.bitmask), _ptr(np.ascontiguousarray(vals)), _ptr(p.tile_offsets), _code(p.dtype),
+                         p.N, p.K, _ptr(out))
+    return out
 
 
 def unpack(p: Packed) -> np.ndarray:

@@ -25,6 +25,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libspl.so")
 
 F16, BF16, I8 = 1, 2, 3
+LAYOUT = {"rows": 0, "tile16": 1}
 ALGO = {"auto": 0, "decode": 1, "prefill": 2}
 _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "overflow", 4: "HIP runtime error"}
 _TORCH_DTYPE = {torch.float16: F16, torch.bfloat16: BF16, torch.int8: I8}
@@ -42,11 +43,12 @@ class _Matrix(ctypes.Structure):
         ("rows", ctypes.c_int64),
         ("cols", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("layout", ctypes.c_int32),
         ("nnz", ctypes.c_int64),
         ("bitmask", ctypes.c_void_p),
         ("values", ctypes.c_void_p),
         ("row_offsets", ctypes.c_void_p),
+        ("tile_offsets", ctypes.c_void_p),
     ]
 
 
@@ -67,6 +69,8 @@ def lib() -> ctypes.CDLL:
         "spl_version": (I32, []),
         "spl_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "spl_check_matrix": (ctypes.c_int, [MP]),
+        "spl_tile16_count": (I64, [I64, I64]),
+        "spl_retile16": (ctypes.c_int, [MP, P, P, P, P]),
         "spl_pack_count": (ctypes.c_int, [P, I32, P, I64, I64, P, ctypes.POINTER(I64), P]),
         "spl_pack_sparse": (ctypes.c_int, [P, I32, P, I64, I64, P, P, P, P]),
         "spl_unpack": (ctypes.c_int, [MP, P, P]),
@@ -109,43 +113,54 @@ def _dev_tensor(t: torch.Tensor, name: str) -> torch.Tensor:
 
 @dataclass
 class SparseMatrix:
-    """A compressed [N][K] matrix: the canonical bitmask-expansion encoding."""
+    """A compressed [N][K] matrix in one of the two layouts of include/spl.h:
+    "rows" (row-layout bitmask, values, row_offsets) or "tile16" (16 x 32
+    submatrices: tile-major bitmask, values, tile_offsets)."""
 
-    bitmask: torch.Tensor      # int32 view of uint32 words [N][ceil(K/32)]
-    values: torch.Tensor       # payloads (fp16 / bf16 / int8), length >= nnz
-    row_offsets: torch.Tensor  # int32 [N+1]
+    bitmask: torch.Tensor              # int32 view of the uint32 bitmask words
+    values: torch.Tensor               # payloads (fp16 / bf16 / int8), length >= nnz (+16 bytes of tail)
+    row_offsets: torch.Tensor | None   # int32 [N+1] (rows layout)
+    tile_offsets: torch.Tensor | None  # int32 [B*S+1] (tile16 layout)
     rows: int
     cols: int
     nnz: int
+    layout: str = "rows"
 
     @property
     def dtype(self) -> torch.dtype:
         return self.values.dtype
 
     def view(self) -> _Matrix:
-        return _Matrix(self.rows, self.cols, _TORCH_DTYPE[self.values.dtype], 0, self.nnz,
-                       self.bitmask.data_ptr(), self.values.data_ptr() if self.nnz > 0 else 0,
-                       self.row_offsets.data_ptr())
+        return _Matrix(self.rows, self.cols, _TORCH_DTYPE[self.values.dtype], LAYOUT[self.layout], self.nnz,
+                       self.bitmask.data_ptr(), self.values.data_ptr(),
+                       self.row_offsets.data_ptr() if self.row_offsets is not None else 0,
+                       self.tile_offsets.data_ptr() if self.tile_offsets is not None else 0)
 
     def compressed_bytes(self) -> int:
-        """Bytes of the encoding: payloads + bitmask + row offsets."""
-        return self.nnz * self.values.element_size() + self.bitmask.numel() * 4 + self.row_offsets.numel() * 4
+        """Bytes of the encoding: payloads + bitmask + offsets."""
+        offs = self.row_offsets if self.layout == "rows" else self.tile_offsets
+        return self.nnz * self.values.element_size() + self.bitmask.numel() * 4 + offs.numel() * 4
 
 
 def _values_buffer(nnz: int, dtype: torch.dtype, device) -> torch.Tensor:
-    # whole 16-byte blocks, so vector reads of the last payloads stay inside the allocation
+    # payloads rounded up to 16 bytes plus 16 readable bytes of tail: kernels may
+    # read (never write) up to 16 bytes past the last payload
     esz = torch.empty((), dtype=dtype).element_size()
-    n = max(16, ((nnz * esz + 15) // 16) * 16) // esz
+    n = (((nnz * esz + 15) // 16) * 16 + 16) // esz
     return torch.zeros(n, dtype=dtype, device=device)
 
 
-def pack_sparse(W: torch.Tensor, mask: torch.Tensor | None = None, stream=None) -> SparseMatrix:
+def pack_sparse(W: torch.Tensor, mask: torch.Tensor | None = None, layout: str = "tile16",
+                stream=None) -> SparseMatrix:
     """Compress W [N][K] (fp16/bf16/int8) under `mask` (uint8/bool, non-zero = kept;
-    None = keep the non-zero payloads)."""
+    None = keep the non-zero payloads).  layout="tile16" (default) is the layout
+    the linear kernels read; "rows" is the row-layout interchange format."""
     L = lib()
     _dev_tensor(W, "W")
     if W.dim() != 2 or W.dtype not in _TORCH_DTYPE:
         raise ValueError("W must be a 2-D fp16/bf16/int8 tensor")
+    if layout not in LAYOUT:
+        raise ValueError(f"unknown layout {layout!r}")
     N, K = W.shape
     if mask is not None:
         _dev_tensor(mask, "mask")
@@ -166,7 +181,24 @@ def pack_sparse(W: torch.Tensor, mask: torch.Tensor | None = None, stream=None) 
     values = _values_buffer(nnz.value, W.dtype, W.device)
     _check("spl_pack_sparse", L.spl_pack_sparse(_ptr(W), code, _ptr(mask), N, K, _ptr(row_offsets),
                                                 _ptr(bitmask), _ptr(values), s))
-    return SparseMatrix(bitmask, values, row_offsets, N, K, nnz.value)
+    rows = SparseMatrix(bitmask, values, row_offsets, None, N, K, nnz.value, "rows")
+    return rows if layout == "rows" else retile16(rows, stream=stream)
+
+
+def retile16(Wc: SparseMatrix, stream=None) -> SparseMatrix:
+    """Row layout -> tile layout (16 x 32 submatrices)."""
+    L = lib()
+    if Wc.layout != "rows":
+        raise ValueError("retile16 expects the row layout")
+    T = int(L.spl_tile16_count(Wc.rows, Wc.cols))
+    dev = Wc.values.device
+    bitmask = torch.empty(T * 16, dtype=torch.int32, device=dev)
+    tile_offsets = torch.empty(T + 1, dtype=torch.int32, device=dev)
+    values = _values_buffer(Wc.nnz, Wc.dtype, dev)
+    view = Wc.view()
+    _check("spl_retile16", L.spl_retile16(ctypes.byref(view), _ptr(bitmask), _ptr(values), _ptr(tile_offsets),
+                                          _stream(stream)))
+    return SparseMatrix(bitmask, values, None, tile_offsets, Wc.rows, Wc.cols, Wc.nnz, "tile16")
 
 
 def unpack(Wc: SparseMatrix, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

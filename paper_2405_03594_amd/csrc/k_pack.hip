@@ -8,6 +8,9 @@
 //              kept lane's rank among them (v_mbcnt) is its slot in `values`.
 // unpack     : the inverse walk; a lane whose bit is set takes the value at its
 //              rank, every other lane writes +0.
+// retile16   : row layout -> tile layout (16 x 32 submatrices, paper section
+//              2.4.2): per-tile counts and a scan give the tile offsets, then one
+//              wave per row moves each word's values to their tile position.
 #include "spl_common.h"
 
 namespace spl {
@@ -128,7 +131,119 @@ __global__ void __launch_bounds__(256) k_unpack(const uint32_t* bitmask, const v
   }
 }
 
+// ---- tile layout (16 x 32 submatrices) ----
+
+// Thread (tile t, row r): copy the row's bitmask word into tile order and
+// count the tile's kept entries into tile_offsets[t].
+__global__ void __launch_bounds__(256) k_tile_count(const uint32_t* __restrict__ bm_rows, int64_t N, int64_t K,
+                                                    uint32_t* __restrict__ bm_tiles, int32_t* __restrict__ counts) {
+  const int64_t S = tile_steps(K);
+  const int64_t T = tile_blocks(N) * S;
+  const int64_t t = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int r = threadIdx.x & 15;
+  uint32_t w = 0;
+  if (t < T) {
+    const int64_t b = t / S, s = t - b * S;
+    const int64_t n = 16 * b + r;
+    if (n < N) w = bm_rows[n * S + s];
+    bm_tiles[t * 16 + r] = w;
+  }
+  uint32_t c = __popc(w);
+  for (int off = 8; off > 0; off >>= 1) c += __shfl_xor(c, off, 16);
+  if (t < T && r == 0) counts[t] = (int32_t)c;
+}
+
+// One wave per row: for each 32-column word, the row's stored values move from
+// their row-layout position to their tile-layout position.
+template <int EB>
+__global__ void __launch_bounds__(256) k_tile_scatter(const uint32_t* __restrict__ bm_rows,
+                                                      const void* __restrict__ vals_rows,
+                                                      const int32_t* __restrict__ row_offsets, int64_t N, int64_t K,
+                                                      const int32_t* __restrict__ tile_offsets,
+                                                      void* __restrict__ vals_tiles) {
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  const int lane = threadIdx.x & 63;
+  const int64_t S = tile_steps(K);
+  const int64_t b = n / 16;
+  const int r = (int)(n - 16 * b);
+  int64_t carry = row_offsets[n];
+  for (int64_t s0 = 0; s0 < S; s0 += kWave) {
+    const int64_t s = s0 + lane;
+    const uint32_t w = s < S ? bm_rows[n * S + s] : 0u;
+    const uint32_t pc = __popc(w);
+    uint32_t incl = pc;
+    for (int d = 1; d < kWave; d <<= 1) {
+      const uint32_t up = __shfl_up(incl, d);
+      if (lane >= d) incl += up;
+    }
+    const uint32_t total = __shfl(incl, kWave - 1);
+    if (pc) {
+      int64_t src = carry + (incl - pc);
+      int64_t dst = tile_offsets[b * S + s];
+      for (int rr = 0; rr < r; ++rr) dst += __popc(bm_rows[(16 * b + rr) * S + s]);
+      for (uint32_t i = 0; i < pc; ++i) {
+        if constexpr (EB == 2) {
+          static_cast<uint16_t*>(vals_tiles)[dst + i] = static_cast<const uint16_t*>(vals_rows)[src + i];
+        } else {
+          static_cast<int8_t*>(vals_tiles)[dst + i] = static_cast<const int8_t*>(vals_rows)[src + i];
+        }
+      }
+    }
+    carry += total;
+  }
+}
+
+// Thread (tile t, row r): decode one tile row into the dense matrix.
+template <int EB>
+__global__ void __launch_bounds__(256) k_unpack_tiled(const uint32_t* __restrict__ bm_tiles,
+                                                      const void* __restrict__ values,
+                                                      const int32_t* __restrict__ tile_offsets, int64_t N, int64_t K,
+                                                      void* __restrict__ Wd) {
+  const int64_t S = tile_steps(K);
+  const int64_t T = tile_blocks(N) * S;
+  const int64_t t = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int r = threadIdx.x & 15;
+  if (t >= T) return;
+  const int64_t b = t / S, s = t - b * S;
+  const int64_t n = 16 * b + r;
+  if (n >= N) return;
+  int64_t src = tile_offsets[t];
+  for (int rr = 0; rr < r; ++rr) src += __popc(bm_tiles[t * 16 + rr]);
+  const uint32_t w = bm_tiles[t * 16 + r];
+  for (int j = 0; j < 32; ++j) {
+    const int64_t k = 32 * s + j;
+    if (k >= K) break;
+    const bool bit = (w >> j) & 1u;
+    if constexpr (EB == 2) {
+      static_cast<uint16_t*>(Wd)[n * K + k] = bit ? static_cast<const uint16_t*>(values)[src] : (uint16_t)0;
+    } else {
+      static_cast<int8_t*>(Wd)[n * K + k] = bit ? static_cast<const int8_t*>(values)[src] : (int8_t)0;
+    }
+    src += bit;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_retile16(const spl_matrix& in, uint32_t* bitmask_t, void* values_t, int32_t* tile_offsets,
+                           hipStream_t s) {
+  const int64_t T = tile_blocks(in.rows) * tile_steps(in.cols);
+  hipLaunchKernelGGL(k_tile_count, dim3((unsigned)((T + 15) / 16)), dim3(256), 0, s, in.bitmask, in.rows, in.cols,
+                     bitmask_t, tile_offsets);
+  hipLaunchKernelGGL(k_scan_offsets, dim3(1), dim3(1024), 0, s, tile_offsets, T);
+  if (in.nnz > 0) {
+    const dim3 grid((unsigned)((in.rows + 3) / 4)), block(256);
+    if (in.dtype == SPL_I8) {
+      hipLaunchKernelGGL(k_tile_scatter<1>, grid, block, 0, s, in.bitmask, in.values, in.row_offsets, in.rows,
+                         in.cols, tile_offsets, values_t);
+    } else {
+      hipLaunchKernelGGL(k_tile_scatter<2>, grid, block, 0, s, in.bitmask, in.values, in.row_offsets, in.rows,
+                         in.cols, tile_offsets, values_t);
+    }
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
                              int32_t* row_offsets, hipStream_t s) {
@@ -154,6 +269,18 @@ hipError_t launch_pack_scatter(const void* W, int32_t dtype, const uint8_t* mask
 }
 
 hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s) {
+  if (Wc.layout == SPL_LAYOUT_TILE16) {
+    const int64_t T = tile_blocks(Wc.rows) * tile_steps(Wc.cols);
+    const dim3 grid((unsigned)((T + 15) / 16)), block(256);
+    if (Wc.dtype == SPL_I8) {
+      hipLaunchKernelGGL(k_unpack_tiled<1>, grid, block, 0, s, Wc.bitmask, Wc.values, Wc.tile_offsets, Wc.rows,
+                         Wc.cols, W_dense);
+    } else {
+      hipLaunchKernelGGL(k_unpack_tiled<2>, grid, block, 0, s, Wc.bitmask, Wc.values, Wc.tile_offsets, Wc.rows,
+                         Wc.cols, W_dense);
+    }
+    return hipGetLastError();
+  }
   const dim3 grid((unsigned)((Wc.rows + 3) / 4)), block(256);
   if (Wc.dtype == SPL_I8) {
     hipLaunchKernelGGL(k_unpack<1>, grid, block, 0, s, Wc.bitmask, Wc.values, Wc.row_offsets, Wc.rows, Wc.cols,

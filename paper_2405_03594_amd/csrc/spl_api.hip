@@ -59,15 +59,38 @@ const char* spl_status_string(spl_status s) {
 spl_status spl_check_matrix(const spl_matrix* Wc) {
   if (!Wc) return SPL_ERR_INVALID_ARG;
   if (!dims_ok(Wc->rows, Wc->cols)) return SPL_ERR_INVALID_ARG;
-  if (!any_dtype(Wc->dtype) || Wc->reserved != 0) return SPL_ERR_INVALID_ARG;
+  if (!any_dtype(Wc->dtype)) return SPL_ERR_INVALID_ARG;
+  if (Wc->layout != SPL_LAYOUT_ROWS && Wc->layout != SPL_LAYOUT_TILE16) return SPL_ERR_INVALID_ARG;
   if (Wc->nnz < 0) return SPL_ERR_INVALID_ARG;
   if (Wc->nnz >= kMaxDim) return SPL_ERR_OVERFLOW;
   if (Wc->nnz > Wc->rows * Wc->cols) return SPL_ERR_INVALID_ARG;
-  if (!Wc->bitmask || !Wc->row_offsets) return SPL_ERR_INVALID_ARG;
+  if (!Wc->bitmask) return SPL_ERR_INVALID_ARG;
+  if (Wc->layout == SPL_LAYOUT_ROWS && !Wc->row_offsets) return SPL_ERR_INVALID_ARG;
+  if (Wc->layout == SPL_LAYOUT_TILE16 && !Wc->tile_offsets) return SPL_ERR_INVALID_ARG;
   if (Wc->nnz > 0 && !Wc->values) return SPL_ERR_INVALID_ARG;
-  if (!aligned(Wc->bitmask, 16) || !aligned(Wc->row_offsets, 4)) return SPL_ERR_INVALID_ARG;
+  if (!aligned(Wc->bitmask, 16)) return SPL_ERR_INVALID_ARG;
+  if (Wc->row_offsets && !aligned(Wc->row_offsets, 4)) return SPL_ERR_INVALID_ARG;
+  if (Wc->tile_offsets && !aligned(Wc->tile_offsets, 4)) return SPL_ERR_INVALID_ARG;
   if (Wc->values && !aligned(Wc->values, 16)) return SPL_ERR_INVALID_ARG;
   return SPL_OK;
+}
+
+int64_t spl_tile16_count(int64_t N, int64_t K) {
+  if (!dims_ok(N, K)) return 0;
+  return ((N + 15) / 16) * ((K + 31) / 32);
+}
+
+spl_status spl_retile16(const spl_matrix* rows_in, uint32_t* bitmask_out, void* values_out,
+                        int32_t* tile_offsets_out, hipStream_t stream) {
+  const spl_status st = spl_check_matrix(rows_in);
+  if (st != SPL_OK) return st;
+  if (rows_in->layout != SPL_LAYOUT_ROWS) return SPL_ERR_INVALID_ARG;
+  if (!bitmask_out || !tile_offsets_out || !aligned(bitmask_out, 16) || !aligned(tile_offsets_out, 4))
+    return SPL_ERR_INVALID_ARG;
+  if (rows_in->nnz > 0 && (!values_out || !aligned(values_out, 16))) return SPL_ERR_INVALID_ARG;
+  if (values_out && values_out == rows_in->values) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_retile16(*rows_in, bitmask_out, values_out, tile_offsets_out, stream));
 }
 
 spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
@@ -108,7 +131,7 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
                                 hipStream_t stream) {
   const spl_status st = spl_check_matrix(Wc);
   if (st != SPL_OK) return st;
-  if (!fp_dtype(Wc->dtype)) return SPL_ERR_UNSUPPORTED;
+  if (!fp_dtype(Wc->dtype) || Wc->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
   if (algo < SPL_ALGO_AUTO || algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
   const spl_status xy = check_xy(X, M, Wc->cols, Wc->rows, Y);
   if (xy != SPL_OK || M == 0) return xy;
@@ -129,7 +152,7 @@ spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream) {
   const spl_status st = spl_check_matrix(Wqc);
   if (st != SPL_OK) return st;
-  if (Wqc->dtype != SPL_I8) return SPL_ERR_UNSUPPORTED;
+  if (Wqc->dtype != SPL_I8 || Wqc->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
   const spl_status xy = check_xy(Xq, M, Wqc->cols, Wqc->rows, Y);
   if (xy != SPL_OK || M == 0) return xy;
   if (!x_scales || !w_scales || !aligned(x_scales, 4) || !aligned(w_scales, 4)) return SPL_ERR_INVALID_ARG;

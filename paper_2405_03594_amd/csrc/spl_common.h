@@ -56,6 +56,9 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 __host__ __device__ __forceinline__ int64_t words_per_row(int64_t K) { return (K + 31) / 32; }
+// Tile layout geometry: 16-row blocks and 32-column steps.
+__host__ __device__ __forceinline__ int64_t tile_blocks(int64_t N) { return (N + 15) / 16; }
+__host__ __device__ __forceinline__ int64_t tile_steps(int64_t K) { return (K + 31) / 32; }
 
 }  // namespace spl
 
@@ -66,6 +69,10 @@ hipError_t launch_pack_count(const void* W, int32_t dtype, const uint8_t* mask, 
 hipError_t launch_pack_scatter(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
                                const int32_t* row_offsets, uint32_t* bitmask, void* values, hipStream_t s);
 hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s);
+hipError_t launch_retile16(const spl_matrix& rows_in, uint32_t* bitmask_t, void* values_t, int32_t* tile_offsets,
+                           hipStream_t s);
+// Y[0..count16) = +0 (16-bit elements).
+hipError_t launch_zero_fill(void* Y, int64_t count16, hipStream_t s);
 
 hipError_t launch_sparse_decode(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
 hipError_t launch_dense_decode(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,

@@ -35,10 +35,14 @@ def from_dev_f64(t) -> np.ndarray:
 
 
 def assert_pack_equal(Wc, ref) -> None:
-    """Bit-exact comparison of a device SparseMatrix with the oracle's Packed."""
+    """Bit-exact comparison of a device SparseMatrix with the oracle's Packed
+    (row layout) or Tiled (tile layout)."""
     assert Wc.nnz == ref.nnz, (Wc.nnz, ref.nnz)
-    assert np.array_equal(Wc.row_offsets.cpu().numpy(), ref.row_offsets)
-    assert np.array_equal(Wc.bitmask.cpu().numpy().view(np.uint32), ref.bitmask)
+    if Wc.layout == "rows":
+        assert np.array_equal(Wc.row_offsets.cpu().numpy(), ref.row_offsets)
+    else:
+        assert np.array_equal(Wc.tile_offsets.cpu().numpy(), ref.tile_offsets)
+    assert np.array_equal(Wc.bitmask.cpu().numpy().view(np.uint32).reshape(-1), ref.bitmask.reshape(-1))
     vals = Wc.values[: Wc.nnz].cpu()
     if ref.dtype == "i8":
         got = vals.numpy()

@@ -51,7 +51,8 @@ def test_status_strings(L):
 def _mat(**kw):
     from paper_2405_03594_amd import _Matrix
 
-    d = dict(rows=4, cols=64, dtype=2, reserved=0, nnz=10, bitmask=0x10000, values=0x20000, row_offsets=0x30000)
+    d = dict(rows=4, cols=64, dtype=2, layout=0, nnz=10, bitmask=0x10000, values=0x20000, row_offsets=0x30000,
+             tile_offsets=0)
     d.update(kw)
     return _Matrix(**d)
 
@@ -61,7 +62,10 @@ def _mat(**kw):
     (dict(rows=0), INVALID),
     (dict(cols=-1), INVALID),
     (dict(dtype=9), INVALID),
-    (dict(reserved=1), INVALID),
+    (dict(layout=2), INVALID),
+    (dict(layout=1), INVALID),                          # tile layout needs tile_offsets
+    (dict(layout=1, tile_offsets=0x40000, row_offsets=0), OK),
+    (dict(layout=1, tile_offsets=0x40002), INVALID),
     (dict(nnz=-1), INVALID),
     (dict(nnz=257), INVALID),
     (dict(rows=1 << 20, cols=1 << 20, nnz=1 << 31), OVERFLOW),
@@ -83,7 +87,7 @@ def test_null_view(L):
 
 
 def test_sparse_linear_argument_checks(L):
-    m = _mat()
+    m = _mat(layout=1, tile_offsets=0x40000)
     X, Y = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000)
     f = L.spl_sparse_linear_ex
     assert f(None, 2, ctypes.byref(m), Y, 0, None) == INVALID
@@ -93,23 +97,25 @@ def test_sparse_linear_argument_checks(L):
     assert f(ctypes.c_void_p(0x40002), 2, ctypes.byref(m), Y, 0, None) == INVALID
     assert f(X, 2, ctypes.byref(m), Y, 7, None) == INVALID            # unknown algorithm
     assert f(X, 33, ctypes.byref(m), Y, 1, None) == UNSUPPORTED       # decode family is M <= 32
-    m8 = _mat(dtype=3)
+    m8 = _mat(dtype=3, layout=1, tile_offsets=0x40000)
     assert f(X, 2, ctypes.byref(m8), Y, 0, None) == UNSUPPORTED       # int8 view needs the int8 entry
-    mk = _mat(cols=100)
+    mr = _mat()
+    assert f(X, 2, ctypes.byref(mr), Y, 0, None) == UNSUPPORTED       # row layout: retile first
+    mk = _mat(cols=100, layout=1, tile_offsets=0x40000)
     assert f(X, 2, ctypes.byref(mk), Y, 0, None) == UNSUPPORTED       # K % 8 != 0
     assert f(X, 2, None, Y, 0, None) == INVALID
 
 
 def test_int8_argument_checks(L):
-    m = _mat(dtype=3)
+    m = _mat(dtype=3, layout=1, tile_offsets=0x40000)
     X, Y, s = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x60000)
     f = L.spl_sparse_linear_int8
     assert f(X, None, 2, ctypes.byref(m), s, Y, None, None) == INVALID
     assert f(X, s, 2, ctypes.byref(m), None, Y, None, None) == INVALID
     assert f(X, s, 2, ctypes.byref(m), s, Y, ctypes.c_void_p(0x70004), None) == INVALID
-    mk = _mat(dtype=3, cols=40)
+    mk = _mat(dtype=3, cols=40, layout=1, tile_offsets=0x40000)
     assert f(X, s, 2, ctypes.byref(mk), s, Y, None, None) == UNSUPPORTED
-    mb = _mat(dtype=2)
+    mb = _mat(dtype=2, layout=1, tile_offsets=0x40000)
     assert f(X, s, 2, ctypes.byref(mb), s, Y, None, None) == UNSUPPORTED
     assert f(None, None, 0, ctypes.byref(m), None, None, None, None) == OK
 
@@ -134,3 +140,16 @@ def test_dense_argument_checks(L):
     assert L.spl_dense_linear_ex(X, 40, W, 2, 8, 8, Y, 1, None) == UNSUPPORTED
     assert L.spl_dense_linear_int8(X, None, 2, W, X, 8, 16, Y, None, None) == INVALID
     assert L.spl_dense_linear_int8(X, X, 2, W, X, 8, 24, Y, None, None) == UNSUPPORTED
+
+
+def test_tile_count_and_retile_checks(L):
+    assert L.spl_tile16_count(4096, 4096) == 256 * 128
+    assert L.spl_tile16_count(17, 33) == 2 * 2
+    assert L.spl_tile16_count(0, 4) == 0
+    rows = _mat()
+    tiles = _mat(layout=1, tile_offsets=0x40000)
+    B, V, T = ctypes.c_void_p(0x50000), ctypes.c_void_p(0x60000), ctypes.c_void_p(0x70000)
+    assert L.spl_retile16(ctypes.byref(tiles), B, V, T, None) == INVALID       # input must be the row layout
+    assert L.spl_retile16(ctypes.byref(rows), None, V, T, None) == INVALID
+    assert L.spl_retile16(ctypes.byref(rows), B, V, None, None) == INVALID
+    assert L.spl_retile16(ctypes.byref(rows), B, ctypes.c_void_p(0x20000), T, None) == INVALID  # aliasing

@@ -24,11 +24,14 @@ def spl():
 def test_pack_small(orc, spl, dtype, N, K, s):
     W, mask = synth.weight(100 + N + K, N, K, dtype, s)
     ref = orc.pack(W, dtype, mask)
-    Wc = spl.pack_sparse(to_dev(W, dtype), to_dev(mask, "i8").view(dtype=__import__("torch").uint8))
+    Wc = spl.pack_sparse(to_dev(W, dtype), to_dev(mask, "i8").view(dtype=__import__("torch").uint8), layout="rows")
     assert_pack_equal(Wc, ref)
     dense = spl.unpack(Wc)
     from tests._helpers import from_dev_bits
     assert np.array_equal(from_dev_bits(dense), orc.unpack(ref))
+    Wt = spl.retile16(Wc)                               # tile layout, bit-exact against the oracle's encoder
+    assert_pack_equal(Wt, orc.pack_tiled(W, dtype, mask))
+    assert np.array_equal(from_dev_bits(spl.unpack(Wt)), orc.unpack(ref))
 
 
 @pytest.mark.parametrize("name,N,K,dtype,s", [
@@ -43,9 +46,10 @@ def test_pack_llama_shapes(orc, spl, name, N, K, dtype, s):
 
     W, mask = synth.weight(7, N, K, dtype, s)
     ref = orc.pack(W, dtype, mask)
-    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda(), layout="rows")
     assert Wc.nnz == N * K - int(s * N * K)
     assert_pack_equal(Wc, ref)
+    assert_pack_equal(spl.retile16(Wc), orc.pack_tiled(W, dtype, mask))
 
 
 def test_pack_without_mask_keeps_nonzero_payloads(orc, spl):
@@ -55,8 +59,9 @@ def test_pack_without_mask_keeps_nonzero_payloads(orc, spl):
     W[:, 1::7] = 0x8000                 # -0.0: not kept without a mask
     W[:, 2::11] = 0x7FC1                # NaN payloads are kept and copied bit for bit
     ref = orc.pack(W, "bf16", None)
-    Wc = spl.pack_sparse(to_dev(W, "bf16"), None)
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), None, layout="rows")
     assert_pack_equal(Wc, ref)
+    assert_pack_equal(spl.pack_sparse(to_dev(W, "bf16"), None), orc.pack_tiled(W, "bf16", None))
 
 
 def test_pack_keeps_masked_zero_payloads(orc, spl):
@@ -67,7 +72,7 @@ def test_pack_keeps_masked_zero_payloads(orc, spl):
     mask = np.ones((8, 64), dtype=np.uint8)
     mask[:, 5::9] = 0
     ref = orc.pack(W, "f16", mask)
-    Wc = spl.pack_sparse(to_dev(W, "f16"), torch.from_numpy(mask).cuda())
+    Wc = spl.pack_sparse(to_dev(W, "f16"), torch.from_numpy(mask).cuda(), layout="rows")
     assert_pack_equal(Wc, ref)
 
 
@@ -77,7 +82,10 @@ def test_pack_int8(orc, spl, N, K):
 
     Wq, mask, _ = synth.int8_weight(9, N, K, 0.7)
     ref = orc.pack(Wq, "i8", mask)
-    Wc = spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda())
+    Wc = spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda(), layout="rows")
     assert_pack_equal(Wc, ref)
     dense = spl.unpack(Wc).cpu().numpy()
     assert np.array_equal(dense, orc.unpack(ref))
+    Wt = spl.retile16(Wc)
+    assert_pack_equal(Wt, orc.pack_tiled(Wq, "i8", mask))
+    assert np.array_equal(spl.unpack(Wt).cpu().numpy(), orc.unpack(ref))

@@ -370,3 +370,44 @@ def test_activation_rows_are_prefixes():
     a = synth.activations(5, 16, 64, "bf16")
     b = synth.activations(5, 4, 64, "bf16")
     assert np.array_equal(a[:4], b)
+
+
+# ------------------------------------------------------------ tiled (GPU submatrix) layout
+
+@pytest.mark.parametrize("N,K,s", [(16, 32, 0.5), (33, 70, 0.6), (5, 300, 0.3), (48, 96, 0.0), (17, 40, 1.0)])
+def test_tiled_round_trip_and_invariants(orc, N, K, s):
+    W, mask = synth.weight(71 + N + K, N, K, "bf16", s)
+    t = orc.pack_tiled(W, "bf16", mask)
+    m = mask.astype(bool)
+    B, S = -(-N // 16), -(-K // 32)
+    assert t.bitmask.shape == (B * S * 16,) and t.tile_offsets.shape == (B * S + 1,)
+    assert t.nnz == int(m.sum())
+    # round trip: decode gives W where kept, +0 elsewhere, bit for bit
+    assert np.array_equal(orc.unpack_tiled(t), np.where(m, W, np.uint16(0)))
+    # every tile's word is the mask block read LSB-first; tile offsets step by the tile popcounts
+    padded = np.zeros((B * 16, S * 32), dtype=bool)
+    padded[:N, :K] = m
+    blocks = padded.reshape(B, 16, S, 32).transpose(0, 2, 1, 3)        # [B][S][16][32]
+    words = (blocks.astype(np.uint64) << np.arange(32, dtype=np.uint64)).sum(axis=-1)
+    assert np.array_equal(t.bitmask.astype(np.uint64), words.reshape(-1))
+    counts = blocks.reshape(B * S, -1).sum(axis=1)
+    assert np.array_equal(np.diff(t.tile_offsets.astype(np.int64)), counts)
+    # values: tile by tile, each tile row-major (NumPy boolean indexing of the tile block)
+    Wp = np.zeros((B * 16, S * 32), dtype=np.uint16)
+    Wp[:N, :K] = W
+    wb = Wp.reshape(B, 16, S, 32).transpose(0, 2, 1, 3)
+    expect = np.concatenate([wb[b, s_][blocks[b, s_]] for b in range(B) for s_ in range(S)] + [np.zeros(0, np.uint16)])
+    assert np.array_equal(t.values, expect)
+
+
+def test_tiled_and_row_layouts_hold_the_same_entries(orc):
+    W, mask = synth.weight(5, 50, 200, "f16", 0.7)
+    a = orc.unpack(orc.pack(W, "f16", mask))
+    b = orc.unpack_tiled(orc.pack_tiled(W, "f16", mask))
+    assert np.array_equal(a, b)
+
+
+def test_tiled_int8(orc):
+    Wq, mask, _ = synth.int8_weight(6, 40, 96, 0.7)
+    t = orc.pack_tiled(Wq, "i8", mask)
+    assert np.array_equal(orc.unpack_tiled(t), np.where(mask.astype(bool), Wq, np.int8(0)))
