@@ -36,8 +36,12 @@ struct F16 {
   static __device__ __forceinline__ float to_f32(uint32_t bits16) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
   }
+  // binary32 -> binary16, round to nearest even.  The empty asm keeps the
+  // compiler from folding a preceding multiply or add into the conversion
+  // (v_fma_mixlo_f16 rounds the exact result once, straight to binary16).
   static __device__ __forceinline__ uint16_t from_f32(float f) {
-    return __builtin_bit_cast(uint16_t, (_Float16)f);   // v_cvt_f16_f32: round to nearest even
+    asm("" : "+v"(f));
+    return __builtin_bit_cast(uint16_t, (_Float16)f);   // v_cvt_f16_f32
   }
 };
 

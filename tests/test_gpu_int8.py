@@ -1,0 +1,153 @@
+"""Sparse-quantized (int8 weights, int8 activations) linear layers on the GPU
+vs the oracle: int32 accumulators and fp16 outputs are compared bit for bit."""
+import numpy as np
+import pytest
+
+import synth
+from tests._helpers import to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def spl():
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    return spl
+
+
+def _run_sparse(spl, Xq, sx, Wq, mask, sw):
+    import torch
+
+    Wqc = spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda())
+    M, N = Xq.shape[0], Wq.shape[0]
+    acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    Y = spl.sparse_linear_int8(to_dev(Xq, "i8"), torch.from_numpy(sx).cuda(), Wqc, torch.from_numpy(sw).cuda(),
+                               acc_out=acc)
+    return acc.cpu().numpy(), Y.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def _assert_equal(got, ref, what):
+    if not np.array_equal(got, ref):
+        bad = np.argwhere(got != ref)
+        i = tuple(bad[0])
+        raise AssertionError(f"{what}: {len(bad)} of {ref.size} differ; first at {i}: got {got[i]!r}, "
+                             f"oracle {ref[i]!r}")
+
+
+INT8_M = [1, 5, 16, 17, 32, 33, 64, 65, 100]
+
+
+@pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (16, 48, 0.5), (33, 64, 0.7), (100, 1008, 0.7), (64, 4096, 0.5),
+                                   (200, 336, 0.0), (17, 512, 1.0), (48, 2064, 0.9)])
+def test_int8_small(orc, spl, N, K, s):
+    Wq, mask, sw = synth.int8_weight(600 + N, N, K, s)
+    Xq, sx = synth.int8_activations(700 + K, max(INT8_M), K)
+    p = orc.pack(Wq, "i8", mask)
+    for M in INT8_M:
+        acc_ref, y_ref = orc.linear_i8(Xq[:M], sx[:M], p, sw)
+        acc, y = _run_sparse(spl, Xq[:M], sx[:M], Wq, mask, sw)
+        _assert_equal(acc, acc_ref, f"acc N={N} K={K} s={s} M={M}")
+        _assert_equal(y, y_ref, f"Y N={N} K={K} s={s} M={M}")
+
+
+def test_int8_full_code_range(orc, spl):
+    """Codes over the whole int8 range, -128 included, and accumulators near the
+    largest magnitude a 4096-column row can reach."""
+    rng = np.random.default_rng(41)
+    N, K, M = 64, 4096, 20
+    Wq = rng.integers(-128, 128, size=(N, K)).astype(np.int8)
+    Xq = rng.integers(-128, 128, size=(M, K)).astype(np.int8)
+    Wq[0, :] = -128
+    Xq[0, :] = -128                                   # acc[0][0] = 4096 * 2^14 = 2^26
+    mask = (rng.random((N, K)) < 0.4).astype(np.uint8)
+    mask[0, :] = 1
+    sx = rng.uniform(1e-4, 1e-2, size=M).astype(np.float32)
+    sw = rng.uniform(1e-4, 1e-2, size=N).astype(np.float32)
+    acc_ref, y_ref = orc.linear_i8(Xq, sx, orc.pack(Wq, "i8", mask), sw)
+    assert acc_ref[0, 0] == 4096 * 128 * 128
+    acc, y = _run_sparse(spl, Xq, sx, Wq, mask, sw)
+    _assert_equal(acc, acc_ref, "acc")
+    _assert_equal(y, y_ref, "Y")
+
+
+def test_int8_without_acc_out(orc, spl):
+    import torch
+
+    Wq, mask, sw = synth.int8_weight(31, 50, 320, 0.7)
+    Xq, sx = synth.int8_activations(32, 3, 320)
+    _, y_ref = orc.linear_i8(Xq, sx, orc.pack(Wq, "i8", mask), sw)
+    Wqc = spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda())
+    Y = spl.sparse_linear_int8(to_dev(Xq, "i8"), torch.from_numpy(sx).cuda(), Wqc, torch.from_numpy(sw).cuda())
+    _assert_equal(Y.cpu().view(torch.int16).numpy().view(np.uint16), y_ref, "Y")
+
+
+@pytest.mark.parametrize("name,N,K", synth.LLAMA2_7B_LINEARS[3:])   # o, gate, up, down
+def test_int8_llama_shapes_70(orc, spl, name, N, K):
+    j = [n for n, _, _ in synth.LLAMA2_7B_LINEARS].index(name)
+    Wq, mask, sw = synth.int8_weight(synth.weight_seed(0, j), N, K, 0.7)
+    Xq, sx = synth.int8_activations(synth.activation_seed(j), 64, K)
+    p = orc.pack(Wq, "i8", mask)
+    for M in (1, 16, 64):
+        acc_ref, y_ref = orc.linear_i8(Xq[:M], sx[:M], p, sw)
+        acc, y = _run_sparse(spl, Xq[:M], sx[:M], Wq, mask, sw)
+        _assert_equal(acc, acc_ref, f"{name} acc M={M}")
+        _assert_equal(y, y_ref, f"{name} Y M={M}")
+
+
+@pytest.mark.parametrize("N,K", [(16, 64), (100, 1008), (130, 272), (4096, 4096)])
+def test_dense_int8(orc, spl, N, K):
+    import torch
+
+    rng = np.random.default_rng(N + K)
+    Wq = rng.integers(-128, 128, size=(N, K)).astype(np.int8)
+    Xq, sx = synth.int8_activations(55, 65, K)
+    sw = rng.uniform(1e-4, 1e-2, size=N).astype(np.float32)
+    Wd = to_dev(Wq, "i8")
+    for M in (1, 16, 17, 64, 65):
+        acc_ref, y_ref = orc.dense_i8(Xq[:M], sx[:M], Wq, sw)
+        acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+        Y = spl.dense_linear_int8(to_dev(Xq[:M], "i8"), torch.from_numpy(sx[:M]).cuda(), Wd,
+                                  torch.from_numpy(sw).cuda(), acc_out=acc)
+        _assert_equal(acc.cpu().numpy(), acc_ref, f"dense acc M={M}")
+        _assert_equal(Y.cpu().view(torch.int16).numpy().view(np.uint16), y_ref, f"dense Y M={M}")
+
+
+def _tie_cases(count, seed=0):
+    """(acc, sx, sw) whose binary32 result (float(acc) * sx) * sw lies exactly
+    halfway between two binary16 values while the exact product does not: a
+    single-rounding multiply-and-convert would round these differently."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        acc = rng.integers(1, 128, size=200000)
+        sx = rng.uniform(0.5, 1.0, size=acc.size).astype(np.float32)
+        sw = rng.uniform(2.0 ** -6, 2.0 ** -5, size=acc.size).astype(np.float32)
+        t = (acc * sx.astype(np.float64)).astype(np.float32)
+        y64 = t.astype(np.float64) * sw.astype(np.float64)           # exact: 24 + 24 bits
+        y = y64.astype(np.float32)
+        bits = y.view(np.uint32)
+        tie = ((bits & 0x1FFF) == 0x1000) & (y64 != y.astype(np.float64))
+        for i in np.flatnonzero(tie):
+            out.append((int(acc[i]), sx[i], sw[i]))
+    return out[:count]
+
+
+def test_int8_epilogue_rounds_each_product(orc, spl):
+    cases = _tie_cases(48)
+    M = N = len(cases)
+    K = 32
+    Xq = np.zeros((M, K), dtype=np.int8)
+    Wq = np.zeros((N, K), dtype=np.int8)
+    mask = np.zeros((N, K), dtype=np.uint8)
+    Xq[:, 3] = [c[0] for c in cases]
+    Wq[:, 3] = 1
+    mask[:, 3] = 1
+    sx = np.array([c[1] for c in cases], dtype=np.float32)
+    sw = np.array([c[2] for c in cases], dtype=np.float32)
+    acc_ref, y_ref = orc.linear_i8(Xq, sx, orc.pack(Wq, "i8", mask), sw)
+    acc, y = _run_sparse(spl, Xq, sx, Wq, mask, sw)
+    _assert_equal(acc, acc_ref, "acc")
+    _assert_equal(np.diag(y), np.diag(y_ref), "Y at the ties")
+    _assert_equal(y, y_ref, "Y")

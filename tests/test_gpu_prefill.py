@@ -1,0 +1,151 @@
+"""Prefill-shaped (large batch) sparse and dense fp16/bf16 linear layers on the
+GPU vs the oracle.
+
+Tolerance (fp16/bf16 outputs): |y - y64| <= max(2e-2, 1e-2 |y64|) per element.
+Small shapes span several 64 x 128 output blocks with ragged edges in N, M
+and K and are compared in full; the full Llama-2-7B shapes at the batch sizes
+of the prefill workloads (M = 512, 2048) are compared on sampled outputs that
+the oracle computes one by one."""
+import numpy as np
+import pytest
+
+import synth
+from tests._helpers import assert_close, from_dev_bits, from_dev_f64, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def spl():
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    return spl
+
+
+def _pack(spl, W, mask, dtype):
+    import torch
+
+    return spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+
+
+PREFILL_M = [1, 16, 33, 64, 127, 128, 129, 300]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (16, 32, 0.5), (65, 72, 0.7), (130, 1000, 0.7), (64, 4096, 0.5),
+                                   (200, 328, 0.0), (33, 512, 1.0), (17, 264, 0.9)])
+def test_prefill_small(orc, spl, dtype, N, K, s):
+    W, mask = synth.weight(400 + N, N, K, dtype, s)
+    X = synth.activations(500 + K, max(PREFILL_M), K, dtype)
+    ref_p = orc.pack(W, dtype, mask)
+    Wc = _pack(spl, W, mask, dtype)
+    Xd = to_dev(X, dtype)
+    ref = orc.linear_f64(X, ref_p)
+    for M in PREFILL_M:
+        Y = spl.sparse_linear(Xd[:M].contiguous(), Wc, algo="prefill")
+        assert_close(from_dev_f64(Y), ref[:M], f"prefill {dtype} N={N} K={K} s={s} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_prefill_exact_arithmetic(orc, spl, dtype):
+    rng = np.random.default_rng(23)
+    N, K, M = 150, 1064, 200
+    wi = rng.integers(-15, 16, size=(N, K))
+    xi = rng.integers(-3, 4, size=(M, K))
+    W = synth.round_to((wi / 64.0).astype(np.float32), dtype)
+    X = synth.round_to(xi.astype(np.float32), dtype)
+    mask = (rng.random((N, K)) < 0.35).astype(np.uint8)
+    ref = orc.linear_f64(X, orc.pack(W, dtype, mask))      # exact: all partial sums are multiples of 2^-6
+    expect = synth.round_to(ref.astype(np.float32), dtype)
+    Y = spl.sparse_linear(to_dev(X, dtype), _pack(spl, W, mask, dtype), algo="prefill")
+    norm = lambda a: np.where(a == 0x8000, np.uint16(0), a)   # +0 == -0
+    assert np.array_equal(norm(from_dev_bits(Y)), norm(expect))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_prefill_identity_activations(spl, dtype):
+    N, K = 70, 96                                      # X = I_K -> Y = (W . Mask)^T, bit for bit
+    W, mask = synth.weight(78, N, K, dtype, 0.6)
+    X = synth.round_to(np.eye(K, dtype=np.float32), dtype)
+    Y = spl.sparse_linear(to_dev(X, dtype), _pack(spl, W, mask, dtype), algo="prefill")
+    norm = lambda a: np.where(a == 0x8000, 0, a)
+    assert np.array_equal(norm(from_dev_bits(Y)), norm(np.where(mask.astype(bool), W, np.uint16(0)).T))
+
+
+def _sample(rng, M, N, count):
+    """Sampled output positions: the four corners, the block edges, random interior points."""
+    ms = [0, 0, M - 1, M - 1, 127, 128, M // 2]
+    ns = [0, N - 1, 0, N - 1, 63, 64, N // 2]
+    ms += list(rng.integers(0, M, size=count))
+    ns += list(rng.integers(0, N, size=count))
+    return np.array(ms, dtype=np.int64), np.array(ns, dtype=np.int64)
+
+
+@pytest.mark.parametrize("name,N,K,M,s", [
+    ("q 4096x4096", 4096, 4096, 512, 0.7),
+    ("gate 11008x4096", 11008, 4096, 512, 0.7),
+    ("down 4096x11008", 4096, 11008, 512, 0.7),
+    ("up 11008x4096", 11008, 4096, 2048, 0.5),
+    ("o 4096x4096", 4096, 4096, 2048, 0.5),
+])
+def test_prefill_llama_shapes_sampled(orc, spl, name, N, K, M, s):
+    j = [n for n, _, _ in synth.LLAMA2_7B_LINEARS].index(name.split()[0])
+    W, mask = synth.weight(synth.weight_seed(0, j), N, K, "bf16", s)
+    X = synth.activations(synth.activation_seed(j), M, K, "bf16")
+    ref_p = orc.pack(W, "bf16", mask)
+    Y = spl.sparse_linear(to_dev(X, "bf16"), _pack(spl, W, mask, "bf16"))        # auto -> prefill at these M
+    ms, ns = _sample(np.random.default_rng(N + K + M), M, N, 3000)
+    ref = orc.linear_f64_pairs(X, ref_p, ms, ns)
+    got = from_dev_f64(Y)[ms, ns]
+    assert_close(got, ref, f"{name} M={M} s={s}")
+    assert np.isfinite(from_dev_f64(Y)).all()
+
+
+def test_prefill_matches_decode_where_both_apply(orc, spl):
+    W, mask = synth.weight(61, 300, 1024, "bf16", 0.7)
+    X = synth.activations(62, 32, 1024, "bf16")
+    Wc = _pack(spl, W, mask, "bf16")
+    Xd = to_dev(X, "bf16")
+    ref = orc.linear_f64(X, orc.pack(W, "bf16", mask))
+    for algo in ("decode", "prefill"):
+        assert_close(from_dev_f64(spl.sparse_linear(Xd, Wc, algo=algo)), ref, algo)
+
+
+def test_prefill_deterministic_and_overwrites(spl):
+    import torch
+
+    W, mask = synth.weight(9, 300, 2048, "bf16", 0.7)
+    X = synth.activations(10, 130, 2048, "bf16")
+    Wc = _pack(spl, W, mask, "bf16")
+    Xd = to_dev(X, "bf16")
+    buf = torch.full((130 * 300 + 64,), float("nan"), dtype=torch.bfloat16, device="cuda")
+    Y1 = buf[: 130 * 300].view(130, 300)
+    spl.sparse_linear(Xd, Wc, out=Y1, algo="prefill")
+    assert not torch.isnan(Y1).any()
+    assert torch.isnan(buf[130 * 300:]).all()
+    Y2 = spl.sparse_linear(Xd, Wc, algo="prefill")
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K", [(16, 64), (100, 1000), (130, 264)])
+def test_dense_prefill_small(orc, spl, dtype, N, K):
+    W, _ = synth.weight(910 + N, N, K, dtype, 0.0)
+    X = synth.activations(911, 300, K, dtype)
+    ref = orc.dense_f64(X, W, dtype)
+    Wd = to_dev(W, dtype)
+    Xd = to_dev(X, dtype)
+    for M in (1, 64, 129, 300):
+        Y = spl.dense_linear(Xd[:M].contiguous(), Wd, algo="prefill")
+        assert_close(from_dev_f64(Y), ref[:M], f"dense prefill {dtype} M={M}")
+
+
+def test_dense_prefill_llama_sampled(orc, spl):
+    N, K, M = 11008, 4096, 512
+    W, mask = synth.weight(912, N, K, "bf16", 0.0)
+    X = synth.activations(913, M, K, "bf16")
+    Y = spl.dense_linear(to_dev(X, "bf16"), to_dev(W, "bf16"))
+    ms, ns = _sample(np.random.default_rng(5), M, N, 3000)
+    ref = orc.linear_f64_pairs(X, orc.pack(W, "bf16", mask), ms, ns)   # all-ones mask: the dense product
+    assert_close(from_dev_f64(Y)[ms, ns], ref, "dense prefill gate M=512")
