@@ -1,14 +1,29 @@
-"""Host-side replay of the decode kernel's wave-local LDS slot indexing.
+"""Host-side replay of the decode kernels' indexing (no GPU).
 
-The sparse decode kernel stages each wave's tiles in a zero-padded LDS region
-and prefetches one group of k-steps ahead; this test replays the kernel's
-loop (with the constants read from its source) for many shapes and checks
-that every slot it reads lies inside the region.  Regression test for a
-fault where the prefetch ran past a region padded by one group only."""
+The decode kernels split a 16-row block's k-steps (32-column tiles) into one
+contiguous range per wave and walk each range in chunks: as many tiles as
+fit a staging buffer (at most C), whose values are fetched with aligned
+16-byte loads into LDS.  This test replays that schedule, with the constants
+read from the kernel source and the tile offsets of real encodings from the
+oracle, and checks that
+
+  * the wave ranges partition [0, S) and the chunks partition each range;
+  * every tile offset, bitmask word, 16-byte value piece, LDS window and
+    activation element the schedule touches lies inside its buffer
+    (values: the encoding rounded up to 16 bytes plus a 16-byte tail);
+  * a lane's 8-byte window read from the staging buffer, realigned with
+    v_alignbyte_b32 and expanded with the selector table, equals the dense
+    masked tile row.
+
+It guards against an earlier fault in which a prefetch ran past a wave's
+staging region."""
 import os
 import re
 
+import numpy as np
 import pytest
+
+import synth
 
 SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                    "paper_2405_03594_amd", "csrc", "k_decode.hip")
@@ -17,35 +32,140 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
 def _constants():
     src = open(SRC).read()
     waves = int(re.search(r"constexpr int kDecWaves = (\d+);", src).group(1))
-    group = int(re.search(r"constexpr int kGroup = (\d+);", src).group(1))
-    pad = re.search(r"const int Lp = \(S \+ kDecWaves - 1\) / kDecWaves \+ (\d+) \* kGroup;", src)
-    assert pad, "padding formula changed: update this replay"
-    return waves, group, int(pad.group(1)) * group
+    m = re.search(r"static constexpr int C = MT == 1 \? (\d+) : (\d+);", src)
+    assert m, "chunk size formula changed: update this replay"
+    vbuf = int(re.search(r"constexpr int kVBuf = (\d+);", src).group(1))
+    alloc = re.search(r"constexpr int kVBufAlloc = kVBuf \+ (\d+);", src)
+    assert alloc, "staging buffer size changed: update this replay"
+    assert "constexpr int kPieceRounds = kVBuf / 16 / kWave;" in src
+    return waves, {1: int(m.group(1)), 2: int(m.group(2))}, vbuf, vbuf + int(alloc.group(1))
 
 
-def _slots_read(L, G):
-    reads = []
-
-    def issue(j0):
-        reads.extend(j0 + i for i in range(G))
-
-    issue(0)
-    j0 = 0
-    while j0 < L:
-        issue(j0 + G)
-        if j0 + G >= L:
-            break
-        issue(j0 + 2 * G)
-        j0 += 2 * G
-    return reads
+def _wave_range(S, waves, w):
+    L = -(-S // waves)
+    b = min(w * L, S)
+    return b, min(b + L, S)
 
 
-@pytest.mark.parametrize("K", [8, 16, 24, 32, 64, 96, 264, 1000, 2056, 4096, 11008, 16384, 49152])
-def test_prefetch_stays_inside_the_wave_region(K):
-    waves, G, pad = _constants()
-    S = -(-K // 32)
-    Lp = -(-S // waves) + pad
-    for w in range(waves):
-        L = S * (w + 1) // waves - S * w // waves
-        if L > 0:
-            assert max(_slots_read(L, G)) <= Lp - 1, (K, w, L, Lp)
+def _chunks(tob, kbeg, kend, C, vbuf):
+    """The kernel's chunk selection: [(c0, cn, a0, np)]."""
+    out = []
+    c0 = kbeg
+    while c0 < kend:
+        to = [int(tob[c0 + j if c0 + j < kend else kend]) for j in range(C + 1)]
+        a0 = (2 * to[0]) & ~15
+        cn = 1
+        for j in range(2, C + 1):
+            if c0 + j <= kend and ((2 * to[j] + 15) & ~15) - a0 <= vbuf:
+                cn = j
+        np_ = (2 * to[cn] - a0 + 15) >> 4
+        out.append((c0, cn, a0, np_, to))
+        c0 += cn
+    return out
+
+
+def _replay(T, N, K, MT):
+    waves, Cs, vbuf, alloc = _constants()
+    C = Cs[MT]
+    S, B = -(-K // 32), -(-N // 16)
+    value_bytes = -(-2 * T.nnz // 16) * 16 + 16           # allocation of the values buffer
+    for b in range(B):
+        tob = T.tile_offsets[b * S:(b + 1) * S + 1]
+        covered = np.zeros(S, dtype=np.int64)
+        for w in range(waves):
+            kbeg, kend = _wave_range(S, waves, w)
+            for c0, cn, a0, np_, to in _chunks(tob, kbeg, kend, C, vbuf):
+                assert 1 <= cn <= C and c0 + cn <= kend
+                covered[c0:c0 + cn] += 1
+                assert np_ <= vbuf // 16, (b, w, c0, np_)       # pieces fit the rounds of loads
+                assert a0 + 16 * np_ <= value_bytes             # global value reads
+                for j in range(cn):
+                    assert 2 * to[j + 1] - a0 + 12 <= alloc     # third dword of any window stays in the buffer
+                    for fg in range(4):
+                        k = 32 * (c0 + j) + 8 * fg
+                        assert k >= K or k + 8 <= K             # activation reads (K % 8 == 0)
+        assert (covered == 1).all(), b
+
+
+@pytest.mark.parametrize("MT", [1, 2])
+@pytest.mark.parametrize("N,K,s", [(16, 8, 0.5), (33, 40, 0.0), (20, 264, 0.7), (17, 520, 1.0), (48, 1064, 0.5),
+                                   (16, 4096, 0.0), (32, 4104, 0.7), (16, 11008, 0.5), (16, 16384, 0.0)])
+def test_schedule_stays_in_bounds(orc, N, K, s, MT):
+    W, mask = synth.weight(11 + N + K, N, K, "bf16", s)
+    _replay(orc.pack_tiled(W, "bf16", mask), N, K, MT)
+
+
+# ---------------------------------------------------------------- expansion
+
+def _popc(x):
+    return bin(int(x) & 0xFFFFFFFF).count("1")
+
+
+def _perm(s0, s1, sel):
+    src = int(s1).to_bytes(4, "little") + int(s0).to_bytes(4, "little")
+    out = 0
+    for j in range(4):
+        b = (sel >> (8 * j)) & 0xFF
+        assert b < 8 or b == 12
+        out |= (src[b] if b < 8 else 0) << (8 * j)
+    return out
+
+
+def _nibble_selector(nib, h):
+    sel = 0
+    for e in range(2):
+        j = 2 * h + e
+        s16 = 0x0C0C
+        if (nib >> j) & 1:
+            r = _popc(nib & ((1 << j) - 1))
+            s16 = (2 * r) | ((2 * r + 1) << 8)
+        sel |= s16 << (16 * e)
+    return sel
+
+
+@pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (17, 264, 0.9), (33, 96, 0.0), (20, 520, 0.7)])
+def test_lane_expansion_matches_dense_rows(orc, N, K, s):
+    waves, Cs, vbuf, alloc = _constants()
+    C = Cs[1]
+    W, mask = synth.weight(31 + N, N, K, "bf16", s)
+    T = orc.pack_tiled(W, "bf16", mask)
+    vals = np.concatenate([T.values.view(np.uint8), np.zeros(16 + 16, np.uint8)])
+    dense = np.where(mask.astype(bool), W, np.uint16(0))
+    S, B = -(-K // 32), -(-N // 16)
+    bm = T.bitmask.reshape(-1)
+
+    def alignbyte(hi, lo, sh):
+        return ((int(hi) << 32 | int(lo)) >> (8 * (sh & 3))) & 0xFFFFFFFF
+
+    for b in range(B):
+        tob = T.tile_offsets[b * S:(b + 1) * S + 1]
+        for w in range(waves):
+            kbeg, kend = _wave_range(S, waves, w)
+            for c0, cn, a0, np_, to in _chunks(tob, kbeg, kend, C, vbuf):
+                stage = np.zeros(alloc, np.uint8)
+                stage[:16 * np_] = vals[a0:a0 + 16 * np_]
+                st32 = stage.view(np.uint32)
+                for j in range(cn):
+                    t = b * S + c0 + j
+                    words = [int(bm[t * 16 + r]) for r in range(16)]
+                    for lane in range(64):
+                        fr, fg = lane & 15, lane >> 4
+                        wd = words[fr]
+                        above = sum(_popc(words[r]) for r in range(fr))
+                        byte = (wd >> (8 * fg)) & 0xFF
+                        oa = to[j] + above + _popc(wd & ((1 << (8 * fg)) - 1))
+                        ob = oa + _popc(byte & 0xF)
+                        pa, pb = 2 * oa - a0, 2 * ob - a0
+                        qa, qb = pa >> 2, pb >> 2
+                        vlo, vhi = alignbyte(st32[qa + 1], st32[qa], pa), alignbyte(st32[qa + 2], st32[qa + 1], pa)
+                        ulo, uhi = alignbyte(st32[qb + 1], st32[qb], pb), alignbyte(st32[qb + 2], st32[qb + 1], pb)
+                        lo, hi = byte & 15, byte >> 4
+                        a = [_perm(vhi, vlo, _nibble_selector(lo, 0)), _perm(vhi, vlo, _nibble_selector(lo, 1)),
+                             _perm(uhi, ulo, _nibble_selector(hi, 0)), _perm(uhi, ulo, _nibble_selector(hi, 1))]
+                        got = np.array(a, dtype=np.uint32).view(np.uint16)
+                        n, k0 = b * 16 + fr, 32 * (c0 + j) + 8 * fg
+                        exp = np.zeros(8, np.uint16)
+                        if n < N:
+                            seg = dense[n, k0:min(k0 + 8, K)]
+                            exp[:seg.size] = seg
+                        assert np.array_equal(got, exp), (b, c0 + j, lane)
