@@ -188,6 +188,36 @@ spl_status spl_dense_linear_int8(const int8_t* Xq, const float* x_scales, int64_
                                  const float* w_scales, int64_t N, int64_t K, void* Y, int32_t* acc_out,
                                  hipStream_t stream);
 
+/* Grouped launches: up to SPL_MAX_GROUP independent linear layers that share
+ * the dtype and the batch size M, computed by one kernel launch (for example
+ * the q, k and v projections of a decoder layer, or gate and up).  Each task
+ * has its own X [M][K], W and Y [M][N] with the shapes, layouts and alignment
+ * that the single-task entry point requires; the outputs are the ones that
+ * entry point gives with the same algo (DECODE: one launch for all tasks;
+ * PREFILL: one launch per task; AUTO picks by M as above).  The task array
+ * is read on the host during the call and need not outlive it.  Tasks must
+ * not write overlapping outputs. */
+#define SPL_MAX_GROUP 16
+
+typedef struct {
+  const void* X;                 /* [M][K] of W->dtype */
+  const spl_matrix* W;           /* tile layout, fp16 or bf16 */
+  void* Y;                       /* out [M][N] of W->dtype */
+} spl_sparse_task;
+
+typedef struct {
+  const void* X;                 /* [M][K] of the group's dtype */
+  const void* W;                 /* dense [N][K] */
+  int64_t N;
+  int64_t K;
+  void* Y;                       /* out [M][N] */
+} spl_dense_task;
+
+spl_status spl_sparse_linear_group(const spl_sparse_task* tasks, int32_t count, int64_t M, int32_t algo,
+                                   hipStream_t stream);
+spl_status spl_dense_linear_group(const spl_dense_task* tasks, int32_t count, int64_t M, int32_t dtype,
+                                  int32_t algo, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,6 +11,8 @@ Names follow the C ABI without its ``spl_`` prefix:
   row offsets; paper section 2.4.1);
 * ``sparse_linear(X, Wc)`` -> ``Y = X (W . Mask)^T`` for fp16/bf16 (section 2.4.2);
 * ``sparse_linear_int8(Xq, x_scales, Wqc, w_scales)`` -> fp16 ``Y`` (section 3.4);
+* ``sparse_linear_group`` / ``dense_linear_group``: several independent
+  linears (e.g. q, k, v) of one batch size in one launch;
 * ``unpack``, ``dense_linear``, ``dense_linear_int8``: decoder and dense comparators.
 """
 from __future__ import annotations
@@ -52,6 +54,16 @@ class _Matrix(ctypes.Structure):
     ]
 
 
+class _SparseTask(ctypes.Structure):
+    _fields_ = [("X", ctypes.c_void_p), ("W", ctypes.POINTER(_Matrix)), ("Y", ctypes.c_void_p)]
+
+
+class _DenseTask(ctypes.Structure):
+    _fields_ = [("X", ctypes.c_void_p), ("W", ctypes.c_void_p), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("Y", ctypes.c_void_p)]
+
+
+MAX_GROUP = 16
 _lib = None
 
 
@@ -80,6 +92,8 @@ def lib() -> ctypes.CDLL:
         "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
         "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
+        "spl_sparse_linear_group": (ctypes.c_int, [ctypes.POINTER(_SparseTask), I32, I64, I32, P]),
+        "spl_dense_linear_group": (ctypes.c_int, [ctypes.POINTER(_DenseTask), I32, I64, I32, I32, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -270,3 +284,50 @@ def dense_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wq: torch.Tensor
                                                             _ptr(w_scales), N, K, _ptr(out), _ptr(acc_out),
                                                             _stream(stream)))
     return out
+
+
+def sparse_linear_group(Xs, Wcs, outs=None, algo: str = "auto", stream=None):
+    """Y_i = X_i (W_i . Mask_i)^T for up to MAX_GROUP independent layers sharing the
+    batch size and dtype, in one launch (decode) or one launch per layer (prefill)."""
+    L = lib()
+    n = len(Xs)
+    if n != len(Wcs) or not 1 <= n <= MAX_GROUP:
+        raise ValueError("need 1..MAX_GROUP (X, W) pairs")
+    M = Xs[0].shape[0]
+    if outs is None:
+        outs = [torch.empty((M, W.rows), dtype=X.dtype, device=X.device) for X, W in zip(Xs, Wcs)]
+    views = [W.view() for W in Wcs]
+    tasks = (_SparseTask * n)()
+    for i, (X, W, Y) in enumerate(zip(Xs, Wcs, outs)):
+        _dev_tensor(X, "X")
+        if X.shape[0] != M or X.dtype != W.dtype or Y.dtype != X.dtype:
+            raise ValueError("every layer of a group shares M and the fp16/bf16 dtype")
+        tasks[i].X = X.data_ptr()
+        tasks[i].W = ctypes.pointer(views[i])
+        tasks[i].Y = Y.data_ptr()
+    _check("spl_sparse_linear_group", L.spl_sparse_linear_group(tasks, n, M, ALGO[algo], _stream(stream)))
+    return outs
+
+
+def dense_linear_group(Xs, Ws, outs=None, algo: str = "auto", stream=None):
+    """Dense comparator of :func:`sparse_linear_group`."""
+    L = lib()
+    n = len(Xs)
+    if n != len(Ws) or not 1 <= n <= MAX_GROUP:
+        raise ValueError("need 1..MAX_GROUP (X, W) pairs")
+    M = Xs[0].shape[0]
+    if outs is None:
+        outs = [torch.empty((M, W.shape[0]), dtype=X.dtype, device=X.device) for X, W in zip(Xs, Ws)]
+    tasks = (_DenseTask * n)()
+    for i, (X, W, Y) in enumerate(zip(Xs, Ws, outs)):
+        _dev_tensor(X, "X")
+        _dev_tensor(W, "W")
+        if X.shape[0] != M or X.dtype != W.dtype or Y.dtype != X.dtype:
+            raise ValueError("every layer of a group shares M and the fp16/bf16 dtype")
+        tasks[i].X = X.data_ptr()
+        tasks[i].W = W.data_ptr()
+        tasks[i].N, tasks[i].K = W.shape
+        tasks[i].Y = Y.data_ptr()
+    _check("spl_dense_linear_group", L.spl_dense_linear_group(tasks, n, M, _TORCH_DTYPE[Xs[0].dtype], ALGO[algo],
+                                                              _stream(stream)))
+    return outs

@@ -6,30 +6,39 @@
 //
 //   * W is stored as 16 x 32 tiles, each with its 16 bitmask words and its
 //     dense values (one tile = one MFMA A operand).  A workgroup owns one
-//     16-row block; its 16 waves split the block's k-steps (tiles) into
-//     contiguous ranges, so a 4096-column matrix gives every wave 8 tiles;
+//     16-row block of one matrix of the group; its 16 waves split the block's
+//     k-steps (tiles) into contiguous ranges;
 //   * the values of consecutive tiles are contiguous, so a wave fetches a
-//     whole chunk of tiles (as many as fit a 4 KB staging buffer, at most 8)
-//     with aligned, coalesced 16-byte loads into its LDS buffer; the chunk's
-//     bitmask words arrive with one coalesced load per 4 tiles and are
-//     regrouped by row in LDS, and tile offsets come through the scalar cache;
+//     chunk of tiles (as many as fit a 3 KB buffer, at most 8) with aligned,
+//     coalesced 16-byte loads and stages them in LDS; the chunk's bitmask
+//     words arrive with one coalesced load per 4 tiles and are regrouped by
+//     row in LDS; the tile offsets of a wave's whole range come with one load
+//     (one lane per tile) and size every chunk with a ballot;
+//   * each wave is software-pipelined: the next chunk's values and words are
+//     in flight while the current chunk is multiplied;
 //   * lane (fr, fg) supplies tile row fr, columns 8fg..8fg+7, exactly its A
 //     operand of v_mfma_f32_16x16x32 (8 bf16/fp16 values).  Their offset in the
 //     stored values is the tile offset + the kept count of the tile rows above
-//     (a 16-lane DPP scan of popcounts, two k-steps per scan in 16-bit halves)
-//     + the popcount of the lower bits of the row's word.  Each 4-column
+//     (a 16-lane DPP scan of popcounts, two tiles per scan in 16-bit halves) +
+//     the popcount of the lower bits of the row's word.  Each 4-column
 //     nibble's values are read from LDS as an 8-byte window (aligned dword
-//     reads + v_alignbyte_b32) and a 256-entry selector table expands them
+//     reads + v_alignbyte_b32) and a 16-entry selector table expands them
 //     with v_perm_b32 into the operand dwords (zero bytes where the bit is
 //     clear);
 //   * activations form the B operand (batch padded to 16 or 32 columns; the
-//     padding lanes hold zeros).  When M x K fits 48 KB the workgroup copies
-//     X into LDS once; otherwise each k-step's operand is loaded directly;
+//     padding lanes hold zeros).  When every M x K of the group fits 22 KB the
+//     workgroup copies its X into LDS once (and the kernel is held to 64
+//     VGPRs so that two workgroups share a CU); otherwise each chunk's
+//     operands are loaded directly;
 //   * the waves' partial 16x16 results are summed in a fixed order
 //     (deterministic) and rounded once to the output type.
 //
-// Dense comparator: the same schedule with the A operand loaded directly from
-// the dense rows of W (aligned 16-byte loads).
+// One launch covers a group of independent matrices (for example q, k and v):
+// the workgroups of all of them form one grid, so the launch and its ramp-up
+// and tail are paid once.
+//
+// Dense comparator: the same decomposition and pipelining with the A operand
+// loaded directly from the dense rows of W (aligned 16-byte loads).
 #include <type_traits>
 
 #include "spl_common.h"
@@ -40,16 +49,18 @@ namespace {
 constexpr int kDecWaves = 16;
 constexpr int kDecThreads = kDecWaves * kWave;
 constexpr int kDecRows = 16;
-constexpr int kVBuf = 4096;                 // staged value bytes per wave and chunk
+constexpr int kChunk = 8;                   // sparse: at most this many tiles per chunk (4 when M > 16)
+constexpr int kDenseChunk = 4;              // dense: tiles per chunk
+constexpr int kVBuf = 3072;                 // staged value bytes per wave and chunk
 constexpr int kVBufAlloc = kVBuf + 16;      // + room for the last 8-byte window's third dword
-constexpr int kXLdsMax = 48 * 1024;         // activations staged in LDS when M*K*2 fits
-
-// k-steps per chunk: every load of a chunk is in flight at once, so the
-// register budget (<= 128 VGPRs for 4 waves per SIMD) sets it.
-template <int MT>
-struct DecChunk {
-  static constexpr int C = MT == 1 ? 8 : 4;
-};
+constexpr int kPieceRounds = kVBuf / 16 / kWave;
+constexpr int kOffsetLanes = kWave - 1;      // tiles whose offsets one load covers (lane i: tile base + i)
+// Activations are staged in LDS when every task's M * 32S * 2 bytes fit this
+// budget: 32 KB for the dense kernel; 22 KB for the sparse kernel, so that two
+// of its workgroups (3 KB value buffer per wave) still share a CU's 160 KB.
+constexpr int kXLdsMax = 32 * 1024;
+constexpr int kXLdsMaxSparse = 22 * 1024;
+constexpr int kXRounds = kXLdsMax / 16 / kDecThreads;   // staged pieces per thread (bounds M * 4S)
 
 template <class T>
 struct Mfma16;
@@ -86,19 +97,10 @@ __device__ __forceinline__ uint32_t nibble_selector(uint32_t nib, int h) {
   return sel;
 }
 
-// Entry b expands bitmask byte b (two nibbles) into four operand dwords.
-__device__ __forceinline__ void build_selector_table(u32x4* lut) {
-  for (int b = threadIdx.x; b < 256; b += blockDim.x) {
-    lut[b] = u32x4{nibble_selector(b & 15u, 0), nibble_selector(b & 15u, 1), nibble_selector(b >> 4, 0),
-                   nibble_selector(b >> 4, 1)};
-  }
-}
-
-// 8 bytes at any 2-byte aligned offset (gfx950 serves unaligned global loads).
-__device__ __forceinline__ u32x2 load8_at(const unsigned char* __restrict__ base, uint32_t byte_off) {
-  u32x2 v;
-  __builtin_memcpy(&v, base + byte_off, 8);
-  return v;
+// Entry n expands a 4-column nibble n into two operand dwords.  16 entries of
+// 8 bytes cover 32 LDS banks once, so lookups never conflict.
+__device__ __forceinline__ void build_nibble_table(u32x2* lut) {
+  if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{nibble_selector(threadIdx.x, 0), nibble_selector(threadIdx.x, 1)};
 }
 
 // Inclusive prefix sum across each group of 16 lanes (DPP row shifts).
@@ -142,31 +144,78 @@ struct XGlobal {
   }
 };
 
-// Activations staged in LDS (MT == 1, M*K*2 <= kXLdsMax): rows of K + 8
-// elements (the 16-byte pad spreads rows over the LDS banks).
+// Activations staged in LDS (MT == 1): rows of xs_stride(K) = 32*S + 8
+// elements, zero past K (so a ragged last tile reads zeros), the 16-byte pad
+// spreading rows over the LDS banks.  Lanes of padding batch rows (m >= M)
+// read a 64-byte zero area and do not advance with k.
+__host__ __device__ __forceinline__ int64_t xs_stride(int64_t K) { return 32 * tile_steps(K) + 8; }
+
+typedef __attribute__((address_space(3))) unsigned char lds_t;
+
+// 32-bit LDS offset of a pointer into shared memory, and 16-/4-byte loads at such offsets.
+__device__ __forceinline__ uint32_t lds_off(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_t*)p;     // address-space cast: generic -> LDS offset
+}
+__device__ __forceinline__ u32x4 lds_load16(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>((uintptr_t)addr);
+}
+__device__ __forceinline__ uint32_t lds_load4(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>((uintptr_t)addr);
+}
+__device__ __forceinline__ u32x2 lds_load8(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x2*>((uintptr_t)addr);
+}
+
 struct XShared {
-  const uint16_t* row;
-  bool live;
-  __device__ __forceinline__ XShared(const uint16_t* xs, int M, int64_t K, int fr, int fg) {
-    live = fr < M;
-    row = xs + (int64_t)(live ? fr : 0) * (K + 8) + 8 * fg;
-  }
-  __device__ __forceinline__ void load(u32x4 (&xb)[1], int s, bool kin) const {
-    xb[0] = u32x4{0u, 0u, 0u, 0u};
-    if (kin && live) xb[0] = *reinterpret_cast<const u32x4*>(row + 32 * s);
+  uint32_t addr;     // LDS byte address of k-step 0 of this lane's operand
+  uint32_t step;     // bytes per k-step: 64, or 0 for padding rows
+  __device__ __forceinline__ XShared(const uint16_t* xs, const u32x4* zero, int M, int64_t K, int fr, int fg) {
+    const bool live = fr < M;
+    const uint16_t* p = xs + (int64_t)fr * xs_stride(K) + 8 * fg;
+    addr = live ? lds_off(p) : lds_off(zero + fg);
+    step = live ? 64u : 0u;
   }
 };
 
-// Cooperative copy of X [M][K] into LDS rows of K + 8 elements.
-__device__ __forceinline__ void stage_x(uint16_t* xs, const uint16_t* __restrict__ X, int M, int64_t K) {
-  const int per_row = (int)(K / 8);
-  const int total = M * per_row;
-  for (int p = threadIdx.x; p < total; p += kDecThreads) {
-    const int m = p / per_row, q = p - m * per_row;
-    *reinterpret_cast<u32x4*>(xs + (int64_t)m * (K + 8) + 8 * q) =
-        *reinterpret_cast<const u32x4*>(X + (int64_t)m * K + 8 * q);
+// Cooperative copy of X [M][K] into LDS rows of xs_stride(K) elements with
+// zeros from K to 32*S, split so that the loads can be issued early.
+struct XStager {
+  u32x4 r[kXRounds];
+  int per_row, total, kp;
+  float inv;
+  // row of piece p (p < 2^12, per_row < 2^12): a float estimate corrected by one step
+  __device__ __forceinline__ int row_of(int p) const {
+    int m = (int)((float)p * inv);
+    if (m * per_row > p) --m;
+    if ((m + 1) * per_row <= p) ++m;
+    return m;
   }
-}
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int M, int64_t K) {
+    per_row = (int)(4 * tile_steps(K));          // 16-byte pieces per staged row (up to 32*S)
+    kp = (int)(K / 8);                           // pieces that hold activations
+    total = M * per_row;
+    inv = 1.0f / (float)per_row;
+#pragma unroll
+    for (int i = 0; i < kXRounds; ++i) {
+      const int p = threadIdx.x + i * kDecThreads;
+      r[i] = u32x4{0u, 0u, 0u, 0u};
+      if (p < total) {
+        const int m = row_of(p), q = p - m * per_row;
+        if (q < kp) r[i] = *reinterpret_cast<const u32x4*>(X + (int64_t)m * K + 8 * q);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(uint16_t* xs, int64_t K) const {
+#pragma unroll
+    for (int i = 0; i < kXRounds; ++i) {
+      const int p = threadIdx.x + i * kDecThreads;
+      if (p < total) {
+        const int m = row_of(p), q = p - m * per_row;
+        *reinterpret_cast<u32x4*>(xs + (int64_t)m * xs_stride(K) + 8 * q) = r[i];
+      }
+    }
+  }
+};
 
 // Sum the waves' partial accumulators (lane layout of the 16x16 MFMA result:
 // lane l, register i holds row 4*(l/16)+i, column l%16) and store Y[m][n].
@@ -194,191 +243,314 @@ __device__ __forceinline__ void reduce_store(float* red, const f32x4 (&acc)[MT],
   }
 }
 
-// Dynamic LDS: per-wave value staging buffers, then (XL) the staged activations.
-__host__ __device__ constexpr size_t dec_vbuf_bytes() { return (size_t)kDecWaves * kVBufAlloc; }
+// ------------------------------------------------------------------ groups
+
+struct SparseTaskArg {
+  const uint16_t* X;
+  uint16_t* Y;
+  const uint32_t* bm;
+  const uint16_t* values;
+  const int32_t* toff;
+  int64_t N, K;
+};
+struct SparseGroupArg {
+  SparseTaskArg t[SPL_MAX_GROUP];
+  int32_t first[SPL_MAX_GROUP + 1];   // first workgroup of each task; first[count] = grid size
+  int32_t count;
+  int32_t M;
+};
+struct DenseTaskArg {
+  const uint16_t* X;
+  uint16_t* Y;
+  const uint16_t* W;
+  int64_t N, K;
+};
+struct DenseGroupArg {
+  DenseTaskArg t[SPL_MAX_GROUP];
+  int32_t first[SPL_MAX_GROUP + 1];
+  int32_t count;
+  int32_t M;
+};
+
+// Task of this workgroup (wave-uniform).
+__device__ __forceinline__ int find_task(const int32_t* first, int count) {
+  int ti = 0;
+  for (int i = 1; i < count; ++i) ti = (int)blockIdx.x >= first[i] ? i : ti;
+  return ti;
+}
+
+// Dynamic LDS of the sparse kernel: per-wave value staging buffers (later the
+// reduction buffer), then (XL) the staged activations.
+constexpr size_t kSparseVBufBytes = (size_t)kDecWaves * kVBufAlloc;
+
+// A chunk: `cn` tiles from c0 whose values occupy the 16-byte pieces
+// [a0, a0 + 16 np) of the value bytes.
+struct Chunk {
+  int cn;
+  uint32_t a0;
+  int np;
+};
 
 template <class T, int MT, bool XL>
-__global__ void __launch_bounds__(kDecThreads) k_sparse_decode(const uint16_t* __restrict__ X, int M, int64_t K,
-                                                               const uint32_t* __restrict__ bm_tiles,
-                                                               const uint16_t* __restrict__ values,
-                                                               const int32_t* __restrict__ tile_offsets, int64_t N,
-                                                               uint16_t* __restrict__ Y) {
-  constexpr int C = DecChunk<MT>::C;
+__global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_sparse_decode(const SparseGroupArg g) {
+  constexpr int C = MT == 1 ? kChunk : kChunk / 2;
   extern __shared__ __align__(16) unsigned char dsm[];
-  __shared__ u32x4 lut[256];
+  __shared__ u32x2 lut[16];
+  __shared__ u32x4 xzero[4];
   __shared__ __align__(16) uint32_t words[kDecWaves][16 * C];   // per wave: [row][tile of the chunk]
+  const int ti = find_task(g.first, g.count);
+  const SparseTaskArg tk = g.t[ti];
+  const int M = g.M;
+  const int64_t K = tk.K;
+  const int64_t blk = (int64_t)blockIdx.x - g.first[ti];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
-  const int64_t blk = blockIdx.x;
   const int S = (int)tile_steps(K);
   int kbeg, kend;
   wave_range(S, wave, &kbeg, &kend);
   unsigned char* vbuf = dsm + wave * kVBufAlloc;
   const uint32_t* vbuf32 = reinterpret_cast<const uint32_t*>(vbuf);
-  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + dec_vbuf_bytes());
-
-  build_selector_table(lut);
-  if constexpr (XL) stage_x(xs, X, M, K);
-  __syncthreads();
-
-  const uint32_t* bmb = bm_tiles + blk * S * 16;      // this row block's tiles, 16 words each
-  const int32_t* tob = tile_offsets + blk * S;        // + S + 1 entries (the next block's first = this end)
-  const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
-  using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
-  const XOp xop = [&]() {
-    if constexpr (XL) return XShared(xs, M, K, fr, fg);
-    else return XGlobal<MT>(X, M, K, fr, fg);
-  }();
+  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + kSparseVBufBytes);
+  const uint32_t* bmb = tk.bm + blk * S * 16;         // this row block's tiles, 16 words each
+  const int32_t* tob = tk.toff + blk * S;             // S + 1 entries (the next block's first = this end)
+  const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(tk.values);
   const uint32_t lowmask = (1u << (8 * fg)) - 1u;      // bits of the word below my byte
   uint32_t* wl = words[wave];
+
+  // Offsets of the wave's tiles: lane i holds the offset of tile ob + i
+  // (clamped to the range end), for tiles ob .. ob + kOffsetLanes; one load
+  // covers every chunk of a range of up to kOffsetLanes tiles.
+  int ob = kbeg;
+  auto load_offsets = [&](int base) {
+    const int t = base + lane < kend ? base + lane : kend;
+    return tob[t];
+  };
+  // The most tiles (<= C, inside the range) from c0 whose values fit the
+  // staging buffer: tile j fits iff its end offset <= (a0 + kVBuf) / 2, and
+  // the offsets do not decrease, so the count of fitting lanes is the length.
+  auto shape = [&](int32_t o, int c0) {
+    Chunk ch;
+    const int r = c0 - ob;                                  // lane of tile c0 (r + C <= kOffsetLanes)
+    ch.a0 = (2u * (uint32_t)__builtin_amdgcn_readlane(o, r)) & ~15u;
+    const uint32_t lim = (ch.a0 + kVBuf) >> 1;
+    const int jmax = kend - c0 < C ? kend - c0 : C;
+    const bool fit = lane >= r + 1 && lane <= r + jmax && (uint32_t)o <= lim;
+    ch.cn = __builtin_popcountll(__ballot(fit));            // >= 1: one tile is at most 1 KB
+    const uint32_t end = (uint32_t)__builtin_amdgcn_readlane(o, r + ch.cn);
+    ch.np = (int)((2u * end - ch.a0 + 15u) >> 4);           // <= kVBuf / 16
+    return ch;
+  };
+  u32x4 vp[kPieceRounds];
+  uint32_t wv[C / 4];
+  auto issue = [&](const Chunk& ch, int c0) {
+    // 32-bit offsets from wave-uniform bases (values < 2^32 bytes: nnz < 2^31 of 2 bytes)
+#pragma unroll
+    for (int r = 0; r < kPieceRounds; ++r) {
+      vp[r] = u32x4{0u, 0u, 0u, 0u};
+      const uint32_t off = ch.a0 + 16u * (uint32_t)(lane + kWave * r);
+      if (lane + kWave * r < ch.np) vp[r] = *reinterpret_cast<const u32x4*>(vbytes + off);
+    }
+#pragma unroll
+    for (int i = 0; i < C / 4; ++i) {
+      wv[i] = 0u;
+      const uint32_t wi = (uint32_t)(c0 + fg + 4 * i) * 16u + (uint32_t)fr;
+      if (fg + 4 * i < ch.cn) wv[i] = bmb[wi];
+    }
+  };
+
+  // prologue: activations, the range's offsets and the first chunk in flight, then the shared tables
+  XStager xst;
+  if constexpr (XL) xst.load(tk.X, M, K);
+  int32_t orng = 0;
+  Chunk ch{0, 0u, 0};
+  if (kbeg < kend) {
+    orng = load_offsets(ob);
+    ch = shape(orng, kbeg);
+    issue(ch, kbeg);
+  }
+  build_nibble_table(lut);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
+  if constexpr (XL) xst.store(xs, K);
+  __syncthreads();
+
+  using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
+  const XOp xop = [&]() {
+    if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
+    else return XGlobal<MT>(tk.X, M, K, fr, fg);
+  }();
+  const uint32_t lut_addr = lds_off(lut);
+  const uint32_t vbuf_addr = lds_off(vbuf);
+  u32x4 xlive = u32x4{0u, 0u, 0u, 0u};
 
   f32x4 acc[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int c0 = kbeg; c0 < kend;) {
-    // tile offsets of the chunk's tiles and of its end (wave-uniform: scalar loads)
-    int32_t to[C + 1];
-#pragma unroll
-    for (int j = 0; j <= C; ++j) to[j] = tob[c0 + j < kend ? c0 + j : kend];
-    // chunk length: the most tiles (<= C, inside the range) whose values fit the staging buffer
-    const uint32_t a0 = (2u * (uint32_t)to[0]) & ~15u;
-    int cn = 1;
-#pragma unroll
-    for (int j = 2; j <= C; ++j)
-      if (c0 + j <= kend && ((2u * (uint32_t)to[j] + 15u) & ~15u) - a0 <= (uint32_t)kVBuf) cn = j;
-    const int np = (int)((2u * (uint32_t)to[cn] - a0 + 15u) >> 4);    // 16-byte pieces, <= kVBuf / 16
-
-    // issue: value pieces, bitmask words, activations
-    constexpr int kPieceRounds = kVBuf / 16 / kWave;
-    u32x4 vp[kPieceRounds];
-#pragma unroll
-    for (int r = 0; r < kPieceRounds; ++r) {
-      vp[r] = u32x4{0u, 0u, 0u, 0u};
-      if (lane + kWave * r < np)
-        vp[r] = *reinterpret_cast<const u32x4*>(vbytes + a0 + 16u * (uint32_t)(lane + kWave * r));
-    }
-    uint32_t wv[C / 4];
-#pragma unroll
-    for (int i = 0; i < C / 4; ++i) {
-      wv[i] = 0u;
-      if (fg + 4 * i < cn) wv[i] = bmb[(int64_t)(c0 + fg + 4 * i) * 16 + fr];
-    }
-    u32x4 xb[C][MT];
-#pragma unroll
-    for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
-
-    // stage values and regroup words by row
+    // 1. stage the current chunk: values into the buffer, words regrouped by row
 #pragma unroll
     for (int r = 0; r < kPieceRounds; ++r)
-      if (lane + kWave * r < np) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
+      if (lane + kWave * r < ch.np) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
 #pragma unroll
     for (int i = 0; i < C / 4; ++i) wl[fr * C + fg + 4 * i] = wv[i];
     wave_lds_sync();
-    uint32_t w[C];
+    const Chunk cur = ch;
+    int32_t tc[C];                                     // the chunk's tile offsets (wave-uniform)
 #pragma unroll
-    for (int q = 0; q < C / 4; ++q) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(wl + fr * C + 4 * q);
-      w[4 * q] = v.x;
-      w[4 * q + 1] = v.y;
-      w[4 * q + 2] = v.z;
-      w[4 * q + 3] = v.w;
+    for (int j = 0; j < C; ++j) tc[j] = __builtin_amdgcn_readlane(orng, c0 - ob + j);
+
+    // 2. the current chunk's activations (direct path), then the next chunk's loads
+    u32x4 xb[XL ? 1 : C][MT];
+    if constexpr (!XL) {
+#pragma unroll
+      for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cur.cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
     }
-    // kept count of the rows above mine, two tiles per scan (16-bit halves, sums <= 512)
-    uint32_t above[C];
-#pragma unroll
-    for (int j = 0; j < C; j += 2) {
-      const uint32_t pc = __popc(w[j]) | (__popc(w[j + 1]) << 16);
-      const uint32_t ex = row16_inclusive_scan(pc) - pc;
-      above[j] = ex & 0xffffu;
-      above[j + 1] = ex >> 16;
+    const int c1 = c0 + cur.cn;
+    if (c1 < kend) {
+      if (c1 - ob + C > kOffsetLanes) {                // past the loaded offsets (ranges over 63 - C tiles)
+        ob = c1;
+        orng = load_offsets(ob);
+      }
+      ch = shape(orng, c1);
+      issue(ch, c1);
     }
+
+    // 3. expand and multiply the current chunk, two tiles at a time
+    const uint32_t vrel = vbuf_addr - cur.a0;          // LDS address of value byte 0 (a multiple of 4 apart)
+    uint32_t xaddr = 0;
+    if constexpr (XL) xaddr = xop.addr + xop.step * (uint32_t)c0;
 #pragma unroll
-    for (int j = 0; j < C; ++j) {
-      if (j < cn) {
-        const uint32_t byte = (w[j] >> (8 * fg)) & 0xffu;
-        const uint32_t oa = (uint32_t)to[j] + above[j] + __popc(w[j] & lowmask);
-        const uint32_t ob = oa + __popc(byte & 0xfu);
-        // 8-byte windows at byte positions pa, pb of the staging buffer
-        const uint32_t pa = 2u * oa - a0, pb = 2u * ob - a0;
-        const uint32_t qa = pa >> 2, qb = pb >> 2, sa = pa & 3u, sb = pb & 3u;
-        const uint32_t a_0 = vbuf32[qa], a_1 = vbuf32[qa + 1], a_2 = vbuf32[qa + 2];
-        const uint32_t b_0 = vbuf32[qb], b_1 = vbuf32[qb + 1], b_2 = vbuf32[qb + 2];
-        const uint32_t vlo = __builtin_amdgcn_alignbyte(a_1, a_0, sa), vhi = __builtin_amdgcn_alignbyte(a_2, a_1, sa);
-        const uint32_t ulo = __builtin_amdgcn_alignbyte(b_1, b_0, sb), uhi = __builtin_amdgcn_alignbyte(b_2, b_1, sb);
-        const u32x4 sel = lut[byte];
-        u32x4 a;
-        a.x = __builtin_amdgcn_perm(vhi, vlo, sel.x);
-        a.y = __builtin_amdgcn_perm(vhi, vlo, sel.y);
-        a.z = __builtin_amdgcn_perm(uhi, ulo, sel.z);
-        a.w = __builtin_amdgcn_perm(uhi, ulo, sel.w);
+    for (int jp = 0; jp < C; jp += 2) {
+      if (jp < cur.cn) {
+        const u32x2 wp = *reinterpret_cast<const u32x2*>(wl + fr * C + jp);
+        // kept count of the rows above mine for both tiles (16-bit halves, sums <= 512)
+        const uint32_t pc = __popc(wp.x) | (__popc(wp.y) << 16);
+        const uint32_t ex = row16_inclusive_scan(pc) - pc;
 #pragma unroll
-        for (int t = 0; t < MT; ++t) acc[t] = Mfma16<T>::run(a, xb[j][t], acc[t]);
+        for (int h = 0; h < 2; ++h) {
+          const int j = jp + h;
+          if (j < cur.cn) {
+            const uint32_t wj = h ? wp.y : wp.x;
+            const uint32_t above = h ? ex >> 16 : ex & 0xffffu;
+            const uint32_t nlo = __builtin_amdgcn_ubfe(wj, 8 * fg, 4);      // my two nibbles
+            const uint32_t nhi = __builtin_amdgcn_ubfe(wj, 8 * fg + 4, 4);
+            const uint32_t tile0 = (uint32_t)tc[j];
+            const uint32_t oa = __popc(wj & lowmask) + above + tile0;       // first value of each nibble
+            const uint32_t ob = oa + __popc(nlo);
+            // LDS byte addresses of the two 8-byte windows; their low 2 bits are the realignment
+            const uint32_t pa = 2u * oa + vrel, pb = 2u * ob + vrel;
+            const uint32_t da = pa & ~3u, db = pb & ~3u;
+            const uint32_t a_0 = lds_load4(da), a_1 = lds_load4(da + 4), a_2 = lds_load4(da + 8);
+            const uint32_t b_0 = lds_load4(db), b_1 = lds_load4(db + 4), b_2 = lds_load4(db + 8);
+            const uint32_t vlo = __builtin_amdgcn_alignbyte(a_1, a_0, pa);
+            const uint32_t vhi = __builtin_amdgcn_alignbyte(a_2, a_1, pa);
+            const uint32_t ulo = __builtin_amdgcn_alignbyte(b_1, b_0, pb);
+            const uint32_t uhi = __builtin_amdgcn_alignbyte(b_2, b_1, pb);
+            const u32x2 slo = lds_load8(lut_addr + 8u * nlo), shi = lds_load8(lut_addr + 8u * nhi);
+            u32x4 a;
+            a.x = __builtin_amdgcn_perm(vhi, vlo, slo.x);
+            a.y = __builtin_amdgcn_perm(vhi, vlo, slo.y);
+            a.z = __builtin_amdgcn_perm(uhi, ulo, shi.x);
+            a.w = __builtin_amdgcn_perm(uhi, ulo, shi.y);
+            if constexpr (XL) {
+              if (xop.step) xlive = lds_load16(xaddr);   // padding rows keep their zero operand
+              acc[0] = Mfma16<T>::run(a, xlive, acc[0]);
+              xaddr += xop.step;
+            } else {
+#pragma unroll
+              for (int t = 0; t < MT; ++t) acc[t] = Mfma16<T>::run(a, xb[j][t], acc[t]);
+            }
+          }
+        }
       }
     }
     wave_lds_sync();                                   // the next chunk overwrites the buffers
-    c0 += cn;
+    c0 = c1;
   }
   __syncthreads();                                     // every wave is done with its staging buffer
-  reduce_store<T, MT>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, N, Y);
+  reduce_store<T, MT>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, tk.N, tk.Y);
 }
 
 template <class T, int MT, bool XL>
-__global__ void __launch_bounds__(kDecThreads) k_dense_decode(const uint16_t* __restrict__ X, int M, int64_t K,
-                                                              const uint16_t* __restrict__ W, int64_t N,
-                                                              uint16_t* __restrict__ Y) {
-  constexpr int C = DecChunk<MT>::C;
+__global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_dense_decode(const DenseGroupArg g) {
+  constexpr int C = kDenseChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
+  const int ti = find_task(g.first, g.count);
+  const DenseTaskArg tk = g.t[ti];
+  const int M = g.M;
+  const int64_t K = tk.K, N = tk.N;
+  const int64_t blk = (int64_t)blockIdx.x - g.first[ti];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
-  const int64_t blk = blockIdx.x;
   const int S = (int)tile_steps(K);
   int kbeg, kend;
   wave_range(S, wave, &kbeg, &kend);
-  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + dec_vbuf_bytes());
-  if constexpr (XL) stage_x(xs, X, M, K);
-  __syncthreads();
+  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm);
+  __shared__ u32x4 xzero[4];
   const int64_t row = blk * kDecRows + fr < N ? blk * kDecRows + fr : N - 1;   // rows past N feed discarded outputs
-  const uint16_t* wrow = W + row * K + 8 * fg;
+  const uint16_t* wrow = tk.W + row * K + 8 * fg;
+  auto load_a = [&](u32x4 (&dst)[C], int c0) {
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+      const int s = c0 + j;
+      dst[j] = u32x4{0u, 0u, 0u, 0u};
+      if (s < kend && 32 * (int64_t)s + 8 * fg < K) dst[j] = *reinterpret_cast<const u32x4*>(wrow + 32 * (int64_t)s);
+    }
+  };
+
+  XStager xst;
+  if constexpr (XL) xst.load(tk.X, M, K);
+  u32x4 a[C], an[C];
+  if (kbeg < kend) load_a(a, kbeg);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
+  if constexpr (XL) xst.store(xs, K);
+  __syncthreads();
   using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
   const XOp xop = [&]() {
-    if constexpr (XL) return XShared(xs, M, K, fr, fg);
-    else return XGlobal<MT>(X, M, K, fr, fg);
+    if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
+    else return XGlobal<MT>(tk.X, M, K, fr, fg);
   }();
 
   f32x4 acc[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int c0 = kbeg; c0 < kend; c0 += C) {
-    u32x4 a[C];
-    u32x4 xb[C][MT];
+    if constexpr (XL) {
+      if (c0 + C < kend) load_a(an, c0 + C);
+      uint32_t xaddr = xop.addr + xop.step * (uint32_t)c0;
 #pragma unroll
-    for (int j = 0; j < C; ++j) {
-      const int s = c0 + j;
-      const bool kin = s < kend && 32 * (int64_t)s + 8 * fg < K;
-      a[j] = u32x4{0u, 0u, 0u, 0u};
-      if (kin) a[j] = *reinterpret_cast<const u32x4*>(wrow + 32 * (int64_t)s);
-      xop.load(xb[j], s, kin);
+      for (int j = 0; j < C; ++j) {
+        if (c0 + j < kend) acc[0] = Mfma16<T>::run(a[j], lds_load16(xaddr), acc[0]);   // staged columns only
+        xaddr += xop.step;
+      }
+    } else {
+      u32x4 xb[C][MT];
+#pragma unroll
+      for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, c0 + j < kend && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+      if (c0 + C < kend) load_a(an, c0 + C);
+#pragma unroll
+      for (int j = 0; j < C; ++j)
+#pragma unroll
+        for (int t = 0; t < MT; ++t) acc[t] = Mfma16<T>::run(a[j], xb[j][t], acc[t]);
     }
 #pragma unroll
-    for (int j = 0; j < C; ++j)
-#pragma unroll
-      for (int t = 0; t < MT; ++t) acc[t] = Mfma16<T>::run(a[j], xb[j][t], acc[t]);
+    for (int j = 0; j < C; ++j) a[j] = an[j];
   }
-  reduce_store<T, MT>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, N, Y);
+  __syncthreads();                                     // every wave is done with the staged activations
+  reduce_store<T, MT>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, N, tk.Y);
 }
 
 __global__ void __launch_bounds__(256) k_zero_out(uint16_t* __restrict__ Y, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) Y[i] = 0;
 }
 
-bool x_in_lds(int64_t M, int64_t K) { return M <= 16 && M * K * 2 <= kXLdsMax; }
+size_t x_lds_bytes(int64_t M, int64_t K) { return (size_t)M * (size_t)xs_stride(K) * 2; }
+constexpr size_t kXLdsAlloc = (size_t)kXLdsMax + 16 * 16;   // the most x_lds_bytes(M, K) can be (see variant)
+constexpr size_t kRedBytes = (size_t)kDecWaves * 2 * 256 * sizeof(float);
 
-size_t x_lds_bytes(int64_t M, int64_t K) { return (size_t)M * (size_t)(K + 8) * 2; }
-
-// Raise the kernel's dynamic LDS limit once (it is above the 64 KB default).
+// Raise a kernel's dynamic LDS limit once (above the 64 KB default).
 template <class F>
 hipError_t allow_lds(F* kernel, size_t bytes) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -386,43 +558,50 @@ hipError_t allow_lds(F* kernel, size_t bytes) {
 }
 
 template <class T, int MT, bool XL>
-hipError_t sparse_decode_launch(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+hipError_t sparse_group_launch(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
   auto* kernel = k_sparse_decode<T, MT, XL>;
-  const size_t lds = dec_vbuf_bytes() + (XL ? x_lds_bytes(M, Wc.cols) : 0);
-  static const hipError_t attr = allow_lds(kernel, dec_vbuf_bytes() + (XL ? x_lds_bytes(16, kXLdsMax / 32) : 0));
+  static const hipError_t attr = allow_lds(kernel, kSparseVBufBytes + (XL ? kXLdsAlloc : 0));   // an upper bound
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(kernel, dim3((unsigned)tile_blocks(Wc.rows)), dim3(kDecThreads), lds, s,
-                     static_cast<const uint16_t*>(X), (int)M, Wc.cols, Wc.bitmask,
-                     static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows, static_cast<uint16_t*>(Y));
+  const size_t lds = kSparseVBufBytes + (XL ? x_lds_bytes(g.M, kmax) : 0);
+  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(kDecThreads), lds, s, g);
   return hipGetLastError();
-}
-
-template <class T>
-hipError_t sparse_decode_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
-  if (x_in_lds(M, Wc.cols)) return sparse_decode_launch<T, 1, true>(X, M, Wc, Y, s);
-  if (M <= 16) return sparse_decode_launch<T, 1, false>(X, M, Wc, Y, s);
-  return sparse_decode_launch<T, 2, false>(X, M, Wc, Y, s);
 }
 
 template <class T, int MT, bool XL>
-hipError_t dense_decode_launch(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y,
-                               hipStream_t s) {
+hipError_t dense_group_launch(const DenseGroupArg& g, int64_t kmax, hipStream_t s) {
   auto* kernel = k_dense_decode<T, MT, XL>;
-  const size_t lds = dec_vbuf_bytes() + (XL ? x_lds_bytes(M, K) : 0);
-  static const hipError_t attr = allow_lds(kernel, dec_vbuf_bytes() + (XL ? x_lds_bytes(16, kXLdsMax / 32) : 0));
+  static const hipError_t attr = allow_lds(kernel, kRedBytes > kXLdsAlloc ? kRedBytes : kXLdsAlloc);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(kernel, dim3((unsigned)tile_blocks(N)), dim3(kDecThreads), lds, s,
-                     static_cast<const uint16_t*>(X), (int)M, K, static_cast<const uint16_t*>(W), N,
-                     static_cast<uint16_t*>(Y));
+  const size_t xb = XL ? x_lds_bytes(g.M, kmax) : 0;
+  const size_t lds = xb > kRedBytes ? xb : kRedBytes;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(kDecThreads), lds, s, g);
   return hipGetLastError();
 }
 
+// Kernel variant for a group: activations in LDS when every task's staged
+// rows fit (M * 32S * 2 <= kXLdsMax, so x_lds_bytes <= kXLdsAlloc), each
+// piece of them within the kXRounds loads of a thread.
+int variant(int64_t M, int64_t kmax, int64_t budget) {
+  if (M <= 16 && M * 32 * tile_steps(kmax) * 2 <= budget) return 0;
+  return M <= 16 ? 1 : 2;
+}
+
 template <class T>
-hipError_t dense_decode_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  if (x_in_lds(M, K)) return dense_decode_launch<T, 1, true>(X, M, W, N, K, Y, s);
-  if (M <= 16) return dense_decode_launch<T, 1, false>(X, M, W, N, K, Y, s);
-  return dense_decode_launch<T, 2, false>(X, M, W, N, K, Y, s);
+hipError_t sparse_group_t(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
+  switch (variant(g.M, kmax, kXLdsMaxSparse)) {
+    case 0: return sparse_group_launch<T, 1, true>(g, kmax, s);
+    case 1: return sparse_group_launch<T, 1, false>(g, kmax, s);
+    default: return sparse_group_launch<T, 2, false>(g, kmax, s);
+  }
+}
+
+template <class T>
+hipError_t dense_group_t(const DenseGroupArg& g, int64_t kmax, hipStream_t s) {
+  switch (variant(g.M, kmax, kXLdsMax)) {
+    case 0: return dense_group_launch<T, 1, true>(g, kmax, s);
+    case 1: return dense_group_launch<T, 1, false>(g, kmax, s);
+    default: return dense_group_launch<T, 2, false>(g, kmax, s);
+  }
 }
 
 }  // namespace
@@ -438,13 +617,35 @@ hipError_t launch_zero_fill(void* Y, int64_t count16, hipStream_t s) {
 // No per-K limit: a wave walks its k-range in chunks.
 int decode_max_k() { return 1 << 30; }
 
-hipError_t launch_sparse_decode(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  return Wc.dtype == SPL_BF16 ? sparse_decode_t<Bf16>(X, M, Wc, Y, s) : sparse_decode_t<F16>(X, M, Wc, Y, s);
+hipError_t launch_sparse_decode(const spl_sparse_task* tasks, int count, int64_t M, hipStream_t s) {
+  SparseGroupArg g{};
+  int64_t kmax = 0;
+  g.first[0] = 0;
+  for (int i = 0; i < count; ++i) {
+    const spl_matrix& W = *tasks[i].W;
+    g.t[i] = SparseTaskArg{static_cast<const uint16_t*>(tasks[i].X), static_cast<uint16_t*>(tasks[i].Y), W.bitmask,
+                           static_cast<const uint16_t*>(W.values), W.tile_offsets, W.rows, W.cols};
+    g.first[i + 1] = g.first[i] + (int32_t)tile_blocks(W.rows);
+    if (W.cols > kmax) kmax = W.cols;
+  }
+  g.count = count;
+  g.M = (int32_t)M;
+  return tasks[0].W->dtype == SPL_BF16 ? sparse_group_t<Bf16>(g, kmax, s) : sparse_group_t<F16>(g, kmax, s);
 }
 
-hipError_t launch_dense_decode(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
-                               void* Y, hipStream_t s) {
-  return dtype == SPL_BF16 ? dense_decode_t<Bf16>(X, M, W, N, K, Y, s) : dense_decode_t<F16>(X, M, W, N, K, Y, s);
+hipError_t launch_dense_decode(const spl_dense_task* tasks, int count, int64_t M, int32_t dtype, hipStream_t s) {
+  DenseGroupArg g{};
+  int64_t kmax = 0;
+  g.first[0] = 0;
+  for (int i = 0; i < count; ++i) {
+    g.t[i] = DenseTaskArg{static_cast<const uint16_t*>(tasks[i].X), static_cast<uint16_t*>(tasks[i].Y),
+                          static_cast<const uint16_t*>(tasks[i].W), tasks[i].N, tasks[i].K};
+    g.first[i + 1] = g.first[i] + (int32_t)tile_blocks(tasks[i].N);
+    if (tasks[i].K > kmax) kmax = tasks[i].K;
+  }
+  g.count = count;
+  g.M = (int32_t)M;
+  return dtype == SPL_BF16 ? dense_group_t<Bf16>(g, kmax, s) : dense_group_t<F16>(g, kmax, s);
 }
 
 }  // namespace spl

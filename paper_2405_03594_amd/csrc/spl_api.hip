@@ -127,21 +127,61 @@ spl_status spl_unpack(const spl_matrix* Wc, void* W_dense, hipStream_t stream) {
   return launched(spl::launch_unpack(*Wc, W_dense, stream));
 }
 
-spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
-                                hipStream_t stream) {
+// Checks of one fp16/bf16 sparse task; *algo is resolved from AUTO.
+static spl_status check_sparse_task(const void* X, int64_t M, const spl_matrix* Wc, const void* Y, int32_t* algo) {
   const spl_status st = spl_check_matrix(Wc);
   if (st != SPL_OK) return st;
   if (!fp_dtype(Wc->dtype) || Wc->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
-  if (algo < SPL_ALGO_AUTO || algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
+  if (*algo < SPL_ALGO_AUTO || *algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
   const spl_status xy = check_xy(X, M, Wc->cols, Wc->rows, Y);
-  if (xy != SPL_OK || M == 0) return xy;
+  if (xy != SPL_OK) return xy;
   if (Wc->cols % 8 != 0) return SPL_ERR_UNSUPPORTED;
-  if (algo == SPL_ALGO_AUTO)
-    algo = (M <= kDecodeMaxM && Wc->cols <= spl::decode_max_k()) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
-  if (algo == SPL_ALGO_DECODE && (M > kDecodeMaxM || Wc->cols > spl::decode_max_k())) return SPL_ERR_UNSUPPORTED;
+  if (*algo == SPL_ALGO_AUTO)
+    *algo = (M <= kDecodeMaxM && Wc->cols <= spl::decode_max_k()) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (*algo == SPL_ALGO_DECODE && (M > kDecodeMaxM || Wc->cols > spl::decode_max_k())) return SPL_ERR_UNSUPPORTED;
+  return SPL_OK;
+}
+
+static spl_status check_dense_task(const spl_dense_task* t, int64_t M, int32_t dtype, int32_t* algo) {
+  if (!t->W || !fp_dtype(dtype) || !dims_ok(t->N, t->K) || !aligned(t->W, 16)) return SPL_ERR_INVALID_ARG;
+  if (*algo < SPL_ALGO_AUTO || *algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
+  const spl_status xy = check_xy(t->X, M, t->K, t->N, t->Y);
+  if (xy != SPL_OK) return xy;
+  if (t->K % 8 != 0) return SPL_ERR_UNSUPPORTED;
+  if (*algo == SPL_ALGO_AUTO) *algo = M <= kDecodeMaxM ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (*algo == SPL_ALGO_DECODE && M > kDecodeMaxM) return SPL_ERR_UNSUPPORTED;
+  return SPL_OK;
+}
+
+spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
+                                hipStream_t stream) {
+  const spl_sparse_task t{X, Wc, Y};
+  return spl_sparse_linear_group(&t, 1, M, algo, stream);
+}
+
+spl_status spl_sparse_linear_group(const spl_sparse_task* tasks, int32_t count, int64_t M, int32_t algo,
+                                   hipStream_t stream) {
+  if (!tasks || count < 1 || count > SPL_MAX_GROUP || M < 0) return SPL_ERR_INVALID_ARG;
+  int64_t blocks = 0;
+  int32_t resolved = algo;
+  for (int32_t i = 0; i < count; ++i) {
+    if (!tasks[i].W) return SPL_ERR_INVALID_ARG;
+    int32_t a = algo;
+    const spl_status st = check_sparse_task(tasks[i].X, M, tasks[i].W, tasks[i].Y, &a);
+    if (st != SPL_OK) return st;
+    if (tasks[i].W->dtype != tasks[0].W->dtype) return SPL_ERR_INVALID_ARG;
+    resolved = a;                                      // AUTO depends on M only: the same for every task
+    blocks += spl::tile_blocks(tasks[i].W->rows);
+  }
+  if (blocks >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
   (void)hipGetLastError();
-  if (algo == SPL_ALGO_DECODE) return launched(spl::launch_sparse_decode(X, M, *Wc, Y, stream));
-  return launched(spl::launch_sparse_prefill(X, M, *Wc, Y, stream));
+  if (resolved == SPL_ALGO_DECODE) return launched(spl::launch_sparse_decode(tasks, count, M, stream));
+  for (int32_t i = 0; i < count; ++i) {
+    const spl_status st = launched(spl::launch_sparse_prefill(tasks[i].X, M, *tasks[i].W, tasks[i].Y, stream));
+    if (st != SPL_OK) return st;
+  }
+  return SPL_OK;
 }
 
 spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, void* Y, hipStream_t stream) {
@@ -164,16 +204,32 @@ spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64
 
 spl_status spl_dense_linear_ex(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
                                void* Y, int32_t algo, hipStream_t stream) {
-  if (!W || !fp_dtype(dtype) || !dims_ok(N, K) || !aligned(W, 16)) return SPL_ERR_INVALID_ARG;
-  if (algo < SPL_ALGO_AUTO || algo > SPL_ALGO_PREFILL) return SPL_ERR_INVALID_ARG;
-  const spl_status xy = check_xy(X, M, K, N, Y);
-  if (xy != SPL_OK || M == 0) return xy;
-  if (K % 8 != 0) return SPL_ERR_UNSUPPORTED;
-  if (algo == SPL_ALGO_AUTO) algo = M <= kDecodeMaxM ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
-  if (algo == SPL_ALGO_DECODE && M > kDecodeMaxM) return SPL_ERR_UNSUPPORTED;
+  const spl_dense_task t{X, W, N, K, Y};
+  return spl_dense_linear_group(&t, 1, M, dtype, algo, stream);
+}
+
+spl_status spl_dense_linear_group(const spl_dense_task* tasks, int32_t count, int64_t M, int32_t dtype,
+                                  int32_t algo, hipStream_t stream) {
+  if (!tasks || count < 1 || count > SPL_MAX_GROUP || M < 0) return SPL_ERR_INVALID_ARG;
+  int64_t blocks = 0;
+  int32_t resolved = algo;
+  for (int32_t i = 0; i < count; ++i) {
+    int32_t a = algo;
+    const spl_status st = check_dense_task(&tasks[i], M, dtype, &a);
+    if (st != SPL_OK) return st;
+    resolved = a;
+    blocks += spl::tile_blocks(tasks[i].N);
+  }
+  if (blocks >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
   (void)hipGetLastError();
-  if (algo == SPL_ALGO_DECODE) return launched(spl::launch_dense_decode(X, M, W, dtype, N, K, Y, stream));
-  return launched(spl::launch_dense_prefill(X, M, W, dtype, N, K, Y, stream));
+  if (resolved == SPL_ALGO_DECODE) return launched(spl::launch_dense_decode(tasks, count, M, dtype, stream));
+  for (int32_t i = 0; i < count; ++i) {
+    const spl_status st = launched(spl::launch_dense_prefill(tasks[i].X, M, tasks[i].W, dtype, tasks[i].N,
+                                                             tasks[i].K, tasks[i].Y, stream));
+    if (st != SPL_OK) return st;
+  }
+  return SPL_OK;
 }
 
 spl_status spl_dense_linear(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,

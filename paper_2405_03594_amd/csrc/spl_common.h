@@ -78,9 +78,9 @@ hipError_t launch_retile16(const spl_matrix& rows_in, uint32_t* bitmask_t, void*
 // Y[0..count16) = +0 (16-bit elements).
 hipError_t launch_zero_fill(void* Y, int64_t count16, hipStream_t s);
 
-hipError_t launch_sparse_decode(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
-hipError_t launch_dense_decode(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
-                               void* Y, hipStream_t s);
+// Decode kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
+hipError_t launch_sparse_decode(const spl_sparse_task* tasks, int count, int64_t M, hipStream_t s);
+hipError_t launch_dense_decode(const spl_dense_task* tasks, int count, int64_t M, int32_t dtype, hipStream_t s);
 hipError_t launch_sparse_prefill(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
 hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
                                 void* Y, hipStream_t s);

@@ -153,3 +153,41 @@ def test_tile_count_and_retile_checks(L):
     assert L.spl_retile16(ctypes.byref(rows), None, V, T, None) == INVALID
     assert L.spl_retile16(ctypes.byref(rows), B, V, None, None) == INVALID
     assert L.spl_retile16(ctypes.byref(rows), B, ctypes.c_void_p(0x20000), T, None) == INVALID  # aliasing
+
+
+def test_group_argument_checks(L):
+    from paper_2405_03594_amd import MAX_GROUP, _DenseTask, _SparseTask
+
+    m = _mat(layout=1, tile_offsets=0x40000)
+    m16 = _mat(dtype=1, layout=1, tile_offsets=0x40000)
+    X, Y = 0x40000, 0x50000
+
+    def tasks(*mats):
+        arr = (_SparseTask * max(1, len(mats)))()
+        for i, mm in enumerate(mats):
+            arr[i].X, arr[i].Y = X, Y + 0x1000 * i
+            arr[i].W = ctypes.pointer(mm) if mm is not None else None
+        return arr
+
+    f = L.spl_sparse_linear_group
+    assert f(tasks(m, m), 2, 0, 0, None) == OK                    # M = 0: checked, then a no-op
+    assert f(tasks(m), 0, 2, 0, None) == INVALID                  # empty group
+    assert f(None, 1, 2, 0, None) == INVALID
+    assert f(tasks(*([m] * (MAX_GROUP + 1))), MAX_GROUP + 1, 2, 0, None) == INVALID
+    assert f(tasks(m, None), 2, 2, 0, None) == INVALID            # missing matrix
+    assert f(tasks(m, m16), 2, 0, 0, None) == INVALID             # mixed dtypes
+    assert f(tasks(m, _mat(layout=1, tile_offsets=0x40000, rows=0)), 2, 0, 0, None) == INVALID
+    assert f(tasks(m), 1, -1, 0, None) == INVALID
+    assert f(tasks(m), 1, 33, 1, None) == UNSUPPORTED             # decode family is M <= 32
+
+    g = L.spl_dense_linear_group
+    d = (_DenseTask * 2)()
+    for i in range(2):
+        d[i].X, d[i].W, d[i].N, d[i].K, d[i].Y = X, 0x60000, 8, 64, Y
+    assert g(d, 2, 0, 2, 0, None) == OK
+    assert g(d, 2, 2, 3, 0, None) == INVALID                      # int8 has its own entry point
+    assert g(d, 0, 2, 2, 0, None) == INVALID
+    d[1].K = 60
+    assert g(d, 2, 2, 2, 0, None) == UNSUPPORTED                  # K % 8 != 0
+    d[1].K, d[1].W = 64, 0x60008
+    assert g(d, 2, 2, 2, 0, None) == INVALID                      # misaligned W

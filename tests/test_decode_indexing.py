@@ -32,13 +32,19 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
 def _constants():
     src = open(SRC).read()
     waves = int(re.search(r"constexpr int kDecWaves = (\d+);", src).group(1))
-    m = re.search(r"static constexpr int C = MT == 1 \? (\d+) : (\d+);", src)
-    assert m, "chunk size formula changed: update this replay"
+    chunk = int(re.search(r"constexpr int kChunk = (\d+);", src).group(1))
+    assert "constexpr int C = MT == 1 ? kChunk : kChunk / 2;" in src, "chunk size formula changed: update this replay"
     vbuf = int(re.search(r"constexpr int kVBuf = (\d+);", src).group(1))
     alloc = re.search(r"constexpr int kVBufAlloc = kVBuf \+ (\d+);", src)
     assert alloc, "staging buffer size changed: update this replay"
     assert "constexpr int kPieceRounds = kVBuf / 16 / kWave;" in src
-    return waves, {1: int(m.group(1)), 2: int(m.group(2))}, vbuf, vbuf + int(alloc.group(1))
+    assert "const int t = base + lane < kend ? base + lane : kend;" in src, "offset clamp changed: update this replay"
+    assert "const uint32_t lim = (ch.a0 + kVBuf) >> 1;" in src and \
+        "const bool fit = lane >= r + 1 && lane <= r + jmax && (uint32_t)o <= lim;" in src, \
+        "chunk rule changed: update this replay"
+    assert "if (c1 - ob + C > kOffsetLanes) {" in src and "constexpr int kOffsetLanes = kWave - 1;" in src, \
+        "offset window changed: update this replay"
+    return waves, {1: chunk, 2: chunk // 2}, vbuf, vbuf + int(alloc.group(1))
 
 
 def _wave_range(S, waves, w):
@@ -48,16 +54,24 @@ def _wave_range(S, waves, w):
 
 
 def _chunks(tob, kbeg, kend, C, vbuf):
-    """The kernel's chunk selection: [(c0, cn, a0, np)]."""
+    """The kernel's chunk selection: [(c0, cn, a0, np, offsets)].  Offsets come
+    from a window of 64 lanes (lane i: tile ob + i, clamped to the range end)
+    that is reloaded at a chunk that would reach past lane 63."""
     out = []
     c0 = kbeg
+    ob = kbeg
     while c0 < kend:
-        to = [int(tob[c0 + j if c0 + j < kend else kend]) for j in range(C + 1)]
+        if c0 - ob + C > 63:
+            ob = c0
+        window = [int(tob[min(ob + i, kend)]) for i in range(64)]
+        r = c0 - ob
+        assert 0 <= r and r + C <= 63                  # every readlane index of the chunk is a lane
+        to = [window[r + j] for j in range(C + 1)]
         a0 = (2 * to[0]) & ~15
-        cn = 1
-        for j in range(2, C + 1):
-            if c0 + j <= kend and ((2 * to[j] + 15) & ~15) - a0 <= vbuf:
-                cn = j
+        lim = (a0 + vbuf) >> 1                          # a tile fits iff its end offset <= lim
+        jmax = min(kend - c0, C)
+        cn = sum(1 for j in range(1, C + 1) if j <= jmax and to[j] <= lim)
+        assert cn >= 1 and all(to[j] <= lim for j in range(1, cn + 1))   # the fitting lanes form a prefix
         np_ = (2 * to[cn] - a0 + 15) >> 4
         out.append((c0, cn, a0, np_, to))
         c0 += cn
@@ -89,7 +103,8 @@ def _replay(T, N, K, MT):
 
 @pytest.mark.parametrize("MT", [1, 2])
 @pytest.mark.parametrize("N,K,s", [(16, 8, 0.5), (33, 40, 0.0), (20, 264, 0.7), (17, 520, 1.0), (48, 1064, 0.5),
-                                   (16, 4096, 0.0), (32, 4104, 0.7), (16, 11008, 0.5), (16, 16384, 0.0)])
+                                   (16, 4096, 0.0), (32, 4104, 0.7), (16, 11008, 0.5), (16, 16384, 0.0),
+                                   (16, 65536, 0.7), (16, 65544, 0.0)])   # ranges longer than the offset window
 def test_schedule_stays_in_bounds(orc, N, K, s, MT):
     W, mask = synth.weight(11 + N + K, N, K, "bf16", s)
     _replay(orc.pack_tiled(W, "bf16", mask), N, K, MT)

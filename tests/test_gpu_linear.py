@@ -146,3 +146,65 @@ def test_zero_batch_is_noop(spl):
     Wc = _pack(spl, W, mask, "bf16")
     Y = spl.sparse_linear(torch.empty((0, 64), dtype=torch.bfloat16, device="cuda"), Wc)
     assert Y.shape == (0, 8)
+
+
+@pytest.mark.parametrize("M", [1, 4, 16, 17, 32])
+def test_decode_group_matches_single_calls(orc, spl, M):
+    """One launch over several matrices of different shapes (ragged N and K,
+    an all-pruned matrix) gives each matrix the oracle's result, bit for bit
+    the same as one call per matrix."""
+    import torch
+
+    shapes = [(100, 1000, 0.7), (48, 2056, 0.5), (17, 264, 0.9), (64, 4096, 0.7), (33, 512, 1.0), (16, 11008, 0.7)]
+    Ws, refs, Xs = [], [], []
+    for i, (N, K, s) in enumerate(shapes):
+        W, mask = synth.weight(700 + i, N, K, "bf16", s)
+        X = synth.activations(800 + i, M, K, "bf16")
+        Ws.append(_pack(spl, W, mask, "bf16"))
+        Xs.append(to_dev(X, "bf16"))
+        refs.append(orc.linear_f64(X, orc.pack(W, "bf16", mask)))
+    Ys = spl.sparse_linear_group(Xs, Ws, algo="decode")
+    for i, (Y, ref) in enumerate(zip(Ys, refs)):
+        assert_close(from_dev_f64(Y), ref, f"group task {i} M={M}")
+        single = spl.sparse_linear(Xs[i], Ws[i], algo="decode")
+        assert torch.equal(Y.view(torch.int16), single.view(torch.int16)), f"task {i}"
+
+
+@pytest.mark.parametrize("M", [1, 4, 17])
+def test_dense_decode_group(orc, spl, M):
+    shapes = [(100, 1000), (48, 2056), (64, 4096), (16, 11008)]
+    Ws, Xs, refs = [], [], []
+    for i, (N, K) in enumerate(shapes):
+        W, _ = synth.weight(720 + i, N, K, "f16", 0.0)
+        X = synth.activations(820 + i, M, K, "f16")
+        Ws.append(to_dev(W, "f16"))
+        Xs.append(to_dev(X, "f16"))
+        refs.append(orc.dense_f64(X, W, "f16"))
+    for i, (Y, ref) in enumerate(zip(spl.dense_linear_group(Xs, Ws, algo="decode"), refs)):
+        assert_close(from_dev_f64(Y), ref, f"dense group task {i} M={M}")
+
+
+def test_prefill_group(orc, spl):
+    Ws, Xs, refs = [], [], []
+    for i, (N, K) in enumerate([(100, 1000), (130, 264)]):
+        W, mask = synth.weight(740 + i, N, K, "bf16", 0.7)
+        X = synth.activations(840 + i, 70, K, "bf16")
+        Ws.append(_pack(spl, W, mask, "bf16"))
+        Xs.append(to_dev(X, "bf16"))
+        refs.append(orc.linear_f64(X, orc.pack(W, "bf16", mask)))
+    for i, (Y, ref) in enumerate(zip(spl.sparse_linear_group(Xs, Ws), refs)):   # auto -> prefill at M = 70
+        assert_close(from_dev_f64(Y), ref, f"prefill group task {i}")
+
+
+@pytest.mark.parametrize("s", [0.7, 0.0])
+def test_decode_long_rows(orc, spl, s):
+    """K = 40960: each wave's range (80 tiles) outgrows one load of tile offsets."""
+    N, K = 40, 40960
+    W, mask = synth.weight(950, N, K, "bf16", s)
+    X = synth.activations(951, 17, K, "bf16")
+    ref = orc.linear_f64(X, orc.pack(W, "bf16", mask))
+    Wc = _pack(spl, W, mask, "bf16")
+    Xd = to_dev(X, "bf16")
+    for M in (1, 5, 17):
+        Y = spl.sparse_linear(Xd[:M].contiguous(), Wc, algo="decode")
+        assert_close(from_dev_f64(Y), ref[:M], f"long rows s={s} M={M}")
