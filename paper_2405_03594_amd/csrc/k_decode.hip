@@ -26,7 +26,7 @@
 //     with v_perm_b32 into the operand dwords (zero bytes where the bit is
 //     clear);
 //   * activations form the B operand (batch padded to 16 or 32 columns; the
-//     padding lanes hold zeros).  When every M x K of the group fits 22 KB the
+//     padding lanes hold zeros).  When every M x K of the group fits 32 KB the
 //     workgroup copies its X into LDS once (and the kernel is held to 64
 //     VGPRs so that two workgroups share a CU); otherwise each chunk's
 //     operands are loaded directly;
@@ -46,7 +46,7 @@
 namespace spl {
 namespace {
 
-constexpr int kDecWaves = 16;
+constexpr int kDecWaves = 8;
 constexpr int kDecThreads = kDecWaves * kWave;
 constexpr int kDecRows = 16;
 constexpr int kChunk = 8;                   // sparse: at most this many tiles per chunk (4 when M > 16)
@@ -56,10 +56,10 @@ constexpr int kVBufAlloc = kVBuf + 16;      // + room for the last 8-byte window
 constexpr int kPieceRounds = kVBuf / 16 / kWave;
 constexpr int kOffsetLanes = kWave - 1;      // tiles whose offsets one load covers (lane i: tile base + i)
 // Activations are staged in LDS when every task's M * 32S * 2 bytes fit this
-// budget: 32 KB for the dense kernel; 22 KB for the sparse kernel, so that two
-// of its workgroups (3 KB value buffer per wave) still share a CU's 160 KB.
+// budget (32 KB): a sparse workgroup then needs at most ~61 KB of LDS (3 KB
+// value buffer per wave), so at least two share a CU's 160 KB.
 constexpr int kXLdsMax = 32 * 1024;
-constexpr int kXLdsMaxSparse = 22 * 1024;
+constexpr int kXLdsMaxSparse = 32 * 1024;
 constexpr int kXRounds = kXLdsMax / 16 / kDecThreads;   // staged pieces per thread (bounds M * 4S)
 
 template <class T>
