@@ -46,8 +46,9 @@
 namespace spl {
 namespace {
 
-constexpr int kDecWaves = 8;
-constexpr int kDecThreads = kDecWaves * kWave;
+// Waves per workgroup (W) is a template parameter: 8 for large grids, 16
+// (a finer split of each row block's k-steps) when a launch has fewer than
+// two row blocks per CU.
 constexpr int kDecRows = 16;
 constexpr int kChunk = 8;                   // sparse: at most this many tiles per chunk (4 when M > 16)
 constexpr int kDenseChunk = 4;              // dense: tiles per chunk
@@ -60,7 +61,6 @@ constexpr int kOffsetLanes = kWave - 1;      // tiles whose offsets one load cov
 // value buffer per wave), so at least two share a CU's 160 KB.
 constexpr int kXLdsMax = 32 * 1024;
 constexpr int kXLdsMaxSparse = 32 * 1024;
-constexpr int kXRounds = kXLdsMax / 16 / kDecThreads;   // staged pieces per thread (bounds M * 4S)
 
 template <class T>
 struct Mfma16;
@@ -112,9 +112,10 @@ __device__ __forceinline__ uint32_t row16_inclusive_scan(uint32_t x) {
   return x;
 }
 
-// This wave's contiguous range of k-steps [*beg, *end) of S.
+// This wave's contiguous range of k-steps [*beg, *end) of S (W waves).
+template <int W>
 __device__ __forceinline__ void wave_range(int S, int wave, int* beg, int* end) {
-  const int L = (S + kDecWaves - 1) / kDecWaves;
+  const int L = (S + W - 1) / W;
   const int b = wave * L < S ? wave * L : S;
   *beg = b;
   *end = b + L < S ? b + L : S;
@@ -179,7 +180,10 @@ struct XShared {
 
 // Cooperative copy of X [M][K] into LDS rows of xs_stride(K) elements with
 // zeros from K to 32*S, split so that the loads can be issued early.
+template <int W>
 struct XStager {
+  static constexpr int kThreads = W * kWave;
+  static constexpr int kXRounds = kXLdsMax / 16 / kThreads;   // staged pieces per thread (bounds M * 4S)
   u32x4 r[kXRounds];
   int per_row, total, kp;
   float inv;
@@ -197,7 +201,7 @@ struct XStager {
     inv = 1.0f / (float)per_row;
 #pragma unroll
     for (int i = 0; i < kXRounds; ++i) {
-      const int p = threadIdx.x + i * kDecThreads;
+      const int p = threadIdx.x + i * kThreads;
       r[i] = u32x4{0u, 0u, 0u, 0u};
       if (p < total) {
         const int m = row_of(p), q = p - m * per_row;
@@ -208,7 +212,7 @@ struct XStager {
   __device__ __forceinline__ void store(uint16_t* xs, int64_t K) const {
 #pragma unroll
     for (int i = 0; i < kXRounds; ++i) {
-      const int p = threadIdx.x + i * kDecThreads;
+      const int p = threadIdx.x + i * kThreads;
       if (p < total) {
         const int m = row_of(p), q = p - m * per_row;
         *reinterpret_cast<u32x4*>(xs + (int64_t)m * xs_stride(K) + 8 * q) = r[i];
@@ -220,7 +224,7 @@ struct XStager {
 // Sum the waves' partial accumulators (lane layout of the 16x16 MFMA result:
 // lane l, register i holds row 4*(l/16)+i, column l%16) and store Y[m][n].
 // Called by every thread after all waves have finished with `red`'s memory.
-template <class T, int MT>
+template <class T, int MT, int W>
 __device__ __forceinline__ void reduce_store(float* red, const f32x4 (&acc)[MT], int M, int64_t n0, int64_t N,
                                              uint16_t* __restrict__ Y) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -228,7 +232,7 @@ __device__ __forceinline__ void reduce_store(float* red, const f32x4 (&acc)[MT],
 #pragma unroll
   for (int t = 0; t < MT; ++t) *reinterpret_cast<f32x4*>(red + ((wave * MT + t) * 64 + lane) * 4) = acc[t];
   __syncthreads();
-  for (int e = threadIdx.x; e < 256 * MT; e += kDecThreads) {
+  for (int e = threadIdx.x; e < 256 * MT; e += W * kWave) {
     const int t = e >> 8;
     const int li = (e >> 2) & 63;
     const int ri = e & 3;
@@ -237,7 +241,7 @@ __device__ __forceinline__ void reduce_store(float* red, const f32x4 (&acc)[MT],
     if (m < M && n < N) {
       float s = 0.f;
 #pragma unroll
-      for (int w = 0; w < kDecWaves; ++w) s += red[((w * MT + t) * 64 + li) * 4 + ri];
+      for (int w = 0; w < W; ++w) s += red[((w * MT + t) * 64 + li) * 4 + ri];
       Y[(int64_t)m * N + n] = T::from_f32(s);
     }
   }
@@ -281,7 +285,8 @@ __device__ __forceinline__ int find_task(const int32_t* first, int count) {
 
 // Dynamic LDS of the sparse kernel: per-wave value staging buffers (later the
 // reduction buffer), then (XL) the staged activations.
-constexpr size_t kSparseVBufBytes = (size_t)kDecWaves * kVBufAlloc;
+template <int W>
+constexpr size_t sparse_vbuf_bytes() { return (size_t)W * kVBufAlloc; }
 
 // A chunk: `cn` tiles from c0 whose values occupy the 16-byte pieces
 // [a0, a0 + 16 np) of the value bytes.
@@ -291,13 +296,13 @@ struct Chunk {
   int np;
 };
 
-template <class T, int MT, bool XL>
-__global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_sparse_decode(const SparseGroupArg g) {
+template <class T, int MT, bool XL, int W>
+__global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const SparseGroupArg g) {
   constexpr int C = MT == 1 ? kChunk : kChunk / 2;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
   __shared__ u32x4 xzero[4];
-  __shared__ __align__(16) uint32_t words[kDecWaves][16 * C];   // per wave: [row][tile of the chunk]
+  __shared__ __align__(16) uint32_t words[W][16 * C];   // per wave: [row][tile of the chunk]
   const int ti = find_task(g.first, g.count);
   const SparseTaskArg tk = g.t[ti];
   const int M = g.M;
@@ -308,10 +313,10 @@ __global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_sparse_decode(const
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
   int kbeg, kend;
-  wave_range(S, wave, &kbeg, &kend);
+  wave_range<W>(S, wave, &kbeg, &kend);
   unsigned char* vbuf = dsm + wave * kVBufAlloc;
   const uint32_t* vbuf32 = reinterpret_cast<const uint32_t*>(vbuf);
-  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + kSparseVBufBytes);
+  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + sparse_vbuf_bytes<W>());
   const uint32_t* bmb = tk.bm + blk * S * 16;         // this row block's tiles, 16 words each
   const int32_t* tob = tk.toff + blk * S;             // S + 1 entries (the next block's first = this end)
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(tk.values);
@@ -360,7 +365,7 @@ __global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_sparse_decode(const
   };
 
   // prologue: activations, the range's offsets and the first chunk in flight, then the shared tables
-  XStager xst;
+  XStager<W> xst;
   if constexpr (XL) xst.load(tk.X, M, K);
   int32_t orng = 0;
   Chunk ch{0, 0u, 0};
@@ -469,11 +474,11 @@ __global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_sparse_decode(const
     c0 = c1;
   }
   __syncthreads();                                     // every wave is done with its staging buffer
-  reduce_store<T, MT>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, tk.N, tk.Y);
+  reduce_store<T, MT, W>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, tk.N, tk.Y);
 }
 
-template <class T, int MT, bool XL>
-__global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_dense_decode(const DenseGroupArg g) {
+template <class T, int MT, bool XL, int W>
+__global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const DenseGroupArg g) {
   constexpr int C = kDenseChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
   const int ti = find_task(g.first, g.count);
@@ -486,7 +491,7 @@ __global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_dense_decode(const 
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
   int kbeg, kend;
-  wave_range(S, wave, &kbeg, &kend);
+  wave_range<W>(S, wave, &kbeg, &kend);
   uint16_t* xs = reinterpret_cast<uint16_t*>(dsm);
   __shared__ u32x4 xzero[4];
   const int64_t row = blk * kDecRows + fr < N ? blk * kDecRows + fr : N - 1;   // rows past N feed discarded outputs
@@ -500,7 +505,7 @@ __global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_dense_decode(const 
     }
   };
 
-  XStager xst;
+  XStager<W> xst;
   if constexpr (XL) xst.load(tk.X, M, K);
   u32x4 a[C], an[C];
   if (kbeg < kend) load_a(a, kbeg);
@@ -539,7 +544,7 @@ __global__ void __launch_bounds__(kDecThreads, XL ? 8 : 4) k_dense_decode(const 
     for (int j = 0; j < C; ++j) a[j] = an[j];
   }
   __syncthreads();                                     // every wave is done with the staged activations
-  reduce_store<T, MT>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, N, tk.Y);
+  reduce_store<T, MT, W>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, N, tk.Y);
 }
 
 __global__ void __launch_bounds__(256) k_zero_out(uint16_t* __restrict__ Y, int64_t count) {
@@ -548,7 +553,8 @@ __global__ void __launch_bounds__(256) k_zero_out(uint16_t* __restrict__ Y, int6
 
 size_t x_lds_bytes(int64_t M, int64_t K) { return (size_t)M * (size_t)xs_stride(K) * 2; }
 constexpr size_t kXLdsAlloc = (size_t)kXLdsMax + 16 * 16;   // the most x_lds_bytes(M, K) can be (see variant)
-constexpr size_t kRedBytes = (size_t)kDecWaves * 2 * 256 * sizeof(float);
+template <int W>
+constexpr size_t red_bytes() { return (size_t)W * 2 * 256 * sizeof(float); }
 
 // Raise a kernel's dynamic LDS limit once (above the 64 KB default).
 template <class F>
@@ -557,51 +563,73 @@ hipError_t allow_lds(F* kernel, size_t bytes) {
                              (int)bytes);
 }
 
-template <class T, int MT, bool XL>
+template <class T, int MT, bool XL, int W>
 hipError_t sparse_group_launch(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
-  auto* kernel = k_sparse_decode<T, MT, XL>;
-  static const hipError_t attr = allow_lds(kernel, kSparseVBufBytes + (XL ? kXLdsAlloc : 0));   // an upper bound
+  auto* kernel = k_sparse_decode<T, MT, XL, W>;
+  static const hipError_t attr = allow_lds(kernel, sparse_vbuf_bytes<W>() + (XL ? kXLdsAlloc : 0));   // an upper bound
   if (attr != hipSuccess) return attr;
-  const size_t lds = kSparseVBufBytes + (XL ? x_lds_bytes(g.M, kmax) : 0);
-  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(kDecThreads), lds, s, g);
+  const size_t lds = sparse_vbuf_bytes<W>() + (XL ? x_lds_bytes(g.M, kmax) : 0);
+  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(W * kWave), lds, s, g);
   return hipGetLastError();
 }
 
-template <class T, int MT, bool XL>
+template <class T, int MT, bool XL, int W>
 hipError_t dense_group_launch(const DenseGroupArg& g, int64_t kmax, hipStream_t s) {
-  auto* kernel = k_dense_decode<T, MT, XL>;
-  static const hipError_t attr = allow_lds(kernel, kRedBytes > kXLdsAlloc ? kRedBytes : kXLdsAlloc);
+  auto* kernel = k_dense_decode<T, MT, XL, W>;
+  static const hipError_t attr = allow_lds(kernel, red_bytes<W>() > kXLdsAlloc ? red_bytes<W>() : kXLdsAlloc);
   if (attr != hipSuccess) return attr;
   const size_t xb = XL ? x_lds_bytes(g.M, kmax) : 0;
-  const size_t lds = xb > kRedBytes ? xb : kRedBytes;
-  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(kDecThreads), lds, s, g);
+  const size_t lds = xb > red_bytes<W>() ? xb : red_bytes<W>();
+  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(W * kWave), lds, s, g);
   return hipGetLastError();
 }
 
 // Kernel variant for a group: activations in LDS when every task's staged
-// rows fit (M * 32S * 2 <= kXLdsMax, so x_lds_bytes <= kXLdsAlloc), each
-// piece of them within the kXRounds loads of a thread.
+// rows fit (M * 32S * 2 <= budget, so x_lds_bytes <= kXLdsAlloc), each
+// piece of them within the staging loads of a thread.
 int variant(int64_t M, int64_t kmax, int64_t budget) {
   if (M <= 16 && M * 32 * tile_steps(kmax) * 2 <= budget) return 0;
   return M <= 16 ? 1 : 2;
 }
 
+// 16 waves per workgroup when the launch has fewer than two row blocks per CU.
+bool small_grid(int64_t blocks) {
+  static int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                   hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  return blocks < 2 * (int64_t)cus;
+}
+
+template <class T, int W>
+hipError_t sparse_group_w(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
+  switch (variant(g.M, kmax, kXLdsMaxSparse)) {
+    case 0: return sparse_group_launch<T, 1, true, W>(g, kmax, s);
+    case 1: return sparse_group_launch<T, 1, false, W>(g, kmax, s);
+    default: return sparse_group_launch<T, 2, false, W>(g, kmax, s);
+  }
+}
+
 template <class T>
 hipError_t sparse_group_t(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
-  switch (variant(g.M, kmax, kXLdsMaxSparse)) {
-    case 0: return sparse_group_launch<T, 1, true>(g, kmax, s);
-    case 1: return sparse_group_launch<T, 1, false>(g, kmax, s);
-    default: return sparse_group_launch<T, 2, false>(g, kmax, s);
+  return small_grid(g.first[g.count]) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);
+}
+
+template <class T, int W>
+hipError_t dense_group_w(const DenseGroupArg& g, int64_t kmax, hipStream_t s) {
+  switch (variant(g.M, kmax, kXLdsMax)) {
+    case 0: return dense_group_launch<T, 1, true, W>(g, kmax, s);
+    case 1: return dense_group_launch<T, 1, false, W>(g, kmax, s);
+    default: return dense_group_launch<T, 2, false, W>(g, kmax, s);
   }
 }
 
 template <class T>
 hipError_t dense_group_t(const DenseGroupArg& g, int64_t kmax, hipStream_t s) {
-  switch (variant(g.M, kmax, kXLdsMax)) {
-    case 0: return dense_group_launch<T, 1, true>(g, kmax, s);
-    case 1: return dense_group_launch<T, 1, false>(g, kmax, s);
-    default: return dense_group_launch<T, 2, false>(g, kmax, s);
-  }
+  return small_grid(g.first[g.count]) ? dense_group_w<T, 16>(g, kmax, s) : dense_group_w<T, 8>(g, kmax, s);
 }
 
 }  // namespace

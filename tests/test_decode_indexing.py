@@ -31,7 +31,9 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
 
 def _constants():
     src = open(SRC).read()
-    waves = int(re.search(r"constexpr int kDecWaves = (\d+);", src).group(1))
+    assert "return small_grid(g.first[g.count]) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);" \
+        in src, "waves per workgroup changed: update this replay"
+    waves = (8, 16)
     chunk = int(re.search(r"constexpr int kChunk = (\d+);", src).group(1))
     assert "constexpr int C = MT == 1 ? kChunk : kChunk / 2;" in src, "chunk size formula changed: update this replay"
     vbuf = int(re.search(r"constexpr int kVBuf = (\d+);", src).group(1))
@@ -78,8 +80,9 @@ def _chunks(tob, kbeg, kend, C, vbuf):
     return out
 
 
-def _replay(T, N, K, MT):
-    waves, Cs, vbuf, alloc = _constants()
+def _replay(T, N, K, MT, W):
+    _, Cs, vbuf, alloc = _constants()
+    waves = W
     C = Cs[MT]
     S, B = -(-K // 32), -(-N // 16)
     value_bytes = -(-2 * T.nnz // 16) * 16 + 16           # allocation of the values buffer
@@ -101,13 +104,14 @@ def _replay(T, N, K, MT):
         assert (covered == 1).all(), b
 
 
+@pytest.mark.parametrize("W", [8, 16])
 @pytest.mark.parametrize("MT", [1, 2])
 @pytest.mark.parametrize("N,K,s", [(16, 8, 0.5), (33, 40, 0.0), (20, 264, 0.7), (17, 520, 1.0), (48, 1064, 0.5),
                                    (16, 4096, 0.0), (32, 4104, 0.7), (16, 11008, 0.5), (16, 16384, 0.0),
                                    (16, 65536, 0.7), (16, 65544, 0.0)])   # ranges longer than the offset window
-def test_schedule_stays_in_bounds(orc, N, K, s, MT):
-    W, mask = synth.weight(11 + N + K, N, K, "bf16", s)
-    _replay(orc.pack_tiled(W, "bf16", mask), N, K, MT)
+def test_schedule_stays_in_bounds(orc, N, K, s, MT, W):
+    Wt, mask = synth.weight(11 + N + K, N, K, "bf16", s)
+    _replay(orc.pack_tiled(Wt, "bf16", mask), N, K, MT, W)
 
 
 # ---------------------------------------------------------------- expansion
@@ -140,7 +144,8 @@ def _nibble_selector(nib, h):
 
 @pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (17, 264, 0.9), (33, 96, 0.0), (20, 520, 0.7)])
 def test_lane_expansion_matches_dense_rows(orc, N, K, s):
-    waves, Cs, vbuf, alloc = _constants()
+    _, Cs, vbuf, alloc = _constants()
+    waves = 8
     C = Cs[1]
     W, mask = synth.weight(31 + N, N, K, "bf16", s)
     T = orc.pack_tiled(W, "bf16", mask)
