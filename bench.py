@@ -194,6 +194,305 @@ def cpu_baseline(dtype: str, sparsity: float, batches, min_seconds: float = 10.0
                       f"times: fp64 product on the decoded weights, {dt:.1f} s on {threads} threads"}
 
 
+# ---------------------------------------------------------------- other workloads
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def _need_gpu():
+    import torch
+
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    return torch, spl
+
+
+def _line(args, metric, value, unit, ms, workload, roofline, cpu, extra=None, dtype="bf16", higher=True):
+    out = {"metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": higher, "scaling": "weak",
+           "vs_baseline": None, "dtype": dtype, "data": "synthetic", "config": {"workload": workload}}
+    if extra:
+        out["config"].update(extra)
+    out["roofline"] = roofline
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    return out
+
+
+def _timed(units, fn, steps, warmup, keys):
+    """One graph per key; time `steps` replays rotating over the keys.  Returns
+    (wall ms per step, GPU ms per step)."""
+    graphs = []
+    for k in keys:
+        graphs += capture_graphs([k], units, [None], lambda li, u, M, k=k: fn(k, u))
+    wall, ms = time_graphs(graphs, steps, warmup)
+    return wall * 1e3 / steps, float(np.mean(ms))
+
+
+def _oracle_repeat(fn, min_seconds=10.0, max_reps=5000):
+    reps, t0 = 0, time.perf_counter()
+    while reps < max_reps and (reps == 0 or time.perf_counter() - t0 < min_seconds):
+        fn()
+        reps += 1
+    return reps, time.perf_counter() - t0
+
+
+def run_single(args):
+    """One 4096x4096 fp16 matrix at 50% magnitude sparsity (W seed 0), one
+    activation row (X seed 1); 8 device copies of the packed matrix rotated."""
+    torch, spl = _need_gpu()
+    N = K = 4096
+    W, mask = synth.weight(0, N, K, "f16", 0.5)
+    X = synth.activations(1, 1, K, "f16")
+    Wd = _to_dev(W, "f16", torch)
+    Wc = spl.pack_sparse(Wd, torch.from_numpy(mask).cuda())
+    copies = 8
+    mats = [spl.SparseMatrix(Wc.bitmask.clone(), Wc.values.clone(), None, Wc.tile_offsets.clone(), N, K, Wc.nnz,
+                             "tile16") for _ in range(copies)]
+    dens = [Wd.clone() for _ in range(copies)]
+    Xd = _to_dev(X, "f16", torch)
+    Y = torch.empty((1, N), dtype=torch.float16, device="cuda")
+    sp_wall, sp_gpu = _timed([0], lambda li, u: spl.sparse_linear(Xd, mats[li], out=Y), args.steps, args.warmup,
+                             range(copies))
+    dn_wall, dn_gpu = _timed([0], lambda li, u: spl.dense_linear(Xd, dens[li], out=Y), args.steps, args.warmup,
+                             range(copies))
+    nbytes = Wc.compressed_bytes() + 2 * K + 2 * N
+    achieved = nbytes / (sp_gpu * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        p = oracle.pack(W, "f16", mask)
+        threads = oracle.max_threads()
+        reps, dt = _oracle_repeat(lambda: oracle.linear_f64(X, p, nthreads=threads))
+        cpu = {"value": round(reps / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"the same matrix and activation row, fp64 product on the decoded weights, repeated "
+                         f"{reps} times ({dt:.1f} s on {threads} threads)"}
+    return _line(args, "sparse-linear tokens/s + achieved HBM GB/s, 4096x4096 fp16 at 50% sparsity, batch 1",
+                 round(1.0 / (sp_wall * 1e-3), 1), "tokens/s", sp_wall,
+                 "one 4096x4096 fp16 matrix, 50% unstructured magnitude sparsity (seed 0), batch 1 (seed 1), "
+                 "8 device copies rotated",
+                 {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_decode",
+                  "bytes_per_launch": int(nbytes), "avg_launch_us": round(sp_gpu * 1e3, 3)},
+                 cpu, {"gpu_us": round(sp_gpu * 1e3, 3), "dense_gpu_us": round(dn_gpu * 1e3, 3),
+                       "speedup_vs_dense": round(dn_gpu / sp_gpu, 3)}, dtype="f16")
+
+
+def run_prefill(args):
+    """One layer's seven matrices at M = 512 and 2048 (prefill kernels)."""
+    torch, spl = _need_gpu()
+    host = generate_layers(1, "bf16", args.sparsity, args.workers)
+    layers = upload_layers(host, "bf16", keep_dense=not args.no_dense)
+    del host
+    Ms = [512, 2048]
+    xs = make_activations("bf16", max(Ms))
+    shapes = synth.LLAMA2_7B_LINEARS
+    ys = {(M, j): torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms for j, (_, N, _) in
+          enumerate(shapes)}
+    xsl = {(M, j): xs[j][:M].contiguous() for M in Ms for j in range(len(shapes))}
+    units = [(M, j) for M in Ms for j in range(len(shapes))]
+
+    def sparse_fn(li, u):
+        spl.sparse_linear(xsl[u], layers[0][u[1]][0], out=ys[u], algo="prefill")
+
+    def dense_fn(li, u):
+        spl.dense_linear(xsl[u], layers[0][u[1]][1], out=ys[u], algo="prefill")
+
+    sp_wall, sp_gpu = _timed(units, sparse_fn, args.steps, args.warmup, [0])
+    flops = sum(2.0 * M * N * K for M in Ms for (_, N, K) in shapes)
+    launch_ms = sp_gpu / len(units)
+    achieved = flops / len(units) / (launch_ms * 1e-3) / 1e12
+    per_M = {}
+    for M in Ms:
+        uM = [u for u in units if u[0] == M]
+        _, g = _timed(uM, sparse_fn, max(10, args.steps // 4), 2, [0])
+        f = sum(2.0 * M * N * K for (_, N, K) in shapes)
+        d = {"layer_us": round(g * 1e3, 2), "dense_equiv_tflops": round(f / (g * 1e-3) / 1e12, 1)}
+        if not args.no_dense:
+            _, gd = _timed(uM, dense_fn, max(10, args.steps // 4), 2, [0])
+            d.update({"dense_layer_us": round(gd * 1e3, 2), "dense_tflops": round(f / (gd * 1e-3) / 1e12, 1),
+                      "speedup_vs_dense": round(gd / g, 3)})
+        per_M[str(M)] = d
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        W, mask = synth.weight(synth.weight_seed(0, 0), 4096, 4096, "bf16", args.sparsity)
+        p = oracle.pack(W, "bf16", mask)
+        X = synth.activations(synth.activation_seed(0), 64, 4096, "bf16")
+        threads = oracle.max_threads()
+        reps, dt = _oracle_repeat(lambda: oracle.linear_f64(X, p, nthreads=threads))
+        # tokens/s of the whole layer at this rate: 64 rows of q per repetition, scaled by the layer's work
+        layer_over_q = sum(N * K for (_, N, K) in shapes) / (4096 * 4096)
+        cpu = {"value": round(reps * 64 / dt / layer_over_q, 3), "unit": "tokens/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"64 activation rows through the q matrix (4096x4096), fp64, repeated {reps} times "
+                         f"({dt:.1f} s on {threads} threads), scaled to the layer's seven matrices by their "
+                         f"element count ({layer_over_q:.2f}x q)"}
+    return _line(args, "sparse-linear prefill tokens/s, Llama-2-7B layer shapes", round(sum(Ms) / (sp_wall * 1e-3), 1),
+                 "tokens/s", sp_wall,
+                 f"Llama-2-7B decoder layer, 7 linears, bf16, {int(args.sparsity * 100)}% unstructured magnitude "
+                 f"sparsity, prefill M = 512 and 2048",
+                 {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                  "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": "k_sparse_prefill",
+                  "flops_per_launch": "dense-equivalent 2*M*N*K", "avg_launch_us": round(launch_ms * 1e3, 3)},
+                 cpu, {"per_M": per_M, "sparsity": args.sparsity})
+
+
+def _gen_int8(args):
+    layer, j, N, K = args
+    Wq, mask, sw = synth.int8_weight(synth.weight_seed(layer, j), N, K, 0.7)
+    return layer, j, Wq, mask, sw
+
+
+def run_int8(args):
+    """One layer's seven matrices, int8 weights and activations at 70%, batches 1, 16, 64; 4 layers rotated."""
+    torch, spl = _need_gpu()
+    nl = 4
+    shapes = synth.LLAMA2_7B_LINEARS
+    jobs = [(l, j, N, K) for l in range(nl) for j, (_, N, K) in enumerate(shapes)]
+    host = [[None] * len(shapes) for _ in range(nl)]
+    with cf.ProcessPoolExecutor(max_workers=args.workers) as ex:
+        for l, j, Wq, mask, sw in ex.map(_gen_int8, jobs):
+            host[l][j] = (Wq, mask, sw)
+    layers = []
+    for hl in host:
+        row = []
+        for Wq, mask, sw in hl:
+            Wd = torch.from_numpy(Wq).cuda()
+            Wc = spl.pack_sparse(Wd, torch.from_numpy(mask).cuda())
+            row.append((Wc, Wd if not args.no_dense else None, torch.from_numpy(sw).cuda()))
+        layers.append(row)
+    Ms = [1, 16, 64]
+    xq, sx = [], []
+    for j, (_, N, K) in enumerate(shapes):
+        q, s_ = synth.int8_activations(synth.activation_seed(j), max(Ms), K)
+        xq.append(torch.from_numpy(q).cuda())
+        sx.append(torch.from_numpy(s_).cuda())
+    ys = {(M, j): torch.empty((M, N), dtype=torch.float16, device="cuda") for M in Ms for j, (_, N, _) in
+          enumerate(shapes)}
+    xs = {(M, j): (xq[j][:M].contiguous(), sx[j][:M].contiguous()) for M in Ms for j in range(len(shapes))}
+    units = [(M, j) for M in Ms for j in range(len(shapes))]
+
+    def sparse_fn(li, u):
+        X, s_ = xs[u]
+        Wc, _, sw = layers[li][u[1]]
+        spl.sparse_linear_int8(X, s_, Wc, sw, out=ys[u])
+
+    def dense_fn(li, u):
+        X, s_ = xs[u]
+        _, Wd, sw = layers[li][u[1]]
+        spl.dense_linear_int8(X, s_, Wd, sw, out=ys[u])
+
+    sp_wall, sp_gpu = _timed(units, sparse_fn, args.steps, args.warmup, range(nl))
+
+    def nbytes(M, j):
+        N, K = shapes[j][1], shapes[j][2]
+        return layers[0][j][0].compressed_bytes() + 4 * N + M * K + 4 * M + 2 * M * N
+
+    step_bytes = sum(nbytes(M, j) for (M, j) in units)
+    launch_ms = sp_gpu / len(units)
+    achieved = step_bytes / len(units) / (launch_ms * 1e-3) / 1e9
+    per_M = {}
+    for M in Ms:
+        uM = [u for u in units if u[0] == M]
+        _, g = _timed(uM, sparse_fn, max(20, args.steps // 4), 3, range(nl))
+        b = sum(nbytes(M, j) for (_, j) in uM)
+        d = {"layer_us": round(g * 1e3, 2), "hbm_gbs": round(b / (g * 1e-3) / 1e9, 1)}
+        if not args.no_dense:
+            _, gd = _timed(uM, dense_fn, max(20, args.steps // 4), 3, range(nl))
+            d.update({"dense_layer_us": round(gd * 1e3, 2), "speedup_vs_dense": round(gd / g, 3)})
+        per_M[str(M)] = d
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        packs = [oracle.pack(host[0][j][0], "i8", host[0][j][1]) for j in range(len(shapes))]
+        xh = [synth.int8_activations(synth.activation_seed(j), max(Ms), K) for j, (_, N, K) in enumerate(shapes)]
+        threads = oracle.max_threads()
+
+        def one():
+            for M in Ms:
+                for j in range(len(shapes)):
+                    oracle.linear_i8(xh[j][0][:M], xh[j][1][:M], packs[j], host[0][j][2], nthreads=threads)
+
+        reps, dt = _oracle_repeat(one)
+        cpu = {"value": round(reps * sum(Ms) / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"layer 0's seven int8 matrices at batches {Ms}, int64 sums and the fp16 epilogue, "
+                         f"repeated {reps} times ({dt:.1f} s on {threads} threads)"}
+    return _line(args, "sparse-quantized linear tokens/s + achieved HBM GB/s, Llama-2-7B layer at 70%",
+                 round(sum(Ms) / (sp_wall * 1e-3), 1), "tokens/s", sp_wall,
+                 "Llama-2-7B decoder layer, 7 linears, int8 weights (per-row scales) and int8 activations "
+                 "(per-token scales), 70% sparsity, batches 1, 16, 64, 4 layers rotated",
+                 {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_int8",
+                  "bytes_per_launch": int(step_bytes / len(units)), "avg_launch_us": round(launch_ms * 1e3, 3)},
+                 cpu, {"per_M": per_M}, dtype="i8")
+
+
+def run_stack(args):
+    """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
+    after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
+    torch, spl = _need_gpu()
+    nl = 32
+    host = generate_layers(nl, "bf16", 0.7, args.workers)
+    layers = upload_layers(host, "bf16", keep_dense=not args.no_dense)
+    del host
+    Ms = [1, 2, 4, 8, 16, 32]
+    xs = make_activations("bf16", max(Ms))
+    shapes = synth.LLAMA2_7B_LINEARS
+    xsl = {(M, j): xs[j][:M].contiguous() for M in Ms for j in range(len(shapes))}
+    ys = {(M, j): torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms for j, (_, N, _) in
+          enumerate(shapes)}
+    per_M, tot_tokens, tot_ms, tot_wall = {}, 0, 0.0, 0.0
+    reps = max(5, args.steps // 20)
+    for M in Ms:
+        def sparse_stack(key, unit, M=M):          # layer after layer, 4 grouped launches each
+            for l in range(nl):
+                for u in GROUPED:
+                    spl.sparse_linear_group([xsl[(M, j)] for j in u], [layers[l][j][0] for j in u],
+                                            outs=[ys[(M, j)] for j in u])
+
+        def dense_stack(key, unit, M=M):
+            for l in range(nl):
+                for u in GROUPED:
+                    spl.dense_linear_group([xsl[(M, j)] for j in u], [layers[l][j][1] for j in u],
+                                           outs=[ys[(M, j)] for j in u])
+
+        # one graph = the whole stack (32 layers x 4 launches) at batch M
+        wall, g = _timed(["stack"], sparse_stack, reps, 2, [0])
+        d = {"step_us": round(g * 1e3, 1), "tokens_per_s": round(M / (g * 1e-3), 1)}
+        if not args.no_dense:
+            _, gd = _timed(["stack"], dense_stack, reps, 2, [0])
+            d.update({"dense_step_us": round(gd * 1e3, 1), "speedup_vs_dense": round(gd / g, 3)})
+        per_M[str(M)] = d
+        tot_tokens += M
+        tot_ms += g
+        tot_wall += wall
+    step_bytes = sum(layers[l][j][0].compressed_bytes() for l in range(nl) for j in range(len(shapes)))
+    launches = nl * len(GROUPED)
+    avg_launch_ms = tot_ms / len(Ms) / launches
+    achieved = (step_bytes + sum(M * 156160 * nl for M in Ms) / len(Ms)) / launches / (avg_launch_ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline("bf16", 0.7, [1])
+        cpu["value"] = round(cpu["value"] / nl, 4)
+        cpu["sample"] += f"; tokens/s of the 32-layer stack = that rate / {nl}"
+    return _line(args, "sparse-linear tokens/s, Llama-2-7B 32-layer linear stack at 70%",
+                 round(tot_tokens / (tot_wall * 1e-3), 1), "tokens/s", tot_wall,
+                 "Llama-2-7B linear stack, 32 layers x 7 matrices (distinct seeds), bf16, 70% sparsity, "
+                 f"decode batches {Ms}, grouped driver (4 launches per layer), one graph per batch size",
+                 {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_decode",
+                  "avg_launch_us": round(avg_launch_ms * 1e3, 3)},
+                 cpu, {"per_M": per_M, "compressed_bytes": int(step_bytes)})
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -207,6 +506,10 @@ def main():
     ap.add_argument("--workers", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
+    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "stack"], default="decode",
+                    help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
+                         "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
+                         "int8 weights and activations, batches 1,16,64; stack: all 32 layers at batches 1..32")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -226,6 +529,11 @@ def main():
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
               f"(multi-GPU sharding is a design note only)", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload != "decode":
+        out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "stack": run_stack}[args.workload](args)
+        print(json.dumps(out), flush=True)
+        return
 
     dtype = "bf16"
     batches = [int(b) for b in args.batches.split(",")]
