@@ -103,15 +103,6 @@ __device__ __forceinline__ void build_nibble_table(u32x2* lut) {
   if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{nibble_selector(threadIdx.x, 0), nibble_selector(threadIdx.x, 1)};
 }
 
-// Inclusive prefix sum across each group of 16 lanes (DPP row shifts).
-__device__ __forceinline__ uint32_t row16_inclusive_scan(uint32_t x) {
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);   // row_shr:1
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);   // row_shr:2
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);   // row_shr:4
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);   // row_shr:8
-  return x;
-}
-
 // This wave's contiguous range of k-steps [*beg, *end) of S (W waves).
 template <int W>
 __device__ __forceinline__ void wave_range(int S, int wave, int* beg, int* end) {
@@ -150,22 +141,6 @@ struct XGlobal {
 // spreading rows over the LDS banks.  Lanes of padding batch rows (m >= M)
 // read a 64-byte zero area and do not advance with k.
 __host__ __device__ __forceinline__ int64_t xs_stride(int64_t K) { return 32 * tile_steps(K) + 8; }
-
-typedef __attribute__((address_space(3))) unsigned char lds_t;
-
-// 32-bit LDS offset of a pointer into shared memory, and 16-/4-byte loads at such offsets.
-__device__ __forceinline__ uint32_t lds_off(const void* p) {
-  return (uint32_t)(uintptr_t)(const lds_t*)p;     // address-space cast: generic -> LDS offset
-}
-__device__ __forceinline__ u32x4 lds_load16(uint32_t addr) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>((uintptr_t)addr);
-}
-__device__ __forceinline__ uint32_t lds_load4(uint32_t addr) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>((uintptr_t)addr);
-}
-__device__ __forceinline__ u32x2 lds_load8(uint32_t addr) {
-  return *reinterpret_cast<const __attribute__((address_space(3))) u32x2*>((uintptr_t)addr);
-}
 
 struct XShared {
   uint32_t addr;     // LDS byte address of k-step 0 of this lane's operand

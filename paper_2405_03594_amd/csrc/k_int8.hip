@@ -6,51 +6,58 @@
 //   Y[m][n] = fp16_rne( (float(acc) * sx[m]) * sw[n] )
 // with each product rounded to binary32 (no fused multiply-add).
 //
-// One MFMA covers 64 columns, i.e. two consecutive 16 x 32 tiles of the
-// bitmask layout: lanes 0-31 take tile s, lanes 32-63 tile s + 1; each lane
-// expands 16 int8 values of one tile row from two unaligned 8-byte loads and
-// a byte-indexed v_perm_b32 selector table (paper section 2.4.1).
-//
-// Grid: x = 16-row tile block, y = 16*MT-row batch chunk.  A workgroup of
-// kI8Waves waves splits the column range in groups of kI8Unroll tile pairs;
-// partial int32 sums are combined through LDS (integer addition, so the
-// result does not depend on the order).
+// Sparse kernel (the decode kernel's design with 1-byte payloads): a
+// workgroup owns one 16-row block and its waves split the block's tile pairs
+// into contiguous ranges.  One MFMA covers a pair of consecutive 16 x 32
+// tiles: lanes 0-31 take tile s, lanes 32-63 tile s + 1, lane (fr, fg) row fr,
+// columns 16 (fg % 2) .. +16 of its tile.  A wave stages a chunk of tiles
+// (whole pairs, as many as fit a 3 KB buffer) with aligned 16-byte loads in
+// LDS, the tile offsets of its whole range come with one load, and the next
+// chunk is in flight while the current one is multiplied.  Each lane expands
+// its four 4-column nibbles: the nibble's values start at the tile offset +
+// the kept count of the rows above (16-lane DPP scan) + the popcount of the
+// lower bits of its row, are read as an aligned dword pair realigned with
+// v_alignbyte_b32, and a 16-entry selector table (conflict-free) drives
+// v_perm_b32 (paper section 2.4.1).  Activations of small batches are staged
+// in LDS once per workgroup; int32 partial sums of the waves are added in LDS
+// (integer addition: the order does not matter).
 #include "spl_common.h"
 
 namespace spl {
 namespace {
 
-constexpr int kI8Waves = 8;
+constexpr int kI8Waves = 8;                 // dense kernel
 constexpr int kI8Threads = 64 * kI8Waves;
-constexpr int kI8Unroll = 4;   // tile pairs per wave per group
-
-__device__ __forceinline__ uint32_t i8_nibble_selector(uint32_t byte, int e) {
-  uint32_t sel = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int bit = 4 * e + j;
-    uint32_t s = 0x0Cu;                       // v_perm_b32: selector 12 yields a zero byte
-    if ((byte >> bit) & 1u) s = __popc(byte & ((1u << bit) - 1u));
-    sel |= s << (8 * j);
-  }
-  return sel;
-}
-
-__device__ __forceinline__ uint32_t i8_row16_inclusive_scan(uint32_t x) {
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);   // row_shr:1
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);   // row_shr:2
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);   // row_shr:4
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);   // row_shr:8
-  return x;
-}
+constexpr int kI8Unroll = 4;                // dense kernel: 64-column steps per wave per group
+constexpr int kI8Chunk = 8;                 // sparse: at most this many tiles (4 pairs) per chunk (4 when M > 32)
+constexpr int kI8VBuf = 3072;               // staged value bytes per wave and chunk
+constexpr int kI8VBufAlloc = kI8VBuf + 16;  // + room past the last window
+constexpr int kI8PieceRounds = kI8VBuf / 16 / kWave;
+constexpr int kI8XLdsMax = 32 * 1024;       // activations staged in LDS when M * 64 ceil(S/2) bytes fit
+constexpr int kI8OffsetLanes = kWave - 1;
 
 __device__ __forceinline__ i32x4 mfma_i8(u32x4 a, u32x4 b, i32x4 c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0, 0,
                                                0);
 }
 
-// Combine the waves' partial sums and run the epilogue.  part: [kI8Waves][MT][4][64] int32 in LDS.
-template <int MT>
+// v_perm_b32 selector that expands one 4-column nibble of 1-byte values: byte
+// j takes the value of rank popcount(nib & ((1 << j) - 1)) if bit j is set,
+// else selector 12 (a zero byte).
+__device__ __forceinline__ uint32_t i8_nibble_selector(uint32_t nib) {
+  uint32_t sel = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t b = 0x0Cu;
+    if ((nib >> j) & 1u) b = __popc(nib & ((1u << j) - 1u));
+    sel |= b << (8 * j);
+  }
+  return sel;
+}
+
+// Combine the waves' int32 partial sums and run the epilogue.
+// part: [W][MT][4][64] int32 in LDS; output (f, r, l): n = n0 + 4*(l/16) + r, m = m0 + 16 f + l%16.
+template <int MT, int W>
 __device__ __forceinline__ void i8_finish(const i32x4 (&acc)[MT], int32_t* part, int wave, int lane, int64_t n0,
                                           int64_t N, int64_t m0, int64_t M, const float* __restrict__ sx,
                                           const float* __restrict__ sw, uint16_t* __restrict__ Y,
@@ -60,15 +67,14 @@ __device__ __forceinline__ void i8_finish(const i32x4 (&acc)[MT], int32_t* part,
 #pragma unroll
     for (int r = 0; r < 4; ++r) part[((wave * MT + f) * 4 + r) * 64 + lane] = acc[f][r];
   __syncthreads();
-  // output (f, r, l): n = n0 + 4*(l/16) + r, m = m0 + 16 f + l%16
-  for (int o = threadIdx.x; o < MT * 4 * 64; o += kI8Threads) {
-    int32_t s = 0;
-#pragma unroll
-    for (int w = 0; w < kI8Waves; ++w) s += part[w * MT * 256 + o];
+  for (int o = threadIdx.x; o < MT * 4 * 64; o += W * kWave) {
     const int f = o / 256, r = (o / 64) & 3, l = o & 63;
     const int64_t n = n0 + 4 * (l >> 4) + r;
     const int64_t m = m0 + 16 * f + (l & 15);
     if (n < N && m < M) {
+      int32_t s = 0;
+#pragma unroll
+      for (int w = 0; w < W; ++w) s += part[w * MT * 256 + o];
       if (acc_out) acc_out[m * N + n] = s;
       const float a = static_cast<float>(s);
       const float t = __fmul_rn(a, sx[m]);
@@ -78,99 +84,214 @@ __device__ __forceinline__ void i8_finish(const i32x4 (&acc)[MT], int32_t* part,
   }
 }
 
-template <int MT>
-__global__ void __launch_bounds__(kI8Threads) k_sparse_int8(const int8_t* __restrict__ Xq, const float* __restrict__ sx,
-                                                            int64_t M, int64_t K, const uint32_t* __restrict__ bm_tiles,
-                                                            const int8_t* __restrict__ values,
-                                                            const int32_t* __restrict__ tile_offsets, int64_t N,
-                                                            const float* __restrict__ sw, uint16_t* __restrict__ Y,
-                                                            int32_t* __restrict__ acc_out, int any_values) {
-  __shared__ u32x2 lut[256];
-  __shared__ int32_t part[kI8Waves * MT * 256];
+// int8 activations staged in LDS: rows of 64 * ceil(S / 2) + 16 bytes (whole
+// tile pairs, so the second tile of a last half pair reads zeros), zero past
+// K.  Lanes of padding batch rows read a 64-byte zero area and do not advance.
+__host__ __device__ __forceinline__ int64_t i8_xs_stride(int64_t K) { return 64 * ((tile_steps(K) + 1) / 2) + 16; }
+
+template <int W>
+__device__ __forceinline__ void i8_stage_x(uint8_t* xs, const int8_t* __restrict__ X, int M, int64_t K) {
+  const int per_row = (int)(4 * ((tile_steps(K) + 1) / 2));   // 16-byte pieces per staged row (whole pairs)
+  const int kp = (int)(K / 16);                           // pieces holding activations
+  const int total = M * per_row;
+  for (int p = threadIdx.x; p < total; p += W * kWave) {
+    const int m = p / per_row, q = p - m * per_row;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (q < kp) v = *reinterpret_cast<const u32x4*>(X + (int64_t)m * K + 16 * q);
+    *reinterpret_cast<u32x4*>(xs + (int64_t)m * i8_xs_stride(K) + 16 * q) = v;
+  }
+}
+
+struct I8Chunk {
+  int cn;
+  uint32_t a0;
+  int np;
+};
+
+template <int MT, bool XL, int W>
+__global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
+    const int8_t* __restrict__ Xq, const float* __restrict__ sx, int64_t M, int64_t K,
+    const uint32_t* __restrict__ bm_tiles, const uint8_t* __restrict__ values, const int32_t* __restrict__ tile_offsets,
+    int64_t N, const float* __restrict__ sw, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+  constexpr int C = MT == 4 ? kI8Chunk / 2 : kI8Chunk;     // four batch fragments: half the operands in flight
+  extern __shared__ __align__(16) unsigned char dsm[];     // value buffers (later the partial sums), then X
+  __shared__ uint32_t lut[16];
+  __shared__ u32x4 xzero[4];
+  __shared__ __align__(16) uint32_t words[W][16 * C];       // per wave: [row][tile of the chunk]
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
-  const int half = fg & 1, tsel = fg >> 1;
-  const int S = (int)tile_steps(K);
-  const int P = (S + 1) / 2;                              // tile pairs
-  const int G = (P + kI8Unroll - 1) / kI8Unroll;          // groups of pairs
-  const int64_t b = blockIdx.x;
+  const int tsel = fg >> 1, half = fg & 1;
+  const int64_t blk = blockIdx.x;
   const int64_t m0 = (int64_t)blockIdx.y * 16 * MT;
+  const int S = (int)tile_steps(K);
+  const int P = (S + 1) / 2;
+  // this wave's tiles: whole pairs [2 pb, 2 pe) clipped to S
+  int kbeg, kend;
+  {
+    const int Lp = (P + W - 1) / W;
+    const int pb = wave * Lp < P ? wave * Lp : P;
+    const int pe = pb + Lp < P ? pb + Lp : P;
+    kbeg = 2 * pb;
+    kend = 2 * pe < S ? 2 * pe : S;
+    if (kbeg > kend) kbeg = kend;
+  }
+  const size_t vbytes_region = (size_t)W * kI8VBufAlloc > (size_t)W * MT * 1024 ? (size_t)W * kI8VBufAlloc
+                                                                                  : (size_t)W * MT * 1024;
+  unsigned char* vbuf = dsm + wave * kI8VBufAlloc;
+  uint8_t* xs = reinterpret_cast<uint8_t*>(dsm + vbytes_region);
+  const uint32_t* bmb = bm_tiles + blk * S * 16;
+  const int32_t* tob = tile_offsets + blk * S;
+  uint32_t* wl = words[wave];
 
-  for (int i = threadIdx.x; i < 256; i += kI8Threads)
-    lut[i] = u32x2{i8_nibble_selector(i, 0), i8_nibble_selector(i, 1)};
+  int ob = kbeg;
+  auto load_offsets = [&](int base) {
+    const int t = base + lane < kend ? base + lane : kend;
+    return tob[t];
+  };
+  // whole pairs that fit the staging buffer (1-byte values: offsets are byte positions)
+  auto shape = [&](int32_t o, int c0) {
+    I8Chunk ch;
+    const int r = c0 - ob;
+    ch.a0 = (uint32_t)__builtin_amdgcn_readlane(o, r) & ~15u;
+    const uint32_t lim = ch.a0 + kI8VBuf;
+    const int jmax = kend - c0 < C ? kend - c0 : C;
+    const bool fit = lane >= r + 1 && lane <= r + jmax && (uint32_t)o <= lim;
+    int cn = __builtin_popcountll(__ballot(fit));          // >= 2 when jmax >= 2: two tiles are at most 1 KB
+    if (cn < jmax) cn &= ~1;                                // chunks end on a pair boundary, or at the range end
+    ch.cn = cn;
+    const uint32_t end = (uint32_t)__builtin_amdgcn_readlane(o, r + cn);
+    ch.np = (int)((end - ch.a0 + 15u) >> 4);
+    return ch;
+  };
+  u32x4 vp[kI8PieceRounds];
+  uint32_t wv[C / 4];
+  auto issue = [&](const I8Chunk& ch, int c0) {
+#pragma unroll
+    for (int r = 0; r < kI8PieceRounds; ++r) {
+      vp[r] = u32x4{0u, 0u, 0u, 0u};
+      const uint32_t off = ch.a0 + 16u * (uint32_t)(lane + kWave * r);
+      if (lane + kWave * r < ch.np) vp[r] = *reinterpret_cast<const u32x4*>(values + off);
+    }
+#pragma unroll
+    for (int i = 0; i < C / 4; ++i) {
+      wv[i] = 0u;
+      const uint32_t wi = (uint32_t)(c0 + fg + 4 * i) * 16u + (uint32_t)fr;
+      if (fg + 4 * i < ch.cn) wv[i] = bmb[wi];
+    }
+  };
+
+  int32_t orng = 0;
+  I8Chunk ch{0, 0u, 0};
+  if (kbeg < kend) {
+    orng = load_offsets(ob);
+    ch = shape(orng, kbeg);
+    issue(ch, kbeg);
+  }
+  if (threadIdx.x < 16) lut[threadIdx.x] = i8_nibble_selector(threadIdx.x);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
+  if constexpr (XL) i8_stage_x<W>(xs, Xq, (int)M, K);
   __syncthreads();
 
-  int64_t xrow[MT];
-#pragma unroll
-  for (int f = 0; f < MT; ++f) {
-    const int64_t m = m0 + 16 * f + fr;
-    xrow[f] = (m < M ? m : M - 1) * K;
+  // activation operands: staged (XL) or direct
+  uint32_t xaddr0 = 0, xstep = 0;
+  if constexpr (XL) {
+    const bool live = fr < M;
+    xaddr0 = live ? lds_off(xs + (int64_t)fr * i8_xs_stride(K) + 16 * fg) : lds_off(xzero + fg);
+    xstep = live ? 64u : 0u;
   }
-  const unsigned char* vb = reinterpret_cast<const unsigned char*>(values);
-  const int hshift = 16 * half;
+  const int8_t* xrow[MT];
+  bool xlive[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    const int64_t m = m0 + 16 * t + fr;
+    xlive[t] = m < M;
+    xrow[t] = Xq + (xlive[t] ? m : 0) * K + 16 * fg;
+  }
+  const uint32_t lut_addr = lds_off(lut);
+  const uint32_t vbuf_addr = lds_off(vbuf);
   const uint32_t lowmask = half ? 0xffffu : 0u;
+  u32x4 xs_op = u32x4{0u, 0u, 0u, 0u};
 
   i32x4 acc[MT];
 #pragma unroll
-  for (int f = 0; f < MT; ++f) acc[f] = i32x4{0, 0, 0, 0};
+  for (int t = 0; t < MT; ++t) acc[t] = i32x4{0, 0, 0, 0};
 
-  for (int g = wave; g < G; g += kI8Waves) {
-    uint32_t w[kI8Unroll];
-    uint32_t to[kI8Unroll];
-    bool live[kI8Unroll];
+  for (int c0 = kbeg; c0 < kend;) {
+    // 1. stage the current chunk
 #pragma unroll
-    for (int u = 0; u < kI8Unroll; ++u) {
-      const int p = g * kI8Unroll + u;
-      const int s = 2 * p + tsel;
-      live[u] = p < P && s < S;
-      const int sc = s < S ? s : S - 1;
-      const int64_t t = b * S + sc;
-      w[u] = bm_tiles[t * 16 + fr];
-      to[u] = (uint32_t)tile_offsets[t];
-      if (!live[u]) w[u] = 0u;
+    for (int r = 0; r < kI8PieceRounds; ++r)
+      if (lane + kWave * r < ch.np) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
+#pragma unroll
+    for (int i = 0; i < C / 4; ++i) wl[fr * C + fg + 4 * i] = wv[i];
+    wave_lds_sync();
+    const I8Chunk cur = ch;
+    int32_t tc[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) tc[j] = __builtin_amdgcn_readlane(orng, c0 - ob + j);
+
+    // 2. direct activations for this chunk, then the next chunk's loads
+    u32x4 xb[XL ? 1 : C / 2][MT];
+    if constexpr (!XL) {
+#pragma unroll
+      for (int q = 0; q < C / 2; ++q)
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          const int64_t k = 32 * (int64_t)(c0 + 2 * q) + 16 * fg;
+          xb[q][t] = u32x4{0u, 0u, 0u, 0u};
+          if (2 * q < cur.cn && k < K && xlive[t]) xb[q][t] = *reinterpret_cast<const u32x4*>(xrow[t] + 32 * (int64_t)(c0 + 2 * q));
+        }
     }
-    u32x2 v0[kI8Unroll], v1[kI8Unroll];
-    uint32_t b0[kI8Unroll], b1[kI8Unroll];
-    u32x4 xb[kI8Unroll][MT];
-#pragma unroll
-    for (int u = 0; u < kI8Unroll; ++u) {
-      const uint32_t pc = __popc(w[u]);
-      const uint32_t above = i8_row16_inclusive_scan(pc) - pc;
-      const uint32_t bits = (w[u] >> hshift) & 0xffffu;
-      b0[u] = bits & 0xffu;
-      b1[u] = bits >> 8;
-      const uint32_t oa = to[u] + above + __popc(w[u] & lowmask);
-      const uint32_t ob = oa + __popc(b0[u]);
-      v0[u] = v1[u] = u32x2{0u, 0u};
-      if (any_values) {                                   // values may be absent when nnz == 0
-        __builtin_memcpy(&v0[u], vb + oa, 8);
-        __builtin_memcpy(&v1[u], vb + ob, 8);
+    const int c1 = c0 + cur.cn;
+    if (c1 < kend) {
+      if (c1 - ob + C > kI8OffsetLanes) {
+        ob = c1;
+        orng = load_offsets(ob);
       }
-      const int p = g * kI8Unroll + u;
-      int64_t k = (int64_t)p * 64 + 16 * fg;
-      const bool kok = k < K && p < P;
-      if (!kok) k = 0;
+      ch = shape(orng, c1);
+      issue(ch, c1);
+    }
+
+    // 3. expand and multiply, one tile pair per MFMA
+    const uint32_t vrel = vbuf_addr - cur.a0;
 #pragma unroll
-      for (int f = 0; f < MT; ++f) {
-        u32x4 x = *reinterpret_cast<const u32x4*>(Xq + xrow[f] + k);
-        if (!kok) x = u32x4{0u, 0u, 0u, 0u};
-        xb[u][f] = x;
+    for (int q = 0; q < C / 2; ++q) {
+      if (2 * q < cur.cn) {
+        const int j = 2 * q + tsel;                            // this lane's tile in the chunk
+        uint32_t w = wl[fr * C + j];
+        if (j >= cur.cn) w = 0u;                               // a range ending on half a pair
+        const uint32_t pc = __popc(w);
+        const uint32_t above = row16_inclusive_scan(pc) - pc;
+        // this lane's tile offset: the pair's first or second (arithmetic select keeps tc[] in registers)
+        const uint32_t tile0 = (uint32_t)tc[2 * q] + (((uint32_t)tc[2 * q + 1] - (uint32_t)tc[2 * q]) & (0u - (uint32_t)tsel));
+        const uint32_t oa = tile0 + above + __popc(w & lowmask);
+        u32x4 a;
+        uint32_t o = oa;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t nib = __builtin_amdgcn_ubfe(w, 16 * half + 4 * i, 4);
+          const uint32_t p = o + vrel;
+          const uint32_t d = p & ~3u;
+          const uint32_t lo = lds_load4(d), hi = lds_load4(d + 4);
+          const uint32_t win = __builtin_amdgcn_alignbyte(hi, lo, p);
+          const uint32_t sel = lds_load4(lut_addr + 4u * nib);
+          a[i] = __builtin_amdgcn_perm(0u, win, sel);
+          o += __popc(nib);
+        }
+        if constexpr (XL) {
+          if (xstep) xs_op = lds_load16(xaddr0 + xstep * (uint32_t)((c0 >> 1) + q));
+          acc[0] = mfma_i8(a, xs_op, acc[0]);
+        } else {
+#pragma unroll
+          for (int t = 0; t < MT; ++t) acc[t] = mfma_i8(a, xb[q][t], acc[t]);
+        }
       }
     }
-#pragma unroll
-    for (int u = 0; u < kI8Unroll; ++u) {
-      const u32x2 s0 = lut[b0[u]], s1 = lut[b1[u]];
-      u32x4 a;
-      a.x = __builtin_amdgcn_perm(v0[u].y, v0[u].x, s0.x);
-      a.y = __builtin_amdgcn_perm(v0[u].y, v0[u].x, s0.y);
-      a.z = __builtin_amdgcn_perm(v1[u].y, v1[u].x, s1.x);
-      a.w = __builtin_amdgcn_perm(v1[u].y, v1[u].x, s1.y);
-#pragma unroll
-      for (int f = 0; f < MT; ++f) acc[f] = mfma_i8(a, xb[u][f], acc[f]);
-    }
+    wave_lds_sync();
+    c0 = c1;
   }
-  i8_finish<MT>(acc, part, wave, lane, b * 16, N, m0, M, sx, sw, Y, acc_out);
+  __syncthreads();
+  i8_finish<MT, W>(acc, reinterpret_cast<int32_t*>(dsm), wave, lane, blk * 16, N, m0, M, sx, sw, Y, acc_out);
 }
 
 template <int MT>
@@ -220,30 +341,59 @@ __global__ void __launch_bounds__(kI8Threads) k_dense_int8(const int8_t* __restr
 #pragma unroll
       for (int f = 0; f < MT; ++f) acc[f] = mfma_i8(a[u], xb[u][f], acc[f]);
   }
-  i8_finish<MT>(acc, part, wave, lane, n0, N, m0, M, sx, sw, Y, acc_out);
+  i8_finish<MT, kI8Waves>(acc, part, wave, lane, n0, N, m0, M, sx, sw, Y, acc_out);
 }
 
 int i8_fragments(int64_t M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
+
+template <int MT, bool XL, int W>
+hipError_t sparse_int8_launch(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc, const float* sw,
+                              void* Y, int32_t* acc_out, hipStream_t s) {
+  auto* kernel = k_sparse_int8<MT, XL, W>;
+  const size_t region = (size_t)W * kI8VBufAlloc > (size_t)W * MT * 1024 ? (size_t)W * kI8VBufAlloc
+                                                                          : (size_t)W * MT * 1024;
+  const size_t xbytes = XL ? (size_t)M * (size_t)i8_xs_stride(Wc.cols) : 0;
+  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                     (int)(region + (XL ? kI8XLdsMax + 16 * 16 : 0)));
+  if (attr != hipSuccess) return attr;
+  const dim3 grid((unsigned)tile_blocks(Wc.rows), (unsigned)((M + 16 * MT - 1) / (16 * MT)));
+  hipLaunchKernelGGL(kernel, grid, dim3(W * kWave), region + xbytes, s, Xq, sx, M, Wc.cols, Wc.bitmask,
+                     static_cast<const uint8_t*>(Wc.values), Wc.tile_offsets, Wc.rows, sw,
+                     static_cast<uint16_t*>(Y), acc_out);
+  return hipGetLastError();
+}
+
+template <int W>
+hipError_t sparse_int8_w(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc, const float* sw,
+                         void* Y, int32_t* acc_out, hipStream_t s) {
+  const int MT = i8_fragments(M);
+  if (MT == 1 && M * 64 * ((tile_steps(Wc.cols) + 1) / 2) <= kI8XLdsMax)
+    return sparse_int8_launch<1, true, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
+  if (MT == 1) return sparse_int8_launch<1, false, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
+  if (MT == 2) return sparse_int8_launch<2, false, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
+  return sparse_int8_launch<4, false, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
+}
+
+// 16 waves per workgroup when the grid has fewer than two row blocks per CU.
+bool i8_small_grid(int64_t blocks) {
+  static int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                   hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  return blocks < 2 * (int64_t)cus;
+}
 
 }  // namespace
 
 hipError_t launch_sparse_int8(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc, const float* sw,
                               void* Y, int32_t* acc_out, hipStream_t s) {
-  const int MT = i8_fragments(M);
-  const dim3 grid((unsigned)tile_blocks(Wc.rows), (unsigned)((M + 16 * MT - 1) / (16 * MT))), block(kI8Threads);
-  const int8_t* vals = static_cast<const int8_t*>(Wc.values);
-  const int any = Wc.nnz > 0 ? 1 : 0;
-  uint16_t* y = static_cast<uint16_t*>(Y);
-  if (MT == 1)
-    hipLaunchKernelGGL((k_sparse_int8<1>), grid, block, 0, s, Xq, sx, M, Wc.cols, Wc.bitmask, vals, Wc.tile_offsets,
-                       Wc.rows, sw, y, acc_out, any);
-  else if (MT == 2)
-    hipLaunchKernelGGL((k_sparse_int8<2>), grid, block, 0, s, Xq, sx, M, Wc.cols, Wc.bitmask, vals, Wc.tile_offsets,
-                       Wc.rows, sw, y, acc_out, any);
-  else
-    hipLaunchKernelGGL((k_sparse_int8<4>), grid, block, 0, s, Xq, sx, M, Wc.cols, Wc.bitmask, vals, Wc.tile_offsets,
-                       Wc.rows, sw, y, acc_out, any);
-  return hipGetLastError();
+  const int64_t blocks = tile_blocks(Wc.rows) * ((M + 63) / 64);
+  return i8_small_grid(blocks) ? sparse_int8_w<16>(Xq, sx, M, Wc, sw, Y, acc_out, s)
+                               : sparse_int8_w<8>(Xq, sx, M, Wc, sw, Y, acc_out, s);
 }
 
 hipError_t launch_dense_int8(const int8_t* Xq, const float* sx, int64_t M, const int8_t* Wq, const float* sw,

@@ -60,13 +60,6 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
   return sel;
 }
 
-__device__ __forceinline__ uint32_t pf_row16_inclusive_scan(uint32_t x) {
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);   // row_shr:1
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);   // row_shr:2
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);   // row_shr:4
-  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);   // row_shr:8
-  return x;
-}
 
 // Activation staging: thread t moves X[m0 + t/2][32s + 16(t%2) .. +16] for
 // the k-steps of one stage (two 16-byte pieces per k-step).  Rows past M and
@@ -148,7 +141,7 @@ __global__ void __launch_bounds__(kPfThreads) k_sparse_prefill(const uint16_t* _
         uint32_t w = bm_tiles[t * 16 + fr];
         if (!bok[u] || s0 + j >= S) w = 0u;
         const uint32_t pc = __popc(w);
-        const uint32_t above = pf_row16_inclusive_scan(pc) - pc;
+        const uint32_t above = row16_inclusive_scan(pc) - pc;
         const uint32_t b = (w >> byte_shift) & 0xffu;
         const uint32_t oa = (uint32_t)tile_offsets[t] + above + __popc(w & lowmask);
         const uint32_t ob = oa + __popc(b & 0xfu);

@@ -59,6 +59,32 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Inclusive prefix sum across each group of 16 lanes (DPP row shifts; lanes
+// shifted in from outside the row contribute 0).
+__device__ __forceinline__ uint32_t row16_inclusive_scan(uint32_t x) {
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+  return x;
+}
+
+typedef __attribute__((address_space(3))) unsigned char lds_t;
+
+// 32-bit LDS offset of a pointer into shared memory, and loads at such offsets.
+__device__ __forceinline__ uint32_t lds_off(const void* p) {
+  return (uint32_t)(uintptr_t)(const lds_t*)p;     // address-space cast: generic -> LDS offset
+}
+__device__ __forceinline__ u32x4 lds_load16(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>((uintptr_t)addr);
+}
+__device__ __forceinline__ uint32_t lds_load4(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) uint32_t*>((uintptr_t)addr);
+}
+__device__ __forceinline__ u32x2 lds_load8(uint32_t addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) u32x2*>((uintptr_t)addr);
+}
+
 __host__ __device__ __forceinline__ int64_t words_per_row(int64_t K) { return (K + 31) / 32; }
 // Tile layout geometry: 16-row blocks and 32-column steps.
 __host__ __device__ __forceinline__ int64_t tile_blocks(int64_t N) { return (N + 15) / 16; }
