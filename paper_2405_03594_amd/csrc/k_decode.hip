@@ -277,7 +277,10 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
   __shared__ u32x4 xzero[4];
-  __shared__ __align__(16) uint32_t words[W][16 * C];   // per wave: [row][tile of the chunk]
+  // per wave: [row][tile of the chunk]; the row stride C + 2 (even, for the 8-byte pair reads) puts
+  // the 16 rows in distinct banks
+  constexpr int WS = C + 2;
+  __shared__ __align__(16) uint32_t words[W][16 * WS];
   const int ti = find_task(g.first, g.count);
   const SparseTaskArg tk = g.t[ti];
   const int M = g.M;
@@ -373,7 +376,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     for (int r = 0; r < kPieceRounds; ++r)
       if (lane + kWave * r < ch.np) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
 #pragma unroll
-    for (int i = 0; i < C / 4; ++i) wl[fr * C + fg + 4 * i] = wv[i];
+    for (int i = 0; i < C / 4; ++i) wl[fr * WS + fg + 4 * i] = wv[i];
     wave_lds_sync();
     const Chunk cur = ch;
     int32_t tc[C];                                     // the chunk's tile offsets (wave-uniform)
@@ -403,7 +406,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
 #pragma unroll
     for (int jp = 0; jp < C; jp += 2) {
       if (jp < cur.cn) {
-        const u32x2 wp = *reinterpret_cast<const u32x2*>(wl + fr * C + jp);
+        const u32x2 wp = *reinterpret_cast<const u32x2*>(wl + fr * WS + jp);
         // kept count of the rows above mine for both tiles (16-bit halves, sums <= 512)
         const uint32_t pc = __popc(wp.x) | (__popc(wp.y) << 16);
         const uint32_t ex = row16_inclusive_scan(pc) - pc;

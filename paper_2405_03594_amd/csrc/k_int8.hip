@@ -117,7 +117,9 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
   extern __shared__ __align__(16) unsigned char dsm[];     // value buffers (later the partial sums), then X
   __shared__ uint32_t lut[16];
   __shared__ u32x4 xzero[4];
-  __shared__ __align__(16) uint32_t words[W][16 * C];       // per wave: [row][tile of the chunk]
+  // per wave: [row][tile of the chunk]; the odd row stride C + 1 puts the 16 rows in distinct banks
+  constexpr int WS = C + 1;
+  __shared__ __align__(16) uint32_t words[W][16 * WS];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
@@ -223,7 +225,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
     for (int r = 0; r < kI8PieceRounds; ++r)
       if (lane + kWave * r < ch.np) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
 #pragma unroll
-    for (int i = 0; i < C / 4; ++i) wl[fr * C + fg + 4 * i] = wv[i];
+    for (int i = 0; i < C / 4; ++i) wl[fr * WS + fg + 4 * i] = wv[i];
     wave_lds_sync();
     const I8Chunk cur = ch;
     int32_t tc[C];
@@ -258,7 +260,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
     for (int q = 0; q < C / 2; ++q) {
       if (2 * q < cur.cn) {
         const int j = 2 * q + tsel;                            // this lane's tile in the chunk
-        uint32_t w = wl[fr * C + j];
+        uint32_t w = wl[fr * WS + j];
         if (j >= cur.cn) w = 0u;                               // a range ending on half a pair
         const uint32_t pc = __popc(w);
         const uint32_t above = row16_inclusive_scan(pc) - pc;
