@@ -1,32 +1,35 @@
-// Prefill-shaped kernels (any batch M, sized for M >= 64) for gfx950.
+// Prefill-shaped kernels (any batch M, sized for M >= 128) for gfx950.
 //
-// Sparse (paper section 2.4.2): the compressed 16 x 32 submatrices of W are
-// expanded in registers into MFMA A operands (bitmask-guided v_perm_b32 of
-// the stored values, as in the decode kernel) and multiplied at the dense
-// rate against activation tiles staged in LDS.
+// One GEMM core serves both kernels.  A workgroup (4 waves) computes a
+// 128 (n) x 128 (m) block of Y = X W^T; wave (wn, wm) owns 64 x 64 of it,
+// 4 x 4 v_mfma_f32_16x16x32 fragments per 32-column k-step.  K advances 64
+// columns per stage through two LDS buffers per operand: 128 rows of 64
+// elements, padded to 144 bytes so that the 16-byte fragment reads of eight
+// consecutive rows fall in distinct banks.  The next stage's global loads are
+// in flight while the current stage is multiplied, and one barrier per stage
+// hands the buffers over.
 //
-//   * a workgroup (4 waves) owns a 64 (n) x 128 (m) output block; wave
-//     (wn, wm) owns 32 x 64: two W tiles (rows) by four 16-column batch
-//     fragments, i.e. eight v_mfma_f32_16x16x32 per 32-column k-step;
-//   * activations X[m0 .. m0+128)[k-step] go HBM -> registers -> LDS, double
-//     buffered two k-steps at a time; each wave reads its B operands with
-//     16-byte LDS reads;
-//   * W operands for the next k-step pair are fetched (words, tile offsets,
-//     nibble windows) while the current pair is multiplied.
-// Dense comparator: the same schedule with W operands loaded directly from
-// the dense rows.
+//   * dense (comparator): W rows are copied into the A buffer exactly like
+//     X rows into the B buffer;
+//   * sparse (paper section 2.4.2): the A buffer is filled by expanding the
+//     stage's sixteen compressed 16 x 32 tiles (8 row blocks x 2 k-steps,
+//     four per wave), each once per workgroup: bitmask words are fetched two
+//     stages ahead and value windows one stage ahead; a lane expands its row's
+//     8 columns with v_perm_b32 under a nibble selector table, as in the decode
+//     kernel, and writes them with one 16-byte LDS store.
 #include "spl_common.h"
 
 namespace spl {
 namespace {
 
 constexpr int kPfThreads = 256;
-constexpr int kPfBN = 64;                  // W rows per workgroup
-constexpr int kPfBM = 128;                 // batch rows per workgroup
-constexpr int kPfStage = 2;                // k-steps (32 columns each) per LDS stage
-constexpr int kPfXStride = 64 + 16;        // bytes per staged activation row of one k-step (padded)
-constexpr int kPfXStep = kPfBM * kPfXStride;          // bytes per k-step of staged activations
-constexpr int kPfXBuf = kPfStage * kPfXStep;          // bytes per stage buffer
+constexpr int kPfBN = 128;                       // W rows (n) per workgroup
+constexpr int kPfBM = 128;                       // X rows (m) per workgroup
+constexpr int kPfBK = 64;                        // k columns per stage: two 32-column tile steps
+constexpr int kPfRow = kPfBK * 2 + 16;           // bytes per staged row (padded)
+constexpr int kPfBuf = 128 * kPfRow;             // bytes of one operand buffer
+constexpr int kPfLds = 4 * kPfBuf;               // A and B, two buffers each
+constexpr int kPfPieces = 128 * kPfBK / 8 / kPfThreads;   // 16-byte pieces per thread per operand per stage
 
 template <class T>
 struct MfmaP;
@@ -45,6 +48,9 @@ struct MfmaP<F16> {
   }
 };
 
+// v_perm_b32 selector for the 16-bit elements (2h, 2h+1) of a 4-column nibble
+// whose stored values sit, in order, in the 8 source bytes: a kept element
+// takes the two bytes of its rank, a dropped one 0x0C (a zero byte).
 __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
   uint32_t sel = 0;
 #pragma unroll
@@ -60,257 +66,266 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
   return sel;
 }
 
-
-// Activation staging: thread t moves X[m0 + t/2][32s + 16(t%2) .. +16] for
-// the k-steps of one stage (two 16-byte pieces per k-step).  Rows past M and
-// columns past K are zero.
-struct XStage {
-  u32x4 v[kPfStage][2];
+// Rows [r0, r0 + 128) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
+// moved through registers: thread t holds rows r0 + t/8 + 32i (i < 4), columns
+// k0 + 8 (t % 8) .. +8; rows past R and columns past K read as zeros
+// (K % 8 == 0, so a 16-byte piece is wholly inside or outside).
+struct Slab {
+  u32x4 v[kPfPieces];
 };
 
-__device__ __forceinline__ void x_fetch(XStage& st, const uint16_t* __restrict__ X, int64_t M, int64_t K, int64_t m0,
-                                        int s0, int S) {
-  const int t = threadIdx.x;
-  const int64_t m = m0 + (t >> 1);
-  const bool mok = m < M;
-  const int64_t mm = mok ? m : M - 1;
+struct SlabSrc {
+  const uint16_t* row0;   // this thread's first row at column 8 (t % 8)
+  int64_t stride;         // elements between its rows (32 K)
+  int rows_left;          // rows of the matrix from its first row on
+  int col;                // its column offset 8 (t % 8)
+
+  __device__ __forceinline__ SlabSrc(const uint16_t* __restrict__ A, int64_t R, int64_t K, int64_t r0) {
+    const int64_t r = r0 + (threadIdx.x >> 3);
+    col = 8 * (threadIdx.x & 7);
+    rows_left = r < R ? (int)(R - r) : 0;
+    row0 = A + (r < R ? r : 0) * K + col;
+    stride = 32 * K;
+  }
+  __device__ __forceinline__ void fetch(Slab& sl, int64_t K, int64_t k0) const {
+    const bool kok = k0 + col < K;
 #pragma unroll
-  for (int j = 0; j < kPfStage; ++j) {
-    const int s = s0 + j < S ? s0 + j : S - 1;
+    for (int i = 0; i < kPfPieces; ++i) {
+      sl.v[i] = u32x4{0u, 0u, 0u, 0u};
+      if (kok && 32 * i < rows_left) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
+    }
+  }
+};
+
+__device__ __forceinline__ void slab_store(const Slab& sl, uint32_t buf) {
+  const uint32_t base = buf + (threadIdx.x >> 3) * kPfRow + 16 * (threadIdx.x & 7);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      int64_t k = (int64_t)s * 32 + (t & 1) * 16 + h * 8;
-      const bool kok = k < K && s0 + j < S;
-      if (k > K - 8) k = K - 8;
-      u32x4 v = *reinterpret_cast<const u32x4*>(X + mm * K + k);
-      if (!(mok && kok)) v = u32x4{0u, 0u, 0u, 0u};
-      st.v[j][h] = v;
+  for (int i = 0; i < kPfPieces; ++i)
+    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(base + 32 * kPfRow * i)) = sl.v[i];
+}
+
+// One stage of MFMA work: wave (wn, wm) multiplies its 64 x 64 block over the
+// stage's two k-steps from the A (W) and B (X) buffers.
+template <class T>
+__device__ __forceinline__ void pf_mfma_stage(f32x4 (&acc)[4][4], uint32_t abuf, uint32_t bbuf, int wn, int wm, int fr,
+                                              int fg) {
+  const uint32_t a0 = abuf + (wn * 64 + fr) * kPfRow + 16 * fg;
+  const uint32_t b0 = bbuf + (wm * 64 + fr) * kPfRow + 16 * fg;
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    u32x4 a[4], b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = lds_load16(a0 + 16 * kPfRow * i + 64 * ks);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = lds_load16(b0 + 16 * kPfRow * j + 64 * ks);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = MfmaP<T>::run(a[i], b[j], acc[i][j]);
+  }
+}
+
+// D layout: lane l, register r -> row (n) 4 (l / 16) + r, column (m) l % 16.
+template <class T>
+__device__ __forceinline__ void pf_store(const f32x4 (&acc)[4][4], uint16_t* __restrict__ Y, int64_t M, int64_t N,
+                                         int64_t n0, int64_t m0, int wn, int wm, int fr, int fg) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t m = m0 + wm * 64 + 16 * j + fr;
+    if (m >= M) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t n = n0 + wn * 64 + 16 * i + 4 * fg;
+      uint16_t* y = Y + m * N + n;
+      if (n + 3 < N && (N & 3) == 0) {
+        u32x2 p;
+        p.x = (uint32_t)T::from_f32(acc[i][j][0]) | ((uint32_t)T::from_f32(acc[i][j][1]) << 16);
+        p.y = (uint32_t)T::from_f32(acc[i][j][2]) | ((uint32_t)T::from_f32(acc[i][j][3]) << 16);
+        *reinterpret_cast<u32x2*>(y) = p;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (n + r < N) y[r] = T::from_f32(acc[i][j][r]);
+      }
     }
   }
 }
 
-__device__ __forceinline__ void x_store(const XStage& st, unsigned char* buf) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int j = 0; j < kPfStage; ++j)
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-      *reinterpret_cast<u32x4*>(buf + j * kPfXStep + (t >> 1) * kPfXStride + (t & 1) * 32 + h * 16) = st.v[j][h];
-}
-
-// W operands of one wave for one stage: two tiles x kPfStage k-steps.
-struct WStage {
-  u32x2 v0[kPfStage][2], v1[kPfStage][2];
-  uint32_t byte[kPfStage][2];
+// Compressed operands of a wave's four tiles of one stage: tile i is row block
+// 2 wave + i / 2 of the workgroup's eight, k-step i % 2 of the stage.
+struct TileWords {
+  uint32_t w[4];        // bitmask word of row fr
+  int32_t off[4];       // tile offset (index of the tile's first value)
+};
+struct TileWindows {
+  uint32_t byte[4];     // this lane's 8 columns of row fr
+  u32x2 v0[4], v1[4];   // 8-byte windows from the first value of each nibble
 };
 
 template <class T>
-__global__ void __launch_bounds__(kPfThreads) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
-                                                               const uint32_t* __restrict__ bm_tiles,
-                                                               const uint16_t* __restrict__ values,
-                                                               const int32_t* __restrict__ tile_offsets, int64_t N,
-                                                               uint16_t* __restrict__ Y) {
-  __shared__ __align__(16) unsigned char xs[2][kPfXBuf];
-  __shared__ u32x4 lut[256];
+__global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
+                                                                  const uint32_t* __restrict__ bm_tiles,
+                                                                  const uint16_t* __restrict__ values,
+                                                                  const int32_t* __restrict__ tile_offsets, int64_t N,
+                                                                  uint16_t* __restrict__ Y) {
+  extern __shared__ __align__(16) unsigned char dsm[];
+  __shared__ u32x2 lut[16];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
+  const int nst = (S + 1) / 2;
   const int64_t B = tile_blocks(N);
+  const int64_t n0 = (int64_t)blockIdx.x * kPfBN;
   const int64_t m0 = (int64_t)blockIdx.y * kPfBM;
-  const int64_t b0 = (int64_t)blockIdx.x * (kPfBN / 16) + 2 * wn;   // first of the wave's two tile rows
-  const int64_t bt[2] = {b0 < B ? b0 : B - 1, b0 + 1 < B ? b0 + 1 : B - 1};
-  const bool bok[2] = {b0 < B, b0 + 1 < B};
-
-  for (int b = threadIdx.x; b < 256; b += kPfThreads)
-    lut[b] = u32x4{pf_nibble_selector(b & 15u, 0), pf_nibble_selector(b & 15u, 1), pf_nibble_selector(b >> 4, 0),
-                   pf_nibble_selector(b >> 4, 1)};
-
+  const int64_t nb0 = n0 / 16;
+  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + kPfBuf)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * kPfBuf), lds_off(dsm + 3 * kPfBuf)};
+  const uint32_t lut_addr = lds_off(lut);
   const uint32_t lowmask = (1u << (8 * fg)) - 1u;
-  const int byte_shift = 8 * fg;
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
+  if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{pf_nibble_selector(threadIdx.x, 0), pf_nibble_selector(threadIdx.x, 1)};
 
-  auto w_fetch = [&](WStage& ws, int s0) {
+  auto fetch_words = [&](TileWords& tw, int st) {
 #pragma unroll
-    for (int j = 0; j < kPfStage; ++j) {
-      const int s = s0 + j < S ? s0 + j : S - 1;
+    for (int i = 0; i < 4; ++i) {
+      const int64_t b = nb0 + 2 * wave + (i >> 1);
+      const int s = 2 * st + (i & 1);
+      const bool ok = b < B && s < S;
+      const int64_t t = ok ? b * S + s : 0;
+      tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;
+      tw.off[i] = tile_offsets[t];
+    }
+  };
+  auto fetch_windows = [&](TileWindows& tv, const TileWords& tw) {
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int64_t t = bt[u] * S + s;
-        uint32_t w = bm_tiles[t * 16 + fr];
-        if (!bok[u] || s0 + j >= S) w = 0u;
-        const uint32_t pc = __popc(w);
-        const uint32_t above = row16_inclusive_scan(pc) - pc;
-        const uint32_t b = (w >> byte_shift) & 0xffu;
-        const uint32_t oa = (uint32_t)tile_offsets[t] + above + __popc(w & lowmask);
-        const uint32_t ob = oa + __popc(b & 0xfu);
-        ws.byte[j][u] = b;
-        __builtin_memcpy(&ws.v0[j][u], vbytes + oa * 2u, 8);
-        __builtin_memcpy(&ws.v1[j][u], vbytes + ob * 2u, 8);
-      }
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t w = tw.w[i];
+      const uint32_t pc = __popc(w);
+      const uint32_t above = row16_inclusive_scan(pc) - pc;          // kept values of the rows above mine
+      const uint32_t oa = (uint32_t)tw.off[i] + above + __popc(w & lowmask);
+      const uint32_t byte = __builtin_amdgcn_ubfe(w, 8 * fg, 8);
+      const uint32_t ob = oa + __popc(byte & 0xfu);
+      tv.byte[i] = byte;
+      __builtin_memcpy(&tv.v0[i], vbytes + 2u * oa, 8);
+      __builtin_memcpy(&tv.v1[i], vbytes + 2u * ob, 8);
+    }
+  };
+  auto expand_store = [&](const TileWindows& tv, uint32_t buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const u32x2 slo = lds_load8(lut_addr + 8u * (tv.byte[i] & 0xfu));
+      const u32x2 shi = lds_load8(lut_addr + 8u * (tv.byte[i] >> 4));
+      u32x4 a;
+      a.x = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.x);
+      a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.y);
+      a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.x);
+      a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.y);
+      const uint32_t at = buf + (16 * (2 * wave + (i >> 1)) + fr) * kPfRow + 64 * (i & 1) + 16 * fg;
+      *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)at) = a;
     }
   };
 
-  f32x4 acc[2][4];
+  f32x4 acc[4][4];
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int f = 0; f < 4; ++f) acc[u][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  XStage xst;
-  WStage ws;
-  x_fetch(xst, X, M, K, m0, 0, S);
-  w_fetch(ws, 0);
-  x_store(xst, xs[0]);
+  const SlabSrc xsrc(X, M, K, m0);
+  Slab xs;
+  TileWords tw;
+  TileWindows tv;
+  fetch_words(tw, 0);
+  xsrc.fetch(xs, K, 0);
+  fetch_windows(tv, tw);
+  if (nst > 1) fetch_words(tw, 1);
+  __syncthreads();                                     // the selector table
+  expand_store(tv, abuf[0]);
+  slab_store(xs, bbuf[0]);
   __syncthreads();
-  int buf = 0;
-  for (int s0 = 0; s0 < S; s0 += kPfStage) {
-    const bool more = s0 + kPfStage < S;
-    // expand this stage's W operands before the registers are refilled
-    u32x4 a[kPfStage][2];
-#pragma unroll
-    for (int j = 0; j < kPfStage; ++j)
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const u32x4 sel = lut[ws.byte[j][u]];
-        a[j][u].x = __builtin_amdgcn_perm(ws.v0[j][u].y, ws.v0[j][u].x, sel.x);
-        a[j][u].y = __builtin_amdgcn_perm(ws.v0[j][u].y, ws.v0[j][u].x, sel.y);
-        a[j][u].z = __builtin_amdgcn_perm(ws.v1[j][u].y, ws.v1[j][u].x, sel.z);
-        a[j][u].w = __builtin_amdgcn_perm(ws.v1[j][u].y, ws.v1[j][u].x, sel.w);
-      }
+  for (int st = 0; st < nst; ++st) {
+    const int cur = st & 1;
+    const bool more = st + 1 < nst;
     if (more) {
-      x_fetch(xst, X, M, K, m0, s0 + kPfStage, S);
-      w_fetch(ws, s0 + kPfStage);
+      // stage st + 1: its words were fetched a stage ago, so the windows go out first (the wait for
+      // the words must not also wait for this stage's activation loads)
+      fetch_windows(tv, tw);
+      xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
+      if (st + 2 < nst) fetch_words(tw, st + 2);
     }
-    const unsigned char* xb = xs[buf];
-#pragma unroll
-    for (int j = 0; j < kPfStage; ++j) {
-      if (s0 + j < S) {
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const u32x4 bop = *reinterpret_cast<const u32x4*>(xb + j * kPfXStep + (wm * 64 + f * 16 + fr) * kPfXStride +
-                                                            fg * 16);
-#pragma unroll
-          for (int u = 0; u < 2; ++u) acc[u][f] = MfmaP<T>::run(a[j][u], bop, acc[u][f]);
-        }
-      }
-    }
+    pf_mfma_stage<T>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
-      x_store(xst, xs[buf ^ 1]);
+      expand_store(tv, abuf[cur ^ 1]);
+      slab_store(xs, bbuf[cur ^ 1]);
       __syncthreads();
-      buf ^= 1;
     }
   }
-
-  // D layout: lane l, register i -> row (n) 4*(l/16)+i of the tile, column (m) l%16
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int64_t nb = (b0 + u) * 16 + 4 * fg;
-#pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      const int64_t m = m0 + wm * 64 + f * 16 + fr;
-      if (m < M && b0 + u < B) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (nb + i < N) Y[m * N + nb + i] = T::from_f32(acc[u][f][i]);
-      }
-    }
-  }
+  pf_store<T>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
 template <class T>
-__global__ void __launch_bounds__(kPfThreads) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
-                                                              const uint16_t* __restrict__ W, int64_t N,
-                                                              uint16_t* __restrict__ Y) {
-  __shared__ __align__(16) unsigned char xs[2][kPfXBuf];
+__global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
+                                                                 const uint16_t* __restrict__ W, int64_t N,
+                                                                 uint16_t* __restrict__ Y) {
+  extern __shared__ __align__(16) unsigned char dsm[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
+  const int nst = (S + 1) / 2;
+  const int64_t n0 = (int64_t)blockIdx.x * kPfBN;
   const int64_t m0 = (int64_t)blockIdx.y * kPfBM;
-  const int64_t n0 = (int64_t)blockIdx.x * kPfBN + 32 * wn;
-  const int64_t rows[2] = {n0 + fr < N ? n0 + fr : N - 1, n0 + 16 + fr < N ? n0 + 16 + fr : N - 1};
+  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + kPfBuf)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * kPfBuf), lds_off(dsm + 3 * kPfBuf)};
 
-  struct WD {
-    u32x4 a[kPfStage][2];
-  };
-  auto w_fetch = [&](WD& wd, int s0) {
+  f32x4 acc[4][4];
 #pragma unroll
-    for (int j = 0; j < kPfStage; ++j) {
-      const int s = s0 + j < S ? s0 + j : S - 1;
-      int64_t k = (int64_t)s * 32 + fg * 8;
-      const bool kok = k < K && s0 + j < S;
-      if (k > K - 8) k = K - 8;
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        u32x4 v = *reinterpret_cast<const u32x4*>(W + rows[u] * K + k);
-        if (!kok) v = u32x4{0u, 0u, 0u, 0u};
-        wd.a[j][u] = v;
-      }
-    }
-  };
-  f32x4 acc[2][4];
-#pragma unroll
-  for (int u = 0; u < 2; ++u)
-#pragma unroll
-    for (int f = 0; f < 4; ++f) acc[u][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  XStage xst;
-  WD wd;
-  x_fetch(xst, X, M, K, m0, 0, S);
-  w_fetch(wd, 0);
-  x_store(xst, xs[0]);
+  const SlabSrc xsrc(X, M, K, m0), wsrc(W, N, K, n0);
+  Slab xs, ws;
+  xsrc.fetch(xs, K, 0);
+  wsrc.fetch(ws, K, 0);
+  slab_store(ws, abuf[0]);
+  slab_store(xs, bbuf[0]);
   __syncthreads();
-  int buf = 0;
-  for (int s0 = 0; s0 < S; s0 += kPfStage) {
-    const bool more = s0 + kPfStage < S;
-    WD cur = wd;
+  for (int st = 0; st < nst; ++st) {
+    const int cur = st & 1;
+    const bool more = st + 1 < nst;
     if (more) {
-      x_fetch(xst, X, M, K, m0, s0 + kPfStage, S);
-      w_fetch(wd, s0 + kPfStage);
+      xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
+      wsrc.fetch(ws, K, (int64_t)kPfBK * (st + 1));
     }
-    const unsigned char* xb = xs[buf];
-#pragma unroll
-    for (int j = 0; j < kPfStage; ++j) {
-      if (s0 + j < S) {
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const u32x4 bop = *reinterpret_cast<const u32x4*>(xb + j * kPfXStep + (wm * 64 + f * 16 + fr) * kPfXStride +
-                                                            fg * 16);
-#pragma unroll
-          for (int u = 0; u < 2; ++u) acc[u][f] = MfmaP<T>::run(cur.a[j][u], bop, acc[u][f]);
-        }
-      }
-    }
+    pf_mfma_stage<T>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
-      x_store(xst, xs[buf ^ 1]);
+      slab_store(ws, abuf[cur ^ 1]);
+      slab_store(xs, bbuf[cur ^ 1]);
       __syncthreads();
-      buf ^= 1;
     }
   }
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int64_t nb = n0 + 16 * u + 4 * fg;
-#pragma unroll
-    for (int f = 0; f < 4; ++f) {
-      const int64_t m = m0 + wm * 64 + f * 16 + fr;
-      if (m < M) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (nb + i < N) Y[m * N + nb + i] = T::from_f32(acc[u][f][i]);
-      }
-    }
-  }
+  pf_store<T>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+}
+
+// Raise a kernel's dynamic LDS limit (above the 64 KB default) once.
+template <class F>
+hipError_t pf_allow_lds(F* kernel) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             kPfLds);
 }
 
 template <class T>
 hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
   if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
+  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T>);
+  if (attr != hipSuccess) return attr;
   const dim3 grid((unsigned)((Wc.rows + kPfBN - 1) / kPfBN), (unsigned)((M + kPfBM - 1) / kPfBM)),
       block(kPfThreads);
-  hipLaunchKernelGGL((k_sparse_prefill<T>), grid, block, 0, s, static_cast<const uint16_t*>(X), M, Wc.cols,
+  hipLaunchKernelGGL((k_sparse_prefill<T>), grid, block, kPfLds, s, static_cast<const uint16_t*>(X), M, Wc.cols,
                      Wc.bitmask, static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows,
                      static_cast<uint16_t*>(Y));
   return hipGetLastError();
@@ -318,8 +333,10 @@ hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void
 
 template <class T>
 hipError_t dense_prefill_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T>);
+  if (attr != hipSuccess) return attr;
   const dim3 grid((unsigned)((N + kPfBN - 1) / kPfBN), (unsigned)((M + kPfBM - 1) / kPfBM)), block(kPfThreads);
-  hipLaunchKernelGGL((k_dense_prefill<T>), grid, block, 0, s, static_cast<const uint16_t*>(X), M, K,
+  hipLaunchKernelGGL((k_dense_prefill<T>), grid, block, kPfLds, s, static_cast<const uint16_t*>(X), M, K,
                      static_cast<const uint16_t*>(W), N, static_cast<uint16_t*>(Y));
   return hipGetLastError();
 }
