@@ -4,8 +4,9 @@
 // 128 (n) x 128 (m) block of Y = X W^T; wave (wn, wm) owns 64 x 64 of it,
 // 4 x 4 v_mfma_f32_16x16x32 fragments per 32-column k-step.  K advances 64
 // columns per stage through two LDS buffers per operand: 128 rows of 64
-// elements, padded to 144 bytes so that the 16-byte fragment reads of eight
-// consecutive rows fall in distinct banks.  The next stage's global loads are
+// elements (128 bytes), the 16-byte chunk c of row r stored at chunk
+// c ^ (r % 8), so that eight consecutive rows' fragment reads (and the
+// staging writes of one row) fall in distinct banks.  The next stage's global loads are
 // in flight while the current stage is multiplied, and one barrier per stage
 // hands the buffers over.
 //
@@ -26,7 +27,7 @@ constexpr int kPfThreads = 256;
 constexpr int kPfBN = 128;                       // W rows (n) per workgroup
 constexpr int kPfBM = 128;                       // X rows (m) per workgroup
 constexpr int kPfBK = 64;                        // k columns per stage: two 32-column tile steps
-constexpr int kPfRow = kPfBK * 2 + 16;           // bytes per staged row (padded)
+constexpr int kPfRow = kPfBK * 2;                // bytes per staged row (8 chunks of 16 bytes, swizzled)
 constexpr int kPfBuf = 128 * kPfRow;             // bytes of one operand buffer
 constexpr int kPfLds = 4 * kPfBuf;               // A and B, two buffers each
 constexpr int kPfPieces = 128 * kPfBK / 8 / kPfThreads;   // 16-byte pieces per thread per operand per stage
@@ -97,8 +98,12 @@ struct SlabSrc {
   }
 };
 
+// Byte offset of 16-byte chunk c (0..7) of staged row r.
+__device__ __forceinline__ uint32_t pf_chunk(int r, int c) { return (uint32_t)(r * kPfRow + 16 * (c ^ (r & 7))); }
+
 __device__ __forceinline__ void slab_store(const Slab& sl, uint32_t buf) {
-  const uint32_t base = buf + (threadIdx.x >> 3) * kPfRow + 16 * (threadIdx.x & 7);
+  // rows t/8 + 32i share their row % 8 with row t/8
+  const uint32_t base = buf + pf_chunk(threadIdx.x >> 3, threadIdx.x & 7);
 #pragma unroll
   for (int i = 0; i < kPfPieces; ++i)
     *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(base + 32 * kPfRow * i)) = sl.v[i];
@@ -109,15 +114,16 @@ __device__ __forceinline__ void slab_store(const Slab& sl, uint32_t buf) {
 template <class T>
 __device__ __forceinline__ void pf_mfma_stage(f32x4 (&acc)[4][4], uint32_t abuf, uint32_t bbuf, int wn, int wm, int fr,
                                               int fg) {
-  const uint32_t a0 = abuf + (wn * 64 + fr) * kPfRow + 16 * fg;
-  const uint32_t b0 = bbuf + (wm * 64 + fr) * kPfRow + 16 * fg;
+  // fragment rows differ by multiples of 16, so every row a lane reads has row % 8 == fr % 8
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
+    const uint32_t a0 = abuf + pf_chunk(wn * 64 + fr, 4 * ks + fg);
+    const uint32_t b0 = bbuf + pf_chunk(wm * 64 + fr, 4 * ks + fg);
     u32x4 a[4], b[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = lds_load16(a0 + 16 * kPfRow * i + 64 * ks);
+    for (int i = 0; i < 4; ++i) a[i] = lds_load16(a0 + 16 * kPfRow * i);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = lds_load16(b0 + 16 * kPfRow * j + 64 * ks);
+    for (int j = 0; j < 4; ++j) b[j] = lds_load16(b0 + 16 * kPfRow * j);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -222,7 +228,7 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
       a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.y);
       a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.x);
       a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.y);
-      const uint32_t at = buf + (16 * (2 * wave + (i >> 1)) + fr) * kPfRow + 64 * (i & 1) + 16 * fg;
+      const uint32_t at = buf + pf_chunk(16 * (2 * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);
       *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)at) = a;
     }
   };
