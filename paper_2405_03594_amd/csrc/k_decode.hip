@@ -6,8 +6,9 @@
 //
 //   * W is stored as 16 x 32 tiles, each with its 16 bitmask words and its
 //     dense values (one tile = one MFMA A operand).  A workgroup owns one
-//     16-row block of one matrix of the group; its 16 waves split the block's
-//     k-steps (tiles) into contiguous ranges;
+//     16-row block of one matrix of the group; its waves (8, or 16 when the
+//     grid has fewer than two row blocks per CU) split the block's k-steps
+//     (tiles) into contiguous ranges;
 //   * the values of consecutive tiles are contiguous, so a wave fetches a
 //     chunk of tiles (as many as fit a 3 KB buffer, at most 8) with aligned,
 //     coalesced 16-byte loads and stages them in LDS; the chunk's bitmask
@@ -28,8 +29,9 @@
 //   * activations form the B operand (batch padded to 16 or 32 columns; the
 //     padding lanes hold zeros).  When every M x K of the group fits 32 KB the
 //     workgroup copies its X into LDS once (and the kernel is held to 64
-//     VGPRs so that two workgroups share a CU); otherwise each chunk's
-//     operands are loaded directly;
+//     VGPRs, eight waves per SIMD, so that LDS rather than registers bounds
+//     the workgroups per CU); otherwise each chunk's operands are loaded
+//     directly;
 //   * the waves' partial 16x16 results are summed in a fixed order
 //     (deterministic) and rounded once to the output type.
 //
