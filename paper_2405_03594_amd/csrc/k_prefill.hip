@@ -1,9 +1,10 @@
 // Prefill-shaped kernels (any batch M, sized for M >= 128) for gfx950.
 //
 // One GEMM core serves both kernels.  A workgroup (4 waves) computes a
-// 128 (n) x 128 (m) block of Y = X W^T; wave (wn, wm) owns 64 x 64 of it,
-// 4 x 4 v_mfma_f32_16x16x32 fragments per 32-column k-step.  K advances 64
-// columns per stage through two LDS buffers per operand: 128 rows of 64
+// BN (n) x 128 (m) block of Y = X W^T, BN = 128 (or 64 for launches that
+// would leave CUs idle); wave (wn, wm) owns BN/2 x 64 of it, BN/32 x 4
+// v_mfma_f32_16x16x32 fragments per 32-column k-step.  K advances 64
+// columns per stage through two LDS buffers per operand: rows of 64
 // elements (128 bytes), the 16-byte chunk c of row r stored at chunk
 // c ^ (r % 8), so that eight consecutive rows' fragment reads (and the
 // staging writes of one row) fall in distinct banks.  The next stage's global loads are
@@ -13,8 +14,8 @@
 //   * dense (comparator): W rows are copied into the A buffer exactly like
 //     X rows into the B buffer;
 //   * sparse (paper section 2.4.2): the A buffer is filled by expanding the
-//     stage's sixteen compressed 16 x 32 tiles (8 row blocks x 2 k-steps,
-//     four per wave), each once per workgroup: bitmask words are fetched two
+//     stage's compressed 16 x 32 tiles (BN/16 row blocks x 2 k-steps, BN/32
+//     per wave), each once per workgroup: bitmask words are fetched two
 //     stages ahead and value windows one stage ahead; a lane expands its row's
 //     8 columns with v_perm_b32 under a nibble selector table, as in the decode
 //     kernel, and writes them with one 16-byte LDS store.
@@ -24,13 +25,12 @@ namespace spl {
 namespace {
 
 constexpr int kPfThreads = 256;
-constexpr int kPfBN = 128;                       // W rows (n) per workgroup
 constexpr int kPfBM = 128;                       // X rows (m) per workgroup
 constexpr int kPfBK = 64;                        // k columns per stage: two 32-column tile steps
 constexpr int kPfRow = kPfBK * 2;                // bytes per staged row (8 chunks of 16 bytes, swizzled)
-constexpr int kPfBuf = 128 * kPfRow;             // bytes of one operand buffer
-constexpr int kPfLds = 4 * kPfBuf;               // A and B, two buffers each
-constexpr int kPfPieces = 128 * kPfBK / 8 / kPfThreads;   // 16-byte pieces per thread per operand per stage
+constexpr int kPfBBuf = kPfBM * kPfRow;          // bytes of one X (B operand) buffer
+// LDS of a BN-row workgroup: two W (A operand) buffers of BN rows, two X buffers
+constexpr int pf_lds(int BN) { return 2 * BN * kPfRow + 2 * kPfBBuf; }
 
 template <class T>
 struct MfmaP;
@@ -67,12 +67,13 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
   return sel;
 }
 
-// Rows [r0, r0 + 128) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
-// moved through registers: thread t holds rows r0 + t/8 + 32i (i < 4), columns
+// Rows [r0, r0 + 32P) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
+// moved through registers: thread t holds rows r0 + t/8 + 32i (i < P), columns
 // k0 + 8 (t % 8) .. +8; rows past R and columns past K read as zeros
 // (K % 8 == 0, so a 16-byte piece is wholly inside or outside).
+template <int P>
 struct Slab {
-  u32x4 v[kPfPieces];
+  u32x4 v[P];
 };
 
 struct SlabSrc {
@@ -88,10 +89,11 @@ struct SlabSrc {
     row0 = A + (r < R ? r : 0) * K + col;
     stride = 32 * K;
   }
-  __device__ __forceinline__ void fetch(Slab& sl, int64_t K, int64_t k0) const {
+  template <int P>
+  __device__ __forceinline__ void fetch(Slab<P>& sl, int64_t K, int64_t k0) const {
     const bool kok = k0 + col < K;
 #pragma unroll
-    for (int i = 0; i < kPfPieces; ++i) {
+    for (int i = 0; i < P; ++i) {
       sl.v[i] = u32x4{0u, 0u, 0u, 0u};
       if (kok && 32 * i < rows_left) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
     }
@@ -101,47 +103,48 @@ struct SlabSrc {
 // Byte offset of 16-byte chunk c (0..7) of staged row r.
 __device__ __forceinline__ uint32_t pf_chunk(int r, int c) { return (uint32_t)(r * kPfRow + 16 * (c ^ (r & 7))); }
 
-__device__ __forceinline__ void slab_store(const Slab& sl, uint32_t buf) {
+template <int P>
+__device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf) {
   // rows t/8 + 32i share their row % 8 with row t/8
   const uint32_t base = buf + pf_chunk(threadIdx.x >> 3, threadIdx.x & 7);
 #pragma unroll
-  for (int i = 0; i < kPfPieces; ++i)
+  for (int i = 0; i < P; ++i)
     *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(base + 32 * kPfRow * i)) = sl.v[i];
 }
 
-// One stage of MFMA work: wave (wn, wm) multiplies its 64 x 64 block over the
-// stage's two k-steps from the A (W) and B (X) buffers.
-template <class T>
-__device__ __forceinline__ void pf_mfma_stage(f32x4 (&acc)[4][4], uint32_t abuf, uint32_t bbuf, int wn, int wm, int fr,
-                                              int fg) {
+// One stage of MFMA work: wave (wn, wm) multiplies its 16 FN x 64 block over
+// the stage's two k-steps from the A (W) and B (X) buffers.
+template <class T, int FN>
+__device__ __forceinline__ void pf_mfma_stage(f32x4 (&acc)[FN][4], uint32_t abuf, uint32_t bbuf, int wn, int wm,
+                                              int fr, int fg) {
   // fragment rows differ by multiples of 16, so every row a lane reads has row % 8 == fr % 8
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
-    const uint32_t a0 = abuf + pf_chunk(wn * 64 + fr, 4 * ks + fg);
+    const uint32_t a0 = abuf + pf_chunk(wn * 16 * FN + fr, 4 * ks + fg);
     const uint32_t b0 = bbuf + pf_chunk(wm * 64 + fr, 4 * ks + fg);
-    u32x4 a[4], b[4];
+    u32x4 a[FN], b[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = lds_load16(a0 + 16 * kPfRow * i);
+    for (int i = 0; i < FN; ++i) a[i] = lds_load16(a0 + 16 * kPfRow * i);
 #pragma unroll
     for (int j = 0; j < 4; ++j) b[j] = lds_load16(b0 + 16 * kPfRow * j);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < FN; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = MfmaP<T>::run(a[i], b[j], acc[i][j]);
   }
 }
 
 // D layout: lane l, register r -> row (n) 4 (l / 16) + r, column (m) l % 16.
-template <class T>
-__device__ __forceinline__ void pf_store(const f32x4 (&acc)[4][4], uint16_t* __restrict__ Y, int64_t M, int64_t N,
+template <class T, int FN>
+__device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][4], uint16_t* __restrict__ Y, int64_t M, int64_t N,
                                          int64_t n0, int64_t m0, int wn, int wm, int fr, int fg) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int64_t m = m0 + wm * 64 + 16 * j + fr;
     if (m >= M) continue;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t n = n0 + wn * 64 + 16 * i + 4 * fg;
+    for (int i = 0; i < FN; ++i) {
+      const int64_t n = n0 + wn * 16 * FN + 16 * i + 4 * fg;
       uint16_t* y = Y + m * N + n;
       if (n + 3 < N && (N & 3) == 0) {
         u32x2 p;
@@ -157,18 +160,21 @@ __device__ __forceinline__ void pf_store(const f32x4 (&acc)[4][4], uint16_t* __r
   }
 }
 
-// Compressed operands of a wave's four tiles of one stage: tile i is row block
-// 2 wave + i / 2 of the workgroup's eight, k-step i % 2 of the stage.
+// Compressed operands of a wave's TW = BN/32 tiles of one stage: tile i is
+// row block (TW/2) wave + i/2 of the workgroup's BN/16, k-step i % 2 of the
+// stage.
+template <int TW>
 struct TileWords {
-  uint32_t w[4];        // bitmask word of row fr
-  int32_t off[4];       // tile offset (index of the tile's first value)
+  uint32_t w[TW];         // bitmask word of row fr
+  int32_t off[TW];        // tile offset (index of the tile's first value)
 };
+template <int TW>
 struct TileWindows {
-  uint32_t byte[4];     // this lane's 8 columns of row fr
-  u32x2 v0[4], v1[4];   // 8-byte windows from the first value of each nibble
+  uint32_t byte[TW];      // this lane's 8 columns of row fr
+  u32x2 v0[TW], v1[TW];   // 8-byte windows from the first value of each nibble
 };
 
-template <class T>
+template <class T, int BN>
 __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
                                                                   const uint32_t* __restrict__ bm_tiles,
                                                                   const uint16_t* __restrict__ values,
@@ -183,20 +189,21 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
   const int S = (int)tile_steps(K);
   const int nst = (S + 1) / 2;
   const int64_t B = tile_blocks(N);
-  const int64_t n0 = (int64_t)blockIdx.x * kPfBN;
+  constexpr int FN = BN / 32, TW = BN / 32;          // n-fragments per wave, tiles per wave per stage
+  const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * kPfBM;
   const int64_t nb0 = n0 / 16;
-  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + kPfBuf)};
-  const uint32_t bbuf[2] = {lds_off(dsm + 2 * kPfBuf), lds_off(dsm + 3 * kPfBuf)};
+  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + 2 * BN * kPfRow + kPfBBuf)};
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t lowmask = (1u << (8 * fg)) - 1u;
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
   if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{pf_nibble_selector(threadIdx.x, 0), pf_nibble_selector(threadIdx.x, 1)};
 
-  auto fetch_words = [&](TileWords& tw, int st) {
+  auto fetch_words = [&](TileWords<TW>& tw, int st) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t b = nb0 + 2 * wave + (i >> 1);
+    for (int i = 0; i < TW; ++i) {
+      const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);
       const int s = 2 * st + (i & 1);
       const bool ok = b < B && s < S;
       const int64_t t = ok ? b * S + s : 0;
@@ -204,9 +211,9 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
       tw.off[i] = tile_offsets[t];
     }
   };
-  auto fetch_windows = [&](TileWindows& tv, const TileWords& tw) {
+  auto fetch_windows = [&](TileWindows<TW>& tv, const TileWords<TW>& tw) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < TW; ++i) {
       const uint32_t w = tw.w[i];
       const uint32_t pc = __popc(w);
       const uint32_t above = row16_inclusive_scan(pc) - pc;          // kept values of the rows above mine
@@ -218,9 +225,9 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
       __builtin_memcpy(&tv.v1[i], vbytes + 2u * ob, 8);
     }
   };
-  auto expand_store = [&](const TileWindows& tv, uint32_t buf) {
+  auto expand_store = [&](const TileWindows<TW>& tv, uint32_t buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < TW; ++i) {
       const u32x2 slo = lds_load8(lut_addr + 8u * (tv.byte[i] & 0xfu));
       const u32x2 shi = lds_load8(lut_addr + 8u * (tv.byte[i] >> 4));
       u32x4 a;
@@ -228,21 +235,21 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
       a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.y);
       a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.x);
       a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.y);
-      const uint32_t at = buf + pf_chunk(16 * (2 * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);
+      const uint32_t at = buf + pf_chunk(16 * ((TW / 2) * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);
       *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)at) = a;
     }
   };
 
-  f32x4 acc[4][4];
+  f32x4 acc[FN][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FN; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const SlabSrc xsrc(X, M, K, m0);
-  Slab xs;
-  TileWords tw;
-  TileWindows tv;
+  Slab<kPfBM / 32> xs;
+  TileWords<TW> tw;
+  TileWindows<TW> tv;
   fetch_words(tw, 0);
   xsrc.fetch(xs, K, 0);
   fetch_windows(tv, tw);
@@ -261,17 +268,17 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
       xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
       if (st + 2 < nst) fetch_words(tw, st + 2);
     }
-    pf_mfma_stage<T>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
+    pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
       expand_store(tv, abuf[cur ^ 1]);
       slab_store(xs, bbuf[cur ^ 1]);
       __syncthreads();
     }
   }
-  pf_store<T>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+  pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
-template <class T>
+template <class T, int BN>
 __global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
                                                                  const uint16_t* __restrict__ W, int64_t N,
                                                                  uint16_t* __restrict__ Y) {
@@ -282,19 +289,21 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t*
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
   const int nst = (S + 1) / 2;
-  const int64_t n0 = (int64_t)blockIdx.x * kPfBN;
+  constexpr int FN = BN / 32;                         // n-fragments per wave
+  const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * kPfBM;
-  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + kPfBuf)};
-  const uint32_t bbuf[2] = {lds_off(dsm + 2 * kPfBuf), lds_off(dsm + 3 * kPfBuf)};
+  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + 2 * BN * kPfRow + kPfBBuf)};
 
-  f32x4 acc[4][4];
+  f32x4 acc[FN][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FN; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const SlabSrc xsrc(X, M, K, m0), wsrc(W, N, K, n0);
-  Slab xs, ws;
+  Slab<kPfBM / 32> xs;
+  Slab<BN / 32> ws;
   xsrc.fetch(xs, K, 0);
   wsrc.fetch(ws, K, 0);
   slab_store(ws, abuf[0]);
@@ -307,44 +316,64 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t*
       xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
       wsrc.fetch(ws, K, (int64_t)kPfBK * (st + 1));
     }
-    pf_mfma_stage<T>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
+    pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
       slab_store(ws, abuf[cur ^ 1]);
       slab_store(xs, bbuf[cur ^ 1]);
       __syncthreads();
     }
   }
-  pf_store<T>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+  pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
 // Raise a kernel's dynamic LDS limit (above the 64 KB default) once.
 template <class F>
-hipError_t pf_allow_lds(F* kernel) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                             kPfLds);
+hipError_t pf_allow_lds(F* kernel, int bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
-template <class T>
-hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
-  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T>);
+// 64-row blocks when 128-row blocks would give fewer workgroups than two per CU.
+bool pf_small_grid(int64_t N, int64_t M) {
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                 hipSuccess)
+      return 256;
+    return n;
+  }();
+  return ((N + 127) / 128) * ((M + kPfBM - 1) / kPfBM) < 2 * (int64_t)cus;
+}
+
+template <class T, int BN>
+hipError_t sparse_prefill_bn(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T, BN>, pf_lds(BN));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((Wc.rows + kPfBN - 1) / kPfBN), (unsigned)((M + kPfBM - 1) / kPfBM)),
-      block(kPfThreads);
-  hipLaunchKernelGGL((k_sparse_prefill<T>), grid, block, kPfLds, s, static_cast<const uint16_t*>(X), M, Wc.cols,
-                     Wc.bitmask, static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows,
+  const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + kPfBM - 1) / kPfBM)), block(kPfThreads);
+  hipLaunchKernelGGL((k_sparse_prefill<T, BN>), grid, block, pf_lds(BN), s, static_cast<const uint16_t*>(X), M,
+                     Wc.cols, Wc.bitmask, static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows,
                      static_cast<uint16_t*>(Y));
   return hipGetLastError();
 }
 
 template <class T>
-hipError_t dense_prefill_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T>);
+hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+  if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
+  return pf_small_grid(Wc.rows, M) ? sparse_prefill_bn<T, 64>(X, M, Wc, Y, s) : sparse_prefill_bn<T, 128>(X, M, Wc, Y, s);
+}
+
+template <class T, int BN>
+hipError_t dense_prefill_bn(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T, BN>, pf_lds(BN));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((N + kPfBN - 1) / kPfBN), (unsigned)((M + kPfBM - 1) / kPfBM)), block(kPfThreads);
-  hipLaunchKernelGGL((k_dense_prefill<T>), grid, block, kPfLds, s, static_cast<const uint16_t*>(X), M, K,
+  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + kPfBM - 1) / kPfBM)), block(kPfThreads);
+  hipLaunchKernelGGL((k_dense_prefill<T, BN>), grid, block, pf_lds(BN), s, static_cast<const uint16_t*>(X), M, K,
                      static_cast<const uint16_t*>(W), N, static_cast<uint16_t*>(Y));
   return hipGetLastError();
+}
+
+template <class T>
+hipError_t dense_prefill_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
+  return pf_small_grid(N, M) ? dense_prefill_bn<T, 64>(X, M, W, N, K, Y, s) : dense_prefill_bn<T, 128>(X, M, W, N, K, Y, s);
 }
 
 }  // namespace

@@ -2,8 +2,9 @@
 GPU vs the oracle.
 
 Tolerance (fp16/bf16 outputs): |y - y64| <= max(2e-2, 1e-2 |y64|) per element.
-Small shapes span several 64 x 128 output blocks with ragged edges in N, M
-and K and are compared in full; the full Llama-2-7B shapes at the batch sizes
+Small shapes span several output blocks (64 x 128 for launches that would
+leave CUs idle, 128 x 128 otherwise) with ragged edges in N, M and K and are
+compared in full; the full Llama-2-7B shapes at the batch sizes
 of the prefill workloads (M = 512, 2048) are compared on sampled outputs that
 the oracle computes one by one."""
 import numpy as np
@@ -149,3 +150,20 @@ def test_dense_prefill_llama_sampled(orc, spl):
     ms, ns = _sample(np.random.default_rng(5), M, N, 3000)
     ref = orc.linear_f64_pairs(X, orc.pack(W, "bf16", mask), ms, ns)   # all-ones mask: the dense product
     assert_close(from_dev_f64(Y)[ms, ns], ref, "dense prefill gate M=512")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_prefill_large_grid_ragged(orc, spl, dtype):
+    """A grid of at least two 128-row blocks per CU (the 128 x 128 tiling) with
+    ragged N, M and an odd number of 32-column steps, compared in full, sparse
+    and dense."""
+    N, K, M, s = 2000, 72, 4100, 0.7          # 16 x 33 = 528 workgroups of 128 x 128
+    W, mask = synth.weight(930, N, K, dtype, s)
+    X = synth.activations(931, M, K, dtype)
+    ref = orc.linear_f64(X, orc.pack(W, dtype, mask))
+    Xd = to_dev(X, dtype)
+    Y = spl.sparse_linear(Xd, _pack(spl, W, mask, dtype), algo="prefill")
+    assert_close(from_dev_f64(Y), ref, f"prefill {dtype} N={N} K={K} M={M}")
+    Wm = np.where(mask.astype(bool), W, np.zeros_like(W))
+    Yd = spl.dense_linear(Xd, to_dev(Wm, dtype), algo="prefill")
+    assert_close(from_dev_f64(Yd), ref, f"dense prefill {dtype} N={N} K={K} M={M}")
