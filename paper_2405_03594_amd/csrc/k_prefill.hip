@@ -1,9 +1,10 @@
 // Prefill-shaped kernels (any batch M, sized for M >= 128) for gfx950.
 //
-// One GEMM core serves both kernels.  A workgroup (4 waves) computes a
-// BN (n) x 128 (m) block of Y = X W^T, BN = 128 (or 64 for launches that
-// would leave CUs idle); wave (wn, wm) owns BN/2 x 64 of it, BN/32 x 4
-// v_mfma_f32_16x16x32 fragments per 32-column k-step.  K advances 64
+// One GEMM core serves both kernels.  A workgroup of NW waves computes a
+// BN (n) x BM (m) block of Y = X W^T: 128 x 256 with 8 waves for large grids,
+// 64 x 128 with 4 waves for launches that would leave CUs idle; wave
+// (wn, wm) owns BN/2 x 64 of it, BN/32 x 4 v_mfma_f32_16x16x32 fragments per
+// 32-column k-step.  K advances 64
 // columns per stage through two LDS buffers per operand: rows of 64
 // elements (128 bytes), the 16-byte chunk c of row r stored at chunk
 // c ^ (r % 8), so that eight consecutive rows' fragment reads (and the
@@ -14,8 +15,8 @@
 //   * dense (comparator): W rows are copied into the A buffer exactly like
 //     X rows into the B buffer;
 //   * sparse (paper section 2.4.2): the A buffer is filled by expanding the
-//     stage's compressed 16 x 32 tiles (BN/16 row blocks x 2 k-steps, BN/32
-//     per wave), each once per workgroup: bitmask words are fetched two
+//     stage's compressed 16 x 32 tiles (BN/16 row blocks x 2 k-steps, shared
+//     out over the waves), each once per workgroup: bitmask words are fetched two
 //     stages ahead and value windows one stage ahead; a lane expands its row's
 //     8 columns with v_perm_b32 under a nibble selector table, as in the decode
 //     kernel, and writes them with one 16-byte LDS store.
@@ -24,13 +25,10 @@
 namespace spl {
 namespace {
 
-constexpr int kPfThreads = 256;
-constexpr int kPfBM = 128;                       // X rows (m) per workgroup
 constexpr int kPfBK = 64;                        // k columns per stage: two 32-column tile steps
 constexpr int kPfRow = kPfBK * 2;                // bytes per staged row (8 chunks of 16 bytes, swizzled)
-constexpr int kPfBBuf = kPfBM * kPfRow;          // bytes of one X (B operand) buffer
-// LDS of a BN-row workgroup: two W (A operand) buffers of BN rows, two X buffers
-constexpr int pf_lds(int BN) { return 2 * BN * kPfRow + 2 * kPfBBuf; }
+// LDS of a BN x BM workgroup: two W (A operand) buffers of BN rows, two X (B operand) buffers of BM rows
+constexpr int pf_lds(int BN, int BM) { return 2 * (BN + BM) * kPfRow; }
 
 template <class T>
 struct MfmaP;
@@ -67,18 +65,20 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
   return sel;
 }
 
-// Rows [r0, r0 + 32P) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
-// moved through registers: thread t holds rows r0 + t/8 + 32i (i < P), columns
-// k0 + 8 (t % 8) .. +8; rows past R and columns past K read as zeros
-// (K % 8 == 0, so a 16-byte piece is wholly inside or outside).
+// Rows [r0, r0 + RR P) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
+// moved through registers by a workgroup of 8 RR threads: thread t holds rows
+// r0 + t/8 + RR i (i < P), columns k0 + 8 (t % 8) .. +8; rows past R and
+// columns past K read as zeros (K % 8 == 0, so a 16-byte piece is wholly
+// inside or outside).
 template <int P>
 struct Slab {
   u32x4 v[P];
 };
 
+template <int RR>
 struct SlabSrc {
   const uint16_t* row0;   // this thread's first row at column 8 (t % 8)
-  int64_t stride;         // elements between its rows (32 K)
+  int64_t stride;         // elements between its rows (RR K)
   int rows_left;          // rows of the matrix from its first row on
   int col;                // its column offset 8 (t % 8)
 
@@ -87,7 +87,7 @@ struct SlabSrc {
     col = 8 * (threadIdx.x & 7);
     rows_left = r < R ? (int)(R - r) : 0;
     row0 = A + (r < R ? r : 0) * K + col;
-    stride = 32 * K;
+    stride = RR * K;
   }
   template <int P>
   __device__ __forceinline__ void fetch(Slab<P>& sl, int64_t K, int64_t k0) const {
@@ -95,7 +95,7 @@ struct SlabSrc {
 #pragma unroll
     for (int i = 0; i < P; ++i) {
       sl.v[i] = u32x4{0u, 0u, 0u, 0u};
-      if (kok && 32 * i < rows_left) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
+      if (kok && RR * i < rows_left) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
     }
   }
 };
@@ -103,13 +103,13 @@ struct SlabSrc {
 // Byte offset of 16-byte chunk c (0..7) of staged row r.
 __device__ __forceinline__ uint32_t pf_chunk(int r, int c) { return (uint32_t)(r * kPfRow + 16 * (c ^ (r & 7))); }
 
-template <int P>
+template <int RR, int P>
 __device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf) {
-  // rows t/8 + 32i share their row % 8 with row t/8
+  // rows t/8 + RR i share their row % 8 with row t/8 (RR is a multiple of 8)
   const uint32_t base = buf + pf_chunk(threadIdx.x >> 3, threadIdx.x & 7);
 #pragma unroll
   for (int i = 0; i < P; ++i)
-    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(base + 32 * kPfRow * i)) = sl.v[i];
+    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(base + RR * kPfRow * i)) = sl.v[i];
 }
 
 // One stage of MFMA work: wave (wn, wm) multiplies its 16 FN x 64 block over
@@ -160,9 +160,8 @@ __device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][4], uint16_t* __
   }
 }
 
-// Compressed operands of a wave's TW = BN/32 tiles of one stage: tile i is
-// row block (TW/2) wave + i/2 of the workgroup's BN/16, k-step i % 2 of the
-// stage.
+// Compressed operands of a wave's TW tiles of one stage: tile i is row block
+// (TW/2) wave + i/2 of the workgroup's BN/16, k-step i % 2 of the stage.
 template <int TW>
 struct TileWords {
   uint32_t w[TW];         // bitmask word of row fr
@@ -174,8 +173,8 @@ struct TileWindows {
   u32x2 v0[TW], v1[TW];   // 8-byte windows from the first value of each nibble
 };
 
-template <class T, int BN>
-__global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
+template <class T, int BN, int BM, int NW>
+__global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
                                                                   const uint32_t* __restrict__ bm_tiles,
                                                                   const uint16_t* __restrict__ values,
                                                                   const int32_t* __restrict__ tile_offsets, int64_t N,
@@ -189,12 +188,15 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
   const int S = (int)tile_steps(K);
   const int nst = (S + 1) / 2;
   const int64_t B = tile_blocks(N);
-  constexpr int FN = BN / 32, TW = BN / 32;          // n-fragments per wave, tiles per wave per stage
+  constexpr int FN = BN / 32;                        // n-fragments per wave
+  constexpr int TW = BN / 8 / NW;                    // tiles per wave per stage (whole k-step pairs)
+  constexpr int RR = 8 * NW;                         // rows per staging round
+  static_assert(BM == 32 * NW && TW % 2 == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
-  const int64_t m0 = (int64_t)blockIdx.y * kPfBM;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
   const int64_t nb0 = n0 / 16;
   const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
-  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + 2 * BN * kPfRow + kPfBBuf)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + (2 * BN + BM) * kPfRow)};
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t lowmask = (1u << (8 * fg)) - 1u;
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
@@ -246,8 +248,8 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const SlabSrc xsrc(X, M, K, m0);
-  Slab<kPfBM / 32> xs;
+  const SlabSrc<RR> xsrc(X, M, K, m0);
+  Slab<BM / RR> xs;
   TileWords<TW> tw;
   TileWindows<TW> tv;
   fetch_words(tw, 0);
@@ -256,7 +258,7 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
   if (nst > 1) fetch_words(tw, 1);
   __syncthreads();                                     // the selector table
   expand_store(tv, abuf[0]);
-  slab_store(xs, bbuf[0]);
+  slab_store<RR>(xs, bbuf[0]);
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int cur = st & 1;
@@ -271,15 +273,15 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_sparse_prefill(const uint16_t
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
       expand_store(tv, abuf[cur ^ 1]);
-      slab_store(xs, bbuf[cur ^ 1]);
+      slab_store<RR>(xs, bbuf[cur ^ 1]);
       __syncthreads();
     }
   }
   pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
-template <class T, int BN>
-__global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
+template <class T, int BN, int BM, int NW>
+__global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
                                                                  const uint16_t* __restrict__ W, int64_t N,
                                                                  uint16_t* __restrict__ Y) {
   extern __shared__ __align__(16) unsigned char dsm[];
@@ -290,10 +292,12 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t*
   const int S = (int)tile_steps(K);
   const int nst = (S + 1) / 2;
   constexpr int FN = BN / 32;                         // n-fragments per wave
+  constexpr int RR = 8 * NW;                          // rows per staging round
+  static_assert(BM == 32 * NW && BN % RR == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
-  const int64_t m0 = (int64_t)blockIdx.y * kPfBM;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
   const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
-  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + 2 * BN * kPfRow + kPfBBuf)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + (2 * BN + BM) * kPfRow)};
 
   f32x4 acc[FN][4];
 #pragma unroll
@@ -301,13 +305,13 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t*
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const SlabSrc xsrc(X, M, K, m0), wsrc(W, N, K, n0);
-  Slab<kPfBM / 32> xs;
-  Slab<BN / 32> ws;
+  const SlabSrc<RR> xsrc(X, M, K, m0), wsrc(W, N, K, n0);
+  Slab<BM / RR> xs;
+  Slab<BN / RR> ws;
   xsrc.fetch(xs, K, 0);
   wsrc.fetch(ws, K, 0);
-  slab_store(ws, abuf[0]);
-  slab_store(xs, bbuf[0]);
+  slab_store<RR>(ws, abuf[0]);
+  slab_store<RR>(xs, bbuf[0]);
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int cur = st & 1;
@@ -318,8 +322,8 @@ __global__ void __launch_bounds__(kPfThreads, 2) k_dense_prefill(const uint16_t*
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
-      slab_store(ws, abuf[cur ^ 1]);
-      slab_store(xs, bbuf[cur ^ 1]);
+      slab_store<RR>(ws, abuf[cur ^ 1]);
+      slab_store<RR>(xs, bbuf[cur ^ 1]);
       __syncthreads();
     }
   }
@@ -332,8 +336,9 @@ hipError_t pf_allow_lds(F* kernel, int bytes) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
-// 64-row blocks when 128-row blocks would give fewer workgroups than two per CU.
-bool pf_small_grid(int64_t N, int64_t M) {
+// Workgroup tile of a launch: 128 x 256 (8 waves) when that still gives every
+// CU a workgroup, else 64 x 128 (4 waves, four times as many workgroups).
+bool pf_large_tile(int64_t N, int64_t M) {
   static const int cus = [] {
     int dev = 0, n = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
@@ -341,39 +346,42 @@ bool pf_small_grid(int64_t N, int64_t M) {
       return 256;
     return n;
   }();
-  return ((N + 127) / 128) * ((M + kPfBM - 1) / kPfBM) < 2 * (int64_t)cus;
+  return ((N + 127) / 128) * ((M + 255) / 256) >= (int64_t)cus;
 }
 
-template <class T, int BN>
-hipError_t sparse_prefill_bn(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T, BN>, pf_lds(BN));
+template <class T, int BN, int BM, int NW>
+hipError_t sparse_prefill_tile(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T, BN, BM, NW>, pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + kPfBM - 1) / kPfBM)), block(kPfThreads);
-  hipLaunchKernelGGL((k_sparse_prefill<T, BN>), grid, block, pf_lds(BN), s, static_cast<const uint16_t*>(X), M,
-                     Wc.cols, Wc.bitmask, static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows,
-                     static_cast<uint16_t*>(Y));
+  const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW);
+  hipLaunchKernelGGL((k_sparse_prefill<T, BN, BM, NW>), grid, block, pf_lds(BN, BM), s,
+                     static_cast<const uint16_t*>(X), M, Wc.cols, Wc.bitmask, static_cast<const uint16_t*>(Wc.values),
+                     Wc.tile_offsets, Wc.rows, static_cast<uint16_t*>(Y));
   return hipGetLastError();
 }
 
 template <class T>
 hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
   if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
-  return pf_small_grid(Wc.rows, M) ? sparse_prefill_bn<T, 64>(X, M, Wc, Y, s) : sparse_prefill_bn<T, 128>(X, M, Wc, Y, s);
+  return pf_large_tile(Wc.rows, M) ? sparse_prefill_tile<T, 128, 256, 8>(X, M, Wc, Y, s)
+                                    : sparse_prefill_tile<T, 64, 128, 4>(X, M, Wc, Y, s);
 }
 
-template <class T, int BN>
-hipError_t dense_prefill_bn(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T, BN>, pf_lds(BN));
+template <class T, int BN, int BM, int NW>
+hipError_t dense_prefill_tile(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T, BN, BM, NW>, pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + kPfBM - 1) / kPfBM)), block(kPfThreads);
-  hipLaunchKernelGGL((k_dense_prefill<T, BN>), grid, block, pf_lds(BN), s, static_cast<const uint16_t*>(X), M, K,
-                     static_cast<const uint16_t*>(W), N, static_cast<uint16_t*>(Y));
+  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW);
+  hipLaunchKernelGGL((k_dense_prefill<T, BN, BM, NW>), grid, block, pf_lds(BN, BM), s,
+                     static_cast<const uint16_t*>(X), M, K, static_cast<const uint16_t*>(W), N,
+                     static_cast<uint16_t*>(Y));
   return hipGetLastError();
 }
 
 template <class T>
 hipError_t dense_prefill_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  return pf_small_grid(N, M) ? dense_prefill_bn<T, 64>(X, M, W, N, K, Y, s) : dense_prefill_bn<T, 128>(X, M, W, N, K, Y, s);
+  return pf_large_tile(N, M) ? dense_prefill_tile<T, 128, 256, 8>(X, M, W, N, K, Y, s)
+                             : dense_prefill_tile<T, 64, 128, 4>(X, M, W, N, K, Y, s);
 }
 
 }  // namespace

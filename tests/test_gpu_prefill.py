@@ -3,7 +3,7 @@ GPU vs the oracle.
 
 Tolerance (fp16/bf16 outputs): |y - y64| <= max(2e-2, 1e-2 |y64|) per element.
 Small shapes span several output blocks (64 x 128 for launches that would
-leave CUs idle, 128 x 128 otherwise) with ragged edges in N, M and K and are
+leave CUs idle, 128 x 256 otherwise) with ragged edges in N, M and K and are
 compared in full; the full Llama-2-7B shapes at the batch sizes
 of the prefill workloads (M = 512, 2048) are compared on sampled outputs that
 the oracle computes one by one."""
@@ -154,10 +154,10 @@ def test_dense_prefill_llama_sampled(orc, spl):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_prefill_large_grid_ragged(orc, spl, dtype):
-    """A grid of at least two 128-row blocks per CU (the 128 x 128 tiling) with
+    """A grid of at least one 128 x 256 block per CU (the large tiling) with
     ragged N, M and an odd number of 32-column steps, compared in full, sparse
     and dense."""
-    N, K, M, s = 2000, 72, 4100, 0.7          # 16 x 33 = 528 workgroups of 128 x 128
+    N, K, M, s = 2000, 72, 4100, 0.7          # 16 x 17 = 272 workgroups of 128 x 256
     W, mask = synth.weight(930, N, K, dtype, s)
     X = synth.activations(931, M, K, dtype)
     ref = orc.linear_f64(X, orc.pack(W, dtype, mask))
