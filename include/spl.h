@@ -52,8 +52,11 @@
  *     bitmask      uint32 [B*S][16]: word r of tile t holds row 16b+r,
  *                  columns 32s..32s+31 (bit j = column 32s+j); rows >= N and
  *                  columns >= K are 0;
- *     values       each tile's kept payloads in tile order, inside a tile row
- *                  by row in ascending column order;
+ *     values       each tile's kept payloads in tile order; inside a tile by
+ *                  column group, then row, then ascending column, where a
+ *                  column group is the 16 bytes of payload one matrix-core
+ *                  lane holds (8 columns of fp16/bf16, 16 of int8: groups
+ *                  cover columns 8g..8g+7, resp. 16g..16g+15);
  *     tile_offsets int32 [B*S + 1]: index in `values` of tile t's first
  *                  payload; tile_offsets[B*S] = nnz.
  *   Both layouts hold the same payloads; spl_retile16 converts rows -> tiles.

@@ -185,10 +185,15 @@ void orc_unpack(const uint32_t* bitmask, const void* values, const int32_t* row_
  * rows 16b..16b+15 and columns 32s..32s+31.  Tiles are ordered by b, then s.
  *   bitmask_t[(b*S + s)*16 + r]: bit j set iff (16b + r, 32s + j) is kept
  *                                (0 for rows >= N and columns >= K);
- *   values_t: each tile's kept payloads, row by row, ascending column;
+ *   values_t: each tile's kept payloads, column group by column group, inside
+ *             a group row by row, inside a row ascending column.  A column
+ *             group is the 16 bytes of dense payload one matrix-core lane
+ *             holds: G = 16 / element bytes columns (8 for fp16/bf16, 16 for
+ *             int8), groups g = 0 .. 32/G - 1 covering columns G g .. G g + G - 1;
  *   tile_offsets[b*S + s]: index in values_t of the tile's first payload;
  *   tile_offsets[B*S] = nnz.   (B = ceil(N/16) row blocks, S = ceil(K/32).)
  */
+static int64_t tile_group_cols(int32_t dtype) { return 16 / elem_bytes(dtype); }
 int64_t orc_tile_blocks(int64_t N) { return (N + 15) / 16; }
 int64_t orc_tile_ksteps(int64_t K) { return (K + 31) / 32; }
 
@@ -196,23 +201,25 @@ void orc_pack_tiled(const void* W, int32_t dtype, const uint8_t* mask, int64_t N
                     uint32_t* bitmask_t, void* values_t, int32_t* tile_offsets) {
   int64_t B = orc_tile_blocks(N), S = orc_tile_ksteps(K);
   int eb = elem_bytes(dtype);
+  int64_t G = tile_group_cols(dtype);
   int64_t c = 0;
   for (int64_t b = 0; b < B; ++b) {
     for (int64_t s = 0; s < S; ++s) {
       int64_t t = b * S + s;
       tile_offsets[t] = (int32_t)c;
-      for (int64_t r = 0; r < 16; ++r) {
-        uint32_t word = 0;
-        int64_t n = 16 * b + r;
-        for (int64_t j = 0; j < 32; ++j) {
-          int64_t k = 32 * s + j;
-          if (n < N && k < K && is_kept(W, dtype, mask, n * K + k)) {
-            word |= (uint32_t)1u << j;
-            memcpy((char*)values_t + c * eb, (const char*)W + (n * K + k) * eb, (size_t)eb);
-            ++c;
+      for (int64_t r = 0; r < 16; ++r) bitmask_t[t * 16 + r] = 0;
+      for (int64_t g = 0; g < 32 / G; ++g) {
+        for (int64_t r = 0; r < 16; ++r) {
+          int64_t n = 16 * b + r;
+          for (int64_t j = G * g; j < G * g + G; ++j) {
+            int64_t k = 32 * s + j;
+            if (n < N && k < K && is_kept(W, dtype, mask, n * K + k)) {
+              bitmask_t[t * 16 + r] |= (uint32_t)1u << j;
+              memcpy((char*)values_t + c * eb, (const char*)W + (n * K + k) * eb, (size_t)eb);
+              ++c;
+            }
           }
         }
-        bitmask_t[t * 16 + r] = word;
       }
     }
   }
@@ -223,17 +230,20 @@ void orc_unpack_tiled(const uint32_t* bitmask_t, const void* values_t, const int
                       int64_t N, int64_t K, void* W_out) {
   int64_t B = orc_tile_blocks(N), S = orc_tile_ksteps(K);
   int eb = elem_bytes(dtype);
+  int64_t G = tile_group_cols(dtype);
   memset(W_out, 0, (size_t)(N * K * eb));
   for (int64_t b = 0; b < B; ++b) {
     for (int64_t s = 0; s < S; ++s) {
       int64_t t = b * S + s;
       int64_t c = tile_offsets[t];
-      for (int64_t r = 0; r < 16; ++r) {
-        for (int64_t j = 0; j < 32; ++j) {
-          if ((bitmask_t[t * 16 + r] >> j) & 1u) {
-            int64_t n = 16 * b + r, k = 32 * s + j;
-            memcpy((char*)W_out + (n * K + k) * eb, (const char*)values_t + c * eb, (size_t)eb);
-            ++c;
+      for (int64_t g = 0; g < 32 / G; ++g) {
+        for (int64_t r = 0; r < 16; ++r) {
+          for (int64_t j = G * g; j < G * g + G; ++j) {
+            if ((bitmask_t[t * 16 + r] >> j) & 1u) {
+              int64_t n = 16 * b + r, k = 32 * s + j;
+              memcpy((char*)W_out + (n * K + k) * eb, (const char*)values_t + c * eb, (size_t)eb);
+              ++c;
+            }
           }
         }
       }

@@ -18,10 +18,11 @@
 //   * each wave is software-pipelined: the next chunk's values and words are
 //     in flight while the current chunk is multiplied;
 //   * lane (fr, fg) supplies tile row fr, columns 8fg..8fg+7, exactly its A
-//     operand of v_mfma_f32_16x16x32 (8 bf16/fp16 values).  Their offset in the
-//     stored values is the tile offset + the kept count of the tile rows above
-//     (a 16-lane DPP scan of popcounts, two tiles per scan in 16-bit halves) +
-//     the popcount of the lower bits of the row's word.  Each 4-column
+//     operand of v_mfma_f32_16x16x32 (8 bf16/fp16 values).  A tile's values
+//     are stored by column group, then row, i.e. in lane order, so their
+//     offset is the tile offset + the kept count of the lanes before (a wave
+//     DPP scan of popcounts, two tiles per scan in 16-bit halves), and the
+//     lanes of a half-wave read one contiguous run of LDS.  Each 4-column
 //     nibble's values are read from LDS as an 8-byte window (aligned dword
 //     reads + v_alignbyte_b32) and a 16-entry selector table expands them
 //     with v_perm_b32 into the operand dwords (zero bytes where the bit is
@@ -300,7 +301,6 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   const uint32_t* bmb = tk.bm + blk * S * 16;         // this row block's tiles, 16 words each
   const int32_t* tob = tk.toff + blk * S;             // S + 1 entries (the next block's first = this end)
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(tk.values);
-  const uint32_t lowmask = (1u << (8 * fg)) - 1u;      // bits of the word below my byte
   uint32_t* wl = words[wave];
 
   // Offsets of the wave's tiles: lane i holds the offset of tile ob + i
@@ -409,19 +409,22 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     for (int jp = 0; jp < C; jp += 2) {
       if (jp < cur.cn) {
         const u32x2 wp = *reinterpret_cast<const u32x2*>(wl + fr * WS + jp);
-        // kept count of the rows above mine for both tiles (16-bit halves, sums <= 512)
-        const uint32_t pc = __popc(wp.x) | (__popc(wp.y) << 16);
-        const uint32_t ex = row16_inclusive_scan(pc) - pc;
+        // values stored before mine in both tiles: a tile's values are ordered by
+        // column group (my fg), then row (my fr), so this is the exclusive wave
+        // scan of the lanes' kept counts (16-bit halves, sums <= 512)
+        const uint32_t pc = __popc(__builtin_amdgcn_ubfe(wp.x, 8 * fg, 8)) |
+                            (__popc(__builtin_amdgcn_ubfe(wp.y, 8 * fg, 8)) << 16);
+        const uint32_t ex = wave_inclusive_scan(pc) - pc;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int j = jp + h;
           if (j < cur.cn) {
             const uint32_t wj = h ? wp.y : wp.x;
-            const uint32_t above = h ? ex >> 16 : ex & 0xffffu;
+            const uint32_t before = h ? ex >> 16 : ex & 0xffffu;
             const uint32_t nlo = __builtin_amdgcn_ubfe(wj, 8 * fg, 4);      // my two nibbles
             const uint32_t nhi = __builtin_amdgcn_ubfe(wj, 8 * fg + 4, 4);
             const uint32_t tile0 = (uint32_t)tc[j];
-            const uint32_t oa = __popc(wj & lowmask) + above + tile0;       // first value of each nibble
+            const uint32_t oa = before + tile0;                             // first value of each nibble
             const uint32_t ob = oa + __popc(nlo);
             // LDS byte addresses of the two 8-byte windows; their low 2 bits are the realignment
             const uint32_t pa = 2u * oa + vrel, pb = 2u * ob + vrel;

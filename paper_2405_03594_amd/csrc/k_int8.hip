@@ -14,9 +14,10 @@
 // (whole pairs, as many as fit a 3 KB buffer) with aligned 16-byte loads in
 // LDS, the tile offsets of its whole range come with one load, and the next
 // chunk is in flight while the current one is multiplied.  Each lane expands
-// its four 4-column nibbles: the nibble's values start at the tile offset +
-// the kept count of the rows above (16-lane DPP scan) + the popcount of the
-// lower bits of its row, are read as an aligned dword pair realigned with
+// its four 4-column nibbles: a tile's values are stored by 16-column group,
+// then row, i.e. in the order of the tile's 32 lanes, so the nibble's values
+// start at the tile offset + the kept count of the lanes before (a 32-lane
+// DPP scan) + the nibbles before it, are read as an aligned dword pair realigned with
 // v_alignbyte_b32, and a 16-entry selector table (conflict-free) drives
 // v_perm_b32 (paper section 2.4.1).  Activations of small batches are staged
 // in LDS once per workgroup; int32 partial sums of the waves are added in LDS
@@ -212,7 +213,6 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
   }
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr = lds_off(vbuf);
-  const uint32_t lowmask = half ? 0xffffu : 0u;
   u32x4 xs_op = u32x4{0u, 0u, 0u, 0u};
 
   i32x4 acc[MT];
@@ -262,11 +262,14 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
         const int j = 2 * q + tsel;                            // this lane's tile in the chunk
         uint32_t w = wl[fr * WS + j];
         if (j >= cur.cn) w = 0u;                               // a range ending on half a pair
-        const uint32_t pc = __popc(w);
-        const uint32_t above = row16_inclusive_scan(pc) - pc;
+        // values stored before mine in my tile: a tile's values are ordered by 16-column group (my
+        // half), then row (my fr), i.e. in the order of the tile's 32 lanes, so this is the
+        // exclusive scan of the kept counts over my half of the wave
+        const uint32_t pc = __popc(__builtin_amdgcn_ubfe(w, 16 * half, 16));
+        const uint32_t before = half_inclusive_scan(pc) - pc;
         // this lane's tile offset: the pair's first or second (arithmetic select keeps tc[] in registers)
         const uint32_t tile0 = (uint32_t)tc[2 * q] + (((uint32_t)tc[2 * q + 1] - (uint32_t)tc[2 * q]) & (0u - (uint32_t)tsel));
-        const uint32_t oa = tile0 + above + __popc(w & lowmask);
+        const uint32_t oa = tile0 + before;
         u32x4 a;
         uint32_t o = oa;
 #pragma unroll

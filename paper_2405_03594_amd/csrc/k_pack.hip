@@ -153,14 +153,30 @@ __global__ void __launch_bounds__(256) k_tile_count(const uint32_t* __restrict__
   if (t < T && r == 0) counts[t] = (int32_t)c;
 }
 
+// Position, inside tile t, of the first value of row r's column group g:
+// tile values are ordered by column group (G columns = 16 bytes of payload),
+// then row, then column, so it is the kept count of every row below group g
+// plus that of the rows above r inside group g.  `words` holds the tile's 16
+// bitmask words.
+template <int G>
+__device__ __forceinline__ uint32_t tile_group_start(const uint32_t (&words)[16], int r, int g) {
+  const uint32_t below = (1u << (G * g)) - 1u;                           // G g < 32
+  const uint32_t gm = (G == 32 ? 0xffffffffu : ((1u << G) - 1u)) << (G * g);
+  uint32_t pos = 0;
+#pragma unroll
+  for (int rr = 0; rr < 16; ++rr) pos += __popc(words[rr] & below) + (rr < r ? __popc(words[rr] & gm) : 0u);
+  return pos;
+}
+
 // One wave per row: for each 32-column word, the row's stored values move from
-// their row-layout position to their tile-layout position.
+// their row-layout position to their tile-layout position, group by group.
 template <int EB>
 __global__ void __launch_bounds__(256) k_tile_scatter(const uint32_t* __restrict__ bm_rows,
                                                       const void* __restrict__ vals_rows,
                                                       const int32_t* __restrict__ row_offsets, int64_t N, int64_t K,
                                                       const int32_t* __restrict__ tile_offsets,
                                                       void* __restrict__ vals_tiles) {
+  constexpr int G = 16 / EB;                           // columns per group
   const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (n >= N) return;
   const int lane = threadIdx.x & 63;
@@ -179,15 +195,23 @@ __global__ void __launch_bounds__(256) k_tile_scatter(const uint32_t* __restrict
     }
     const uint32_t total = __shfl(incl, kWave - 1);
     if (pc) {
+      uint32_t words[16];
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) words[rr] = 16 * b + rr < N ? bm_rows[(16 * b + rr) * S + s] : 0u;
       int64_t src = carry + (incl - pc);
-      int64_t dst = tile_offsets[b * S + s];
-      for (int rr = 0; rr < r; ++rr) dst += __popc(bm_rows[(16 * b + rr) * S + s]);
-      for (uint32_t i = 0; i < pc; ++i) {
-        if constexpr (EB == 2) {
-          static_cast<uint16_t*>(vals_tiles)[dst + i] = static_cast<const uint16_t*>(vals_rows)[src + i];
-        } else {
-          static_cast<int8_t*>(vals_tiles)[dst + i] = static_cast<const int8_t*>(vals_rows)[src + i];
+      const int64_t t0 = tile_offsets[b * S + s];
+#pragma unroll
+      for (int g = 0; g < 32 / G; ++g) {
+        const uint32_t cg = __popc(w & (((1u << G) - 1u) << (G * g)));
+        const int64_t dst = t0 + tile_group_start<G>(words, r, g);
+        for (uint32_t i = 0; i < cg; ++i) {
+          if constexpr (EB == 2) {
+            static_cast<uint16_t*>(vals_tiles)[dst + i] = static_cast<const uint16_t*>(vals_rows)[src + i];
+          } else {
+            static_cast<int8_t*>(vals_tiles)[dst + i] = static_cast<const int8_t*>(vals_rows)[src + i];
+          }
         }
+        src += cg;
       }
     }
     carry += total;
@@ -200,6 +224,7 @@ __global__ void __launch_bounds__(256) k_unpack_tiled(const uint32_t* __restrict
                                                       const void* __restrict__ values,
                                                       const int32_t* __restrict__ tile_offsets, int64_t N, int64_t K,
                                                       void* __restrict__ Wd) {
+  constexpr int G = 16 / EB;
   const int64_t S = tile_steps(K);
   const int64_t T = tile_blocks(N) * S;
   const int64_t t = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
@@ -208,19 +233,23 @@ __global__ void __launch_bounds__(256) k_unpack_tiled(const uint32_t* __restrict
   const int64_t b = t / S, s = t - b * S;
   const int64_t n = 16 * b + r;
   if (n >= N) return;
-  int64_t src = tile_offsets[t];
-  for (int rr = 0; rr < r; ++rr) src += __popc(bm_tiles[t * 16 + rr]);
-  const uint32_t w = bm_tiles[t * 16 + r];
-  for (int j = 0; j < 32; ++j) {
-    const int64_t k = 32 * s + j;
-    if (k >= K) break;
-    const bool bit = (w >> j) & 1u;
-    if constexpr (EB == 2) {
-      static_cast<uint16_t*>(Wd)[n * K + k] = bit ? static_cast<const uint16_t*>(values)[src] : (uint16_t)0;
-    } else {
-      static_cast<int8_t*>(Wd)[n * K + k] = bit ? static_cast<const int8_t*>(values)[src] : (int8_t)0;
+  uint32_t words[16];
+#pragma unroll
+  for (int rr = 0; rr < 16; ++rr) words[rr] = bm_tiles[t * 16 + rr];
+  const uint32_t w = words[r];
+  for (int g = 0; g < 32 / G; ++g) {
+    int64_t src = tile_offsets[t] + tile_group_start<G>(words, r, g);
+    for (int j = G * g; j < G * g + G; ++j) {
+      const int64_t k = 32 * s + j;
+      if (k >= K) break;
+      const bool bit = (w >> j) & 1u;
+      if constexpr (EB == 2) {
+        static_cast<uint16_t*>(Wd)[n * K + k] = bit ? static_cast<const uint16_t*>(values)[src] : (uint16_t)0;
+      } else {
+        static_cast<int8_t*>(Wd)[n * K + k] = bit ? static_cast<const int8_t*>(values)[src] : (int8_t)0;
+      }
+      src += bit;
     }
-    src += bit;
   }
 }
 

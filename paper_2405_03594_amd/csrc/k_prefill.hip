@@ -198,7 +198,6 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
   const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
   const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + (2 * BN + BM) * kPfRow)};
   const uint32_t lut_addr = lds_off(lut);
-  const uint32_t lowmask = (1u << (8 * fg)) - 1u;
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
   if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{pf_nibble_selector(threadIdx.x, 0), pf_nibble_selector(threadIdx.x, 1)};
 
@@ -217,10 +216,11 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
 #pragma unroll
     for (int i = 0; i < TW; ++i) {
       const uint32_t w = tw.w[i];
-      const uint32_t pc = __popc(w);
-      const uint32_t above = row16_inclusive_scan(pc) - pc;          // kept values of the rows above mine
-      const uint32_t oa = (uint32_t)tw.off[i] + above + __popc(w & lowmask);
       const uint32_t byte = __builtin_amdgcn_ubfe(w, 8 * fg, 8);
+      // values stored before mine: a tile's values are ordered by column group (fg), then row (fr),
+      // i.e. in lane order, so this is the exclusive wave scan of the lanes' kept counts
+      const uint32_t pc = __popc(byte);
+      const uint32_t oa = (uint32_t)tw.off[i] + wave_inclusive_scan(pc) - pc;
       const uint32_t ob = oa + __popc(byte & 0xfu);
       tv.byte[i] = byte;
       __builtin_memcpy(&tv.v0[i], vbytes + 2u * oa, 8);

@@ -69,6 +69,23 @@ __device__ __forceinline__ uint32_t row16_inclusive_scan(uint32_t x) {
   return x;
 }
 
+// Inclusive prefix sum across each half (32 lanes) of the wave: the 16-lane
+// scans, then lane 15's total added to lanes 16-31 and lane 47's to 48-63
+// (DPP row_bcast:15 into rows 1 and 3).
+__device__ __forceinline__ uint32_t half_inclusive_scan(uint32_t x) {
+  x = row16_inclusive_scan(x);
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x142, 0xa, 0xf, false);   // row_bcast:15, rows 1 and 3
+  return x;
+}
+
+// Inclusive prefix sum across the whole wave (64 lanes): the half scans, then
+// lane 31's total added to lanes 32-63 (DPP row_bcast:31 into rows 2 and 3).
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  x = half_inclusive_scan(x);
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x143, 0xc, 0xf, false);   // row_bcast:31, rows 2 and 3
+  return x;
+}
+
 typedef __attribute__((address_space(3))) unsigned char lds_t;
 
 // 32-bit LDS offset of a pointer into shared memory, and loads at such offsets.

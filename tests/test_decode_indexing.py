@@ -171,9 +171,11 @@ def test_lane_expansion_matches_dense_rows(orc, N, K, s):
                     for lane in range(64):
                         fr, fg = lane & 15, lane >> 4
                         wd = words[fr]
-                        above = sum(_popc(words[r]) for r in range(fr))
                         byte = (wd >> (8 * fg)) & 0xFF
-                        oa = to[j] + above + _popc(wd & ((1 << (8 * fg)) - 1))
+                        # values before this lane's: column groups before fg (all rows), then rows above fr in fg
+                        before = sum(_popc((words[r] >> (8 * g)) & 0xFF) for g in range(fg) for r in range(16)) + \
+                            sum(_popc((words[r] >> (8 * fg)) & 0xFF) for r in range(fr))
+                        oa = to[j] + before
                         ob = oa + _popc(byte & 0xF)
                         pa, pb = 2 * oa - a0, 2 * ob - a0
                         qa, qb = pa >> 2, pb >> 2

@@ -155,7 +155,9 @@ def test_int8_lane_expansion_matches_dense_rows(orc, N, K, s):
                         t = b * S + c0 + j
                         words = [int(bm[t * 16 + r]) if j < cn else 0 for r in range(16)]
                         w = words[fr]
-                        o = to[j] + sum(_popc(words[r]) for r in range(fr)) + _popc(w & (0xFFFF if half else 0))
+                        # values before this lane's: the 16-column group before (all rows), then rows above fr
+                        o = to[j] + sum(_popc((words[r] >> (16 * g)) & 0xFFFF) for g in range(half) for r in range(16)) + \
+                            sum(_popc((words[r] >> (16 * half)) & 0xFFFF) for r in range(fr))
                         got = []
                         for i in range(4):
                             nib = (w >> (16 * half + 4 * i)) & 15

@@ -392,11 +392,14 @@ def test_tiled_round_trip_and_invariants(orc, N, K, s):
     assert np.array_equal(t.bitmask.astype(np.uint64), words.reshape(-1))
     counts = blocks.reshape(B * S, -1).sum(axis=1)
     assert np.array_equal(np.diff(t.tile_offsets.astype(np.int64)), counts)
-    # values: tile by tile, each tile row-major (NumPy boolean indexing of the tile block)
+    # values: tile by tile; inside a tile by 8-column group, then row, then column (NumPy boolean
+    # indexing of the tile block viewed as [group][row][column in group])
     Wp = np.zeros((B * 16, S * 32), dtype=np.uint16)
     Wp[:N, :K] = W
     wb = Wp.reshape(B, 16, S, 32).transpose(0, 2, 1, 3)
-    expect = np.concatenate([wb[b, s_][blocks[b, s_]] for b in range(B) for s_ in range(S)] + [np.zeros(0, np.uint16)])
+    grouped = lambda x: x.reshape(16, 4, 8).transpose(1, 0, 2)
+    expect = np.concatenate([grouped(wb[b, s_])[grouped(blocks[b, s_])] for b in range(B) for s_ in range(S)]
+                            + [np.zeros(0, np.uint16)])
     assert np.array_equal(t.values, expect)
 
 
@@ -411,3 +414,31 @@ def test_tiled_int8(orc):
     Wq, mask, _ = synth.int8_weight(6, 40, 96, 0.7)
     t = orc.pack_tiled(Wq, "i8", mask)
     assert np.array_equal(orc.unpack_tiled(t), np.where(mask.astype(bool), Wq, np.int8(0)))
+    # int8 column groups are 16 columns wide (16 bytes, like the 8 columns of a 16-bit payload)
+    N, K = Wq.shape
+    B, S = -(-N // 16), -(-K // 32)
+    Wp = np.zeros((B * 16, S * 32), dtype=np.int8)
+    Wp[:N, :K] = Wq
+    Mp = np.zeros((B * 16, S * 32), dtype=bool)
+    Mp[:N, :K] = mask.astype(bool)
+    tiles = lambda x: x.reshape(B, 16, S, 32).transpose(0, 2, 1, 3).reshape(B * S, 16, 2, 16).transpose(0, 2, 1, 3)
+    wt, mt = tiles(Wp), tiles(Mp)
+    expect = np.concatenate([wt[i][mt[i]] for i in range(B * S)])
+    assert np.array_equal(t.values, expect)
+
+
+@pytest.mark.parametrize("dtype,G", [("bf16", 8), ("i8", 16)])
+def test_tiled_value_order_worked_example(orc, dtype, G):
+    """One 16 x 32 tile: row 0 keeps columns 0, 9 and 17, row 1 keeps 1 and 8,
+    the other rows nothing; entry (r, j) holds 100 r + j.  Column groups of G
+    columns, rows inside a group, columns inside a row."""
+    W = (100 * np.arange(16)[:, None] + np.arange(32)[None, :]).astype(np.uint16 if dtype == "bf16" else np.int16)
+    if dtype == "i8":
+        W = (W % 128).astype(np.int8)
+    mask = np.zeros((16, 32), np.uint8)
+    mask[0, [0, 9, 17]] = 1
+    mask[1, [1, 8]] = 1
+    t = orc.pack_tiled(W, dtype, mask)
+    order = [(0, 0), (1, 1), (0, 9), (1, 8), (0, 17)] if G == 8 else [(0, 0), (0, 9), (1, 1), (1, 8), (0, 17)]
+    assert [int(v) for v in t.values] == [int(W[r, j]) for r, j in order]
+    assert list(t.bitmask[:2]) == [(1 << 0) | (1 << 9) | (1 << 17), (1 << 1) | (1 << 8)]
