@@ -377,32 +377,38 @@ def run_int8(args):
     ys = {(M, j): torch.empty((M, N), dtype=torch.float16, device="cuda") for M in Ms for j, (_, N, _) in
           enumerate(shapes)}
     xs = {(M, j): (xq[j][:M].contiguous(), sx[j][:M].contiguous()) for M in Ms for j in range(len(shapes))}
-    units = [(M, j) for M in Ms for j in range(len(shapes))]
+    # grouped launches as in the decode driver: q|k|v, o, gate|up, down
+    units = [(M, grp) for M in Ms for grp in GROUPED]
 
     def sparse_fn(li, u):
-        X, s_ = xs[u]
-        Wc, _, sw = layers[li][u[1]]
-        spl.sparse_linear_int8(X, s_, Wc, sw, out=ys[u])
+        M, grp = u
+        spl.sparse_linear_int8_group([xs[(M, j)][0] for j in grp], [xs[(M, j)][1] for j in grp],
+                                     [layers[li][j][0] for j in grp], [layers[li][j][2] for j in grp],
+                                     outs=[ys[(M, j)] for j in grp])
 
     def dense_fn(li, u):
-        X, s_ = xs[u]
-        _, Wd, sw = layers[li][u[1]]
-        spl.dense_linear_int8(X, s_, Wd, sw, out=ys[u])
+        M, grp = u
+        spl.dense_linear_int8_group([xs[(M, j)][0] for j in grp], [xs[(M, j)][1] for j in grp],
+                                    [layers[li][j][1] for j in grp], [layers[li][j][2] for j in grp],
+                                    outs=[ys[(M, j)] for j in grp])
 
     sp_wall, sp_gpu = _timed(units, sparse_fn, args.steps, args.warmup, range(nl))
 
-    def nbytes(M, j):
-        N, K = shapes[j][1], shapes[j][2]
-        return layers[0][j][0].compressed_bytes() + 4 * N + M * K + 4 * M + 2 * M * N
+    def nbytes(M, grp):
+        total = 0
+        for j in grp:
+            N, K = shapes[j][1], shapes[j][2]
+            total += layers[0][j][0].compressed_bytes() + 4 * N + M * K + 4 * M + 2 * M * N
+        return total
 
-    step_bytes = sum(nbytes(M, j) for (M, j) in units)
+    step_bytes = sum(nbytes(M, grp) for (M, grp) in units)
     launch_ms = sp_gpu / len(units)
     achieved = step_bytes / len(units) / (launch_ms * 1e-3) / 1e9
     per_M = {}
     for M in Ms:
         uM = [u for u in units if u[0] == M]
         _, g = _timed(uM, sparse_fn, max(20, args.steps // 4), 3, range(nl))
-        b = sum(nbytes(M, j) for (_, j) in uM)
+        b = sum(nbytes(M, grp) for (_, grp) in uM)
         d = {"layer_us": round(g * 1e3, 2), "hbm_gbs": round(b / (g * 1e-3) / 1e9, 1)}
         if not args.no_dense:
             _, gd = _timed(uM, dense_fn, max(20, args.steps // 4), 3, range(nl))
@@ -427,8 +433,9 @@ def run_int8(args):
                          f"repeated {reps} times ({dt:.1f} s on {threads} threads)"}
     return _line(args, "sparse-quantized linear tokens/s + achieved HBM GB/s, Llama-2-7B layer at 70%",
                  round(sum(Ms) / (sp_wall * 1e-3), 1), "tokens/s", sp_wall,
-                 "Llama-2-7B decoder layer, 7 linears, int8 weights (per-row scales) and int8 activations "
-                 "(per-token scales), 70% sparsity, batches 1, 16, 64, 4 layers rotated",
+                 "Llama-2-7B decoder layer, 7 linears (grouped launches q|k|v, o, gate|up, down), int8 weights "
+                 "(per-row scales) and int8 activations (per-token scales), 70% sparsity, batches 1, 16, 64, "
+                 "4 layers rotated",
                  {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                   "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_int8",
                   "bytes_per_launch": int(step_bytes / len(units)), "avg_launch_us": round(launch_ms * 1e3, 3)},

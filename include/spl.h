@@ -221,6 +221,39 @@ spl_status spl_sparse_linear_group(const spl_sparse_task* tasks, int32_t count, 
 spl_status spl_dense_linear_group(const spl_dense_task* tasks, int32_t count, int64_t M, int32_t dtype,
                                   int32_t algo, hipStream_t stream);
 
+/* Grouped sparse-quantized launches (paper section 3.4): up to SPL_MAX_GROUP
+ * independent int8 linear layers that share the batch size M, one kernel
+ * launch for all of them.  Each task carries the arguments of
+ * spl_sparse_linear_int8 (resp. spl_dense_linear_int8), with the same
+ * requirements and the same bit-exact outputs; spl_sparse_linear_int8 and
+ * spl_dense_linear_int8 are groups of one.  Errors as for those calls (the
+ * first failing task's status; nothing is launched then).  The task array is
+ * read on the host during the call and need not outlive it.  Tasks must not
+ * write overlapping outputs. */
+typedef struct {
+  const int8_t* Xq;              /* [M][K] activation codes */
+  const float* x_scales;         /* [M] */
+  const spl_matrix* Wq;          /* tile layout, int8 */
+  const float* w_scales;         /* [N] */
+  void* Y;                       /* out [M][N] fp16 */
+  int32_t* acc_out;              /* optional out [M][N] int32 sums, or NULL */
+} spl_int8_task;
+
+typedef struct {
+  const int8_t* Xq;              /* [M][K] activation codes */
+  const float* x_scales;         /* [M] */
+  const int8_t* Wq;              /* dense [N][K] codes */
+  const float* w_scales;         /* [N] */
+  int64_t N;
+  int64_t K;
+  void* Y;                       /* out [M][N] fp16 */
+  int32_t* acc_out;              /* optional out [M][N] int32 sums, or NULL */
+} spl_dense_int8_task;
+
+spl_status spl_sparse_linear_int8_group(const spl_int8_task* tasks, int32_t count, int64_t M, hipStream_t stream);
+spl_status spl_dense_linear_int8_group(const spl_dense_int8_task* tasks, int32_t count, int64_t M,
+                                       hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

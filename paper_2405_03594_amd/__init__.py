@@ -63,6 +63,17 @@ class _DenseTask(ctypes.Structure):
                 ("Y", ctypes.c_void_p)]
 
 
+class _Int8Task(ctypes.Structure):
+    _fields_ = [("Xq", ctypes.c_void_p), ("x_scales", ctypes.c_void_p), ("Wq", ctypes.POINTER(_Matrix)),
+                ("w_scales", ctypes.c_void_p), ("Y", ctypes.c_void_p), ("acc_out", ctypes.c_void_p)]
+
+
+class _DenseInt8Task(ctypes.Structure):
+    _fields_ = [("Xq", ctypes.c_void_p), ("x_scales", ctypes.c_void_p), ("Wq", ctypes.c_void_p),
+                ("w_scales", ctypes.c_void_p), ("N", ctypes.c_int64), ("K", ctypes.c_int64), ("Y", ctypes.c_void_p),
+                ("acc_out", ctypes.c_void_p)]
+
+
 MAX_GROUP = 16
 _lib = None
 
@@ -94,6 +105,8 @@ def lib() -> ctypes.CDLL:
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
         "spl_sparse_linear_group": (ctypes.c_int, [ctypes.POINTER(_SparseTask), I32, I64, I32, P]),
         "spl_dense_linear_group": (ctypes.c_int, [ctypes.POINTER(_DenseTask), I32, I64, I32, I32, P]),
+        "spl_sparse_linear_int8_group": (ctypes.c_int, [ctypes.POINTER(_Int8Task), I32, I64, P]),
+        "spl_dense_linear_int8_group": (ctypes.c_int, [ctypes.POINTER(_DenseInt8Task), I32, I64, P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -330,4 +343,54 @@ def dense_linear_group(Xs, Ws, outs=None, algo: str = "auto", stream=None):
         tasks[i].Y = Y.data_ptr()
     _check("spl_dense_linear_group", L.spl_dense_linear_group(tasks, n, M, _TORCH_DTYPE[Xs[0].dtype], ALGO[algo],
                                                               _stream(stream)))
+    return outs
+
+
+def sparse_linear_int8_group(Xqs, x_scales, Wqcs, w_scales, outs=None, acc_outs=None, stream=None):
+    """fp16 Y_i = dequant(int32 Xq_i (Wq_i . Mask_i)^T) for up to MAX_GROUP independent
+    int8 layers sharing the batch size, in one launch."""
+    L = lib()
+    n = len(Xqs)
+    if not (n == len(x_scales) == len(Wqcs) == len(w_scales)) or not 1 <= n <= MAX_GROUP:
+        raise ValueError("need 1..MAX_GROUP (Xq, x_scales, Wq, w_scales) tuples")
+    M = Xqs[0].shape[0]
+    if outs is None:
+        outs = [torch.empty((M, W.rows), dtype=torch.float16, device=X.device) for X, W in zip(Xqs, Wqcs)]
+    accs = acc_outs if acc_outs is not None else [None] * n
+    views = [W.view() for W in Wqcs]
+    tasks = (_Int8Task * n)()
+    for i in range(n):
+        for t, nm in ((Xqs[i], "Xq"), (x_scales[i], "x_scales"), (w_scales[i], "w_scales")):
+            _dev_tensor(t, nm)
+        if Xqs[i].shape[0] != M:
+            raise ValueError("every layer of a group shares M")
+        tasks[i].Xq, tasks[i].x_scales = Xqs[i].data_ptr(), x_scales[i].data_ptr()
+        tasks[i].Wq = ctypes.pointer(views[i])
+        tasks[i].w_scales, tasks[i].Y = w_scales[i].data_ptr(), outs[i].data_ptr()
+        tasks[i].acc_out = None if accs[i] is None else accs[i].data_ptr()
+    _check("spl_sparse_linear_int8_group", L.spl_sparse_linear_int8_group(tasks, n, M, _stream(stream)))
+    return outs
+
+
+def dense_linear_int8_group(Xqs, x_scales, Wqs, w_scales, outs=None, acc_outs=None, stream=None):
+    """Dense comparator of :func:`sparse_linear_int8_group`."""
+    L = lib()
+    n = len(Xqs)
+    if not (n == len(x_scales) == len(Wqs) == len(w_scales)) or not 1 <= n <= MAX_GROUP:
+        raise ValueError("need 1..MAX_GROUP (Xq, x_scales, Wq, w_scales) tuples")
+    M = Xqs[0].shape[0]
+    if outs is None:
+        outs = [torch.empty((M, W.shape[0]), dtype=torch.float16, device=X.device) for X, W in zip(Xqs, Wqs)]
+    accs = acc_outs if acc_outs is not None else [None] * n
+    tasks = (_DenseInt8Task * n)()
+    for i in range(n):
+        for t, nm in ((Xqs[i], "Xq"), (x_scales[i], "x_scales"), (Wqs[i], "Wq"), (w_scales[i], "w_scales")):
+            _dev_tensor(t, nm)
+        if Xqs[i].shape[0] != M:
+            raise ValueError("every layer of a group shares M")
+        tasks[i].Xq, tasks[i].x_scales, tasks[i].Wq = Xqs[i].data_ptr(), x_scales[i].data_ptr(), Wqs[i].data_ptr()
+        tasks[i].w_scales, tasks[i].Y = w_scales[i].data_ptr(), outs[i].data_ptr()
+        tasks[i].N, tasks[i].K = Wqs[i].shape
+        tasks[i].acc_out = None if accs[i] is None else accs[i].data_ptr()
+    _check("spl_dense_linear_int8_group", L.spl_dense_linear_int8_group(tasks, n, M, _stream(stream)))
     return outs

@@ -254,12 +254,6 @@ struct DenseGroupArg {
   int32_t M;
 };
 
-// Task of this workgroup (wave-uniform).
-__device__ __forceinline__ int find_task(const int32_t* first, int count) {
-  int ti = 0;
-  for (int i = 1; i < count; ++i) ti = (int)blockIdx.x >= first[i] ? i : ti;
-  return ti;
-}
 
 // Dynamic LDS of the sparse kernel: per-wave value staging buffers (later the
 // reduction buffer), then (XL) the staged activations.

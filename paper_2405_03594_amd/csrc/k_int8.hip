@@ -109,11 +109,54 @@ struct I8Chunk {
   int np;
 };
 
+// Grouped launches: task i owns the row blocks [first[i], first[i + 1]) of the
+// grid's x dimension; every task has the group's batch M (grid y).
+struct I8TaskArg {
+  const int8_t* Xq;
+  const float* sx;
+  const uint32_t* bm;
+  const uint8_t* values;
+  const int32_t* toff;
+  int64_t N, K;
+  const float* sw;
+  uint16_t* Y;
+  int32_t* acc;
+};
+struct I8GroupArg {
+  I8TaskArg t[SPL_MAX_GROUP];
+  int32_t first[SPL_MAX_GROUP + 1];
+  int32_t count;
+  int32_t M;
+};
+struct I8DenseTaskArg {
+  const int8_t* Xq;
+  const float* sx;
+  const int8_t* W;
+  int64_t N, K;
+  const float* sw;
+  uint16_t* Y;
+  int32_t* acc;
+};
+struct I8DenseGroupArg {
+  I8DenseTaskArg t[SPL_MAX_GROUP];
+  int32_t first[SPL_MAX_GROUP + 1];
+  int32_t count;
+  int32_t M;
+};
+
 template <int MT, bool XL, int W>
-__global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
-    const int8_t* __restrict__ Xq, const float* __restrict__ sx, int64_t M, int64_t K,
-    const uint32_t* __restrict__ bm_tiles, const uint8_t* __restrict__ values, const int32_t* __restrict__ tile_offsets,
-    int64_t N, const float* __restrict__ sw, uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+__global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(const I8GroupArg g) {
+  const int ti = find_task(g.first, g.count);
+  const I8TaskArg tk = g.t[ti];
+  const int8_t* __restrict__ Xq = tk.Xq;
+  const float* __restrict__ sx = tk.sx;
+  const int64_t M = g.M, K = tk.K, N = tk.N;
+  const uint32_t* __restrict__ bm_tiles = tk.bm;
+  const uint8_t* __restrict__ values = tk.values;
+  const int32_t* __restrict__ tile_offsets = tk.toff;
+  const float* __restrict__ sw = tk.sw;
+  uint16_t* __restrict__ Y = tk.Y;
+  int32_t* __restrict__ acc_out = tk.acc;
   constexpr int C = MT == 4 ? kI8Chunk / 2 : kI8Chunk;     // four batch fragments: half the operands in flight
   extern __shared__ __align__(16) unsigned char dsm[];     // value buffers (later the partial sums), then X
   __shared__ uint32_t lut[16];
@@ -125,7 +168,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
   const int tsel = fg >> 1, half = fg & 1;
-  const int64_t blk = blockIdx.x;
+  const int64_t blk = (int64_t)blockIdx.x - g.first[ti];
   const int64_t m0 = (int64_t)blockIdx.y * 16 * MT;
   const int S = (int)tile_steps(K);
   const int P = (S + 1) / 2;
@@ -300,17 +343,23 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(
 }
 
 template <int MT>
-__global__ void __launch_bounds__(kI8Threads) k_dense_int8(const int8_t* __restrict__ Xq, const float* __restrict__ sx,
-                                                           int64_t M, int64_t K, const int8_t* __restrict__ Wq,
-                                                           int64_t N, const float* __restrict__ sw,
-                                                           uint16_t* __restrict__ Y, int32_t* __restrict__ acc_out) {
+__global__ void __launch_bounds__(kI8Threads) k_dense_int8(const I8DenseGroupArg g) {
+  const int ti = find_task(g.first, g.count);
+  const I8DenseTaskArg tk = g.t[ti];
+  const int8_t* __restrict__ Xq = tk.Xq;
+  const float* __restrict__ sx = tk.sx;
+  const int8_t* __restrict__ Wq = tk.W;
+  const int64_t M = g.M, K = tk.K, N = tk.N;
+  const float* __restrict__ sw = tk.sw;
+  uint16_t* __restrict__ Y = tk.Y;
+  int32_t* __restrict__ acc_out = tk.acc;
   __shared__ int32_t part[kI8Waves * MT * 256];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
   const int Q = (int)((K + 63) / 64);                     // 64-column steps
   const int G = (Q + kI8Unroll - 1) / kI8Unroll;
-  const int64_t n0 = (int64_t)blockIdx.x * 16;
+  const int64_t n0 = ((int64_t)blockIdx.x - g.first[ti]) * 16;
   const int64_t m0 = (int64_t)blockIdx.y * 16 * MT;
   const int64_t wrow = (n0 + fr < N ? n0 + fr : N - 1) * K;
   int64_t xrow[MT];
@@ -352,35 +401,31 @@ __global__ void __launch_bounds__(kI8Threads) k_dense_int8(const int8_t* __restr
 int i8_fragments(int64_t M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 
 template <int MT, bool XL, int W>
-hipError_t sparse_int8_launch(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc, const float* sw,
-                              void* Y, int32_t* acc_out, hipStream_t s) {
+hipError_t sparse_int8_launch(const I8GroupArg& g, int64_t kmax, hipStream_t s) {
   auto* kernel = k_sparse_int8<MT, XL, W>;
   const size_t region = (size_t)W * kI8VBufAlloc > (size_t)W * MT * 1024 ? (size_t)W * kI8VBufAlloc
                                                                           : (size_t)W * MT * 1024;
-  const size_t xbytes = XL ? (size_t)M * (size_t)i8_xs_stride(Wc.cols) : 0;
+  const size_t xbytes = XL ? (size_t)g.M * (size_t)i8_xs_stride(kmax) : 0;
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                                      (int)(region + (XL ? kI8XLdsMax + 16 * 16 : 0)));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)tile_blocks(Wc.rows), (unsigned)((M + 16 * MT - 1) / (16 * MT)));
-  hipLaunchKernelGGL(kernel, grid, dim3(W * kWave), region + xbytes, s, Xq, sx, M, Wc.cols, Wc.bitmask,
-                     static_cast<const uint8_t*>(Wc.values), Wc.tile_offsets, Wc.rows, sw,
-                     static_cast<uint16_t*>(Y), acc_out);
+  const dim3 grid((unsigned)g.first[g.count], (unsigned)((g.M + 16 * MT - 1) / (16 * MT)));
+  hipLaunchKernelGGL(kernel, grid, dim3(W * kWave), region + xbytes, s, g);
   return hipGetLastError();
 }
 
+// Activations staged in LDS when every task's M x 64 ceil(S/2) bytes fit.
 template <int W>
-hipError_t sparse_int8_w(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc, const float* sw,
-                         void* Y, int32_t* acc_out, hipStream_t s) {
-  const int MT = i8_fragments(M);
-  if (MT == 1 && M * 64 * ((tile_steps(Wc.cols) + 1) / 2) <= kI8XLdsMax)
-    return sparse_int8_launch<1, true, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
-  if (MT == 1) return sparse_int8_launch<1, false, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
-  if (MT == 2) return sparse_int8_launch<2, false, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
-  return sparse_int8_launch<4, false, W>(Xq, sx, M, Wc, sw, Y, acc_out, s);
+hipError_t sparse_int8_w(const I8GroupArg& g, int64_t kmax, hipStream_t s) {
+  const int MT = i8_fragments(g.M);
+  if (MT == 1 && (int64_t)g.M * 64 * ((tile_steps(kmax) + 1) / 2) <= kI8XLdsMax)
+    return sparse_int8_launch<1, true, W>(g, kmax, s);
+  if (MT == 1) return sparse_int8_launch<1, false, W>(g, kmax, s);
+  if (MT == 2) return sparse_int8_launch<2, false, W>(g, kmax, s);
+  return sparse_int8_launch<4, false, W>(g, kmax, s);
 }
 
-// 16 waves per workgroup when the grid has fewer than two row blocks per CU.
 bool i8_small_grid(int64_t blocks) {
   static int cus = [] {
     int dev = 0, n = 0;
@@ -394,24 +439,42 @@ bool i8_small_grid(int64_t blocks) {
 
 }  // namespace
 
-hipError_t launch_sparse_int8(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc, const float* sw,
-                              void* Y, int32_t* acc_out, hipStream_t s) {
-  const int64_t blocks = tile_blocks(Wc.rows) * ((M + 63) / 64);
-  return i8_small_grid(blocks) ? sparse_int8_w<16>(Xq, sx, M, Wc, sw, Y, acc_out, s)
-                               : sparse_int8_w<8>(Xq, sx, M, Wc, sw, Y, acc_out, s);
+hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s) {
+  I8GroupArg g{};
+  g.count = count;
+  g.M = (int32_t)M;
+  g.first[0] = 0;
+  int64_t kmax = 0;
+  for (int i = 0; i < count; ++i) {
+    const spl_matrix& W = *tasks[i].Wq;
+    g.t[i] = I8TaskArg{tasks[i].Xq, tasks[i].x_scales, W.bitmask, static_cast<const uint8_t*>(W.values),
+                       W.tile_offsets, W.rows, W.cols, tasks[i].w_scales, static_cast<uint16_t*>(tasks[i].Y),
+                       tasks[i].acc_out};
+    g.first[i + 1] = g.first[i] + (int32_t)tile_blocks(W.rows);
+    kmax = W.cols > kmax ? W.cols : kmax;
+  }
+  const int64_t blocks = (int64_t)g.first[count] * ((M + 63) / 64);
+  return i8_small_grid(blocks) ? sparse_int8_w<16>(g, kmax, s) : sparse_int8_w<8>(g, kmax, s);
 }
 
-hipError_t launch_dense_int8(const int8_t* Xq, const float* sx, int64_t M, const int8_t* Wq, const float* sw,
-                             int64_t N, int64_t K, void* Y, int32_t* acc_out, hipStream_t s) {
+hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s) {
+  I8DenseGroupArg g{};
+  g.count = count;
+  g.M = (int32_t)M;
+  g.first[0] = 0;
+  for (int i = 0; i < count; ++i) {
+    g.t[i] = I8DenseTaskArg{tasks[i].Xq, tasks[i].x_scales, tasks[i].Wq, tasks[i].N, tasks[i].K, tasks[i].w_scales,
+                            static_cast<uint16_t*>(tasks[i].Y), tasks[i].acc_out};
+    g.first[i + 1] = g.first[i] + (int32_t)((tasks[i].N + 15) / 16);
+  }
   const int MT = i8_fragments(M);
-  const dim3 grid((unsigned)((N + 15) / 16), (unsigned)((M + 16 * MT - 1) / (16 * MT))), block(kI8Threads);
-  uint16_t* y = static_cast<uint16_t*>(Y);
+  const dim3 grid((unsigned)g.first[count], (unsigned)((M + 16 * MT - 1) / (16 * MT))), block(kI8Threads);
   if (MT == 1)
-    hipLaunchKernelGGL((k_dense_int8<1>), grid, block, 0, s, Xq, sx, M, K, Wq, N, sw, y, acc_out);
+    hipLaunchKernelGGL((k_dense_int8<1>), grid, block, 0, s, g);
   else if (MT == 2)
-    hipLaunchKernelGGL((k_dense_int8<2>), grid, block, 0, s, Xq, sx, M, K, Wq, N, sw, y, acc_out);
+    hipLaunchKernelGGL((k_dense_int8<2>), grid, block, 0, s, g);
   else
-    hipLaunchKernelGGL((k_dense_int8<4>), grid, block, 0, s, Xq, sx, M, K, Wq, N, sw, y, acc_out);
+    hipLaunchKernelGGL((k_dense_int8<4>), grid, block, 0, s, g);
   return hipGetLastError();
 }
 

@@ -188,18 +188,37 @@ spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, voi
   return spl_sparse_linear_ex(X, M, Wc, Y, SPL_ALGO_AUTO, stream);
 }
 
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
+  const spl_status st = spl_check_matrix(t->Wq);
+  if (st != SPL_OK) return st;
+  if (t->Wq->dtype != SPL_I8 || t->Wq->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
+  const spl_status xy = check_xy(t->Xq, M, t->Wq->cols, t->Wq->rows, t->Y);
+  if (xy != SPL_OK || M == 0) return xy;                 // M == 0: nothing is read or written
+  if (!t->x_scales || !t->w_scales || !aligned(t->x_scales, 4) || !aligned(t->w_scales, 4)) return SPL_ERR_INVALID_ARG;
+  if (t->acc_out && !aligned(t->acc_out, 16)) return SPL_ERR_INVALID_ARG;
+  if (t->Wq->cols % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  return SPL_OK;
+}
+
 spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream) {
-  const spl_status st = spl_check_matrix(Wqc);
-  if (st != SPL_OK) return st;
-  if (Wqc->dtype != SPL_I8 || Wqc->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
-  const spl_status xy = check_xy(Xq, M, Wqc->cols, Wqc->rows, Y);
-  if (xy != SPL_OK || M == 0) return xy;
-  if (!x_scales || !w_scales || !aligned(x_scales, 4) || !aligned(w_scales, 4)) return SPL_ERR_INVALID_ARG;
-  if (acc_out && !aligned(acc_out, 16)) return SPL_ERR_INVALID_ARG;
-  if (Wqc->cols % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  const spl_int8_task t{Xq, x_scales, Wqc, w_scales, Y, acc_out};
+  return spl_sparse_linear_int8_group(&t, 1, M, stream);
+}
+
+spl_status spl_sparse_linear_int8_group(const spl_int8_task* tasks, int32_t count, int64_t M, hipStream_t stream) {
+  if (!tasks || count < 1 || count > SPL_MAX_GROUP || M < 0) return SPL_ERR_INVALID_ARG;
+  int64_t blocks = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const spl_status st = check_int8_task(&tasks[i], M);
+    if (st != SPL_OK) return st;
+    blocks += spl::tile_blocks(tasks[i].Wq->rows);
+  }
+  if (blocks >= kMaxDim || M >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
   (void)hipGetLastError();
-  return launched(spl::launch_sparse_int8(Xq, x_scales, M, *Wqc, w_scales, Y, acc_out, stream));
+  return launched(spl::launch_sparse_int8(tasks, count, M, stream));
 }
 
 spl_status spl_dense_linear_ex(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
@@ -237,17 +256,37 @@ spl_status spl_dense_linear(const void* X, int64_t M, const void* W, int32_t dty
   return spl_dense_linear_ex(X, M, W, dtype, N, K, Y, SPL_ALGO_AUTO, stream);
 }
 
+// Arguments of one dense int8 task (those of spl_dense_linear_int8).
+static spl_status check_dense_int8_task(const spl_dense_int8_task* t, int64_t M) {
+  if (!t->Wq || !dims_ok(t->N, t->K) || !aligned(t->Wq, 16)) return SPL_ERR_INVALID_ARG;
+  const spl_status xy = check_xy(t->Xq, M, t->K, t->N, t->Y);
+  if (xy != SPL_OK || M == 0) return xy;                 // M == 0: nothing is read or written
+  if (!t->x_scales || !t->w_scales || !aligned(t->x_scales, 4) || !aligned(t->w_scales, 4)) return SPL_ERR_INVALID_ARG;
+  if (t->acc_out && !aligned(t->acc_out, 16)) return SPL_ERR_INVALID_ARG;
+  if (t->K % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  return SPL_OK;
+}
+
 spl_status spl_dense_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const int8_t* Wq,
                                  const float* w_scales, int64_t N, int64_t K, void* Y, int32_t* acc_out,
                                  hipStream_t stream) {
-  if (!Wq || !dims_ok(N, K) || !aligned(Wq, 16)) return SPL_ERR_INVALID_ARG;
-  const spl_status xy = check_xy(Xq, M, K, N, Y);
-  if (xy != SPL_OK || M == 0) return xy;
-  if (!x_scales || !w_scales || !aligned(x_scales, 4) || !aligned(w_scales, 4)) return SPL_ERR_INVALID_ARG;
-  if (acc_out && !aligned(acc_out, 16)) return SPL_ERR_INVALID_ARG;
-  if (K % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  const spl_dense_int8_task t{Xq, x_scales, Wq, w_scales, N, K, Y, acc_out};
+  return spl_dense_linear_int8_group(&t, 1, M, stream);
+}
+
+spl_status spl_dense_linear_int8_group(const spl_dense_int8_task* tasks, int32_t count, int64_t M,
+                                       hipStream_t stream) {
+  if (!tasks || count < 1 || count > SPL_MAX_GROUP || M < 0) return SPL_ERR_INVALID_ARG;
+  int64_t blocks = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const spl_status st = check_dense_int8_task(&tasks[i], M);
+    if (st != SPL_OK) return st;
+    blocks += (tasks[i].N + 15) / 16;
+  }
+  if (blocks >= kMaxDim || M >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
   (void)hipGetLastError();
-  return launched(spl::launch_dense_int8(Xq, x_scales, M, Wq, w_scales, N, K, Y, acc_out, stream));
+  return launched(spl::launch_dense_int8(tasks, count, M, stream));
 }
 
 }  // extern "C"

@@ -86,6 +86,14 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   return x;
 }
 
+// Task of this workgroup in a grouped launch whose task i owns workgroups
+// [first[i], first[i + 1]) along x (wave-uniform).
+__device__ __forceinline__ int find_task(const int32_t* first, int count) {
+  int ti = 0;
+  for (int i = 1; i < count; ++i) ti = (int)blockIdx.x >= first[i] ? i : ti;
+  return ti;
+}
+
 typedef __attribute__((address_space(3))) unsigned char lds_t;
 
 // 32-bit LDS offset of a pointer into shared memory, and loads at such offsets.
@@ -127,8 +135,7 @@ hipError_t launch_dense_decode(const spl_dense_task* tasks, int count, int64_t M
 hipError_t launch_sparse_prefill(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
 hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
                                 void* Y, hipStream_t s);
-hipError_t launch_sparse_int8(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& Wc,
-                              const float* sw, void* Y, int32_t* acc, hipStream_t s);
-hipError_t launch_dense_int8(const int8_t* Xq, const float* sx, int64_t M, const int8_t* Wq, const float* sw,
-                             int64_t N, int64_t K, void* Y, int32_t* acc, hipStream_t s);
+// Sparse-quantized kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
+hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s);
+hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s);
 }  // namespace spl

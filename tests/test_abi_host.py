@@ -191,3 +191,45 @@ def test_group_argument_checks(L):
     assert g(d, 2, 2, 2, 0, None) == UNSUPPORTED                  # K % 8 != 0
     d[1].K, d[1].W = 64, 0x60008
     assert g(d, 2, 2, 2, 0, None) == INVALID                      # misaligned W
+
+
+def test_int8_group_argument_checks(L):
+    from paper_2405_03594_amd import MAX_GROUP, _DenseInt8Task, _Int8Task
+
+    m = _mat(dtype=3, layout=1, tile_offsets=0x40000)
+    mbf = _mat(dtype=2, layout=1, tile_offsets=0x40000)
+    X, Y, s = 0x40000, 0x50000, 0x60000
+
+    def tasks(*mats, scales=s):
+        arr = (_Int8Task * max(1, len(mats)))()
+        for i, mm in enumerate(mats):
+            arr[i].Xq, arr[i].x_scales, arr[i].w_scales = X, scales, scales
+            arr[i].Y = Y + 0x1000 * i
+            arr[i].Wq = ctypes.pointer(mm) if mm is not None else None
+        return arr
+
+    f = L.spl_sparse_linear_int8_group
+    assert f(tasks(m, m), 2, 0, None) == OK                       # M = 0: checked, then a no-op
+    assert f(tasks(m, m, scales=None), 2, 0, None) == OK          # M = 0 reads no scales
+    assert f(tasks(m), 0, 2, None) == INVALID                     # empty group
+    assert f(None, 1, 2, None) == INVALID
+    assert f(tasks(*([m] * (MAX_GROUP + 1))), MAX_GROUP + 1, 2, None) == INVALID
+    assert f(tasks(m, None), 2, 0, None) == INVALID               # missing matrix
+    assert f(tasks(m, mbf), 2, 0, None) == UNSUPPORTED            # a bf16 matrix in an int8 group
+    assert f(tasks(m, m, scales=None), 2, 2, None) == INVALID     # scales required when M > 0
+    assert f(tasks(m), 1, -1, None) == INVALID
+    bad = tasks(m, m)
+    bad[1].acc_out = 0x70004                                       # misaligned int32 output
+    assert f(bad, 2, 2, None) == INVALID
+
+    g = L.spl_dense_linear_int8_group
+    d = (_DenseInt8Task * 2)()
+    for i in range(2):
+        d[i].Xq, d[i].x_scales, d[i].Wq, d[i].w_scales = X, s, 0x10000, s
+        d[i].N, d[i].K, d[i].Y = 8, 64, Y + 0x1000 * i
+    assert g(d, 2, 0, None) == OK
+    assert g(d, 0, 2, None) == INVALID
+    d[1].K = 24
+    assert g(d, 2, 2, None) == UNSUPPORTED                        # K % 16 != 0
+    d[1].K, d[1].Wq = 64, 0x10008
+    assert g(d, 2, 2, None) == INVALID                            # misaligned W

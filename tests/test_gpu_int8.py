@@ -151,3 +151,34 @@ def test_int8_epilogue_rounds_each_product(orc, spl):
     _assert_equal(acc, acc_ref, "acc")
     _assert_equal(np.diag(y), np.diag(y_ref), "Y at the ties")
     _assert_equal(y, y_ref, "Y")
+
+
+@pytest.mark.parametrize("M", [1, 16, 40, 70])
+def test_int8_group_matches_oracle_and_single_calls(orc, spl, M):
+    """A group of three layers with different N and K (one launch for all):
+    every task's int32 sums and fp16 outputs equal the oracle and the single
+    calls bit for bit, sparse and dense (M = 1: staged activations; 16, 40,
+    70: one, two and four batch fragments, 70 on two batch blocks)."""
+    import torch
+
+    shapes = [(40, 96, 0.7), (100, 528, 0.5), (33, 96, 0.9)]
+    Xqs, sxs, Wcs, sws, dense, refs = [], [], [], [], [], []
+    for i, (N, K, s) in enumerate(shapes):
+        Wq, mask, sw = synth.int8_weight(800 + i, N, K, s)
+        Xq, sx = synth.int8_activations(810 + i, M, K)
+        refs.append(orc.linear_i8(Xq, sx, orc.pack(Wq, "i8", mask), sw))
+        Xqs.append(to_dev(Xq, "i8"))
+        sxs.append(torch.from_numpy(sx).cuda())
+        Wcs.append(spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda()))
+        sws.append(torch.from_numpy(sw).cuda())
+        dense.append(to_dev(np.where(mask.astype(bool), Wq, np.int8(0)), "i8"))
+    accs = [torch.empty((M, N), dtype=torch.int32, device="cuda") for N, _, _ in shapes]
+    outs = spl.sparse_linear_int8_group(Xqs, sxs, Wcs, sws, acc_outs=accs)
+    daccs = [torch.empty((M, N), dtype=torch.int32, device="cuda") for N, _, _ in shapes]
+    douts = spl.dense_linear_int8_group(Xqs, sxs, dense, sws, acc_outs=daccs)
+    for i, (acc_ref, y_ref) in enumerate(refs):
+        for what, acc, y in (("sparse", accs[i], outs[i]), ("dense", daccs[i], douts[i])):
+            _assert_equal(acc.cpu().numpy(), acc_ref, f"{what} group task {i} acc M={M}")
+            _assert_equal(y.cpu().view(torch.int16).numpy().view(np.uint16), y_ref, f"{what} group task {i} Y M={M}")
+        single = spl.sparse_linear_int8(Xqs[i], sxs[i], Wcs[i], sws[i])
+        assert torch.equal(single.view(torch.int16), outs[i].view(torch.int16))
