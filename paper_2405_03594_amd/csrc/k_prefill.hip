@@ -16,10 +16,11 @@
 //     X rows into the B buffer;
 //   * sparse (paper section 2.4.2): the A buffer is filled by expanding the
 //     stage's compressed 16 x 32 tiles (BN/16 row blocks x 2 k-steps, shared
-//     out over the waves), each once per workgroup: bitmask words are fetched two
-//     stages ahead and value windows one stage ahead; a lane expands its row's
-//     8 columns with v_perm_b32 under a nibble selector table, as in the decode
-//     kernel, and writes them with one 16-byte LDS store.
+//     out over the waves), each once per workgroup and one stage ahead, before
+//     the current stage's MFMAs: bitmask words are fetched three stages ahead
+//     and value windows two ahead; a lane expands its row's 8 columns with
+//     v_perm_b32 under a nibble selector table, as in the decode kernel, and
+//     writes them with one 16-byte LDS store.
 #include "spl_common.h"
 
 namespace spl {
@@ -248,31 +249,40 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Pipeline: bitmask words three stages ahead, value windows two ahead; a
+  // stage's W tiles are expanded into LDS one stage ahead, before the current
+  // stage's MFMAs, so that their ALU work can interleave with the matrix
+  // cores; X slabs are fetched one stage ahead and stored after the MFMAs.
   const SlabSrc<RR> xsrc(X, M, K, m0);
   Slab<BM / RR> xs;
   TileWords<TW> tw;
   TileWindows<TW> tv;
   fetch_words(tw, 0);
   xsrc.fetch(xs, K, 0);
-  fetch_windows(tv, tw);
+  fetch_windows(tv, tw);                               // stage 0
   if (nst > 1) fetch_words(tw, 1);
   __syncthreads();                                     // the selector table
   expand_store(tv, abuf[0]);
   slab_store<RR>(xs, bbuf[0]);
+  if (nst > 1) {
+    fetch_windows(tv, tw);                             // stage 1
+    if (nst > 2) fetch_words(tw, 2);
+  }
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int cur = st & 1;
     const bool more = st + 1 < nst;
     if (more) {
-      // stage st + 1: its words were fetched a stage ago, so the windows go out first (the wait for
-      // the words must not also wait for this stage's activation loads)
-      fetch_windows(tv, tw);
+      // buffers cur ^ 1 were last read by stage st - 1's MFMAs, before the previous barrier
+      expand_store(tv, abuf[cur ^ 1]);                 // stage st + 1
+      if (st + 2 < nst) {
+        fetch_windows(tv, tw);                         // stage st + 2 (its words were fetched a stage ago)
+        if (st + 3 < nst) fetch_words(tw, st + 3);
+      }
       xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
-      if (st + 2 < nst) fetch_words(tw, st + 2);
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (more) {
-      expand_store(tv, abuf[cur ^ 1]);
       slab_store<RR>(xs, bbuf[cur ^ 1]);
       __syncthreads();
     }
@@ -305,27 +315,37 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Global loads run two stages ahead of the multiplication: register sets
+  // (x0, w0) and (x1, w1) alternate, the loop unrolled by two stages.
   const SlabSrc<RR> xsrc(X, M, K, m0), wsrc(W, N, K, n0);
-  Slab<BM / RR> xs;
-  Slab<BN / RR> ws;
-  xsrc.fetch(xs, K, 0);
-  wsrc.fetch(ws, K, 0);
-  slab_store<RR>(ws, abuf[0]);
-  slab_store<RR>(xs, bbuf[0]);
+  Slab<BM / RR> x0, x1;
+  Slab<BN / RR> w0, w1;
+  xsrc.fetch(x0, K, 0);
+  wsrc.fetch(w0, K, 0);
+  if (nst > 1) {
+    xsrc.fetch(x1, K, kPfBK);
+    wsrc.fetch(w1, K, kPfBK);
+  }
+  slab_store<RR>(w0, abuf[0]);
+  slab_store<RR>(x0, bbuf[0]);
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
+  // stage st is in the LDS buffers st % 2; (xl, wl) hold stage st + 1 and receive stage st + 2
+  auto step = [&](int st, Slab<BM / RR>& xn, Slab<BN / RR>& wn_, Slab<BM / RR>& xl, Slab<BN / RR>& wl) {
     const int cur = st & 1;
-    const bool more = st + 1 < nst;
-    if (more) {
-      xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
-      wsrc.fetch(ws, K, (int64_t)kPfBK * (st + 1));
+    if (st + 2 < nst) {
+      xsrc.fetch(xn, K, (int64_t)kPfBK * (st + 2));
+      wsrc.fetch(wn_, K, (int64_t)kPfBK * (st + 2));
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
-    if (more) {
-      slab_store<RR>(ws, abuf[cur ^ 1]);
-      slab_store<RR>(xs, bbuf[cur ^ 1]);
+    if (st + 1 < nst) {
+      slab_store<RR>(wl, abuf[cur ^ 1]);
+      slab_store<RR>(xl, bbuf[cur ^ 1]);
       __syncthreads();
     }
+  };
+  for (int st = 0; st < nst; st += 2) {
+    step(st, x0, w0, x1, w1);                          // stage st + 2 -> set 0, stage st + 1 from set 1
+    if (st + 1 < nst) step(st + 1, x1, w1, x0, w0);    // stage st + 3 -> set 1, stage st + 2 from set 0
   }
   pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
