@@ -316,7 +316,9 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Global loads run two stages ahead of the multiplication: register sets
-  // (x0, w0) and (x1, w1) alternate, the loop unrolled by two stages.
+  // (x0, w0) and (x1, w1) alternate, the loop unrolled by two stages.  Stage
+  // st + 1 is stored to LDS at the start of stage st, so one barrier per stage
+  // both publishes it and retires stage st's reads.
   const SlabSrc<RR> xsrc(X, M, K, m0), wsrc(W, N, K, n0);
   Slab<BM / RR> x0, x1;
   Slab<BN / RR> w0, w1;
@@ -329,19 +331,22 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
   slab_store<RR>(w0, abuf[0]);
   slab_store<RR>(x0, bbuf[0]);
   __syncthreads();
-  // stage st is in the LDS buffers st % 2; (xl, wl) hold stage st + 1 and receive stage st + 2
+  // stage st is in the LDS buffers st % 2; (xl, wl) hold stage st + 1, which
+  // is written to the other buffers before this stage's MFMAs (their last
+  // readers, stage st - 1's MFMAs, finished before the previous barrier), and
+  // (xn, wn_) receive stage st + 2
   auto step = [&](int st, Slab<BM / RR>& xn, Slab<BN / RR>& wn_, Slab<BM / RR>& xl, Slab<BN / RR>& wl) {
     const int cur = st & 1;
+    if (st + 1 < nst) {
+      slab_store<RR>(wl, abuf[cur ^ 1]);
+      slab_store<RR>(xl, bbuf[cur ^ 1]);
+    }
     if (st + 2 < nst) {
       xsrc.fetch(xn, K, (int64_t)kPfBK * (st + 2));
       wsrc.fetch(wn_, K, (int64_t)kPfBK * (st + 2));
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
-    if (st + 1 < nst) {
-      slab_store<RR>(wl, abuf[cur ^ 1]);
-      slab_store<RR>(xl, bbuf[cur ^ 1]);
-      __syncthreads();
-    }
+    if (st + 1 < nst) __syncthreads();
   };
   for (int st = 0; st < nst; st += 2) {
     step(st, x0, w0, x1, w1);                          // stage st + 2 -> set 0, stage st + 1 from set 1
