@@ -249,43 +249,49 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Pipeline: bitmask words three stages ahead, value windows two ahead; a
-  // stage's W tiles are expanded into LDS one stage ahead, before the current
-  // stage's MFMAs, so that their ALU work can interleave with the matrix
-  // cores; X slabs are fetched one stage ahead and stored after the MFMAs.
+  // Pipeline: bitmask words three stages ahead, value windows and X slabs two
+  // ahead (X in alternating register sets, the loop unrolled by two stages).
+  // At the start of stage st, stage st + 1's W tiles are expanded into the
+  // other LDS buffers and its X slab stored there (their last readers, stage
+  // st - 1's MFMAs, finished before the previous barrier), so that this ALU
+  // and LDS work can interleave with the matrix cores; one barrier per stage.
   const SlabSrc<RR> xsrc(X, M, K, m0);
-  Slab<BM / RR> xs;
+  Slab<BM / RR> x0, x1;
   TileWords<TW> tw;
   TileWindows<TW> tv;
   fetch_words(tw, 0);
-  xsrc.fetch(xs, K, 0);
+  xsrc.fetch(x0, K, 0);
   fetch_windows(tv, tw);                               // stage 0
-  if (nst > 1) fetch_words(tw, 1);
+  if (nst > 1) {
+    fetch_words(tw, 1);
+    xsrc.fetch(x1, K, kPfBK);
+  }
   __syncthreads();                                     // the selector table
   expand_store(tv, abuf[0]);
-  slab_store<RR>(xs, bbuf[0]);
+  slab_store<RR>(x0, bbuf[0]);
   if (nst > 1) {
     fetch_windows(tv, tw);                             // stage 1
     if (nst > 2) fetch_words(tw, 2);
   }
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
+  // (xl holds stage st + 1; xn receives stage st + 2)
+  auto step = [&](int st, Slab<BM / RR>& xn, Slab<BM / RR>& xl) {
     const int cur = st & 1;
-    const bool more = st + 1 < nst;
-    if (more) {
-      // buffers cur ^ 1 were last read by stage st - 1's MFMAs, before the previous barrier
+    if (st + 1 < nst) {
       expand_store(tv, abuf[cur ^ 1]);                 // stage st + 1
+      slab_store<RR>(xl, bbuf[cur ^ 1]);
       if (st + 2 < nst) {
         fetch_windows(tv, tw);                         // stage st + 2 (its words were fetched a stage ago)
         if (st + 3 < nst) fetch_words(tw, st + 3);
+        xsrc.fetch(xn, K, (int64_t)kPfBK * (st + 2));
       }
-      xsrc.fetch(xs, K, (int64_t)kPfBK * (st + 1));
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
-    if (more) {
-      slab_store<RR>(xs, bbuf[cur ^ 1]);
-      __syncthreads();
-    }
+    if (st + 1 < nst) __syncthreads();
+  };
+  for (int st = 0; st < nst; st += 2) {
+    step(st, x0, x1);                                  // stage st + 1 from set 1, stage st + 2 -> set 0
+    if (st + 1 < nst) step(st + 1, x1, x0);            // stage st + 2 from set 0, stage st + 3 -> set 1
   }
   pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
