@@ -454,6 +454,206 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   reduce_store<T, MT, W>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, tk.N, tk.Y);
 }
 
+// Two row blocks per workgroup, for batches of up to 16 rows whose activations
+// are loaded directly: every wave walks the same k-range of both blocks, so
+// each activation load feeds two MFMAs (halving the activation loads, which
+// bound this case).  Each block keeps its own offsets window, half of the
+// staging buffer, regrouped words and accumulator; a chunk is as many tiles as
+// fit both halves.  The second block of a pair past the last row block aliases
+// the first with zero words and is not stored.  Otherwise the same steps as
+// k_sparse_decode.
+constexpr int kHalfVBuf = kVBuf / 2;                 // staged value bytes per block and chunk
+constexpr int kHalfVBufAlloc = kHalfVBuf + 16;       // + room for an 8-byte window at the last value
+constexpr int kHalfPieceRounds = (kHalfVBuf / 16 + kWave - 1) / kWave;
+
+template <int W>
+constexpr size_t sparse2_vbuf_bytes() { return (size_t)W * 2 * kHalfVBufAlloc; }
+
+struct Chunk2 {
+  int cn;
+  uint32_t a0[2];
+  int np[2];
+};
+
+template <class T, int W>
+__global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGroupArg g) {
+  constexpr int C = kChunk;
+  extern __shared__ __align__(16) unsigned char dsm[];
+  __shared__ u32x2 lut[16];
+  constexpr int WS = C + 2;                          // word row stride (see k_sparse_decode)
+  __shared__ __align__(16) uint32_t words[W][2][16 * WS];
+  const int ti = find_task(g.first, g.count);
+  const SparseTaskArg tk = g.t[ti];
+  const int M = g.M;
+  const int64_t K = tk.K;
+  const int64_t B = tile_blocks(tk.N);
+  const int64_t blk0 = 2 * ((int64_t)blockIdx.x - g.first[ti]);
+  const bool live1 = blk0 + 1 < B;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int S = (int)tile_steps(K);
+  int kbeg, kend;
+  wave_range<W>(S, wave, &kbeg, &kend);
+  unsigned char* vbuf[2] = {dsm + wave * 2 * kHalfVBufAlloc, dsm + wave * 2 * kHalfVBufAlloc + kHalfVBufAlloc};
+  const int64_t blkb[2] = {blk0, live1 ? blk0 + 1 : blk0};
+  const uint32_t* bmb[2] = {tk.bm + blkb[0] * S * 16, tk.bm + blkb[1] * S * 16};
+  const int32_t* tob[2] = {tk.toff + blkb[0] * S, tk.toff + blkb[1] * S};
+  const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(tk.values);
+
+  int ob = kbeg;
+  auto load_offsets = [&](int b, int base) {
+    const int t = base + lane < kend ? base + lane : kend;
+    return tob[b][t];
+  };
+  auto shape = [&](const int32_t (&o)[2], int c0) {
+    Chunk2 ch;
+    const int r = c0 - ob;                             // lane of tile c0 (r + C <= kOffsetLanes)
+    const int jmax = kend - c0 < C ? kend - c0 : C;
+    int cn = C;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      ch.a0[b] = (2u * (uint32_t)__builtin_amdgcn_readlane(o[b], r)) & ~15u;
+      const uint32_t lim = (ch.a0[b] + kHalfVBuf) >> 1;
+      const bool fit = lane >= r + 1 && lane <= r + jmax && (uint32_t)o[b] <= lim;
+      const int cb = __builtin_popcountll(__ballot(fit));   // >= 1: one tile is at most 1 KB
+      cn = cb < cn ? cb : cn;
+    }
+    ch.cn = cn;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const uint32_t end = (uint32_t)__builtin_amdgcn_readlane(o[b], r + cn);
+      ch.np[b] = (int)((2u * end - ch.a0[b] + 15u) >> 4);  // <= kHalfVBuf / 16
+    }
+    return ch;
+  };
+  u32x4 vp[2][kHalfPieceRounds];
+  uint32_t wv[2][C / 4];
+  auto issue = [&](const Chunk2& ch, int c0) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+#pragma unroll
+      for (int r = 0; r < kHalfPieceRounds; ++r) {
+        vp[b][r] = u32x4{0u, 0u, 0u, 0u};
+        const uint32_t off = ch.a0[b] + 16u * (uint32_t)(lane + kWave * r);
+        if (lane + kWave * r < ch.np[b]) vp[b][r] = *reinterpret_cast<const u32x4*>(vbytes + off);
+      }
+#pragma unroll
+      for (int i = 0; i < C / 4; ++i) {
+        wv[b][i] = 0u;
+        const uint32_t wi = (uint32_t)(c0 + fg + 4 * i) * 16u + (uint32_t)fr;
+        if (fg + 4 * i < ch.cn && (b == 0 || live1)) wv[b][i] = bmb[b][wi];
+      }
+    }
+  };
+
+  int32_t orng[2] = {0, 0};
+  Chunk2 ch{0, {0u, 0u}, {0, 0}};
+  if (kbeg < kend) {
+    orng[0] = load_offsets(0, ob);
+    orng[1] = load_offsets(1, ob);
+    ch = shape(orng, kbeg);
+    issue(ch, kbeg);
+  }
+  build_nibble_table(lut);
+  __syncthreads();
+
+  const XGlobal<1> xop(tk.X, M, K, fr, fg);
+  const uint32_t lut_addr = lds_off(lut);
+  const uint32_t vbuf_addr[2] = {lds_off(vbuf[0]), lds_off(vbuf[1])};
+  f32x4 acc[2][1] = {{f32x4{0.f, 0.f, 0.f, 0.f}}, {f32x4{0.f, 0.f, 0.f, 0.f}}};
+
+  for (int c0 = kbeg; c0 < kend;) {
+    // 1. stage the current chunk of both blocks
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+#pragma unroll
+      for (int r = 0; r < kHalfPieceRounds; ++r)
+        if (lane + kWave * r < ch.np[b]) *reinterpret_cast<u32x4*>(vbuf[b] + 16 * (lane + kWave * r)) = vp[b][r];
+#pragma unroll
+      for (int i = 0; i < C / 4; ++i) words[wave][b][fr * WS + fg + 4 * i] = wv[b][i];
+    }
+    wave_lds_sync();
+    const Chunk2 cur = ch;
+    int32_t tc[2][C];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int j = 0; j < C; ++j) tc[b][j] = __builtin_amdgcn_readlane(orng[b], c0 - ob + j);
+
+    // 2. the chunk's activations, then the next chunk's loads
+    u32x4 xb[C][1];
+#pragma unroll
+    for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cur.cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+    const int c1 = c0 + cur.cn;
+    if (c1 < kend) {
+      if (c1 - ob + C > kOffsetLanes) {
+        ob = c1;
+        orng[0] = load_offsets(0, ob);
+        orng[1] = load_offsets(1, ob);
+      }
+      ch = shape(orng, c1);
+      issue(ch, c1);
+    }
+
+    // 3. expand both blocks' tiles and multiply each with the shared activation operand
+    const uint32_t vrel[2] = {vbuf_addr[0] - cur.a0[0], vbuf_addr[1] - cur.a0[1]};
+#pragma unroll
+    for (int jp = 0; jp < C; jp += 2) {
+      if (jp < cur.cn) {
+        u32x2 wp[2];
+        uint32_t ex[2];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          wp[b] = *reinterpret_cast<const u32x2*>(&words[wave][b][fr * WS + jp]);
+          const uint32_t pc = __popc(__builtin_amdgcn_ubfe(wp[b].x, 8 * fg, 8)) |
+                              (__popc(__builtin_amdgcn_ubfe(wp[b].y, 8 * fg, 8)) << 16);
+          ex[b] = wave_inclusive_scan(pc) - pc;
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int j = jp + h;
+          if (j < cur.cn) {
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              const uint32_t wj = h ? wp[b].y : wp[b].x;
+              const uint32_t before = h ? ex[b] >> 16 : ex[b] & 0xffffu;
+              const uint32_t nlo = __builtin_amdgcn_ubfe(wj, 8 * fg, 4);
+              const uint32_t nhi = __builtin_amdgcn_ubfe(wj, 8 * fg + 4, 4);
+              const uint32_t oa = before + (uint32_t)tc[b][j];
+              const uint32_t obv = oa + __popc(nlo);
+              const uint32_t pa = 2u * oa + vrel[b], pb = 2u * obv + vrel[b];
+              const uint32_t da = pa & ~3u, db = pb & ~3u;
+              const uint32_t a_0 = lds_load4(da), a_1 = lds_load4(da + 4), a_2 = lds_load4(da + 8);
+              const uint32_t b_0 = lds_load4(db), b_1 = lds_load4(db + 4), b_2 = lds_load4(db + 8);
+              const uint32_t vlo = __builtin_amdgcn_alignbyte(a_1, a_0, pa);
+              const uint32_t vhi = __builtin_amdgcn_alignbyte(a_2, a_1, pa);
+              const uint32_t ulo = __builtin_amdgcn_alignbyte(b_1, b_0, pb);
+              const uint32_t uhi = __builtin_amdgcn_alignbyte(b_2, b_1, pb);
+              const u32x2 slo = lds_load8(lut_addr + 8u * nlo), shi = lds_load8(lut_addr + 8u * nhi);
+              u32x4 a;
+              a.x = __builtin_amdgcn_perm(vhi, vlo, slo.x);
+              a.y = __builtin_amdgcn_perm(vhi, vlo, slo.y);
+              a.z = __builtin_amdgcn_perm(uhi, ulo, shi.x);
+              a.w = __builtin_amdgcn_perm(uhi, ulo, shi.y);
+              acc[b][0] = Mfma16<T>::run(a, xb[j][0], acc[b][0]);
+            }
+          }
+        }
+      }
+    }
+    wave_lds_sync();
+    c0 = c1;
+  }
+  __syncthreads();                                     // every wave is done with its staging buffers
+  float* red = reinterpret_cast<float*>(dsm);
+  reduce_store<T, 1, W>(red, acc[0], M, blk0 * kDecRows, tk.N, tk.Y);
+  if (live1) {
+    __syncthreads();                                   // the first block's sums are read before red is reused
+    reduce_store<T, 1, W>(red, acc[1], M, (blk0 + 1) * kDecRows, tk.N, tk.Y);
+  }
+}
+
 template <class T, int MT, bool XL, int W>
 __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const DenseGroupArg g) {
   constexpr int C = kDenseChunk;
@@ -590,9 +790,26 @@ hipError_t sparse_group_w(const SparseGroupArg& g, int64_t kmax, hipStream_t s) 
   }
 }
 
+// Two row blocks per workgroup (direct activations, M <= 16): the same group
+// with each task's workgroups counted in pairs of row blocks.
+template <class T, int W>
+hipError_t sparse_pair_launch(const SparseGroupArg& g1, hipStream_t s) {
+  SparseGroupArg g = g1;
+  for (int i = 0; i < g.count; ++i)
+    g.first[i + 1] = g.first[i] + (int32_t)((tile_blocks(g1.t[i].N) + 1) / 2);
+  auto* kernel = k_sparse_decode2<T, W>;
+  static const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>());
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(W * kWave), sparse2_vbuf_bytes<W>(), s, g);
+  return hipGetLastError();
+}
+
 template <class T>
 hipError_t sparse_group_t(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
-  return small_grid(g.first[g.count]) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);
+  const int64_t blocks = g.first[g.count];
+  // direct activations of up to 16 rows: pairs of row blocks when the pairs still fill the chip
+  if (variant(g.M, kmax, kXLdsMaxSparse) == 1 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);
+  return small_grid(blocks) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);
 }
 
 template <class T, int W>

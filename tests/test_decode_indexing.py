@@ -31,7 +31,7 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
 
 def _constants():
     src = open(SRC).read()
-    assert "return small_grid(g.first[g.count]) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);" \
+    assert "return small_grid(blocks) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);" \
         in src, "waves per workgroup changed: update this replay"
     waves = (8, 16)
     chunk = int(re.search(r"constexpr int kChunk = (\d+);", src).group(1))
@@ -191,3 +191,67 @@ def test_lane_expansion_matches_dense_rows(orc, N, K, s):
                             seg = dense[n, k0:min(k0 + 8, K)]
                             exp[:seg.size] = seg
                         assert np.array_equal(got, exp), (b, c0 + j, lane)
+
+
+# ---------------------------------------------------------------- two row blocks per workgroup
+
+def _pair_constants():
+    src = open(SRC).read()
+    vbuf = int(re.search(r"constexpr int kVBuf = (\d+);", src).group(1))
+    assert "constexpr int kHalfVBuf = kVBuf / 2;" in src and "constexpr int kHalfVBufAlloc = kHalfVBuf + 16;" in src
+    assert "constexpr int kHalfPieceRounds = (kHalfVBuf / 16 + kWave - 1) / kWave;" in src
+    assert "const uint32_t lim = (ch.a0[b] + kHalfVBuf) >> 1;" in src and "cn = cb < cn ? cb : cn;" in src, \
+        "pair chunk rule changed: update this replay"
+    assert "if (variant(g.M, kmax, kXLdsMaxSparse) == 1 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);" \
+        in src, "pair launch rule changed: update this replay"
+    half = vbuf // 2
+    return half, half + 16, -(-(half // 16) // 64)
+
+
+def _pair_chunks(tobs, kbeg, kend, C, half):
+    """Chunks of the pair kernel: per block a 64-lane offsets window (reloaded
+    together) and half the buffer; the chunk is the shorter of the two fits."""
+    out, c0, ob = [], kbeg, kbeg
+    while c0 < kend:
+        if c0 - ob + C > 63:
+            ob = c0
+        r = c0 - ob
+        assert r + C <= 63
+        tos = [[int(t[min(ob + r + j, kend)]) for j in range(C + 1)] for t in tobs]
+        jmax = min(kend - c0, C)
+        cn, a0s = C, []
+        for to in tos:
+            a0 = (2 * to[0]) & ~15
+            lim = (a0 + half) >> 1
+            cb = sum(1 for j in range(1, C + 1) if j <= jmax and to[j] <= lim)
+            assert cb >= 1
+            cn, a0s = min(cn, cb), a0s + [a0]
+        nps = [(2 * to[cn] - a0 + 15) >> 4 for to, a0 in zip(tos, a0s)]
+        out.append((c0, cn, a0s, nps, tos))
+        c0 += cn
+    return out
+
+
+@pytest.mark.parametrize("N,K,s", [(16, 1056, 0.5), (48, 1056, 0.7), (40, 3296, 0.0), (17, 11008, 0.5),
+                                   (33, 4096, 0.9), (16, 65552, 0.7)])
+def test_pair_schedule_stays_in_bounds(orc, N, K, s):
+    half, alloc, rounds = _pair_constants()
+    C = _constants()[1][1]
+    W, mask = synth.weight(61 + N, N, K, "bf16", s)
+    T = orc.pack_tiled(W, "bf16", mask)
+    S, B = -(-K // 32), -(-N // 16)
+    value_bytes = -(-2 * T.nnz // 16) * 16 + 16
+    for p in range(-(-B // 2)):
+        blocks = (2 * p, 2 * p + 1 if 2 * p + 1 < B else 2 * p)           # a missing second block aliases the first
+        tobs = [T.tile_offsets[b * S:(b + 1) * S + 1] for b in blocks]
+        covered = np.zeros(S, dtype=np.int64)
+        for w in range(8):
+            kbeg, kend = _wave_range(S, 8, w)
+            for c0, cn, a0s, nps, tos in _pair_chunks(tobs, kbeg, kend, C, half):
+                covered[c0:c0 + cn] += 1
+                for a0, np_, to in zip(a0s, nps, tos):
+                    assert np_ <= half // 16 and np_ <= 64 * rounds       # pieces fit the rounds of loads
+                    assert a0 + 16 * np_ <= value_bytes                   # global value reads
+                    for j in range(cn):
+                        assert 2 * to[j + 1] - a0 + 12 <= alloc          # windows stay in the block's half
+        assert (covered == 1).all(), p

@@ -208,3 +208,24 @@ def test_decode_long_rows(orc, spl, s):
     for M in (1, 5, 17):
         Y = spl.sparse_linear(Xd[:M].contiguous(), Wc, algo="decode")
         assert_close(from_dev_f64(Y), ref[:M], f"long rows s={s} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,M", [(8200, 1056, 16), (8200, 3296, 5), (8192, 2112, 9)])
+def test_decode_row_block_pairs(orc, spl, dtype, N, K, M):
+    """Launches of at least 512 row blocks whose activations are loaded directly
+    (M x K too large to stage in LDS) run two row blocks per workgroup: an
+    odd row-block count (8200 rows = 512 blocks + a ragged 8-row block, the
+    last pair half empty) and an even one, compared in full with the oracle,
+    and as one task of a group with a smaller matrix."""
+    W, mask = synth.weight(950 + M, N, K, dtype, 0.7)
+    X = synth.activations(951, M, K, dtype)
+    ref = orc.linear_f64(X, orc.pack(W, dtype, mask))
+    Xd, Wc = to_dev(X, dtype), _pack(spl, W, mask, dtype)
+    Y = spl.sparse_linear(Xd, Wc, algo="decode")
+    assert_close(from_dev_f64(Y), ref, f"pairs {dtype} N={N} K={K} M={M}")
+    W2, mask2 = synth.weight(952, 40, K, dtype, 0.5)
+    ref2 = orc.linear_f64(X, orc.pack(W2, dtype, mask2))
+    Y1, Y2 = spl.sparse_linear_group([Xd, Xd], [Wc, _pack(spl, W2, mask2, dtype)], algo="decode")
+    assert_close(from_dev_f64(Y1), ref, f"pairs group task 0 {dtype} N={N} K={K} M={M}")
+    assert_close(from_dev_f64(Y2), ref2, f"pairs group task 1 {dtype} N=40 K={K} M={M}")
