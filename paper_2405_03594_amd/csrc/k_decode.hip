@@ -290,7 +290,6 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   int kbeg, kend;
   wave_range<W>(S, wave, &kbeg, &kend);
   unsigned char* vbuf = dsm + wave * kVBufAlloc;
-  const uint32_t* vbuf32 = reinterpret_cast<const uint32_t*>(vbuf);
   uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + sparse_vbuf_bytes<W>());
   const uint32_t* bmb = tk.bm + blk * S * 16;         // this row block's tiles, 16 words each
   const int32_t* tob = tk.toff + blk * S;             // S + 1 entries (the next block's first = this end)
