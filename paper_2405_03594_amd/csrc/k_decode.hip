@@ -58,6 +58,7 @@ constexpr int kDenseChunk = 4;              // dense: tiles per chunk
 constexpr int kVBuf = 3072;                 // staged value bytes per wave and chunk
 constexpr int kVBufAlloc = kVBuf + 16;      // + room for the last 8-byte window's third dword
 constexpr int kPieceRounds = kVBuf / 16 / kWave;
+static_assert(kPieceRounds * kWave * 16 == kVBuf, "every round of 16-byte pieces is staged unconditionally");
 constexpr int kOffsetLanes = kWave - 1;      // tiles whose offsets one load covers (lane i: tile base + i)
 // Activations are staged in LDS when every task's M * 32S * 2 bytes fit this
 // budget (32 KB): a sparse workgroup then needs at most ~61 KB of LDS (3 KB
@@ -321,19 +322,23 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   };
   u32x4 vp[kPieceRounds];
   uint32_t wv[C / 4];
+  // Unconditional loads: a piece past the chunk's np reloads piece 0 of the
+  // chunk, a tile past the range reloads the range's last tile; what they
+  // bring is staged but never read (the expansion selects only kept values of
+  // the chunk's tiles).  32-bit byte offsets from wave-uniform bases (values
+  // < 2^32 bytes: nnz < 2^31 of 2 bytes; bitmask < 2^32 bytes per matrix).
   auto issue = [&](const Chunk& ch, int c0) {
-    // 32-bit offsets from wave-uniform bases (values < 2^32 bytes: nnz < 2^31 of 2 bytes)
 #pragma unroll
     for (int r = 0; r < kPieceRounds; ++r) {
-      vp[r] = u32x4{0u, 0u, 0u, 0u};
-      const uint32_t off = ch.a0 + 16u * (uint32_t)(lane + kWave * r);
-      if (lane + kWave * r < ch.np) vp[r] = *reinterpret_cast<const u32x4*>(vbytes + off);
+      const uint32_t piece = (uint32_t)(lane + kWave * r);
+      const uint32_t off = ch.a0 + (piece < (uint32_t)ch.np ? 16u * piece : 0u);
+      vp[r] = *reinterpret_cast<const u32x4*>(vbytes + off);
     }
 #pragma unroll
     for (int i = 0; i < C / 4; ++i) {
-      wv[i] = 0u;
-      const uint32_t wi = (uint32_t)(c0 + fg + 4 * i) * 16u + (uint32_t)fr;
-      if (fg + 4 * i < ch.cn) wv[i] = bmb[wi];
+      const int t = c0 + fg + 4 * i < kend ? c0 + fg + 4 * i : kend - 1;
+      const uint32_t wb = 4u * ((uint32_t)t * 16u + (uint32_t)fr);
+      wv[i] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const unsigned char*>(bmb) + wb);
     }
   };
 
@@ -368,8 +373,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   for (int c0 = kbeg; c0 < kend;) {
     // 1. stage the current chunk: values into the buffer, words regrouped by row
 #pragma unroll
-    for (int r = 0; r < kPieceRounds; ++r)
-      if (lane + kWave * r < ch.np) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
+    for (int r = 0; r < kPieceRounds; ++r) *reinterpret_cast<u32x4*>(vbuf + 16 * (lane + kWave * r)) = vp[r];
 #pragma unroll
     for (int i = 0; i < C / 4; ++i) wl[fr * WS + fg + 4 * i] = wv[i];
     wave_lds_sync();
