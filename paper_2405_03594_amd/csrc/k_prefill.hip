@@ -114,25 +114,38 @@ __device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf) {
 }
 
 // One stage of MFMA work: wave (wn, wm) multiplies its 16 FN x 64 block over
-// the stage's two k-steps from the A (W) and B (X) buffers.
+// the stage's two k-steps from the A (W) and B (X) buffers.  Both k-steps'
+// fragments are read up front; the scheduling hints issue the first k-step's
+// reads, then put one second-k-step read after each of the first MFMAs, so
+// the LDS reads overlap the matrix cores instead of waiting ahead of them.
 template <class T, int FN>
 __device__ __forceinline__ void pf_mfma_stage(f32x4 (&acc)[FN][4], uint32_t abuf, uint32_t bbuf, int wn, int wm,
                                               int fr, int fg) {
   // fragment rows differ by multiples of 16, so every row a lane reads has row % 8 == fr % 8
+  u32x4 a[2][FN], b[2][4];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     const uint32_t a0 = abuf + pf_chunk(wn * 16 * FN + fr, 4 * ks + fg);
     const uint32_t b0 = bbuf + pf_chunk(wm * 64 + fr, 4 * ks + fg);
-    u32x4 a[FN], b[4];
 #pragma unroll
-    for (int i = 0; i < FN; ++i) a[i] = lds_load16(a0 + 16 * kPfRow * i);
+    for (int i = 0; i < FN; ++i) a[ks][i] = lds_load16(a0 + 16 * kPfRow * i);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = lds_load16(b0 + 16 * kPfRow * j);
+    for (int j = 0; j < 4; ++j) b[ks][j] = lds_load16(b0 + 16 * kPfRow * j);
+  }
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int i = 0; i < FN; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = MfmaP<T>::run(a[i], b[j], acc[i][j]);
+      for (int j = 0; j < 4; ++j) acc[i][j] = MfmaP<T>::run(a[ks][i], b[ks][j], acc[i][j]);
+  // masks: 0x100 LDS read, 0x008 MFMA
+  __builtin_amdgcn_sched_group_barrier(0x100, FN + 4, 0);
+#pragma unroll
+  for (int q = 0; q < FN + 4; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
+  __builtin_amdgcn_sched_group_barrier(0x008, 8 * FN - (FN + 4), 0);
 }
 
 // D layout: lane l, register r -> row (n) 4 (l / 16) + r, column (m) l % 16.
@@ -215,17 +228,23 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
   };
   auto fetch_windows = [&](TileWindows<TW>& tv, const TileWords<TW>& tw) {
 #pragma unroll
-    for (int i = 0; i < TW; ++i) {
-      const uint32_t w = tw.w[i];
-      const uint32_t byte = __builtin_amdgcn_ubfe(w, 8 * fg, 8);
+    for (int i = 0; i < TW; i += 2) {
       // values stored before mine: a tile's values are ordered by column group (fg), then row (fr),
-      // i.e. in lane order, so this is the exclusive wave scan of the lanes' kept counts
-      const uint32_t pc = __popc(byte);
-      const uint32_t oa = (uint32_t)tw.off[i] + wave_inclusive_scan(pc) - pc;
-      const uint32_t ob = oa + __popc(byte & 0xfu);
-      tv.byte[i] = byte;
-      __builtin_memcpy(&tv.v0[i], vbytes + 2u * oa, 8);
-      __builtin_memcpy(&tv.v1[i], vbytes + 2u * ob, 8);
+      // i.e. in lane order, so this is the exclusive wave scan of the lanes' kept counts; the
+      // pair of tiles shares one scan in 16-bit halves (sums <= 512)
+      const uint32_t b0 = __builtin_amdgcn_ubfe(tw.w[i], 8 * fg, 8);
+      const uint32_t b1 = __builtin_amdgcn_ubfe(tw.w[i + 1], 8 * fg, 8);
+      const uint32_t pc = __popc(b0) | (__popc(b1) << 16);
+      const uint32_t ex = wave_inclusive_scan(pc) - pc;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t byte = h ? b1 : b0;
+        const uint32_t oa = (uint32_t)tw.off[i + h] + (h ? ex >> 16 : ex & 0xffffu);
+        const uint32_t ob = oa + __popc(byte & 0xfu);
+        tv.byte[i + h] = byte;
+        __builtin_memcpy(&tv.v0[i + h], vbytes + 2u * oa, 8);
+        __builtin_memcpy(&tv.v1[i + h], vbytes + 2u * ob, 8);
+      }
     }
   };
   auto expand_store = [&](const TileWindows<TW>& tv, uint32_t buf) {

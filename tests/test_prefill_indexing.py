@@ -1,0 +1,154 @@
+"""Host-side replay of the sparse prefill kernel's indexing (no GPU).
+
+A workgroup of NW waves owns BN output rows (BN/16 row blocks) and walks K
+in stages of two 32-column k-steps.  At every stage each wave expands TW
+tiles: tile i is row block (TW/2) wave + i/2 of the workgroup, k-step
+2 st + i % 2.  Lane (fr, fg) reads the tile's bitmask word of row fr, the
+pair of tiles shares one exclusive wave scan of the lanes' kept counts (in
+16-bit halves), and the lane loads two 8-byte value windows (unaligned) at
+the first value of each of its nibbles.
+
+This test replays that schedule with the constants read from the kernel
+source and real encodings from the oracle, and checks that
+
+  * every tile is expanded exactly once per workgroup, and tiles past the
+    matrix (row blocks >= B, k-steps >= S) read tile 0's offset and a zero
+    word;
+  * every window lies inside the values buffer the interface guarantees
+    (the payloads plus a 16-byte readable tail);
+  * every expanded 16-byte chunk lands inside the workgroup's A buffer, in
+    a distinct slot;
+  * the expanded chunk (selector table + v_perm_b32) equals the dense
+    masked row segment."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                   "paper_2405_03594_amd", "csrc", "k_prefill.hip")
+
+
+def _constants():
+    src = open(SRC).read()
+    bk = int(re.search(r"constexpr int kPfBK = (\d+);", src).group(1))
+    assert "constexpr int kPfRow = kPfBK * 2;" in src
+    for line in ("constexpr int TW = BN / 8 / NW;",
+                 "const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);",
+                 "const int s = 2 * st + (i & 1);",
+                 "const int64_t t = ok ? b * S + s : 0;",
+                 "tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;",
+                 "const uint32_t pc = __popc(b0) | (__popc(b1) << 16);",
+                 "const uint32_t oa = (uint32_t)tw.off[i + h] + (h ? ex >> 16 : ex & 0xffffu);",
+                 "const uint32_t ob = oa + __popc(byte & 0xfu);",
+                 "__builtin_memcpy(&tv.v0[i + h], vbytes + 2u * oa, 8);",
+                 "__builtin_memcpy(&tv.v1[i + h], vbytes + 2u * ob, 8);",
+                 "const uint32_t at = buf + pf_chunk(16 * ((TW / 2) * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);",
+                 "? sparse_prefill_tile<T, 128, 256, 8>(X, M, Wc, Y, s)",
+                 ": sparse_prefill_tile<T, 64, 128, 4>(X, M, Wc, Y, s);"):
+        assert line in src, f"kernel changed: update this replay ({line})"
+    return bk, [(128, 8), (64, 4)]                      # (BN, NW) of the two workgroup shapes
+
+
+def _popc(x):
+    return bin(int(x) & 0xFFFFFFFF).count("1")
+
+
+def _nibble_selector(nib, h):
+    sel = 0
+    for e in range(2):
+        j = 2 * h + e
+        s16 = 0x0C0C
+        if (nib >> j) & 1:
+            r = _popc(nib & ((1 << j) - 1))
+            s16 = (2 * r) | ((2 * r + 1) << 8)
+        sel |= s16 << (16 * e)
+    return sel
+
+
+def _perm(s0, s1, sel):
+    src = int(s1).to_bytes(4, "little") + int(s0).to_bytes(4, "little")
+    out = 0
+    for j in range(4):
+        b = (sel >> (8 * j)) & 0xFF
+        assert b < 8 or b == 12
+        out |= (src[b] if b < 8 else 0) << (8 * j)
+    return out
+
+
+def _chunk(r, c, row_bytes):
+    return r * row_bytes + 16 * (c ^ (r & 7))
+
+
+@pytest.mark.parametrize("N,K,s", [(16, 32, 0.5), (48, 200, 0.7), (300, 96, 0.0), (33, 264, 1.0), (130, 520, 0.9)])
+def test_prefill_schedule_and_expansion(orc, N, K, s):
+    bk, shapes = _constants()
+    row_bytes = 2 * bk
+    W, mask = synth.weight(57 + N + K, N, K, "bf16", s)
+    T = orc.pack_tiled(W, "bf16", mask)
+    vbytes = np.concatenate([T.values.view(np.uint8), np.zeros(16, np.uint8)])   # the readable tail
+    limit = 2 * T.nnz + 16
+    dense = np.where(mask.astype(bool), W.view(np.uint16), 0).astype(np.uint16)
+    S, B = -(-K // 32), -(-N // 16)
+    nst = (S + 1) // 2
+    bm = T.bitmask.reshape(-1).astype(np.uint64)
+    offs = T.tile_offsets.astype(np.int64)
+    for BN, NW in shapes:
+        TW = BN // 8 // NW
+        assert TW % 2 == 0
+        for wg in range(-(-N // BN)):
+            nb0 = wg * BN // 16
+            for st in range(nst):
+                seen = {}
+                for wave in range(NW):
+                    for i in range(0, TW, 2):
+                        tiles = []
+                        for h in range(2):
+                            b = nb0 + (TW // 2) * wave + ((i + h) >> 1)
+                            sk = 2 * st + ((i + h) & 1)
+                            ok = b < B and sk < S
+                            t = b * S + sk if ok else 0
+                            words = [int(bm[t * 16 + r]) if ok else 0 for r in range(16)]
+                            tiles.append((b, sk, ok, int(offs[t]), words))
+                            if ok:
+                                assert (b, sk) not in seen, "tile expanded twice"
+                                seen[(b, sk)] = True
+                        # the pair's scan: counts in lane order (fg-major, fr within), 16-bit halves
+                        cnt = np.array([[_popc((tiles[h][4][l & 15] >> (8 * (l >> 4))) & 0xFF) for l in range(64)]
+                                        for h in range(2)])
+                        packed = cnt[0] | (cnt[1] << 16)
+                        ex = np.cumsum(packed) - packed
+                        assert (np.cumsum(cnt, axis=1) <= 512).all()
+                        for h in range(2):
+                            b, sk, ok, off, words = tiles[h]
+                            for lane in range(64):
+                                fr, fg = lane & 15, lane >> 4
+                                byte = (words[fr] >> (8 * fg)) & 0xFF
+                                e = int(ex[lane] >> 16) if h else int(ex[lane] & 0xFFFF)
+                                oa = off + e
+                                ob = oa + _popc(byte & 0xF)
+                                for o in (oa, ob):
+                                    assert 0 <= 2 * o and 2 * o + 8 <= limit, (wg, st, wave, i + h, lane)
+                                at = _chunk(16 * ((TW // 2) * wave + ((i + h) >> 1)) + fr, 4 * ((i + h) & 1) + fg,
+                                            row_bytes)
+                                assert 0 <= at and at + 16 <= BN * row_bytes
+                                v0 = vbytes[2 * oa:2 * oa + 8].view(np.uint32)
+                                v1 = vbytes[2 * ob:2 * ob + 8].view(np.uint32)
+                                lo, hi = byte & 0xF, byte >> 4
+                                got = [_perm(v0[1], v0[0], _nibble_selector(lo, 0)),
+                                       _perm(v0[1], v0[0], _nibble_selector(lo, 1)),
+                                       _perm(v1[1], v1[0], _nibble_selector(hi, 0)),
+                                       _perm(v1[1], v1[0], _nibble_selector(hi, 1))]
+                                got = np.array(got, dtype=np.uint32).view(np.uint16)
+                                exp = np.zeros(8, np.uint16)
+                                n, k0 = 16 * b + fr, 32 * sk + 8 * fg
+                                if ok and n < N and k0 < K:
+                                    seg = dense[n, k0:min(k0 + 8, K)]
+                                    exp[:seg.size] = seg
+                                assert np.array_equal(got, exp), (wg, st, wave, i + h, lane)
+                # the workgroup's row blocks inside the matrix, both k-steps of the stage, each once
+                want = {(b, sk) for b in range(nb0, min(nb0 + BN // 16, B)) for sk in (2 * st, 2 * st + 1) if sk < S}
+                assert set(seen) == want
