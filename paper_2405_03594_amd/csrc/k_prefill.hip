@@ -68,9 +68,10 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
 
 // Rows [r0, r0 + RR P) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
 // moved through registers by a workgroup of 8 RR threads: thread t holds rows
-// r0 + t/8 + RR i (i < P), columns k0 + 8 (t % 8) .. +8; rows past R and
-// columns past K read as zeros (K % 8 == 0, so a 16-byte piece is wholly
-// inside or outside).
+// r0 + t/8 + RR i (i < P), columns k0 + 8 (t % 8) .. +8.  Checked fetches
+// read rows past R and columns past K as zeros (K % 8 == 0, so a 16-byte
+// piece is wholly inside or outside); unchecked ones are for launches whose
+// blocks and stages all lie inside the matrix, and load without branches.
 template <int P>
 struct Slab {
   u32x4 v[P];
@@ -90,13 +91,18 @@ struct SlabSrc {
     row0 = A + (r < R ? r : 0) * K + col;
     stride = RR * K;
   }
-  template <int P>
+  template <bool kChecked, int P>
   __device__ __forceinline__ void fetch(Slab<P>& sl, int64_t K, int64_t k0) const {
-    const bool kok = k0 + col < K;
+    if constexpr (kChecked) {
+      const bool kok = k0 + col < K;
 #pragma unroll
-    for (int i = 0; i < P; ++i) {
-      sl.v[i] = u32x4{0u, 0u, 0u, 0u};
-      if (kok && RR * i < rows_left) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
+      for (int i = 0; i < P; ++i) {
+        sl.v[i] = u32x4{0u, 0u, 0u, 0u};
+        if (kok && RR * i < rows_left) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < P; ++i) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);
     }
   }
 };
@@ -187,7 +193,7 @@ struct TileWindows {
   u32x2 v0[TW], v1[TW];   // 8-byte windows from the first value of each nibble
 };
 
-template <class T, int BN, int BM, int NW>
+template <class T, int BN, int BM, int NW, bool kChecked>
 __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
                                                                   const uint32_t* __restrict__ bm_tiles,
                                                                   const uint16_t* __restrict__ values,
@@ -220,10 +226,16 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
     for (int i = 0; i < TW; ++i) {
       const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);
       const int s = 2 * st + (i & 1);
-      const bool ok = b < B && s < S;
-      const int64_t t = ok ? b * S + s : 0;
-      tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;
-      tw.off[i] = tile_offsets[t];
+      if constexpr (kChecked) {
+        const bool ok = b < B && s < S;
+        const int64_t t = ok ? b * S + s : 0;
+        tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;
+        tw.off[i] = tile_offsets[t];
+      } else {                                       // N % BN == 0 and S even: always inside
+        const int64_t t = b * S + s;
+        tw.w[i] = bm_tiles[t * 16 + fr];
+        tw.off[i] = tile_offsets[t];
+      }
     }
   };
   auto fetch_windows = [&](TileWindows<TW>& tv, const TileWords<TW>& tw) {
@@ -279,11 +291,11 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
   TileWords<TW> tw;
   TileWindows<TW> tv;
   fetch_words(tw, 0);
-  xsrc.fetch(x0, K, 0);
+  xsrc.template fetch<kChecked>(x0, K, 0);
   fetch_windows(tv, tw);                               // stage 0
   if (nst > 1) {
     fetch_words(tw, 1);
-    xsrc.fetch(x1, K, kPfBK);
+    xsrc.template fetch<kChecked>(x1, K, kPfBK);
   }
   __syncthreads();                                     // the selector table
   expand_store(tv, abuf[0]);
@@ -302,7 +314,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
       if (st + 2 < nst) {
         fetch_windows(tv, tw);                         // stage st + 2 (its words were fetched a stage ago)
         if (st + 3 < nst) fetch_words(tw, st + 3);
-        xsrc.fetch(xn, K, (int64_t)kPfBK * (st + 2));
+        xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (st + 2));
       }
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
@@ -315,7 +327,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
   pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
-template <class T, int BN, int BM, int NW>
+template <class T, int BN, int BM, int NW, bool kChecked>
 __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
                                                                  const uint16_t* __restrict__ W, int64_t N,
                                                                  uint16_t* __restrict__ Y) {
@@ -347,11 +359,11 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
   const SlabSrc<RR> xsrc(X, M, K, m0), wsrc(W, N, K, n0);
   Slab<BM / RR> x0, x1;
   Slab<BN / RR> w0, w1;
-  xsrc.fetch(x0, K, 0);
-  wsrc.fetch(w0, K, 0);
+  xsrc.template fetch<kChecked>(x0, K, 0);
+  wsrc.template fetch<kChecked>(w0, K, 0);
   if (nst > 1) {
-    xsrc.fetch(x1, K, kPfBK);
-    wsrc.fetch(w1, K, kPfBK);
+    xsrc.template fetch<kChecked>(x1, K, kPfBK);
+    wsrc.template fetch<kChecked>(w1, K, kPfBK);
   }
   slab_store<RR>(w0, abuf[0]);
   slab_store<RR>(x0, bbuf[0]);
@@ -367,8 +379,8 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
       slab_store<RR>(xl, bbuf[cur ^ 1]);
     }
     if (st + 2 < nst) {
-      xsrc.fetch(xn, K, (int64_t)kPfBK * (st + 2));
-      wsrc.fetch(wn_, K, (int64_t)kPfBK * (st + 2));
+      xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (st + 2));
+      wsrc.template fetch<kChecked>(wn_, K, (int64_t)kPfBK * (st + 2));
     }
     pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (st + 1 < nst) __syncthreads();
@@ -399,15 +411,26 @@ bool pf_large_tile(int64_t N, int64_t M) {
   return ((N + 127) / 128) * ((M + 255) / 256) >= (int64_t)cus;
 }
 
-template <class T, int BN, int BM, int NW>
-hipError_t sparse_prefill_tile(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T, BN, BM, NW>, pf_lds(BN, BM));
+// Blocks and stages all inside the matrix: the unchecked (branch-free) loads apply.
+constexpr bool pf_inside(int64_t N, int64_t M, int64_t K, int BN, int BM) {
+  return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;
+}
+
+template <class T, int BN, int BM, int NW, bool kChecked>
+hipError_t sparse_prefill_launch(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T, BN, BM, NW, kChecked>, pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
   const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW);
-  hipLaunchKernelGGL((k_sparse_prefill<T, BN, BM, NW>), grid, block, pf_lds(BN, BM), s,
+  hipLaunchKernelGGL((k_sparse_prefill<T, BN, BM, NW, kChecked>), grid, block, pf_lds(BN, BM), s,
                      static_cast<const uint16_t*>(X), M, Wc.cols, Wc.bitmask, static_cast<const uint16_t*>(Wc.values),
                      Wc.tile_offsets, Wc.rows, static_cast<uint16_t*>(Y));
   return hipGetLastError();
+}
+
+template <class T, int BN, int BM, int NW>
+hipError_t sparse_prefill_tile(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+  return pf_inside(Wc.rows, M, Wc.cols, BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, false>(X, M, Wc, Y, s)
+                                                : sparse_prefill_launch<T, BN, BM, NW, true>(X, M, Wc, Y, s);
 }
 
 template <class T>
@@ -417,15 +440,22 @@ hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void
                                     : sparse_prefill_tile<T, 64, 128, 4>(X, M, Wc, Y, s);
 }
 
-template <class T, int BN, int BM, int NW>
-hipError_t dense_prefill_tile(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T, BN, BM, NW>, pf_lds(BN, BM));
+template <class T, int BN, int BM, int NW, bool kChecked>
+hipError_t dense_prefill_launch(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y,
+                                hipStream_t s) {
+  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T, BN, BM, NW, kChecked>, pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
   const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW);
-  hipLaunchKernelGGL((k_dense_prefill<T, BN, BM, NW>), grid, block, pf_lds(BN, BM), s,
+  hipLaunchKernelGGL((k_dense_prefill<T, BN, BM, NW, kChecked>), grid, block, pf_lds(BN, BM), s,
                      static_cast<const uint16_t*>(X), M, K, static_cast<const uint16_t*>(W), N,
                      static_cast<uint16_t*>(Y));
   return hipGetLastError();
+}
+
+template <class T, int BN, int BM, int NW>
+hipError_t dense_prefill_tile(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
+  return pf_inside(N, M, K, BN, BM) ? dense_prefill_launch<T, BN, BM, NW, false>(X, M, W, N, K, Y, s)
+                                    : dense_prefill_launch<T, BN, BM, NW, true>(X, M, W, N, K, Y, s);
 }
 
 template <class T>

@@ -167,3 +167,19 @@ def test_prefill_large_grid_ragged(orc, spl, dtype):
     Wm = np.where(mask.astype(bool), W, np.zeros_like(W))
     Yd = spl.dense_linear(Xd, to_dev(Wm, dtype), algo="prefill")
     assert_close(from_dev_f64(Yd), ref, f"dense prefill {dtype} N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("N,K,M", [(2048, 128, 8192), (256, 192, 256)])
+def test_prefill_aligned_grids(orc, spl, N, K, M):
+    """Launches whose blocks and stages all lie inside the matrix take the
+    unchecked (branch-free) kernels: a 128 x 256 grid with two blocks per CU
+    and a 64 x 128 grid, compared in full, sparse and dense."""
+    W, mask = synth.weight(940 + N, N, K, "bf16", 0.7)
+    X = synth.activations(941 + K, M, K, "bf16")
+    ref = orc.linear_f64(X, orc.pack(W, "bf16", mask))
+    Xd = to_dev(X, "bf16")
+    Y = spl.sparse_linear(Xd, _pack(spl, W, mask, "bf16"), algo="prefill")
+    assert_close(from_dev_f64(Y), ref, f"prefill N={N} K={K} M={M}")
+    Wm = np.where(mask.astype(bool), W, np.zeros_like(W))
+    Yd = spl.dense_linear(Xd, to_dev(Wm, "bf16"), algo="prefill")
+    assert_close(from_dev_f64(Yd), ref, f"dense prefill N={N} K={K} M={M}")

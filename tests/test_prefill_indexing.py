@@ -152,3 +152,38 @@ def test_prefill_schedule_and_expansion(orc, N, K, s):
                 # the workgroup's row blocks inside the matrix, both k-steps of the stage, each once
                 want = {(b, sk) for b in range(nb0, min(nb0 + BN // 16, B)) for sk in (2 * st, 2 * st + 1) if sk < S}
                 assert set(seen) == want
+
+
+def _inside_rule():
+    src = open(SRC).read()
+    rule = "return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;"
+    assert rule in src, "launch rule for the unchecked kernels changed: update this replay"
+    for line in ("? sparse_prefill_launch<T, BN, BM, NW, false>(X, M, Wc, Y, s)",
+                 "? dense_prefill_launch<T, BN, BM, NW, false>(X, M, W, N, K, Y, s)",
+                 "const int64_t t = b * S + s;",
+                 "for (int i = 0; i < P; ++i) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);"):
+        assert line in src, f"kernel changed: update this replay ({line})"
+    return lambda N, M, K, BN, BM, bk: N % BN == 0 and M % BM == 0 and K % bk == 0
+
+
+@pytest.mark.parametrize("N,M,K", [(4096, 512, 4096), (11008, 2048, 4096), (4096, 2048, 11008), (128, 256, 64),
+                                   (64, 128, 128), (2000, 4100, 72), (130, 300, 1000)])
+def test_unchecked_loads_stay_inside(N, M, K):
+    """Launches the host sends to the unchecked kernels (every block and stage
+    inside the matrix) touch only valid tiles, rows and columns."""
+    bk, shapes = _constants()
+    inside = _inside_rule()
+    S, B = -(-K // 32), -(-N // 16)
+    nst = (S + 1) // 2
+    for BN, NW in shapes:
+        BM, RR, TW = 32 * NW, 8 * NW, BN // 8 // NW
+        if not inside(N, M, K, BN, BM, bk):
+            continue
+        # tiles: b = nb0 + (TW/2) wave + i/2 over every workgroup and wave, k-step 2 st + i % 2
+        bs = {wg * BN // 16 + (TW // 2) * w + i // 2 for wg in range(N // BN) for w in range(NW) for i in range(TW)}
+        assert max(bs) < B and 2 * (nst - 1) + 1 < S
+        # slabs: rows r0 + t/8 + RR i of BM (X) and BN (W) rows, columns k0 + 8 (t % 8) .. + 8 of every stage
+        for rows, R in ((BM, M), (BN, N)):
+            last = (R // rows - 1) * rows + (64 * NW - 1) // 8 + RR * (rows // RR - 1)
+            assert last < R
+        assert bk * (nst - 1) + 8 * 7 + 8 <= K
