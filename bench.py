@@ -283,6 +283,26 @@ def run_single(args):
                        "speedup_vs_dense": round(dn_gpu / sp_gpu, 3)}, dtype="f16")
 
 
+def _library_linear_ms(torch, pairs, reps: int) -> float:
+    """Cross-check of the dense comparator: torch.nn.functional.linear (the
+    vendor GEMM library) over the same (X, W) pairs, eager, timed with events
+    around `reps` passes; GPU ms per pass."""
+    import torch.nn.functional as F
+
+    for _ in range(2):
+        for x, w in pairs:
+            F.linear(x, w)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        for x, w in pairs:
+            F.linear(x, w)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
 def run_prefill(args):
     """One layer's seven matrices at M = 512 and 2048 (prefill kernels)."""
     torch, spl = _need_gpu()
@@ -317,6 +337,9 @@ def run_prefill(args):
             _, gd = _timed(uM, dense_fn, max(10, args.steps // 4), 2, [0])
             d.update({"dense_layer_us": round(gd * 1e3, 2), "dense_tflops": round(f / (gd * 1e-3) / 1e12, 1),
                       "speedup_vs_dense": round(gd / g, 3)})
+            gl = _library_linear_ms(torch, [(xsl[u], layers[0][u[1]][1]) for u in uM], max(10, args.steps // 4))
+            d.update({"library_dense_layer_us": round(gl * 1e3, 2),
+                      "library_dense_tflops": round(f / (gl * 1e-3) / 1e12, 1)})
         per_M[str(M)] = d
     cpu = None
     if not args.no_cpu_baseline:
