@@ -772,6 +772,8 @@ int variant(int64_t M, int64_t kmax, int64_t budget) {
   return M <= 16 ? 1 : 2;
 }
 
+
+
 // 16 waves per workgroup when the launch has fewer than two row blocks per CU.
 bool small_grid(int64_t blocks) {
   static int cus = [] {
@@ -784,9 +786,21 @@ bool small_grid(int64_t blocks) {
   return blocks < 2 * (int64_t)cus;
 }
 
+// Activation path of the sparse kernels.  One row: staged in LDS when it fits
+// (32 KB).  Two to 16 rows: staged only where the launch has two or more row
+// blocks per CU and the copy fits 16 KB (so that three workgroups still share
+// a CU); otherwise loaded directly, which fetches only the live rows.  Two row
+// blocks per workgroup (direct path) pay off above four rows.
+int sparse_variant(int64_t M, int64_t kmax, int64_t blocks) {
+  const int64_t xbytes = M * 32 * tile_steps(kmax) * 2;
+  if (M == 1 && xbytes <= kXLdsMaxSparse) return 0;
+  if (M > 1 && M <= 16 && xbytes <= kXLdsMaxSparse / 2 && !small_grid(blocks)) return 0;
+  return M <= 16 ? 1 : 2;
+}
+
 template <class T, int W>
 hipError_t sparse_group_w(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
-  switch (variant(g.M, kmax, kXLdsMaxSparse)) {
+  switch (sparse_variant(g.M, kmax, g.first[g.count])) {
     case 0: return sparse_group_launch<T, 1, true, W>(g, kmax, s);
     case 1: return sparse_group_launch<T, 1, false, W>(g, kmax, s);
     default: return sparse_group_launch<T, 2, false, W>(g, kmax, s);
@@ -811,7 +825,7 @@ template <class T>
 hipError_t sparse_group_t(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
   const int64_t blocks = g.first[g.count];
   // direct activations of up to 16 rows: pairs of row blocks when the pairs still fill the chip
-  if (variant(g.M, kmax, kXLdsMaxSparse) == 1 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);
+  if (sparse_variant(g.M, kmax, blocks) == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);
   return small_grid(blocks) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);
 }
 

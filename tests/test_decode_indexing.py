@@ -202,7 +202,7 @@ def _pair_constants():
     assert "constexpr int kHalfPieceRounds = (kHalfVBuf / 16 + kWave - 1) / kWave;" in src
     assert "const uint32_t lim = (ch.a0[b] + kHalfVBuf) >> 1;" in src and "cn = cb < cn ? cb : cn;" in src, \
         "pair chunk rule changed: update this replay"
-    assert "if (variant(g.M, kmax, kXLdsMaxSparse) == 1 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);" \
+    assert "if (sparse_variant(g.M, kmax, blocks) == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);" \
         in src, "pair launch rule changed: update this replay"
     half = vbuf // 2
     return half, half + 16, -(-(half // 16) // 64)
