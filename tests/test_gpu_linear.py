@@ -229,3 +229,15 @@ def test_decode_row_block_pairs(orc, spl, dtype, N, K, M):
     Y1, Y2 = spl.sparse_linear_group([Xd, Xd], [Wc, _pack(spl, W2, mask2, dtype)], algo="decode")
     assert_close(from_dev_f64(Y1), ref, f"pairs group task 0 {dtype} N={N} K={K} M={M}")
     assert_close(from_dev_f64(Y2), ref2, f"pairs group task 1 {dtype} N=40 K={K} M={M}")
+
+
+@pytest.mark.parametrize("N,K,M", [(8200, 1056, 2), (8192, 4096, 2), (8200, 3296, 3), (8192, 4096, 4)])
+def test_decode_large_grid_small_batches(orc, spl, N, K, M):
+    """Launches of at least 512 row blocks at batches 2-4: activations staged in
+    LDS while the copy fits 16 KB (2 x 1056, 2 x 4096), loaded directly by the
+    single-block kernel otherwise (3 x 3296, 4 x 4096), compared in full."""
+    W, mask = synth.weight(960 + M + K, N, K, "bf16", 0.7)
+    X = synth.activations(961, M, K, "bf16")
+    ref = orc.linear_f64(X, orc.pack(W, "bf16", mask))
+    Y = spl.sparse_linear(to_dev(X, "bf16"), _pack(spl, W, mask, "bf16"), algo="decode")
+    assert_close(from_dev_f64(Y), ref, f"large grid N={N} K={K} M={M}")
