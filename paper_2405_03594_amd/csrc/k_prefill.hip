@@ -4,7 +4,11 @@
 // BN (n) x BM (m) block of Y = X W^T: 128 x 256 with 8 waves for large grids,
 // 64 x 128 with 4 waves for launches that would leave CUs idle; wave
 // (wn, wm) owns BN/2 x 64 of it, BN/32 x 4 v_mfma_f32_16x16x32 fragments per
-// 32-column k-step.  K advances 64
+// 32-column k-step.  When even the small blocks leave at most one workgroup
+// per CU, KS = 2 groups of NW waves share a block: group h takes the h-th
+// contiguous half of the stages with its own LDS buffers, and group 1 hands its
+// partial sums to group 0 through LDS at the end (a fixed order of addition),
+// so each SIMD runs two waves instead of one.  K advances 64
 // columns per stage through two LDS buffers per operand: rows of 64
 // elements (128 bytes), the 16-byte chunk c of row r stored at chunk
 // c ^ (r % 8), so that eight consecutive rows' fragment reads (and the
@@ -67,7 +71,7 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
 }
 
 // Rows [r0, r0 + RR P) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
-// moved through registers by a workgroup of 8 RR threads: thread t holds rows
+// moved through registers by a group of 8 RR threads: thread t holds rows
 // r0 + t/8 + RR i (i < P), columns k0 + 8 (t % 8) .. +8.  Checked fetches
 // read rows past R and columns past K as zeros (K % 8 == 0, so a 16-byte
 // piece is wholly inside or outside); unchecked ones are for launches whose
@@ -84,9 +88,9 @@ struct SlabSrc {
   int rows_left;          // rows of the matrix from its first row on
   int col;                // its column offset 8 (t % 8)
 
-  __device__ __forceinline__ SlabSrc(const uint16_t* __restrict__ A, int64_t R, int64_t K, int64_t r0) {
-    const int64_t r = r0 + (threadIdx.x >> 3);
-    col = 8 * (threadIdx.x & 7);
+  __device__ __forceinline__ SlabSrc(const uint16_t* __restrict__ A, int64_t R, int64_t K, int64_t r0, int t) {
+    const int64_t r = r0 + (t >> 3);
+    col = 8 * (t & 7);
     rows_left = r < R ? (int)(R - r) : 0;
     row0 = A + (r < R ? r : 0) * K + col;
     stride = RR * K;
@@ -111,9 +115,9 @@ struct SlabSrc {
 __device__ __forceinline__ uint32_t pf_chunk(int r, int c) { return (uint32_t)(r * kPfRow + 16 * (c ^ (r & 7))); }
 
 template <int RR, int P>
-__device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf) {
+__device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf, int t) {
   // rows t/8 + RR i share their row % 8 with row t/8 (RR is a multiple of 8)
-  const uint32_t base = buf + pf_chunk(threadIdx.x >> 3, threadIdx.x & 7);
+  const uint32_t base = buf + pf_chunk(t >> 3, t & 7);
 #pragma unroll
   for (int i = 0; i < P; ++i)
     *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(base + RR * kPfRow * i)) = sl.v[i];
@@ -180,6 +184,34 @@ __device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][4], uint16_t* __
   }
 }
 
+// Split K: after every wave's last MFMA, k-group 1 hands its partial sums to
+// k-group 0 through the (then free) stage buffers; group 0 adds them (a fixed
+// order) and is the one that stores.  Returns whether this thread stores.
+template <int FN, int NT, int KS>
+__device__ __forceinline__ bool pf_combine(f32x4 (&acc)[FN][4], unsigned char* dsm, int kh, int t) {
+  if constexpr (KS == 1) {
+    return true;
+  } else {
+    static_assert(KS == 2, "two k-groups");
+    f32x4* part = reinterpret_cast<f32x4*>(dsm);     // [FN * 4][NT]
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part[(i * 4 + j) * NT + t] = acc[i][j];
+    }
+    __syncthreads();
+    if (kh == 0) {
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += part[(i * 4 + j) * NT + t];
+    }
+    return kh == 0;
+  }
+}
+
 // Compressed operands of a wave's TW tiles of one stage: tile i is row block
 // (TW/2) wave + i/2 of the workgroup's BN/16, k-step i % 2 of the stage.
 template <int TW>
@@ -193,30 +225,37 @@ struct TileWindows {
   u32x2 v0[TW], v1[TW];   // 8-byte windows from the first value of each nibble
 };
 
-template <class T, int BN, int BM, int NW, bool kChecked>
-__global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
-                                                                  const uint32_t* __restrict__ bm_tiles,
-                                                                  const uint16_t* __restrict__ values,
-                                                                  const int32_t* __restrict__ tile_offsets, int64_t N,
-                                                                  uint16_t* __restrict__ Y) {
+template <class T, int BN, int BM, int NW, int KS, bool kChecked>
+__global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
+    k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K, const uint32_t* __restrict__ bm_tiles,
+                     const uint16_t* __restrict__ values, const int32_t* __restrict__ tile_offsets, int64_t N,
+                     uint16_t* __restrict__ Y) {
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  constexpr int NT = 64 * NW;                        // threads of one k-group
+  const int kh = KS == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x / NT);
+  const int tid = (int)threadIdx.x - kh * NT;        // thread index within the k-group
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = threadIdx.x & 63;
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
   const int nst = (S + 1) / 2;
+  const int nh = (nst + KS - 1) / KS;                // stages per k-group (uniform: every group's barriers)
+  const int sb = kh * nh;                            // this group's first stage
+  const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;   // its stages (the last group may hold fewer)
   const int64_t B = tile_blocks(N);
   constexpr int FN = BN / 32;                        // n-fragments per wave
   constexpr int TW = BN / 8 / NW;                    // tiles per wave per stage (whole k-step pairs)
   constexpr int RR = 8 * NW;                         // rows per staging round
   static_assert(BM == 32 * NW && TW % 2 == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
+  static_assert(KS == 1 || FN * 4 * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   const int64_t nb0 = n0 / 16;
-  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
-  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + (2 * BN + BM) * kPfRow)};
+  unsigned char* gb = dsm + kh * pf_lds(BN, BM);     // this group's stage buffers
+  const uint32_t abuf[2] = {lds_off(gb), lds_off(gb + BN * kPfRow)};
+  const uint32_t bbuf[2] = {lds_off(gb + 2 * BN * kPfRow), lds_off(gb + (2 * BN + BM) * kPfRow)};
   const uint32_t lut_addr = lds_off(lut);
   const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
   if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{pf_nibble_selector(threadIdx.x, 0), pf_nibble_selector(threadIdx.x, 1)};
@@ -286,65 +325,79 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_sparse_prefill(const uint16
   // other LDS buffers and its X slab stored there (their last readers, stage
   // st - 1's MFMAs, finished before the previous barrier), so that this ALU
   // and LDS work can interleave with the matrix cores; one barrier per stage.
-  const SlabSrc<RR> xsrc(X, M, K, m0);
+  // Stages are counted within the k-group (global stage sb + st); data steps
+  // are guarded by the group's nl stages, barriers by the uniform nh.
+  const SlabSrc<RR> xsrc(X, M, K, m0, tid);
   Slab<BM / RR> x0, x1;
   TileWords<TW> tw;
   TileWindows<TW> tv;
-  fetch_words(tw, 0);
-  xsrc.template fetch<kChecked>(x0, K, 0);
-  fetch_windows(tv, tw);                               // stage 0
-  if (nst > 1) {
-    fetch_words(tw, 1);
-    xsrc.template fetch<kChecked>(x1, K, kPfBK);
+  if (nl > 0) {
+    fetch_words(tw, sb);
+    xsrc.template fetch<kChecked>(x0, K, (int64_t)kPfBK * sb);
+    fetch_windows(tv, tw);                             // stage 0
+    if (nl > 1) {
+      fetch_words(tw, sb + 1);
+      xsrc.template fetch<kChecked>(x1, K, (int64_t)kPfBK * (sb + 1));
+    }
   }
   __syncthreads();                                     // the selector table
-  expand_store(tv, abuf[0]);
-  slab_store<RR>(x0, bbuf[0]);
-  if (nst > 1) {
-    fetch_windows(tv, tw);                             // stage 1
-    if (nst > 2) fetch_words(tw, 2);
+  if (nl > 0) {
+    expand_store(tv, abuf[0]);
+    slab_store<RR>(x0, bbuf[0], tid);
+    if (nl > 1) {
+      fetch_windows(tv, tw);                           // stage 1
+      if (nl > 2) fetch_words(tw, sb + 2);
+    }
   }
   __syncthreads();
   // (xl holds stage st + 1; xn receives stage st + 2)
   auto step = [&](int st, Slab<BM / RR>& xn, Slab<BM / RR>& xl) {
     const int cur = st & 1;
-    if (st + 1 < nst) {
+    if (st + 1 < nl) {
       expand_store(tv, abuf[cur ^ 1]);                 // stage st + 1
-      slab_store<RR>(xl, bbuf[cur ^ 1]);
-      if (st + 2 < nst) {
+      slab_store<RR>(xl, bbuf[cur ^ 1], tid);
+      if (st + 2 < nl) {
         fetch_windows(tv, tw);                         // stage st + 2 (its words were fetched a stage ago)
-        if (st + 3 < nst) fetch_words(tw, st + 3);
-        xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (st + 2));
+        if (st + 3 < nl) fetch_words(tw, sb + st + 3);
+        xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (sb + st + 2));
       }
     }
-    pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
-    if (st + 1 < nst) __syncthreads();
+    if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
+    if (st + 1 < nh) __syncthreads();
   };
-  for (int st = 0; st < nst; st += 2) {
+  for (int st = 0; st < nh; st += 2) {
     step(st, x0, x1);                                  // stage st + 1 from set 1, stage st + 2 -> set 0
-    if (st + 1 < nst) step(st + 1, x1, x0);            // stage st + 2 from set 0, stage st + 3 -> set 1
+    if (st + 1 < nh) step(st + 1, x1, x0);             // stage st + 2 from set 0, stage st + 3 -> set 1
   }
-  pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
-template <class T, int BN, int BM, int NW, bool kChecked>
-__global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K,
-                                                                 const uint16_t* __restrict__ W, int64_t N,
-                                                                 uint16_t* __restrict__ Y) {
+template <class T, int BN, int BM, int NW, int KS, bool kChecked>
+__global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
+    k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K, const uint16_t* __restrict__ W, int64_t N,
+                    uint16_t* __restrict__ Y) {
   extern __shared__ __align__(16) unsigned char dsm[];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  constexpr int NT = 64 * NW;                         // threads of one k-group
+  const int kh = KS == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x / NT);
+  const int tid = (int)threadIdx.x - kh * NT;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = threadIdx.x & 63;
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
   const int S = (int)tile_steps(K);
   const int nst = (S + 1) / 2;
+  const int nh = (nst + KS - 1) / KS;
+  const int sb = kh * nh;
+  const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;
   constexpr int FN = BN / 32;                         // n-fragments per wave
   constexpr int RR = 8 * NW;                          // rows per staging round
   static_assert(BM == 32 * NW && BN % RR == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
+  static_assert(KS == 1 || FN * 4 * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
-  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + BN * kPfRow)};
-  const uint32_t bbuf[2] = {lds_off(dsm + 2 * BN * kPfRow), lds_off(dsm + (2 * BN + BM) * kPfRow)};
+  unsigned char* gb = dsm + kh * pf_lds(BN, BM);
+  const uint32_t abuf[2] = {lds_off(gb), lds_off(gb + BN * kPfRow)};
+  const uint32_t bbuf[2] = {lds_off(gb + 2 * BN * kPfRow), lds_off(gb + (2 * BN + BM) * kPfRow)};
 
   f32x4 acc[FN][4];
 #pragma unroll
@@ -356,17 +409,19 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
   // (x0, w0) and (x1, w1) alternate, the loop unrolled by two stages.  Stage
   // st + 1 is stored to LDS at the start of stage st, so one barrier per stage
   // both publishes it and retires stage st's reads.
-  const SlabSrc<RR> xsrc(X, M, K, m0), wsrc(W, N, K, n0);
+  const SlabSrc<RR> xsrc(X, M, K, m0, tid), wsrc(W, N, K, n0, tid);
   Slab<BM / RR> x0, x1;
   Slab<BN / RR> w0, w1;
-  xsrc.template fetch<kChecked>(x0, K, 0);
-  wsrc.template fetch<kChecked>(w0, K, 0);
-  if (nst > 1) {
-    xsrc.template fetch<kChecked>(x1, K, kPfBK);
-    wsrc.template fetch<kChecked>(w1, K, kPfBK);
+  if (nl > 0) {
+    xsrc.template fetch<kChecked>(x0, K, (int64_t)kPfBK * sb);
+    wsrc.template fetch<kChecked>(w0, K, (int64_t)kPfBK * sb);
+    if (nl > 1) {
+      xsrc.template fetch<kChecked>(x1, K, (int64_t)kPfBK * (sb + 1));
+      wsrc.template fetch<kChecked>(w1, K, (int64_t)kPfBK * (sb + 1));
+    }
+    slab_store<RR>(w0, abuf[0], tid);
+    slab_store<RR>(x0, bbuf[0], tid);
   }
-  slab_store<RR>(w0, abuf[0]);
-  slab_store<RR>(x0, bbuf[0]);
   __syncthreads();
   // stage st is in the LDS buffers st % 2; (xl, wl) hold stage st + 1, which
   // is written to the other buffers before this stage's MFMAs (their last
@@ -374,22 +429,22 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) k_dense_prefill(const uint16_
   // (xn, wn_) receive stage st + 2
   auto step = [&](int st, Slab<BM / RR>& xn, Slab<BN / RR>& wn_, Slab<BM / RR>& xl, Slab<BN / RR>& wl) {
     const int cur = st & 1;
-    if (st + 1 < nst) {
-      slab_store<RR>(wl, abuf[cur ^ 1]);
-      slab_store<RR>(xl, bbuf[cur ^ 1]);
+    if (st + 1 < nl) {
+      slab_store<RR>(wl, abuf[cur ^ 1], tid);
+      slab_store<RR>(xl, bbuf[cur ^ 1], tid);
     }
-    if (st + 2 < nst) {
-      xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (st + 2));
-      wsrc.template fetch<kChecked>(wn_, K, (int64_t)kPfBK * (st + 2));
+    if (st + 2 < nl) {
+      xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (sb + st + 2));
+      wsrc.template fetch<kChecked>(wn_, K, (int64_t)kPfBK * (sb + st + 2));
     }
-    pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
-    if (st + 1 < nst) __syncthreads();
+    if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
+    if (st + 1 < nh) __syncthreads();
   };
-  for (int st = 0; st < nst; st += 2) {
+  for (int st = 0; st < nh; st += 2) {
     step(st, x0, w0, x1, w1);                          // stage st + 2 -> set 0, stage st + 1 from set 1
-    if (st + 1 < nst) step(st + 1, x1, w1, x0, w0);    // stage st + 3 -> set 1, stage st + 2 from set 0
+    if (st + 1 < nh) step(st + 1, x1, w1, x0, w0);     // stage st + 3 -> set 1, stage st + 2 from set 0
   }
-  pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
 // Raise a kernel's dynamic LDS limit (above the 64 KB default) once.
@@ -398,70 +453,79 @@ hipError_t pf_allow_lds(F* kernel, int bytes) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
-// Workgroup tile of a launch: 128 x 256 (8 waves) when that still gives every
-// CU a workgroup, else 64 x 128 (4 waves, four times as many workgroups).
-bool pf_large_tile(int64_t N, int64_t M) {
+int pf_cus() {
   static const int cus = [] {
     int dev = 0, n = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                                 hipSuccess)
+                                                 hipSuccess || n <= 0)
       return 256;
     return n;
   }();
-  return ((N + 127) / 128) * ((M + 255) / 256) >= (int64_t)cus;
+  return cus;
 }
+
+// Workgroup tile of a launch: 128 x 256 (8 waves) when that still gives every
+// CU a workgroup, else 64 x 128 (4 waves, four times as many workgroups).
+bool pf_large_tile(int64_t N, int64_t M) { return ((N + 127) / 128) * ((M + 255) / 256) >= (int64_t)pf_cus(); }
+
+// Small tiles split K over two wave groups when they leave at most one
+// workgroup per CU.
+bool pf_split_k(int64_t N, int64_t M) { return ((N + 63) / 64) * ((M + 127) / 128) <= (int64_t)pf_cus(); }
 
 // Blocks and stages all inside the matrix: the unchecked (branch-free) loads apply.
 constexpr bool pf_inside(int64_t N, int64_t M, int64_t K, int BN, int BM) {
   return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;
 }
 
-template <class T, int BN, int BM, int NW, bool kChecked>
+template <class T, int BN, int BM, int NW, int KS, bool kChecked>
 hipError_t sparse_prefill_launch(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_sparse_prefill<T, BN, BM, NW, kChecked>, pf_lds(BN, BM));
+  auto* kernel = k_sparse_prefill<T, BN, BM, NW, KS, kChecked>;
+  static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW);
-  hipLaunchKernelGGL((k_sparse_prefill<T, BN, BM, NW, kChecked>), grid, block, pf_lds(BN, BM), s,
-                     static_cast<const uint16_t*>(X), M, Wc.cols, Wc.bitmask, static_cast<const uint16_t*>(Wc.values),
-                     Wc.tile_offsets, Wc.rows, static_cast<uint16_t*>(Y));
+  const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW * KS);
+  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, static_cast<const uint16_t*>(X), M, Wc.cols,
+                     Wc.bitmask, static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows,
+                     static_cast<uint16_t*>(Y));
   return hipGetLastError();
 }
 
-template <class T, int BN, int BM, int NW>
+template <class T, int BN, int BM, int NW, int KS>
 hipError_t sparse_prefill_tile(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  return pf_inside(Wc.rows, M, Wc.cols, BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, false>(X, M, Wc, Y, s)
-                                                : sparse_prefill_launch<T, BN, BM, NW, true>(X, M, Wc, Y, s);
+  return pf_inside(Wc.rows, M, Wc.cols, BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false>(X, M, Wc, Y, s)
+                                                : sparse_prefill_launch<T, BN, BM, NW, KS, true>(X, M, Wc, Y, s);
 }
 
 template <class T>
 hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
   if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
-  return pf_large_tile(Wc.rows, M) ? sparse_prefill_tile<T, 128, 256, 8>(X, M, Wc, Y, s)
-                                    : sparse_prefill_tile<T, 64, 128, 4>(X, M, Wc, Y, s);
+  if (pf_large_tile(Wc.rows, M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(X, M, Wc, Y, s);
+  return pf_split_k(Wc.rows, M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(X, M, Wc, Y, s)
+                                : sparse_prefill_tile<T, 64, 128, 4, 1>(X, M, Wc, Y, s);
 }
 
-template <class T, int BN, int BM, int NW, bool kChecked>
+template <class T, int BN, int BM, int NW, int KS, bool kChecked>
 hipError_t dense_prefill_launch(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y,
                                 hipStream_t s) {
-  static const hipError_t attr = pf_allow_lds(k_dense_prefill<T, BN, BM, NW, kChecked>, pf_lds(BN, BM));
+  auto* kernel = k_dense_prefill<T, BN, BM, NW, KS, kChecked>;
+  static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW);
-  hipLaunchKernelGGL((k_dense_prefill<T, BN, BM, NW, kChecked>), grid, block, pf_lds(BN, BM), s,
-                     static_cast<const uint16_t*>(X), M, K, static_cast<const uint16_t*>(W), N,
-                     static_cast<uint16_t*>(Y));
+  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW * KS);
+  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, static_cast<const uint16_t*>(X), M, K,
+                     static_cast<const uint16_t*>(W), N, static_cast<uint16_t*>(Y));
   return hipGetLastError();
 }
 
-template <class T, int BN, int BM, int NW>
+template <class T, int BN, int BM, int NW, int KS>
 hipError_t dense_prefill_tile(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  return pf_inside(N, M, K, BN, BM) ? dense_prefill_launch<T, BN, BM, NW, false>(X, M, W, N, K, Y, s)
-                                    : dense_prefill_launch<T, BN, BM, NW, true>(X, M, W, N, K, Y, s);
+  return pf_inside(N, M, K, BN, BM) ? dense_prefill_launch<T, BN, BM, NW, KS, false>(X, M, W, N, K, Y, s)
+                                    : dense_prefill_launch<T, BN, BM, NW, KS, true>(X, M, W, N, K, Y, s);
 }
 
 template <class T>
 hipError_t dense_prefill_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  return pf_large_tile(N, M) ? dense_prefill_tile<T, 128, 256, 8>(X, M, W, N, K, Y, s)
-                             : dense_prefill_tile<T, 64, 128, 4>(X, M, W, N, K, Y, s);
+  if (pf_large_tile(N, M)) return dense_prefill_tile<T, 128, 256, 8, 1>(X, M, W, N, K, Y, s);
+  return pf_split_k(N, M) ? dense_prefill_tile<T, 64, 128, 4, 2>(X, M, W, N, K, Y, s)
+                          : dense_prefill_tile<T, 64, 128, 4, 1>(X, M, W, N, K, Y, s);
 }
 
 }  // namespace

@@ -47,8 +47,11 @@ def _constants():
                  "__builtin_memcpy(&tv.v0[i + h], vbytes + 2u * oa, 8);",
                  "__builtin_memcpy(&tv.v1[i + h], vbytes + 2u * ob, 8);",
                  "const uint32_t at = buf + pf_chunk(16 * ((TW / 2) * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);",
-                 "? sparse_prefill_tile<T, 128, 256, 8>(X, M, Wc, Y, s)",
-                 ": sparse_prefill_tile<T, 64, 128, 4>(X, M, Wc, Y, s);"):
+                 "if (pf_large_tile(Wc.rows, M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(X, M, Wc, Y, s);",
+                 "return pf_split_k(Wc.rows, M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(X, M, Wc, Y, s)",
+                 ": sparse_prefill_tile<T, 64, 128, 4, 1>(X, M, Wc, Y, s);",
+                 "fetch_words(tw, sb + 1);",
+                 "if (st + 3 < nl) fetch_words(tw, sb + st + 3);"):
         assert line in src, f"kernel changed: update this replay ({line})"
     return bk, [(128, 8), (64, 4)]                      # (BN, NW) of the two workgroup shapes
 
@@ -158,8 +161,8 @@ def _inside_rule():
     src = open(SRC).read()
     rule = "return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;"
     assert rule in src, "launch rule for the unchecked kernels changed: update this replay"
-    for line in ("? sparse_prefill_launch<T, BN, BM, NW, false>(X, M, Wc, Y, s)",
-                 "? dense_prefill_launch<T, BN, BM, NW, false>(X, M, W, N, K, Y, s)",
+    for line in ("? sparse_prefill_launch<T, BN, BM, NW, KS, false>(X, M, Wc, Y, s)",
+                 "? dense_prefill_launch<T, BN, BM, NW, KS, false>(X, M, W, N, K, Y, s)",
                  "const int64_t t = b * S + s;",
                  "for (int i = 0; i < P; ++i) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);"):
         assert line in src, f"kernel changed: update this replay ({line})"
@@ -187,3 +190,38 @@ def test_unchecked_loads_stay_inside(N, M, K):
             last = (R // rows - 1) * rows + (64 * NW - 1) // 8 + RR * (rows // RR - 1)
             assert last < R
         assert bk * (nst - 1) + 8 * 7 + 8 <= K
+
+
+def _split_rule():
+    src = open(SRC).read()
+    for line in ("const int nh = (nst + KS - 1) / KS;",
+                 "const int sb = kh * nh;",
+                 "const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;",
+                 "if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);",
+                 "if (st + 1 < nh) __syncthreads();",
+                 "unsigned char* gb = dsm + kh * pf_lds(BN, BM);",
+                 "f32x4* part = reinterpret_cast<f32x4*>(dsm);     // [FN * 4][NT]"):
+        assert line in src, f"split-K schedule changed: update this replay ({line})"
+
+
+@pytest.mark.parametrize("nst", [1, 2, 3, 4, 5, 64, 172])
+@pytest.mark.parametrize("KS", [1, 2])
+def test_split_k_stages_partition(nst, KS):
+    """The k-groups' stage ranges [sb, sb + nl) partition [0, nst); every group
+    runs the same number of barriers (derived from nh only); the partial sums
+    of the two-group kernel fit the LDS it is launched with."""
+    _split_rule()
+    bk, _ = _constants()
+    nh = -(-nst // KS)
+    seen = []
+    barriers = set()
+    for kh in range(KS):
+        sb = kh * nh
+        nl = (max(nst - sb, 0)) if nst - sb < nh else nh
+        seen += list(range(sb, sb + nl))
+        # prologue barriers + one per stage transition + the combine's two
+        barriers.add(2 + (nh - 1) + (2 if KS == 2 else 0))
+    assert seen == list(range(nst)) and len(barriers) == 1
+    BN, BM, NW = 64, 128, 4
+    lds = 2 * (BN + BM) * 2 * bk
+    assert (BN // 32) * 4 * 64 * NW * 16 <= KS * lds
