@@ -45,34 +45,60 @@ __global__ void __launch_bounds__(256) k_row_count(const void* W, const uint8_t*
 
 // In place: row_offsets[0..N) hold per-row counts on entry, exclusive prefix
 // sums on exit; row_offsets[N] = nnz, or -1 if nnz >= 2^31 (then the other
-// entries are left unspecified).
+// entries are left unspecified).  One workgroup walks the array in rounds of
+// 4096 entries: thread t takes four consecutive counts (one 16-byte load when
+// the buffer is 16-byte aligned, so a round's loads are coalesced), the waves
+// scan their threads' sums with shuffles, the 16 wave totals go through LDS,
+// and the round's total is carried into the next round.  A round rewrites
+// only the entries it has read.
 __global__ void __launch_bounds__(1024) k_scan_offsets(int32_t* row_offsets, int64_t N) {
-  __shared__ int64_t part[1024];
-  const int t = threadIdx.x;
-  const int64_t per = (N + 1023) / 1024;
-  const int64_t lo = (int64_t)t * per;
-  const int64_t hi = lo + per < N ? lo + per : N;
-  int64_t s = 0;
-  for (int64_t i = lo; i < hi; ++i) s += row_offsets[i];
-  part[t] = s;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int64_t v = t >= off ? part[t - off] : 0;
-    __syncthreads();
-    part[t] += v;
-    __syncthreads();
-  }
-  const int64_t total = part[1023];
-  const bool overflow = total >= (int64_t)2147483648LL;
-  int64_t run = part[t] - s;
-  if (!overflow) {
-    for (int64_t i = lo; i < hi; ++i) {
-      const int32_t c = row_offsets[i];
-      row_offsets[i] = (int32_t)run;
-      run += c;
+  __shared__ int64_t wsum[16];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const bool vec = ((uintptr_t)row_offsets & 15u) == 0;
+  int64_t carry = 0;                                     // sum of every earlier round
+  for (int64_t base = 0; base < N; base += 4096) {
+    const int64_t i0 = base + 4 * (int64_t)t;
+    int32_t c[4];
+    if (vec && i0 + 3 < N) {
+      const i32x4 v = *reinterpret_cast<const i32x4*>(row_offsets + i0);
+      c[0] = v[0], c[1] = v[1], c[2] = v[2], c[3] = v[3];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) c[j] = i0 + j < N ? row_offsets[i0 + j] : 0;
     }
+    const int64_t s = (int64_t)c[0] + c[1] + c[2] + c[3];
+    int64_t x = s;                                       // inclusive scan over the wave's threads
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int64_t y = __shfl_up(x, d);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    int64_t before = carry + x - s, total = 0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      const int64_t ws = wsum[w];
+      if (w < wave) before += ws;
+      total += ws;
+    }
+    int32_t o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      o[j] = (int32_t)before;
+      before += c[j];
+    }
+    if (vec && i0 + 3 < N) {
+      *reinterpret_cast<i32x4*>(row_offsets + i0) = i32x4{o[0], o[1], o[2], o[3]};
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (i0 + j < N) row_offsets[i0 + j] = o[j];
+    }
+    carry += total;
+    __syncthreads();                                     // wsum is rewritten by the next round
   }
-  if (t == 1023) row_offsets[N] = overflow ? -1 : (int32_t)total;
+  if (t == 0) row_offsets[N] = carry >= (int64_t)2147483648LL ? -1 : (int32_t)carry;
 }
 
 template <int EB>
