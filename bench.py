@@ -556,8 +556,8 @@ def main():
         print(json.dumps({"copy_calibration_bytes": args.copy_calibration}), flush=True)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
-              f"(multi-GPU sharding is a design note only)", file=sys.stderr)
+        print(f"bench.py: measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(the kernels run on a single GPU; sharding across GPUs is not implemented)", file=sys.stderr)
         sys.exit(2)
 
     if args.workload != "decode":

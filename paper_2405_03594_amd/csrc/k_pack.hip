@@ -45,17 +45,17 @@ __global__ void __launch_bounds__(256) k_row_count(const void* W, const uint8_t*
 
 // In place: row_offsets[0..N) hold per-row counts on entry, exclusive prefix
 // sums on exit; row_offsets[N] = nnz, or -1 if nnz >= 2^31 (then the other
-// entries are left unspecified).  One workgroup walks the array in rounds of
+// entries are left unspecified).  One workgroup walks the array in passes of
 // 4096 entries: thread t takes four consecutive counts (one 16-byte load when
-// the buffer is 16-byte aligned, so a round's loads are coalesced), the waves
+// the buffer is 16-byte aligned, so a pass's loads are coalesced), the waves
 // scan their threads' sums with shuffles, the 16 wave totals go through LDS,
-// and the round's total is carried into the next round.  A round rewrites
-// only the entries it has read.
+// and the pass's total is carried into the next pass.  A pass rewrites only
+// the entries it has read.
 __global__ void __launch_bounds__(1024) k_scan_offsets(int32_t* row_offsets, int64_t N) {
   __shared__ int64_t wsum[16];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const bool vec = ((uintptr_t)row_offsets & 15u) == 0;
-  int64_t carry = 0;                                     // sum of every earlier round
+  int64_t carry = 0;                                     // sum of every earlier pass
   for (int64_t base = 0; base < N; base += 4096) {
     const int64_t i0 = base + 4 * (int64_t)t;
     int32_t c[4];
@@ -96,7 +96,7 @@ __global__ void __launch_bounds__(1024) k_scan_offsets(int32_t* row_offsets, int
         if (i0 + j < N) row_offsets[i0 + j] = o[j];
     }
     carry += total;
-    __syncthreads();                                     // wsum is rewritten by the next round
+    __syncthreads();                                     // wsum is rewritten by the next pass
   }
   if (t == 0) row_offsets[N] = carry >= (int64_t)2147483648LL ? -1 : (int32_t)carry;
 }
