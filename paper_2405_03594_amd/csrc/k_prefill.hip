@@ -14,7 +14,9 @@
 // c ^ (r % 8), so that eight consecutive rows' fragment reads (and the
 // staging writes of one row) fall in distinct banks.  The next stage's global loads are
 // in flight while the current stage is multiplied, and one barrier per stage
-// hands the buffers over.
+// hands the buffers over; within a stage the second k-step's fragment reads
+// are interleaved with the first k-step's MFMAs.  Launches whose blocks and
+// stages all lie inside the matrix use loads without bounds branches.
 //
 //   * dense (comparator): W rows are copied into the A buffer exactly like
 //     X rows into the B buffer;
@@ -22,7 +24,8 @@
 //     stage's compressed 16 x 32 tiles (BN/16 row blocks x 2 k-steps, shared
 //     out over the waves), each once per workgroup and one stage ahead, before
 //     the current stage's MFMAs: bitmask words are fetched three stages ahead
-//     and value windows two ahead; a lane expands its row's 8 columns with
+//     and value windows two ahead (the two tiles a wave expands per stage
+//     share one offset scan); a lane expands its row's 8 columns with
 //     v_perm_b32 under a nibble selector table, as in the decode kernel, and
 //     writes them with one 16-byte LDS store.
 #include "spl_common.h"
