@@ -28,11 +28,13 @@
 //     with v_perm_b32 into the operand dwords (zero bytes where the bit is
 //     clear);
 //   * activations form the B operand (batch padded to 16 or 32 columns; the
-//     padding lanes hold zeros).  When every M x K of the group fits 32 KB the
-//     workgroup copies its X into LDS once (and the kernel is held to 64
-//     VGPRs, eight waves per SIMD, so that LDS rather than registers bounds
-//     the workgroups per CU); otherwise each chunk's operands are loaded
-//     directly;
+//     padding lanes hold zeros).  The workgroup copies its X into LDS once
+//     (and the kernel is held to 64 VGPRs, eight waves per SIMD, so that LDS
+//     rather than registers bounds the workgroups per CU) when the copy is
+//     small enough to leave several workgroups per CU: a single row (up to
+//     32 KB; the dense comparator: any batch up to 32 KB), or a small batch
+//     in a large grid (up to 16 KB); otherwise each chunk's operands are
+//     loaded directly, which fetches only the live rows;
 //   * the waves' partial 16x16 results are summed in a fixed order
 //     (deterministic) and rounded once to the output type.
 //
