@@ -62,6 +62,7 @@ def _load():
         "orc_dense_f64": (None, [P, I64, I64, I32, P, I64, P, ctypes.c_int]),
         "orc_linear_i8": (ctypes.c_int, [P, P, I64, I64, P, P, P, P, I64, P, P, ctypes.c_int]),
         "orc_dense_i8": (ctypes.c_int, [P, P, I64, I64, P, P, I64, P, P, ctypes.c_int]),
+        "orc_quantize_rows_i8": (None, [P, I32, I64, I64, P, P]),
         "orc_tile_blocks": (I64, [I64]),
         "orc_tile_ksteps": (I64, [I64]),
         "orc_pack_tiled": (None, [P, I32, P, I64, I64, P, P, P]),
@@ -261,6 +262,18 @@ def dense_i8(Xq: np.ndarray, sx: np.ndarray, Wq: np.ndarray, sw: np.ndarray, nth
     if rc != 0:
         raise OverflowError("int8 accumulator outside the int32 range")
     return acc, Y
+
+
+def quantize_rows_i8(X: np.ndarray, dtype: str):
+    """Per-token int8 codes and binary32 scales of fp16/bf16 activation bits
+    (the reading of section 3.4 in orc_quantize_rows_i8)."""
+    lib = _load()
+    X = np.ascontiguousarray(X, dtype=np.uint16)
+    M, K = X.shape
+    Xq = np.zeros((M, K), dtype=np.int8)
+    sx = np.zeros(M, dtype=np.float32)
+    lib.orc_quantize_rows_i8(_ptr(X), _code(dtype), M, K, _ptr(Xq), _ptr(sx))
+    return Xq, sx
 
 
 def f16_to_f64(bits: np.ndarray) -> np.ndarray:

@@ -401,6 +401,32 @@ int orc_dense_i8(const int8_t* Xq, const float* sx, int64_t M, int64_t K, const 
   return bad ? -1 : 0;
 }
 
+/* Per-token activation quantisation for the sparse-quantized path (section
+ * 3.4 quantises activations to int8; the reading taken: symmetric, one scale
+ * per row, binary32).  For each row m of X (fp16 or bf16 payload bits):
+ *   amax = max over k of |x|,  scale = amax / 127 (1 when amax is 0),
+ *   code = clamp(round-half-to-even(x / scale), -127, 127),
+ * each division rounded to binary32. */
+void orc_quantize_rows_i8(const uint16_t* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx) {
+  for (int64_t m = 0; m < M; ++m) {
+    float amax = 0.0f;
+    for (int64_t k = 0; k < K; ++k) {
+      const float a = fabsf((float)elem_to_f64(X, m * K + k, dtype));   /* fp16/bf16 -> binary32 is exact */
+      if (a > amax) amax = a;
+    }
+    volatile float scale = amax / 127.0f;
+    if (amax == 0.0f) scale = 1.0f;
+    sx[m] = scale;
+    for (int64_t k = 0; k < K; ++k) {
+      volatile float r = (float)elem_to_f64(X, m * K + k, dtype) / scale;
+      float q = nearbyintf(r);                                          /* default mode: to nearest, ties even */
+      if (q > 127.0f) q = 127.0f;
+      if (q < -127.0f) q = -127.0f;
+      Xq[m * K + k] = (int8_t)q;
+    }
+  }
+}
+
 /* Element-wise helpers exposed for the oracle's own checks. */
 void orc_f16_to_f64_array(const uint16_t* in, int64_t n, double* out) {
   for (int64_t i = 0; i < n; ++i) out[i] = orc_f16_to_f64(in[i]);

@@ -442,3 +442,53 @@ def test_tiled_value_order_worked_example(orc, dtype, G):
     order = [(0, 0), (1, 1), (0, 9), (1, 8), (0, 17)] if G == 8 else [(0, 0), (0, 9), (1, 1), (1, 8), (0, 17)]
     assert [int(v) for v in t.values] == [int(W[r, j]) for r, j in order]
     assert list(t.bitmask[:2]) == [(1 << 0) | (1 << 9) | (1 << 17), (1 << 1) | (1 << 8)]
+
+
+# ---------------------------------------------------------------- per-token activation quantisation
+
+def _bits(vals, dtype):
+    return synth.round_to(np.asarray(vals, dtype=np.float32), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_quantize_rows_closed_forms(orc, dtype):
+    """Rows whose scale is exact (amax 127 -> 1, amax 254 -> 2) give codes that
+    are the round-half-to-even of x / scale by hand; a zero row gets scale 1."""
+    X = np.stack([
+        _bits([127, 2.5, 3.5, -2.5, 126.5, -0.5, 1.5, 0.25], dtype),
+        _bits([254, 5, 7, -254, 253, -3, 1, 0], dtype),
+        _bits([0] * 8, dtype),
+        _bits([-127, 127, -1, 1, 0.5, -1.5, 4.5, -4.5], dtype),
+    ])
+    Xq, sx = orc.quantize_rows_i8(X, dtype)
+    assert sx.tolist() == [1.0, 2.0, 1.0, 1.0]
+    assert Xq.tolist() == [[127, 2, 4, -2, 126, 0, 2, 0],
+                           [127, 2, 4, -127, 126, -2, 0, 0],
+                           [0] * 8,
+                           [-127, 127, -1, 1, 0, -2, 4, -4]]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_quantize_rows_invariants(orc, dtype):
+    """Random rows: |code| <= 127, the largest magnitude of a row codes to +-127,
+    and code * scale is within half a step (and rounding) of the value."""
+    rng = np.random.default_rng(3)
+    v = (rng.standard_normal((40, 300)) * rng.uniform(0.01, 50, (40, 1))).astype(np.float32)
+    X = synth.round_to(v, dtype)
+    x = orc.to_f64(X, dtype)
+    Xq, sx = orc.quantize_rows_i8(X, dtype)
+    assert np.abs(Xq.astype(np.int64)).max() <= 127
+    arg = np.argmax(np.abs(x), axis=1)
+    assert (np.abs(Xq[np.arange(40), arg]) == 127).all()
+    assert np.allclose(sx.astype(np.float64), np.abs(x).max(axis=1) / 127.0, rtol=1e-6)
+    err = np.abs(x - Xq.astype(np.float64) * sx[:, None].astype(np.float64))
+    assert (err <= sx[:, None] * (0.5 + 1e-5)).all()
+
+
+def test_quantize_rows_agrees_with_generator(orc):
+    """The oracle's quantiser and the input generator's (NumPy) coding of the
+    int8 activations give the same codes and scales bit for bit."""
+    x = synth.activations(7, 33, 520, "bf16")
+    q1, s1 = orc.quantize_rows_i8(x, "bf16")
+    q2, s2 = synth.quantize_rows_int8(synth.bits_to_f32(x, "bf16"))
+    assert np.array_equal(q1, q2) and np.array_equal(s1.view(np.uint32), s2.view(np.uint32))

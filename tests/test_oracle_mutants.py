@@ -6,7 +6,9 @@ the pin tests of tests/test_oracle.py against the copy in a subprocess and
 requires that at least one pin fails.  Planted: a shifted bitmask bit, a
 reversed k index, wrong fp16 and bf16 exponent biases, a swapped dequant
 scale, floor instead of round-to-nearest-even, an off-by-one value index, a
-perturbed int8 sum, a shifted row offset and a dropped k term."""
+perturbed int8 sum, a shifted row offset, a dropped k term, and in the
+activation quantiser truncation instead of round-to-nearest-even and a
+divisor of 128 instead of 127."""
 import os
 import shutil
 import subprocess
@@ -29,6 +31,8 @@ MUTANTS = [
     ("row offset", "row_offsets[n] = (int32_t)c;", "row_offsets[n] = (int32_t)(c + (n == 1));"),
     ("bf16 bias", "v = ldexp((double)(128 + f), e - 134);", "v = ldexp((double)(128 + f), e - 133);"),
     ("dropped k", "for (int64_t k = 0; k < K; ++k) s += Xd", "for (int64_t k = 1; k < K; ++k) s += Xd"),
+    ("quantiser rounding", "float q = nearbyintf(r);", "float q = truncf(r);"),
+    ("quantiser scale", "volatile float scale = amax / 127.0f;", "volatile float scale = amax / 128.0f;"),
 ]
 
 
