@@ -180,6 +180,19 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
 spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream);
 
+/* Per-token activation quantisation for the sparse-quantized layer (paper
+ * section 3.4 runs it on int8 activations; the reading taken: symmetric, one
+ * binary32 scale per row).  For each row m of X:
+ *   x_scales[m] = max_k |X[m][k]| / 127 (1 when the row is all zeros),
+ *   Xq[m][k]    = clamp(round-half-to-even(X[m][k] / x_scales[m]), -127, 127),
+ * each division correctly rounded to binary32.
+ *   X         [M][K] fp16 or bf16 (dtype), 16-byte aligned; K % 8 == 0
+ *             (SPL_ERR_UNSUPPORTED otherwise, and for other dtypes).
+ *   Xq        out [M][K] int8, 16-byte aligned; x_scales out [M] float32.
+ * M == 0 is a no-op.  Asynchronous on `stream`. */
+spl_status spl_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* x_scales,
+                                hipStream_t stream);
+
 /* Dense comparators: the same products with a dense W [N][K].
  * spl_dense_linear: fp16/bf16 (K % 8 == 0); spl_dense_linear_int8: int8
  * with the epilogue of spl_sparse_linear_int8 (K % 16 == 0). */

@@ -100,6 +100,7 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_linear": (ctypes.c_int, [P, I64, MP, P, P]),
         "spl_sparse_linear_ex": (ctypes.c_int, [P, I64, MP, P, I32, P]),
         "spl_sparse_linear_int8": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
+        "spl_quantize_rows_i8": (ctypes.c_int, [P, ctypes.c_int32, I64, I64, P, P, P]),
         "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
         "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
@@ -251,6 +252,22 @@ def sparse_linear(X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = 
     _check("spl_sparse_linear_ex", L.spl_sparse_linear_ex(_ptr(X), M, ctypes.byref(view), _ptr(out), ALGO[algo],
                                                           _stream(stream)))
     return out
+
+
+def quantize_rows_i8(X: torch.Tensor, out: torch.Tensor | None = None, scales: torch.Tensor | None = None,
+                     stream=None):
+    """Per-token int8 codes and binary32 scales of fp16/bf16 activations X [M][K]
+    (section 3.4; see spl_quantize_rows_i8).  Returns (Xq int8 [M][K], x_scales f32 [M])."""
+    L = lib()
+    _dev_tensor(X, "X")
+    M, K = X.shape
+    if out is None:
+        out = torch.empty((M, K), dtype=torch.int8, device=X.device)
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=X.device)
+    _check("spl_quantize_rows_i8", L.spl_quantize_rows_i8(_ptr(X), _TORCH_DTYPE[X.dtype], M, K, _ptr(out),
+                                                          _ptr(scales), _stream(stream)))
+    return out, scales
 
 
 def sparse_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wqc: SparseMatrix, w_scales: torch.Tensor,

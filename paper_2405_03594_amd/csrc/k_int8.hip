@@ -426,6 +426,48 @@ hipError_t sparse_int8_w(const I8GroupArg& g, int64_t kmax, hipStream_t s) {
   return sparse_int8_launch<4, false, W>(g, kmax, s);
 }
 
+// Per-token activation quantisation (paper section 3.4 quantises the
+// activations to int8; symmetric, one binary32 scale per row): one workgroup
+// per row of X [M][K] (K % 8 == 0, 16-byte pieces of 8 fp16/bf16 values)
+// finds amax = max |x| (a wave reduction, then the 4 wave maxima), sets
+// scale = amax / 127 (1 when amax is 0), and re-reads the row (from L2) to
+// write the codes clamp(round-half-even(x / scale), -127, 127); each division
+// is correctly rounded.
+template <class T>
+__global__ void __launch_bounds__(256) k_quantize_rows(const uint16_t* __restrict__ X, int64_t K,
+                                                       int8_t* __restrict__ Xq, float* __restrict__ sx) {
+  __shared__ float wmax[4];
+  const int64_t m = blockIdx.x;
+  const uint16_t* x = X + m * K;
+  const int64_t P = K / 8;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  float amax = 0.0f;
+  for (int64_t p = t; p < P; p += 256) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(x + 8 * p);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(T::to_f32((v[e >> 1] >> (16 * (e & 1))) & 0xffffu)));
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) amax = fmaxf(amax, __shfl_xor(amax, d));
+  if (lane == 0) wmax[wave] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+  const float scale = amax == 0.0f ? 1.0f : __fdiv_rn(amax, 127.0f);
+  if (t == 0) sx[m] = scale;
+  int8_t* q = Xq + m * K;
+  for (int64_t p = t; p < P; p += 256) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(x + 8 * p);
+    uint32_t c[2] = {0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float r = rintf(__fdiv_rn(T::to_f32((v[e >> 1] >> (16 * (e & 1))) & 0xffffu), scale));
+      r = fminf(fmaxf(r, -127.0f), 127.0f);
+      c[e >> 2] |= ((uint32_t)(int32_t)r & 0xffu) << (8 * (e & 3));
+    }
+    *reinterpret_cast<u32x2*>(q + 8 * p) = u32x2{c[0], c[1]};
+  }
+}
+
 bool i8_small_grid(int64_t blocks) {
   static int cus = [] {
     int dev = 0, n = 0;
@@ -475,6 +517,16 @@ hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_
     hipLaunchKernelGGL((k_dense_int8<2>), grid, block, 0, s, g);
   else
     hipLaunchKernelGGL((k_dense_int8<4>), grid, block, 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
+                                   hipStream_t s) {
+  const uint16_t* x = static_cast<const uint16_t*>(X);
+  if (dtype == SPL_BF16)
+    hipLaunchKernelGGL(k_quantize_rows<Bf16>, dim3((unsigned)M), dim3(256), 0, s, x, K, Xq, sx);
+  else
+    hipLaunchKernelGGL(k_quantize_rows<F16>, dim3((unsigned)M), dim3(256), 0, s, x, K, Xq, sx);
   return hipGetLastError();
 }
 

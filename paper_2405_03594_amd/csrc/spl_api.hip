@@ -289,4 +289,16 @@ spl_status spl_dense_linear_int8_group(const spl_dense_int8_task* tasks, int32_t
   return launched(spl::launch_dense_int8(tasks, count, M, stream));
 }
 
+spl_status spl_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* x_scales,
+                                hipStream_t stream) {
+  if (M < 0) return SPL_ERR_INVALID_ARG;
+  if (!fp_dtype(dtype)) return SPL_ERR_UNSUPPORTED;
+  if (M == 0) return SPL_OK;
+  if (!X || !Xq || !x_scales || !dims_ok(M, K)) return SPL_ERR_INVALID_ARG;
+  if (K % 8 != 0) return SPL_ERR_UNSUPPORTED;
+  if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(x_scales, 4)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_quantize_rows_i8(X, dtype, M, K, Xq, x_scales, stream));
+}
+
 }  // extern "C"

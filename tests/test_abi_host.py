@@ -233,3 +233,19 @@ def test_int8_group_argument_checks(L):
     assert g(d, 2, 2, None) == UNSUPPORTED                        # K % 16 != 0
     d[1].K, d[1].Wq = 64, 0x10008
     assert g(d, 2, 2, None) == INVALID                            # misaligned W
+
+
+def test_quantize_rows_argument_checks(L):
+    """Checks that return before any HIP call (no device needed)."""
+    f = L.spl_quantize_rows_i8
+    X, Q, s = 0x40000, 0x50000, 0x60000
+    assert f(X, 2, 0, 64, Q, s, None) == OK                       # M = 0: a no-op
+    assert f(X, 2, -1, 64, Q, s, None) == INVALID
+    assert f(X, 3, 4, 64, Q, s, None) == UNSUPPORTED              # int8 input
+    assert f(X, 2, 4, 60, Q, s, None) == UNSUPPORTED              # K % 8 != 0
+    assert f(None, 2, 4, 64, Q, s, None) == INVALID
+    assert f(X, 2, 4, 64, None, s, None) == INVALID
+    assert f(X, 2, 4, 64, Q, None, None) == INVALID
+    assert f(X + 8, 2, 4, 64, Q, s, None) == INVALID              # misaligned X
+    assert f(X, 1, 4, 64, Q + 4, s, None) == INVALID              # misaligned codes
+    assert f(X, 2, 4, 0, Q, s, None) == INVALID                   # K = 0

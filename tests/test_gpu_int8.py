@@ -182,3 +182,21 @@ def test_int8_group_matches_oracle_and_single_calls(orc, spl, M):
             _assert_equal(y.cpu().view(torch.int16).numpy().view(np.uint16), y_ref, f"{what} group task {i} Y M={M}")
         single = spl.sparse_linear_int8(Xqs[i], sxs[i], Wcs[i], sws[i])
         assert torch.equal(single.view(torch.int16), outs[i].view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("M,K", [(1, 8), (3, 520), (300, 4096), (17, 11008)])
+def test_quantize_rows_matches_oracle(orc, spl, dtype, M, K):
+    """Per-token activation quantisation on the GPU: codes and scales bit for
+    bit equal to the oracle's, with a zero row, rows of exact ties and rows of
+    large magnitude mixed in."""
+    rng = np.random.default_rng(M + K)
+    v = (rng.standard_normal((M, K)) * rng.uniform(0.05, 20.0, (M, 1))).astype(np.float32)
+    if M >= 3:
+        v[1] = 0.0
+        v[2] = np.resize(np.array([127, 2.5, 3.5, -2.5, 126.5, -0.5, 1.5, 0.25], np.float32), K)
+    X = synth.round_to(v, dtype)
+    ref_q, ref_s = orc.quantize_rows_i8(X, dtype)
+    q, s = spl.quantize_rows_i8(to_dev(X, dtype))
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), ref_s.view(np.uint32)), "scales differ"
+    assert np.array_equal(q.cpu().numpy(), ref_q), "codes differ"
