@@ -36,6 +36,9 @@ constexpr int kI8VBufAlloc = kI8VBuf + 16;  // + room past the last window
 constexpr int kI8PieceRounds = kI8VBuf / 16 / kWave;
 constexpr int kI8XLdsMax = 32 * 1024;       // activations staged in LDS when M * 64 ceil(S/2) bytes fit
 constexpr int kI8OffsetLanes = kWave - 1;
+// Batches from this size on use the prefill kernels' MFMA tiling (activations staged in LDS and
+// shared by the row blocks of a workgroup) instead of the streaming kernels below.
+constexpr int64_t kI8PrefillMinM = 128;
 
 __device__ __forceinline__ i32x4 mfma_i8(u32x4 a, u32x4 b, i32x4 c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0, 0,
@@ -482,6 +485,13 @@ bool i8_small_grid(int64_t blocks) {
 }  // namespace
 
 hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s) {
+  if (M >= kI8PrefillMinM) {                         // MFMA-tiled kernel with activations shared in LDS
+    for (int i = 0; i < count; ++i) {
+      const hipError_t e = launch_sparse_prefill_i8(tasks[i], M, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   I8GroupArg g{};
   g.count = count;
   g.M = (int32_t)M;
@@ -500,6 +510,13 @@ hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, 
 }
 
 hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s) {
+  if (M >= kI8PrefillMinM) {
+    for (int i = 0; i < count; ++i) {
+      const hipError_t e = launch_dense_prefill_i8(tasks[i], M, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   I8DenseGroupArg g{};
   g.count = count;
   g.M = (int32_t)M;

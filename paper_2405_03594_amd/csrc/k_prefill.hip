@@ -28,6 +28,8 @@
 //     share one offset scan); a lane expands its row's 8 columns with
 //     v_perm_b32 under a nibble selector table, as in the decode kernel, and
 //     writes them with one 16-byte LDS store.
+#include <type_traits>
+
 #include "spl_common.h"
 
 namespace spl {
@@ -38,10 +40,14 @@ constexpr int kPfRow = kPfBK * 2;                // bytes per staged row (8 chun
 // LDS of a BN x BM workgroup: two W (A operand) buffers of BN rows, two X (B operand) buffers of BM rows
 constexpr int pf_lds(int BN, int BM) { return 2 * (BN + BM) * kPfRow; }
 
+// int8 payloads (paper section 3.4): int8 weights and activations, exact int32 sums.
+struct I8P {};
+
 template <class T>
 struct MfmaP;
 template <>
 struct MfmaP<Bf16> {
+  using acc_t = f32x4;
   static __device__ __forceinline__ f32x4 run(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
                                                    0, 0, 0);
@@ -49,9 +55,20 @@ struct MfmaP<Bf16> {
 };
 template <>
 struct MfmaP<F16> {
+  using acc_t = f32x4;
   static __device__ __forceinline__ f32x4 run(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
                                                   0, 0);
+  }
+};
+// One 16 x 16 x 64 int8 product: a 128-byte staged row holds the same two
+// k-steps (of 64 int8 columns) as it holds for 16-bit payloads (32 columns).
+template <>
+struct MfmaP<I8P> {
+  using acc_t = i32x4;
+  static __device__ __forceinline__ i32x4 run(u32x4 a, u32x4 b, i32x4 c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0, 0,
+                                                 0);
   }
 };
 
@@ -69,6 +86,21 @@ __device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
       s16 = (2u * r) | ((2u * r + 1u) << 8);
     }
     sel |= s16 << (16 * e);
+  }
+  return sel;
+}
+
+// v_perm_b32 selector for a 4-column nibble of 1-byte values whose stored
+// values start at byte p of an 8-byte window: a kept column takes byte
+// p + rank, a dropped one 0x0C (a zero byte).  p + rank <= 7 (p is the kept
+// count of the nibble before, at most 4).
+__device__ __forceinline__ uint32_t pf_i8_selector(uint32_t nib, uint32_t p) {
+  uint32_t sel = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t b = 0x0Cu;
+    if ((nib >> j) & 1u) b = p + __popc(nib & ((1u << j) - 1u));
+    sel |= b << (8 * j);
   }
   return sel;
 }
@@ -132,8 +164,8 @@ __device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf, int 
 // reads, then put one second-k-step read after each of the first MFMAs, so
 // the LDS reads overlap the matrix cores instead of waiting ahead of them.
 template <class T, int FN>
-__device__ __forceinline__ void pf_mfma_stage(f32x4 (&acc)[FN][4], uint32_t abuf, uint32_t bbuf, int wn, int wm,
-                                              int fr, int fg) {
+__device__ __forceinline__ void pf_mfma_stage(typename MfmaP<T>::acc_t (&acc)[FN][4], uint32_t abuf, uint32_t bbuf,
+                                              int wn, int wm, int fr, int fg) {
   // fragment rows differ by multiples of 16, so every row a lane reads has row % 8 == fr % 8
   u32x4 a[2][FN], b[2][4];
 #pragma unroll
@@ -187,16 +219,44 @@ __device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][4], uint16_t* __
   }
 }
 
+// The int8 epilogue: Y = fp16_rne((float(acc) * sx[m]) * sw[n]), each product
+// rounded to binary32 (no fused multiply-add); acc_out (optional) gets the
+// exact int32 sums.
+template <int FN>
+__device__ __forceinline__ void pf_store_i8(const i32x4 (&acc)[FN][4], uint16_t* __restrict__ Y,
+                                            int32_t* __restrict__ acc_out, const float* __restrict__ sx,
+                                            const float* __restrict__ sw, int64_t M, int64_t N, int64_t n0,
+                                            int64_t m0, int wn, int wm, int fr, int fg) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t m = m0 + wm * 64 + 16 * j + fr;
+    if (m >= M) continue;
+    const float xs = sx[m];
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+      const int64_t n = n0 + wn * 16 * FN + 16 * i + 4 * fg;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (n + r >= N) continue;
+        const int32_t v = acc[i][j][r];
+        if (acc_out) acc_out[m * N + n + r] = v;
+        const float y = __fmul_rn(__fmul_rn((float)v, xs), sw[n + r]);
+        Y[m * N + n + r] = F16::from_f32(y);
+      }
+    }
+  }
+}
+
 // Split K: after every wave's last MFMA, k-group 1 hands its partial sums to
 // k-group 0 through the (then free) stage buffers; group 0 adds them (a fixed
 // order) and is the one that stores.  Returns whether this thread stores.
-template <int FN, int NT, int KS>
-__device__ __forceinline__ bool pf_combine(f32x4 (&acc)[FN][4], unsigned char* dsm, int kh, int t) {
+template <int FN, int NT, int KS, class A>
+__device__ __forceinline__ bool pf_combine(A (&acc)[FN][4], unsigned char* dsm, int kh, int t) {
   if constexpr (KS == 1) {
     return true;
   } else {
     static_assert(KS == 2, "two k-groups");
-    f32x4* part = reinterpret_cast<f32x4*>(dsm);     // [FN * 4][NT]
+    A* part = reinterpret_cast<A*>(dsm);             // [FN * 4][NT]
     __syncthreads();
     if (kh == 1) {
 #pragma unroll
@@ -224,17 +284,32 @@ struct TileWords {
 };
 template <int TW>
 struct TileWindows {
-  uint32_t byte[TW];      // this lane's 8 columns of row fr
+  uint32_t byte[TW];      // this lane's 8 columns of row fr (16 for int8)
   u32x2 v0[TW], v1[TW];   // 8-byte windows from the first value of each nibble
 };
 
+// Arguments of a prefill launch.  Activations and dense weights are read as
+// rows of 16-bit units: a row of K int8 values is K/2 units.
+struct PfArgs {
+  const uint16_t* X;             // [M][K] activations
+  const uint16_t* W;             // dense comparator: [N][K] weights
+  const uint32_t* bm;            // sparse: tile bitmask words
+  const unsigned char* values;   // sparse: payload bytes (followed by 16 readable bytes)
+  const int32_t* toff;           // sparse: tile offsets
+  int64_t M, N, K;               // K in payload elements
+  uint16_t* Y;                   // out [M][N]: the payload type, fp16 for int8
+  const float* sx;               // int8: activation scales [M]
+  const float* sw;               // int8: weight scales [N]
+  int32_t* acc;                  // int8: optional exact sums [M][N]
+};
+
 template <class T, int BN, int BM, int NW, int KS, bool kChecked>
-__global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
-    k_sparse_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K, const uint32_t* __restrict__ bm_tiles,
-                     const uint16_t* __restrict__ values, const int32_t* __restrict__ tile_offsets, int64_t N,
-                     uint16_t* __restrict__ Y) {
+__global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(const PfArgs g) {
   extern __shared__ __align__(16) unsigned char dsm[];
-  __shared__ u32x2 lut[16];
+  constexpr bool kI8 = std::is_same<T, I8P>::value;
+  // selector tables: 16 x 8 bytes (16-bit payloads), or 16 nibbles x 5 window starts (int8)
+  __shared__ __align__(16) uint32_t lut[80];
+  using Acc = typename MfmaP<T>::acc_t;
   constexpr int NT = 64 * NW;                        // threads of one k-group
   const int kh = KS == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x / NT);
   const int tid = (int)threadIdx.x - kh * NT;        // thread index within the k-group
@@ -242,14 +317,16 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
   const int lane = threadIdx.x & 63;
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
+  const int64_t M = g.M, N = g.N, K = g.K;
+  const int64_t Kh = kI8 ? K / 2 : K;                // activation row in 16-bit units
   const int S = (int)tile_steps(K);
-  const int nst = (S + 1) / 2;
+  const int nst = (int)((Kh + kPfBK - 1) / kPfBK);   // stages of 128 bytes per row: 2 tiles (4 for int8)
   const int nh = (nst + KS - 1) / KS;                // stages per k-group (uniform: every group's barriers)
   const int sb = kh * nh;                            // this group's first stage
   const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;   // its stages (the last group may hold fewer)
   const int64_t B = tile_blocks(N);
   constexpr int FN = BN / 32;                        // n-fragments per wave
-  constexpr int TW = BN / 8 / NW;                    // tiles per wave per stage (whole k-step pairs)
+  constexpr int TW = BN / 8 / NW;                    // operand units per wave per stage: tiles (int8: tile pairs)
   constexpr int RR = 8 * NW;                         // rows per staging round
   static_assert(BM == 32 * NW && TW % 2 == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
   static_assert(KS == 1 || FN * 4 * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
@@ -260,20 +337,32 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
   const uint32_t abuf[2] = {lds_off(gb), lds_off(gb + BN * kPfRow)};
   const uint32_t bbuf[2] = {lds_off(gb + 2 * BN * kPfRow), lds_off(gb + (2 * BN + BM) * kPfRow)};
   const uint32_t lut_addr = lds_off(lut);
-  const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(values);
-  if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{pf_nibble_selector(threadIdx.x, 0), pf_nibble_selector(threadIdx.x, 1)};
+  const unsigned char* vbytes = g.values;
+  const uint32_t* __restrict__ bm_tiles = g.bm;
+  const int32_t* __restrict__ tile_offsets = g.toff;
+  if constexpr (kI8) {
+    if (threadIdx.x < 80) lut[threadIdx.x] = pf_i8_selector(threadIdx.x / 5, threadIdx.x % 5);
+  } else {
+    if (threadIdx.x < 16) {
+      lut[2 * threadIdx.x] = pf_nibble_selector(threadIdx.x, 0);
+      lut[2 * threadIdx.x + 1] = pf_nibble_selector(threadIdx.x, 1);
+    }
+  }
 
+  // Unit i of a stage is row block (TW/2) wave + i/2 of the workgroup's BN/16
+  // and k-step 2 st + i % 2: one tile (16-bit payloads), or the pair of tiles
+  // 4 st + 2 (i % 2) + {0, 1} (int8: lanes 0-31 the first, 32-63 the second).
   auto fetch_words = [&](TileWords<TW>& tw, int st) {
 #pragma unroll
     for (int i = 0; i < TW; ++i) {
       const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);
-      const int s = 2 * st + (i & 1);
+      const int s = kI8 ? 4 * st + 2 * (i & 1) + (fg >> 1) : 2 * st + (i & 1);
       if constexpr (kChecked) {
         const bool ok = b < B && s < S;
         const int64_t t = ok ? b * S + s : 0;
         tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;
         tw.off[i] = tile_offsets[t];
-      } else {                                       // N % BN == 0 and S even: always inside
+      } else {                                       // N % BN == 0 and whole stages: always inside
         const int64_t t = b * S + s;
         tw.w[i] = bm_tiles[t * 16 + fr];
         tw.off[i] = tile_offsets[t];
@@ -283,44 +372,76 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
   auto fetch_windows = [&](TileWindows<TW>& tv, const TileWords<TW>& tw) {
 #pragma unroll
     for (int i = 0; i < TW; i += 2) {
-      // values stored before mine: a tile's values are ordered by column group (fg), then row (fr),
-      // i.e. in lane order, so this is the exclusive wave scan of the lanes' kept counts; the
-      // pair of tiles shares one scan in 16-bit halves (sums <= 512)
-      const uint32_t b0 = __builtin_amdgcn_ubfe(tw.w[i], 8 * fg, 8);
-      const uint32_t b1 = __builtin_amdgcn_ubfe(tw.w[i + 1], 8 * fg, 8);
-      const uint32_t pc = __popc(b0) | (__popc(b1) << 16);
-      const uint32_t ex = wave_inclusive_scan(pc) - pc;
+      if constexpr (kI8) {
+        // my 16 columns: half fg % 2 of my tile's word.  A tile's values are ordered by 16-column
+        // group, then row, i.e. in the order of the tile's 32 lanes, so the values before mine are
+        // the exclusive scan over my half of the wave (two units per scan in 16-bit halves)
+        const uint32_t h0 = __builtin_amdgcn_ubfe(tw.w[i], 16 * (fg & 1), 16);
+        const uint32_t h1 = __builtin_amdgcn_ubfe(tw.w[i + 1], 16 * (fg & 1), 16);
+        const uint32_t pc = __popc(h0) | (__popc(h1) << 16);
+        const uint32_t ex = half_inclusive_scan(pc) - pc;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint32_t byte = h ? b1 : b0;
-        const uint32_t oa = (uint32_t)tw.off[i + h] + (h ? ex >> 16 : ex & 0xffffu);
-        const uint32_t ob = oa + __popc(byte & 0xfu);
-        tv.byte[i + h] = byte;
-        __builtin_memcpy(&tv.v0[i + h], vbytes + 2u * oa, 8);
-        __builtin_memcpy(&tv.v1[i + h], vbytes + 2u * ob, 8);
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t hw = h ? h1 : h0;
+          const uint32_t oa = (uint32_t)tw.off[i + h] + (h ? ex >> 16 : ex & 0xffffu);
+          const uint32_t ob = oa + __popc(hw & 0xffu);   // nibbles 2 and 3 start after nibbles 0 and 1
+          tv.byte[i + h] = hw;
+          __builtin_memcpy(&tv.v0[i + h], vbytes + oa, 8);
+          __builtin_memcpy(&tv.v1[i + h], vbytes + ob, 8);
+        }
+      } else {
+        // values stored before mine: a tile's values are ordered by column group (fg), then row (fr),
+        // i.e. in lane order, so this is the exclusive wave scan of the lanes' kept counts; the
+        // pair of tiles shares one scan in 16-bit halves (sums <= 512)
+        const uint32_t b0 = __builtin_amdgcn_ubfe(tw.w[i], 8 * fg, 8);
+        const uint32_t b1 = __builtin_amdgcn_ubfe(tw.w[i + 1], 8 * fg, 8);
+        const uint32_t pc = __popc(b0) | (__popc(b1) << 16);
+        const uint32_t ex = wave_inclusive_scan(pc) - pc;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t byte = h ? b1 : b0;
+          const uint32_t oa = (uint32_t)tw.off[i + h] + (h ? ex >> 16 : ex & 0xffffu);
+          const uint32_t ob = oa + __popc(byte & 0xfu);
+          tv.byte[i + h] = byte;
+          __builtin_memcpy(&tv.v0[i + h], vbytes + 2u * oa, 8);
+          __builtin_memcpy(&tv.v1[i + h], vbytes + 2u * ob, 8);
+        }
       }
     }
   };
   auto expand_store = [&](const TileWindows<TW>& tv, uint32_t buf) {
 #pragma unroll
     for (int i = 0; i < TW; ++i) {
-      const u32x2 slo = lds_load8(lut_addr + 8u * (tv.byte[i] & 0xfu));
-      const u32x2 shi = lds_load8(lut_addr + 8u * (tv.byte[i] >> 4));
       u32x4 a;
-      a.x = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.x);
-      a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.y);
-      a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.x);
-      a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.y);
+      if constexpr (kI8) {
+        const uint32_t hw = tv.byte[i];
+        const uint32_t n0_ = hw & 15u, n1 = (hw >> 4) & 15u, n2 = (hw >> 8) & 15u, n3 = hw >> 12;
+        const uint32_t s0 = lds_load4(lut_addr + 20u * n0_);
+        const uint32_t s1 = lds_load4(lut_addr + 20u * n1 + 4u * __popc(n0_));
+        const uint32_t s2 = lds_load4(lut_addr + 20u * n2);
+        const uint32_t s3 = lds_load4(lut_addr + 20u * n3 + 4u * __popc(n2));
+        a.x = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, s0);
+        a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, s1);
+        a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, s2);
+        a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, s3);
+      } else {
+        const u32x2 slo = lds_load8(lut_addr + 8u * (tv.byte[i] & 0xfu));
+        const u32x2 shi = lds_load8(lut_addr + 8u * (tv.byte[i] >> 4));
+        a.x = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.x);
+        a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.y);
+        a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.x);
+        a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.y);
+      }
       const uint32_t at = buf + pf_chunk(16 * ((TW / 2) * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);
       *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)at) = a;
     }
   };
 
-  f32x4 acc[FN][4];
+  Acc acc[FN][4];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
   // Pipeline: bitmask words three stages ahead, value windows and X slabs two
   // ahead (X in alternating register sets, the loop unrolled by two stages).
@@ -330,17 +451,17 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
   // and LDS work can interleave with the matrix cores; one barrier per stage.
   // Stages are counted within the k-group (global stage sb + st); data steps
   // are guarded by the group's nl stages, barriers by the uniform nh.
-  const SlabSrc<RR> xsrc(X, M, K, m0, tid);
+  const SlabSrc<RR> xsrc(g.X, M, Kh, m0, tid);
   Slab<BM / RR> x0, x1;
   TileWords<TW> tw;
   TileWindows<TW> tv;
   if (nl > 0) {
     fetch_words(tw, sb);
-    xsrc.template fetch<kChecked>(x0, K, (int64_t)kPfBK * sb);
+    xsrc.template fetch<kChecked>(x0, Kh, (int64_t)kPfBK * sb);
     fetch_windows(tv, tw);                             // stage 0
     if (nl > 1) {
       fetch_words(tw, sb + 1);
-      xsrc.template fetch<kChecked>(x1, K, (int64_t)kPfBK * (sb + 1));
+      xsrc.template fetch<kChecked>(x1, Kh, (int64_t)kPfBK * (sb + 1));
     }
   }
   __syncthreads();                                     // the selector table
@@ -362,7 +483,7 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
       if (st + 2 < nl) {
         fetch_windows(tv, tw);                         // stage st + 2 (its words were fetched a stage ago)
         if (st + 3 < nl) fetch_words(tw, sb + st + 3);
-        xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (sb + st + 2));
+        xsrc.template fetch<kChecked>(xn, Kh, (int64_t)kPfBK * (sb + st + 2));
       }
     }
     if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
@@ -372,14 +493,19 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
     step(st, x0, x1);                                  // stage st + 1 from set 1, stage st + 2 -> set 0
     if (st + 1 < nh) step(st + 1, x1, x0);             // stage st + 2 from set 0, stage st + 3 -> set 1
   }
-  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) {
+    if constexpr (kI8)
+      pf_store_i8<FN>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+    else
+      pf_store<T, FN>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
+  }
 }
 
 template <class T, int BN, int BM, int NW, int KS, bool kChecked>
-__global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
-    k_dense_prefill(const uint16_t* __restrict__ X, int64_t M, int64_t K, const uint16_t* __restrict__ W, int64_t N,
-                    uint16_t* __restrict__ Y) {
+__global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(const PfArgs g) {
   extern __shared__ __align__(16) unsigned char dsm[];
+  constexpr bool kI8 = std::is_same<T, I8P>::value;
+  using Acc = typename MfmaP<T>::acc_t;
   constexpr int NT = 64 * NW;                         // threads of one k-group
   const int kh = KS == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x / NT);
   const int tid = (int)threadIdx.x - kh * NT;
@@ -387,8 +513,9 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
   const int lane = threadIdx.x & 63;
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
-  const int S = (int)tile_steps(K);
-  const int nst = (S + 1) / 2;
+  const int64_t M = g.M, N = g.N, K = g.K;
+  const int64_t Kh = kI8 ? K / 2 : K;
+  const int nst = (int)((Kh + kPfBK - 1) / kPfBK);
   const int nh = (nst + KS - 1) / KS;
   const int sb = kh * nh;
   const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;
@@ -402,25 +529,25 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
   const uint32_t abuf[2] = {lds_off(gb), lds_off(gb + BN * kPfRow)};
   const uint32_t bbuf[2] = {lds_off(gb + 2 * BN * kPfRow), lds_off(gb + (2 * BN + BM) * kPfRow)};
 
-  f32x4 acc[FN][4];
+  Acc acc[FN][4];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
   // Global loads run two stages ahead of the multiplication: register sets
   // (x0, w0) and (x1, w1) alternate, the loop unrolled by two stages.  Stage
   // st + 1 is stored to LDS at the start of stage st, so one barrier per stage
   // both publishes it and retires stage st's reads.
-  const SlabSrc<RR> xsrc(X, M, K, m0, tid), wsrc(W, N, K, n0, tid);
+  const SlabSrc<RR> xsrc(g.X, M, Kh, m0, tid), wsrc(g.W, N, Kh, n0, tid);
   Slab<BM / RR> x0, x1;
   Slab<BN / RR> w0, w1;
   if (nl > 0) {
-    xsrc.template fetch<kChecked>(x0, K, (int64_t)kPfBK * sb);
-    wsrc.template fetch<kChecked>(w0, K, (int64_t)kPfBK * sb);
+    xsrc.template fetch<kChecked>(x0, Kh, (int64_t)kPfBK * sb);
+    wsrc.template fetch<kChecked>(w0, Kh, (int64_t)kPfBK * sb);
     if (nl > 1) {
-      xsrc.template fetch<kChecked>(x1, K, (int64_t)kPfBK * (sb + 1));
-      wsrc.template fetch<kChecked>(w1, K, (int64_t)kPfBK * (sb + 1));
+      xsrc.template fetch<kChecked>(x1, Kh, (int64_t)kPfBK * (sb + 1));
+      wsrc.template fetch<kChecked>(w1, Kh, (int64_t)kPfBK * (sb + 1));
     }
     slab_store<RR>(w0, abuf[0], tid);
     slab_store<RR>(x0, bbuf[0], tid);
@@ -437,8 +564,8 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
       slab_store<RR>(xl, bbuf[cur ^ 1], tid);
     }
     if (st + 2 < nl) {
-      xsrc.template fetch<kChecked>(xn, K, (int64_t)kPfBK * (sb + st + 2));
-      wsrc.template fetch<kChecked>(wn_, K, (int64_t)kPfBK * (sb + st + 2));
+      xsrc.template fetch<kChecked>(xn, Kh, (int64_t)kPfBK * (sb + st + 2));
+      wsrc.template fetch<kChecked>(wn_, Kh, (int64_t)kPfBK * (sb + st + 2));
     }
     if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (st + 1 < nh) __syncthreads();
@@ -447,7 +574,12 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS))
     step(st, x0, w0, x1, w1);                          // stage st + 2 -> set 0, stage st + 1 from set 1
     if (st + 1 < nh) step(st + 1, x1, w1, x0, w0);     // stage st + 3 -> set 1, stage st + 2 from set 0
   }
-  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) pf_store<T, FN>(acc, Y, M, N, n0, m0, wn, wm, fr, fg);
+  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) {
+    if constexpr (kI8)
+      pf_store_i8<FN>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+    else
+      pf_store<T, FN>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
+  }
 }
 
 // Raise a kernel's dynamic LDS limit (above the 64 KB default) once.
@@ -481,65 +613,108 @@ constexpr bool pf_inside(int64_t N, int64_t M, int64_t K, int BN, int BM) {
 }
 
 template <class T, int BN, int BM, int NW, int KS, bool kChecked>
-hipError_t sparse_prefill_launch(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
+hipError_t sparse_prefill_launch(const PfArgs& a, hipStream_t s) {
   auto* kernel = k_sparse_prefill<T, BN, BM, NW, KS, kChecked>;
   static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((Wc.rows + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW * KS);
-  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, static_cast<const uint16_t*>(X), M, Wc.cols,
-                     Wc.bitmask, static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows,
-                     static_cast<uint16_t*>(Y));
+  const dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
+  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, a);
   return hipGetLastError();
 }
 
+// Row length of the activations in 16-bit units.
+template <class T>
+constexpr int64_t pf_units(int64_t K) { return std::is_same<T, I8P>::value ? K / 2 : K; }
+
 template <class T, int BN, int BM, int NW, int KS>
-hipError_t sparse_prefill_tile(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  return pf_inside(Wc.rows, M, Wc.cols, BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false>(X, M, Wc, Y, s)
-                                                : sparse_prefill_launch<T, BN, BM, NW, KS, true>(X, M, Wc, Y, s);
+hipError_t sparse_prefill_tile(const PfArgs& a, hipStream_t s) {
+  return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false>(a, s)
+                                                       : sparse_prefill_launch<T, BN, BM, NW, KS, true>(a, s);
 }
 
 template <class T>
-hipError_t sparse_prefill_t(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
-  if (pf_large_tile(Wc.rows, M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(X, M, Wc, Y, s);
-  return pf_split_k(Wc.rows, M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(X, M, Wc, Y, s)
-                                : sparse_prefill_tile<T, 64, 128, 4, 1>(X, M, Wc, Y, s);
+hipError_t sparse_prefill_t(const PfArgs& a, hipStream_t s) {
+  if (pf_large_tile(a.N, a.M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(a, s);
+  return pf_split_k(a.N, a.M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(a, s)
+                              : sparse_prefill_tile<T, 64, 128, 4, 1>(a, s);
 }
 
 template <class T, int BN, int BM, int NW, int KS, bool kChecked>
-hipError_t dense_prefill_launch(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y,
-                                hipStream_t s) {
+hipError_t dense_prefill_launch(const PfArgs& a, hipStream_t s) {
   auto* kernel = k_dense_prefill<T, BN, BM, NW, KS, kChecked>;
   static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)), block(64 * NW * KS);
-  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, static_cast<const uint16_t*>(X), M, K,
-                     static_cast<const uint16_t*>(W), N, static_cast<uint16_t*>(Y));
+  const dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
+  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, a);
   return hipGetLastError();
 }
 
 template <class T, int BN, int BM, int NW, int KS>
-hipError_t dense_prefill_tile(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  return pf_inside(N, M, K, BN, BM) ? dense_prefill_launch<T, BN, BM, NW, KS, false>(X, M, W, N, K, Y, s)
-                                    : dense_prefill_launch<T, BN, BM, NW, KS, true>(X, M, W, N, K, Y, s);
+hipError_t dense_prefill_tile(const PfArgs& a, hipStream_t s) {
+  return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? dense_prefill_launch<T, BN, BM, NW, KS, false>(a, s)
+                                                       : dense_prefill_launch<T, BN, BM, NW, KS, true>(a, s);
 }
 
 template <class T>
-hipError_t dense_prefill_t(const void* X, int64_t M, const void* W, int64_t N, int64_t K, void* Y, hipStream_t s) {
-  if (pf_large_tile(N, M)) return dense_prefill_tile<T, 128, 256, 8, 1>(X, M, W, N, K, Y, s);
-  return pf_split_k(N, M) ? dense_prefill_tile<T, 64, 128, 4, 2>(X, M, W, N, K, Y, s)
-                          : dense_prefill_tile<T, 64, 128, 4, 1>(X, M, W, N, K, Y, s);
+hipError_t dense_prefill_t(const PfArgs& a, hipStream_t s) {
+  if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1>(a, s);
+  return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2>(a, s)
+                              : dense_prefill_tile<T, 64, 128, 4, 1>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_sparse_prefill(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s) {
-  return Wc.dtype == SPL_BF16 ? sparse_prefill_t<Bf16>(X, M, Wc, Y, s) : sparse_prefill_t<F16>(X, M, Wc, Y, s);
+  if (Wc.nnz == 0) return launch_zero_fill(Y, M * Wc.rows, s);
+  PfArgs a{};
+  a.X = static_cast<const uint16_t*>(X);
+  a.bm = Wc.bitmask;
+  a.values = static_cast<const unsigned char*>(Wc.values);
+  a.toff = Wc.tile_offsets;
+  a.M = M, a.N = Wc.rows, a.K = Wc.cols;
+  a.Y = static_cast<uint16_t*>(Y);
+  return Wc.dtype == SPL_BF16 ? sparse_prefill_t<Bf16>(a, s) : sparse_prefill_t<F16>(a, s);
 }
 
 hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
                                 void* Y, hipStream_t s) {
-  return dtype == SPL_BF16 ? dense_prefill_t<Bf16>(X, M, W, N, K, Y, s) : dense_prefill_t<F16>(X, M, W, N, K, Y, s);
+  PfArgs a{};
+  a.X = static_cast<const uint16_t*>(X);
+  a.W = static_cast<const uint16_t*>(W);
+  a.M = M, a.N = N, a.K = K;
+  a.Y = static_cast<uint16_t*>(Y);
+  return dtype == SPL_BF16 ? dense_prefill_t<Bf16>(a, s) : dense_prefill_t<F16>(a, s);
+}
+
+// int8 (K % 16 == 0: activation rows are whole 16-byte pieces).
+hipError_t launch_sparse_prefill_i8(const spl_int8_task& t, int64_t M, hipStream_t s) {
+  const spl_matrix& W = *t.Wq;
+  if (W.nnz == 0) {
+    if (t.acc_out) {
+      const hipError_t e = launch_zero_fill(t.acc_out, 2 * M * W.rows, s);
+      if (e != hipSuccess) return e;
+    }
+    return launch_zero_fill(t.Y, M * W.rows, s);     // (float(0) * sx) * sw = +0
+  }
+  PfArgs a{};
+  a.X = reinterpret_cast<const uint16_t*>(t.Xq);
+  a.bm = W.bitmask;
+  a.values = static_cast<const unsigned char*>(W.values);
+  a.toff = W.tile_offsets;
+  a.M = M, a.N = W.rows, a.K = W.cols;
+  a.Y = static_cast<uint16_t*>(t.Y);
+  a.sx = t.x_scales, a.sw = t.w_scales, a.acc = t.acc_out;
+  return sparse_prefill_t<I8P>(a, s);
+}
+
+hipError_t launch_dense_prefill_i8(const spl_dense_int8_task& t, int64_t M, hipStream_t s) {
+  PfArgs a{};
+  a.X = reinterpret_cast<const uint16_t*>(t.Xq);
+  a.W = reinterpret_cast<const uint16_t*>(t.Wq);
+  a.M = M, a.N = t.N, a.K = t.K;
+  a.Y = static_cast<uint16_t*>(t.Y);
+  a.sx = t.x_scales, a.sw = t.w_scales, a.acc = t.acc_out;
+  return dense_prefill_t<I8P>(a, s);
 }
 
 }  // namespace spl

@@ -138,6 +138,8 @@ hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t
 // Sparse-quantized kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
 hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s);
 hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s);
+hipError_t launch_sparse_prefill_i8(const spl_int8_task& t, int64_t M, hipStream_t s);
+hipError_t launch_dense_prefill_i8(const spl_dense_int8_task& t, int64_t M, hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

@@ -134,8 +134,9 @@ def _tie_cases(count, seed=0):
     return out[:count]
 
 
-def test_int8_epilogue_rounds_each_product(orc, spl):
-    cases = _tie_cases(48)
+@pytest.mark.parametrize("count", [48, 160])          # 160: the batch takes the prefill tiling
+def test_int8_epilogue_rounds_each_product(orc, spl, count):
+    cases = _tie_cases(count)
     M = N = len(cases)
     K = 32
     Xq = np.zeros((M, K), dtype=np.int8)
@@ -153,12 +154,13 @@ def test_int8_epilogue_rounds_each_product(orc, spl):
     _assert_equal(y, y_ref, "Y")
 
 
-@pytest.mark.parametrize("M", [1, 16, 40, 70])
+@pytest.mark.parametrize("M", [1, 16, 40, 70, 130])
 def test_int8_group_matches_oracle_and_single_calls(orc, spl, M):
     """A group of three layers with different N and K (one launch for all):
     every task's int32 sums and fp16 outputs equal the oracle and the single
     calls bit for bit, sparse and dense (M = 1: staged activations; 16, 40,
-    70: one, two and four batch fragments, 70 on two batch blocks)."""
+    70: one, two and four batch fragments, 70 on two batch blocks; 130: the
+    prefill tiling, one launch per task)."""
     import torch
 
     shapes = [(40, 96, 0.7), (100, 528, 0.5), (33, 96, 0.9)]
@@ -182,6 +184,96 @@ def test_int8_group_matches_oracle_and_single_calls(orc, spl, M):
             _assert_equal(y.cpu().view(torch.int16).numpy().view(np.uint16), y_ref, f"{what} group task {i} Y M={M}")
         single = spl.sparse_linear_int8(Xqs[i], sxs[i], Wcs[i], sws[i])
         assert torch.equal(single.view(torch.int16), outs[i].view(torch.int16))
+
+
+PREFILL_I8_M = [128, 129, 300]
+
+
+def _sample_rows(M, seed, count=62):
+    rows = np.concatenate([[0, M - 1], np.random.default_rng(seed).choice(np.arange(1, M - 1), count, replace=False)])
+    return np.sort(rows)
+
+
+@pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (33, 64, 0.7), (130, 1008, 0.7), (64, 4096, 0.5), (200, 336, 0.0),
+                                   (17, 512, 1.0), (48, 2064, 0.9), (300, 144, 0.5)])
+def test_int8_prefill_small(orc, spl, N, K, s):
+    """Batches of 128 rows and more take the MFMA-tiled prefill kernel: ragged
+    N, M and K (a partial last 128-byte stage) compared in full, bit for bit."""
+    Wq, mask, sw = synth.int8_weight(620 + N, N, K, s)
+    Xq, sx = synth.int8_activations(720 + K, max(PREFILL_I8_M), K)
+    p = orc.pack(Wq, "i8", mask)
+    for M in PREFILL_I8_M:
+        acc_ref, y_ref = orc.linear_i8(Xq[:M], sx[:M], p, sw)
+        acc, y = _run_sparse(spl, Xq[:M], sx[:M], Wq, mask, sw)
+        _assert_equal(acc, acc_ref, f"acc N={N} K={K} s={s} M={M}")
+        _assert_equal(y, y_ref, f"Y N={N} K={K} s={s} M={M}")
+
+
+def _run_dense(spl, Xq, sx, Wd, sw):
+    import torch
+
+    M, N = Xq.shape[0], Wd.shape[0]
+    acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    Y = spl.dense_linear_int8(to_dev(Xq, "i8"), torch.from_numpy(sx).cuda(), to_dev(Wd, "i8"),
+                              torch.from_numpy(sw).cuda(), acc_out=acc)
+    return acc.cpu().numpy(), Y.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("N,K,M,s", [(2000, 144, 4100, 0.7), (2048, 128, 8192, 0.7), (256, 256, 256, 0.5)])
+def test_int8_prefill_grids(orc, spl, N, K, M, s):
+    """A ragged grid of at least one 128 x 256 block per CU, an aligned grid of
+    two blocks per CU (branch-free loads) and an aligned grid small enough to
+    split the reduction in two: compared in full, sparse and dense."""
+    Wq, mask, sw = synth.int8_weight(950 + N, N, K, s)
+    Xq, sx = synth.int8_activations(951 + K, M, K)
+    acc_ref, y_ref = orc.linear_i8(Xq, sx, orc.pack(Wq, "i8", mask), sw)
+    acc, y = _run_sparse(spl, Xq, sx, Wq, mask, sw)
+    _assert_equal(acc, acc_ref, f"acc N={N} K={K} M={M}")
+    _assert_equal(y, y_ref, f"Y N={N} K={K} M={M}")
+    acc, y = _run_dense(spl, Xq, sx, np.where(mask.astype(bool), Wq, np.int8(0)), sw)
+    _assert_equal(acc, acc_ref, f"dense acc N={N} K={K} M={M}")
+    _assert_equal(y, y_ref, f"dense Y N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("name,M,s", [("q", 512, 0.7), ("gate", 512, 0.7), ("down", 512, 0.7), ("up", 2048, 0.5),
+                                      ("o", 2048, 0.7)])
+def test_int8_prefill_llama_shapes_sampled(orc, spl, name, M, s):
+    """Llama-2-7B shapes at the prefill batch sizes: every output of 64 rows
+    (the first, the last and 62 seeded ones) equals the oracle bit for bit;
+    the rows are independent, so the oracle runs on those rows alone."""
+    j = [n for n, _, _ in synth.LLAMA2_7B_LINEARS].index(name)
+    _, N, K = synth.LLAMA2_7B_LINEARS[j]
+    Wq, mask, sw = synth.int8_weight(synth.weight_seed(0, j), N, K, s)
+    Xq, sx = synth.int8_activations(synth.activation_seed(j), M, K)
+    rows = _sample_rows(M, N + M)
+    acc_ref, y_ref = orc.linear_i8(Xq[rows], sx[rows], orc.pack(Wq, "i8", mask), sw)
+    acc, y = _run_sparse(spl, Xq, sx, Wq, mask, sw)
+    _assert_equal(acc[rows], acc_ref, f"{name} acc M={M}")
+    _assert_equal(y[rows], y_ref, f"{name} Y M={M}")
+
+
+def test_dense_int8_prefill(orc, spl):
+    """The dense int8 comparator at prefill batch sizes: ragged shapes in full,
+    the gate shape at M = 512 on 64 sampled rows."""
+    rng = np.random.default_rng(77)
+    for N, K in ((100, 1008), (130, 272), (16, 64)):
+        Wq = rng.integers(-128, 128, size=(N, K)).astype(np.int8)
+        sw = rng.uniform(1e-4, 1e-2, size=N).astype(np.float32)
+        Xq, sx = synth.int8_activations(78, 300, K)
+        for M in (128, 129, 300):
+            acc_ref, y_ref = orc.dense_i8(Xq[:M], sx[:M], Wq, sw)
+            acc, y = _run_dense(spl, Xq[:M], sx[:M], Wq, sw)
+            _assert_equal(acc, acc_ref, f"dense acc N={N} K={K} M={M}")
+            _assert_equal(y, y_ref, f"dense Y N={N} K={K} M={M}")
+    N, K, M = 11008, 4096, 512
+    Wq = rng.integers(-128, 128, size=(N, K)).astype(np.int8)
+    sw = rng.uniform(1e-4, 1e-2, size=N).astype(np.float32)
+    Xq, sx = synth.int8_activations(79, M, K)
+    rows = _sample_rows(M, 80)
+    acc_ref, y_ref = orc.dense_i8(Xq[rows], sx[rows], Wq, sw)
+    acc, y = _run_dense(spl, Xq, sx, Wq, sw)
+    _assert_equal(acc[rows], acc_ref, "dense gate acc M=512")
+    _assert_equal(y[rows], y_ref, "dense gate Y M=512")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])

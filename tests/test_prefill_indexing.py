@@ -38,7 +38,7 @@ def _constants():
     assert "constexpr int kPfRow = kPfBK * 2;" in src
     for line in ("constexpr int TW = BN / 8 / NW;",
                  "const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);",
-                 "const int s = 2 * st + (i & 1);",
+                 "const int s = kI8 ? 4 * st + 2 * (i & 1) + (fg >> 1) : 2 * st + (i & 1);",
                  "const int64_t t = ok ? b * S + s : 0;",
                  "tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;",
                  "const uint32_t pc = __popc(b0) | (__popc(b1) << 16);",
@@ -47,9 +47,9 @@ def _constants():
                  "__builtin_memcpy(&tv.v0[i + h], vbytes + 2u * oa, 8);",
                  "__builtin_memcpy(&tv.v1[i + h], vbytes + 2u * ob, 8);",
                  "const uint32_t at = buf + pf_chunk(16 * ((TW / 2) * wave + (i >> 1)) + fr, 4 * (i & 1) + fg);",
-                 "if (pf_large_tile(Wc.rows, M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(X, M, Wc, Y, s);",
-                 "return pf_split_k(Wc.rows, M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(X, M, Wc, Y, s)",
-                 ": sparse_prefill_tile<T, 64, 128, 4, 1>(X, M, Wc, Y, s);",
+                 "if (pf_large_tile(a.N, a.M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(a, s);",
+                 "return pf_split_k(a.N, a.M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(a, s)",
+                 ": sparse_prefill_tile<T, 64, 128, 4, 1>(a, s);",
                  "fetch_words(tw, sb + 1);",
                  "if (st + 3 < nl) fetch_words(tw, sb + st + 3);"):
         assert line in src, f"kernel changed: update this replay ({line})"
@@ -161,8 +161,8 @@ def _inside_rule():
     src = open(SRC).read()
     rule = "return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;"
     assert rule in src, "launch rule for the unchecked kernels changed: update this replay"
-    for line in ("? sparse_prefill_launch<T, BN, BM, NW, KS, false>(X, M, Wc, Y, s)",
-                 "? dense_prefill_launch<T, BN, BM, NW, KS, false>(X, M, W, N, K, Y, s)",
+    for line in ("return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false>(a, s)",
+                 "return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? dense_prefill_launch<T, BN, BM, NW, KS, false>(a, s)",
                  "const int64_t t = b * S + s;",
                  "for (int i = 0; i < P; ++i) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);"):
         assert line in src, f"kernel changed: update this replay ({line})"
@@ -200,7 +200,7 @@ def _split_rule():
                  "if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);",
                  "if (st + 1 < nh) __syncthreads();",
                  "unsigned char* gb = dsm + kh * pf_lds(BN, BM);",
-                 "f32x4* part = reinterpret_cast<f32x4*>(dsm);     // [FN * 4][NT]"):
+                 "A* part = reinterpret_cast<A*>(dsm);             // [FN * 4][NT]"):
         assert line in src, f"split-K schedule changed: update this replay ({line})"
 
 
@@ -225,3 +225,110 @@ def test_split_k_stages_partition(nst, KS):
     BN, BM, NW = 64, 128, 4
     lds = 2 * (BN + BM) * 2 * bk
     assert (BN // 32) * 4 * 64 * NW * 16 <= KS * lds
+
+
+
+# ---------------------------------------------------------------- int8 payloads
+
+def _i8_lines():
+    src = open(SRC).read()
+    for line in ("const uint32_t h0 = __builtin_amdgcn_ubfe(tw.w[i], 16 * (fg & 1), 16);",
+                 "const uint32_t ex = half_inclusive_scan(pc) - pc;",
+                 "const uint32_t ob = oa + __popc(hw & 0xffu);   // nibbles 2 and 3 start after nibbles 0 and 1",
+                 "__builtin_memcpy(&tv.v0[i + h], vbytes + oa, 8);",
+                 "__builtin_memcpy(&tv.v1[i + h], vbytes + ob, 8);",
+                 "const uint32_t s1 = lds_load4(lut_addr + 20u * n1 + 4u * __popc(n0_));",
+                 "const uint32_t s3 = lds_load4(lut_addr + 20u * n3 + 4u * __popc(n2));",
+                 "if (threadIdx.x < 80) lut[threadIdx.x] = pf_i8_selector(threadIdx.x / 5, threadIdx.x % 5);",
+                 "const int nst = (int)((Kh + kPfBK - 1) / kPfBK);   // stages of 128 bytes per row: 2 tiles (4 for int8)",
+                 "const int64_t Kh = kI8 ? K / 2 : K;                // activation row in 16-bit units"):
+        assert line in src, f"int8 expansion changed: update this replay ({line})"
+
+
+def _i8_selector(nib, p):
+    sel = 0
+    for j in range(4):
+        b = 0x0C
+        if (nib >> j) & 1:
+            b = p + _popc(nib & ((1 << j) - 1))
+        sel |= b << (8 * j)
+    return sel
+
+
+@pytest.mark.parametrize("N,K,s", [(16, 128, 0.5), (48, 400, 0.7), (130, 256, 0.0), (33, 528, 1.0), (70, 1040, 0.9)])
+def test_prefill_i8_schedule_and_expansion(orc, N, K, s):
+    """int8 payloads: per stage (128 columns) a wave expands two tile pairs of
+    its row block; lane (fr, fg) takes tile 4 st + 2 (i % 2) + fg / 2, columns
+    16 (fg % 2) .. +16 of row fr; its values start at the tile offset plus the
+    exclusive scan over the tile's 32 lanes; two 8-byte windows (nibbles 0-1
+    and 2-3) and the offset-aware selectors rebuild the 16 dense bytes."""
+    _i8_lines()
+    bk, shapes = _constants()
+    row_bytes = 2 * bk
+    Wq, mask, _ = synth.int8_weight(77 + N + K, N, K, s)
+    T = orc.pack_tiled(Wq, "i8", mask)
+    vbytes = np.concatenate([T.values.view(np.uint8), np.zeros(16, np.uint8)])
+    limit = T.nnz + 16
+    dense = np.where(mask.astype(bool), Wq, 0).astype(np.int8).view(np.uint8)
+    S, B = -(-K // 32), -(-N // 16)
+    nst = -(-(K // 2) // bk)
+    bm = T.bitmask.reshape(-1).astype(np.uint64)
+    offs = T.tile_offsets.astype(np.int64)
+    for BN, NW in shapes:
+        TW = BN // 8 // NW
+        for wg in range(-(-N // BN)):
+            nb0 = wg * BN // 16
+            for st in range(nst):
+                seen = set()
+                for wave in range(NW):
+                    for i in range(0, TW, 2):
+                        units = []
+                        for h in range(2):
+                            b = nb0 + (TW // 2) * wave + ((i + h) >> 1)
+                            lanes = []
+                            for lane in range(64):
+                                fr, fg = lane & 15, lane >> 4
+                                sk = 4 * st + 2 * ((i + h) & 1) + (fg >> 1)
+                                ok = b < B and sk < S
+                                t = b * S + sk if ok else 0
+                                w = int(bm[t * 16 + fr]) if ok else 0
+                                hw = (w >> (16 * (fg & 1))) & 0xFFFF
+                                lanes.append((b, sk, ok, int(offs[t]), hw))
+                                if ok:
+                                    seen.add((b, sk))
+                            units.append(lanes)
+                        cnt = np.array([[_popc(units[h][l][4]) for l in range(64)] for h in range(2)])
+                        ex = np.zeros((2, 64), np.int64)
+                        for h in range(2):
+                            for half in range(2):
+                                seg = cnt[h, 32 * half:32 * half + 32]
+                                ex[h, 32 * half:32 * half + 32] = np.cumsum(seg) - seg
+                                assert seg.sum() <= 512
+                        for h in range(2):
+                            for lane in range(64):
+                                fr, fg = lane & 15, lane >> 4
+                                b, sk, ok, off, hw = units[h][lane]
+                                oa = off + int(ex[h, lane])
+                                ob = oa + _popc(hw & 0xFF)
+                                for o in (oa, ob):
+                                    assert 0 <= o and o + 8 <= limit, (wg, st, wave, i + h, lane)
+                                at = _chunk(16 * ((TW // 2) * wave + ((i + h) >> 1)) + fr, 4 * ((i + h) & 1) + fg,
+                                            row_bytes)
+                                assert 0 <= at and at + 16 <= BN * row_bytes
+                                v0 = vbytes[oa:oa + 8].view(np.uint32)
+                                v1 = vbytes[ob:ob + 8].view(np.uint32)
+                                n = [(hw >> (4 * j)) & 15 for j in range(4)]
+                                got = [_perm(v0[1], v0[0], _i8_selector(n[0], 0)),
+                                       _perm(v0[1], v0[0], _i8_selector(n[1], _popc(n[0]))),
+                                       _perm(v1[1], v1[0], _i8_selector(n[2], 0)),
+                                       _perm(v1[1], v1[0], _i8_selector(n[3], _popc(n[2])))]
+                                got = np.array(got, dtype=np.uint32).view(np.uint8)
+                                exp = np.zeros(16, np.uint8)
+                                row, k0 = 16 * b + fr, 32 * sk + 16 * (fg & 1)
+                                if ok and row < N and k0 < K:
+                                    seg = dense[row, k0:min(k0 + 16, K)]
+                                    exp[:seg.size] = seg
+                                assert np.array_equal(got, exp), (wg, st, wave, i + h, lane)
+                want = {(b, sk) for b in range(nb0, min(nb0 + BN // 16, B)) for sk in range(4 * st, 4 * st + 4)
+                        if sk < S}
+                assert seen == want
