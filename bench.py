@@ -368,8 +368,9 @@ def run_prefill(args):
 
 
 def _gen_int8(args):
-    layer, j, N, K = args
-    Wq, mask, sw = synth.int8_weight(synth.weight_seed(layer, j), N, K, 0.7)
+    layer, j, N, K = args[:4]
+    sparsity = args[4] if len(args) > 4 else 0.7
+    Wq, mask, sw = synth.int8_weight(synth.weight_seed(layer, j), N, K, sparsity)
     return layer, j, Wq, mask, sw
 
 
@@ -465,6 +466,110 @@ def run_int8(args):
                  cpu, {"per_M": per_M}, dtype="i8")
 
 
+MFMA_I8_PEAK_TOPS = 5000.0
+# the four distinct inputs of a decoder layer's linears: q|k|v share one, gate|up share one
+INPUT_OF_GROUP = {(0, 1, 2): 0, (3,): 3, (4, 5): 4, (6,): 6}
+
+
+def run_int8_prefill(args):
+    """One layer's seven matrices with int8 weights at prefill batch sizes M =
+    512 and 2048: each step quantizes the layer's four distinct bf16 inputs per
+    token, then runs the seven sparse int8 linears (grouped as q|k|v, o,
+    gate|up, down)."""
+    torch, spl = _need_gpu()
+    shapes = synth.LLAMA2_7B_LINEARS
+    jobs = [(0, j, N, K, args.sparsity) for j, (_, N, K) in enumerate(shapes)]
+    host = [None] * len(shapes)
+    with cf.ProcessPoolExecutor(max_workers=min(args.workers, len(jobs))) as ex:
+        for _, j, Wq, mask, sw in ex.map(_gen_int8, jobs):
+            host[j] = (Wq, mask, sw)
+    mats = []
+    for Wq, mask, sw in host:
+        Wd = torch.from_numpy(Wq).cuda()
+        mats.append((spl.pack_sparse(Wd, torch.from_numpy(mask).cuda()), Wd if not args.no_dense else None,
+                     torch.from_numpy(sw).cuda()))
+    Ms = [512, 2048]
+    xb = {j: _to_dev(synth.activations(synth.activation_seed(j), max(Ms), shapes[j][2], "bf16"), "bf16", torch)
+          for j in INPUT_OF_GROUP.values()}
+    xin = {(M, j): xb[j][:M].contiguous() for M in Ms for j in xb}
+    xq = {(M, j): torch.empty((M, shapes[j][2]), dtype=torch.int8, device="cuda") for M in Ms for j in xb}
+    sx = {(M, j): torch.empty((M,), dtype=torch.float32, device="cuda") for M in Ms for j in xb}
+    ys = {(M, j): torch.empty((M, N), dtype=torch.float16, device="cuda") for M in Ms for j, (_, N, _) in
+          enumerate(shapes)}
+    units = [(M, grp) for M in Ms for grp in GROUPED]
+
+    def quantize(M, grp):
+        i = INPUT_OF_GROUP[grp]
+        spl.quantize_rows_i8(xin[(M, i)], out=xq[(M, i)], scales=sx[(M, i)])
+
+    def linears(M, grp, dense=False):
+        i = INPUT_OF_GROUP[grp]
+        call = spl.dense_linear_int8_group if dense else spl.sparse_linear_int8_group
+        call([xq[(M, i)]] * len(grp), [sx[(M, i)]] * len(grp), [mats[j][1 if dense else 0] for j in grp],
+             [mats[j][2] for j in grp], outs=[ys[(M, j)] for j in grp])
+
+    def step_fn(li, u):
+        quantize(*u)
+        linears(*u)
+
+    for u in units:                                     # quantized inputs in place before linears-only timing
+        quantize(*u)
+    torch.cuda.synchronize()
+    sp_wall, sp_gpu = _timed(units, step_fn, args.steps, args.warmup, [0])
+    _, lin_gpu = _timed(units, lambda li, u: linears(*u), args.steps, args.warmup, [0])
+    launches = len(Ms) * len(shapes)
+    launch_ms = lin_gpu / launches
+    ops = sum(2.0 * M * N * K for M in Ms for (_, N, K) in shapes)
+    achieved = ops / launches / (launch_ms * 1e-3) / 1e12
+    per_M = {}
+    for M in Ms:
+        uM = [u for u in units if u[0] == M]
+        reps = max(10, args.steps // 4)
+        _, g = _timed(uM, step_fn, reps, 2, [0])
+        _, gl = _timed(uM, lambda li, u: linears(*u), reps, 2, [0])
+        _, gq = _timed(uM, lambda li, u: quantize(*u), reps, 2, [0])
+        f = sum(2.0 * M * N * K for (_, N, K) in shapes)
+        qbytes = sum(3 * M * shapes[j][2] + 4 * M for j in xb)
+        d = {"layer_us": round(g * 1e3, 2), "linears_us": round(gl * 1e3, 2),
+             "linears_dense_equiv_tops": round(f / (gl * 1e-3) / 1e12, 1), "quantize_us": round(gq * 1e3, 2),
+             "quantize_hbm_gbs": round(qbytes / (gq * 1e-3) / 1e9, 1)}
+        if not args.no_dense:
+            _, gd = _timed(uM, lambda li, u: linears(*u, dense=True), reps, 2, [0])
+            d.update({"dense_linears_us": round(gd * 1e3, 2), "dense_tops": round(f / (gd * 1e-3) / 1e12, 1),
+                      "speedup_vs_dense": round(gd / gl, 3)})
+        per_M[str(M)] = d
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        threads = oracle.max_threads()
+        rows = 64
+        packs = [oracle.pack(Wq, "i8", mask) for Wq, mask, _ in host]
+        xh = {j: synth.activations(synth.activation_seed(j), rows, shapes[j][2], "bf16") for j in xb}
+
+        def one():
+            q = {j: oracle.quantize_rows_i8(xh[j], "bf16") for j in xh}
+            for grp, i in INPUT_OF_GROUP.items():
+                for j in grp:
+                    oracle.linear_i8(q[i][0], q[i][1], packs[j], host[j][2], nthreads=threads)
+
+        reps, dt = _oracle_repeat(one)
+        cpu = {"value": round(reps * rows / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"{rows} tokens through the whole step (the four inputs quantized per token, the seven "
+                         f"int8 matrices with int64 sums and the fp16 epilogue), repeated {reps} times "
+                         f"({dt:.1f} s on {threads} threads)"}
+    return _line(args, "sparse-quantized prefill tokens/s, Llama-2-7B layer shapes",
+                 round(sum(Ms) / (sp_wall * 1e-3), 1), "tokens/s", sp_wall,
+                 f"Llama-2-7B decoder layer, 7 linears (q|k|v, o, gate|up, down), int8 weights (per-row scales), "
+                 f"bf16 activations quantized per token in the step, {int(args.sparsity * 100)}% unstructured "
+                 f"magnitude sparsity, prefill M = 512 and 2048",
+                 {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_I8_PEAK_TOPS, "unit": "TOP/s",
+                  "frac": round(achieved / MFMA_I8_PEAK_TOPS, 4), "traffic": None,
+                  "kernel": "k_sparse_prefill<int8>", "ops_per_launch": "dense-equivalent 2*M*N*K",
+                  "avg_launch_us": round(launch_ms * 1e3, 3)},
+                 cpu, {"per_M": per_M, "sparsity": args.sparsity}, dtype="i8")
+
+
 def run_stack(args):
     """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
     after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
@@ -536,10 +641,12 @@ def main():
     ap.add_argument("--workers", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
-    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "stack"], default="decode",
+    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "stack"],
+                    default="decode",
                     help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
                          "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
-                         "int8 weights and activations, batches 1,16,64; stack: all 32 layers at batches 1..32")
+                         "int8 weights and activations, batches 1,16,64; int8-prefill: one layer, int8 weights, "
+                         "activations quantized per token, M=512 and 2048; stack: all 32 layers at batches 1..32")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -561,7 +668,8 @@ def main():
         sys.exit(2)
 
     if args.workload != "decode":
-        out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "stack": run_stack}[args.workload](args)
+        out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
+               "stack": run_stack}[args.workload](args)
         print(json.dumps(out), flush=True)
         return
 

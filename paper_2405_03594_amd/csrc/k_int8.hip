@@ -433,22 +433,35 @@ hipError_t sparse_int8_w(const I8GroupArg& g, int64_t kmax, hipStream_t s) {
 // activations to int8; symmetric, one binary32 scale per row): one workgroup
 // per row of X [M][K] (K % 8 == 0, 16-byte pieces of 8 fp16/bf16 values)
 // finds amax = max |x| (a wave reduction, then the 4 wave maxima), sets
-// scale = amax / 127 (1 when amax is 0), and re-reads the row (from L2) to
-// write the codes clamp(round-half-even(x / scale), -127, 127); each division
-// is correctly rounded.
-template <class T>
+// scale = amax / 127 (1 when amax is 0), and writes the codes
+// clamp(round-half-even(x / scale), -127, 127); each division is correctly
+// rounded.  Rows of up to 256 PT pieces stay in registers between the two
+// steps (one read of X); PT = 0 re-reads longer rows (from L2).
+template <class T, int PT>
 __global__ void __launch_bounds__(256) k_quantize_rows(const uint16_t* __restrict__ X, int64_t K,
                                                        int8_t* __restrict__ Xq, float* __restrict__ sx) {
+  constexpr int R = PT > 0 ? PT : 1;
   __shared__ float wmax[4];
   const int64_t m = blockIdx.x;
   const uint16_t* x = X + m * K;
   const int64_t P = K / 8;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  float amax = 0.0f;
-  for (int64_t p = t; p < P; p += 256) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(x + 8 * p);
+  auto amax8 = [](const u32x4& v, float a) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(T::to_f32((v[e >> 1] >> (16 * (e & 1))) & 0xffffu)));
+    for (int e = 0; e < 8; ++e) a = fmaxf(a, fabsf(T::to_f32((v[e >> 1] >> (16 * (e & 1))) & 0xffffu)));
+    return a;
+  };
+  float amax = 0.0f;
+  u32x4 v[R];
+  if constexpr (PT > 0) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int64_t p = t + 256 * i;
+      v[i] = p < P ? *reinterpret_cast<const u32x4*>(x + 8 * p) : u32x4{0u, 0u, 0u, 0u};
+      amax = amax8(v[i], amax);
+    }
+  } else {
+    for (int64_t p = t; p < P; p += 256) amax = amax8(*reinterpret_cast<const u32x4*>(x + 8 * p), amax);
   }
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) amax = fmaxf(amax, __shfl_xor(amax, d));
@@ -458,17 +471,41 @@ __global__ void __launch_bounds__(256) k_quantize_rows(const uint16_t* __restric
   const float scale = amax == 0.0f ? 1.0f : __fdiv_rn(amax, 127.0f);
   if (t == 0) sx[m] = scale;
   int8_t* q = Xq + m * K;
-  for (int64_t p = t; p < P; p += 256) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(x + 8 * p);
+  auto put8 = [&](const u32x4& w, int64_t p) {
     uint32_t c[2] = {0u, 0u};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float r = rintf(__fdiv_rn(T::to_f32((v[e >> 1] >> (16 * (e & 1))) & 0xffffu), scale));
+      float r = rintf(__fdiv_rn(T::to_f32((w[e >> 1] >> (16 * (e & 1))) & 0xffffu), scale));
       r = fminf(fmaxf(r, -127.0f), 127.0f);
       c[e >> 2] |= ((uint32_t)(int32_t)r & 0xffu) << (8 * (e & 3));
     }
     *reinterpret_cast<u32x2*>(q + 8 * p) = u32x2{c[0], c[1]};
+  };
+  if constexpr (PT > 0) {
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int64_t p = t + 256 * i;
+      if (p < P) put8(v[i], p);
+    }
+  } else {
+    for (int64_t p = t; p < P; p += 256) put8(*reinterpret_cast<const u32x4*>(x + 8 * p), p);
   }
+}
+
+template <class T>
+void quantize_rows_launch(const uint16_t* x, int64_t M, int64_t K, int8_t* Xq, float* sx, hipStream_t s) {
+  const int64_t P = K / 8;
+  const dim3 grid((unsigned)M), block(256);
+  if (P <= 256)
+    hipLaunchKernelGGL((k_quantize_rows<T, 1>), grid, block, 0, s, x, K, Xq, sx);
+  else if (P <= 512)
+    hipLaunchKernelGGL((k_quantize_rows<T, 2>), grid, block, 0, s, x, K, Xq, sx);
+  else if (P <= 1024)
+    hipLaunchKernelGGL((k_quantize_rows<T, 4>), grid, block, 0, s, x, K, Xq, sx);
+  else if (P <= 2048)
+    hipLaunchKernelGGL((k_quantize_rows<T, 8>), grid, block, 0, s, x, K, Xq, sx);
+  else
+    hipLaunchKernelGGL((k_quantize_rows<T, 0>), grid, block, 0, s, x, K, Xq, sx);
 }
 
 bool i8_small_grid(int64_t blocks) {
@@ -541,9 +578,9 @@ hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int6
                                    hipStream_t s) {
   const uint16_t* x = static_cast<const uint16_t*>(X);
   if (dtype == SPL_BF16)
-    hipLaunchKernelGGL(k_quantize_rows<Bf16>, dim3((unsigned)M), dim3(256), 0, s, x, K, Xq, sx);
+    quantize_rows_launch<Bf16>(x, M, K, Xq, sx, s);
   else
-    hipLaunchKernelGGL(k_quantize_rows<F16>, dim3((unsigned)M), dim3(256), 0, s, x, K, Xq, sx);
+    quantize_rows_launch<F16>(x, M, K, Xq, sx, s);
   return hipGetLastError();
 }
 
