@@ -216,6 +216,26 @@ def linear_f64_pairs(X: np.ndarray, p: Packed, ms: np.ndarray, ns: np.ndarray, n
     return out
 
 
+def _silu_mul(g: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """silu(g) * u = g / (1 + e^-g) * u in binary64 (e^-g overflowing to inf gives -0)."""
+    with np.errstate(over="ignore"):
+        return g / (1.0 + np.exp(-g)) * u
+
+
+def silu_mul_f64(X: np.ndarray, pg: Packed, pu: Packed, nthreads: int = 0) -> np.ndarray:
+    """The gated half of a Llama MLP on two sparse weights that share X:
+    Y = silu(X (Wg.Mg)^T) * (X (Wu.Mu)^T), elementwise, in binary64, with
+    silu(z) = z / (1 + e^-z).  Both products are the plain definition above."""
+    assert pg.N == pu.N and pg.K == pu.K
+    return _silu_mul(linear_f64(X, pg, nthreads), linear_f64(X, pu, nthreads))
+
+
+def silu_mul_f64_pairs(X: np.ndarray, pg: Packed, pu: Packed, ms: np.ndarray, ns: np.ndarray,
+                       nthreads: int = 0) -> np.ndarray:
+    """The same at selected output positions (ms[i], ns[i])."""
+    assert pg.N == pu.N and pg.K == pu.K
+    return _silu_mul(linear_f64_pairs(X, pg, ms, ns, nthreads), linear_f64_pairs(X, pu, ms, ns, nthreads))
+
 def dense_f64(X: np.ndarray, W: np.ndarray, dtype: str, nthreads: int = 0) -> np.ndarray:
     """Plain dense product in binary64: Y = X W^T, W is [N][K]."""
     lib = _load()

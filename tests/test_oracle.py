@@ -492,3 +492,51 @@ def test_quantize_rows_agrees_with_generator(orc):
     q1, s1 = orc.quantize_rows_i8(x, "bf16")
     q2, s2 = synth.quantize_rows_int8(synth.bits_to_f32(x, "bf16"))
     assert np.array_equal(q1, q2) and np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+
+
+def test_silu_mul_identities(orc):
+    """silu(z) - silu(-z) = z and silu(z) + silu(-z) = z tanh(z / 2): with the
+    gate negated (the same mask) the two outputs differ by exactly g * u and
+    sum to g tanh(g / 2) u, where g and u come from the plain products; a zero
+    gate or a zero up matrix gives zeros."""
+    N, K, M = 40, 96, 7
+    Wg, mask = synth.weight(71, N, K, "bf16", 0.5)
+    Wu, masku = synth.weight(72, N, K, "bf16", 0.7)
+    X = synth.activations(73, M, K, "bf16")
+    neg = Wg ^ np.uint16(0x8000)                          # exact negation of every bf16 payload
+    pg, pn, pu = orc.pack(Wg, "bf16", mask), orc.pack(neg, "bf16", mask), orc.pack(Wu, "bf16", masku)
+    g, u = orc.linear_f64(X, pg), orc.linear_f64(X, pu)
+    assert np.array_equal(orc.linear_f64(X, pn), -g)
+    a, b = orc.silu_mul_f64(X, pg, pu), orc.silu_mul_f64(X, pn, pu)
+    assert np.allclose(a - b, g * u, rtol=1e-12, atol=1e-15)
+    assert np.allclose(a + b, g * np.tanh(g / 2) * u, rtol=1e-12, atol=1e-15)
+    zero = orc.pack(np.zeros((N, K), np.uint16), "bf16", mask)
+    assert not orc.silu_mul_f64(X, zero, pu).any()
+    assert not orc.silu_mul_f64(X, pg, orc.pack(np.zeros((N, K), np.uint16), "bf16", masku)).any()
+
+
+def test_silu_mul_matches_library_and_limits(orc):
+    """Against scipy's logistic function (silu(z) = z expit(z)) on random
+    layers, at chosen output pairs too, and the limits silu(z) -> z for large
+    z and -> 0 for very negative z (identity activations make g = the stored
+    gate weights, chosen here)."""
+    from scipy.special import expit
+
+    N, K, M = 33, 64, 5
+    Wg, mg = synth.weight(81, N, K, "f16", 0.7)
+    Wu, mu = synth.weight(82, N, K, "f16", 0.5)
+    X = synth.activations(83, M, K, "f16")
+    pg, pu = orc.pack(Wg, "f16", mg), orc.pack(Wu, "f16", mu)
+    g, u = orc.linear_f64(X, pg), orc.linear_f64(X, pu)
+    y = orc.silu_mul_f64(X, pg, pu)
+    assert np.allclose(y, g * expit(g) * u, rtol=1e-13, atol=1e-16)
+    ms, ns = np.array([0, 4, 2, 3]), np.array([0, 32, 7, 20])
+    assert np.allclose(orc.silu_mul_f64_pairs(X, pg, pu, ms, ns), y[ms, ns], rtol=1e-15, atol=0)
+    big = np.array([[40.0, -800.0, 0.0, 1.0]])
+    G = synth.round_to(np.diag(big[0]).astype(np.float32), "f16")          # 4 x 4, gate row n = e_n * big[n]
+    U = synth.round_to(np.eye(4, dtype=np.float32) * 3.0, "f16")
+    I = synth.round_to(np.eye(4, dtype=np.float32), "f16")
+    out = orc.silu_mul_f64(I, orc.pack(G, "f16"), orc.pack(U, "f16", np.ones((4, 4), np.uint8)))
+    d = np.diag(out)
+    assert abs(d[0] - 3 * 40.0) < 1e-12 and d[1] == 0.0 and d[2] == 0.0
+    assert abs(d[3] - 3.0 / (1.0 + np.exp(-1.0))) < 1e-15
