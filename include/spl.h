@@ -167,6 +167,19 @@ spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, voi
 spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
                                 hipStream_t stream);
 
+/* The gated half of a Llama MLP on two sparse weights sharing X (the model
+ * the paper sparsifies; its MLP is down(silu(gate(x)) * up(x))):
+ *   Y[m][n] = silu(g) * u,  g = sum_k X[m][k] Wg[n][k],  u = likewise with Wu,
+ *   silu(z) = z / (1 + e^-z), g and u the kernels' fp32 sums, one rounding of
+ *   the result to the payload type.  One launch, no intermediate in memory.
+ *   Wgate, Wup  views in the tile layout with the same dtype, rows (N) and cols (K).
+ *   X, Y        as in spl_sparse_linear (Y [M][N]).
+ *   algo        SPL_ALGO_AUTO (DECODE for M <= 16, else PREFILL), DECODE
+ *               (M <= 16, SPL_ERR_UNSUPPORTED otherwise) or PREFILL (any M).
+ * Errors as spl_sparse_linear; mismatched dtypes or shapes -> SPL_ERR_INVALID_ARG. */
+spl_status spl_sparse_linear_silu_mul(const void* X, int64_t M, const spl_matrix* Wgate, const spl_matrix* Wup,
+                                      void* Y, int32_t algo, hipStream_t stream);
+
 /* Sparse-quantized linear layer (paper section 3.4: int8 weights and
  * int8 activations).
  *   Xq        [M][K] int8 activation codes; x_scales [M] float32.

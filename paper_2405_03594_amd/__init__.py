@@ -101,6 +101,7 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_linear_ex": (ctypes.c_int, [P, I64, MP, P, I32, P]),
         "spl_sparse_linear_int8": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
         "spl_quantize_rows_i8": (ctypes.c_int, [P, ctypes.c_int32, I64, I64, P, P, P]),
+        "spl_sparse_linear_silu_mul": (ctypes.c_int, [P, I64, MP, MP, P, I32, P]),
         "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
         "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
@@ -251,6 +252,23 @@ def sparse_linear(X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = 
     view = Wc.view()
     _check("spl_sparse_linear_ex", L.spl_sparse_linear_ex(_ptr(X), M, ctypes.byref(view), _ptr(out), ALGO[algo],
                                                           _stream(stream)))
+    return out
+
+
+def sparse_linear_silu_mul(X: torch.Tensor, Wgate: SparseMatrix, Wup: SparseMatrix, out: torch.Tensor | None = None,
+                           algo: str = "auto", stream=None) -> torch.Tensor:
+    """Y [M][N] = silu(X Wgate^T) * (X Wup^T): the gated half of a Llama MLP in
+    one launch (see spl_sparse_linear_silu_mul)."""
+    L = lib()
+    _dev_tensor(X, "X")
+    M = X.shape[0]
+    if out is None:
+        out = torch.empty((M, Wgate.rows), dtype=X.dtype, device=X.device)
+    if X.dtype != Wgate.dtype or Wup.dtype != Wgate.dtype or out.dtype != X.dtype:
+        raise ValueError("X, both weights and Y must share one fp16/bf16 dtype")
+    vg, vu = Wgate.view(), Wup.view()
+    _check("spl_sparse_linear_silu_mul", L.spl_sparse_linear_silu_mul(_ptr(X), M, ctypes.byref(vg), ctypes.byref(vu),
+                                                                      _ptr(out), ALGO[algo], _stream(stream)))
     return out
 
 

@@ -228,6 +228,33 @@ __device__ __forceinline__ void reduce_store(float* red, const f32x4 (&acc)[MT],
   }
 }
 
+// As reduce_store for a gate and an up accumulator of the same row block:
+// Y[m][n] = silu(g) * u with g and u the fp32 sums of the waves (fixed order).
+template <class T, int W>
+__device__ __forceinline__ void reduce_store_gated(float* red, const f32x4& ag, const f32x4& au, int M, int64_t n0,
+                                                   int64_t N, uint16_t* __restrict__ Y) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  *reinterpret_cast<f32x4*>(red + ((wave * 2 + 0) * 64 + lane) * 4) = ag;
+  *reinterpret_cast<f32x4*>(red + ((wave * 2 + 1) * 64 + lane) * 4) = au;
+  __syncthreads();
+  for (int e = threadIdx.x; e < 256; e += W * kWave) {
+    const int li = (e >> 2) & 63;
+    const int ri = e & 3;
+    const int64_t n = n0 + 4 * (li >> 4) + ri;
+    const int m = li & 15;
+    if (m < M && n < N) {
+      float sg = 0.f, su = 0.f;
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        sg += red[((w * 2 + 0) * 64 + li) * 4 + ri];
+        su += red[((w * 2 + 1) * 64 + li) * 4 + ri];
+      }
+      Y[(int64_t)m * N + n] = T::from_f32(sg / (1.0f + expf(-sg)) * su);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ groups
 
 struct SparseTaskArg {
@@ -480,20 +507,24 @@ struct Chunk2 {
   int np[2];
 };
 
-template <class T, int W>
+// kGated: the gated half of a Llama MLP.  Task 0 is the gate and task 1 the up
+// projection (same X, N, K); workgroup j pairs row block j of both and stores
+// silu(gate) * up (silu(z) = z / (1 + e^-z), from the fp32 sums) into task 0's Y.
+template <class T, int W, bool kGated>
 __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGroupArg g) {
   constexpr int C = kChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
   constexpr int WS = C + 2;                          // word row stride (see k_sparse_decode)
   __shared__ __align__(16) uint32_t words[W][2][16 * WS];
-  const int ti = find_task(g.first, g.count);
+  const int ti = kGated ? 0 : find_task(g.first, g.count);
   const SparseTaskArg tk = g.t[ti];
+  const SparseTaskArg tu = g.t[kGated ? 1 : ti];
   const int M = g.M;
   const int64_t K = tk.K;
   const int64_t B = tile_blocks(tk.N);
-  const int64_t blk0 = 2 * ((int64_t)blockIdx.x - g.first[ti]);
-  const bool live1 = blk0 + 1 < B;
+  const int64_t blk0 = kGated ? (int64_t)blockIdx.x : 2 * ((int64_t)blockIdx.x - g.first[ti]);
+  const bool live1 = kGated || blk0 + 1 < B;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int fr = lane & 15, fg = lane >> 4;
@@ -501,10 +532,11 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   int kbeg, kend;
   wave_range<W>(S, wave, &kbeg, &kend);
   unsigned char* vbuf[2] = {dsm + wave * 2 * kHalfVBufAlloc, dsm + wave * 2 * kHalfVBufAlloc + kHalfVBufAlloc};
-  const int64_t blkb[2] = {blk0, live1 ? blk0 + 1 : blk0};
-  const uint32_t* bmb[2] = {tk.bm + blkb[0] * S * 16, tk.bm + blkb[1] * S * 16};
-  const int32_t* tob[2] = {tk.toff + blkb[0] * S, tk.toff + blkb[1] * S};
-  const unsigned char* vbytes = reinterpret_cast<const unsigned char*>(tk.values);
+  const int64_t blkb[2] = {blk0, kGated ? blk0 : (live1 ? blk0 + 1 : blk0)};
+  const uint32_t* bmb[2] = {tk.bm + blkb[0] * S * 16, tu.bm + blkb[1] * S * 16};
+  const int32_t* tob[2] = {tk.toff + blkb[0] * S, tu.toff + blkb[1] * S};
+  const unsigned char* vbs[2] = {reinterpret_cast<const unsigned char*>(tk.values),
+                                 reinterpret_cast<const unsigned char*>(tu.values)};
 
   int ob = kbeg;
   auto load_offsets = [&](int b, int base) {
@@ -541,7 +573,7 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
       for (int r = 0; r < kHalfPieceRounds; ++r) {
         vp[b][r] = u32x4{0u, 0u, 0u, 0u};
         const uint32_t off = ch.a0[b] + 16u * (uint32_t)(lane + kWave * r);
-        if (lane + kWave * r < ch.np[b]) vp[b][r] = *reinterpret_cast<const u32x4*>(vbytes + off);
+        if (lane + kWave * r < ch.np[b]) vp[b][r] = *reinterpret_cast<const u32x4*>(vbs[b] + off);
       }
 #pragma unroll
       for (int i = 0; i < C / 4; ++i) {
@@ -652,6 +684,10 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   }
   __syncthreads();                                     // every wave is done with its staging buffers
   float* red = reinterpret_cast<float*>(dsm);
+  if constexpr (kGated) {
+    reduce_store_gated<T, W>(red, acc[0][0], acc[1][0], M, blk0 * kDecRows, tk.N, tk.Y);
+    return;
+  }
   reduce_store<T, 1, W>(red, acc[0], M, blk0 * kDecRows, tk.N, tk.Y);
   if (live1) {
     __syncthreads();                                   // the first block's sums are read before red is reused
@@ -816,7 +852,7 @@ hipError_t sparse_pair_launch(const SparseGroupArg& g1, hipStream_t s) {
   SparseGroupArg g = g1;
   for (int i = 0; i < g.count; ++i)
     g.first[i + 1] = g.first[i] + (int32_t)((tile_blocks(g1.t[i].N) + 1) / 2);
-  auto* kernel = k_sparse_decode2<T, W>;
+  auto* kernel = k_sparse_decode2<T, W, false>;
   static const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>());
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(W * kWave), sparse2_vbuf_bytes<W>(), s, g);
@@ -872,6 +908,29 @@ hipError_t launch_sparse_decode(const spl_sparse_task* tasks, int count, int64_t
   g.count = count;
   g.M = (int32_t)M;
   return tasks[0].W->dtype == SPL_BF16 ? sparse_group_t<Bf16>(g, kmax, s) : sparse_group_t<F16>(g, kmax, s);
+}
+
+// Gated half of a Llama MLP at batches of up to 16 rows: workgroup j pairs
+// row block j of the gate and of the up matrix (k_sparse_decode2, kGated).
+hipError_t launch_gated_decode(const void* X, int64_t M, const spl_matrix& Wg, const spl_matrix& Wu, void* Y,
+                               hipStream_t s) {
+  if (Wg.nnz == 0 || Wu.nnz == 0) return launch_zero_fill(Y, M * Wg.rows, s);   // silu(0) u = silu(g) 0 = 0
+  constexpr int W = 8;
+  static_assert(W * 2 * kWave * 4 * sizeof(float) <= sparse2_vbuf_bytes<W>(), "both blocks' partial sums fit");
+  SparseGroupArg g{};
+  const int32_t B = (int32_t)tile_blocks(Wg.rows);
+  g.t[0] = SparseTaskArg{static_cast<const uint16_t*>(X), static_cast<uint16_t*>(Y), Wg.bitmask,
+                         static_cast<const uint16_t*>(Wg.values), Wg.tile_offsets, Wg.rows, Wg.cols};
+  g.t[1] = SparseTaskArg{static_cast<const uint16_t*>(X), static_cast<uint16_t*>(Y), Wu.bitmask,
+                         static_cast<const uint16_t*>(Wu.values), Wu.tile_offsets, Wu.rows, Wu.cols};
+  g.first[0] = 0, g.first[1] = B, g.first[2] = B;
+  g.count = 2;
+  g.M = (int32_t)M;
+  auto* kernel = Wg.dtype == SPL_BF16 ? k_sparse_decode2<Bf16, W, true> : k_sparse_decode2<F16, W, true>;
+  const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>());
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)B), dim3(W * kWave), sparse2_vbuf_bytes<W>(), s, g);
+  return hipGetLastError();
 }
 
 hipError_t launch_dense_decode(const spl_dense_task* tasks, int count, int64_t M, int32_t dtype, hipStream_t s) {

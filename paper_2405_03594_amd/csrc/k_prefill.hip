@@ -247,6 +247,32 @@ __device__ __forceinline__ void pf_store_i8(const i32x4 (&acc)[FN][4], uint16_t*
   }
 }
 
+// The gated epilogue (the gated half of a Llama MLP): the workgroup's virtual
+// rows alternate 16-row blocks of the gate and the up matrix, so fragments 2p
+// and 2p + 1 of a wave hold the gate and up sums of the same outputs, in the
+// same lanes.  Y[m][n] = silu(g) * u, silu(z) = z / (1 + e^-z), from the fp32
+// sums; n0 is the workgroup's first real row.
+template <class T, int FN>
+__device__ __forceinline__ void pf_store_gated(const f32x4 (&acc)[FN][4], uint16_t* __restrict__ Y, int64_t M,
+                                               int64_t N, int64_t n0, int64_t m0, int wn, int wm, int fr, int fg) {
+  static_assert(FN % 2 == 0, "gate and up fragments pair up");
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t m = m0 + wm * 64 + 16 * j + fr;
+    if (m >= M) continue;
+#pragma unroll
+    for (int p = 0; p < FN / 2; ++p) {
+      const int64_t n = n0 + wn * 8 * FN + 16 * p + 4 * fg;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (n + r >= N) continue;
+        const float gs = acc[2 * p][j][r], us = acc[2 * p + 1][j][r];
+        Y[m * N + n + r] = T::from_f32(gs / (1.0f + expf(-gs)) * us);
+      }
+    }
+  }
+}
+
 // Split K: after every wave's last MFMA, k-group 1 hands its partial sums to
 // k-group 0 through the (then free) stage buffers; group 0 adds them (a fixed
 // order) and is the one that stores.  Returns whether this thread stores.
@@ -296,6 +322,9 @@ struct PfArgs {
   const uint32_t* bm;            // sparse: tile bitmask words
   const unsigned char* values;   // sparse: payload bytes (followed by 16 readable bytes)
   const int32_t* toff;           // sparse: tile offsets
+  const uint32_t* bm2;           // gated: the up matrix (bm, values, toff are the gate)
+  const unsigned char* values2;
+  const int32_t* toff2;
   int64_t M, N, K;               // K in payload elements
   uint16_t* Y;                   // out [M][N]: the payload type, fp16 for int8
   const float* sx;               // int8: activation scales [M]
@@ -303,7 +332,10 @@ struct PfArgs {
   int32_t* acc;                  // int8: optional exact sums [M][N]
 };
 
-template <class T, int BN, int BM, int NW, int KS, bool kChecked>
+// kGated: the workgroup's BN virtual rows are BN/32 row blocks of the gate and
+// of the up matrix, alternating (wave w expands virtual block w: matrix w % 2,
+// real block BN/32 x + w / 2), stored through pf_store_gated.
+template <class T, int BN, int BM, int NW, int KS, bool kChecked, bool kGated = false>
 __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(const PfArgs g) {
   extern __shared__ __align__(16) unsigned char dsm[];
   constexpr bool kI8 = std::is_same<T, I8P>::value;
@@ -332,14 +364,17 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
   static_assert(KS == 1 || FN * 4 * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
-  const int64_t nb0 = n0 / 16;
+  static_assert(!kGated || (!kI8 && TW == 2), "gated: 16-bit payloads, one row block per wave");
+  const int gm = kGated ? (wave & 1) : 0;            // gated: this wave's matrix (0 gate, 1 up)
+  // first row block of this wave's units
+  const int64_t wb = kGated ? (int64_t)blockIdx.x * (BN / 32) + (wave >> 1) : n0 / 16 + (TW / 2) * wave;
   unsigned char* gb = dsm + kh * pf_lds(BN, BM);     // this group's stage buffers
   const uint32_t abuf[2] = {lds_off(gb), lds_off(gb + BN * kPfRow)};
   const uint32_t bbuf[2] = {lds_off(gb + 2 * BN * kPfRow), lds_off(gb + (2 * BN + BM) * kPfRow)};
   const uint32_t lut_addr = lds_off(lut);
-  const unsigned char* vbytes = g.values;
-  const uint32_t* __restrict__ bm_tiles = g.bm;
-  const int32_t* __restrict__ tile_offsets = g.toff;
+  const unsigned char* vbytes = gm ? g.values2 : g.values;
+  const uint32_t* __restrict__ bm_tiles = gm ? g.bm2 : g.bm;
+  const int32_t* __restrict__ tile_offsets = gm ? g.toff2 : g.toff;
   if constexpr (kI8) {
     if (threadIdx.x < 80) lut[threadIdx.x] = pf_i8_selector(threadIdx.x / 5, threadIdx.x % 5);
   } else {
@@ -355,7 +390,7 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
   auto fetch_words = [&](TileWords<TW>& tw, int st) {
 #pragma unroll
     for (int i = 0; i < TW; ++i) {
-      const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);
+      const int64_t b = wb + (i >> 1);
       const int s = kI8 ? 4 * st + 2 * (i & 1) + (fg >> 1) : 2 * st + (i & 1);
       if constexpr (kChecked) {
         const bool ok = b < B && s < S;
@@ -496,6 +531,8 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
   if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) {
     if constexpr (kI8)
       pf_store_i8<FN>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+    else if constexpr (kGated)
+      pf_store_gated<T, FN>(acc, g.Y, M, N, (int64_t)blockIdx.x * (BN / 2), m0, wn, wm, fr, fg);
     else
       pf_store<T, FN>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
   }
@@ -612,12 +649,13 @@ constexpr bool pf_inside(int64_t N, int64_t M, int64_t K, int BN, int BM) {
   return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;
 }
 
-template <class T, int BN, int BM, int NW, int KS, bool kChecked>
+template <class T, int BN, int BM, int NW, int KS, bool kChecked, bool kGated = false>
 hipError_t sparse_prefill_launch(const PfArgs& a, hipStream_t s) {
-  auto* kernel = k_sparse_prefill<T, BN, BM, NW, KS, kChecked>;
+  auto* kernel = k_sparse_prefill<T, BN, BM, NW, KS, kChecked, kGated>;
   static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
+  constexpr int RN = kGated ? BN / 2 : BN;            // real rows per workgroup
+  const dim3 grid((unsigned)((a.N + RN - 1) / RN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
   hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, a);
   return hipGetLastError();
 }
@@ -637,6 +675,20 @@ hipError_t sparse_prefill_t(const PfArgs& a, hipStream_t s) {
   if (pf_large_tile(a.N, a.M)) return sparse_prefill_tile<T, 128, 256, 8, 1>(a, s);
   return pf_split_k(a.N, a.M) ? sparse_prefill_tile<T, 64, 128, 4, 2>(a, s)
                               : sparse_prefill_tile<T, 64, 128, 4, 1>(a, s);
+}
+
+// Gated: the tiling of a launch of 2N virtual rows; inside when N % (BN / 2) == 0.
+template <class T, int BN, int BM, int NW, int KS>
+hipError_t gated_prefill_tile(const PfArgs& a, hipStream_t s) {
+  return pf_inside(2 * a.N, a.M, a.K, BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false, true>(a, s)
+                                              : sparse_prefill_launch<T, BN, BM, NW, KS, true, true>(a, s);
+}
+
+template <class T>
+hipError_t gated_prefill_t(const PfArgs& a, hipStream_t s) {
+  const int64_t Nv = 2 * a.N;
+  if (pf_large_tile(Nv, a.M)) return gated_prefill_tile<T, 128, 256, 8, 1>(a, s);
+  return pf_split_k(Nv, a.M) ? gated_prefill_tile<T, 64, 128, 4, 2>(a, s) : gated_prefill_tile<T, 64, 128, 4, 1>(a, s);
 }
 
 template <class T, int BN, int BM, int NW, int KS, bool kChecked>
@@ -684,6 +736,19 @@ hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t
   a.M = M, a.N = N, a.K = K;
   a.Y = static_cast<uint16_t*>(Y);
   return dtype == SPL_BF16 ? dense_prefill_t<Bf16>(a, s) : dense_prefill_t<F16>(a, s);
+}
+
+// Gated half of a Llama MLP: Y = silu(X Wg^T) * (X Wu^T) (same dtype and shape).
+hipError_t launch_gated_prefill(const void* X, int64_t M, const spl_matrix& Wg, const spl_matrix& Wu, void* Y,
+                                hipStream_t s) {
+  if (Wg.nnz == 0 || Wu.nnz == 0) return launch_zero_fill(Y, M * Wg.rows, s);   // silu(0) u = silu(g) 0 = 0
+  PfArgs a{};
+  a.X = static_cast<const uint16_t*>(X);
+  a.bm = Wg.bitmask, a.values = static_cast<const unsigned char*>(Wg.values), a.toff = Wg.tile_offsets;
+  a.bm2 = Wu.bitmask, a.values2 = static_cast<const unsigned char*>(Wu.values), a.toff2 = Wu.tile_offsets;
+  a.M = M, a.N = Wg.rows, a.K = Wg.cols;
+  a.Y = static_cast<uint16_t*>(Y);
+  return Wg.dtype == SPL_BF16 ? gated_prefill_t<Bf16>(a, s) : gated_prefill_t<F16>(a, s);
 }
 
 // int8 (K % 16 == 0: activation rows are whole 16-byte pieces).

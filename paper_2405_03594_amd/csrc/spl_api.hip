@@ -14,6 +14,7 @@ namespace {
 constexpr int64_t kMaxDim = (int64_t)1 << 31;        // N, K, M < 2^31
 constexpr int64_t kMaxElems = (int64_t)1 << 40;      // N * K, M * K, M * N
 constexpr int64_t kDecodeMaxM = 32;
+constexpr int64_t kGatedDecodeMaxM = 16;           // the paired decode kernel holds one 16-row batch tile
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -188,7 +189,25 @@ spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, voi
   return spl_sparse_linear_ex(X, M, Wc, Y, SPL_ALGO_AUTO, stream);
 }
 
-// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+spl_status spl_sparse_linear_silu_mul(const void* X, int64_t M, const spl_matrix* Wgate, const spl_matrix* Wup,
+                                      void* Y, int32_t algo, hipStream_t stream) {
+  if (!Wgate || !Wup || M < 0) return SPL_ERR_INVALID_ARG;
+  int32_t ag = algo, au = algo;
+  spl_status st = check_sparse_task(X, M, Wgate, Y, &ag);
+  if (st != SPL_OK) return st;
+  st = check_sparse_task(X, M, Wup, Y, &au);
+  if (st != SPL_OK) return st;
+  if (Wup->dtype != Wgate->dtype || Wup->rows != Wgate->rows || Wup->cols != Wgate->cols) return SPL_ERR_INVALID_ARG;
+  if (algo == SPL_ALGO_AUTO) ag = M <= kGatedDecodeMaxM ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (ag == SPL_ALGO_DECODE && M > kGatedDecodeMaxM) return SPL_ERR_UNSUPPORTED;
+  if (2 * spl::tile_blocks(Wgate->rows) >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
+  (void)hipGetLastError();
+  if (ag == SPL_ALGO_DECODE) return launched(spl::launch_gated_decode(X, M, *Wgate, *Wup, Y, stream));
+  return launched(spl::launch_gated_prefill(X, M, *Wgate, *Wup, Y, stream));
+}
+
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
 static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
   const spl_status st = spl_check_matrix(t->Wq);
   if (st != SPL_OK) return st;

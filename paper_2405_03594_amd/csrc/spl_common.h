@@ -140,6 +140,11 @@ hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, 
 hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s);
 hipError_t launch_sparse_prefill_i8(const spl_int8_task& t, int64_t M, hipStream_t s);
 hipError_t launch_dense_prefill_i8(const spl_dense_int8_task& t, int64_t M, hipStream_t s);
+// Gated half of a Llama MLP, Y = silu(X Wg^T) * (X Wu^T): M <= 16 (decode) or any M (prefill).
+hipError_t launch_gated_decode(const void* X, int64_t M, const spl_matrix& Wg, const spl_matrix& Wu, void* Y,
+                               hipStream_t s);
+hipError_t launch_gated_prefill(const void* X, int64_t M, const spl_matrix& Wg, const spl_matrix& Wu, void* Y,
+                                hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

@@ -249,3 +249,25 @@ def test_quantize_rows_argument_checks(L):
     assert f(X + 8, 2, 4, 64, Q, s, None) == INVALID              # misaligned X
     assert f(X, 1, 4, 64, Q + 4, s, None) == INVALID              # misaligned codes
     assert f(X, 2, 4, 0, Q, s, None) == INVALID                   # K = 0
+
+
+def test_silu_mul_argument_checks(L):
+    """Checks that return before any HIP call (no device needed)."""
+    g = _mat(layout=1, tile_offsets=0x40000)
+    u = _mat(layout=1, tile_offsets=0x40000)
+    X, Y = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000)
+    f = L.spl_sparse_linear_silu_mul
+    assert f(None, 0, ctypes.byref(g), ctypes.byref(u), None, 0, None) == OK       # M = 0 is a no-op
+    assert f(X, -1, ctypes.byref(g), ctypes.byref(u), Y, 0, None) == INVALID
+    assert f(X, 2, None, ctypes.byref(u), Y, 0, None) == INVALID
+    assert f(X, 2, ctypes.byref(g), None, Y, 0, None) == INVALID
+    assert f(X, 2, ctypes.byref(g), ctypes.byref(u), None, 0, None) == INVALID
+    assert f(X, 2, ctypes.byref(g), ctypes.byref(u), Y, 7, None) == INVALID        # unknown algorithm
+    assert f(X, 17, ctypes.byref(g), ctypes.byref(u), Y, 1, None) == UNSUPPORTED   # paired decode is M <= 16
+    for bad in (_mat(rows=8, layout=1, tile_offsets=0x40000), _mat(cols=128, layout=1, tile_offsets=0x40000),
+                _mat(dtype=1, layout=1, tile_offsets=0x40000)):
+        assert f(X, 2, ctypes.byref(g), ctypes.byref(bad), Y, 0, None) == INVALID  # shape or dtype mismatch
+    i8 = _mat(dtype=3, layout=1, tile_offsets=0x40000)
+    assert f(X, 2, ctypes.byref(i8), ctypes.byref(i8), Y, 0, None) == UNSUPPORTED
+    rows = _mat()
+    assert f(X, 2, ctypes.byref(rows), ctypes.byref(rows), Y, 0, None) == UNSUPPORTED   # row layout
