@@ -570,6 +570,81 @@ def run_int8_prefill(args):
                  cpu, {"per_M": per_M, "sparsity": args.sparsity}, dtype="i8")
 
 
+def run_gated(args):
+    """The gated half of a Llama MLP, silu(X Wgate^T) * (X Wup^T), for 4
+    rotated layers' gate/up pairs (11008 x 4096, --sparsity): one step = the
+    fused launch at decode batches 1, 4 and 16; prefill batches 512 and 2048
+    and the unfused path (grouped gate|up launch, then torch's silu and
+    product) are timed alongside."""
+    nl = 4
+    N, K = 11008, 4096
+    jobs = [(l, j, N, K, "bf16", args.sparsity) for l in range(nl) for j in (4, 5)]
+    host = {}
+    with cf.ProcessPoolExecutor(max_workers=min(args.workers, len(jobs))) as ex:
+        for layer, j, W, mask in ex.map(_gen_matrix, jobs):
+            host[(layer, j)] = (W, mask)
+    torch, spl = _need_gpu()
+    import torch.nn.functional as F
+
+    mats = [[spl.pack_sparse(_to_dev(host[(l, j)][0], "bf16", torch), torch.from_numpy(host[(l, j)][1]).cuda())
+             for j in (4, 5)] for l in range(nl)]
+    Ms = [1, 4, 16]
+    Mp = [512, 2048]
+    xb = _to_dev(synth.activations(synth.activation_seed(4), max(Mp), K, "bf16"), "bf16", torch)
+    xs = {M: xb[:M].contiguous() for M in Ms + Mp}
+    ys = {M: torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms + Mp}
+    gs = {M: torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms + Mp}
+    us = {M: torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms + Mp}
+
+    def fused(li, M):
+        spl.sparse_linear_silu_mul(xs[M], mats[li][0], mats[li][1], out=ys[M])
+
+    def unfused(li, M):
+        spl.sparse_linear_group([xs[M], xs[M]], mats[li], outs=[gs[M], us[M]])
+        torch.mul(F.silu(gs[M]), us[M], out=ys[M])
+
+    sp_wall, sp_gpu = _timed(Ms, lambda li, M: fused(li, M), args.steps, args.warmup, range(nl))
+    nbytes = {M: mats[0][0].compressed_bytes() + mats[0][1].compressed_bytes() + 2 * M * K + 2 * M * N for M in Ms}
+    launch_ms = sp_gpu / len(Ms)
+    achieved = sum(nbytes.values()) / len(Ms) / (launch_ms * 1e-3) / 1e9
+    per_M = {}
+    for M in Ms + Mp:
+        reps = max(10, args.steps // 4) if M in Ms else 10
+        _, g = _timed([M], lambda li, u: fused(li, u), reps, 2, range(nl))
+        _, gu = _timed([M], lambda li, u: unfused(li, u), reps, 2, range(nl))
+        d = {"fused_us": round(g * 1e3, 2), "unfused_us": round(gu * 1e3, 2), "fused_speedup": round(gu / g, 3)}
+        if M in Ms:
+            d["hbm_gbs"] = round(nbytes[M] / (g * 1e-3) / 1e9, 1)
+        else:
+            d["dense_equiv_tflops"] = round(2.0 * 2 * M * N * K / (g * 1e-3) / 1e12, 1)
+        per_M[str(M)] = d
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        threads = oracle.max_threads()
+        pg = oracle.pack(host[(0, 4)][0], "bf16", host[(0, 4)][1])
+        pu = oracle.pack(host[(0, 5)][0], "bf16", host[(0, 5)][1])
+        X = synth.activations(synth.activation_seed(4), max(Ms), K, "bf16")
+
+        def one():
+            for M in Ms:
+                oracle.silu_mul_f64(X[:M], pg, pu, nthreads=threads)
+
+        reps, dt = _oracle_repeat(one)
+        cpu = {"value": round(reps * sum(Ms) / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"layer 0's gate/up pair at batches {Ms}, binary64 products and silu, repeated {reps} "
+                         f"times ({dt:.1f} s on {threads} threads)"}
+    return _line(args, "gated MLP half (silu(gate) * up) tokens/s + achieved HBM GB/s, Llama-2-7B gate/up",
+                 round(sum(Ms) / (sp_wall * 1e-3), 1), "tokens/s", sp_wall,
+                 f"Llama-2-7B gate and up (11008x4096 each), bf16, {int(args.sparsity * 100)}% unstructured "
+                 f"magnitude sparsity, fused silu(gate) * up, batches 1, 4, 16, 4 layers rotated",
+                 {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_decode2<gated>",
+                  "bytes_per_launch": int(sum(nbytes.values()) / len(Ms)), "avg_launch_us": round(launch_ms * 1e3, 3)},
+                 cpu, {"per_M": per_M, "sparsity": args.sparsity})
+
+
 def run_stack(args):
     """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
     after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
@@ -641,12 +716,13 @@ def main():
     ap.add_argument("--workers", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
-    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "stack"],
+    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "gated", "stack"],
                     default="decode",
                     help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
                          "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
                          "int8 weights and activations, batches 1,16,64; int8-prefill: one layer, int8 weights, "
-                         "activations quantized per token, M=512 and 2048; stack: all 32 layers at batches 1..32")
+                         "activations quantized per token, M=512 and 2048; gated: fused silu(gate)*up "
+                         "of gate/up at batches 1,4,16; stack: all 32 layers at batches 1..32")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -669,7 +745,7 @@ def main():
 
     if args.workload != "decode":
         out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
-               "stack": run_stack}[args.workload](args)
+               "gated": run_gated, "stack": run_stack}[args.workload](args)
         print(json.dumps(out), flush=True)
         return
 
