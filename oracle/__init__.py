@@ -296,6 +296,21 @@ def quantize_rows_i8(X: np.ndarray, dtype: str):
     return Xq, sx
 
 
+def magnitude_mask(W: np.ndarray, dtype: str, prune: int) -> np.ndarray:
+    """Keep-mask (uint8 [N][K], 1 = kept) of one matrix after one-shot
+    magnitude pruning (section 2: the smallest-magnitude weights are removed).
+    Reading: exactly `prune` entries are zeroed per matrix, those of smallest
+    |w| as decoded from the fp16/bf16 payload, ties in ascending row-major
+    index.  The plain definition: a stable sort of |w| (binary64, exact);
+    NaN payloads have no magnitude and are rejected."""
+    mag = np.abs(to_f64(np.ascontiguousarray(W, dtype=np.uint16), dtype)).ravel()
+    assert not np.isnan(mag).any(), "NaN payloads have no magnitude"
+    assert 0 <= prune <= mag.size
+    order = np.argsort(mag, kind="stable")
+    keep = np.ones(mag.size, dtype=np.uint8)
+    keep[order[:prune]] = 0
+    return keep.reshape(np.shape(W))
+
 def f16_to_f64(bits: np.ndarray) -> np.ndarray:
     lib = _load()
     bits = np.ascontiguousarray(bits, dtype=np.uint16)

@@ -540,3 +540,61 @@ def test_silu_mul_matches_library_and_limits(orc):
     d = np.diag(out)
     assert abs(d[0] - 3 * 40.0) < 1e-12 and d[1] == 0.0 and d[2] == 0.0
     assert abs(d[3] - 3.0 / (1.0 + np.exp(-1.0))) < 1e-15
+
+
+def _prune_by_selection(mags, prune):
+    """Brute force: repeatedly remove the smallest remaining magnitude, the
+    lowest index among equals."""
+    left = list(range(len(mags)))
+    keep = [1] * len(mags)
+    for _ in range(prune):
+        i = min(left, key=lambda j: (mags[j], j))
+        keep[i] = 0
+        left.remove(i)
+    return keep
+
+
+def test_magnitude_mask_worked_cases(orc):
+    """Hand-derived: |w| = [3, 1, 1, 3, 0, 2] (the -0 and +0 tie, -1 and 1 tie,
+    -3 and 3 tie); each extra pruned entry follows magnitude, then index."""
+    W = _bits([3, -1, 1, -3, -0.0, 2], "bf16").reshape(2, 3)
+    want = {0: [1, 1, 1, 1, 1, 1], 1: [1, 1, 1, 1, 0, 1], 2: [1, 0, 1, 1, 0, 1], 3: [1, 0, 0, 1, 0, 1],
+            4: [1, 0, 0, 1, 0, 0], 5: [0, 0, 0, 1, 0, 0], 6: [0, 0, 0, 0, 0, 0]}
+    for prune, keep in want.items():
+        assert orc.magnitude_mask(W, "bf16", prune).ravel().tolist() == keep, prune
+    Z = _bits([0.0, -0.0, 0.0, -0.0], "f16").reshape(1, 4)
+    assert orc.magnitude_mask(Z, "f16", 2).ravel().tolist() == [0, 0, 1, 1]
+
+
+def test_magnitude_mask_brute_force(orc):
+    """Every 2 x 3 matrix over {0, +-1, 2} (signs and ties included) at every
+    prune count against selection by brute force."""
+    vals = [0.0, 1.0, -1.0, 2.0]
+    for combo in itertools.product(range(4), repeat=6):
+        v = [vals[c] for c in combo]
+        W = _bits(v, "f16").reshape(2, 3)
+        mags = [abs(x) for x in v]
+        for prune in range(7):
+            assert orc.magnitude_mask(W, "f16", prune).ravel().tolist() == _prune_by_selection(mags, prune)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("sparsity", [0.5, 0.7, 0.9])
+def test_magnitude_mask_invariants_and_generator(orc, dtype, sparsity):
+    """Random N(0, 0.02) matrices (bf16 has many equal magnitudes): exactly
+    the requested count is zeroed, no kept |w| is below a pruned one, at the
+    threshold magnitude every pruned index precedes every kept one, and the
+    input generator's own (histogram) formulation gives the same mask."""
+    N, K = 96, 200
+    W = synth.round_to(synth.normal_f32(11, (N, K), 0.02), dtype)
+    num, den = synth.parse_sparsity(sparsity)
+    prune = N * K * num // den
+    keep = orc.magnitude_mask(W, dtype, prune)
+    mag = np.abs(orc.to_f64(W, dtype)).ravel()
+    k = keep.ravel().astype(bool)
+    assert (~k).sum() == prune
+    t = mag[~k].max()
+    assert t <= mag[k].min()
+    cut, kept = np.flatnonzero(~k & (mag == t)), np.flatnonzero(k & (mag == t))
+    assert cut.size and (not kept.size or cut.max() < kept.min())
+    assert np.array_equal(keep, synth.magnitude_mask(W, sparsity))
