@@ -167,6 +167,22 @@ spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, voi
 spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
                                 hipStream_t stream);
 
+/* One-shot magnitude pruning on the GPU (paper section 2 removes the weights
+ * of smallest magnitude; the reading taken: per matrix, exactly `prune`
+ * entries are zeroed, those of smallest decoded |w|, ties in ascending
+ * row-major index).  Writes the keep-mask that spl_pack_sparse takes.
+ *   W          [N][K] fp16/bf16 payloads (dtype), 16-byte aligned; K % 8 == 0
+ *              and N K < 2^31 (SPL_ERR_UNSUPPORTED otherwise).  NaN payloads
+ *              are ordered above +inf by their bits (no magnitude is defined).
+ *   prune      0 <= prune <= N K (SPL_ERR_INVALID_ARG otherwise).
+ *   mask       out [N][K] uint8: 1 kept, 0 pruned; 8-byte aligned.
+ *   workspace  device scratch of spl_magnitude_mask_workspace_bytes() bytes,
+ *              16-byte aligned, owned by the caller; contents are overwritten.
+ * Asynchronous on `stream` (five kernels, no host synchronisation). */
+int64_t spl_magnitude_mask_workspace_bytes(void);
+spl_status spl_magnitude_mask(const void* W, int32_t dtype, int64_t N, int64_t K, int64_t prune, uint8_t* mask,
+                              void* workspace, hipStream_t stream);
+
 /* The gated half of a Llama MLP on two sparse weights sharing X (the model
  * the paper sparsifies; its MLP is down(silu(gate(x)) * up(x))):
  *   Y[m][n] = silu(g) * u,  g = sum_k X[m][k] Wg[n][k],  u = likewise with Wu,

@@ -102,6 +102,8 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_linear_int8": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
         "spl_quantize_rows_i8": (ctypes.c_int, [P, ctypes.c_int32, I64, I64, P, P, P]),
         "spl_sparse_linear_silu_mul": (ctypes.c_int, [P, I64, MP, MP, P, I32, P]),
+        "spl_magnitude_mask_workspace_bytes": (I64, []),
+        "spl_magnitude_mask": (ctypes.c_int, [P, I32, I64, I64, I64, P, P, P]),
         "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
         "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
@@ -269,6 +271,22 @@ def sparse_linear_silu_mul(X: torch.Tensor, Wgate: SparseMatrix, Wup: SparseMatr
     vg, vu = Wgate.view(), Wup.view()
     _check("spl_sparse_linear_silu_mul", L.spl_sparse_linear_silu_mul(_ptr(X), M, ctypes.byref(vg), ctypes.byref(vu),
                                                                       _ptr(out), ALGO[algo], _stream(stream)))
+    return out
+
+
+def magnitude_mask(W: torch.Tensor, prune: int, out: torch.Tensor | None = None,
+                   workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Keep-mask (uint8 [N][K]) zeroing exactly `prune` entries of smallest |w|,
+    ties by ascending row-major index (see spl_magnitude_mask)."""
+    L = lib()
+    _dev_tensor(W, "W")
+    N, K = W.shape
+    if out is None:
+        out = torch.empty((N, K), dtype=torch.uint8, device=W.device)
+    if workspace is None:
+        workspace = torch.empty((L.spl_magnitude_mask_workspace_bytes(),), dtype=torch.uint8, device=W.device)
+    _check("spl_magnitude_mask", L.spl_magnitude_mask(_ptr(W), _TORCH_DTYPE[W.dtype], N, K, int(prune), _ptr(out),
+                                                      _ptr(workspace), _stream(stream)))
     return out
 
 

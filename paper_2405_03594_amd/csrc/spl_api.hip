@@ -207,7 +207,21 @@ spl_status spl_sparse_linear_silu_mul(const void* X, int64_t M, const spl_matrix
   return launched(spl::launch_gated_prefill(X, M, *Wgate, *Wup, Y, stream));
 }
 
-// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+int64_t spl_magnitude_mask_workspace_bytes(void) { return 4 * spl::magnitude_mask_workspace_words(); }
+
+spl_status spl_magnitude_mask(const void* W, int32_t dtype, int64_t N, int64_t K, int64_t prune, uint8_t* mask,
+                              void* workspace, hipStream_t stream) {
+  if (!W || !mask || !workspace || !dims_ok(N, K)) return SPL_ERR_INVALID_ARG;
+  if (!fp_dtype(dtype)) return SPL_ERR_UNSUPPORTED;
+  if (K % 8 != 0 || N * K >= ((int64_t)1 << 31)) return SPL_ERR_UNSUPPORTED;
+  if (prune < 0 || prune > N * K) return SPL_ERR_INVALID_ARG;
+  if (!aligned(W, 16) || !aligned(mask, 8) || !aligned(workspace, 16)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_magnitude_mask(static_cast<const uint16_t*>(W), N * K, (uint32_t)prune, mask,
+                                             static_cast<uint32_t*>(workspace), stream));
+}
+
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
 static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
   const spl_status st = spl_check_matrix(t->Wq);
   if (st != SPL_OK) return st;

@@ -145,6 +145,11 @@ hipError_t launch_gated_decode(const void* X, int64_t M, const spl_matrix& Wg, c
                                hipStream_t s);
 hipError_t launch_gated_prefill(const void* X, int64_t M, const spl_matrix& Wg, const spl_matrix& Wu, void* Y,
                                 hipStream_t s);
+// Magnitude pruning mask of n = N K fp16/bf16 entries (n % 8 == 0, n < 2^31)
+// with a workspace of magnitude_mask_workspace_words() 32-bit words.
+int64_t magnitude_mask_workspace_words();
+hipError_t launch_magnitude_mask(const uint16_t* W, int64_t n, uint32_t prune, uint8_t* mask, uint32_t* ws,
+                                 hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

@@ -271,3 +271,21 @@ def test_silu_mul_argument_checks(L):
     assert f(X, 2, ctypes.byref(i8), ctypes.byref(i8), Y, 0, None) == UNSUPPORTED
     rows = _mat()
     assert f(X, 2, ctypes.byref(rows), ctypes.byref(rows), Y, 0, None) == UNSUPPORTED   # row layout
+
+
+def test_magnitude_mask_argument_checks(L):
+    """Checks that return before any HIP call (no device needed)."""
+    f = L.spl_magnitude_mask
+    W, m, ws = 0x40000, 0x50000, 0x60000
+    assert L.spl_magnitude_mask_workspace_bytes() >= 4 * (1 << 15)
+    assert f(None, 2, 4, 64, 10, m, ws, None) == INVALID
+    assert f(W, 2, 4, 64, 10, None, ws, None) == INVALID
+    assert f(W, 2, 4, 64, 10, m, None, None) == INVALID
+    assert f(W, 3, 4, 64, 10, m, ws, None) == UNSUPPORTED                  # int8 payloads
+    assert f(W, 2, 4, 60, 10, m, ws, None) == UNSUPPORTED                  # K % 8 != 0
+    assert f(W, 2, 1 << 16, 1 << 15, 10, m, ws, None) == UNSUPPORTED       # N K >= 2^31
+    assert f(W, 2, 4, 64, -1, m, ws, None) == INVALID
+    assert f(W, 2, 4, 64, 257, m, ws, None) == INVALID                     # prune > N K
+    assert f(W + 8, 2, 4, 64, 10, m, ws, None) == INVALID                  # misaligned W
+    assert f(W, 2, 4, 64, 10, m + 4, ws, None) == INVALID                  # misaligned mask
+    assert f(W, 2, 0, 64, 10, m, ws, None) == INVALID                      # N = 0
