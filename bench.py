@@ -645,6 +645,56 @@ def run_gated(args):
                  cpu, {"per_M": per_M, "sparsity": args.sparsity})
 
 
+def run_prune(args):
+    """Magnitude pruning of one Llama-2-7B layer's seven bf16 matrices on the
+    GPU (keep-masks at --sparsity), then packing them (pack_sparse): one step
+    = mask + pack for all seven; 2 layers rotated."""
+    nl = 2
+    shapes = synth.LLAMA2_7B_LINEARS
+    torch, spl = _need_gpu()
+    ws = torch.empty((spl.lib().spl_magnitude_mask_workspace_bytes(),), dtype=torch.uint8, device="cuda")
+    num, den = synth.parse_sparsity(args.sparsity)
+    Ws = [[_to_dev(synth.round_to(synth.normal_f32(synth.weight_seed(l, j), (N, K), synth.WEIGHT_STD), "bf16"),
+                   "bf16", torch) for j, (_, N, K) in enumerate(shapes)] for l in range(nl)]
+    masks = [torch.empty((N, K), dtype=torch.uint8, device="cuda") for (_, N, K) in shapes]
+    prunes = [N * K * num // den for (_, N, K) in shapes]
+
+    def mask_fn(li, j):
+        spl.magnitude_mask(Ws[li][j], prunes[j], out=masks[j], workspace=ws)
+
+    units = list(range(len(shapes)))
+    sp_wall, sp_gpu = _timed(units, mask_fn, args.steps, args.warmup, range(nl))
+    algo_bytes = sum(3 * N * K for (_, N, K) in shapes)          # read W (2 B) once, write the mask (1 B)
+    launch_ms = sp_gpu / len(units)
+    achieved = algo_bytes / len(units) / (launch_ms * 1e-3) / 1e9
+    t0 = time.perf_counter()
+    torch.cuda.synchronize()
+    reps = 5
+    for _ in range(reps):
+        for j in units:
+            spl.pack_sparse(Ws[0][j], masks[j])
+    torch.cuda.synchronize()
+    pack_ms = (time.perf_counter() - t0) * 1e3 / reps
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        W = synth.round_to(synth.normal_f32(synth.weight_seed(0, 0), (4096, 4096), synth.WEIGHT_STD), "bf16")
+        reps_c, dt = _oracle_repeat(lambda: oracle.magnitude_mask(W, "bf16", prunes[0]), min_seconds=10.0)
+        layer_over_q = sum(N * K for (_, N, K) in shapes) / (4096 * 4096)
+        cpu = {"value": round(reps_c / dt / layer_over_q, 4), "unit": "layers/s", "cores": 1, "kind": "oracle",
+               "sample": f"the q matrix (4096x4096) masked {reps_c} times ({dt:.1f} s, one thread: a stable sort), "
+                         f"scaled to the layer's seven matrices by element count ({layer_over_q:.2f}x q)"}
+    return _line(args, "magnitude-pruning masks per second, one Llama-2-7B layer (7 matrices)",
+                 round(1.0 / (sp_wall * 1e-3), 2), "layers/s", sp_wall,
+                 f"Llama-2-7B decoder layer's seven bf16 matrices, N(0, 0.02), masks at "
+                 f"{int(args.sparsity * 100)}% (exact count per matrix, ties by index), 2 layers rotated",
+                 {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_mag_* (5 launches)",
+                  "bytes_per_launch": int(algo_bytes / len(units)), "avg_launch_us": round(launch_ms * 1e3, 3)},
+                 cpu, {"pack_sparse_ms_per_layer": round(pack_ms, 3), "sparsity": args.sparsity}, dtype="bf16")
+
+
 def run_stack(args):
     """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
     after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
@@ -716,13 +766,15 @@ def main():
     ap.add_argument("--workers", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
-    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "gated", "stack"],
+    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "gated", "prune",
+                                                   "stack"],
                     default="decode",
                     help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
                          "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
                          "int8 weights and activations, batches 1,16,64; int8-prefill: one layer, int8 weights, "
                          "activations quantized per token, M=512 and 2048; gated: fused silu(gate)*up "
-                         "of gate/up at batches 1,4,16; stack: all 32 layers at batches 1..32")
+                         "of gate/up at batches 1,4,16; prune: magnitude masks of one layer; stack: all 32 layers at "
+                         "batches 1..32")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -745,7 +797,8 @@ def main():
 
     if args.workload != "decode":
         out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
-               "gated": run_gated, "stack": run_stack}[args.workload](args)
+               "gated": run_gated, "prune": run_prune,
+               "stack": run_stack}[args.workload](args)
         print(json.dumps(out), flush=True)
         return
 
