@@ -311,6 +311,33 @@ def magnitude_mask(W: np.ndarray, dtype: str, prune: int) -> np.ndarray:
     keep[order[:prune]] = 0
     return keep.reshape(np.shape(W))
 
+def weight_grad_f64(dY: np.ndarray, X: np.ndarray, dtype: str, p: Packed) -> np.ndarray:
+    """Gradient of a sparse linear layer Y = X (W.Mask)^T with respect to its
+    kept weights (Algorithm 1 trains with the mask held fixed, so pruned
+    entries get no gradient): G[n][k] = Mask[n][k] * sum_m dY[m][n] X[m][k],
+    dense [N][K] binary64 (zeros off the mask)."""
+    g = to_f64(dY, dtype).T @ to_f64(X, dtype)
+    return g * mask_of(p)
+
+
+def input_grad_f64(dY: np.ndarray, dtype: str, p: Packed) -> np.ndarray:
+    """Gradient with respect to the activations: dX = dY (W.Mask), [M][K] binary64."""
+    return to_f64(dY, dtype) @ to_f64(unpack(p), dtype)
+
+
+def sgd_f64(w: np.ndarray, g: np.ndarray, lr: float) -> np.ndarray:
+    """One masked SGD step on the kept weights (Algorithm 1: theta <- theta - lr grad,
+    then masked; the kept values are the only ones stored): w - lr g in binary64."""
+    return np.asarray(w, dtype=np.float64) - float(lr) * np.asarray(g, dtype=np.float64)
+
+
+def mask_of(p: Packed) -> np.ndarray:
+    """The keep-mask [N][K] (0/1 float64) of a row-layout pack, from its bitmask."""
+    words = (p.K + 31) // 32
+    bm = np.ascontiguousarray(p.bitmask, dtype=np.uint32).reshape(p.N, words)
+    bits = (bm[:, :, None] >> np.arange(32, dtype=np.uint32)[None, None, :]) & 1
+    return bits.reshape(p.N, words * 32)[:, :p.K].astype(np.float64)
+
 def f16_to_f64(bits: np.ndarray) -> np.ndarray:
     lib = _load()
     bits = np.ascontiguousarray(bits, dtype=np.uint16)

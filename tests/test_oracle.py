@@ -598,3 +598,59 @@ def test_magnitude_mask_invariants_and_generator(orc, dtype, sparsity):
     cut, kept = np.flatnonzero(~k & (mag == t)), np.flatnonzero(k & (mag == t))
     assert cut.size and (not kept.size or cut.max() < kept.min())
     assert np.array_equal(keep, synth.magnitude_mask(W, sparsity))
+
+
+def _loss(orc, X, p, dY, dtype):
+    """L = sum_{m,n} dY[m][n] Y[m][n] with Y from the forward oracle."""
+    return float((orc.to_f64(dY, dtype) * orc.linear_f64(X, p)).sum())
+
+
+def test_weight_grad_finite_difference(orc):
+    """L is linear in each weight, so replacing a kept weight w by w' changes
+    the forward oracle's L by exactly (w' - w) G[n][k] (up to binary64
+    rounding); a pruned position has no gradient."""
+    N, K, M = 24, 64, 9
+    W, mask = synth.weight(91, N, K, "bf16", 0.6)
+    X = synth.activations(92, M, K, "bf16")
+    dY = synth.activations(93, M, N, "bf16")
+    p = orc.pack(W, "bf16", mask)
+    G = orc.weight_grad_f64(dY, X, "bf16", p)
+    assert not G[mask == 0].any()
+    base = _loss(orc, X, p, dY, "bf16")
+    rng = np.random.default_rng(0)
+    kept = np.argwhere(mask == 1)
+    for n, k in kept[rng.choice(len(kept), 12, replace=False)]:
+        W2 = W.copy()
+        W2[n, k] = synth.round_to(np.array([0.375], np.float32), "bf16")[0]
+        delta = orc.to_f64(W2[n:n + 1, k:k + 1], "bf16")[0, 0] - orc.to_f64(W[n:n + 1, k:k + 1], "bf16")[0, 0]
+        dl = _loss(orc, X, orc.pack(W2, "bf16", mask), dY, "bf16") - base
+        assert abs(dl - delta * G[n, k]) <= 1e-9 * (1 + abs(dl))
+
+
+def test_input_grad_finite_difference_and_library(orc):
+    """dX from the oracle: changing X[m][k] to x' changes L by (x' - x) dX[m][k];
+    and dY (W.Mask) by numpy on the unpacked weights."""
+    N, K, M = 20, 48, 6
+    W, mask = synth.weight(94, N, K, "f16", 0.7)
+    X = synth.activations(95, M, K, "f16")
+    dY = synth.activations(96, M, N, "f16")
+    p = orc.pack(W, "f16", mask)
+    D = orc.input_grad_f64(dY, "f16", p)
+    dense = orc.to_f64(W, "f16") * mask
+    assert np.allclose(D, orc.to_f64(dY, "f16") @ dense, rtol=1e-13, atol=1e-15)
+    base = _loss(orc, X, p, dY, "f16")
+    for m, k in [(0, 0), (5, 47), (3, 11), (2, 30)]:
+        X2 = X.copy()
+        X2[m, k] = synth.round_to(np.array([2.5], np.float32), "f16")[0]
+        delta = orc.to_f64(X2[m:m + 1, k:k + 1], "f16")[0, 0] - orc.to_f64(X[m:m + 1, k:k + 1], "f16")[0, 0]
+        dl = _loss(orc, X2, p, dY, "f16") - base
+        assert abs(dl - delta * D[m, k]) <= 1e-9 * (1 + abs(dl))
+
+
+def test_mask_of_and_sgd(orc):
+    """mask_of reproduces the mask given to pack (row layout bits); one SGD
+    step is w - lr g exactly on representable inputs."""
+    W, mask = synth.weight(97, 9, 70, "bf16", 0.5)
+    assert np.array_equal(orc.mask_of(orc.pack(W, "bf16", mask)), mask.astype(np.float64))
+    w = np.array([1.0, -2.0, 0.5]); g = np.array([4.0, 0.25, -1.0])
+    assert orc.sgd_f64(w, g, 0.5).tolist() == [-1.0, -2.125, 1.0]
