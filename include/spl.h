@@ -167,6 +167,33 @@ spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, voi
 spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
                                 hipStream_t stream);
 
+/* Sparse training with the mask held fixed (paper Algorithm 1: the gradient is
+ * masked and so are the weights after each step, i.e. only the kept values
+ * change).  For Y = X (W.Mask)^T with an upstream gradient dY [M][N]:
+ *
+ * spl_sparse_weight_grad: grad_values = the kept entries of dY^T X, in Wc's
+ *   value order (so an update is elementwise on Wc->values):
+ *   grad[n][k] = sum_m dY[m][n] X[m][k], fp32 sums, one rounding to the payload
+ *   type.  dY [M][N] and X [M][K] of Wc->dtype; Wc in the tile layout;
+ *   grad_values out, nnz entries.  Requires M % 8 == 0 (M == 0:
+ *   SPL_ERR_UNSUPPORTED), K % 8 == 0, M <= 4194240.  workspace: device
+ *   scratch of spl_sparse_weight_grad_workspace_bytes(M, N, K) bytes,
+ *   256-byte aligned, caller-owned (transposed dY and X and the dense product).
+ * spl_sparse_sgd_update: Wc->values[i] = RNE(v - lr * g) with v, g decoded
+ *   from the payloads and each operation rounded to binary32; in place.
+ * The input gradient dX = dY (W.Mask) is spl_sparse_linear(dY, Wt) with Wt the
+ * packed transpose: spl_unpack, spl_transpose16, then pack (the same kept
+ * products; kept zeros may be dropped).
+ * spl_transpose16: dst [C][R] = src [R][C]^T for 16-bit payloads (R <= 4194240).
+ * spl_gather_tiled: the entries of a dense [N][K] matrix (16-byte aligned,
+ *   K % 8 == 0) at the kept positions of a tile pattern, in its value order. */
+spl_status spl_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t stream);
+spl_status spl_gather_tiled(const void* W_dense, const spl_matrix* pattern, void* values_out, hipStream_t stream);
+int64_t spl_sparse_weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
+spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix* Wc, void* grad_values,
+                                  void* workspace, hipStream_t stream);
+spl_status spl_sparse_sgd_update(const spl_matrix* Wc, const void* grad_values, float lr, hipStream_t stream);
+
 /* One-shot magnitude pruning on the GPU (paper section 2 removes the weights
  * of smallest magnitude; the reading taken: per matrix, exactly `prune`
  * entries are zeroed, those of smallest decoded |w|, ties in ascending

@@ -104,6 +104,11 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_linear_silu_mul": (ctypes.c_int, [P, I64, MP, MP, P, I32, P]),
         "spl_magnitude_mask_workspace_bytes": (I64, []),
         "spl_magnitude_mask": (ctypes.c_int, [P, I32, I64, I64, I64, P, P, P]),
+        "spl_transpose16": (ctypes.c_int, [P, I64, I64, P, P]),
+        "spl_gather_tiled": (ctypes.c_int, [P, MP, P, P]),
+        "spl_sparse_weight_grad_workspace_bytes": (I64, [I64, I64, I64]),
+        "spl_sparse_weight_grad": (ctypes.c_int, [P, P, I64, MP, P, P, P]),
+        "spl_sparse_sgd_update": (ctypes.c_int, [MP, P, ctypes.c_float, P]),
         "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
         "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
@@ -288,6 +293,54 @@ def magnitude_mask(W: torch.Tensor, prune: int, out: torch.Tensor | None = None,
     _check("spl_magnitude_mask", L.spl_magnitude_mask(_ptr(W), _TORCH_DTYPE[W.dtype], N, K, int(prune), _ptr(out),
                                                       _ptr(workspace), _stream(stream)))
     return out
+
+
+def transpose16(A: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """out [C][R] = A [R][C]^T for a 16-bit matrix (see spl_transpose16)."""
+    L = lib()
+    _dev_tensor(A, "A")
+    R, C = A.shape
+    if out is None:
+        out = torch.empty((C, R), dtype=A.dtype, device=A.device)
+    _check("spl_transpose16", L.spl_transpose16(_ptr(A), R, C, _ptr(out), _stream(stream)))
+    return out
+
+
+def gather_tiled(W: torch.Tensor, pattern: SparseMatrix, out: torch.Tensor | None = None, stream=None):
+    """The entries of dense W [N][K] at the kept positions of `pattern`, in its value order."""
+    L = lib()
+    _dev_tensor(W, "W")
+    if out is None:
+        out = torch.empty_like(pattern.values)
+    view = pattern.view()
+    _check("spl_gather_tiled", L.spl_gather_tiled(_ptr(W), ctypes.byref(view), _ptr(out), _stream(stream)))
+    return out
+
+
+def sparse_weight_grad(dY: torch.Tensor, X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = None,
+                       workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Kept entries of dY^T X in Wc's value order (see spl_sparse_weight_grad)."""
+    L = lib()
+    _dev_tensor(dY, "dY")
+    _dev_tensor(X, "X")
+    M = X.shape[0]
+    if out is None:
+        out = torch.empty_like(Wc.values)
+    if workspace is None:
+        workspace = torch.empty((L.spl_sparse_weight_grad_workspace_bytes(M, Wc.rows, Wc.cols),), dtype=torch.uint8,
+                                device=X.device)
+    view = Wc.view()
+    _check("spl_sparse_weight_grad", L.spl_sparse_weight_grad(_ptr(dY), _ptr(X), M, ctypes.byref(view), _ptr(out),
+                                                              _ptr(workspace), _stream(stream)))
+    return out
+
+
+def sparse_sgd_update(Wc: SparseMatrix, grad_values: torch.Tensor, lr: float, stream=None) -> None:
+    """Wc.values <- Wc.values - lr * grad_values in place (see spl_sparse_sgd_update)."""
+    L = lib()
+    view = Wc.view()
+    _check("spl_sparse_sgd_update", L.spl_sparse_sgd_update(ctypes.byref(view), _ptr(grad_values), float(lr),
+                                                            _stream(stream)))
 
 
 def quantize_rows_i8(X: torch.Tensor, out: torch.Tensor | None = None, scales: torch.Tensor | None = None,

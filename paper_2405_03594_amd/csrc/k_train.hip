@@ -1,0 +1,122 @@
+// Sparse training step with the mask held fixed (paper Algorithm 1): the
+// gradient of Y = X (W.Mask)^T with respect to the kept weights, and the SGD
+// update of the stored values.
+//
+// Weight gradient G = Mask . (dY^T X): both operands are [M][*] row-major and
+// the reduction runs over M, so dY and X are first transposed (LDS-tiled
+// copies) into [N][M] and [K][M]; the dense prefill kernel then computes
+// G = dY^T X as an M-deep product on the matrix cores ([N][K], payload type,
+// fp32 sums); finally the kept entries are gathered into the tile layout's
+// value order (the inverse of the decode kernels' expansion: lane (fr, fg) of
+// a tile's wave owns row fr, columns 8 fg .. 8 fg + 7, and its values start
+// at the exclusive wave scan of the lanes' kept counts).
+#include "spl_common.h"
+
+namespace spl {
+namespace {
+
+constexpr int kTT = 64;                 // transpose tile edge
+
+// dst[c][r] = src[r][c] for a 16-bit [R][C] matrix: 64 x 64 tiles through LDS
+// (a padded row so that the column reads hit distinct banks).
+__global__ void __launch_bounds__(256) k_transpose16(const uint16_t* __restrict__ src, int64_t R, int64_t C,
+                                                     uint16_t* __restrict__ dst) {
+  __shared__ uint16_t tile[kTT][kTT + 2];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t c0 = (int64_t)blockIdx.x * kTT, r0 = (int64_t)blockIdx.y * kTT;
+#pragma unroll 4
+  for (int i = ty; i < kTT; i += 4) {
+    const int64_t r = r0 + i, c = c0 + tx;
+    tile[i][tx] = (r < R && c < C) ? src[r * C + c] : (uint16_t)0;
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int i = ty; i < kTT; i += 4) {
+    const int64_t c = c0 + i, r = r0 + tx;
+    if (c < C && r < R) dst[c * R + r] = tile[tx][i];
+  }
+}
+
+// Kept entries of a dense [N][K] matrix (K % 8 == 0) in the order of a tile
+// pattern: one wave per tile, 4 tiles per workgroup.
+__global__ void __launch_bounds__(256) k_gather_tiled(const uint16_t* __restrict__ dense,
+                                                      const uint32_t* __restrict__ bm_tiles,
+                                                      const int32_t* __restrict__ toff, int64_t N, int64_t K,
+                                                      int64_t tiles, uint16_t* __restrict__ values) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= tiles) return;                            // whole waves leave together
+  const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const int64_t S = tile_steps(K);
+  const int64_t n = (t / S) * 16 + fr;
+  const int64_t k0 = (t % S) * 32 + 8 * fg;
+  const uint32_t byte = (bm_tiles[t * 16 + fr] >> (8 * fg)) & 0xffu;   // pad rows and columns: zero bits
+  const uint32_t cnt = __popc(byte);
+  uint32_t off = (uint32_t)toff[t] + wave_inclusive_scan(cnt) - cnt;
+  if (byte == 0u) return;                            // (after the scan: every lane took part)
+  const u32x4 v = *reinterpret_cast<const u32x4*>(dense + n * K + k0);   // byte != 0: n < N, k0 + 8 <= K
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if ((byte >> j) & 1u) values[off++] = (uint16_t)((v[j >> 1] >> (16 * (j & 1))) & 0xffffu);
+}
+
+// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.
+template <class T>
+__global__ void __launch_bounds__(256) k_sgd(uint16_t* __restrict__ values, const uint16_t* __restrict__ grad,
+                                             int64_t nnz, float lr) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * 256) {
+    const float w = T::to_f32(values[i]), g = T::to_f32(grad[i]);
+    values[i] = T::from_f32(__fsub_rn(w, __fmul_rn(lr, g)));
+  }
+}
+
+constexpr int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+}  // namespace
+
+hipError_t launch_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t s) {
+  const dim3 grid((unsigned)((C + kTT - 1) / kTT), (unsigned)((R + kTT - 1) / kTT));
+  hipLaunchKernelGGL(k_transpose16, grid, dim3(256), 0, s, static_cast<const uint16_t*>(src), R, C,
+                     static_cast<uint16_t*>(dst));
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_tiled(const void* dense, const spl_matrix& P, void* values, hipStream_t s) {
+  const int64_t tiles = tile_blocks(P.rows) * tile_steps(P.cols);
+  hipLaunchKernelGGL(k_gather_tiled, dim3((unsigned)((tiles + 3) / 4)), dim3(256), 0, s,
+                     static_cast<const uint16_t*>(dense), P.bitmask, P.tile_offsets, P.rows, P.cols, tiles,
+                     static_cast<uint16_t*>(values));
+  return hipGetLastError();
+}
+
+int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  return align256(2 * N * M) + align256(2 * K * M) + align256(2 * N * K);
+}
+
+hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
+                              void* ws, hipStream_t s) {
+  const int64_t N = Wc.rows, K = Wc.cols;
+  unsigned char* base = static_cast<unsigned char*>(ws);
+  void* dYt = base;                                  // [N][M]
+  void* Xt = base + align256(2 * N * M);             // [K][M]
+  void* G = base + align256(2 * N * M) + align256(2 * K * M);   // [N][K]
+  hipError_t e = launch_transpose16(dY, M, N, dYt, s);
+  if (e == hipSuccess) e = launch_transpose16(X, M, K, Xt, s);
+  if (e == hipSuccess) e = launch_dense_prefill(dYt, N, Xt, Wc.dtype, K, M, G, s);   // G = dYt Xt^T
+  if (e == hipSuccess && Wc.nnz > 0) e = launch_gather_tiled(G, Wc, grad_values, s);
+  return e;
+}
+
+hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, hipStream_t s) {
+  if (Wc.nnz == 0) return hipSuccess;
+  int64_t blocks = (Wc.nnz + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  uint16_t* v = static_cast<uint16_t*>(const_cast<void*>(Wc.values));   // the view's values, updated in place
+  const uint16_t* g = static_cast<const uint16_t*>(grad_values);
+  if (Wc.dtype == SPL_BF16)
+    hipLaunchKernelGGL(k_sgd<Bf16>, dim3((unsigned)blocks), dim3(256), 0, s, v, g, Wc.nnz, lr);
+  else
+    hipLaunchKernelGGL(k_sgd<F16>, dim3((unsigned)blocks), dim3(256), 0, s, v, g, Wc.nnz, lr);
+  return hipGetLastError();
+}
+
+}  // namespace spl

@@ -221,7 +221,60 @@ spl_status spl_magnitude_mask(const void* W, int32_t dtype, int64_t N, int64_t K
                                              static_cast<uint32_t*>(workspace), stream));
 }
 
-// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+spl_status spl_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t stream) {
+  if (R == 0 || C == 0) return (R < 0 || C < 0) ? SPL_ERR_INVALID_ARG : SPL_OK;
+  if (!src || !dst || !dims_ok(R, C) || !aligned(src, 2) || !aligned(dst, 2)) return SPL_ERR_INVALID_ARG;
+  if ((R + 63) / 64 > 65535) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return launched(spl::launch_transpose16(src, R, C, dst, stream));
+}
+
+// A tile-layout fp16/bf16 pattern whose values can be read or written.
+static spl_status check_tiled_fp(const spl_matrix* P) {
+  const spl_status st = spl_check_matrix(P);
+  if (st != SPL_OK) return st;
+  if (!fp_dtype(P->dtype) || P->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
+  if (P->nnz > 0 && !P->values) return SPL_ERR_INVALID_ARG;
+  return SPL_OK;
+}
+
+spl_status spl_gather_tiled(const void* W_dense, const spl_matrix* pattern, void* values_out, hipStream_t stream) {
+  const spl_status st = check_tiled_fp(pattern);
+  if (st != SPL_OK) return st;
+  if (!W_dense || !values_out || !aligned(W_dense, 16) || !aligned(values_out, 2)) return SPL_ERR_INVALID_ARG;
+  if (pattern->cols % 8 != 0) return SPL_ERR_UNSUPPORTED;
+  if (pattern->nnz == 0) return SPL_OK;
+  (void)hipGetLastError();
+  return launched(spl::launch_gather_tiled(W_dense, *pattern, values_out, stream));
+}
+
+int64_t spl_sparse_weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || !dims_ok(N, K)) return -1;
+  return spl::weight_grad_workspace_bytes(M, N, K);
+}
+
+spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix* Wc, void* grad_values,
+                                  void* workspace, hipStream_t stream) {
+  const spl_status st = check_tiled_fp(Wc);
+  if (st != SPL_OK) return st;
+  if (M < 0 || !grad_values || !aligned(grad_values, 2)) return SPL_ERR_INVALID_ARG;
+  if (M == 0) return SPL_ERR_UNSUPPORTED;            // a sum over no tokens: the caller zeroes the gradient
+  if (!dY || !X || !workspace || !dims_ok(M, Wc->rows) || !dims_ok(M, Wc->cols)) return SPL_ERR_INVALID_ARG;
+  if (!aligned(dY, 2) || !aligned(X, 2) || !aligned(workspace, 256)) return SPL_ERR_INVALID_ARG;
+  if (M % 8 != 0 || Wc->cols % 8 != 0 || (M + 63) / 64 > 65535) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return launched(spl::launch_weight_grad(dY, X, M, *Wc, grad_values, workspace, stream));
+}
+
+spl_status spl_sparse_sgd_update(const spl_matrix* Wc, const void* grad_values, float lr, hipStream_t stream) {
+  const spl_status st = check_tiled_fp(Wc);
+  if (st != SPL_OK) return st;
+  if (Wc->nnz > 0 && (!grad_values || !aligned(grad_values, 2))) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_sgd(*Wc, grad_values, lr, stream));
+}
+
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
 static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
   const spl_status st = spl_check_matrix(t->Wq);
   if (st != SPL_OK) return st;

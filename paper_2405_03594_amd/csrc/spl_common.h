@@ -150,6 +150,14 @@ hipError_t launch_gated_prefill(const void* X, int64_t M, const spl_matrix& Wg, 
 int64_t magnitude_mask_workspace_words();
 hipError_t launch_magnitude_mask(const uint16_t* W, int64_t n, uint32_t prune, uint8_t* mask, uint32_t* ws,
                                  hipStream_t s);
+// Training with the mask held fixed: transposes, gather into a tile pattern,
+// the weight gradient (workspace of weight_grad_workspace_bytes) and SGD.
+hipError_t launch_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t s);
+hipError_t launch_gather_tiled(const void* dense, const spl_matrix& P, void* values, hipStream_t s);
+int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
+                              void* ws, hipStream_t s);
+hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

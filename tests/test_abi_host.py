@@ -289,3 +289,30 @@ def test_magnitude_mask_argument_checks(L):
     assert f(W + 8, 2, 4, 64, 10, m, ws, None) == INVALID                  # misaligned W
     assert f(W, 2, 4, 64, 10, m + 4, ws, None) == INVALID                  # misaligned mask
     assert f(W, 2, 0, 64, 10, m, ws, None) == INVALID                      # N = 0
+
+
+def test_training_argument_checks(L):
+    """Checks that return before any HIP call (no device needed)."""
+    m = _mat(layout=1, tile_offsets=0x40000)
+    A, B, G, ws = 0x40000, 0x50000, 0x60000, 0x70000
+    t = L.spl_transpose16
+    assert t(A, 0, 5, B, None) == OK and t(A, 5, 0, B, None) == OK
+    assert t(A, -1, 5, B, None) == INVALID
+    assert t(None, 4, 4, B, None) == INVALID and t(A, 4, 4, None, None) == INVALID
+    assert t(A, 64 * 65536, 4, B, None) == UNSUPPORTED
+    g = L.spl_gather_tiled
+    assert g(None, ctypes.byref(m), G, None) == INVALID
+    assert g(A + 8, ctypes.byref(m), G, None) == INVALID                       # misaligned dense rows
+    assert g(A, ctypes.byref(_mat()), G, None) == UNSUPPORTED                 # row layout
+    assert g(A, ctypes.byref(_mat(dtype=3, layout=1, tile_offsets=0x40000)), G, None) == UNSUPPORTED
+    w = L.spl_sparse_weight_grad
+    assert L.spl_sparse_weight_grad_workspace_bytes(16, 4, 64) >= 2 * (4 * 16 + 64 * 16 + 4 * 64)
+    assert L.spl_sparse_weight_grad_workspace_bytes(-1, 4, 64) < 0
+    assert w(A, B, 0, ctypes.byref(m), G, ws, None) == UNSUPPORTED             # no tokens
+    assert w(A, B, 12, ctypes.byref(m), G, ws, None) == UNSUPPORTED            # M % 8 != 0
+    assert w(A, B, 16, ctypes.byref(m), G, ws + 16, None) == INVALID           # workspace alignment
+    assert w(None, B, 16, ctypes.byref(m), G, ws, None) == INVALID
+    assert w(A, B, 16, ctypes.byref(m), None, ws, None) == INVALID
+    s = L.spl_sparse_sgd_update
+    assert s(ctypes.byref(m), None, 0.1, None) == INVALID                      # nnz > 0 needs a gradient
+    assert s(ctypes.byref(_mat()), G, 0.1, None) == UNSUPPORTED                # row layout

@@ -1,0 +1,115 @@
+"""Sparse training with the mask held fixed (Algorithm 1) on the GPU vs the
+oracle: the transposes and the gather into a tile pattern are data movement
+(bit for bit); the weight gradient (fp32 sums over M, one rounding) and the
+input gradient (the sparse linear layer on the packed transpose) are checked
+with |y - y64| <= max(2e-2, 1e-2 |y64|); one SGD step (binary32 product and
+difference, one rounding) within 2^-8 |y64| (bf16) / 2^-11 |y64| (fp16), plus
+2^-22 (|w| + lr |g|) for the binary32 steps and the smallest normal of the
+payload type."""
+import numpy as np
+import pytest
+
+import synth
+from tests._helpers import assert_close, from_dev_bits, from_dev_f64, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def spl():
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    return spl
+
+
+def _with_values(spl, Wc, values):
+    return spl.SparseMatrix(Wc.bitmask, values, None, Wc.tile_offsets, Wc.rows, Wc.cols, Wc.nnz, "tile16")
+
+
+@pytest.mark.parametrize("R,C", [(1, 1), (3, 70), (65, 129), (1000, 4096), (4096, 64)])
+def test_transpose16(spl, R, C):
+    A = np.random.default_rng(R * C).integers(0, 1 << 16, size=(R, C), dtype=np.uint16)
+    got = from_dev_bits(spl.transpose16(to_dev(A, "bf16")))
+    assert np.array_equal(got, A.T)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (17, 72, 0.7), (100, 1000, 0.0), (300, 264, 0.9), (33, 512, 1.0)])
+def test_gather_tiled_matches_pack(spl, dtype, N, K, s):
+    """Gathering W's own entries at its pattern reproduces the packed values."""
+    import torch
+
+    W, mask = synth.weight(600 + N, N, K, dtype, s)
+    Wd = to_dev(W, dtype)
+    Wc = spl.pack_sparse(Wd, torch.from_numpy(mask).cuda())
+    got = spl.gather_tiled(Wd, Wc)
+    assert np.array_equal(from_dev_bits(got)[:Wc.nnz], from_dev_bits(Wc.values)[:Wc.nnz])
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,M,s", [(24, 64, 16, 0.6), (100, 1000, 64, 0.7), (300, 264, 136, 0.5), (33, 512, 8, 0.9),
+                                     (130, 96, 520, 0.7)])
+def test_weight_grad(orc, spl, dtype, N, K, M, s):
+    import torch
+
+    W, mask = synth.weight(610 + N, N, K, dtype, s)
+    X = synth.activations(611 + K, M, K, dtype)
+    dY = synth.activations(612 + M, M, N, dtype)
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    g = spl.sparse_weight_grad(to_dev(dY, dtype), to_dev(X, dtype), Wc)
+    G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
+    ref = orc.weight_grad_f64(dY, X, dtype, orc.pack(W, dtype, mask))
+    assert_close(G, ref, f"weight grad {dtype} N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_sgd_update(orc, spl, dtype):
+    import torch
+
+    N, K = 200, 528
+    W, mask = synth.weight(620, N, K, dtype, 0.7)
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    w0 = orc.to_f64(from_dev_bits(Wc.values)[:Wc.nnz], dtype)
+    G = synth.round_to(synth.normal_f32(621, (Wc.values.numel(),), 1.0), dtype)
+    for lr in (0.01, 0.5):
+        w = orc.to_f64(from_dev_bits(Wc.values)[:Wc.nnz], dtype)
+        spl.sparse_sgd_update(Wc, to_dev(G, dtype), lr)
+        got = orc.to_f64(from_dev_bits(Wc.values)[:Wc.nnz], dtype)
+        g = orc.to_f64(G[:Wc.nnz], dtype)
+        ref = orc.sgd_f64(w, g, lr)
+        rel, tiny = (2.0 ** -8, 2.0 ** -126) if dtype == "bf16" else (2.0 ** -11, 2.0 ** -14)
+        # + the binary32 rounding of lr * g and of the difference, relative to the operands
+        tol = rel * np.abs(ref) + 2.0 ** -22 * (np.abs(w) + lr * np.abs(g)) + tiny
+        assert (np.abs(got - ref) <= tol).all(), f"lr={lr}"
+    assert not np.array_equal(got, w0)
+    dense = from_dev_f64(spl.unpack(Wc))
+    assert not dense[mask == 0].any()                  # pruned entries stay zero
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,M,s", [(104, 1000, 64, 0.7), (296, 264, 136, 0.5), (48, 520, 3, 0.9)])
+def test_input_grad_via_packed_transpose(orc, spl, dtype, N, K, M, s):
+    import torch
+
+    W, mask = synth.weight(630 + N, N, K, dtype, s)
+    dY = synth.activations(631 + M, M, N, dtype)
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    Wt = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)))          # [K][N], the non-zero kept entries
+    dX = from_dev_f64(spl.sparse_linear(to_dev(dY, dtype), Wt))       # N % 8 == 0: rows of dY in 16-byte pieces
+    assert_close(dX, orc.input_grad_f64(dY, dtype, orc.pack(W, dtype, mask)), f"dX {dtype} N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("name,j,M", [("q", 0, 256), ("gate", 4, 128), ("down", 6, 64)])
+def test_weight_grad_llama_shapes(orc, spl, name, j, M):
+    import torch
+
+    _, N, K = synth.LLAMA2_7B_LINEARS[j]
+    W, mask = synth.weight(synth.weight_seed(0, j), N, K, "bf16", 0.7)
+    X = synth.activations(synth.activation_seed(j), M, K, "bf16")
+    dY = synth.activations(640 + j, M, N, "bf16")
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), torch.from_numpy(mask).cuda())
+    g = spl.sparse_weight_grad(to_dev(dY, "bf16"), to_dev(X, "bf16"), Wc)
+    G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
+    ref = orc.to_f64(dY, "bf16").T @ orc.to_f64(X, "bf16") * mask
+    assert_close(G, ref, f"{name} weight grad M={M}")
