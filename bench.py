@@ -695,6 +695,94 @@ def run_prune(args):
                  cpu, {"pack_sparse_ms_per_layer": round(pack_ms, 3), "sparsity": args.sparsity}, dtype="bf16")
 
 
+def run_train(args):
+    """One sparse training step of a Llama-2-7B layer's seven linears with the
+    mask held fixed (Algorithm 1), M = 2048 tokens, bf16: per matrix the
+    forward product, the weight gradient in the packed value order, the SGD
+    update of the stored values, a refresh of the packed transpose's values
+    (a permutation gather) and the input gradient through it."""
+    shapes = synth.LLAMA2_7B_LINEARS
+    host = generate_layers(1, "bf16", args.sparsity, args.workers)[0]
+    torch, spl = _need_gpu()
+    M = 2048
+    lr = 1e-3
+    mats, mats_t, perms, ws, grads, xs, dys, ys, dxs = [], [], [], [], [], [], [], [], []
+    for j, (_, N, K) in enumerate(shapes):
+        W, mask = host[j]
+        Wd = _to_dev(W, "bf16", torch)
+        md = torch.from_numpy(mask).cuda()
+        Wc = spl.pack_sparse(Wd, md)
+        Wt = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), md.t().contiguous())   # set-up: the transposed pattern
+        mats.append(Wc)
+        mats_t.append(Wt)
+        perms.append(spl.transpose_perm(Wc, Wt))                          # set-up: Wt's values from Wc's
+        ws.append(torch.empty((spl.lib().spl_sparse_weight_grad_workspace_bytes(M, N, K),), dtype=torch.uint8,
+                              device="cuda"))
+        grads.append(torch.empty_like(Wc.values))
+        xs.append(_to_dev(synth.activations(synth.activation_seed(j), M, K, "bf16"), "bf16", torch))
+        dys.append(_to_dev(synth.activations(700 + j, M, N, "bf16"), "bf16", torch))
+        ys.append(torch.empty((M, N), dtype=torch.bfloat16, device="cuda"))
+        dxs.append(torch.empty((M, K), dtype=torch.bfloat16, device="cuda"))
+    del host
+
+    def step(li, j, part="all"):
+        if part in ("all", "fwd"):
+            spl.sparse_linear(xs[j], mats[j], out=ys[j])
+        if part in ("all", "wgrad"):
+            spl.sparse_weight_grad(dys[j], xs[j], mats[j], out=grads[j], workspace=ws[j])
+        if part in ("all", "update"):
+            spl.sparse_sgd_update(mats[j], grads[j], lr)
+            spl.permute_values(mats[j].values, perms[j], mats[j].nnz, mats_t[j].values)
+        if part in ("all", "dgrad"):
+            spl.sparse_linear(dys[j], mats_t[j], out=dxs[j])
+
+    units = list(range(len(shapes)))
+    wall, gpu = _timed(units, lambda li, j: step(li, j), args.steps, args.warmup, [0])
+    parts = {}
+    for part in ("fwd", "wgrad", "update", "dgrad"):
+        _, g = _timed(units, lambda li, j, part=part: step(li, j, part), max(5, args.steps // 4), 2, [0])
+        parts[part + "_us"] = round(g * 1e3, 1)
+    flops = sum(2.0 * M * N * K for (_, N, K) in shapes)                # one dense-equivalent product
+    wgrad_ms = parts["wgrad_us"] * 1e-3
+    achieved = flops / (wgrad_ms * 1e-3) / 1e12
+    parts["step_dense_equiv_tflops"] = round(3 * flops / (gpu * 1e-3) / 1e12, 1)
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        N, K = shapes[0][1], shapes[0][2]
+        Wq, mq = synth.weight(synth.weight_seed(0, 0), N, K, "bf16", args.sparsity)
+        p = oracle.pack(Wq, "bf16", mq)
+        rows = 64
+        X = synth.activations(synth.activation_seed(0), rows, K, "bf16")
+        dY = synth.activations(700, rows, N, "bf16")
+        threads = oracle.max_threads()
+
+        def one():
+            oracle.linear_f64(X, p, nthreads=threads)
+            oracle.weight_grad_f64(dY, X, "bf16", p)
+            oracle.input_grad_f64(dY, "bf16", p)
+
+        reps, dt = _oracle_repeat(one)
+        layer_over_q = sum(N_ * K_ for (_, N_, K_) in shapes) / (N * K)
+        cpu = {"value": round(reps * rows / dt / layer_over_q, 3), "unit": "tokens/s", "cores": threads,
+               "kind": "oracle",
+               "sample": f"{rows} tokens through the q matrix (forward, weight and input gradients in binary64), "
+                         f"repeated {reps} times ({dt:.1f} s), scaled to the layer's seven matrices by element "
+                         f"count ({layer_over_q:.2f}x q)"}
+    return _line(args, "sparse training step tokens/s (mask held fixed), Llama-2-7B layer's linears",
+                 round(M / (wall * 1e-3), 1), "tokens/s", wall,
+                 f"Llama-2-7B decoder layer, 7 linears, bf16, {int(args.sparsity * 100)}% magnitude sparsity, "
+                 f"M = {M} tokens: forward, weight gradient, SGD on the packed values, transposed-pack refresh "
+                 f"(permutation), "
+                 f"input gradient",
+                 {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                  "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                  "kernel": "weight gradient (k_transpose16 x2, k_dense_prefill, k_gather_tiled)",
+                  "flops_per_launch": "2*M*N*K per matrix", "avg_launch_us": round(parts["wgrad_us"] / 7, 3)},
+                 cpu, {"parts_per_layer": parts, "sparsity": args.sparsity, "lr": lr})
+
+
 def run_stack(args):
     """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
     after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
@@ -767,13 +855,14 @@ def main():
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
     ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "gated", "prune",
-                                                   "stack"],
+                                                   "train", "stack"],
                     default="decode",
                     help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
                          "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
                          "int8 weights and activations, batches 1,16,64; int8-prefill: one layer, int8 weights, "
                          "activations quantized per token, M=512 and 2048; gated: fused silu(gate)*up "
-                         "of gate/up at batches 1,4,16; prune: magnitude masks of one layer; stack: all 32 layers at "
+                         "of gate/up at batches 1,4,16; prune: magnitude masks of one layer; train: a masked training step of one "
+                         "layer at M=2048; stack: all 32 layers at "
                          "batches 1..32")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
@@ -797,7 +886,7 @@ def main():
 
     if args.workload != "decode":
         out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
-               "gated": run_gated, "prune": run_prune,
+               "gated": run_gated, "prune": run_prune, "train": run_train,
                "stack": run_stack}[args.workload](args)
         print(json.dumps(out), flush=True)
         return

@@ -187,6 +187,18 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
  * spl_transpose16: dst [C][R] = src [R][C]^T for 16-bit payloads (R <= 4194240).
  * spl_gather_tiled: the entries of a dense [N][K] matrix (16-byte aligned,
  *   K % 8 == 0) at the kept positions of a tile pattern, in its value order. */
+/* Keeping the packed transpose in step with W after updates, without a dense
+ * pass: spl_transpose_perm computes, once per pattern, perm[i] = the position
+ * in W's values of value i of Wt, where Wt [K][N] is W packed transposed with
+ * the transposed mask (same nnz and dtype; N % 8 == 0 and K % 8 == 0);
+ * workspace: spl_transpose_perm_workspace_bytes(N, K, nnz) bytes, 256-byte
+ * aligned.  spl_permute_values then copies dst[i] = src[perm[i]] (nnz 16-bit
+ * payloads, src holding nnz of them), e.g. Wt.values from W.values after each
+ * SGD step; a perm entry outside [0, nnz) gives 0 and reads nothing. */
+int64_t spl_transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz);
+spl_status spl_transpose_perm(const spl_matrix* W, const spl_matrix* Wt, int32_t* perm, void* workspace,
+                              hipStream_t stream);
+spl_status spl_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t stream);
 spl_status spl_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t stream);
 spl_status spl_gather_tiled(const void* W_dense, const spl_matrix* pattern, void* values_out, hipStream_t stream);
 int64_t spl_sparse_weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);

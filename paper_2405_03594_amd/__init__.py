@@ -109,6 +109,9 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_weight_grad_workspace_bytes": (I64, [I64, I64, I64]),
         "spl_sparse_weight_grad": (ctypes.c_int, [P, P, I64, MP, P, P, P]),
         "spl_sparse_sgd_update": (ctypes.c_int, [MP, P, ctypes.c_float, P]),
+        "spl_transpose_perm_workspace_bytes": (I64, [I64, I64, I64]),
+        "spl_transpose_perm": (ctypes.c_int, [MP, MP, P, P, P]),
+        "spl_permute_values": (ctypes.c_int, [P, P, I64, P, P]),
         "spl_dense_linear": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, P]),
         "spl_dense_linear_ex": (ctypes.c_int, [P, I64, P, I32, I64, I64, P, I32, P]),
         "spl_dense_linear_int8": (ctypes.c_int, [P, P, I64, P, P, I64, I64, P, P, P]),
@@ -341,6 +344,25 @@ def sparse_sgd_update(Wc: SparseMatrix, grad_values: torch.Tensor, lr: float, st
     view = Wc.view()
     _check("spl_sparse_sgd_update", L.spl_sparse_sgd_update(ctypes.byref(view), _ptr(grad_values), float(lr),
                                                             _stream(stream)))
+
+
+def transpose_perm(W: SparseMatrix, Wt: SparseMatrix, stream=None) -> torch.Tensor:
+    """perm (int32 [nnz]): value i of Wt is value perm[i] of W (see spl_transpose_perm)."""
+    L = lib()
+    perm = torch.empty((max(W.nnz, 1),), dtype=torch.int32, device=W.values.device)
+    ws = torch.empty((max(L.spl_transpose_perm_workspace_bytes(W.rows, W.cols, W.nnz), 1),), dtype=torch.uint8,
+                     device=W.values.device)
+    vw, vt = W.view(), Wt.view()
+    _check("spl_transpose_perm", L.spl_transpose_perm(ctypes.byref(vw), ctypes.byref(vt), _ptr(perm), _ptr(ws),
+                                                      _stream(stream)))
+    return perm
+
+
+def permute_values(src: torch.Tensor, perm: torch.Tensor, nnz: int, out: torch.Tensor, stream=None) -> torch.Tensor:
+    """out[i] = src[perm[i]] for i < nnz (see spl_permute_values)."""
+    L = lib()
+    _check("spl_permute_values", L.spl_permute_values(_ptr(src), _ptr(perm), int(nnz), _ptr(out), _stream(stream)))
+    return out
 
 
 def quantize_rows_i8(X: torch.Tensor, out: torch.Tensor | None = None, scales: torch.Tensor | None = None,

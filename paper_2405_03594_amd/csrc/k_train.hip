@@ -59,7 +59,49 @@ __global__ void __launch_bounds__(256) k_gather_tiled(const uint16_t* __restrict
     if ((byte >> j) & 1u) values[off++] = (uint16_t)((v[j >> 1] >> (16 * (j & 1))) & 0xffffu);
 }
 
-// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.
+// The value position of every kept entry of a tile pattern, written into a
+// dense [N][K] image as two 16-bit planes (low and high halves); entries off
+// the pattern are not written.  The same lane schedule as k_gather_tiled.
+__global__ void __launch_bounds__(256) k_scatter_positions(const uint32_t* __restrict__ bm_tiles,
+                                                           const int32_t* __restrict__ toff, int64_t K, int64_t tiles,
+                                                           uint16_t* __restrict__ lo, uint16_t* __restrict__ hi) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= tiles) return;
+  const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const int64_t S = tile_steps(K);
+  const int64_t n = (t / S) * 16 + fr;
+  const int64_t k0 = (t % S) * 32 + 8 * fg;
+  const uint32_t byte = (bm_tiles[t * 16 + fr] >> (8 * fg)) & 0xffu;
+  const uint32_t cnt = __popc(byte);
+  uint32_t off = (uint32_t)toff[t] + wave_inclusive_scan(cnt) - cnt;
+  if (byte == 0u) return;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if ((byte >> j) & 1u) {
+      lo[n * K + k0 + j] = (uint16_t)(off & 0xffffu);
+      hi[n * K + k0 + j] = (uint16_t)(off >> 16);
+      ++off;
+    }
+}
+
+__global__ void __launch_bounds__(256) k_join_halves(const uint16_t* __restrict__ lo, const uint16_t* __restrict__ hi,
+                                                     int64_t nnz, int32_t* __restrict__ perm) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * 256)
+    perm[i] = (int32_t)((uint32_t)lo[i] | ((uint32_t)hi[i] << 16));
+}
+
+// dst[i] = src[perm[i]] (16-bit payloads, src of nnz entries); a position
+// outside [0, nnz) (a permutation of another pattern) reads nothing and gives 0.
+__global__ void __launch_bounds__(256) k_permute_values(const uint16_t* __restrict__ src,
+                                                        const int32_t* __restrict__ perm, int64_t nnz,
+                                                        uint16_t* __restrict__ dst) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nnz; i += (int64_t)gridDim.x * 256) {
+    const int32_t p = perm[i];
+    dst[i] = (p >= 0 && (int64_t)p < nnz) ? src[p] : (uint16_t)0;
+  }
+}
+
+// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.
 template <class T>
 __global__ void __launch_bounds__(256) k_sgd(uint16_t* __restrict__ values, const uint16_t* __restrict__ grad,
                                              int64_t nnz, float lr) {
@@ -104,6 +146,45 @@ hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const sp
   if (e == hipSuccess) e = launch_dense_prefill(dYt, N, Xt, Wc.dtype, K, M, G, s);   // G = dYt Xt^T
   if (e == hipSuccess && Wc.nnz > 0) e = launch_gather_tiled(G, Wc, grad_values, s);
   return e;
+}
+
+int64_t transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz) {
+  return 4 * align256(2 * N * K) + 2 * align256(2 * nnz);
+}
+
+// perm[i] = the position in W's values of the entry that is value i of Wt,
+// Wt's pattern being the transpose of W's: position images of W (two 16-bit
+// planes), transposed, then gathered at Wt's pattern and joined.
+hipError_t launch_transpose_perm(const spl_matrix& W, const spl_matrix& Wt, int32_t* perm, void* ws, hipStream_t s) {
+  const int64_t N = W.rows, K = W.cols;
+  unsigned char* b = static_cast<unsigned char*>(ws);
+  uint16_t* lo = reinterpret_cast<uint16_t*>(b);
+  uint16_t* hi = reinterpret_cast<uint16_t*>(b + align256(2 * N * K));
+  uint16_t* lot = reinterpret_cast<uint16_t*>(b + 2 * align256(2 * N * K));
+  uint16_t* hit = reinterpret_cast<uint16_t*>(b + 3 * align256(2 * N * K));
+  uint16_t* plo = reinterpret_cast<uint16_t*>(b + 4 * align256(2 * N * K));
+  uint16_t* phi = reinterpret_cast<uint16_t*>(b + 4 * align256(2 * N * K) + align256(2 * Wt.nnz));
+  const int64_t tiles = tile_blocks(N) * tile_steps(K);
+  hipLaunchKernelGGL(k_scatter_positions, dim3((unsigned)((tiles + 3) / 4)), dim3(256), 0, s, W.bitmask,
+                     W.tile_offsets, K, tiles, lo, hi);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) e = launch_transpose16(lo, N, K, lot, s);
+  if (e == hipSuccess) e = launch_transpose16(hi, N, K, hit, s);
+  if (e == hipSuccess) e = launch_gather_tiled(lot, Wt, plo, s);
+  if (e == hipSuccess) e = launch_gather_tiled(hit, Wt, phi, s);
+  if (e != hipSuccess) return e;
+  int64_t blocks = (Wt.nnz + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_join_halves, dim3((unsigned)blocks), dim3(256), 0, s, plo, phi, Wt.nnz, perm);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t s) {
+  int64_t blocks = (nnz + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_permute_values, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<const uint16_t*>(src),
+                     perm, nnz, static_cast<uint16_t*>(dst));
+  return hipGetLastError();
 }
 
 hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, hipStream_t s) {

@@ -274,7 +274,36 @@ spl_status spl_sparse_sgd_update(const spl_matrix* Wc, const void* grad_values, 
   return launched(spl::launch_sgd(*Wc, grad_values, lr, stream));
 }
 
-// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+int64_t spl_transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz) {
+  if (!dims_ok(N, K) || nnz < 0) return -1;
+  return spl::transpose_perm_workspace_bytes(N, K, nnz);
+}
+
+spl_status spl_transpose_perm(const spl_matrix* W, const spl_matrix* Wt, int32_t* perm, void* workspace,
+                              hipStream_t stream) {
+  spl_status st = check_tiled_fp(W);
+  if (st != SPL_OK) return st;
+  st = check_tiled_fp(Wt);
+  if (st != SPL_OK) return st;
+  if (Wt->rows != W->cols || Wt->cols != W->rows || Wt->nnz != W->nnz || Wt->dtype != W->dtype)
+    return SPL_ERR_INVALID_ARG;
+  if (W->cols % 8 != 0 || W->rows % 8 != 0 || (W->rows + 63) / 64 > 65535 || (W->cols + 63) / 64 > 65535)
+    return SPL_ERR_UNSUPPORTED;
+  if (W->nnz == 0) return SPL_OK;
+  if (!perm || !workspace || !aligned(perm, 4) || !aligned(workspace, 256)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_transpose_perm(*W, *Wt, perm, workspace, stream));
+}
+
+spl_status spl_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t stream) {
+  if (nnz < 0) return SPL_ERR_INVALID_ARG;
+  if (nnz == 0) return SPL_OK;
+  if (!src || !perm || !dst || !aligned(src, 2) || !aligned(perm, 4) || !aligned(dst, 2)) return SPL_ERR_INVALID_ARG;
+  (void)hipGetLastError();
+  return launched(spl::launch_permute_values(src, perm, nnz, dst, stream));
+}
+
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
 static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
   const spl_status st = spl_check_matrix(t->Wq);
   if (st != SPL_OK) return st;

@@ -158,6 +158,9 @@ int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
                               void* ws, hipStream_t s);
 hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, hipStream_t s);
+int64_t transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz);
+hipError_t launch_transpose_perm(const spl_matrix& W, const spl_matrix& Wt, int32_t* perm, void* ws, hipStream_t s);
+hipError_t launch_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

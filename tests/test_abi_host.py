@@ -316,3 +316,24 @@ def test_training_argument_checks(L):
     s = L.spl_sparse_sgd_update
     assert s(ctypes.byref(m), None, 0.1, None) == INVALID                      # nnz > 0 needs a gradient
     assert s(ctypes.byref(_mat()), G, 0.1, None) == UNSUPPORTED                # row layout
+
+
+def test_transpose_perm_argument_checks(L):
+    """Checks that return before any HIP call (no device needed)."""
+    w = _mat(rows=8, cols=64, layout=1, tile_offsets=0x40000)
+    t = _mat(rows=64, cols=8, layout=1, tile_offsets=0x40000)
+    f = L.spl_transpose_perm
+    P, ws = 0x50000, 0x60000
+    assert f(ctypes.byref(w), ctypes.byref(w), P, ws, None) == INVALID        # not the transposed shape
+    assert f(ctypes.byref(w), ctypes.byref(_mat(rows=64, cols=8, nnz=9, layout=1, tile_offsets=0x40000)), P, ws,
+             None) == INVALID                                                  # nnz differs
+    assert f(ctypes.byref(w), ctypes.byref(t), None, ws, None) == INVALID
+    assert f(ctypes.byref(w), ctypes.byref(t), P, ws + 16, None) == INVALID   # workspace alignment
+    odd = _mat(rows=4, cols=64, layout=1, tile_offsets=0x40000)
+    assert f(ctypes.byref(odd), ctypes.byref(_mat(rows=64, cols=4, layout=1, tile_offsets=0x40000)), P, ws,
+             None) == UNSUPPORTED                                              # N % 8 != 0
+    p = L.spl_permute_values
+    assert p(0x40000, P, 0, 0x70000, None) == OK
+    assert p(0x40000, P, -1, 0x70000, None) == INVALID
+    assert p(None, P, 5, 0x70000, None) == INVALID
+    assert p(0x40000, P + 2, 5, 0x70000, None) == INVALID                    # misaligned perm

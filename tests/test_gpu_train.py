@@ -113,3 +113,25 @@ def test_weight_grad_llama_shapes(orc, spl, name, j, M):
     G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
     ref = orc.to_f64(dY, "bf16").T @ orc.to_f64(X, "bf16") * mask
     assert_close(G, ref, f"{name} weight grad M={M}")
+
+
+@pytest.mark.parametrize("N,K,s", [(8, 8, 0.5), (104, 1000, 0.7), (296, 264, 0.0), (64, 520, 0.9)])
+def test_transpose_perm_keeps_the_transpose_in_step(spl, N, K, s):
+    """The packed transpose (transposed mask) refreshed by the permutation
+    equals a fresh pack of the transposed weights, before and after an SGD
+    step, bit for bit."""
+    import torch
+
+    W, mask = synth.weight(650 + N, N, K, "bf16", s)
+    md = torch.from_numpy(mask).cuda()
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), md)
+    mt = md.t().contiguous()
+    Wt = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), mt)
+    perm = spl.transpose_perm(Wc, Wt)
+    for step in range(2):
+        out = torch.empty_like(Wt.values)
+        spl.permute_values(Wc.values, perm, Wc.nnz, out)
+        fresh = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), mt)
+        assert np.array_equal(from_dev_bits(out)[:Wc.nnz], from_dev_bits(fresh.values)[:Wc.nnz]), step
+        g = torch.full_like(Wc.values, 0.25)
+        spl.sparse_sgd_update(Wc, g, 0.5)
