@@ -37,7 +37,8 @@ def _constants():
     bk = int(re.search(r"constexpr int kPfBK = (\d+);", src).group(1))
     assert "constexpr int kPfRow = kPfBK * 2;" in src
     for line in ("constexpr int TW = BN / 8 / NW;",
-                 "const int64_t b = nb0 + (TW / 2) * wave + (i >> 1);",
+                 "const int64_t wb = kGated ? (int64_t)blockIdx.x * (BN / 32) + (wave >> 1) : n0 / 16 + (TW / 2) * wave;",
+                 "const int64_t b = wb + (i >> 1);",
                  "const int s = kI8 ? 4 * st + 2 * (i & 1) + (fg >> 1) : 2 * st + (i & 1);",
                  "const int64_t t = ok ? b * S + s : 0;",
                  "tw.w[i] = ok ? bm_tiles[t * 16 + fr] : 0u;",
@@ -332,3 +333,38 @@ def test_prefill_i8_schedule_and_expansion(orc, N, K, s):
                 want = {(b, sk) for b in range(nb0, min(nb0 + BN // 16, B)) for sk in range(4 * st, 4 * st + 4)
                         if sk < S}
                 assert seen == want
+
+
+@pytest.mark.parametrize("N", [16, 40, 64, 100, 128, 11008])
+@pytest.mark.parametrize("BN,NW", [(128, 8), (64, 4)])
+def test_gated_block_assignment(N, BN, NW):
+    """Gated prefill: wave w of workgroup x expands row block x BN/32 + w/2 of
+    matrix w % 2; over the grid of ceil(N / (BN/2)) workgroups every row block
+    of both matrices is expanded exactly once, the others are past the last
+    block (the checked loads skip them), and when N % (BN/2) == 0 (the
+    unchecked instantiation) none is past it.  Fragments 2p, 2p + 1 of wave
+    (wn, wm) are virtual blocks wn FN + 2p, + 1: gate and up of one real block."""
+    src = open(SRC).read()
+    for line in ("const int gm = kGated ? (wave & 1) : 0;",
+                 "constexpr int RN = kGated ? BN / 2 : BN;",
+                 "return pf_inside(2 * a.N, a.M, a.K, BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false, true>(a, s)",
+                 "const int64_t n = n0 + wn * 8 * FN + 16 * p + 4 * fg;"):
+        assert line in src, f"kernel changed: update this replay ({line})"
+    B = (N + 15) // 16
+    grid = (N + BN // 2 - 1) // (BN // 2)
+    seen = []
+    for x in range(grid):
+        for w in range(NW):
+            b = x * (BN // 32) + (w >> 1)
+            if b < B:
+                seen.append((w & 1, b))
+            else:
+                assert N % (BN // 2) != 0
+    assert sorted(seen) == sorted((m, b) for m in (0, 1) for b in range(B))
+    assert len(seen) == len(set(seen))
+    FN = BN // 32
+    for wn in range(2):
+        for p in range(FN // 2):
+            g, u = wn * FN + 2 * p, wn * FN + 2 * p + 1      # virtual blocks of the fragments (= expanding waves)
+            assert g % 2 == 0 and u % 2 == 1 and g >> 1 == u >> 1
+            assert (g >> 1) * 16 == wn * 8 * FN + 16 * p      # the real rows pf_store_gated writes
