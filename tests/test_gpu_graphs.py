@@ -78,3 +78,76 @@ def test_graph_replays_match_eager():
         got = snapshot()
         for i, (a, b) in enumerate(zip(got, eager)):
             assert np.array_equal(a, b), f"replay {rep}, output {i} differs from the eager run"
+
+
+def test_graph_replays_new_ops_match_eager():
+    """The gated silu(gate) * up launch (both kernel families), the magnitude
+    mask (zero fill, histogram atomics, tie ranks), the weight gradient
+    (transposes, product, gather) and the packed-transpose permutation in one
+    captured graph: three replays with poisoned outputs and eager work in
+    between reproduce the eager results bit for bit."""
+    import torch
+
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    N, K = 200, 1056
+    Wg, mg = synth.weight(980, N, K, "bf16", 0.7)
+    Wu, mu = synth.weight(981, N, K, "bf16", 0.5)
+    g = spl.pack_sparse(to_dev(Wg, "bf16"), torch.from_numpy(mg).cuda())
+    u = spl.pack_sparse(to_dev(Wu, "bf16"), torch.from_numpy(mu).cuda())
+    gt = spl.pack_sparse(spl.transpose16(spl.unpack(g)), torch.from_numpy(mg).cuda().t().contiguous())
+    perm = spl.transpose_perm(g, gt)
+    X1 = to_dev(synth.activations(982, 8, K, "bf16"), "bf16")
+    X2 = to_dev(synth.activations(983, 136, K, "bf16"), "bf16")
+    dY = to_dev(synth.activations(984, 136, N, "bf16"), "bf16")
+    Wp = to_dev(synth.round_to(synth.normal_f32(985, (300, 4096), 0.02), "bf16"), "bf16")
+    ws_m = torch.empty((spl.lib().spl_magnitude_mask_workspace_bytes(),), dtype=torch.uint8, device="cuda")
+    ws_g = torch.empty((spl.lib().spl_sparse_weight_grad_workspace_bytes(136, N, K),), dtype=torch.uint8,
+                       device="cuda")
+    y1 = torch.empty((8, N), dtype=torch.bfloat16, device="cuda")
+    y2 = torch.empty((136, N), dtype=torch.bfloat16, device="cuda")
+    mask = torch.empty((300, 4096), dtype=torch.uint8, device="cuda")
+    grad = torch.empty_like(g.values)
+    tv = torch.empty_like(gt.values)
+
+    def run():
+        spl.sparse_linear_silu_mul(X1, g, u, out=y1)
+        spl.sparse_linear_silu_mul(X2, g, u, out=y2)
+        spl.magnitude_mask(Wp, 300 * 4096 * 7 // 10, out=mask, workspace=ws_m)
+        spl.sparse_weight_grad(dY, X2, g, out=grad, workspace=ws_g)
+        spl.permute_values(g.values, perm, g.nnz, tv)
+
+    def snapshot():
+        return [from_dev_bits(y1), from_dev_bits(y2), mask.cpu().numpy().copy(), from_dev_bits(grad)[:g.nnz],
+                from_dev_bits(tv)[:g.nnz]]
+
+    def poison():
+        for o in (y1, y2, grad, tv):
+            o.fill_(float("nan"))
+        mask.fill_(7)
+        ws_m.fill_(0xAB)                               # the histogram must be cleared inside the graph
+        ws_g.fill_(0xCD)
+
+    run()
+    torch.cuda.synchronize()
+    eager = snapshot()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    torch.cuda.synchronize()
+    scratch = torch.randn(1 << 20, device="cuda")
+    for rep in range(3):
+        poison()
+        scratch.mul_(1.0001).add_(0.5)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(snapshot(), eager)):
+            assert np.array_equal(a, b), f"replay {rep}, output {i} differs from the eager run"
