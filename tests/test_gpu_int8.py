@@ -36,7 +36,7 @@ def _assert_equal(got, ref, what):
                              f"oracle {ref[i]!r}")
 
 
-INT8_M = [1, 5, 16, 17, 32, 33, 64, 65, 100]
+INT8_M = [1, 5, 16, 17, 32, 33, 64, 65, 100, 127]       # 127: the last batch of the streaming kernels
 
 
 @pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (16, 48, 0.5), (33, 64, 0.7), (100, 1008, 0.7), (64, 4096, 0.5),
