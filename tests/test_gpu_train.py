@@ -135,3 +135,36 @@ def test_transpose_perm_keeps_the_transpose_in_step(spl, N, K, s):
         assert np.array_equal(from_dev_bits(out)[:Wc.nnz], from_dev_bits(fresh.values)[:Wc.nnz]), step
         g = torch.full_like(Wc.values, 0.25)
         spl.sparse_sgd_update(Wc, g, 0.5)
+
+
+@pytest.mark.parametrize("name,j", [("gate", 4), ("down", 6)])
+def test_train_at_bench_size(orc, spl, name, j):
+    """The bench's training configuration (M = 2048 tokens, 70%): the weight
+    gradient at 3000 sampled kept positions (each sum over the 2048 tokens
+    in binary64) and the input gradient on 64 sampled rows, through the packed
+    transpose refreshed by the permutation."""
+    import torch
+
+    _, N, K = synth.LLAMA2_7B_LINEARS[j]
+    M = 2048
+    W, mask = synth.weight(synth.weight_seed(0, j), N, K, "bf16", 0.7)
+    X = synth.activations(synth.activation_seed(j), M, K, "bf16")
+    dY = synth.activations(700 + j, M, N, "bf16")
+    md = torch.from_numpy(mask).cuda()
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), md)
+    g = spl.sparse_weight_grad(to_dev(dY, "bf16"), to_dev(X, "bf16"), Wc)
+    G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
+    rng = np.random.default_rng(j)
+    kept = np.argwhere(mask == 1)
+    pick = kept[rng.choice(len(kept), 3000, replace=False)]
+    x64, dy64 = orc.to_f64(X, "bf16"), orc.to_f64(dY, "bf16")
+    ref = np.einsum("mi,mi->i", dy64[:, pick[:, 0]], x64[:, pick[:, 1]])
+    assert_close(G[pick[:, 0], pick[:, 1]], ref, f"{name} weight grad M={M}")
+    assert not G[mask == 0].any()
+    Wt = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), md.t().contiguous())
+    perm = spl.transpose_perm(Wc, Wt)
+    spl.permute_values(Wc.values, perm, Wc.nnz, Wt.values)
+    dX = from_dev_f64(spl.sparse_linear(to_dev(dY, "bf16"), Wt))
+    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(np.arange(1, M - 1), 62, replace=False)]))
+    ref_dx = orc.input_grad_f64(dY[rows], "bf16", orc.pack(W, "bf16", mask))
+    assert_close(dX[rows], ref_dx, f"{name} input grad M={M}")
