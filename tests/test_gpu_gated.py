@@ -80,18 +80,20 @@ def test_gated_aligned_grids(orc, spl, N, K, M):
 
 @pytest.mark.parametrize("s", [0.7, 0.5])
 def test_gated_llama_gate_up(orc, spl, s):
-    """Llama-2-7B gate/up (11008 x 4096): in full at batches 1 and 16 (paired
-    decode kernel), on sampled outputs at M = 512 (prefill tiling)."""
+    """Llama-2-7B gate/up (11008 x 4096), the benchmark's batches: in full at
+    1, 4 and 16 (paired decode kernel), on sampled outputs at 512 and 2048
+    (prefill tiling)."""
     N, K = 11008, 4096
     (g, u), (pg, pu) = _pair(spl, orc, synth.weight_seed(0, 4), N, K, "bf16", s, s)
-    X = synth.activations(synth.activation_seed(4), 512, K, "bf16")
+    X = synth.activations(synth.activation_seed(4), 2048, K, "bf16")
     Xd = to_dev(X, "bf16")
-    for M in (1, 16):
+    for M in (1, 4, 16):
         Y = spl.sparse_linear_silu_mul(Xd[:M].contiguous(), g, u)
         assert_close(from_dev_f64(Y), orc.silu_mul_f64(X[:M], pg, pu), f"gate/up M={M} s={s}")
     rng = np.random.default_rng(54)
-    ms = np.concatenate([[0, 511, 255, 0], rng.integers(0, 512, 3000)])
-    ns = np.concatenate([[0, N - 1, 5000, 16], rng.integers(0, N, 3000)])
-    Y = from_dev_f64(spl.sparse_linear_silu_mul(Xd, g, u))
-    assert_close(Y[ms, ns], orc.silu_mul_f64_pairs(X, pg, pu, ms, ns), f"gate/up M=512 s={s}")
-    assert np.isfinite(Y).all()
+    for M in (512, 2048):
+        ms = np.concatenate([[0, M - 1, M // 2, 0], rng.integers(0, M, 3000)])
+        ns = np.concatenate([[0, N - 1, 5000, 16], rng.integers(0, N, 3000)])
+        Y = from_dev_f64(spl.sparse_linear_silu_mul(Xd[:M].contiguous(), g, u))
+        assert_close(Y[ms, ns], orc.silu_mul_f64_pairs(X[:M], pg, pu, ms, ns), f"gate/up M={M} s={s}")
+        assert np.isfinite(Y).all()
