@@ -277,7 +277,7 @@ def test_dense_int8_prefill(orc, spl):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
-@pytest.mark.parametrize("M,K", [(1, 8), (3, 520), (5, 6000), (3, 20000), (300, 4096), (17, 11008)])
+@pytest.mark.parametrize("M,K", [(1, 8), (3, 520), (5, 6000), (3, 20000), (300, 4096), (17, 11008), (2048, 11008)])
 def test_quantize_rows_matches_oracle(orc, spl, dtype, M, K):
     """Per-token activation quantisation on the GPU: codes and scales bit for
     bit equal to the oracle's, with a zero row, rows of exact ties and rows of
