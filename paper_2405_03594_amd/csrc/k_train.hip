@@ -144,7 +144,7 @@ hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const sp
   hipError_t e = launch_transpose16(dY, M, N, dYt, s);
   if (e == hipSuccess) e = launch_transpose16(X, M, K, Xt, s);
   if (e == hipSuccess) e = launch_dense_prefill(dYt, N, Xt, Wc.dtype, K, M, G, s);   // G = dYt Xt^T
-  if (e == hipSuccess && Wc.nnz > 0) e = launch_gather_tiled(G, Wc, grad_values, s);
+  if (e == hipSuccess) e = launch_gather_tiled(G, Wc, grad_values, s);   // nnz > 0 (checked by the caller)
   return e;
 }
 

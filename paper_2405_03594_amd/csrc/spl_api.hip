@@ -262,6 +262,7 @@ spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, cons
   if (!dY || !X || !workspace || !dims_ok(M, Wc->rows) || !dims_ok(M, Wc->cols)) return SPL_ERR_INVALID_ARG;
   if (!aligned(dY, 2) || !aligned(X, 2) || !aligned(workspace, 256)) return SPL_ERR_INVALID_ARG;
   if (M % 8 != 0 || Wc->cols % 8 != 0 || (M + 63) / 64 > 65535) return SPL_ERR_UNSUPPORTED;
+  if (Wc->nnz == 0) return SPL_OK;                   // no kept entry: no gradient to write
   (void)hipGetLastError();
   return launched(spl::launch_weight_grad(dY, X, M, *Wc, grad_values, workspace, stream));
 }
