@@ -338,6 +338,31 @@ def mask_of(p: Packed) -> np.ndarray:
     bits = (bm[:, :, None] >> np.arange(32, dtype=np.uint32)[None, None, :]) & 1
     return bits.reshape(p.N, words * 32)[:, :p.K].astype(np.float64)
 
+def pack_i4(codes: np.ndarray) -> np.ndarray:
+    """4-bit payload storage (section 4 names lower-bit payloads as future
+    work; the reading taken): value i of a matrix's value array - an int8 code
+    in [-8, 7] - is the two's-complement nibble at byte i // 2, the low nibble
+    for even i.  An odd count leaves the last high nibble 0.  The value order
+    is that of the int8 tile layout, so the products and the epilogue are
+    those of the int8 path on the same integers (linear_i8)."""
+    c = np.ascontiguousarray(codes, dtype=np.int8).ravel()
+    assert c.size == 0 or (c.min() >= -8 and c.max() <= 7)
+    nib = (c.astype(np.int16) & 0xF).astype(np.uint8)
+    out = np.zeros((c.size + 1) // 2, dtype=np.uint8)
+    for i, v in enumerate(nib):                        # value by value, as defined
+        out[i // 2] |= v << (4 * (i % 2))
+    return out
+
+
+def unpack_i4(b: np.ndarray, count: int) -> np.ndarray:
+    """Inverse of pack_i4: the first `count` codes (int8, sign-extended nibbles)."""
+    b = np.ascontiguousarray(b, dtype=np.uint8)
+    out = np.empty(count, dtype=np.int8)
+    for i in range(count):
+        v = (int(b[i // 2]) >> (4 * (i % 2))) & 0xF
+        out[i] = v - 16 if v >= 8 else v
+    return out
+
 def f16_to_f64(bits: np.ndarray) -> np.ndarray:
     lib = _load()
     bits = np.ascontiguousarray(bits, dtype=np.uint16)

@@ -160,17 +160,18 @@ def activations(seed: int, M: int, K: int, dtype: str) -> np.ndarray:
     return round_to(normal_f32(seed, (M, K), 1.0), dtype)
 
 
-def quantize_rows_int8(v: np.ndarray, keep: np.ndarray | None = None) -> tuple[np.ndarray, np.ndarray]:
-    """Symmetric per-row int8 codes of a binary32 matrix (only `keep` entries
-    count and are coded; the rest become 0).  Returns (codes int8, scales f32)."""
+def quantize_rows_int8(v: np.ndarray, keep: np.ndarray | None = None, qmax: int = 127) -> tuple[np.ndarray, np.ndarray]:
+    """Symmetric per-row integer codes in [-qmax, qmax] of a binary32 matrix
+    (only `keep` entries count and are coded; the rest become 0): 127 for
+    int8, 7 for int4.  Returns (codes int8, scales f32)."""
     v = np.ascontiguousarray(v, dtype=np.float32)
     if keep is not None:
         v = np.where(keep.astype(bool), v, np.float32(0))
     amax = np.max(np.abs(v), axis=1)
-    scale = (amax / np.float32(127.0)).astype(np.float32)
+    scale = (amax / np.float32(qmax)).astype(np.float32)
     scale = np.where(amax == 0, np.float32(1.0), scale).astype(np.float32)
     q = np.rint((v / scale[:, None]).astype(np.float32))
-    q = np.clip(q, -127, 127).astype(np.int8)
+    q = np.clip(q, -qmax, qmax).astype(np.int8)
     return q, scale
 
 
@@ -178,6 +179,14 @@ def int8_weight(seed: int, N: int, K: int, sparsity) -> tuple[np.ndarray, np.nda
     """(Wq int8 [N][K] (0 outside the mask), keep-mask, sw f32 [N]) from the bf16 pruned weight."""
     w, mask = weight(seed, N, K, "bf16", sparsity)
     q, sw = quantize_rows_int8(bits_to_f32(w, "bf16"), mask)
+    return q, mask, sw
+
+
+def int4_weight(seed: int, N: int, K: int, sparsity) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """(Wq int8 codes in [-7, 7] [N][K] (0 outside the mask), keep-mask, sw f32 [N]):
+    4-bit per-row symmetric codes of the bf16 pruned weight, held in int8."""
+    w, mask = weight(seed, N, K, "bf16", sparsity)
+    q, sw = quantize_rows_int8(bits_to_f32(w, "bf16"), mask, qmax=7)
     return q, mask, sw
 
 

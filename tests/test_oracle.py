@@ -654,3 +654,24 @@ def test_mask_of_and_sgd(orc):
     assert np.array_equal(orc.mask_of(orc.pack(W, "bf16", mask)), mask.astype(np.float64))
     w = np.array([1.0, -2.0, 0.5]); g = np.array([4.0, 0.25, -1.0])
     assert orc.sgd_f64(w, g, 0.5).tolist() == [-1.0, -2.125, 1.0]
+
+
+def test_pack_i4_worked_and_round_trip(orc):
+    """Hand-derived bytes (low nibble first, two's complement), an odd count,
+    and unpack(pack(c)) == c over every code in [-8, 7] in both positions."""
+    assert orc.pack_i4(np.array([1, -1, 7, -8, 3], np.int8)).tolist() == [0xF1, 0x87, 0x03]
+    assert orc.pack_i4(np.array([], np.int8)).size == 0
+    codes = np.array([a for a in range(-8, 8) for _ in range(2)] + list(range(7, -9, -1)), np.int8)
+    assert np.array_equal(orc.unpack_i4(orc.pack_i4(codes), codes.size), codes)
+
+
+def test_int4_generator_codes(orc):
+    """The generator's 4-bit codes: within [-7, 7], zero off the mask, each
+    row's largest kept magnitude coded +-7, scale = absmax / 7."""
+    Wq, mask, sw = synth.int4_weight(5, 40, 96, 0.7)
+    assert Wq.min() >= -7 and Wq.max() <= 7 and not Wq[mask == 0].any()
+    w, _ = synth.weight(5, 40, 96, "bf16", 0.7)
+    v = synth.bits_to_f32(w, "bf16") * mask
+    amax = np.abs(v).max(axis=1)
+    assert np.allclose(sw, np.where(amax == 0, 1, amax / 7), rtol=1e-6)
+    assert (np.abs(Wq).max(axis=1)[amax > 0] == 7).all()
