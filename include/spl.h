@@ -79,7 +79,8 @@ typedef enum {
   SPL_ERR_DEVICE = 4         /* the HIP runtime reported an error */
 } spl_status;
 
-typedef enum { SPL_F16 = 1, SPL_BF16 = 2, SPL_I8 = 3 } spl_dtype;
+/* SPL_I4: 4-bit codes stored two per byte (spl_sparse_linear_int4 only). */
+typedef enum { SPL_F16 = 1, SPL_BF16 = 2, SPL_I8 = 3, SPL_I4 = 4 } spl_dtype;
 
 /* Kernel family for spl_sparse_linear_ex / spl_dense_linear_ex.
  * AUTO picks by batch size M.  DECODE is the small-batch kernel (M <= 32):
@@ -246,6 +247,22 @@ spl_status spl_sparse_linear_silu_mul(const void* X, int64_t M, const spl_matrix
  *   acc_out   optional out [M][N] int32 (NULL to skip).
  *   Requires K % 16 == 0. */
 spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
+                                  const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream);
+
+/* 4-bit sparse payloads (paper section 4 names INT4 as future work; the
+ * reading taken: the int8 tile layout's pattern and value order, value i the
+ * two's-complement nibble at byte i / 2, low nibble first, codes in [-8, 7]).
+ * spl_pack_int4: values4 out (spl_int4_values_bytes(nnz) bytes, 16-byte
+ *   aligned; the tail past ceil(nnz/2) is not written) from an int8
+ *   tile-layout view W8 whose codes lie in [-8, 7] (other codes keep their
+ *   low 4 bits).  The view of the result is W8's with dtype SPL_I4 and
+ *   values = values4.
+ * spl_sparse_linear_int4: as spl_sparse_linear_int8 (exact int32 sums, the
+ *   same fp16 epilogue) for a SPL_I4 tile-layout view, decode batches
+ *   0 <= M <= 16 (SPL_ERR_UNSUPPORTED above), K % 16 == 0. */
+int64_t spl_int4_values_bytes(int64_t nnz);
+spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, hipStream_t stream);
+spl_status spl_sparse_linear_int4(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* W4,
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream);
 
 /* Per-token activation quantisation for the sparse-quantized layer (paper

@@ -30,8 +30,9 @@ F16, BF16, I8 = 1, 2, 3
 LAYOUT = {"rows": 0, "tile16": 1}
 ALGO = {"auto": 0, "decode": 1, "prefill": 2}
 _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "overflow", 4: "HIP runtime error"}
-_TORCH_DTYPE = {torch.float16: F16, torch.bfloat16: BF16, torch.int8: I8}
-_CODE_DTYPE = {F16: torch.float16, BF16: torch.bfloat16, I8: torch.int8}
+I4 = 4                                  # 4-bit codes, two per byte (values held as uint8)
+_TORCH_DTYPE = {torch.float16: F16, torch.bfloat16: BF16, torch.int8: I8, torch.uint8: I4}
+_CODE_DTYPE = {F16: torch.float16, BF16: torch.bfloat16, I8: torch.int8, I4: torch.uint8}
 
 
 class SplError(RuntimeError):
@@ -105,6 +106,9 @@ def lib() -> ctypes.CDLL:
         "spl_magnitude_mask_workspace_bytes": (I64, []),
         "spl_magnitude_mask": (ctypes.c_int, [P, I32, I64, I64, I64, P, P, P]),
         "spl_transpose16": (ctypes.c_int, [P, I64, I64, P, P]),
+        "spl_int4_values_bytes": (I64, [I64]),
+        "spl_pack_int4": (ctypes.c_int, [MP, P, P]),
+        "spl_sparse_linear_int4": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
         "spl_gather_tiled": (ctypes.c_int, [P, MP, P, P]),
         "spl_sparse_weight_grad_workspace_bytes": (I64, [I64, I64, I64]),
         "spl_sparse_weight_grad": (ctypes.c_int, [P, P, I64, MP, P, P, P]),
@@ -178,7 +182,8 @@ class SparseMatrix:
     def compressed_bytes(self) -> int:
         """Bytes of the encoding: payloads + bitmask + offsets."""
         offs = self.row_offsets if self.layout == "rows" else self.tile_offsets
-        return self.nnz * self.values.element_size() + self.bitmask.numel() * 4 + offs.numel() * 4
+        payload = (self.nnz + 1) // 2 if self.values.dtype == torch.uint8 else self.nnz * self.values.element_size()
+        return payload + self.bitmask.numel() * 4 + offs.numel() * 4
 
 
 def _values_buffer(nnz: int, dtype: torch.dtype, device) -> torch.Tensor:
@@ -362,6 +367,35 @@ def permute_values(src: torch.Tensor, perm: torch.Tensor, nnz: int, out: torch.T
     """out[i] = src[perm[i]] for i < nnz (see spl_permute_values)."""
     L = lib()
     _check("spl_permute_values", L.spl_permute_values(_ptr(src), _ptr(perm), int(nnz), _ptr(out), _stream(stream)))
+    return out
+
+
+def pack_int4(W8: SparseMatrix, stream=None) -> SparseMatrix:
+    """The 4-bit form of an int8 tile-layout matrix whose codes lie in [-8, 7]
+    (see spl_pack_int4): same pattern, values as uint8 bytes of two nibbles."""
+    L = lib()
+    if W8.dtype != torch.int8 or W8.layout != "tile16":
+        raise ValueError("pack_int4 takes an int8 matrix in the tile layout")
+    v4 = torch.zeros((L.spl_int4_values_bytes(W8.nnz),), dtype=torch.uint8, device=W8.values.device)
+    view = W8.view()
+    _check("spl_pack_int4", L.spl_pack_int4(ctypes.byref(view), _ptr(v4), _stream(stream)))
+    return SparseMatrix(W8.bitmask, v4, None, W8.tile_offsets, W8.rows, W8.cols, W8.nnz, "tile16")
+
+
+def sparse_linear_int4(Xq: torch.Tensor, x_scales: torch.Tensor, W4: SparseMatrix, w_scales: torch.Tensor,
+                       out: torch.Tensor | None = None, acc_out: torch.Tensor | None = None,
+                       stream=None) -> torch.Tensor:
+    """fp16 Y from 4-bit sparse weights and int8 activations, M <= 16 (see spl_sparse_linear_int4)."""
+    L = lib()
+    for t, nm in ((Xq, "Xq"), (x_scales, "x_scales"), (w_scales, "w_scales")):
+        _dev_tensor(t, nm)
+    M = Xq.shape[0]
+    if out is None:
+        out = torch.empty((M, W4.rows), dtype=torch.float16, device=Xq.device)
+    view = W4.view()
+    _check("spl_sparse_linear_int4", L.spl_sparse_linear_int4(_ptr(Xq), _ptr(x_scales), M, ctypes.byref(view),
+                                                              _ptr(w_scales), _ptr(out), _ptr(acc_out),
+                                                              _stream(stream)))
     return out
 
 

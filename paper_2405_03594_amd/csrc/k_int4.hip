@@ -1,0 +1,139 @@
+// 4-bit sparse payloads (paper section 4 lists INT4 among the next steps) for
+// the sparse-quantized linear layer at decode batches (M <= 16).
+//
+// Storage: the pattern of the int8 tile layout (bitmask words, tile offsets;
+// values ordered by 16-column group, then row, then column) with value i held
+// as the two's-complement nibble at byte i / 2, low nibble first.  The codes
+// are the int8 path's integers restricted to [-8, 7], so the products (exact
+// int32 sums on v_mfma_i32_16x16x64_i8) and the epilogue are those of the
+// int8 path:  Y[m][n] = fp16_rne((float(acc) * sx[m]) * sw[n]).
+//
+// Kernel: one workgroup per 16-row block, its 8 waves over contiguous ranges
+// of tile pairs (one MFMA each: lanes 0-31 tile 2p, lanes 32-63 tile 2p + 1,
+// lane (fr, fg) row fr, columns 16 (fg % 2) .. + 16 of its tile).  A lane's
+// first value is nibble toff[t] + the exclusive scan of its tile half's kept
+// counts; its (at most 16) nibbles are read as three aligned dwords, shifted
+// into place with v_alignbit_b32, and placed one by one (sign-extended) into
+// the 16-byte MFMA operand, zeros where the bitmask is clear.  Activation rows
+// are read directly (16 bytes per lane), int32 partial sums added in LDS.
+#include "spl_common.h"
+
+namespace spl {
+namespace {
+
+constexpr int kI4Waves = 8;
+
+__device__ __forceinline__ i32x4 mfma_i8_i4(u32x4 a, u32x4 b, i32x4 c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0, 0,
+                                               0);
+}
+
+__global__ void __launch_bounds__(256) k_pack_nibbles(const int8_t* __restrict__ v8, int64_t nnz,
+                                                      uint8_t* __restrict__ v4) {
+  const int64_t nb = (nnz + 1) / 2;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nb; i += (int64_t)gridDim.x * 256) {
+    const uint32_t lo = (uint32_t)(uint8_t)v8[2 * i] & 0xFu;
+    const uint32_t hi = 2 * i + 1 < nnz ? ((uint32_t)(uint8_t)v8[2 * i + 1] & 0xFu) : 0u;
+    v4[i] = (uint8_t)(lo | (hi << 4));
+  }
+}
+
+struct I4Args {
+  const int8_t* Xq;          // [M][K]
+  const float* sx;           // [M]
+  const uint32_t* bm;        // [B*S][16]
+  const uint8_t* v4;         // nibbles (followed by 16 readable bytes)
+  const int32_t* toff;       // [B*S + 1]
+  const float* sw;           // [N]
+  uint16_t* Y;               // [M][N] fp16
+  int32_t* acc_out;          // optional [M][N]
+  int64_t N, K;
+  int32_t M;
+};
+
+__global__ void __launch_bounds__(kI4Waves * 64) k_sparse_i4(const I4Args g) {
+  __shared__ i32x4 part[kI4Waves][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const int64_t b = blockIdx.x;
+  const int S = (int)tile_steps(g.K);
+  const int P = (S + 1) / 2;                         // tile pairs (64 columns each)
+  const int L = (P + kI4Waves - 1) / kI4Waves;
+  const int pb = wave * L < P ? wave * L : P;
+  const int pe = pb + L < P ? pb + L : P;
+  const bool xlive = fr < g.M;
+  const int8_t* xrow = g.Xq + (int64_t)(xlive ? fr : 0) * g.K;
+  i32x4 acc = i32x4{0, 0, 0, 0};
+  for (int p = pb; p < pe; ++p) {
+    const int s = 2 * p + (fg >> 1), h = fg & 1;
+    uint32_t hw = 0u, base = 0u;
+    if (s < S) {
+      const int64_t t = b * S + s;
+      hw = (g.bm[t * 16 + fr] >> (16 * h)) & 0xffffu;
+      base = (uint32_t)g.toff[t];
+    }
+    const uint32_t cnt = __popc(hw);
+    const uint32_t off = base + half_inclusive_scan(cnt) - cnt;   // nibble index of my first value
+    u32x4 a = u32x4{0u, 0u, 0u, 0u};
+    if (hw != 0u) {                                  // off + cnt <= nnz: bytes read < nnz / 2 + 12
+      const uint32_t byte0 = off >> 1;
+      const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));
+      const uint32_t d0 = d[0], d1 = d[1], d2 = d[2];
+      const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;   // 0 .. 28
+      const uint32_t lo = __builtin_amdgcn_alignbit(d1, d0, sh);    // nibbles off .. off + 7
+      const uint32_t hi = __builtin_amdgcn_alignbit(d2, d1, sh);    // nibbles off + 8 .. off + 15
+      uint32_t r = 0u;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if ((hw >> j) & 1u) {
+          const uint32_t nib = ((r < 8u ? lo >> (4u * r) : hi >> (4u * (r - 8u)))) & 0xFu;
+          const uint32_t byte = (nib ^ 8u) - 8u;     // sign-extended, low byte used
+          a[j >> 2] |= (byte & 0xFFu) << (8 * (j & 3));
+          ++r;
+        }
+      }
+    }
+    u32x4 xb = u32x4{0u, 0u, 0u, 0u};
+    const int64_t k0 = 64 * (int64_t)p + 16 * fg;
+    if (xlive && k0 < g.K) xb = *reinterpret_cast<const u32x4*>(xrow + k0);   // K % 16 == 0
+    acc = mfma_i8_i4(a, xb, acc);
+  }
+  part[wave][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+  i32x4 sum = part[0][lane];
+#pragma unroll
+  for (int w = 1; w < kI4Waves; ++w) sum += part[w][lane];
+  const int m = lane & 15;
+  if (m >= g.M) return;
+  const float xs = g.sx[m];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t n = b * 16 + 4 * (lane >> 4) + r;
+    if (n >= g.N) continue;
+    const int32_t v = sum[r];
+    if (g.acc_out) g.acc_out[(int64_t)m * g.N + n] = v;
+    g.Y[(int64_t)m * g.N + n] = F16::from_f32(__fmul_rn(__fmul_rn((float)v, xs), g.sw[n]));
+  }
+}
+
+}  // namespace
+
+int64_t int4_values_bytes(int64_t nnz) { return ((nnz + 1) / 2 + 16 + 15) / 16 * 16; }
+
+hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, hipStream_t s) {
+  int64_t blocks = ((nnz + 1) / 2 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_pack_nibbles, dim3((unsigned)blocks), dim3(256), 0, s, v8, nnz, v4);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& W4, const float* sw,
+                              void* Y, int32_t* acc_out, hipStream_t s) {
+  I4Args g{Xq, sx, W4.bitmask, static_cast<const uint8_t*>(W4.values), W4.tile_offsets, sw,
+           static_cast<uint16_t*>(Y), acc_out, W4.rows, W4.cols, (int32_t)M};
+  hipLaunchKernelGGL(k_sparse_i4, dim3((unsigned)tile_blocks(W4.rows)), dim3(kI4Waves * 64), 0, s, g);
+  return hipGetLastError();
+}
+
+}  // namespace spl

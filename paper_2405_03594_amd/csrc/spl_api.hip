@@ -304,7 +304,43 @@ spl_status spl_permute_values(const void* src, const int32_t* perm, int64_t nnz,
   return launched(spl::launch_permute_values(src, perm, nnz, dst, stream));
 }
 
-// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+int64_t spl_int4_values_bytes(int64_t nnz) { return nnz < 0 ? -1 : spl::int4_values_bytes(nnz); }
+
+spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, hipStream_t stream) {
+  const spl_status st = spl_check_matrix(W8);
+  if (st != SPL_OK) return st;
+  if (W8->dtype != SPL_I8 || W8->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
+  if (!values4 || !aligned(values4, 16)) return SPL_ERR_INVALID_ARG;
+  if (W8->nnz == 0) return SPL_OK;
+  (void)hipGetLastError();
+  return launched(spl::launch_pack_nibbles(static_cast<const int8_t*>(W8->values), W8->nnz, values4, stream));
+}
+
+// A SPL_I4 view: the checks of spl_check_matrix with the 4-bit dtype and the tile layout.
+static spl_status check_i4_view(const spl_matrix* W) {
+  if (!W) return SPL_ERR_INVALID_ARG;
+  if (W->dtype != SPL_I4 || W->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
+  spl_matrix v = *W;
+  v.dtype = SPL_I8;                                   // same scalar and pointer rules
+  return spl_check_matrix(&v);
+}
+
+spl_status spl_sparse_linear_int4(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* W4,
+                                  const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream) {
+  const spl_status st = check_i4_view(W4);
+  if (st != SPL_OK) return st;
+  if (M < 0) return SPL_ERR_INVALID_ARG;
+  if (M > 16) return SPL_ERR_UNSUPPORTED;
+  const spl_status xy = check_xy(Xq, M, W4->cols, W4->rows, Y);
+  if (xy != SPL_OK || M == 0) return xy;
+  if (!x_scales || !w_scales || !aligned(x_scales, 4) || !aligned(w_scales, 4)) return SPL_ERR_INVALID_ARG;
+  if (acc_out && !aligned(acc_out, 16)) return SPL_ERR_INVALID_ARG;
+  if (W4->cols % 16 != 0) return SPL_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return launched(spl::launch_sparse_int4(Xq, x_scales, M, *W4, w_scales, Y, acc_out, stream));
+}
+
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
 static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
   const spl_status st = spl_check_matrix(t->Wq);
   if (st != SPL_OK) return st;

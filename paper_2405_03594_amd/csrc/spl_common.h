@@ -161,6 +161,11 @@ hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, h
 int64_t transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz);
 hipError_t launch_transpose_perm(const spl_matrix& W, const spl_matrix& Wt, int32_t* perm, void* ws, hipStream_t s);
 hipError_t launch_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t s);
+// 4-bit payloads: nibble packing of int8 tile values and the decode kernel (M <= 16).
+int64_t int4_values_bytes(int64_t nnz);
+hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, hipStream_t s);
+hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& W4, const float* sw,
+                              void* Y, int32_t* acc_out, hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

@@ -337,3 +337,23 @@ def test_transpose_perm_argument_checks(L):
     assert p(0x40000, P, -1, 0x70000, None) == INVALID
     assert p(None, P, 5, 0x70000, None) == INVALID
     assert p(0x40000, P + 2, 5, 0x70000, None) == INVALID                    # misaligned perm
+
+
+def test_int4_argument_checks(L):
+    """Checks that return before any HIP call (no device needed)."""
+    w8 = _mat(dtype=3, layout=1, tile_offsets=0x40000)
+    w4 = _mat(dtype=4, layout=1, tile_offsets=0x40000)
+    X, s, Y = 0x40000, 0x50000, 0x60000
+    assert L.spl_int4_values_bytes(5) >= 3 + 16
+    assert L.spl_check_matrix(ctypes.byref(w4)) == INVALID                # only the int4 entry takes SPL_I4
+    p = L.spl_pack_int4
+    assert p(ctypes.byref(w4), 0x70000, None) == INVALID                  # the source must be an int8 view
+    assert p(ctypes.byref(_mat(layout=1, tile_offsets=0x40000)), 0x70000, None) == UNSUPPORTED   # bf16
+    assert p(ctypes.byref(w8), 0x70008, None) == INVALID                  # misaligned output
+    f = L.spl_sparse_linear_int4
+    assert f(X, s, 0, ctypes.byref(w4), s, Y, None, None) == OK           # M = 0
+    assert f(X, s, 17, ctypes.byref(w4), s, Y, None, None) == UNSUPPORTED # decode batches only
+    assert f(X, s, 2, ctypes.byref(w8), s, Y, None, None) == UNSUPPORTED  # an int8 view
+    assert f(X, None, 2, ctypes.byref(w4), s, Y, None, None) == INVALID
+    assert f(X, s, 2, ctypes.byref(_mat(dtype=4, cols=40, layout=1, tile_offsets=0x40000)), s, Y, None,
+             None) == UNSUPPORTED                                          # K % 16 != 0

@@ -1,0 +1,87 @@
+"""CPU replay of the 4-bit decode kernel's schedule (k_int4.hip): for every
+workgroup, wave, tile pair and lane, the nibble offset from the tile offset
+and the half-wave scan, the three dwords it reads (inside the values buffer
+of spl_int4_values_bytes(nnz) bytes, which the kernel is never allowed to
+leave), and the 16 sign-extended bytes it builds, which must equal the dense
+codes of its row and 16 columns (zeros where pruned).  The packed values come
+from the oracle's tile encoder and 4-bit packer, so this also checks that the
+kernel reads the layout the oracle defines."""
+import os
+
+import numpy as np
+import pytest
+
+import synth
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                   "paper_2405_03594_amd", "csrc", "k_int4.hip")
+
+
+def _values_bytes(nnz):
+    return ((nnz + 1) // 2 + 16 + 15) // 16 * 16
+
+
+@pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (17, 48, 0.7), (40, 96, 0.0), (33, 208, 0.9), (16, 64, 1.0)])
+def test_int4_schedule_reads_and_operands(orc, N, K, s):
+    src = open(SRC).read()
+    for line in ("const int s = 2 * p + (fg >> 1), h = fg & 1;",
+                 "hw = (g.bm[t * 16 + fr] >> (16 * h)) & 0xffffu;",
+                 "const uint32_t off = base + half_inclusive_scan(cnt) - cnt;",
+                 "const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));",
+                 "const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;",
+                 "int64_t int4_values_bytes(int64_t nnz) { return ((nnz + 1) / 2 + 16 + 15) / 16 * 16; }"):
+        assert line in src, f"kernel changed: update this replay ({line})"
+    Wq, mask, _ = synth.int4_weight(300 + N + K, N, K, s)
+    T = orc.pack_tiled(Wq, "i8", mask)
+    nnz = int(T.tile_offsets[-1])
+    packed = np.zeros(_values_bytes(nnz), dtype=np.uint8)
+    packed[:(nnz + 1) // 2] = orc.pack_i4(T.values)
+    words = packed.view(np.uint32)
+    B, S = (N + 15) // 16, (K + 31) // 32
+    P = (S + 1) // 2
+    waves = 8
+    dense = np.where(mask.astype(bool), Wq, np.int8(0))
+    for b in range(B):
+        L = (P + waves - 1) // waves
+        for w in range(waves):
+            pb = min(w * L, P)
+            pe = min(pb + L, P)
+            for p in range(pb, pe):
+                hw = np.zeros(64, np.int64)
+                base = np.zeros(64, np.int64)
+                for lane in range(64):
+                    fr, fg = lane & 15, lane >> 4
+                    sk, h = 2 * p + (fg >> 1), fg & 1
+                    if sk < S:
+                        t = b * S + sk
+                        hw[lane] = (int(T.bitmask[t * 16 + fr]) >> (16 * h)) & 0xFFFF
+                        base[lane] = int(T.tile_offsets[t])
+                cnt = np.array([bin(int(x)).count("1") for x in hw])
+                for half in range(2):
+                    seg = slice(32 * half, 32 * half + 32)
+                    excl = np.cumsum(cnt[seg]) - cnt[seg]
+                    for i, lane in enumerate(range(32 * half, 32 * half + 32)):
+                        if hw[lane] == 0:
+                            continue
+                        off = int(base[lane] + excl[i])
+                        assert off + cnt[lane] <= nnz
+                        byte0 = off >> 1
+                        first = (byte0 & ~3) // 4
+                        assert 0 <= first and (first + 3) * 4 <= packed.size, (b, w, p, lane)
+                        d0, d1, d2 = (int(x) for x in words[first:first + 3])
+                        sh = (byte0 & 3) * 8 + (off & 1) * 4
+                        lo = ((d1 << 32 | d0) >> sh) & 0xFFFFFFFF
+                        hi = ((d2 << 32 | d1) >> sh) & 0xFFFFFFFF
+                        got, r = [], 0
+                        for j in range(16):
+                            if (int(hw[lane]) >> j) & 1:
+                                nib = ((lo >> (4 * r)) if r < 8 else (hi >> (4 * (r - 8)))) & 0xF
+                                got.append(nib - 16 if nib >= 8 else nib)
+                                r += 1
+                            else:
+                                got.append(0)
+                        fr, fg = lane & 15, lane >> 4
+                        n = 16 * b + fr
+                        k0 = 64 * p + 16 * fg
+                        want = [int(dense[n, k0 + j]) if n < N and k0 + j < K else 0 for j in range(16)]
+                        assert got == want, (b, w, p, lane)
