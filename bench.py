@@ -783,6 +783,94 @@ def run_train(args):
                  cpu, {"parts_per_layer": parts, "sparsity": args.sparsity, "lr": lr})
 
 
+def _gen_int4(args):
+    layer, j, N, K = args
+    Wq, mask, sw = synth.int4_weight(synth.weight_seed(layer, j), N, K, 0.7)
+    return layer, j, Wq, mask, sw
+
+
+def run_int4(args):
+    """One layer's seven matrices with 4-bit weights (per-row scales) at 70%,
+    int8 activations, batches 1 and 16, one launch per matrix, 4 layers
+    rotated; the same codes run through the int8 path alongside."""
+    torch, spl = _need_gpu()
+    nl = 4
+    shapes = synth.LLAMA2_7B_LINEARS
+    jobs = [(l, j, N, K) for l in range(nl) for j, (_, N, K) in enumerate(shapes)]
+    host = [[None] * len(shapes) for _ in range(nl)]
+    with cf.ProcessPoolExecutor(max_workers=args.workers) as ex:
+        for l, j, Wq, mask, sw in ex.map(_gen_int4, jobs):
+            host[l][j] = (Wq, mask, sw)
+    layers = []
+    for hl in host:
+        row = []
+        for Wq, mask, sw in hl:
+            W8 = spl.pack_sparse(torch.from_numpy(Wq).cuda(), torch.from_numpy(mask).cuda())
+            row.append((spl.pack_int4(W8), W8, torch.from_numpy(sw).cuda()))
+        layers.append(row)
+    Ms = [1, 16]
+    xq, sx = [], []
+    for j, (_, N, K) in enumerate(shapes):
+        q, s_ = synth.int8_activations(synth.activation_seed(j), max(Ms), K)
+        xq.append(torch.from_numpy(q).cuda())
+        sx.append(torch.from_numpy(s_).cuda())
+    xs = {(M, j): (xq[j][:M].contiguous(), sx[j][:M].contiguous()) for M in Ms for j in range(len(shapes))}
+    ys = {(M, j): torch.empty((M, N), dtype=torch.float16, device="cuda") for M in Ms for j, (_, N, _) in
+          enumerate(shapes)}
+    units = [(M, j) for M in Ms for j in range(len(shapes))]
+
+    def i4_fn(li, u):
+        M, j = u
+        spl.sparse_linear_int4(xs[u][0], xs[u][1], layers[li][j][0], layers[li][j][2], out=ys[u])
+
+    def i8_fn(li, u):
+        M, j = u
+        spl.sparse_linear_int8(xs[u][0], xs[u][1], layers[li][j][1], layers[li][j][2], out=ys[u])
+
+    wall, gpu = _timed(units, i4_fn, args.steps, args.warmup, range(nl))
+
+    def nbytes(M, j):
+        N, K = shapes[j][1], shapes[j][2]
+        return layers[0][j][0].compressed_bytes() + 4 * N + M * K + 4 * M + 2 * M * N
+
+    launch_ms = gpu / len(units)
+    achieved = sum(nbytes(*u) for u in units) / len(units) / (launch_ms * 1e-3) / 1e9
+    per_M = {}
+    for M in Ms:
+        uM = [u for u in units if u[0] == M]
+        _, g4 = _timed(uM, i4_fn, max(20, args.steps // 4), 3, range(nl))
+        _, g8 = _timed(uM, i8_fn, max(20, args.steps // 4), 3, range(nl))
+        b = sum(nbytes(*u) for u in uM)
+        per_M[str(M)] = {"layer_us": round(g4 * 1e3, 2), "hbm_gbs": round(b / (g4 * 1e-3) / 1e9, 1),
+                         "int8_path_layer_us": round(g8 * 1e3, 2), "vs_int8_path": round(g8 / g4, 3)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        packs = [oracle.pack(host[0][j][0], "i8", host[0][j][1]) for j in range(len(shapes))]
+        xh = [synth.int8_activations(synth.activation_seed(j), max(Ms), K) for j, (_, N, K) in enumerate(shapes)]
+        threads = oracle.max_threads()
+
+        def one():
+            for M in Ms:
+                for j in range(len(shapes)):
+                    oracle.linear_i8(xh[j][0][:M], xh[j][1][:M], packs[j], host[0][j][2], nthreads=threads)
+
+        reps, dt = _oracle_repeat(one)
+        cpu = {"value": round(reps * sum(Ms) / dt, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+               "sample": f"layer 0's seven matrices' 4-bit codes at batches {Ms} (int64 sums, fp16 epilogue), "
+                         f"repeated {reps} times ({dt:.1f} s on {threads} threads)"}
+    return _line(args, "4-bit sparse linear tokens/s + achieved HBM GB/s, Llama-2-7B layer at 70%",
+                 round(sum(Ms) / (wall * 1e-3), 1), "tokens/s", wall,
+                 "Llama-2-7B decoder layer, 7 linears, 4-bit weights (per-row scales) and int8 activations "
+                 "(per-token scales), 70% sparsity, batches 1 and 16, one launch per matrix, 4 layers rotated",
+                 {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                  "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_i4",
+                  "bytes_per_launch": int(sum(nbytes(*u) for u in units) / len(units)),
+                  "avg_launch_us": round(launch_ms * 1e3, 3)},
+                 cpu, {"per_M": per_M}, dtype="i8")
+
+
 def run_stack(args):
     """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
     after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
@@ -855,14 +943,14 @@ def main():
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
     ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "gated", "prune",
-                                                   "train", "stack"],
+                                                   "train", "int4", "stack"],
                     default="decode",
                     help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
                          "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
                          "int8 weights and activations, batches 1,16,64; int8-prefill: one layer, int8 weights, "
                          "activations quantized per token, M=512 and 2048; gated: fused silu(gate)*up "
                          "of gate/up at batches 1,4,16; prune: magnitude masks of one layer; train: a masked training step of one "
-                         "layer at M=2048; stack: all 32 layers at "
+                         "layer at M=2048; int4: 4-bit weights at batches 1,16; stack: all 32 layers at "
                          "batches 1..32")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
@@ -886,7 +974,7 @@ def main():
 
     if args.workload != "decode":
         out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
-               "gated": run_gated, "prune": run_prune, "train": run_train,
+               "gated": run_gated, "prune": run_prune, "train": run_train, "int4": run_int4,
                "stack": run_stack}[args.workload](args)
         print(json.dumps(out), flush=True)
         return
