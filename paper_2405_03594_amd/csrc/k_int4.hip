@@ -13,8 +13,10 @@
 // lane (fr, fg) row fr, columns 16 (fg % 2) .. + 16 of its tile).  A lane's
 // first value is nibble toff[t] + the exclusive scan of its tile half's kept
 // counts; its (at most 16) nibbles are read as three aligned dwords, shifted
-// into place with v_alignbit_b32, and placed one by one (sign-extended) into
-// the 16-byte MFMA operand, zeros where the bitmask is clear.  Activation rows
+// into place with v_alignbit_b32; for each 4-column nibble of its mask the 4
+// nibbles from the nibble's first rank are widened to sign-extended bytes and
+// a 16-entry selector table (v_perm_b32) places them, zeros where the bitmask
+// is clear.  Activation rows
 // are read directly (16 bytes per lane), int32 partial sums added in LDS.
 #include "spl_common.h"
 
@@ -22,6 +24,22 @@ namespace spl {
 namespace {
 
 constexpr int kI4Waves = 8;
+
+// v_perm_b32 selector for one 4-column nibble: byte j takes byte
+// popcount(nib & ((1 << j) - 1)) of the source if bit j is set, else 12 (zero).
+__device__ __forceinline__ uint32_t i4_nibble_selector(uint32_t nib) {
+  uint32_t sel = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) sel |= (((nib >> j) & 1u) ? (uint32_t)__popc(nib & ((1u << j) - 1u)) : 0x0Cu) << (8 * j);
+  return sel;
+}
+
+// Four nibbles (bits 0-15) -> four sign-extended bytes.
+__device__ __forceinline__ uint32_t i4_widen(uint32_t w) {
+  uint32_t y = (w & 0xFu) | ((w & 0xF0u) << 4) | ((w & 0xF00u) << 8) | ((w & 0xF000u) << 12);
+  const uint32_t m = y & 0x08080808u;                // sign bits
+  return y | ((m << 5) - (m << 1));                  // 0xF0 into every byte whose sign bit is set (mod 2^32)
+}
 
 __device__ __forceinline__ i32x4 mfma_i8_i4(u32x4 a, u32x4 b, i32x4 c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a), __builtin_bit_cast(i32x4, b), c, 0, 0,
@@ -53,7 +71,10 @@ struct I4Args {
 
 __global__ void __launch_bounds__(kI4Waves * 64) k_sparse_i4(const I4Args g) {
   __shared__ i32x4 part[kI4Waves][64];
+  __shared__ uint32_t sel4[16];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  if (threadIdx.x < 16) sel4[threadIdx.x] = i4_nibble_selector(threadIdx.x);
+  __syncthreads();
   const int64_t b = blockIdx.x;
   const int S = (int)tile_steps(g.K);
   const int P = (S + 1) / 2;                         // tile pairs (64 columns each)
@@ -81,15 +102,14 @@ __global__ void __launch_bounds__(kI4Waves * 64) k_sparse_i4(const I4Args g) {
       const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;   // 0 .. 28
       const uint32_t lo = __builtin_amdgcn_alignbit(d1, d0, sh);    // nibbles off .. off + 7
       const uint32_t hi = __builtin_amdgcn_alignbit(d2, d1, sh);    // nibbles off + 8 .. off + 15
-      uint32_t r = 0u;
+      const uint64_t nibs = ((uint64_t)hi << 32) | lo;
+      uint32_t rank = 0u;                            // values before this 4-column nibble
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if ((hw >> j) & 1u) {
-          const uint32_t nib = ((r < 8u ? lo >> (4u * r) : hi >> (4u * (r - 8u)))) & 0xFu;
-          const uint32_t byte = (nib ^ 8u) - 8u;     // sign-extended, low byte used
-          a[j >> 2] |= (byte & 0xFFu) << (8 * (j & 3));
-          ++r;
-        }
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t m4 = (hw >> (4 * q)) & 0xFu;
+        const uint32_t y = i4_widen((uint32_t)(nibs >> (4u * rank)) & 0xFFFFu);   // ranks rank .. rank + 3
+        a[q] = __builtin_amdgcn_perm(0u, y, sel4[m4]);
+        rank += __popc(m4);
       }
     }
     u32x4 xb = u32x4{0u, 0u, 0u, 0u};

@@ -17,6 +17,27 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                    "paper_2405_03594_amd", "csrc", "k_int4.hip")
 
 
+def _widen(w):
+    """i4_widen: four nibbles -> four bytes, 0xF0 or'ed into those with bit 3 set (mod 2^32)."""
+    y = (w & 0xF) | ((w & 0xF0) << 4) | ((w & 0xF00) << 8) | ((w & 0xF000) << 12)
+    m = y & 0x08080808
+    return (y | (((m << 5) - (m << 1)) & 0xFFFFFFFF)) & 0xFFFFFFFF
+
+
+def _selector(nib):
+    """i4_nibble_selector: byte j <- rank of column j among the nibble's set bits, 12 (zero) if clear."""
+    return [bin(nib & ((1 << j) - 1)).count("1") if (nib >> j) & 1 else 12 for j in range(4)]
+
+
+def _perm0(y, sel):
+    """v_perm_b32(0, y, sel) for selectors 0-3 (bytes of y) and 12 (zero), as signed bytes."""
+    out = []
+    for sj in sel:
+        v = 0 if sj == 12 else (y >> (8 * sj)) & 0xFF
+        out.append(v - 256 if v >= 128 else v)
+    return out
+
+
 def _values_bytes(nnz):
     return ((nnz + 1) // 2 + 16 + 15) // 16 * 16
 
@@ -29,6 +50,9 @@ def test_int4_schedule_reads_and_operands(orc, N, K, s):
                  "const uint32_t off = base + half_inclusive_scan(cnt) - cnt;",
                  "const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));",
                  "const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;",
+                 "const uint32_t y = i4_widen((uint32_t)(nibs >> (4u * rank)) & 0xFFFFu);   // ranks rank .. rank + 3",
+                 "a[q] = __builtin_amdgcn_perm(0u, y, sel4[m4]);",
+                 "return y | ((m << 5) - (m << 1));",
                  "int64_t int4_values_bytes(int64_t nnz) { return ((nnz + 1) / 2 + 16 + 15) / 16 * 16; }"):
         assert line in src, f"kernel changed: update this replay ({line})"
     Wq, mask, _ = synth.int4_weight(300 + N + K, N, K, s)
@@ -80,6 +104,14 @@ def test_int4_schedule_reads_and_operands(orc, N, K, s):
                                 r += 1
                             else:
                                 got.append(0)
+                        # the kernel's formulation: per 4-column nibble, widen 4 nibbles, select by table
+                        nibs, rank, got2 = (hi << 32) | lo, 0, []
+                        for q in range(4):
+                            m4 = (int(hw[lane]) >> (4 * q)) & 0xF
+                            y = _widen((nibs >> (4 * rank)) & 0xFFFF)
+                            got2 += _perm0(y, _selector(m4))
+                            rank += bin(m4).count("1")
+                        assert got2 == got, (b, w, p, lane)
                         fr, fg = lane & 15, lane >> 4
                         n = 16 * b + fr
                         k0 = 64 * p + 16 * fg
