@@ -8,7 +8,8 @@
 // int32 sums on v_mfma_i32_16x16x64_i8) and the epilogue are those of the
 // int8 path:  Y[m][n] = fp16_rne((float(acc) * sx[m]) * sw[n]).
 //
-// Kernel: one workgroup per 16-row block, its 8 waves over contiguous ranges
+// Kernel: one workgroup per 16-row block, its W waves (8, or 16 when the
+// launch has fewer than two row blocks per CU) over contiguous ranges
 // of tile pairs (one MFMA each: lanes 0-31 tile 2p, lanes 32-63 tile 2p + 1,
 // lane (fr, fg) row fr, columns 16 (fg % 2) .. + 16 of its tile).  A lane's
 // first value is nibble toff[t] + the exclusive scan of its tile half's kept
@@ -23,7 +24,6 @@
 namespace spl {
 namespace {
 
-constexpr int kI4Waves = 8;
 
 // v_perm_b32 selector for one 4-column nibble: byte j takes byte
 // popcount(nib & ((1 << j) - 1)) of the source if bit j is set, else 12 (zero).
@@ -69,8 +69,9 @@ struct I4Args {
   int32_t M;
 };
 
-__global__ void __launch_bounds__(kI4Waves * 64) k_sparse_i4(const I4Args g) {
-  __shared__ i32x4 part[kI4Waves][64];
+template <int W>
+__global__ void __launch_bounds__(W * 64) k_sparse_i4(const I4Args g) {
+  __shared__ i32x4 part[W][64];
   __shared__ uint32_t sel4[16];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
   if (threadIdx.x < 16) sel4[threadIdx.x] = i4_nibble_selector(threadIdx.x);
@@ -78,7 +79,7 @@ __global__ void __launch_bounds__(kI4Waves * 64) k_sparse_i4(const I4Args g) {
   const int64_t b = blockIdx.x;
   const int S = (int)tile_steps(g.K);
   const int P = (S + 1) / 2;                         // tile pairs (64 columns each)
-  const int L = (P + kI4Waves - 1) / kI4Waves;
+  const int L = (P + W - 1) / W;
   const int pb = wave * L < P ? wave * L : P;
   const int pe = pb + L < P ? pb + L : P;
   const bool xlive = fr < g.M;
@@ -122,7 +123,7 @@ __global__ void __launch_bounds__(kI4Waves * 64) k_sparse_i4(const I4Args g) {
   if (wave != 0) return;
   i32x4 sum = part[0][lane];
 #pragma unroll
-  for (int w = 1; w < kI4Waves; ++w) sum += part[w][lane];
+  for (int w = 1; w < W; ++w) sum += part[w][lane];
   const int m = lane & 15;
   if (m >= g.M) return;
   const float xs = g.sx[m];
@@ -152,7 +153,18 @@ hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, cons
                               void* Y, int32_t* acc_out, hipStream_t s) {
   I4Args g{Xq, sx, W4.bitmask, static_cast<const uint8_t*>(W4.values), W4.tile_offsets, sw,
            static_cast<uint16_t*>(Y), acc_out, W4.rows, W4.cols, (int32_t)M};
-  hipLaunchKernelGGL(k_sparse_i4, dim3((unsigned)tile_blocks(W4.rows)), dim3(kI4Waves * 64), 0, s, g);
+  const int64_t blocks = tile_blocks(W4.rows);
+  static const int cus = [] {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                   hipSuccess || n <= 0)
+      n = 256;
+    return n;
+  }();
+  if (blocks < 2 * (int64_t)cus)
+    hipLaunchKernelGGL(k_sparse_i4<16>, dim3((unsigned)blocks), dim3(16 * 64), 0, s, g);
+  else
+    hipLaunchKernelGGL(k_sparse_i4<8>, dim3((unsigned)blocks), dim3(8 * 64), 0, s, g);
   return hipGetLastError();
 }
 

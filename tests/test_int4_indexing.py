@@ -42,14 +42,16 @@ def _values_bytes(nnz):
     return ((nnz + 1) // 2 + 16 + 15) // 16 * 16
 
 
+@pytest.mark.parametrize("waves", [8, 16])
 @pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (17, 48, 0.7), (40, 96, 0.0), (33, 208, 0.9), (16, 64, 1.0)])
-def test_int4_schedule_reads_and_operands(orc, N, K, s):
+def test_int4_schedule_reads_and_operands(orc, N, K, s, waves):
     src = open(SRC).read()
     for line in ("const int s = 2 * p + (fg >> 1), h = fg & 1;",
                  "hw = (g.bm[t * 16 + fr] >> (16 * h)) & 0xffffu;",
                  "const uint32_t off = base + half_inclusive_scan(cnt) - cnt;",
                  "const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));",
                  "const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;",
+                 "const int L = (P + W - 1) / W;",
                  "const uint32_t y = i4_widen((uint32_t)(nibs >> (4u * rank)) & 0xFFFFu);   // ranks rank .. rank + 3",
                  "a[q] = __builtin_amdgcn_perm(0u, y, sel4[m4]);",
                  "return y | ((m << 5) - (m << 1));",
@@ -63,7 +65,6 @@ def test_int4_schedule_reads_and_operands(orc, N, K, s):
     words = packed.view(np.uint32)
     B, S = (N + 15) // 16, (K + 31) // 32
     P = (S + 1) // 2
-    waves = 8
     dense = np.where(mask.astype(bool), Wq, np.int8(0))
     for b in range(B):
         L = (P + waves - 1) // waves
