@@ -510,11 +510,14 @@ struct Chunk2 {
 // kGated: the gated half of a Llama MLP.  Task 0 is the gate and task 1 the up
 // projection (same X, N, K); workgroup j pairs row block j of both and stores
 // silu(gate) * up (silu(z) = z / (1 + e^-z), from the fp32 sums) into task 0's Y.
-template <class T, int W, bool kGated>
+// XL (one activation row): the row is staged in LDS after the value buffers,
+// as in k_sparse_decode, and both blocks' MFMAs read it from there.
+template <class T, int W, bool kGated, bool XL = false>
 __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGroupArg g) {
   constexpr int C = kChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
+  __shared__ __align__(16) u32x4 xzero[4];
   constexpr int WS = C + 2;                          // word row stride (see k_sparse_decode)
   __shared__ __align__(16) uint32_t words[W][2][16 * WS];
   const int ti = kGated ? 0 : find_task(g.first, g.count);
@@ -584,6 +587,9 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
     }
   };
 
+  uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + sparse2_vbuf_bytes<W>());
+  XStager<W> xst;
+  if constexpr (XL) xst.load(tk.X, M, K);
   int32_t orng[2] = {0, 0};
   Chunk2 ch{0, {0u, 0u}, {0, 0}};
   if (kbeg < kend) {
@@ -593,9 +599,12 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
     issue(ch, kbeg);
   }
   build_nibble_table(lut);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
+  if constexpr (XL) xst.store(xs, K);
   __syncthreads();
 
   const XGlobal<1> xop(tk.X, M, K, fr, fg);
+  const XShared xsh(xs, xzero, M, K, fr, fg);        // (XL only)
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr[2] = {lds_off(vbuf[0]), lds_off(vbuf[1])};
   f32x4 acc[2][1] = {{f32x4{0.f, 0.f, 0.f, 0.f}}, {f32x4{0.f, 0.f, 0.f, 0.f}}};
@@ -620,8 +629,10 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
 
     // 2. the chunk's activations, then the next chunk's loads
     u32x4 xb[C][1];
+    if constexpr (!XL) {
 #pragma unroll
-    for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cur.cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+      for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cur.cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+    }
     const int c1 = c0 + cur.cn;
     if (c1 < kend) {
       if (c1 - ob + C > kOffsetLanes) {
@@ -651,6 +662,10 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
         for (int h = 0; h < 2; ++h) {
           const int j = jp + h;
           if (j < cur.cn) {
+            if constexpr (XL) {                      // staged row: zeros past K; padding rows stay zero
+              xb[j][0] = u32x4{0u, 0u, 0u, 0u};
+              if (xsh.step) xb[j][0] = lds_load16(xsh.addr + xsh.step * (uint32_t)(c0 + j));
+            }
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
               const uint32_t wj = h ? wp[b].y : wp[b].x;
@@ -926,10 +941,13 @@ hipError_t launch_gated_decode(const void* X, int64_t M, const spl_matrix& Wg, c
   g.first[0] = 0, g.first[1] = B, g.first[2] = B;
   g.count = 2;
   g.M = (int32_t)M;
-  auto* kernel = Wg.dtype == SPL_BF16 ? k_sparse_decode2<Bf16, W, true> : k_sparse_decode2<F16, W, true>;
-  const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>());
+  const bool xl = M == 1 && x_lds_bytes(1, Wg.cols) <= (size_t)kXLdsMax;   // one row: staged in LDS
+  auto* kernel = Wg.dtype == SPL_BF16 ? (xl ? k_sparse_decode2<Bf16, W, true, true> : k_sparse_decode2<Bf16, W, true>)
+                                      : (xl ? k_sparse_decode2<F16, W, true, true> : k_sparse_decode2<F16, W, true>);
+  const size_t lds = sparse2_vbuf_bytes<W>() + (xl ? x_lds_bytes(1, Wg.cols) : 0);
+  const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>() + kXLdsMax);     // an upper bound
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(kernel, dim3((unsigned)B), dim3(W * kWave), sparse2_vbuf_bytes<W>(), s, g);
+  hipLaunchKernelGGL(kernel, dim3((unsigned)B), dim3(W * kWave), lds, s, g);
   return hipGetLastError();
 }
 
