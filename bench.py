@@ -1,26 +1,31 @@
 """Benchmark of the sparse linear hot path on one MI355X.
 
-Default workload: one Llama-2-7B decoder layer's seven linear layers (q, k, v,
-o: 4096x4096; gate, up: 11008x4096; down: 4096x11008) in bf16, weights
-N(0, 0.02) magnitude-pruned to 70% per matrix and stored in the bitmask
-expansion format, activations N(0, 1) at decode batch sizes 1, 4 and 16.
+Default workload (the headline line): the full Llama-2-7B linear stack, 32
+decoder layers x 7 matrices (q, k, v, o: 4096x4096; gate, up: 11008x4096;
+down: 4096x11008), distinct seeds, bf16, weights N(0, 0.02) magnitude-pruned to
+70% per matrix and stored in the bitmask expansion format (4.7 GB, beyond the
+256 MB Infinity Cache), activations N(0, 1), decode batch sizes 1, 2, 4, 8, 16
+and 32.
 
-One step = the seven sparse linears at each of the three batch sizes (1 + 4 +
-16 = 21 tokens) in the order of a decoder layer.  The layer driver launches
-the independent projections together, as a decoder layer allows: q|k|v in one
-grouped launch, o, gate|up in one grouped launch, then down (4 launches per
-batch size, 12 per step; `--driver single` launches the seven separately).
-Each step is one HIP graph; steps rotate over `--layers` distinct layers (8 by
-default, 1.18 GB of compressed weights) so that the 256 MB Infinity Cache
-cannot hold the weights between steps.  Inputs are resident in HBM before
-timing starts.
+One step = the whole stack at every batch size (63 tokens).  Within a batch
+size the layers run in order with a decoder's data dependencies: q|k|v in one
+grouped launch (they share their input), o, gate|up in one grouped launch,
+down - 4 launches per layer, 128 per batch size, one HIP graph per batch size.
+Inputs are resident in HBM before timing starts; `value` is tokens/s over the
+wall time of the timed steps.
 
-Printed (one JSON line): tokens/s of the whole step, the roofline of the
-dominant kernel (sparse decode: algorithmic bytes = stored values + bitmask +
-tile offsets + X + Y per launch; its mean launch duration = GPU time of the
-timed graph replays over launches per step), the same kernels run on dense
-weights (per batch size), and
+Printed (one JSON line): tokens/s of the whole step; per batch size the step
+time, tokens/s and achieved HBM rate, the same kernels on dense weights and
+the vendor GEMM library (torch linear) on the same dense weights; the
+roofline of the dominant kernel (sparse decode: algorithmic bytes = stored
+values + bitmask + tile offsets + X + Y per launch, over its mean launch
+duration = GPU time of the timed replays from HIP events / launches), against
+the nominal 8 TB/s and the read rate this device sustains (spl_read_probe);
 the CPU oracle timed on this host's cores on a bounded sample.
+
+`--workload` selects the other rows' lines (one layer, one matrix, prefill,
+int8, gated MLP half, pruning, training step, int4, the stack with one launch
+per layer).
 """
 from __future__ import annotations
 
@@ -871,62 +876,241 @@ def run_int4(args):
                  cpu, {"per_M": per_M}, dtype="i8")
 
 
-def run_stack(args):
-    """All 32 decoder layers (224 matrices, distinct seeds) at 70%, run layer
-    after layer with the grouped driver, at batches 1, 2, 4, 8, 16, 32."""
-    torch, spl = _need_gpu()
-    nl = 32
-    host = generate_layers(nl, "bf16", 0.7, args.workers)
-    layers = upload_layers(host, "bf16", keep_dense=not args.no_dense)
-    del host
-    Ms = [1, 2, 4, 8, 16, 32]
-    xs = make_activations("bf16", max(Ms))
+def _gen_weight_bits(job):
+    """Worker: the bf16 bits of matrix j of layer l (the generator's draw and
+    rounding; the mask is made on the GPU, bit-exact with the generator's)."""
+    l, j, N, K = job
+    return l, j, synth.round_to(synth.normal_f32(synth.weight_seed(l, j), (N, K), synth.WEIGHT_STD), "bf16")
+
+
+STACK_MS = [1, 2, 4, 8, 16, 32]
+STACK_LAYERS = 32
+
+
+def load_stack(args, keep_dense: bool):
+    """All 32 layers (224 matrices, distinct seeds) at 70%: weights drawn on the
+    host by worker processes started before this process touches the GPU,
+    magnitude masks and packing on the GPU.  Returns (torch, spl, layers) with
+    layers[l][j] = (packed, dense or None)."""
+    import multiprocessing as mp
+
     shapes = synth.LLAMA2_7B_LINEARS
+    num, den = synth.parse_sparsity(args.sparsity)
+    jobs = [(l, j, N, K) for l in range(STACK_LAYERS) for j, (_, N, K) in enumerate(shapes)]
+    with cf.ProcessPoolExecutor(max_workers=args.workers, mp_context=mp.get_context("spawn")) as ex:
+        futures = [ex.submit(_gen_weight_bits, job) for job in jobs]     # workers exist before the GPU is used
+        torch, spl = _need_gpu()
+        ws = torch.empty((spl.lib().spl_magnitude_mask_workspace_bytes(),), dtype=torch.uint8, device="cuda")
+        layers = [[None] * len(shapes) for _ in range(STACK_LAYERS)]
+        for f in futures:
+            l, j, bits = f.result()
+            N, K = bits.shape
+            Wd = _to_dev(bits, "bf16", torch)
+            mask = spl.magnitude_mask(Wd, N * K * num // den, workspace=ws)
+            layers[l][j] = (spl.pack_sparse(Wd, mask), Wd if keep_dense else None)
+            del mask
+    torch.cuda.synchronize()
+    return torch, spl, layers
+
+
+def hbm_probe(torch, spl, nbytes: int = 4 << 30, reps: int = 10) -> float:
+    """Best read rate (GB/s) of spl_read_probe over a buffer far larger than the
+    Infinity Cache."""
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    best = 0.0
+    for i in range(reps + 2):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        spl.read_probe(buf, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        if i >= 2:
+            best = max(best, nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del buf
+    return best
+
+
+def _stack_fns(spl, layers, xsl, ys, units):
+    def sparse_stack(M):
+        for row in layers:
+            for u in units:
+                spl.sparse_linear_group([xsl[(M, j)] for j in u], [row[j][0] for j in u], outs=[ys[(M, j)] for j in u])
+
+    def dense_stack(M):
+        for row in layers:
+            for u in units:
+                spl.dense_linear_group([xsl[(M, j)] for j in u], [row[j][1] for j in u], outs=[ys[(M, j)] for j in u])
+    return sparse_stack, dense_stack
+
+
+def _graph(torch, fn):
+    """fn() captured in one HIP graph (after one eager run that warms the launch path)."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def _replay_ms(torch, g, reps: int, warmup: int = 2) -> float:
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def run_stack(args):
+    """Default workload: the full 32-layer Llama-2-7B linear stack (224
+    matrices, distinct seeds) at 70%, bf16, decode batches 1, 2, 4, 8, 16, 32.
+    One step = the whole stack at every batch size, each batch size layer after
+    layer in a decoder's order with its data dependencies: q|k|v (one grouped
+    launch: they share their input), o, gate|up (one grouped launch), down -
+    4 launches per layer, 128 per batch size, one HIP graph per batch size."""
+    torch, spl, layers = load_stack(args, keep_dense=not args.no_dense)
+    shapes = synth.LLAMA2_7B_LINEARS
+    Ms = STACK_MS
+    xs = make_activations("bf16", max(Ms))
     xsl = {(M, j): xs[j][:M].contiguous() for M in Ms for j in range(len(shapes))}
-    ys = {(M, j): torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms for j, (_, N, _) in
-          enumerate(shapes)}
-    per_M, tot_tokens, tot_ms, tot_wall = {}, 0, 0.0, 0.0
-    reps = max(5, args.steps // 20)
-    for M in Ms:
-        def sparse_stack(key, unit, M=M):          # layer after layer, 4 grouped launches each
-            for l in range(nl):
-                for u in GROUPED:
-                    spl.sparse_linear_group([xsl[(M, j)] for j in u], [layers[l][j][0] for j in u],
-                                            outs=[ys[(M, j)] for j in u])
+    ys = {(M, j): torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms
+          for j, (_, N, _) in enumerate(shapes)}
+    sparse_stack, dense_stack = _stack_fns(spl, layers, xsl, ys, GROUPED)
+    graphs = {M: _graph(torch, lambda M=M: sparse_stack(M)) for M in Ms}
 
-        def dense_stack(key, unit, M=M):
-            for l in range(nl):
-                for u in GROUPED:
-                    spl.dense_linear_group([xsl[(M, j)] for j in u], [layers[l][j][1] for j in u],
-                                           outs=[ys[(M, j)] for j in u])
+    # timed region: `steps` steps, each the stack at every batch size; events per batch size
+    for i in range(args.warmup):
+        for M in Ms:
+            graphs[M].replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = {M: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)] for M in Ms}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        for M in Ms:
+            ev[M][i][0].record(stream)
+            graphs[M].replay()
+            ev[M][i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = {M: float(np.mean([a.elapsed_time(b) for a, b in ev[M]])) for M in Ms}
+    del graphs
 
-        # one graph = the whole stack (32 layers x 4 launches) at batch M
-        wall, g = _timed(["stack"], sparse_stack, reps, 2, [0])
-        d = {"step_us": round(g * 1e3, 1), "tokens_per_s": round(M / (g * 1e-3), 1)}
-        if not args.no_dense:
-            _, gd = _timed(["stack"], dense_stack, reps, 2, [0])
-            d.update({"dense_step_us": round(gd * 1e3, 1), "speedup_vs_dense": round(gd / g, 3)})
-        per_M[str(M)] = d
-        tot_tokens += M
-        tot_ms += g
-        tot_wall += wall
-    step_bytes = sum(layers[l][j][0].compressed_bytes() for l in range(nl) for j in range(len(shapes)))
+    nl = len(layers)
     launches = nl * len(GROUPED)
-    avg_launch_ms = tot_ms / len(Ms) / launches
-    achieved = (step_bytes + sum(M * 156160 * nl for M in Ms) / len(Ms)) / launches / (avg_launch_ms * 1e-3) / 1e9
+    weight_bytes = sum(layers[l][j][0].compressed_bytes() for l in range(nl) for j in range(len(shapes)))
+    xy_bytes = {M: nl * sum(M * (K + N) * 2 for (_, N, K) in shapes) for M in Ms}
+    dense_bytes = nl * sum(N * K * 2 for (_, N, K) in shapes)
+    per_M = {}
+    reps = max(5, args.steps // 4)
+    for M in Ms:
+        g = gpu_ms[M]
+        d = {"step_us": round(g * 1e3, 1), "tokens_per_s": round(M / (g * 1e-3), 1),
+             "hbm_gbs": round((weight_bytes + xy_bytes[M]) / (g * 1e-3) / 1e9, 1),
+             "layer_us": round(g * 1e3 / nl, 2)}
+        if not args.no_dense:
+            gd_graph = _graph(torch, lambda M=M: dense_stack(M))
+            gd = _replay_ms(torch, gd_graph, reps)
+            del gd_graph
+            d.update({"dense_step_us": round(gd * 1e3, 1),
+                      "dense_hbm_gbs": round((dense_bytes + xy_bytes[M]) / (gd * 1e-3) / 1e9, 1),
+                      "speedup_vs_dense": round(gd / g, 3)})
+        per_M[str(M)] = d
+
+    # the vendor library's dense GEMM (torch linear -> hipBLASLt / rocBLAS) on the same
+    # dense weights, as a cross-check of the dense comparator
+    vendor = {}
+    if not args.no_dense:
+        for M in (1, 4, 16):
+            def vendor_stack(M=M):
+                for row in layers:
+                    for j in range(len(shapes)):
+                        torch.nn.functional.linear(xsl[(M, j)], row[j][1], out=ys[(M, j)])
+            vendor_stack()
+            ref = ys[(M, 6)].clone()
+            gv = _graph(torch, vendor_stack)
+            us = _replay_ms(torch, gv, reps) * 1e3
+            same = bool(torch.equal(ys[(M, 6)], ref))          # the graph replays what eager computes
+            del gv
+            vendor[str(M)] = {"step_us": round(us, 1),
+                              "hbm_gbs": round((dense_bytes + xy_bytes[M]) / (us * 1e-6) / 1e9, 1),
+                              "our_dense_vs_vendor": round(us / per_M[str(M)]["dense_step_us"], 3),
+                              "graph_matches_eager": same}
+
+    probe = hbm_probe(torch, spl)
+    avg_launch_ms = sum(gpu_ms.values()) / (len(Ms) * launches)
+    bytes_per_launch = sum(weight_bytes + xy_bytes[M] for M in Ms) / (len(Ms) * launches)
+    achieved = bytes_per_launch / (avg_launch_ms * 1e-3) / 1e9
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline("bf16", 0.7, [1])
+        cpu = cpu_baseline("bf16", args.sparsity, [1])
         cpu["value"] = round(cpu["value"] / nl, 4)
-        cpu["sample"] += f"; tokens/s of the 32-layer stack = that rate / {nl}"
-    return _line(args, "sparse-linear tokens/s, Llama-2-7B 32-layer linear stack at 70%",
-                 round(tot_tokens / (tot_wall * 1e-3), 1), "tokens/s", tot_wall,
-                 "Llama-2-7B linear stack, 32 layers x 7 matrices (distinct seeds), bf16, 70% sparsity, "
-                 f"decode batches {Ms}, grouped driver (4 launches per layer), one graph per batch size",
+        cpu["sample"] += f"; tokens/s of the {nl}-layer stack = that rate / {nl}"
+    tokens = sum(Ms) * args.steps
+    out = _line(args, METRIC, round(tokens / wall, 1), "tokens/s", wall * 1e3 / args.steps,
+                "Llama-2-7B linear stack: 32 layers x 7 matrices (q,k,v,o 4096x4096; gate,up 11008x4096; down "
+                "4096x11008), distinct seeds, bf16, 70% unstructured magnitude sparsity in bitmask format; one step "
+                f"= the stack at decode batches {Ms} ({sum(Ms)} tokens), 4 dependent launches per layer",
+                {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_decode",
+                 "bytes_per_launch": int(bytes_per_launch), "avg_launch_us": round(avg_launch_ms * 1e3, 3),
+                 "peak_measured": round(probe, 1), "frac_of_measured": round(achieved / probe, 4)},
+                cpu,
+                {"batches": Ms, "tokens_per_step": sum(Ms), "launches_per_batch": launches,
+                 "compressed_weight_bytes": int(weight_bytes), "dense_weight_bytes": int(dense_bytes),
+                 "per_M": per_M, "vendor_dense": vendor, "hbm_read_probe_gbs": round(probe, 1),
+                 "gpu_ms_per_step": round(sum(gpu_ms.values()), 4)})
+    return out
+
+
+def run_stack_layer(args):
+    """The same stack with the seven linears of a layer in ONE launch (the
+    benchmark's inputs are not chained from matrix to matrix, so a layer's
+    matrices are independent): 32 launches per batch size.  Shows the kernel
+    without the fixed cost of four launches per layer."""
+    torch, spl, layers = load_stack(args, keep_dense=False)
+    shapes = synth.LLAMA2_7B_LINEARS
+    Ms = STACK_MS
+    xs = make_activations("bf16", max(Ms))
+    xsl = {(M, j): xs[j][:M].contiguous() for M in Ms for j in range(len(shapes))}
+    ys = {(M, j): torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for M in Ms
+          for j, (_, N, _) in enumerate(shapes)}
+    order = [(6, 4, 5, 0, 1, 2, 3)]                 # the longest rows (down) first
+    sparse_stack, _ = _stack_fns(spl, layers, xsl, ys, order)
+    nl = len(layers)
+    weight_bytes = sum(layers[l][j][0].compressed_bytes() for l in range(nl) for j in range(len(shapes)))
+    per_M, wall_ms = {}, 0.0
+    for M in Ms:
+        g = _graph(torch, lambda M=M: sparse_stack(M))
+        ms = _replay_ms(torch, g, args.steps, args.warmup)
+        del g
+        b = weight_bytes + nl * sum(M * (K + N) * 2 for (_, N, K) in shapes)
+        per_M[str(M)] = {"step_us": round(ms * 1e3, 1), "tokens_per_s": round(M / (ms * 1e-3), 1),
+                         "hbm_gbs": round(b / (ms * 1e-3) / 1e9, 1)}
+        wall_ms += ms
+    avg_launch_ms = wall_ms / (len(Ms) * nl)
+    bpl = sum(weight_bytes + nl * sum(M * (K + N) * 2 for (_, N, K) in shapes) for M in Ms) / (len(Ms) * nl)
+    achieved = bpl / (avg_launch_ms * 1e-3) / 1e9
+    return _line(args, METRIC, round(sum(Ms) / (wall_ms * 1e-3), 1), "tokens/s", wall_ms,
+                 "Llama-2-7B linear stack, 32 layers x 7 matrices, bf16, 70%; one launch per layer (its seven "
+                 f"independent matrices), decode batches {Ms}",
                  {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                   "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_sparse_decode",
-                  "avg_launch_us": round(avg_launch_ms * 1e3, 3)},
-                 cpu, {"per_M": per_M, "compressed_bytes": int(step_bytes)})
+                  "bytes_per_launch": int(bpl), "avg_launch_us": round(avg_launch_ms * 1e3, 3)},
+                 None, {"per_M": per_M})
 
 
 def main():
@@ -942,16 +1126,17 @@ def main():
     ap.add_argument("--workers", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--driver", choices=["grouped", "single"], default="grouped",
                     help="grouped: q|k|v and gate|up share a launch (a decoder layer's independent projections)")
-    ap.add_argument("--workload", choices=["decode", "single", "prefill", "int8", "int8-prefill", "gated", "prune",
-                                                   "train", "int4", "stack"],
-                    default="decode",
-                    help="decode: one layer at batches 1,4,16 (default, the headline); single: one 4096x4096 "
+    ap.add_argument("--workload", choices=["stack", "stack-layer", "layer", "decode", "single", "prefill", "int8",
+                                           "int8-prefill", "gated", "prune", "train", "int4"],
+                    default="stack",
+                    help="stack: the 32-layer Llama-2-7B linear stack at batches 1..32, 4 dependent launches per "
+                         "layer (default, the headline); stack-layer: the same with one launch per layer; layer "
+                         "(or decode): one layer at batches 1,4,16; single: one 4096x4096 "
                          "fp16 matrix at 50%%, batch 1; prefill: one layer at M=512 and 2048; int8: one layer, "
                          "int8 weights and activations, batches 1,16,64; int8-prefill: one layer, int8 weights, "
                          "activations quantized per token, M=512 and 2048; gated: fused silu(gate)*up "
                          "of gate/up at batches 1,4,16; prune: magnitude masks of one layer; train: a masked training step of one "
-                         "layer at M=2048; int4: 4-bit weights at batches 1,16; stack: all 32 layers at "
-                         "batches 1..32")
+                         "layer at M=2048; int4: 4-bit weights at batches 1,16")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES ten times (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes) and exit")
@@ -972,10 +1157,9 @@ def main():
               f"(the kernels run on a single GPU; sharding across GPUs is not implemented)", file=sys.stderr)
         sys.exit(2)
 
-    if args.workload != "decode":
-        out = {"single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
-               "gated": run_gated, "prune": run_prune, "train": run_train, "int4": run_int4,
-               "stack": run_stack}[args.workload](args)
+    if args.workload not in ("decode", "layer"):
+        out = {"stack": run_stack, "stack-layer": run_stack_layer, "single": run_single, "prefill": run_prefill, "int8": run_int8, "int8-prefill": run_int8_prefill,
+               "gated": run_gated, "prune": run_prune, "train": run_train, "int4": run_int4}[args.workload](args)
         print(json.dumps(out), flush=True)
         return
 

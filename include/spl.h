@@ -111,6 +111,15 @@ int32_t spl_version(void);
 /* Static text for a status code. */
 const char* spl_status_string(spl_status s);
 
+/* Measurement helper, not part of the method: reads `bytes` (> 0, a multiple
+ * of 16) of the 16-byte aligned device buffer `buf` with coalesced 16-byte
+ * loads from every compute unit, the way a streaming kernel at its best reads
+ * HBM; timing it gives the read rate the device sustains, against which a
+ * kernel's achieved bandwidth is also reported.  `sink` (device, 4 bytes) is
+ * written only if the folded data equal one fixed constant.  Asynchronous on
+ * `stream`. */
+spl_status spl_read_probe(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream);
+
 /* Host-only consistency check of a view's scalar fields and pointers
  * (no device access): rows, cols >= 1, dtype and layout known,
  * 0 <= nnz < 2^31, nnz <= rows*cols, the layout's arrays non-null (values may

@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
     sigs = {
         "spl_version": (I32, []),
         "spl_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "spl_read_probe": (ctypes.c_int, [P, I64, P, P]),
         "spl_check_matrix": (ctypes.c_int, [MP]),
         "spl_tile16_count": (I64, [I64, I64]),
         "spl_retile16": (ctypes.c_int, [MP, P, P, P, P]),
@@ -285,6 +286,17 @@ def sparse_linear_silu_mul(X: torch.Tensor, Wgate: SparseMatrix, Wup: SparseMatr
     _check("spl_sparse_linear_silu_mul", L.spl_sparse_linear_silu_mul(_ptr(X), M, ctypes.byref(vg), ctypes.byref(vu),
                                                                       _ptr(out), ALGO[algo], _stream(stream)))
     return out
+
+
+def read_probe(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """Stream-read every byte of `buf` (a measurement helper; see spl_read_probe)."""
+    L = lib()
+    _dev_tensor(buf, "buf")
+    _dev_tensor(sink, "sink")
+    nbytes = buf.numel() * buf.element_size()
+    if sink.numel() * sink.element_size() < 4:
+        raise ValueError("sink needs 4 bytes")
+    _check("spl_read_probe", L.spl_read_probe(_ptr(buf), nbytes, _ptr(sink), _stream(stream)))
 
 
 def magnitude_mask(W: torch.Tensor, prune: int, out: torch.Tensor | None = None,

@@ -57,6 +57,17 @@ const char* spl_status_string(spl_status s) {
   return "unknown status";
 }
 
+spl_status spl_read_probe(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream) {
+  if (!buf || !sink || bytes <= 0 || bytes % 16 != 0 || !aligned(buf, 16) || !aligned(sink, 4))
+    return SPL_ERR_INVALID_ARG;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return SPL_ERR_DEVICE;
+  (void)hipGetLastError();
+  return launched(spl::launch_read_probe(buf, bytes, sink, cus, stream));
+}
+
 spl_status spl_check_matrix(const spl_matrix* Wc) {
   if (!Wc) return SPL_ERR_INVALID_ARG;
   if (!dims_ok(Wc->rows, Wc->cols)) return SPL_ERR_INVALID_ARG;

@@ -166,6 +166,8 @@ int64_t int4_values_bytes(int64_t nnz);
 hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, hipStream_t s);
 hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& W4, const float* sw,
                               void* Y, int32_t* acc_out, hipStream_t s);
+// Streaming-read probe over `bytes` (a multiple of 16) of a 16-byte aligned buffer.
+hipError_t launch_read_probe(const void* buf, int64_t bytes, uint32_t* sink, int cus, hipStream_t s);
 hipError_t launch_quantize_rows_i8(const void* X, int32_t dtype, int64_t M, int64_t K, int8_t* Xq, float* sx,
                                    hipStream_t s);
 }  // namespace spl

@@ -29,14 +29,8 @@ def _pack(spl, W, mask, dtype):
 DECODE_M = [1, 2, 3, 4, 5, 8, 15, 16, 17, 31, 32]
 
 
-_FAULTED = ("this case took a GPU memory fault under an earlier kernel revision (prefetch read past the "
-            "wave's LDS tile region, shown on the CPU by test_decode_indexing.py); kept off the GPU until "
-            "the next session")
-
-
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
-@pytest.mark.parametrize("N,K,s", [pytest.param(1, 8, 0.5, marks=pytest.mark.skip(reason=_FAULTED)),
-                                   (2, 16, 0.5), (15, 64, 0.7), (17, 264, 0.5), (100, 1000, 0.7),
+@pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (2, 16, 0.5), (15, 64, 0.7), (17, 264, 0.5), (100, 1000, 0.7),
                                    (48, 2056, 0.0), (33, 512, 1.0)])
 def test_decode_small(orc, spl, dtype, N, K, s):
     W, mask = synth.weight(200 + N, N, K, dtype, s)
