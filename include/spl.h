@@ -26,8 +26,11 @@
  *     reported by the HIP runtime at launch map to SPL_ERR_DEVICE.  Nothing
  *     throws across this interface.
  *   - Device buffers must be 16-byte aligned.  The `values` array of a
- *     compressed matrix must be followed by at least 16 readable bytes:
- *     kernels read (never write) up to 16 bytes past the last payload.
+ *     compressed matrix is allocated with spl_values_bytes(dtype, nnz) bytes
+ *     or more (the payloads rounded up to 16 bytes plus 16): kernels read
+ *     (never write) up to 16 bytes past the last payload.  A view states its
+ *     allocation in `values_bytes`, which spl_check_matrix and every entry
+ *     point taking a view check.
  *
  * Two lossless encodings of a compressed matrix
  *
@@ -103,7 +106,14 @@ typedef struct {
   const void* values;            /* [nnz] payloads */
   const int32_t* row_offsets;    /* rows: [N+1]; tiles: unused (may be NULL) */
   const int32_t* tile_offsets;   /* tiles: [B*S + 1]; rows: unused (may be NULL) */
+  int64_t values_bytes;          /* bytes allocated at `values`: >= spl_values_bytes(dtype, nnz) */
 } spl_matrix;
+
+/* Bytes the `values` array of a view with `nnz` payloads of `dtype` must
+ * have: the payload bytes (2 per fp16/bf16 value, 1 per int8 value, one per
+ * two 4-bit values) rounded up to 16, plus 16 bytes the kernels may read past
+ * the last payload.  0 for an unknown dtype or a negative nnz. */
+int64_t spl_values_bytes(int32_t dtype, int64_t nnz);
 
 /* Library version, (major << 16) | minor. */
 int32_t spl_version(void);
@@ -122,9 +132,23 @@ spl_status spl_read_probe(const void* buf, int64_t bytes, uint32_t* sink, hipStr
 
 /* Host-only consistency check of a view's scalar fields and pointers
  * (no device access): rows, cols >= 1, dtype and layout known,
- * 0 <= nnz < 2^31, nnz <= rows*cols, the layout's arrays non-null (values may
- * be NULL only if nnz == 0), 16-byte alignment of bitmask and values. */
+ * 0 <= nnz < 2^31, nnz <= rows*cols, the layout's arrays and `values`
+ * non-null, values_bytes >= spl_values_bytes(dtype, nnz), 16-byte alignment
+ * of bitmask and values. */
 spl_status spl_check_matrix(const spl_matrix* Wc);
+
+/* Device check of a view's format (paper sections 2.4.1 and 2.4.2: a block's
+ * stored values are exactly its kept entries, in order): for every block (a
+ * row, or a 16 x 32 tile) the difference of consecutive offsets equals the
+ * popcount of the block's bitmask words; the first offset is 0 and the last
+ * nnz; bits for columns >= cols (and, in the tile layout, rows >= rows) are 0.
+ * Returns SPL_OK, SPL_ERR_INVALID_ARG for an inconsistent format (or a view
+ * that fails spl_check_matrix), SPL_ERR_DEVICE for a runtime error.  Reads
+ * the bitmask and offsets, not the payloads.  Synchronizes `stream` once to
+ * read the result.  The result word lives in a per-device variable of the
+ * library; calls from several threads take turns (a lock held until the
+ * result is read). */
+spl_status spl_validate(const spl_matrix* Wc, hipStream_t stream);
 
 /* Sizes of the tile layout of an N x K matrix: number of tiles B*S (the
  * bitmask has 16 words per tile, tile_offsets B*S + 1 entries). */
@@ -139,25 +163,35 @@ int64_t spl_tile16_count(int64_t N, int64_t K);
 spl_status spl_retile16(const spl_matrix* rows_in, uint32_t* bitmask_out, void* values_out,
                         int32_t* tile_offsets_out, hipStream_t stream);
 
-/* Pack, step 1 of 2 (paper section 2.4.1: count the kept entries).
+/* Pack, step 1 of 2 (paper section 2.4.1: count the kept entries of every
+ * block, a row or, for the layout the linear kernels read, a 16 x 32 tile).
  *   W           [N][K] payloads of `dtype` (F16, BF16 or I8).
  *   mask        [N][K] uint8, non-zero = kept; or NULL, then an entry is kept
  *               iff its payload is non-zero (fp16/bf16: ignoring the sign bit,
  *               so -0.0 is not kept).
- *   row_offsets out [N+1], written with the exclusive prefix sum of per-row
- *               kept counts.
+ *   layout      SPL_LAYOUT_ROWS or SPL_LAYOUT_TILE16.
+ *   offsets     out: the exclusive prefix sum of per-block kept counts, the
+ *               row_offsets [N+1] (rows) or the tile_offsets [B*S + 1] (tiles)
+ *               of the view the pack describes.
  *   h_nnz       HOST out: number of kept entries.  This call synchronizes
  *               `stream` to read it.  Returns SPL_ERR_OVERFLOW if it would
- *               reach 2^31. */
-spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
-                          int32_t* row_offsets, int64_t* h_nnz, hipStream_t stream);
+ *               reach 2^31.
+ * The caller then allocates the bitmask (rows: N * ceil(K/32) words; tiles:
+ * 16 * spl_tile16_count(N, K) words) and spl_values_bytes(dtype, nnz) bytes
+ * of values. */
+spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K, int32_t layout,
+                          int32_t* offsets, int64_t* h_nnz, hipStream_t stream);
 
 /* Pack, step 2 of 2 (paper section 2.4.1: write bitmask and dense values).
- *   row_offsets from spl_pack_count for the same W and mask.
- *   bitmask     out [N][ceil(K/32)], fully written (pad bits 0).
- *   values      out [nnz] payloads of `dtype`. */
+ *   offsets     from spl_pack_count for the same W, mask and layout.
+ *   bitmask     out, fully written (pad bits 0): rows [N][ceil(K/32)]; tiles
+ *               [B*S][16].
+ *   values      out [nnz] payloads of `dtype`, in the layout's order (the tail
+ *               past nnz is not written).
+ * The result, with nnz and `offsets`, is a view spl_sparse_linear reads
+ * directly when the layout is SPL_LAYOUT_TILE16 (no conversion step). */
 spl_status spl_pack_sparse(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
-                           const int32_t* row_offsets, uint32_t* bitmask, void* values,
+                           int32_t layout, const int32_t* offsets, uint32_t* bitmask, void* values,
                            hipStream_t stream);
 
 /* Decompress (either layout) to a dense [N][K] matrix of the view's dtype:
@@ -263,14 +297,16 @@ spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64
  * two's-complement nibble at byte i / 2, low nibble first, codes in [-8, 7]).
  * spl_pack_int4: values4 out (spl_int4_values_bytes(nnz) bytes, 16-byte
  *   aligned; the tail past ceil(nnz/2) is not written) from an int8
- *   tile-layout view W8 whose codes lie in [-8, 7] (other codes keep their
- *   low 4 bits).  The view of the result is W8's with dtype SPL_I4 and
- *   values = values4.
+ *   tile-layout view W8 whose codes lie in [-8, 7].  A code outside that
+ *   range keeps only its low 4 bits (and so reads back as another value);
+ *   bad_codes (optional device int32, 4-byte aligned) is set, in stream
+ *   order, to the number of such codes, so a caller can reject the result.
+ *   The view of the result is W8's with dtype SPL_I4 and values = values4.
  * spl_sparse_linear_int4: as spl_sparse_linear_int8 (exact int32 sums, the
  *   same fp16 epilogue) for a SPL_I4 tile-layout view, decode batches
  *   0 <= M <= 16 (SPL_ERR_UNSUPPORTED above), K % 16 == 0. */
 int64_t spl_int4_values_bytes(int64_t nnz);
-spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, hipStream_t stream);
+spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, int32_t* bad_codes, hipStream_t stream);
 spl_status spl_sparse_linear_int4(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* W4,
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream);
 

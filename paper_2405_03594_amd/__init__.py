@@ -52,6 +52,7 @@ class _Matrix(ctypes.Structure):
         ("values", ctypes.c_void_p),
         ("row_offsets", ctypes.c_void_p),
         ("tile_offsets", ctypes.c_void_p),
+        ("values_bytes", ctypes.c_int64),
     ]
 
 
@@ -94,10 +95,12 @@ def lib() -> ctypes.CDLL:
         "spl_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "spl_read_probe": (ctypes.c_int, [P, I64, P, P]),
         "spl_check_matrix": (ctypes.c_int, [MP]),
+        "spl_validate": (ctypes.c_int, [MP, P]),
+        "spl_values_bytes": (I64, [I32, I64]),
         "spl_tile16_count": (I64, [I64, I64]),
         "spl_retile16": (ctypes.c_int, [MP, P, P, P, P]),
-        "spl_pack_count": (ctypes.c_int, [P, I32, P, I64, I64, P, ctypes.POINTER(I64), P]),
-        "spl_pack_sparse": (ctypes.c_int, [P, I32, P, I64, I64, P, P, P, P]),
+        "spl_pack_count": (ctypes.c_int, [P, I32, P, I64, I64, I32, P, ctypes.POINTER(I64), P]),
+        "spl_pack_sparse": (ctypes.c_int, [P, I32, P, I64, I64, I32, P, P, P, P]),
         "spl_unpack": (ctypes.c_int, [MP, P, P]),
         "spl_sparse_linear": (ctypes.c_int, [P, I64, MP, P, P]),
         "spl_sparse_linear_ex": (ctypes.c_int, [P, I64, MP, P, I32, P]),
@@ -108,7 +111,7 @@ def lib() -> ctypes.CDLL:
         "spl_magnitude_mask": (ctypes.c_int, [P, I32, I64, I64, I64, P, P, P]),
         "spl_transpose16": (ctypes.c_int, [P, I64, I64, P, P]),
         "spl_int4_values_bytes": (I64, [I64]),
-        "spl_pack_int4": (ctypes.c_int, [MP, P, P]),
+        "spl_pack_int4": (ctypes.c_int, [MP, P, P, P]),
         "spl_sparse_linear_int4": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
         "spl_gather_tiled": (ctypes.c_int, [P, MP, P, P]),
         "spl_sparse_weight_grad_workspace_bytes": (I64, [I64, I64, I64]),
@@ -155,6 +158,49 @@ def _dev_tensor(t: torch.Tensor, name: str) -> torch.Tensor:
     return t
 
 
+def _arg(t, name: str, shape=None, dtype=None, min_numel: int | None = None, device: bool = True) -> torch.Tensor:
+    """An argument tensor's shape, dtype, length and contiguity, checked before
+    its device: the C ABI sees only pointers, so a mismatch here would make a
+    kernel read or write past a buffer."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if min_numel is not None and (t.dim() != 1 or t.numel() < min_numel):
+        raise ValueError(f"{name} must be 1-D with at least {min_numel} entries")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return _dev_tensor(t, name) if device else t
+
+
+def _q_args(Xq, x_scales, N: int, K: int, w_scales, M: int, device: bool = True) -> None:
+    """int8 activations [M][K] and their per-row scales, per-channel weight scales [N]."""
+    _arg(Xq, "Xq", shape=(M, K), dtype=torch.int8, device=False)
+    _arg(x_scales, "x_scales", dtype=torch.float32, min_numel=M, device=False)
+    _arg(w_scales, "w_scales", dtype=torch.float32, min_numel=N, device=False)
+    if device:
+        for t, nm in ((Xq, "Xq"), (x_scales, "x_scales"), (w_scales, "w_scales")):
+            _dev_tensor(t, nm)
+
+
+def _q_outs(out, acc_out, M: int, N: int, device: bool = True) -> None:
+    _arg(out, "out", shape=(M, N), dtype=torch.float16, device=False)
+    if acc_out is not None:
+        _arg(acc_out, "acc_out", shape=(M, N), dtype=torch.int32, device=False)
+    if device:
+        _dev_tensor(out, "out")
+        if acc_out is not None:
+            _dev_tensor(acc_out, "acc_out")
+
+
+def _rows_of(X, name: str) -> int:
+    if not isinstance(X, torch.Tensor) or X.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D tensor")
+    return X.shape[0]
+
+
 @dataclass
 class SparseMatrix:
     """A compressed [N][K] matrix in one of the two layouts of include/spl.h:
@@ -178,7 +224,8 @@ class SparseMatrix:
         return _Matrix(self.rows, self.cols, _TORCH_DTYPE[self.values.dtype], LAYOUT[self.layout], self.nnz,
                        self.bitmask.data_ptr(), self.values.data_ptr(),
                        self.row_offsets.data_ptr() if self.row_offsets is not None else 0,
-                       self.tile_offsets.data_ptr() if self.tile_offsets is not None else 0)
+                       self.tile_offsets.data_ptr() if self.tile_offsets is not None else 0,
+                       self.values.numel() * self.values.element_size())
 
     def compressed_bytes(self) -> int:
         """Bytes of the encoding: payloads + bitmask + offsets."""
@@ -188,46 +235,57 @@ class SparseMatrix:
 
 
 def _values_buffer(nnz: int, dtype: torch.dtype, device) -> torch.Tensor:
-    # payloads rounded up to 16 bytes plus 16 readable bytes of tail: kernels may
-    # read (never write) up to 16 bytes past the last payload
+    # spl_values_bytes: payloads rounded up to 16 bytes plus 16 readable bytes of
+    # tail (kernels may read, never write, up to 16 bytes past the last payload)
     esz = torch.empty((), dtype=dtype).element_size()
-    n = (((nnz * esz + 15) // 16) * 16 + 16) // esz
-    return torch.zeros(n, dtype=dtype, device=device)
+    return torch.zeros(int(lib().spl_values_bytes(_TORCH_DTYPE[dtype], nnz)) // esz, dtype=dtype, device=device)
 
 
 def pack_sparse(W: torch.Tensor, mask: torch.Tensor | None = None, layout: str = "tile16",
                 stream=None) -> SparseMatrix:
     """Compress W [N][K] (fp16/bf16/int8) under `mask` (uint8/bool, non-zero = kept;
-    None = keep the non-zero payloads).  layout="tile16" (default) is the layout
-    the linear kernels read; "rows" is the row-layout interchange format."""
+    None = keep the non-zero payloads) with spl_pack_count + spl_pack_sparse.
+    layout="tile16" (default) is the layout the linear kernels read; "rows" is
+    the row-layout interchange format."""
     L = lib()
-    _dev_tensor(W, "W")
-    if W.dim() != 2 or W.dtype not in _TORCH_DTYPE:
+    if not isinstance(W, torch.Tensor) or W.dim() != 2 or W.dtype not in _TORCH_DTYPE or W.dtype == torch.uint8:
         raise ValueError("W must be a 2-D fp16/bf16/int8 tensor")
     if layout not in LAYOUT:
         raise ValueError(f"unknown layout {layout!r}")
     N, K = W.shape
     if mask is not None:
-        _dev_tensor(mask, "mask")
-        if mask.shape != W.shape:
-            raise ValueError("mask must have W's shape")
         if mask.dtype == torch.bool:
             mask = mask.view(torch.uint8)
-        if mask.dtype != torch.uint8:
-            raise ValueError("mask must be uint8 or bool")
+        _arg(mask, "mask", shape=(N, K), dtype=torch.uint8)
+    _dev_tensor(W, "W")
     code = _TORCH_DTYPE[W.dtype]
-    row_offsets = torch.empty(N + 1, dtype=torch.int32, device=W.device)
-    words = (K + 31) // 32
-    bitmask = torch.empty((N, words), dtype=torch.int32, device=W.device)
+    if layout == "rows":
+        blocks = N
+        bitmask = torch.empty((N, (K + 31) // 32), dtype=torch.int32, device=W.device)
+    else:
+        blocks = int(L.spl_tile16_count(N, K))
+        bitmask = torch.empty(blocks * 16, dtype=torch.int32, device=W.device)
+    offsets = torch.empty(blocks + 1, dtype=torch.int32, device=W.device)
     nnz = ctypes.c_int64(0)
     s = _stream(stream)
-    _check("spl_pack_count", L.spl_pack_count(_ptr(W), code, _ptr(mask), N, K, _ptr(row_offsets),
+    _check("spl_pack_count", L.spl_pack_count(_ptr(W), code, _ptr(mask), N, K, LAYOUT[layout], _ptr(offsets),
                                               ctypes.byref(nnz), s))
     values = _values_buffer(nnz.value, W.dtype, W.device)
-    _check("spl_pack_sparse", L.spl_pack_sparse(_ptr(W), code, _ptr(mask), N, K, _ptr(row_offsets),
+    _check("spl_pack_sparse", L.spl_pack_sparse(_ptr(W), code, _ptr(mask), N, K, LAYOUT[layout], _ptr(offsets),
                                                 _ptr(bitmask), _ptr(values), s))
-    rows = SparseMatrix(bitmask, values, row_offsets, None, N, K, nnz.value, "rows")
-    return rows if layout == "rows" else retile16(rows, stream=stream)
+    if layout == "rows":
+        return SparseMatrix(bitmask, values, offsets, None, N, K, nnz.value, "rows")
+    return SparseMatrix(bitmask, values, None, offsets, N, K, nnz.value, "tile16")
+
+
+def validate(Wc: SparseMatrix, stream=None) -> bool:
+    """Device check of the view's format (spl_validate): True if consistent."""
+    view = Wc.view()
+    st = lib().spl_validate(ctypes.byref(view), _stream(stream))
+    if st == 1:
+        return False
+    _check("spl_validate", st)
+    return True
 
 
 def retile16(Wc: SparseMatrix, stream=None) -> SparseMatrix:
@@ -259,12 +317,12 @@ def sparse_linear(X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = 
                   stream=None) -> torch.Tensor:
     """Y [M][N] = X [M][K] (W . Mask)^T, fp32 accumulation, output in X's dtype."""
     L = lib()
-    _dev_tensor(X, "X")
-    M = X.shape[0]
+    M = _rows_of(X, "X")
+    _arg(X, "X", shape=(M, Wc.cols), dtype=Wc.dtype, device=False)
     if out is None:
         out = torch.empty((M, Wc.rows), dtype=X.dtype, device=X.device)
-    if X.dtype != Wc.dtype or out.dtype != X.dtype:
-        raise ValueError("X, W and Y must share one fp16/bf16 dtype")
+    _arg(out, "out", shape=(M, Wc.rows), dtype=Wc.dtype)
+    _dev_tensor(X, "X")
     view = Wc.view()
     _check("spl_sparse_linear_ex", L.spl_sparse_linear_ex(_ptr(X), M, ctypes.byref(view), _ptr(out), ALGO[algo],
                                                           _stream(stream)))
@@ -276,12 +334,14 @@ def sparse_linear_silu_mul(X: torch.Tensor, Wgate: SparseMatrix, Wup: SparseMatr
     """Y [M][N] = silu(X Wgate^T) * (X Wup^T): the gated half of a Llama MLP in
     one launch (see spl_sparse_linear_silu_mul)."""
     L = lib()
-    _dev_tensor(X, "X")
-    M = X.shape[0]
+    if (Wup.rows, Wup.cols, Wup.dtype) != (Wgate.rows, Wgate.cols, Wgate.dtype):
+        raise ValueError("gate and up must share shape and dtype")
+    M = _rows_of(X, "X")
+    _arg(X, "X", shape=(M, Wgate.cols), dtype=Wgate.dtype, device=False)
     if out is None:
         out = torch.empty((M, Wgate.rows), dtype=X.dtype, device=X.device)
-    if X.dtype != Wgate.dtype or Wup.dtype != Wgate.dtype or out.dtype != X.dtype:
-        raise ValueError("X, both weights and Y must share one fp16/bf16 dtype")
+    _arg(out, "out", shape=(M, Wgate.rows), dtype=Wgate.dtype)
+    _dev_tensor(X, "X")
     vg, vu = Wgate.view(), Wup.view()
     _check("spl_sparse_linear_silu_mul", L.spl_sparse_linear_silu_mul(_ptr(X), M, ctypes.byref(vg), ctypes.byref(vu),
                                                                       _ptr(out), ALGO[algo], _stream(stream)))
@@ -382,15 +442,24 @@ def permute_values(src: torch.Tensor, perm: torch.Tensor, nnz: int, out: torch.T
     return out
 
 
-def pack_int4(W8: SparseMatrix, stream=None) -> SparseMatrix:
+def pack_int4(W8: SparseMatrix, stream=None, check: bool = True) -> SparseMatrix:
     """The 4-bit form of an int8 tile-layout matrix whose codes lie in [-8, 7]
-    (see spl_pack_int4): same pattern, values as uint8 bytes of two nibbles."""
+    (see spl_pack_int4): same pattern, values as uint8 bytes of two nibbles.
+    With check, the library counts codes outside [-8, 7] and a nonzero count
+    raises ValueError (this waits for the stream)."""
     L = lib()
     if W8.dtype != torch.int8 or W8.layout != "tile16":
         raise ValueError("pack_int4 takes an int8 matrix in the tile layout")
-    v4 = torch.zeros((L.spl_int4_values_bytes(W8.nnz),), dtype=torch.uint8, device=W8.values.device)
+    dev = W8.values.device
+    v4 = torch.zeros((L.spl_int4_values_bytes(W8.nnz),), dtype=torch.uint8, device=dev)
+    bad = torch.zeros((1,), dtype=torch.int32, device=dev) if check else None
     view = W8.view()
-    _check("spl_pack_int4", L.spl_pack_int4(ctypes.byref(view), _ptr(v4), _stream(stream)))
+    _check("spl_pack_int4", L.spl_pack_int4(ctypes.byref(view), _ptr(v4), _ptr(bad), _stream(stream)))
+    if check:
+        (stream if stream is not None else torch.cuda.current_stream()).synchronize()
+        n = int(bad.item())
+        if n:
+            raise ValueError(f"pack_int4: {n} codes outside [-8, 7]")
     return SparseMatrix(W8.bitmask, v4, None, W8.tile_offsets, W8.rows, W8.cols, W8.nnz, "tile16")
 
 
@@ -399,11 +468,12 @@ def sparse_linear_int4(Xq: torch.Tensor, x_scales: torch.Tensor, W4: SparseMatri
                        stream=None) -> torch.Tensor:
     """fp16 Y from 4-bit sparse weights and int8 activations, M <= 16 (see spl_sparse_linear_int4)."""
     L = lib()
-    for t, nm in ((Xq, "Xq"), (x_scales, "x_scales"), (w_scales, "w_scales")):
-        _dev_tensor(t, nm)
-    M = Xq.shape[0]
+    M = _rows_of(Xq, "Xq")
+    _q_args(Xq, x_scales, W4.rows, W4.cols, w_scales, M, device=False)
     if out is None:
         out = torch.empty((M, W4.rows), dtype=torch.float16, device=Xq.device)
+    _q_outs(out, acc_out, M, W4.rows)
+    _q_args(Xq, x_scales, W4.rows, W4.cols, w_scales, M)
     view = W4.view()
     _check("spl_sparse_linear_int4", L.spl_sparse_linear_int4(_ptr(Xq), _ptr(x_scales), M, ctypes.byref(view),
                                                               _ptr(w_scales), _ptr(out), _ptr(acc_out),
@@ -416,12 +486,18 @@ def quantize_rows_i8(X: torch.Tensor, out: torch.Tensor | None = None, scales: t
     """Per-token int8 codes and binary32 scales of fp16/bf16 activations X [M][K]
     (section 3.4; see spl_quantize_rows_i8).  Returns (Xq int8 [M][K], x_scales f32 [M])."""
     L = lib()
-    _dev_tensor(X, "X")
-    M, K = X.shape
+    M = _rows_of(X, "X")
+    K = X.shape[1]
+    if X.dtype not in (torch.float16, torch.bfloat16):
+        raise ValueError("X must be fp16 or bf16")
     if out is None:
         out = torch.empty((M, K), dtype=torch.int8, device=X.device)
     if scales is None:
         scales = torch.empty((M,), dtype=torch.float32, device=X.device)
+    _arg(out, "out", shape=(M, K), dtype=torch.int8, device=False)
+    _arg(scales, "scales", dtype=torch.float32, min_numel=M, device=False)
+    for t, nm in ((X, "X"), (out, "out"), (scales, "scales")):
+        _dev_tensor(t, nm)
     _check("spl_quantize_rows_i8", L.spl_quantize_rows_i8(_ptr(X), _TORCH_DTYPE[X.dtype], M, K, _ptr(out),
                                                           _ptr(scales), _stream(stream)))
     return out, scales
@@ -432,11 +508,12 @@ def sparse_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wqc: SparseMatr
                        stream=None) -> torch.Tensor:
     """fp16 Y = dequant(int32 Xq (Wq . Mask)^T) with per-token and per-channel scales."""
     L = lib()
-    for t, nm in ((Xq, "Xq"), (x_scales, "x_scales"), (w_scales, "w_scales")):
-        _dev_tensor(t, nm)
-    M = Xq.shape[0]
+    M = _rows_of(Xq, "Xq")
+    _q_args(Xq, x_scales, Wqc.rows, Wqc.cols, w_scales, M, device=False)
     if out is None:
         out = torch.empty((M, Wqc.rows), dtype=torch.float16, device=Xq.device)
+    _q_outs(out, acc_out, M, Wqc.rows)
+    _q_args(Xq, x_scales, Wqc.rows, Wqc.cols, w_scales, M)
     view = Wqc.view()
     _check("spl_sparse_linear_int8", L.spl_sparse_linear_int8(_ptr(Xq), _ptr(x_scales), M, ctypes.byref(view),
                                                               _ptr(w_scales), _ptr(out), _ptr(acc_out),
@@ -448,12 +525,16 @@ def dense_linear(X: torch.Tensor, W: torch.Tensor, out: torch.Tensor | None = No
                  stream=None) -> torch.Tensor:
     """Dense comparator: Y = X W^T with the same kernel families."""
     L = lib()
-    _dev_tensor(X, "X")
-    _dev_tensor(W, "W")
-    M, K = X.shape
-    N = W.shape[0]
+    M = _rows_of(X, "X")
+    _rows_of(W, "W")
+    N, K = W.shape
+    _arg(X, "X", shape=(M, K), dtype=W.dtype, device=False)
+    _arg(W, "W", shape=(N, K), device=False)
     if out is None:
         out = torch.empty((M, N), dtype=X.dtype, device=X.device)
+    _arg(out, "out", shape=(M, N), dtype=W.dtype)
+    _dev_tensor(X, "X")
+    _dev_tensor(W, "W")
     _check("spl_dense_linear_ex", L.spl_dense_linear_ex(_ptr(X), M, _ptr(W), _TORCH_DTYPE[W.dtype], N, K,
                                                         _ptr(out), ALGO[algo], _stream(stream)))
     return out
@@ -463,10 +544,16 @@ def dense_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wq: torch.Tensor
                       out: torch.Tensor | None = None, acc_out: torch.Tensor | None = None,
                       stream=None) -> torch.Tensor:
     L = lib()
-    M, K = Xq.shape
-    N = Wq.shape[0]
+    M = _rows_of(Xq, "Xq")
+    _rows_of(Wq, "Wq")
+    N, K = Wq.shape
+    _arg(Wq, "Wq", shape=(N, K), dtype=torch.int8, device=False)
+    _q_args(Xq, x_scales, N, K, w_scales, M, device=False)
     if out is None:
         out = torch.empty((M, N), dtype=torch.float16, device=Xq.device)
+    _q_outs(out, acc_out, M, N)
+    _dev_tensor(Wq, "Wq")
+    _q_args(Xq, x_scales, N, K, w_scales, M)
     _check("spl_dense_linear_int8", L.spl_dense_linear_int8(_ptr(Xq), _ptr(x_scales), M, _ptr(Wq),
                                                             _ptr(w_scales), N, K, _ptr(out), _ptr(acc_out),
                                                             _stream(stream)))
@@ -480,15 +567,21 @@ def sparse_linear_group(Xs, Wcs, outs=None, algo: str = "auto", stream=None):
     n = len(Xs)
     if n != len(Wcs) or not 1 <= n <= MAX_GROUP:
         raise ValueError("need 1..MAX_GROUP (X, W) pairs")
-    M = Xs[0].shape[0]
+    M = _rows_of(Xs[0], "X")
     if outs is None:
         outs = [torch.empty((M, W.rows), dtype=X.dtype, device=X.device) for X, W in zip(Xs, Wcs)]
+    if len(outs) != n:
+        raise ValueError("one output per layer")
     views = [W.view() for W in Wcs]
     tasks = (_SparseTask * n)()
     for i, (X, W, Y) in enumerate(zip(Xs, Wcs, outs)):
-        _dev_tensor(X, "X")
-        if X.shape[0] != M or X.dtype != W.dtype or Y.dtype != X.dtype:
+        if W.dtype != Wcs[0].dtype:
             raise ValueError("every layer of a group shares M and the fp16/bf16 dtype")
+        _arg(X, "X", shape=(M, W.cols), dtype=W.dtype, device=False)
+        _arg(Y, "out", shape=(M, W.rows), dtype=W.dtype, device=False)
+    for i, (X, W, Y) in enumerate(zip(Xs, Wcs, outs)):
+        _dev_tensor(X, "X")
+        _dev_tensor(Y, "out")
         tasks[i].X = X.data_ptr()
         tasks[i].W = ctypes.pointer(views[i])
         tasks[i].Y = Y.data_ptr()
@@ -502,15 +595,22 @@ def dense_linear_group(Xs, Ws, outs=None, algo: str = "auto", stream=None):
     n = len(Xs)
     if n != len(Ws) or not 1 <= n <= MAX_GROUP:
         raise ValueError("need 1..MAX_GROUP (X, W) pairs")
-    M = Xs[0].shape[0]
+    M = _rows_of(Xs[0], "X")
     if outs is None:
         outs = [torch.empty((M, W.shape[0]), dtype=X.dtype, device=X.device) for X, W in zip(Xs, Ws)]
+    if len(outs) != n:
+        raise ValueError("one output per layer")
     tasks = (_DenseTask * n)()
     for i, (X, W, Y) in enumerate(zip(Xs, Ws, outs)):
-        _dev_tensor(X, "X")
-        _dev_tensor(W, "W")
-        if X.shape[0] != M or X.dtype != W.dtype or Y.dtype != X.dtype:
+        _rows_of(W, "W")
+        if W.dtype != Xs[0].dtype:
             raise ValueError("every layer of a group shares M and the fp16/bf16 dtype")
+        _arg(W, "W", device=False)
+        _arg(X, "X", shape=(M, W.shape[1]), dtype=W.dtype, device=False)
+        _arg(Y, "out", shape=(M, W.shape[0]), dtype=W.dtype, device=False)
+    for i, (X, W, Y) in enumerate(zip(Xs, Ws, outs)):
+        for t, nm in ((X, "X"), (W, "W"), (Y, "out")):
+            _dev_tensor(t, nm)
         tasks[i].X = X.data_ptr()
         tasks[i].W = W.data_ptr()
         tasks[i].N, tasks[i].K = W.shape
@@ -527,17 +627,20 @@ def sparse_linear_int8_group(Xqs, x_scales, Wqcs, w_scales, outs=None, acc_outs=
     n = len(Xqs)
     if not (n == len(x_scales) == len(Wqcs) == len(w_scales)) or not 1 <= n <= MAX_GROUP:
         raise ValueError("need 1..MAX_GROUP (Xq, x_scales, Wq, w_scales) tuples")
-    M = Xqs[0].shape[0]
+    M = _rows_of(Xqs[0], "Xq")
     if outs is None:
         outs = [torch.empty((M, W.rows), dtype=torch.float16, device=X.device) for X, W in zip(Xqs, Wqcs)]
     accs = acc_outs if acc_outs is not None else [None] * n
+    if len(outs) != n or len(accs) != n:
+        raise ValueError("one output per layer")
     views = [W.view() for W in Wqcs]
     tasks = (_Int8Task * n)()
     for i in range(n):
-        for t, nm in ((Xqs[i], "Xq"), (x_scales[i], "x_scales"), (w_scales[i], "w_scales")):
-            _dev_tensor(t, nm)
-        if Xqs[i].shape[0] != M:
-            raise ValueError("every layer of a group shares M")
+        _q_args(Xqs[i], x_scales[i], Wqcs[i].rows, Wqcs[i].cols, w_scales[i], M, device=False)
+        _q_outs(outs[i], accs[i], M, Wqcs[i].rows, device=False)
+    for i in range(n):
+        _q_args(Xqs[i], x_scales[i], Wqcs[i].rows, Wqcs[i].cols, w_scales[i], M)
+        _q_outs(outs[i], accs[i], M, Wqcs[i].rows)
         tasks[i].Xq, tasks[i].x_scales = Xqs[i].data_ptr(), x_scales[i].data_ptr()
         tasks[i].Wq = ctypes.pointer(views[i])
         tasks[i].w_scales, tasks[i].Y = w_scales[i].data_ptr(), outs[i].data_ptr()
@@ -552,16 +655,22 @@ def dense_linear_int8_group(Xqs, x_scales, Wqs, w_scales, outs=None, acc_outs=No
     n = len(Xqs)
     if not (n == len(x_scales) == len(Wqs) == len(w_scales)) or not 1 <= n <= MAX_GROUP:
         raise ValueError("need 1..MAX_GROUP (Xq, x_scales, Wq, w_scales) tuples")
-    M = Xqs[0].shape[0]
+    M = _rows_of(Xqs[0], "Xq")
     if outs is None:
         outs = [torch.empty((M, W.shape[0]), dtype=torch.float16, device=X.device) for X, W in zip(Xqs, Wqs)]
     accs = acc_outs if acc_outs is not None else [None] * n
+    if len(outs) != n or len(accs) != n:
+        raise ValueError("one output per layer")
     tasks = (_DenseInt8Task * n)()
     for i in range(n):
-        for t, nm in ((Xqs[i], "Xq"), (x_scales[i], "x_scales"), (Wqs[i], "Wq"), (w_scales[i], "w_scales")):
-            _dev_tensor(t, nm)
-        if Xqs[i].shape[0] != M:
-            raise ValueError("every layer of a group shares M")
+        _rows_of(Wqs[i], "Wq")
+        _arg(Wqs[i], "Wq", dtype=torch.int8, device=False)
+        _q_args(Xqs[i], x_scales[i], Wqs[i].shape[0], Wqs[i].shape[1], w_scales[i], M, device=False)
+        _q_outs(outs[i], accs[i], M, Wqs[i].shape[0], device=False)
+    for i in range(n):
+        _dev_tensor(Wqs[i], "Wq")
+        _q_args(Xqs[i], x_scales[i], Wqs[i].shape[0], Wqs[i].shape[1], w_scales[i], M)
+        _q_outs(outs[i], accs[i], M, Wqs[i].shape[0])
         tasks[i].Xq, tasks[i].x_scales, tasks[i].Wq = Xqs[i].data_ptr(), x_scales[i].data_ptr(), Wqs[i].data_ptr()
         tasks[i].w_scales, tasks[i].Y = w_scales[i].data_ptr(), outs[i].data_ptr()
         tasks[i].N, tasks[i].K = Wqs[i].shape

@@ -85,28 +85,10 @@ struct Mfma16<F16> {
   }
 };
 
-// v_perm_b32 selector for the two 16-bit elements (2h, 2h+1) of a 4-column
-// nibble whose stored values sit, in order, in the 8 source bytes {hi:lo}:
-// a kept element takes the two bytes of its rank, a dropped one 0x0C (zero).
-__device__ __forceinline__ uint32_t nibble_selector(uint32_t nib, int h) {
-  uint32_t sel = 0;
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int j = 2 * h + e;
-    uint32_t s16 = 0x0C0Cu;
-    if ((nib >> j) & 1u) {
-      const uint32_t r = __popc(nib & ((1u << j) - 1u));
-      s16 = (2u * r) | ((2u * r + 1u) << 8);
-    }
-    sel |= s16 << (16 * e);
-  }
-  return sel;
-}
-
 // Entry n expands a 4-column nibble n into two operand dwords.  16 entries of
 // 8 bytes cover 32 LDS banks once, so lookups never conflict.
 __device__ __forceinline__ void build_nibble_table(u32x2* lut) {
-  if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{nibble_selector(threadIdx.x, 0), nibble_selector(threadIdx.x, 1)};
+  if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{nibble_selector16(threadIdx.x, 0), nibble_selector16(threadIdx.x, 1)};
 }
 
 // This wave's contiguous range of k-steps [*beg, *end) of S (W waves).
@@ -789,17 +771,11 @@ constexpr size_t kXLdsAlloc = (size_t)kXLdsMax + 16 * 16;   // the most x_lds_by
 template <int W>
 constexpr size_t red_bytes() { return (size_t)W * 2 * 256 * sizeof(float); }
 
-// Raise a kernel's dynamic LDS limit once (above the 64 KB default).
-template <class F>
-hipError_t allow_lds(F* kernel, size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)bytes);
-}
-
 template <class T, int MT, bool XL, int W>
 hipError_t sparse_group_launch(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
   auto* kernel = k_sparse_decode<T, MT, XL, W>;
-  static const hipError_t attr = allow_lds(kernel, sparse_vbuf_bytes<W>() + (XL ? kXLdsAlloc : 0));   // an upper bound
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, sparse_vbuf_bytes<W>() + (XL ? kXLdsAlloc : 0));   // a bound
   if (attr != hipSuccess) return attr;
   const size_t lds = sparse_vbuf_bytes<W>() + (XL ? x_lds_bytes(g.M, kmax) : 0);
   hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(W * kWave), lds, s, g);
@@ -809,7 +785,8 @@ hipError_t sparse_group_launch(const SparseGroupArg& g, int64_t kmax, hipStream_
 template <class T, int MT, bool XL, int W>
 hipError_t dense_group_launch(const DenseGroupArg& g, int64_t kmax, hipStream_t s) {
   auto* kernel = k_dense_decode<T, MT, XL, W>;
-  static const hipError_t attr = allow_lds(kernel, red_bytes<W>() > kXLdsAlloc ? red_bytes<W>() : kXLdsAlloc);
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, red_bytes<W>() > kXLdsAlloc ? red_bytes<W>() : kXLdsAlloc);
   if (attr != hipSuccess) return attr;
   const size_t xb = XL ? x_lds_bytes(g.M, kmax) : 0;
   const size_t lds = xb > red_bytes<W>() ? xb : red_bytes<W>();
@@ -825,19 +802,8 @@ int variant(int64_t M, int64_t kmax, int64_t budget) {
   return M <= 16 ? 1 : 2;
 }
 
-
-
 // 16 waves per workgroup when the launch has fewer than two row blocks per CU.
-bool small_grid(int64_t blocks) {
-  static int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                                   hipSuccess || n <= 0)
-      n = 256;
-    return n;
-  }();
-  return blocks < 2 * (int64_t)cus;
-}
+bool small_grid(int64_t blocks) { return blocks < 2 * (int64_t)device_cus(); }
 
 // Activation path of the sparse kernels.  One row: staged in LDS when it fits
 // (32 KB).  Two to 16 rows: staged only where the launch has two or more row
@@ -868,7 +834,8 @@ hipError_t sparse_pair_launch(const SparseGroupArg& g1, hipStream_t s) {
   for (int i = 0; i < g.count; ++i)
     g.first[i + 1] = g.first[i] + (int32_t)((tile_blocks(g1.t[i].N) + 1) / 2);
   auto* kernel = k_sparse_decode2<T, W, false>;
-  static const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>());
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, sparse2_vbuf_bytes<W>());
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(kernel, dim3((unsigned)g.first[g.count]), dim3(W * kWave), sparse2_vbuf_bytes<W>(), s, g);
   return hipGetLastError();
@@ -945,7 +912,9 @@ hipError_t launch_gated_decode(const void* X, int64_t M, const spl_matrix& Wg, c
   auto* kernel = Wg.dtype == SPL_BF16 ? (xl ? k_sparse_decode2<Bf16, W, true, true> : k_sparse_decode2<Bf16, W, true>)
                                       : (xl ? k_sparse_decode2<F16, W, true, true> : k_sparse_decode2<F16, W, true>);
   const size_t lds = sparse2_vbuf_bytes<W>() + (xl ? x_lds_bytes(1, Wg.cols) : 0);
-  const hipError_t attr = allow_lds(kernel, sparse2_vbuf_bytes<W>() + kXLdsMax);     // an upper bound
+  static PerDeviceFlag lds_set[4];                                                 // one per kernel above
+  const hipError_t attr = allow_lds_once(lds_set[(Wg.dtype == SPL_BF16 ? 2 : 0) + (xl ? 1 : 0)], kernel,
+                                         sparse2_vbuf_bytes<W>() + kXLdsMax);         // an upper bound
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(kernel, dim3((unsigned)B), dim3(W * kWave), lds, s, g);
   return hipGetLastError();

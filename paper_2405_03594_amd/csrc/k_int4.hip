@@ -25,15 +25,6 @@ namespace spl {
 namespace {
 
 
-// v_perm_b32 selector for one 4-column nibble: byte j takes byte
-// popcount(nib & ((1 << j) - 1)) of the source if bit j is set, else 12 (zero).
-__device__ __forceinline__ uint32_t i4_nibble_selector(uint32_t nib) {
-  uint32_t sel = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) sel |= (((nib >> j) & 1u) ? (uint32_t)__popc(nib & ((1u << j) - 1u)) : 0x0Cu) << (8 * j);
-  return sel;
-}
-
 // Four nibbles (bits 0-15) -> four sign-extended bytes.
 __device__ __forceinline__ uint32_t i4_widen(uint32_t w) {
   uint32_t y = (w & 0xFu) | ((w & 0xF0u) << 4) | ((w & 0xF00u) << 8) | ((w & 0xF000u) << 12);
@@ -47,14 +38,19 @@ __device__ __forceinline__ i32x4 mfma_i8_i4(u32x4 a, u32x4 b, i32x4 c) {
 }
 
 __global__ void __launch_bounds__(256) k_pack_nibbles(const int8_t* __restrict__ v8, int64_t nnz,
-                                                      uint8_t* __restrict__ v4) {
+                                                      uint8_t* __restrict__ v4, int32_t* __restrict__ bad) {
   const int64_t nb = (nnz + 1) / 2;
+  int32_t outside = 0;   // codes of this thread outside [-8, 7]
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nb; i += (int64_t)gridDim.x * 256) {
-    const uint32_t lo = (uint32_t)(uint8_t)v8[2 * i] & 0xFu;
-    const uint32_t hi = 2 * i + 1 < nnz ? ((uint32_t)(uint8_t)v8[2 * i + 1] & 0xFu) : 0u;
-    v4[i] = (uint8_t)(lo | (hi << 4));
+    const int32_t a = v8[2 * i];
+    const int32_t b = 2 * i + 1 < nnz ? (int32_t)v8[2 * i + 1] : 0;
+    outside += (a < -8 || a > 7) + (b < -8 || b > 7);
+    v4[i] = (uint8_t)(((uint32_t)a & 0xFu) | (((uint32_t)b & 0xFu) << 4));
   }
+  if (bad && outside) atomicAdd(bad, outside);
 }
+
+__global__ void k_clear_count(int32_t* c) { *c = 0; }
 
 struct I4Args {
   const int8_t* Xq;          // [M][K]
@@ -74,7 +70,7 @@ __global__ void __launch_bounds__(W * 64) k_sparse_i4(const I4Args g) {
   __shared__ i32x4 part[W][64];
   __shared__ uint32_t sel4[16];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
-  if (threadIdx.x < 16) sel4[threadIdx.x] = i4_nibble_selector(threadIdx.x);
+  if (threadIdx.x < 16) sel4[threadIdx.x] = nibble_selector8(threadIdx.x);
   __syncthreads();
   const int64_t b = blockIdx.x;
   const int S = (int)tile_steps(g.K);
@@ -139,13 +135,14 @@ __global__ void __launch_bounds__(W * 64) k_sparse_i4(const I4Args g) {
 
 }  // namespace
 
-int64_t int4_values_bytes(int64_t nnz) { return ((nnz + 1) / 2 + 16 + 15) / 16 * 16; }
+int64_t int4_values_bytes(int64_t nnz) { return spl_values_bytes(SPL_I4, nnz); }
 
-hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, hipStream_t s) {
+hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, int32_t* bad, hipStream_t s) {
   int64_t blocks = ((nnz + 1) / 2 + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_pack_nibbles, dim3((unsigned)blocks), dim3(256), 0, s, v8, nnz, v4);
+  if (bad) hipLaunchKernelGGL(k_clear_count, dim3(1), dim3(1), 0, s, bad);
+  hipLaunchKernelGGL(k_pack_nibbles, dim3((unsigned)blocks), dim3(256), 0, s, v8, nnz, v4, bad);
   return hipGetLastError();
 }
 
@@ -154,14 +151,7 @@ hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, cons
   I4Args g{Xq, sx, W4.bitmask, static_cast<const uint8_t*>(W4.values), W4.tile_offsets, sw,
            static_cast<uint16_t*>(Y), acc_out, W4.rows, W4.cols, (int32_t)M};
   const int64_t blocks = tile_blocks(W4.rows);
-  static const int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                                   hipSuccess || n <= 0)
-      n = 256;
-    return n;
-  }();
-  if (blocks < 2 * (int64_t)cus)
+  if (blocks < 2 * (int64_t)device_cus())
     hipLaunchKernelGGL(k_sparse_i4<16>, dim3((unsigned)blocks), dim3(16 * 64), 0, s, g);
   else
     hipLaunchKernelGGL(k_sparse_i4<8>, dim3((unsigned)blocks), dim3(8 * 64), 0, s, g);

@@ -45,20 +45,6 @@ __device__ __forceinline__ i32x4 mfma_i8(u32x4 a, u32x4 b, i32x4 c) {
                                                0);
 }
 
-// v_perm_b32 selector that expands one 4-column nibble of 1-byte values: byte
-// j takes the value of rank popcount(nib & ((1 << j) - 1)) if bit j is set,
-// else selector 12 (a zero byte).
-__device__ __forceinline__ uint32_t i8_nibble_selector(uint32_t nib) {
-  uint32_t sel = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    uint32_t b = 0x0Cu;
-    if ((nib >> j) & 1u) b = __popc(nib & ((1u << j) - 1u));
-    sel |= b << (8 * j);
-  }
-  return sel;
-}
-
 // Combine the waves' int32 partial sums and run the epilogue.
 // part: [W][MT][4][64] int32 in LDS; output (f, r, l): n = n0 + 4*(l/16) + r, m = m0 + 16 f + l%16.
 template <int MT, int W>
@@ -237,7 +223,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_int8(const I8G
     ch = shape(orng, kbeg);
     issue(ch, kbeg);
   }
-  if (threadIdx.x < 16) lut[threadIdx.x] = i8_nibble_selector(threadIdx.x);
+  if (threadIdx.x < 16) lut[threadIdx.x] = nibble_selector8(threadIdx.x);
   if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
   if constexpr (XL) i8_stage_x<W>(xs, Xq, (int)M, K);
   __syncthreads();
@@ -409,9 +395,8 @@ hipError_t sparse_int8_launch(const I8GroupArg& g, int64_t kmax, hipStream_t s) 
   const size_t region = (size_t)W * kI8VBufAlloc > (size_t)W * MT * 1024 ? (size_t)W * kI8VBufAlloc
                                                                           : (size_t)W * MT * 1024;
   const size_t xbytes = XL ? (size_t)g.M * (size_t)i8_xs_stride(kmax) : 0;
-  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                     (int)(region + (XL ? kI8XLdsMax + 16 * 16 : 0)));
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, region + (XL ? kI8XLdsMax + 16 * 16 : 0));
   if (attr != hipSuccess) return attr;
   const dim3 grid((unsigned)g.first[g.count], (unsigned)((g.M + 16 * MT - 1) / (16 * MT)));
   hipLaunchKernelGGL(kernel, grid, dim3(W * kWave), region + xbytes, s, g);
@@ -508,16 +493,7 @@ void quantize_rows_launch(const uint16_t* x, int64_t M, int64_t K, int8_t* Xq, f
     hipLaunchKernelGGL((k_quantize_rows<T, 0>), grid, block, 0, s, x, K, Xq, sx);
 }
 
-bool i8_small_grid(int64_t blocks) {
-  static int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                                   hipSuccess || n <= 0)
-      n = 256;
-    return n;
-  }();
-  return blocks < 2 * (int64_t)cus;
-}
+bool i8_small_grid(int64_t blocks) { return blocks < 2 * (int64_t)device_cus(); }
 
 }  // namespace
 

@@ -11,6 +11,14 @@
 // retile16   : row layout -> tile layout (16 x 32 submatrices, paper section
 //              2.4.2): per-tile counts and a scan give the tile offsets, then one
 //              wave per row moves each word's values to their tile position.
+// pack into the tile layout straight from W and the mask: per-tile counts and
+//              the same scan, then one wave per tile, lane (row, column group)
+//              in the order the tile stores its values, writes its kept values
+//              at the exclusive wave scan of the lanes' counts and its byte(s) of
+//              the row's bitmask word.
+// validate   : the consistency of a compressed matrix (offsets against the
+//              popcounts of the bitmask, first and last offsets, zero pad bits),
+//              reported as error bits in a device word.
 #include "spl_common.h"
 
 namespace spl {
@@ -279,6 +287,129 @@ __global__ void __launch_bounds__(256) k_unpack_tiled(const uint32_t* __restrict
   }
 }
 
+
+// ---- pack straight into the tile layout ----
+
+// Thread (tile t, row r): the kept count of its 32 columns, summed per tile.
+template <int EB>
+__global__ void __launch_bounds__(256) k_tile_count_direct(const void* W, const uint8_t* mask, int64_t N, int64_t K,
+                                                           int32_t* __restrict__ counts) {
+  const int64_t S = tile_steps(K);
+  const int64_t T = tile_blocks(N) * S;
+  const int64_t t = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int r = threadIdx.x & 15;
+  uint32_t c = 0;
+  if (t < T) {
+    const int64_t b = t / S, s = t - b * S;
+    const int64_t n = 16 * b + r;
+    if (n < N) {
+      const int64_t k0 = 32 * s;
+      const int64_t k1 = k0 + 32 < K ? k0 + 32 : K;
+      for (int64_t k = k0; k < k1; ++k) c += is_kept<EB>(W, mask, n * K + k) ? 1u : 0u;
+    }
+  }
+  for (int off = 8; off > 0; off >>= 1) c += __shfl_xor(c, off, 16);
+  if (t < T && r == 0) counts[t] = (int32_t)c;
+}
+
+// One wave per tile.  Lane (fr, g) covers row fr and the G = 16 / EB columns
+// of group g (EB = 2: 64 lanes, 4 groups of 8; EB = 1: 32 lanes, 2 groups of
+// 16), which is the order of the tile's values, so the lane's first value sits
+// at the exclusive scan of the lanes' counts.  It writes its kept values in
+// column order and its G bits of the row's bitmask word (byte g, or half-word
+// g for int8), zero for rows >= N and columns >= K.
+template <int EB>
+__global__ void __launch_bounds__(256) k_tile_scatter_direct(const void* W, const uint8_t* mask, int64_t N,
+                                                             int64_t K, const int32_t* __restrict__ tile_offsets,
+                                                             uint32_t* __restrict__ bm_tiles, void* __restrict__ values) {
+  constexpr int G = 16 / EB;
+  constexpr int kLanes = 16 * (32 / G);
+  const int64_t S = tile_steps(K);
+  const int64_t T = tile_blocks(N) * S;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;                                    // wave-uniform
+  const int lane = threadIdx.x & 63;
+  const int fr = lane & 15, g = lane >> 4;
+  const int64_t b = t / S, s = t - b * S;
+  const int64_t n = 16 * b + fr;
+  const int64_t k0 = 32 * s + (int64_t)G * g;
+  uint32_t bits = 0;
+  if (lane < kLanes && n < N) {
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+      if (k0 + j < K && is_kept<EB>(W, mask, n * K + k0 + j)) bits |= 1u << j;
+  }
+  const uint32_t c = __popc(bits);
+  uint32_t incl = c;
+  for (int d = 1; d < kWave; d <<= 1) {
+    const uint32_t up = __shfl_up(incl, d);
+    if (lane >= d) incl += up;
+  }
+  int64_t dst = (int64_t)tile_offsets[t] + (incl - c);
+  if (lane < kLanes) {
+    unsigned char* wb = reinterpret_cast<unsigned char*>(bm_tiles + t * 16 + fr);
+    if constexpr (EB == 2) {
+      wb[g] = (unsigned char)bits;
+    } else {
+      *reinterpret_cast<uint16_t*>(wb + 2 * g) = (uint16_t)bits;
+    }
+    for (int j = 0; j < G; ++j) {
+      if ((bits >> j) & 1u) {
+        if constexpr (EB == 2) {
+          static_cast<uint16_t*>(values)[dst] = static_cast<const uint16_t*>(W)[n * K + k0 + j];
+        } else {
+          static_cast<int8_t*>(values)[dst] = static_cast<const int8_t*>(W)[n * K + k0 + j];
+        }
+        ++dst;
+      }
+    }
+  }
+}
+
+// ---- format check ----
+
+// Error bits of spl_validate.
+constexpr uint32_t kBadCount = 1u;     // offsets[i+1] - offsets[i] != kept count of block i
+constexpr uint32_t kBadEnds = 2u;      // offsets[0] != 0 or offsets[last] != nnz
+constexpr uint32_t kBadPad = 4u;       // a bit set past column K or (tile layout) in a row >= N
+
+// Thread per block (a row, or a tile): its popcount against its offsets, its pad bits.
+__global__ void __launch_bounds__(256) k_validate(const uint32_t* __restrict__ bitmask,
+                                                  const int32_t* __restrict__ offsets, int64_t N, int64_t K,
+                                                  int64_t nnz, int tiled, uint32_t* __restrict__ err) {
+  const int64_t S = tile_steps(K);
+  const int64_t blocks = tiled ? tile_blocks(N) * S : N;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i > blocks) return;
+  uint32_t e = 0;
+  if (i == blocks) {
+    if (offsets[0] != 0 || (int64_t)offsets[blocks] != nnz) e |= kBadEnds;
+  } else {
+    const uint32_t tail = (uint32_t)(K - 32 * (S - 1));                  // columns of the last 32-column step
+    const uint32_t tailmask = tail >= 32 ? 0xffffffffu : ((1u << tail) - 1u);
+    int64_t c = 0;
+    if (tiled) {
+      const int64_t b = i / S, s = i - b * S;
+#pragma unroll 4
+      for (int r = 0; r < 16; ++r) {
+        const uint32_t w = bitmask[i * 16 + r];
+        c += __popc(w);
+        if ((16 * b + r >= N && w) || (s == S - 1 && (w & ~tailmask))) e |= kBadPad;
+      }
+    } else {
+      for (int64_t s = 0; s < S; ++s) {
+        const uint32_t w = bitmask[i * S + s];
+        c += __popc(w);
+        if (s == S - 1 && (w & ~tailmask)) e |= kBadPad;
+      }
+    }
+    if ((int64_t)offsets[i + 1] - (int64_t)offsets[i] != c) e |= kBadCount;
+  }
+  if (e) atomicOr(err, e);
+}
+
+__global__ void k_clear_word(uint32_t* w) { *w = 0u; }
+
 }  // namespace
 
 hipError_t launch_retile16(const spl_matrix& in, uint32_t* bitmask_t, void* values_t, int32_t* tile_offsets,
@@ -320,6 +451,40 @@ hipError_t launch_pack_scatter(const void* W, int32_t dtype, const uint8_t* mask
   } else {
     hipLaunchKernelGGL(k_pack_scatter<2>, grid, block, 0, s, W, mask, N, K, row_offsets, bitmask, values);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_count_tiled(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                                   int32_t* tile_offsets, hipStream_t s) {
+  const int64_t T = tile_blocks(N) * tile_steps(K);
+  const dim3 grid((unsigned)((T + 15) / 16)), block(256);
+  if (dtype == SPL_I8) {
+    hipLaunchKernelGGL(k_tile_count_direct<1>, grid, block, 0, s, W, mask, N, K, tile_offsets);
+  } else {
+    hipLaunchKernelGGL(k_tile_count_direct<2>, grid, block, 0, s, W, mask, N, K, tile_offsets);
+  }
+  hipLaunchKernelGGL(k_scan_offsets, dim3(1), dim3(1024), 0, s, tile_offsets, T);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_scatter_tiled(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                                     const int32_t* tile_offsets, uint32_t* bitmask, void* values, hipStream_t s) {
+  const int64_t T = tile_blocks(N) * tile_steps(K);
+  const dim3 grid((unsigned)((T + 3) / 4)), block(256);
+  if (dtype == SPL_I8) {
+    hipLaunchKernelGGL(k_tile_scatter_direct<1>, grid, block, 0, s, W, mask, N, K, tile_offsets, bitmask, values);
+  } else {
+    hipLaunchKernelGGL(k_tile_scatter_direct<2>, grid, block, 0, s, W, mask, N, K, tile_offsets, bitmask, values);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const spl_matrix& Wc, uint32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_clear_word, dim3(1), dim3(1), 0, s, err);
+  const bool tiled = Wc.layout == SPL_LAYOUT_TILE16;
+  const int64_t blocks = tiled ? tile_blocks(Wc.rows) * tile_steps(Wc.cols) : Wc.rows;
+  hipLaunchKernelGGL(k_validate, dim3((unsigned)((blocks + 1 + 255) / 256)), dim3(256), 0, s, Wc.bitmask,
+                     tiled ? Wc.tile_offsets : Wc.row_offsets, Wc.rows, Wc.cols, Wc.nnz, tiled ? 1 : 0, err);
   return hipGetLastError();
 }
 

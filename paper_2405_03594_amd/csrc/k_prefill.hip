@@ -72,39 +72,6 @@ struct MfmaP<I8P> {
   }
 };
 
-// v_perm_b32 selector for the 16-bit elements (2h, 2h+1) of a 4-column nibble
-// whose stored values sit, in order, in the 8 source bytes: a kept element
-// takes the two bytes of its rank, a dropped one 0x0C (a zero byte).
-__device__ __forceinline__ uint32_t pf_nibble_selector(uint32_t nib, int h) {
-  uint32_t sel = 0;
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int j = 2 * h + e;
-    uint32_t s16 = 0x0C0Cu;
-    if ((nib >> j) & 1u) {
-      const uint32_t r = __popc(nib & ((1u << j) - 1u));
-      s16 = (2u * r) | ((2u * r + 1u) << 8);
-    }
-    sel |= s16 << (16 * e);
-  }
-  return sel;
-}
-
-// v_perm_b32 selector for a 4-column nibble of 1-byte values whose stored
-// values start at byte p of an 8-byte window: a kept column takes byte
-// p + rank, a dropped one 0x0C (a zero byte).  p + rank <= 7 (p is the kept
-// count of the nibble before, at most 4).
-__device__ __forceinline__ uint32_t pf_i8_selector(uint32_t nib, uint32_t p) {
-  uint32_t sel = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    uint32_t b = 0x0Cu;
-    if ((nib >> j) & 1u) b = p + __popc(nib & ((1u << j) - 1u));
-    sel |= b << (8 * j);
-  }
-  return sel;
-}
-
 // Rows [r0, r0 + RR P) x columns [k0, k0 + 64) of a row-major [R][K] matrix,
 // moved through registers by a group of 8 RR threads: thread t holds rows
 // r0 + t/8 + RR i (i < P), columns k0 + 8 (t % 8) .. +8.  Checked fetches
@@ -376,11 +343,11 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
   const uint32_t* __restrict__ bm_tiles = gm ? g.bm2 : g.bm;
   const int32_t* __restrict__ tile_offsets = gm ? g.toff2 : g.toff;
   if constexpr (kI8) {
-    if (threadIdx.x < 80) lut[threadIdx.x] = pf_i8_selector(threadIdx.x / 5, threadIdx.x % 5);
+    if (threadIdx.x < 80) lut[threadIdx.x] = nibble_selector8(threadIdx.x / 5, threadIdx.x % 5);
   } else {
     if (threadIdx.x < 16) {
-      lut[2 * threadIdx.x] = pf_nibble_selector(threadIdx.x, 0);
-      lut[2 * threadIdx.x + 1] = pf_nibble_selector(threadIdx.x, 1);
+      lut[2 * threadIdx.x] = nibble_selector16(threadIdx.x, 0);
+      lut[2 * threadIdx.x + 1] = nibble_selector16(threadIdx.x, 1);
     }
   }
 
@@ -619,22 +586,7 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(c
   }
 }
 
-// Raise a kernel's dynamic LDS limit (above the 64 KB default) once.
-template <class F>
-hipError_t pf_allow_lds(F* kernel, int bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-}
-
-int pf_cus() {
-  static const int cus = [] {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) !=
-                                                 hipSuccess || n <= 0)
-      return 256;
-    return n;
-  }();
-  return cus;
-}
+int pf_cus() { return device_cus(); }
 
 // Workgroup tile of a launch: 128 x 256 (8 waves) when that still gives every
 // CU a workgroup, else 64 x 128 (4 waves, four times as many workgroups).
@@ -652,7 +604,8 @@ constexpr bool pf_inside(int64_t N, int64_t M, int64_t K, int BN, int BM) {
 template <class T, int BN, int BM, int NW, int KS, bool kChecked, bool kGated = false>
 hipError_t sparse_prefill_launch(const PfArgs& a, hipStream_t s) {
   auto* kernel = k_sparse_prefill<T, BN, BM, NW, KS, kChecked, kGated>;
-  static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
   constexpr int RN = kGated ? BN / 2 : BN;            // real rows per workgroup
   const dim3 grid((unsigned)((a.N + RN - 1) / RN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
@@ -694,7 +647,8 @@ hipError_t gated_prefill_t(const PfArgs& a, hipStream_t s) {
 template <class T, int BN, int BM, int NW, int KS, bool kChecked>
 hipError_t dense_prefill_launch(const PfArgs& a, hipStream_t s) {
   auto* kernel = k_dense_prefill<T, BN, BM, NW, KS, kChecked>;
-  static const hipError_t attr = pf_allow_lds(kernel, KS * pf_lds(BN, BM));
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
   const dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
   hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, a);

@@ -163,9 +163,8 @@ hipError_t launch_magnitude_mask(const uint16_t* W, int64_t n, uint32_t prune, u
   chunks = (n + chunk - 1) / chunk;
   hipError_t e = launch_zero_fill(hist, 2 * kBins, s);
   if (e != hipSuccess) return e;
-  static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(k_mag_hist),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                     kBins * (int)sizeof(uint32_t));
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, k_mag_hist, kBins * sizeof(uint32_t));
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(k_mag_hist, dim3((unsigned)chunks), dim3(kPrThreads), kBins * sizeof(uint32_t), s, W, n, chunk,
                      hist);

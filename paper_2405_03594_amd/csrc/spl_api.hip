@@ -2,6 +2,9 @@
 // launches on the caller's stream.  No entry point allocates device memory.
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "spl.h"
 #include "spl_common.h"
 
@@ -60,12 +63,18 @@ const char* spl_status_string(spl_status s) {
 spl_status spl_read_probe(const void* buf, int64_t bytes, uint32_t* sink, hipStream_t stream) {
   if (!buf || !sink || bytes <= 0 || bytes % 16 != 0 || !aligned(buf, 16) || !aligned(sink, 4))
     return SPL_ERR_INVALID_ARG;
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    return SPL_ERR_DEVICE;
   (void)hipGetLastError();
-  return launched(spl::launch_read_probe(buf, bytes, sink, cus, stream));
+  return launched(spl::launch_read_probe(buf, bytes, sink, spl::device_cus(), stream));
+}
+
+int64_t spl_values_bytes(int32_t dtype, int64_t nnz) {
+  if (nnz < 0 || nnz >= kMaxDim) return 0;
+  int64_t payload = 0;
+  if (dtype == SPL_F16 || dtype == SPL_BF16) payload = 2 * nnz;
+  else if (dtype == SPL_I8) payload = nnz;
+  else if (dtype == SPL_I4) payload = (nnz + 1) / 2;
+  else return 0;
+  return (payload + 15) / 16 * 16 + 16;
 }
 
 spl_status spl_check_matrix(const spl_matrix* Wc) {
@@ -79,7 +88,7 @@ spl_status spl_check_matrix(const spl_matrix* Wc) {
   if (!Wc->bitmask) return SPL_ERR_INVALID_ARG;
   if (Wc->layout == SPL_LAYOUT_ROWS && !Wc->row_offsets) return SPL_ERR_INVALID_ARG;
   if (Wc->layout == SPL_LAYOUT_TILE16 && !Wc->tile_offsets) return SPL_ERR_INVALID_ARG;
-  if (Wc->nnz > 0 && !Wc->values) return SPL_ERR_INVALID_ARG;
+  if (!Wc->values || Wc->values_bytes < spl_values_bytes(Wc->dtype, Wc->nnz)) return SPL_ERR_INVALID_ARG;
   if (!aligned(Wc->bitmask, 16)) return SPL_ERR_INVALID_ARG;
   if (Wc->row_offsets && !aligned(Wc->row_offsets, 4)) return SPL_ERR_INVALID_ARG;
   if (Wc->tile_offsets && !aligned(Wc->tile_offsets, 4)) return SPL_ERR_INVALID_ARG;
@@ -105,15 +114,19 @@ spl_status spl_retile16(const spl_matrix* rows_in, uint32_t* bitmask_out, void* 
   return launched(spl::launch_retile16(*rows_in, bitmask_out, values_out, tile_offsets_out, stream));
 }
 
-spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
-                          int32_t* row_offsets, int64_t* h_nnz, hipStream_t stream) {
-  if (!W || !row_offsets || !h_nnz) return SPL_ERR_INVALID_ARG;
+spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K, int32_t layout,
+                          int32_t* offsets, int64_t* h_nnz, hipStream_t stream) {
+  if (!W || !offsets || !h_nnz) return SPL_ERR_INVALID_ARG;
   if (!any_dtype(dtype) || !dims_ok(N, K)) return SPL_ERR_INVALID_ARG;
-  if (!aligned(W, 16) || !aligned(row_offsets, 4)) return SPL_ERR_INVALID_ARG;
+  if (layout != SPL_LAYOUT_ROWS && layout != SPL_LAYOUT_TILE16) return SPL_ERR_INVALID_ARG;
+  if (!aligned(W, 16) || !aligned(offsets, 4)) return SPL_ERR_INVALID_ARG;
+  const int64_t blocks = layout == SPL_LAYOUT_ROWS ? N : spl::tile_blocks(N) * spl::tile_steps(K);
   (void)hipGetLastError();
-  if (spl::launch_pack_count(W, dtype, mask, N, K, row_offsets, stream) != hipSuccess) return SPL_ERR_DEVICE;
+  const hipError_t e = layout == SPL_LAYOUT_ROWS ? spl::launch_pack_count(W, dtype, mask, N, K, offsets, stream)
+                                                 : spl::launch_pack_count_tiled(W, dtype, mask, N, K, offsets, stream);
+  if (e != hipSuccess) return SPL_ERR_DEVICE;
   int32_t total = 0;
-  if (hipMemcpyAsync(&total, row_offsets + N, sizeof(int32_t), hipMemcpyDeviceToHost, stream) != hipSuccess)
+  if (hipMemcpyAsync(&total, offsets + blocks, sizeof(int32_t), hipMemcpyDeviceToHost, stream) != hipSuccess)
     return SPL_ERR_DEVICE;
   if (hipStreamSynchronize(stream) != hipSuccess) return SPL_ERR_DEVICE;
   if (total < 0) return SPL_ERR_OVERFLOW;
@@ -121,14 +134,48 @@ spl_status spl_pack_count(const void* W, int32_t dtype, const uint8_t* mask, int
   return SPL_OK;
 }
 
-spl_status spl_pack_sparse(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
-                           const int32_t* row_offsets, uint32_t* bitmask, void* values, hipStream_t stream) {
-  if (!W || !row_offsets || !bitmask) return SPL_ERR_INVALID_ARG;
+spl_status spl_pack_sparse(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K, int32_t layout,
+                           const int32_t* offsets, uint32_t* bitmask, void* values, hipStream_t stream) {
+  if (!W || !offsets || !bitmask || !values) return SPL_ERR_INVALID_ARG;
   if (!any_dtype(dtype) || !dims_ok(N, K)) return SPL_ERR_INVALID_ARG;
-  if (!aligned(W, 16) || !aligned(bitmask, 16) || !aligned(row_offsets, 4)) return SPL_ERR_INVALID_ARG;
-  if (values && !aligned(values, 16)) return SPL_ERR_INVALID_ARG;
+  if (layout != SPL_LAYOUT_ROWS && layout != SPL_LAYOUT_TILE16) return SPL_ERR_INVALID_ARG;
+  if (!aligned(W, 16) || !aligned(bitmask, 16) || !aligned(offsets, 4) || !aligned(values, 16))
+    return SPL_ERR_INVALID_ARG;
   (void)hipGetLastError();
-  return launched(spl::launch_pack_scatter(W, dtype, mask, N, K, row_offsets, bitmask, values, stream));
+  if (layout == SPL_LAYOUT_TILE16)
+    return launched(spl::launch_pack_scatter_tiled(W, dtype, mask, N, K, offsets, bitmask, values, stream));
+  return launched(spl::launch_pack_scatter(W, dtype, mask, N, K, offsets, bitmask, values, stream));
+}
+
+// The result word of spl_validate: one per device (each device has its own
+// copy of a __device__ variable); its address is looked up once per device.
+__device__ uint32_t g_validate_err;
+
+static uint32_t* validate_word() {
+  static std::atomic<uint32_t*> addr[spl::kMaxDevices];
+  const int dev = spl::current_device();
+  if (dev < 0) return nullptr;
+  uint32_t* p = addr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  void* q = nullptr;
+  if (hipGetSymbolAddress(&q, HIP_SYMBOL(g_validate_err)) != hipSuccess || !q) return nullptr;
+  addr[dev].store(static_cast<uint32_t*>(q), std::memory_order_release);
+  return static_cast<uint32_t*>(q);
+}
+
+spl_status spl_validate(const spl_matrix* Wc, hipStream_t stream) {
+  const spl_status st = spl_check_matrix(Wc);
+  if (st != SPL_OK) return st;
+  static std::mutex one_at_a_time;                 // the word is shared: one validation in flight per process
+  std::lock_guard<std::mutex> hold(one_at_a_time);
+  uint32_t* err = validate_word();
+  if (!err) return SPL_ERR_DEVICE;
+  (void)hipGetLastError();
+  if (spl::launch_validate(*Wc, err, stream) != hipSuccess) return SPL_ERR_DEVICE;
+  uint32_t bits = 0;
+  if (hipMemcpyAsync(&bits, err, sizeof(bits), hipMemcpyDeviceToHost, stream) != hipSuccess) return SPL_ERR_DEVICE;
+  if (hipStreamSynchronize(stream) != hipSuccess) return SPL_ERR_DEVICE;
+  return bits ? SPL_ERR_INVALID_ARG : SPL_OK;
 }
 
 spl_status spl_unpack(const spl_matrix* Wc, void* W_dense, hipStream_t stream) {
@@ -317,22 +364,25 @@ spl_status spl_permute_values(const void* src, const int32_t* perm, int64_t nnz,
 
 int64_t spl_int4_values_bytes(int64_t nnz) { return nnz < 0 ? -1 : spl::int4_values_bytes(nnz); }
 
-spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, hipStream_t stream) {
+spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, int32_t* bad_codes, hipStream_t stream) {
   const spl_status st = spl_check_matrix(W8);
   if (st != SPL_OK) return st;
   if (W8->dtype != SPL_I8 || W8->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
   if (!values4 || !aligned(values4, 16)) return SPL_ERR_INVALID_ARG;
-  if (W8->nnz == 0) return SPL_OK;
+  if (bad_codes && !aligned(bad_codes, 4)) return SPL_ERR_INVALID_ARG;
   (void)hipGetLastError();
-  return launched(spl::launch_pack_nibbles(static_cast<const int8_t*>(W8->values), W8->nnz, values4, stream));
+  return launched(spl::launch_pack_nibbles(static_cast<const int8_t*>(W8->values), W8->nnz, values4, bad_codes,
+                                           stream));
 }
 
 // A SPL_I4 view: the checks of spl_check_matrix with the 4-bit dtype and the tile layout.
 static spl_status check_i4_view(const spl_matrix* W) {
   if (!W) return SPL_ERR_INVALID_ARG;
   if (W->dtype != SPL_I4 || W->layout != SPL_LAYOUT_TILE16) return SPL_ERR_UNSUPPORTED;
+  if (W->values_bytes < spl_values_bytes(SPL_I4, W->nnz)) return SPL_ERR_INVALID_ARG;
   spl_matrix v = *W;
-  v.dtype = SPL_I8;                                   // same scalar and pointer rules
+  v.dtype = SPL_I8;                                   // the same scalar and pointer rules
+  v.values_bytes = spl_values_bytes(SPL_I8, W->nnz);  // (the 4-bit capacity is checked above)
   return spl_check_matrix(&v);
 }
 
@@ -351,7 +401,7 @@ spl_status spl_sparse_linear_int4(const int8_t* Xq, const float* x_scales, int64
   return launched(spl::launch_sparse_int4(Xq, x_scales, M, *W4, w_scales, Y, acc_out, stream));
 }
 
-// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
+// Arguments of one sparse-quantized task (those of spl_sparse_linear_int8).
 static spl_status check_int8_task(const spl_int8_task* t, int64_t M) {
   const spl_status st = spl_check_matrix(t->Wq);
   if (st != SPL_OK) return st;

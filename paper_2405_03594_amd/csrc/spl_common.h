@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "spl.h"
 
 namespace spl {
@@ -94,6 +96,31 @@ __device__ __forceinline__ int find_task(const int32_t* first, int count) {
   return ti;
 }
 
+// v_perm_b32 selectors that expand one 4-column nibble of the bitmask.  The
+// nibble's stored values sit, in order, in the 8 source bytes {hi:lo}; a
+// kept column takes the bytes of its rank among the nibble's set bits, a
+// dropped one selector 0x0C (a zero byte).
+//   selector16: the 16-bit elements (2h, 2h + 1) of the nibble (two bytes each).
+//   selector8: the four 1-byte elements, values starting at byte p (p + rank <= 7).
+__host__ __device__ __forceinline__ uint32_t nibble_rank(uint32_t nib, int j) {
+  return (uint32_t)__builtin_popcount(nib & ((1u << j) - 1u));
+}
+__host__ __device__ __forceinline__ uint32_t nibble_selector16(uint32_t nib, int h) {
+  uint32_t sel = 0;
+  for (int e = 0; e < 2; ++e) {
+    const int j = 2 * h + e;
+    const uint32_t r = nibble_rank(nib, j);
+    const uint32_t s16 = ((nib >> j) & 1u) ? (2u * r) | ((2u * r + 1u) << 8) : 0x0C0Cu;
+    sel |= s16 << (16 * e);
+  }
+  return sel;
+}
+__host__ __device__ __forceinline__ uint32_t nibble_selector8(uint32_t nib, uint32_t p = 0) {
+  uint32_t sel = 0;
+  for (int j = 0; j < 4; ++j) sel |= (((nib >> j) & 1u) ? p + nibble_rank(nib, j) : 0x0Cu) << (8 * j);
+  return sel;
+}
+
 typedef __attribute__((address_space(3))) unsigned char lds_t;
 
 // 32-bit LDS offset of a pointer into shared memory, and loads at such offsets.
@@ -115,6 +142,43 @@ __host__ __device__ __forceinline__ int64_t words_per_row(int64_t K) { return (K
 __host__ __device__ __forceinline__ int64_t tile_blocks(int64_t N) { return (N + 15) / 16; }
 __host__ __device__ __forceinline__ int64_t tile_steps(int64_t K) { return (K + 31) / 32; }
 
+// Host-side facts and settings kept per device: a process may drive several
+// GPUs, so nothing learned with one device current is reused on another.
+constexpr int kMaxDevices = 64;
+
+// The current device, or -1 when it cannot be read or lies past kMaxDevices.
+inline int current_device() {
+  int d = -1;
+  return hipGetDevice(&d) == hipSuccess && d >= 0 && d < kMaxDevices ? d : -1;
+}
+
+// Compute units of the current device (256 when the query fails).
+inline int device_cus() {
+  static std::atomic<int> cache[kMaxDevices];
+  const int d = current_device();
+  if (d < 0) return 256;
+  int n = cache[d].load(std::memory_order_relaxed);
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, d) != hipSuccess || n <= 0) n = 256;
+  cache[d].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+// Raises a kernel's dynamic LDS limit on the current device, once per device;
+// `done` belongs to one kernel (a static at its launch site).
+struct PerDeviceFlag {
+  std::atomic<int> set[kMaxDevices];
+};
+template <class F>
+hipError_t allow_lds_once(PerDeviceFlag& done, F* kernel, size_t bytes) {
+  const int d = current_device();
+  if (d >= 0 && done.set[d].load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess && d >= 0) done.set[d].store(1, std::memory_order_release);
+  return e;
+}
+
 }  // namespace spl
 
 // Launchers implemented in the kernel translation units (host side).
@@ -124,6 +188,13 @@ hipError_t launch_pack_count(const void* W, int32_t dtype, const uint8_t* mask, 
 hipError_t launch_pack_scatter(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
                                const int32_t* row_offsets, uint32_t* bitmask, void* values, hipStream_t s);
 hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s);
+// Pack straight into the tile layout: per-tile counts -> exclusive tile offsets, then bitmask + values.
+hipError_t launch_pack_count_tiled(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                                   int32_t* tile_offsets, hipStream_t s);
+hipError_t launch_pack_scatter_tiled(const void* W, int32_t dtype, const uint8_t* mask, int64_t N, int64_t K,
+                                     const int32_t* tile_offsets, uint32_t* bitmask, void* values, hipStream_t s);
+// Format check of a view: error bits (1 offsets vs popcounts, 2 first/last offset, 4 pad bits) OR-ed into *err.
+hipError_t launch_validate(const spl_matrix& Wc, uint32_t* err, hipStream_t s);
 hipError_t launch_retile16(const spl_matrix& rows_in, uint32_t* bitmask_t, void* values_t, int32_t* tile_offsets,
                            hipStream_t s);
 // Y[0..count16) = +0 (16-bit elements).
@@ -163,7 +234,8 @@ hipError_t launch_transpose_perm(const spl_matrix& W, const spl_matrix& Wt, int3
 hipError_t launch_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t s);
 // 4-bit payloads: nibble packing of int8 tile values and the decode kernel (M <= 16).
 int64_t int4_values_bytes(int64_t nnz);
-hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, hipStream_t s);
+// bad (optional): set to the number of codes outside [-8, 7] (their low 4 bits are stored).
+hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, int32_t* bad, hipStream_t s);
 hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& W4, const float* sw,
                               void* Y, int32_t* acc_out, hipStream_t s);
 // Streaming-read probe over `bytes` (a multiple of 16) of a 16-byte aligned buffer.

@@ -190,6 +190,20 @@ def int4_weight(seed: int, N: int, K: int, sparsity) -> tuple[np.ndarray, np.nda
     return q, mask, sw
 
 
+def int4_weight_full_range(seed: int, N: int, K: int, sparsity) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """int4_weight with the codes' edges planted: every kept code of row 0 and
+    of row N - 1 set to -8 (the one code without a positive twin), row N // 2
+    set to 7, and a seeded eighth of the other kept codes set to -8."""
+    q, mask, sw = int4_weight(seed, N, K, sparsity)
+    q = q.copy()
+    keep = mask.astype(bool)
+    rng = np.random.default_rng(seed ^ 0x1F4B)
+    q[keep & (rng.random(q.shape) < 0.125)] = -8
+    for r, v in ((N // 2, 7), (0, -8), (N - 1, -8)):
+        q[r, keep[r]] = v
+    return q, mask, sw
+
+
 def int8_activations(seed: int, M: int, K: int) -> tuple[np.ndarray, np.ndarray]:
     """(Xq int8 [M][K], sx f32 [M]) from bf16 N(0,1) activations."""
     x = activations(seed, M, K, "bf16")

@@ -52,7 +52,7 @@ def _mat(**kw):
     from paper_2405_03594_amd import _Matrix
 
     d = dict(rows=4, cols=64, dtype=2, layout=0, nnz=10, bitmask=0x10000, values=0x20000, row_offsets=0x30000,
-             tile_offsets=0)
+             tile_offsets=0, values_bytes=1 << 20)
     d.update(kw)
     return _Matrix(**d)
 
@@ -72,7 +72,13 @@ def _mat(**kw):
     (dict(bitmask=0), INVALID),
     (dict(row_offsets=0), INVALID),
     (dict(values=0), INVALID),
-    (dict(values=0, nnz=0), OK),
+    (dict(values=0, nnz=0), INVALID),                   # values always point at an allocation
+    (dict(values_bytes=0), INVALID),
+    (dict(values_bytes=47), INVALID),                   # 10 bf16 payloads: 20 -> 32, + 16 = 48 bytes
+    (dict(values_bytes=48), OK),
+    (dict(dtype=3, values_bytes=31), INVALID),          # 10 int8 payloads: 16 + 16
+    (dict(dtype=3, values_bytes=32), OK),
+    (dict(nnz=0, values_bytes=16), OK),
     (dict(bitmask=0x10004), INVALID),
     (dict(values=0x20008), INVALID),
     (dict(row_offsets=0x30002), INVALID),
@@ -120,16 +126,37 @@ def test_int8_argument_checks(L):
     assert f(None, None, 0, ctypes.byref(m), None, None, None, None) == OK
 
 
-def test_pack_argument_checks(L):
+@pytest.mark.parametrize("layout", [0, 1])
+def test_pack_argument_checks(L, layout):
     W, ro = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x20000)
+    bm, v = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000)
     nnz = ctypes.c_int64(0)
-    assert L.spl_pack_count(None, 2, None, 4, 4, ro, ctypes.byref(nnz), None) == INVALID
-    assert L.spl_pack_count(W, 2, None, 4, 4, ro, None, None) == INVALID
-    assert L.spl_pack_count(W, 5, None, 4, 4, ro, ctypes.byref(nnz), None) == INVALID
-    assert L.spl_pack_count(W, 2, None, 0, 4, ro, ctypes.byref(nnz), None) == INVALID
-    assert L.spl_pack_count(W, 2, None, 1 << 31, 4, ro, ctypes.byref(nnz), None) == INVALID
-    assert L.spl_pack_sparse(W, 2, None, 4, 4, ro, None, None, None) == INVALID
-    assert L.spl_pack_sparse(W, 2, None, 4, 4, ro, ctypes.c_void_p(0x30004), None, None) == INVALID
+    assert L.spl_pack_count(None, 2, None, 4, 4, layout, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 4, 4, layout, ro, None, None) == INVALID
+    assert L.spl_pack_count(W, 5, None, 4, 4, layout, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 0, 4, layout, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 1 << 31, 4, layout, ro, ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_count(W, 2, None, 4, 4, 2, ro, ctypes.byref(nnz), None) == INVALID     # unknown layout
+    assert L.spl_pack_count(W, 2, None, 4, 4, layout, ctypes.c_void_p(0x20002), ctypes.byref(nnz), None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, layout, ro, None, v, None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, layout, ro, ctypes.c_void_p(0x30004), v, None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, layout, ro, bm, None, None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, layout, ro, bm, ctypes.c_void_p(0x40008), None) == INVALID
+    assert L.spl_pack_sparse(W, 2, None, 4, 4, 3, ro, bm, v, None) == INVALID
+
+
+def test_values_bytes(L):
+    assert L.spl_values_bytes(2, 0) == 16 and L.spl_values_bytes(2, 1) == 32 and L.spl_values_bytes(2, 8) == 32
+    assert L.spl_values_bytes(2, 9) == 48 and L.spl_values_bytes(1, 8) == 32
+    assert L.spl_values_bytes(3, 16) == 32 and L.spl_values_bytes(3, 17) == 48
+    assert L.spl_values_bytes(4, 32) == 32 and L.spl_values_bytes(4, 33) == 48
+    assert L.spl_values_bytes(9, 8) == 0 and L.spl_values_bytes(2, -1) == 0
+
+
+def test_validate_rejects_bad_views_on_the_host(L):
+    assert L.spl_validate(None, None) == INVALID
+    m = _mat(values_bytes=0)
+    assert L.spl_validate(ctypes.byref(m), None) == INVALID            # fails spl_check_matrix: no device access
 
 
 def test_dense_argument_checks(L):
@@ -347,9 +374,10 @@ def test_int4_argument_checks(L):
     assert L.spl_int4_values_bytes(5) >= 3 + 16
     assert L.spl_check_matrix(ctypes.byref(w4)) == INVALID                # only the int4 entry takes SPL_I4
     p = L.spl_pack_int4
-    assert p(ctypes.byref(w4), 0x70000, None) == INVALID                  # the source must be an int8 view
-    assert p(ctypes.byref(_mat(layout=1, tile_offsets=0x40000)), 0x70000, None) == UNSUPPORTED   # bf16
-    assert p(ctypes.byref(w8), 0x70008, None) == INVALID                  # misaligned output
+    assert p(ctypes.byref(w4), 0x70000, None, None) == INVALID            # the source must be an int8 view
+    assert p(ctypes.byref(_mat(layout=1, tile_offsets=0x40000)), 0x70000, None, None) == UNSUPPORTED   # bf16
+    assert p(ctypes.byref(w8), 0x70008, None, None) == INVALID            # misaligned output
+    assert p(ctypes.byref(w8), 0x70000, 0x80002, None) == INVALID         # misaligned count word
     f = L.spl_sparse_linear_int4
     assert f(X, s, 0, ctypes.byref(w4), s, Y, None, None) == OK           # M = 0
     assert f(X, s, 17, ctypes.byref(w4), s, Y, None, None) == UNSUPPORTED # decode batches only
@@ -357,3 +385,55 @@ def test_int4_argument_checks(L):
     assert f(X, None, 2, ctypes.byref(w4), s, Y, None, None) == INVALID
     assert f(X, s, 2, ctypes.byref(_mat(dtype=4, cols=40, layout=1, tile_offsets=0x40000)), s, Y, None,
              None) == UNSUPPORTED                                          # K % 16 != 0
+
+
+def _cpu_matrix(N=8, K=64, dtype=None):
+    import torch
+
+    import paper_2405_03594_amd as spl
+
+    dtype = dtype or torch.bfloat16
+    return spl.SparseMatrix(torch.zeros(16 * ((N + 15) // 16) * ((K + 31) // 32), dtype=torch.int32),
+                            torch.zeros(64, dtype=dtype), None, torch.zeros(((N + 15) // 16) * ((K + 31) // 32) + 1,
+                                                                           dtype=torch.int32), N, K, 0, "tile16")
+
+
+def test_wrappers_reject_mismatched_tensors_before_any_launch():
+    """The Python binding checks shapes, dtypes, lengths and contiguity before
+    it calls the C ABI (which sees only pointers)."""
+    import torch
+
+    import paper_2405_03594_amd as spl
+
+    Wc = _cpu_matrix()
+    X = torch.zeros((2, 64), dtype=torch.bfloat16)
+    cases = [
+        (lambda: spl.sparse_linear(torch.zeros((2, 63), dtype=torch.bfloat16), Wc), "shape"),
+        (lambda: spl.sparse_linear(torch.zeros((2, 64), dtype=torch.float16), Wc), "dtype"),
+        (lambda: spl.sparse_linear(X, Wc, out=torch.zeros((2, 9), dtype=torch.bfloat16)), "shape"),
+        (lambda: spl.sparse_linear(X, Wc, out=torch.zeros((8, 2), dtype=torch.bfloat16).t()), "contiguous"),
+        (lambda: spl.sparse_linear(torch.zeros(64, dtype=torch.bfloat16), Wc), "2-D"),
+        (lambda: spl.sparse_linear_group([X, torch.zeros((2, 32), dtype=torch.bfloat16)], [Wc, Wc]), "shape"),
+        (lambda: spl.sparse_linear_silu_mul(torch.zeros((2, 60), dtype=torch.bfloat16), Wc, Wc), "shape"),
+        (lambda: spl.sparse_linear_silu_mul(X, Wc, _cpu_matrix(N=9)), "share"),
+        (lambda: spl.dense_linear(X, torch.zeros((8, 60), dtype=torch.bfloat16)), "shape"),
+    ]
+    W8 = _cpu_matrix(dtype=torch.int8)
+    Xq = torch.zeros((2, 64), dtype=torch.int8)
+    sx, sw = torch.zeros(2, dtype=torch.float32), torch.zeros(8, dtype=torch.float32)
+    cases += [
+        (lambda: spl.sparse_linear_int8(Xq.to(torch.int16), sx, W8, sw), "dtype"),
+        (lambda: spl.sparse_linear_int8(torch.zeros((2, 48), dtype=torch.int8), sx, W8, sw), "shape"),
+        (lambda: spl.sparse_linear_int8(Xq, torch.zeros(1, dtype=torch.float32), W8, sw), "x_scales"),
+        (lambda: spl.sparse_linear_int8(Xq, sx, W8, torch.zeros(7, dtype=torch.float32)), "w_scales"),
+        (lambda: spl.sparse_linear_int8(Xq, sx.double(), W8, sw), "dtype"),
+        (lambda: spl.sparse_linear_int8(Xq, sx, W8, sw, acc_out=torch.zeros((2, 8), dtype=torch.int64)), "dtype"),
+        (lambda: spl.sparse_linear_int8(Xq, sx, W8, sw, out=torch.zeros((2, 8), dtype=torch.float32)), "dtype"),
+        (lambda: spl.sparse_linear_int8_group([Xq], [sx[:1]], [W8], [sw]), "x_scales"),
+        (lambda: spl.sparse_linear_int4(torch.zeros((2, 16), dtype=torch.int8), sx, W8, sw), "shape"),
+        (lambda: spl.dense_linear_int8(Xq, sx, torch.zeros((8, 64), dtype=torch.int8), sw[:4]), "w_scales"),
+        (lambda: spl.quantize_rows_i8(X, scales=torch.zeros(1, dtype=torch.float32)), "scales"),
+    ]
+    for fn, what in cases:
+        with pytest.raises(ValueError, match=what):
+            fn()

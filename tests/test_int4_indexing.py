@@ -25,7 +25,7 @@ def _widen(w):
 
 
 def _selector(nib):
-    """i4_nibble_selector: byte j <- rank of column j among the nibble's set bits, 12 (zero) if clear."""
+    """nibble_selector8(nib, 0): byte j <- rank of column j among the nibble's set bits, 12 (zero) if clear."""
     return [bin(nib & ((1 << j) - 1)).count("1") if (nib >> j) & 1 else 12 for j in range(4)]
 
 
@@ -39,12 +39,14 @@ def _perm0(y, sel):
 
 
 def _values_bytes(nnz):
-    return ((nnz + 1) // 2 + 16 + 15) // 16 * 16
+    """spl_values_bytes(SPL_I4, nnz): the nibble bytes rounded up to 16, plus 16."""
+    return ((nnz + 1) // 2 + 15) // 16 * 16 + 16
 
 
+@pytest.mark.parametrize("gen", ["int4_weight", "int4_weight_full_range"])
 @pytest.mark.parametrize("waves", [8, 16])
 @pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (17, 48, 0.7), (40, 96, 0.0), (33, 208, 0.9), (16, 64, 1.0)])
-def test_int4_schedule_reads_and_operands(orc, N, K, s, waves):
+def test_int4_schedule_reads_and_operands(orc, N, K, s, waves, gen):
     src = open(SRC).read()
     for line in ("const int s = 2 * p + (fg >> 1), h = fg & 1;",
                  "hw = (g.bm[t * 16 + fr] >> (16 * h)) & 0xffffu;",
@@ -55,9 +57,10 @@ def test_int4_schedule_reads_and_operands(orc, N, K, s, waves):
                  "const uint32_t y = i4_widen((uint32_t)(nibs >> (4u * rank)) & 0xFFFFu);   // ranks rank .. rank + 3",
                  "a[q] = __builtin_amdgcn_perm(0u, y, sel4[m4]);",
                  "return y | ((m << 5) - (m << 1));",
-                 "int64_t int4_values_bytes(int64_t nnz) { return ((nnz + 1) / 2 + 16 + 15) / 16 * 16; }"):
+                 "int64_t int4_values_bytes(int64_t nnz) { return spl_values_bytes(SPL_I4, nnz); }",
+                 "outside += (a < -8 || a > 7) + (b < -8 || b > 7);"):
         assert line in src, f"kernel changed: update this replay ({line})"
-    Wq, mask, _ = synth.int4_weight(300 + N + K, N, K, s)
+    Wq, mask, _ = getattr(synth, gen)(300 + N + K, N, K, s)
     T = orc.pack_tiled(Wq, "i8", mask)
     nnz = int(T.tile_offsets[-1])
     packed = np.zeros(_values_bytes(nnz), dtype=np.uint8)

@@ -675,3 +675,15 @@ def test_int4_generator_codes(orc):
     amax = np.abs(v).max(axis=1)
     assert np.allclose(sw, np.where(amax == 0, 1, amax / 7), rtol=1e-6)
     assert (np.abs(Wq).max(axis=1)[amax > 0] == 7).all()
+
+
+def test_int4_full_range_generator(orc):
+    """The planted-edge generator: codes in [-8, 7], rows 0 and N - 1 all -8
+    where kept, row N // 2 all 7, zero off the mask, and -8 in other rows."""
+    N, K = 40, 96
+    Wq, mask, _ = synth.int4_weight_full_range(6, N, K, 0.5)
+    keep = mask.astype(bool)
+    assert Wq.min() == -8 and Wq.max() <= 7 and not Wq[~keep].any()
+    assert (Wq[0, keep[0]] == -8).all() and (Wq[N - 1, keep[N - 1]] == -8).all()
+    assert (Wq[N // 2, keep[N // 2]] == 7).all()
+    assert (Wq[1:N - 1][keep[1:N - 1]] == -8).any()

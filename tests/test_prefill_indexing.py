@@ -240,7 +240,7 @@ def _i8_lines():
                  "__builtin_memcpy(&tv.v1[i + h], vbytes + ob, 8);",
                  "const uint32_t s1 = lds_load4(lut_addr + 20u * n1 + 4u * __popc(n0_));",
                  "const uint32_t s3 = lds_load4(lut_addr + 20u * n3 + 4u * __popc(n2));",
-                 "if (threadIdx.x < 80) lut[threadIdx.x] = pf_i8_selector(threadIdx.x / 5, threadIdx.x % 5);",
+                 "if (threadIdx.x < 80) lut[threadIdx.x] = nibble_selector8(threadIdx.x / 5, threadIdx.x % 5);",
                  "const int nst = (int)((Kh + kPfBK - 1) / kPfBK);   // stages of 128 bytes per row: 2 tiles (4 for int8)",
                  "const int64_t Kh = kI8 ? K / 2 : K;                // activation row in 16-bit units"):
         assert line in src, f"int8 expansion changed: update this replay ({line})"
