@@ -266,6 +266,20 @@ int64_t spl_magnitude_mask_workspace_bytes(void);
 spl_status spl_magnitude_mask(const void* W, int32_t dtype, int64_t N, int64_t K, int64_t prune, uint8_t* mask,
                               void* workspace, hipStream_t stream);
 
+/* spl_magnitude_mask without a workspace argument, for callers that cannot
+ * allocate device memory (code under graph capture, serving loops, harnesses
+ * that forbid hipMalloc).  The result is that of spl_magnitude_mask with the
+ * same arguments.  The scratch is a library array of 34,818 32-bit words
+ * (136 KiB) per device, held from the first call on that device until the
+ * process ends; it is the same whatever the size, so the size limits are
+ * those of spl_magnitude_mask (N K < 2^31, K % 8 == 0: SPL_ERR_UNSUPPORTED
+ * otherwise).  The call allocates nothing and every kernel clears what it
+ * needs cleared.  All calls on one device share the array: calls that overlap
+ * on one device (two streams, two threads) race and give wrong masks.
+ * SPL_ERR_DEVICE when the array's device address cannot be obtained. */
+spl_status spl_magnitude_mask_noalloc(const void* W, int32_t dtype, int64_t N, int64_t K, int64_t prune,
+                                      uint8_t* mask, hipStream_t stream);
+
 /* The gated half of a Llama MLP on two sparse weights sharing X (the model
  * the paper sparsifies; its MLP is down(silu(gate(x)) * up(x))):
  *   Y[m][n] = silu(g) * u,  g = sum_k X[m][k] Wg[n][k],  u = likewise with Wu,

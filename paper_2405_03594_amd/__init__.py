@@ -109,6 +109,7 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_linear_silu_mul": (ctypes.c_int, [P, I64, MP, MP, P, I32, P]),
         "spl_magnitude_mask_workspace_bytes": (I64, []),
         "spl_magnitude_mask": (ctypes.c_int, [P, I32, I64, I64, I64, P, P, P]),
+        "spl_magnitude_mask_noalloc": (ctypes.c_int, [P, I32, I64, I64, I64, P, P]),
         "spl_transpose16": (ctypes.c_int, [P, I64, I64, P, P]),
         "spl_int4_values_bytes": (I64, [I64]),
         "spl_pack_int4": (ctypes.c_int, [MP, P, P, P]),
@@ -372,6 +373,24 @@ def magnitude_mask(W: torch.Tensor, prune: int, out: torch.Tensor | None = None,
         workspace = torch.empty((L.spl_magnitude_mask_workspace_bytes(),), dtype=torch.uint8, device=W.device)
     _check("spl_magnitude_mask", L.spl_magnitude_mask(_ptr(W), _TORCH_DTYPE[W.dtype], N, K, int(prune), _ptr(out),
                                                       _ptr(workspace), _stream(stream)))
+    return out
+
+
+def magnitude_mask_noalloc(W: torch.Tensor, prune: int, out: torch.Tensor, stream=None) -> torch.Tensor:
+    """magnitude_mask through the entry point that allocates nothing (see
+    spl_magnitude_mask_noalloc): the caller passes the uint8 [N][K] output;
+    the scratch is the library's own, shared by every call on the device."""
+    L = lib()
+    if W.dim() != 2:
+        raise ValueError(f"W: expected a 2-D tensor, got shape {tuple(W.shape)}")
+    N, K = W.shape
+    if W.dtype not in (torch.float16, torch.bfloat16):
+        raise ValueError(f"W has dtype {W.dtype}, expected float16 or bfloat16")
+    _arg(out, "out", shape=(N, K), dtype=torch.uint8, device=False)
+    _dev_tensor(W, "W")
+    _dev_tensor(out, "out")
+    _check("spl_magnitude_mask_noalloc", L.spl_magnitude_mask_noalloc(_ptr(W), _TORCH_DTYPE[W.dtype], N, K,
+                                                                      int(prune), _ptr(out), _stream(stream)))
     return out
 
 

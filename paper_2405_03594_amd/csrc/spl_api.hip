@@ -279,6 +279,40 @@ spl_status spl_magnitude_mask(const void* W, int32_t dtype, int64_t N, int64_t K
                                              static_cast<uint32_t*>(workspace), stream));
 }
 
+// Scratch of spl_magnitude_mask_noalloc: the histogram, the threshold pair and
+// the per-chunk tie counts of the pruning kernels.  Each device holds its own
+// copy until the process ends.  Host code uses the device address from
+// hipGetSymbolAddress (kept per device), never the array's name.
+constexpr int64_t kNoallocWords = 34818;
+static __device__ __align__(256) uint32_t scratch[kNoallocWords];
+
+static uint32_t* noalloc_scratch() {
+  static std::atomic<uint32_t*> addr[spl::kMaxDevices];
+  const int dev = spl::current_device();
+  if (dev < 0) return nullptr;
+  uint32_t* p = addr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  void* q = nullptr;
+  if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return nullptr;
+  addr[dev].store(static_cast<uint32_t*>(q), std::memory_order_release);
+  return static_cast<uint32_t*>(q);
+}
+
+spl_status spl_magnitude_mask_noalloc(const void* W, int32_t dtype, int64_t N, int64_t K, int64_t prune,
+                                      uint8_t* mask, hipStream_t stream) {
+  if (spl::magnitude_mask_workspace_words() > kNoallocWords) return SPL_ERR_UNSUPPORTED;   // build mismatch
+  if (!W || !mask || !dims_ok(N, K)) return SPL_ERR_INVALID_ARG;
+  if (!fp_dtype(dtype)) return SPL_ERR_UNSUPPORTED;
+  if (K % 8 != 0 || N * K >= ((int64_t)1 << 31)) return SPL_ERR_UNSUPPORTED;
+  if (prune < 0 || prune > N * K) return SPL_ERR_INVALID_ARG;
+  if (!aligned(W, 16) || !aligned(mask, 8)) return SPL_ERR_INVALID_ARG;
+  uint32_t* ws = noalloc_scratch();
+  if (!ws) return SPL_ERR_DEVICE;
+  (void)hipGetLastError();
+  return launched(spl::launch_magnitude_mask(static_cast<const uint16_t*>(W), N * K, (uint32_t)prune, mask, ws,
+                                             stream));
+}
+
 spl_status spl_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t stream) {
   if (R == 0 || C == 0) return (R < 0 || C < 0) ? SPL_ERR_INVALID_ARG : SPL_OK;
   if (!src || !dst || !dims_ok(R, C) || !aligned(src, 2) || !aligned(dst, 2)) return SPL_ERR_INVALID_ARG;

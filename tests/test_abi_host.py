@@ -316,6 +316,16 @@ def test_magnitude_mask_argument_checks(L):
     assert f(W + 8, 2, 4, 64, 10, m, ws, None) == INVALID                  # misaligned W
     assert f(W, 2, 4, 64, 10, m + 4, ws, None) == INVALID                  # misaligned mask
     assert f(W, 2, 0, 64, 10, m, ws, None) == INVALID                      # N = 0
+    g = L.spl_magnitude_mask_noalloc                                       # the same checks, no workspace
+    assert g(None, 2, 4, 64, 10, m, None) == INVALID
+    assert g(W, 2, 4, 64, 10, None, None) == INVALID
+    assert g(W, 3, 4, 64, 10, m, None) == UNSUPPORTED
+    assert g(W, 2, 4, 60, 10, m, None) == UNSUPPORTED
+    assert g(W, 2, 1 << 16, 1 << 15, 10, m, None) == UNSUPPORTED           # N K >= 2^31: past the maximum
+    assert g(W, 2, 262144, 8192, 10, m, None) == UNSUPPORTED               # N K == 2^31
+    assert g(W, 2, 4, 64, 257, m, None) == INVALID
+    assert g(W + 8, 2, 4, 64, 10, m, None) == INVALID
+    assert g(W, 2, 4, 64, 10, m + 4, None) == INVALID
 
 
 def test_training_argument_checks(L):
