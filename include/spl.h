@@ -118,8 +118,8 @@ int64_t spl_values_bytes(int32_t dtype, int64_t nnz);
 /* Library version, (major << 16) | minor. */
 int32_t spl_version(void);
 
-/* Static text for a status code. */
-const char* spl_status_string(spl_status s);
+/* Static text for a status code (any int: "unknown status" outside spl_status). */
+const char* spl_status_string(int32_t status);
 
 /* Measurement helper, not part of the method: reads `bytes` (> 0, a multiple
  * of 16) of the 16-byte aligned device buffer `buf` with coalesced 16-byte
@@ -238,7 +238,10 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
  * workspace: spl_transpose_perm_workspace_bytes(N, K, nnz) bytes, 256-byte
  * aligned.  spl_permute_values then copies dst[i] = src[perm[i]] (nnz 16-bit
  * payloads, src holding nnz of them), e.g. Wt.values from W.values after each
- * SGD step; a perm entry outside [0, nnz) gives 0 and reads nothing. */
+ * SGD step; a perm entry outside [0, nnz) gives 0 and reads nothing; nnz >=
+ * 2^31 is SPL_ERR_OVERFLOW.
+ * The two *_workspace_bytes functions return -1 for sizes their entry points
+ * reject (N, K or M outside the dimension limits, nnz outside [0, N K]). */
 int64_t spl_transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz);
 spl_status spl_transpose_perm(const spl_matrix* W, const spl_matrix* Wt, int32_t* perm, void* workspace,
                               hipStream_t stream);

@@ -49,8 +49,8 @@ extern "C" {
 
 int32_t spl_version(void) { return (1 << 16) | 0; }
 
-const char* spl_status_string(spl_status s) {
-  switch (s) {
+const char* spl_status_string(int32_t status) {
+  switch (status) {
     case SPL_OK: return "ok";
     case SPL_ERR_INVALID_ARG: return "invalid argument";
     case SPL_ERR_UNSUPPORTED: return "unsupported";
@@ -342,6 +342,7 @@ spl_status spl_gather_tiled(const void* W_dense, const spl_matrix* pattern, void
 
 int64_t spl_sparse_weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K) {
   if (M < 0 || !dims_ok(N, K)) return -1;
+  if (M > 0 && (!dims_ok(M, N) || !dims_ok(M, K))) return -1;   // the sizes below stay far from 2^63
   return spl::weight_grad_workspace_bytes(M, N, K);
 }
 
@@ -368,7 +369,7 @@ spl_status spl_sparse_sgd_update(const spl_matrix* Wc, const void* grad_values, 
 }
 
 int64_t spl_transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz) {
-  if (!dims_ok(N, K) || nnz < 0) return -1;
+  if (!dims_ok(N, K) || nnz < 0 || nnz > N * K) return -1;
   return spl::transpose_perm_workspace_bytes(N, K, nnz);
 }
 
@@ -390,6 +391,7 @@ spl_status spl_transpose_perm(const spl_matrix* W, const spl_matrix* Wt, int32_t
 
 spl_status spl_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t stream) {
   if (nnz < 0) return SPL_ERR_INVALID_ARG;
+  if (nnz >= kMaxDim) return SPL_ERR_OVERFLOW;         // value counts are below 2^31, as nnz everywhere
   if (nnz == 0) return SPL_OK;
   if (!src || !perm || !dst || !aligned(src, 2) || !aligned(perm, 4) || !aligned(dst, 2)) return SPL_ERR_INVALID_ARG;
   (void)hipGetLastError();

@@ -236,7 +236,7 @@ def test_int8_prefill_grids(orc, spl, N, K, M, s):
 
 
 @pytest.mark.parametrize("name,M,s", [("q", 512, 0.7), ("gate", 512, 0.7), ("down", 512, 0.7), ("up", 2048, 0.5),
-                                      ("o", 2048, 0.7)])
+                                      ("o", 2048, 0.7), ("down", 2048, 0.7), ("down", 2048, 0.5)])
 def test_int8_prefill_llama_shapes_sampled(orc, spl, name, M, s):
     """Llama-2-7B shapes at the prefill batch sizes: every output of 64 rows
     (the first, the last and 62 seeded ones) equals the oracle bit for bit;

@@ -36,15 +36,19 @@ def test_transpose16(spl, R, C):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("N,K,s", [(1, 8, 0.5), (17, 72, 0.7), (100, 1000, 0.0), (300, 264, 0.9), (33, 512, 1.0)])
-def test_gather_tiled_matches_pack(spl, dtype, N, K, s):
-    """Gathering W's own entries at its pattern reproduces the packed values."""
+def test_gather_tiled_matches_oracle_encoder(orc, spl, dtype, N, K, s):
+    """Gathering a dense matrix at W's pattern gives the oracle's tile-layout
+    values of that matrix under W's mask: for W itself and for another dense
+    matrix (a gradient's role), whose entries at pruned positions must not
+    leak in."""
     import torch
 
     W, mask = synth.weight(600 + N, N, K, dtype, s)
-    Wd = to_dev(W, dtype)
-    Wc = spl.pack_sparse(Wd, torch.from_numpy(mask).cuda())
-    got = spl.gather_tiled(Wd, Wc)
-    assert np.array_equal(from_dev_bits(got)[:Wc.nnz], from_dev_bits(Wc.values)[:Wc.nnz])
+    D, _ = synth.weight(700 + N, N, K, dtype, 0.0)
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    for name, A in (("W", W), ("D", D)):
+        got = from_dev_bits(spl.gather_tiled(to_dev(A, dtype), Wc))[:Wc.nnz]
+        assert np.array_equal(got, orc.pack_tiled(A, dtype, mask).values), name
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
@@ -116,10 +120,10 @@ def test_weight_grad_llama_shapes(orc, spl, name, j, M):
 
 
 @pytest.mark.parametrize("N,K,s", [(8, 8, 0.5), (104, 1000, 0.7), (296, 264, 0.0), (64, 520, 0.9)])
-def test_transpose_perm_keeps_the_transpose_in_step(spl, N, K, s):
+def test_transpose_perm_keeps_the_transpose_in_step(orc, spl, N, K, s):
     """The packed transpose (transposed mask) refreshed by the permutation
-    equals a fresh pack of the transposed weights, before and after an SGD
-    step, bit for bit."""
+    holds the oracle's tile-layout values of the transposed weights, for the
+    packed weights and again after new values are written into them."""
     import torch
 
     W, mask = synth.weight(650 + N, N, K, "bf16", s)
@@ -128,13 +132,14 @@ def test_transpose_perm_keeps_the_transpose_in_step(spl, N, K, s):
     mt = md.t().contiguous()
     Wt = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), mt)
     perm = spl.transpose_perm(Wc, Wt)
-    for step in range(2):
+    D, _ = synth.weight(660 + N, N, K, "bf16", 0.0)        # the next weights (dense draw; pruned by the mask)
+    for step, A in enumerate((W, D)):
+        if step:
+            Wc.values[:Wc.nnz].copy_(to_dev(orc.pack_tiled(A, "bf16", mask).values, "bf16"))
         out = torch.empty_like(Wt.values)
         spl.permute_values(Wc.values, perm, Wc.nnz, out)
-        fresh = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), mt)
-        assert np.array_equal(from_dev_bits(out)[:Wc.nnz], from_dev_bits(fresh.values)[:Wc.nnz]), step
-        g = torch.full_like(Wc.values, 0.25)
-        spl.sparse_sgd_update(Wc, g, 0.5)
+        ref = orc.pack_tiled(np.ascontiguousarray(A.T), "bf16", np.ascontiguousarray(mask.T)).values
+        assert np.array_equal(from_dev_bits(out)[:Wc.nnz], ref), step
 
 
 @pytest.mark.parametrize("name,j", [("gate", 4), ("down", 6)])
