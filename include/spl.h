@@ -207,7 +207,9 @@ spl_status spl_unpack(const spl_matrix* Wc, void* W_dense, hipStream_t stream);
 spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, void* Y, hipStream_t stream);
 
 /* As spl_sparse_linear with an explicit kernel family (spl_algo).
- * DECODE requires M <= 32. */
+ * DECODE requires M <= 32 and 2 M K <= 2^31 (the activations addressed with
+ * 32-bit byte offsets); SPL_ERR_UNSUPPORTED otherwise, and AUTO then picks
+ * PREFILL. */
 spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
                                 hipStream_t stream);
 

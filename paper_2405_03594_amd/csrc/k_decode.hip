@@ -100,26 +100,36 @@ __device__ __forceinline__ void wave_range(int S, int wave, int* beg, int* end) 
   *end = b + L < S ? b + L : S;
 }
 
-// Activation operand read directly from X: lane (fr, fg) of batch tile t
-// reads X[16t + fr][32s + 8fg .. +8]; rows past M are not read (zeros).
+// Activation operand read directly from X with raw buffer loads: lane
+// (fr, fg) of batch tile t reads X[16t + fr][32s + 8fg .. +8].  The base and
+// the byte size of X sit in the buffer descriptor (SGPRs), each lane keeps one
+// 32-bit byte offset per batch tile (k-step 0) and the k-step goes in the
+// scalar offset, so a load costs no vector ALU work.  A lane whose row is past
+// M, or whose columns are past K, passes an offset beyond the buffer and the
+// hardware returns zeros.  Needs 2 M K <= kXBufMax (the launcher checks).
+constexpr uint32_t kXOob = 0x80000000u;              // an offset past any accepted X
+constexpr int64_t kXBufMax = (int64_t)kXOob;
 template <int MT>
 struct XGlobal {
-  const uint16_t* row[MT];
-  bool live[MT];
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t off[MT];
   __device__ __forceinline__ XGlobal(const uint16_t* __restrict__ X, int M, int64_t K, int fr, int fg) {
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(X), (short)0, (int)(2 * (int64_t)M * K),
+                                             0x00020000);
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
       const int m = 16 * t + fr;
-      live[t] = m < M;
-      row[t] = X + (int64_t)(live[t] ? m : 0) * K + 8 * fg;
+      off[t] = m < M ? 2u * ((uint32_t)m * (uint32_t)K + 8u * (uint32_t)fg) : kXOob;
     }
   }
-  // k-step s; kin: this lane's 8 columns lie inside [0, K)
-  __device__ __forceinline__ void load(u32x4 (&xb)[MT], int s, bool kin) const {
+  // k-step s; ragged (wave-uniform): s is the last k-step and K % 32 != 0, so
+  // some lanes' columns may lie past K
+  __device__ __forceinline__ void load(u32x4 (&xb)[MT], int s, bool ragged, int fg, int64_t K) const {
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
-      xb[t] = u32x4{0u, 0u, 0u, 0u};
-      if (kin && live[t]) xb[t] = *reinterpret_cast<const u32x4*>(row[t] + 32 * (int64_t)s);
+      uint32_t o = off[t];
+      if (ragged && (uint32_t)(32 * s + 8 * fg) >= (uint32_t)K) o = kXOob;
+      xb[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, o, 64 * s, 0));
     }
   }
 };
@@ -142,44 +152,56 @@ struct XShared {
 };
 
 // Cooperative copy of X [M][K] into LDS rows of xs_stride(K) elements with
-// zeros from K to 32*S, split so that the loads can be issued early.
+// zeros from K to 32*S, split so that the loads can be issued early.  Piece p
+// (16 bytes) of the copy is row m = p / per_row, piece q = p % per_row of that
+// row; each thread divides once and steps (m, q) by the thread count between
+// rounds.  Staged copies hold at most kXLdsMax bytes, so every product here
+// is below 2^24 (24-bit multiplies).
 template <int W>
 struct XStager {
   static constexpr int kThreads = W * kWave;
   static constexpr int kXRounds = kXLdsMax / 16 / kThreads;   // staged pieces per thread (bounds M * 4S)
   u32x4 r[kXRounds];
-  int per_row, total, kp;
-  float inv;
-  // row of piece p (p < 2^12, per_row < 2^12): a float estimate corrected by one step
-  __device__ __forceinline__ int row_of(int p) const {
-    int m = (int)((float)p * inv);
-    if (m * per_row > p) --m;
-    if ((m + 1) * per_row <= p) ++m;
-    return m;
-  }
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int M, int64_t K) {
+  int per_row, total, kp, m0, q0, dm, dq;
+  __device__ __forceinline__ void start(int M, int64_t K) {
     per_row = (int)(4 * tile_steps(K));          // 16-byte pieces per staged row (up to 32*S)
     kp = (int)(K / 8);                           // pieces that hold activations
     total = M * per_row;
-    inv = 1.0f / (float)per_row;
+    dm = kThreads / per_row;                     // wave-uniform
+    dq = kThreads - dm * per_row;
+    const int p = threadIdx.x;                   // < kThreads <= 1024: a float estimate corrected by one step
+    int m = (int)((float)p * (1.0f / (float)per_row));
+    if ((int)__umul24(m, per_row) > p) --m;
+    if ((int)__umul24(m + 1, per_row) <= p) ++m;
+    m0 = m;
+    q0 = p - (int)__umul24(m, per_row);
+  }
+  __device__ __forceinline__ void next(int& m, int& q) const {
+    m += dm;
+    q += dq;
+    if (q >= per_row) q -= per_row, ++m;
+  }
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int M, int64_t K) {
+    start(M, K);
+    int m = m0, q = q0;
 #pragma unroll
     for (int i = 0; i < kXRounds; ++i) {
       const int p = threadIdx.x + i * kThreads;
       r[i] = u32x4{0u, 0u, 0u, 0u};
-      if (p < total) {
-        const int m = row_of(p), q = p - m * per_row;
-        if (q < kp) r[i] = *reinterpret_cast<const u32x4*>(X + (int64_t)m * K + 8 * q);
-      }
+      if (p < total && q < kp)   // 32-bit byte offsets from the uniform base (SGPR-based loads)
+        r[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const unsigned char*>(X) +
+                                               2u * (__umul24(m, (uint32_t)K) + 8u * (uint32_t)q));
+      next(m, q);
     }
   }
   __device__ __forceinline__ void store(uint16_t* xs, int64_t K) const {
+    const uint32_t stride = (uint32_t)xs_stride(K);
+    int m = m0, q = q0;
 #pragma unroll
     for (int i = 0; i < kXRounds; ++i) {
       const int p = threadIdx.x + i * kThreads;
-      if (p < total) {
-        const int m = row_of(p), q = p - m * per_row;
-        *reinterpret_cast<u32x4*>(xs + (int64_t)m * xs_stride(K) + 8 * q) = r[i];
-      }
+      if (p < total) *reinterpret_cast<u32x4*>(xs + __umul24(m, stride) + 8 * q) = r[i];
+      next(m, q);
     }
   }
 };
@@ -314,7 +336,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   int ob = kbeg;
   auto load_offsets = [&](int base) {
     const int t = base + lane < kend ? base + lane : kend;
-    return tob[t];
+    return *reinterpret_cast<const int32_t*>(reinterpret_cast<const unsigned char*>(tob) + 4u * (uint32_t)t);
   };
   // The most tiles (<= C, inside the range) from c0 whose values fit the
   // staging buffer: tile j fits iff its end offset <= (a0 + kVBuf) / 2, and
@@ -397,7 +419,8 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     u32x4 xb[XL ? 1 : C][MT];
     if constexpr (!XL) {
 #pragma unroll
-      for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cur.cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+      for (int j = 0; j < C; ++j)
+        if (j < cur.cn) xop.load(xb[j], c0 + j, c0 + j == S - 1 && (K & 31) != 0, fg, K);
     }
     const int c1 = c0 + cur.cn;
     if (c1 < kend) {
@@ -613,7 +636,8 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
     u32x4 xb[C][1];
     if constexpr (!XL) {
 #pragma unroll
-      for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, j < cur.cn && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+      for (int j = 0; j < C; ++j)
+        if (j < cur.cn) xop.load(xb[j], c0 + j, c0 + j == S - 1 && (K & 31) != 0, fg, K);
     }
     const int c1 = c0 + cur.cn;
     if (c1 < kend) {
@@ -748,7 +772,14 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const De
     } else {
       u32x4 xb[C][MT];
 #pragma unroll
-      for (int j = 0; j < C; ++j) xop.load(xb[j], c0 + j, c0 + j < kend && 32 * (int64_t)(c0 + j) + 8 * fg < K);
+      for (int j = 0; j < C; ++j) {
+        if (c0 + j < kend) {
+          xop.load(xb[j], c0 + j, c0 + j == S - 1 && (K & 31) != 0, fg, K);
+        } else {                                       // multiplied below: past the range it must be zero
+#pragma unroll
+          for (int t = 0; t < MT; ++t) xb[j][t] = u32x4{0u, 0u, 0u, 0u};
+        }
+      }
       if (c0 + C < kend) load_a(an, c0 + C);
 #pragma unroll
       for (int j = 0; j < C; ++j)
@@ -874,8 +905,6 @@ hipError_t launch_zero_fill(void* Y, int64_t count16, hipStream_t s) {
 }
 
 // No per-K limit: a wave walks its k-range in chunks.
-int decode_max_k() { return 1 << 30; }
-
 hipError_t launch_sparse_decode(const spl_sparse_task* tasks, int count, int64_t M, hipStream_t s) {
   SparseGroupArg g{};
   int64_t kmax = 0;
@@ -887,6 +916,7 @@ hipError_t launch_sparse_decode(const spl_sparse_task* tasks, int count, int64_t
     g.first[i + 1] = g.first[i] + (int32_t)tile_blocks(W.rows);
     if (W.cols > kmax) kmax = W.cols;
   }
+  if (2 * M * kmax > kXBufMax) return hipErrorNotSupported;   // activations addressed with 32-bit offsets
   g.count = count;
   g.M = (int32_t)M;
   return tasks[0].W->dtype == SPL_BF16 ? sparse_group_t<Bf16>(g, kmax, s) : sparse_group_t<F16>(g, kmax, s);
@@ -897,6 +927,7 @@ hipError_t launch_sparse_decode(const spl_sparse_task* tasks, int count, int64_t
 hipError_t launch_gated_decode(const void* X, int64_t M, const spl_matrix& Wg, const spl_matrix& Wu, void* Y,
                                hipStream_t s) {
   if (Wg.nnz == 0 || Wu.nnz == 0) return launch_zero_fill(Y, M * Wg.rows, s);   // silu(0) u = silu(g) 0 = 0
+  if (2 * M * Wg.cols > kXBufMax) return hipErrorNotSupported;   // activations addressed with 32-bit offsets
   constexpr int W = 8;
   static_assert(W * 2 * kWave * 4 * sizeof(float) <= sparse2_vbuf_bytes<W>(), "both blocks' partial sums fit");
   SparseGroupArg g{};
@@ -930,6 +961,7 @@ hipError_t launch_dense_decode(const spl_dense_task* tasks, int count, int64_t M
     g.first[i + 1] = g.first[i] + (int32_t)tile_blocks(tasks[i].N);
     if (tasks[i].K > kmax) kmax = tasks[i].K;
   }
+  if (2 * M * kmax > kXBufMax) return hipErrorNotSupported;   // activations addressed with 32-bit offsets
   g.count = count;
   g.M = (int32_t)M;
   return dtype == SPL_BF16 ? dense_group_t<Bf16>(g, kmax, s) : dense_group_t<F16>(g, kmax, s);

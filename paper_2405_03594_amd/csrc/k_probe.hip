@@ -3,33 +3,36 @@
 // against besides the vendor's nominal figure.
 //
 // Every lane reads 16 bytes per load, consecutive lanes consecutive pieces
-// (1 KB per wave instruction), eight loads in flight per lane before any is
-// used; workgroups stride over the buffer.  The loaded words are folded into
-// one value that is stored only if it equals a constant no data is expected to
-// produce, so the loads cannot be removed and nothing is written in practice.
+// (1 KB per wave instruction); each workgroup reads a contiguous 16 KB block
+// per step (four loads in flight per lane before any is used) and the
+// workgroups (two per compute unit, the best of a sweep of depth and
+// occupancy on this device) stride over the buffer.  The loaded words are
+// folded into one value that is stored only if it equals a constant no data
+// is expected to produce, so the loads cannot be removed and nothing is
+// written in practice.
 #include "spl_common.h"
 
 namespace spl {
 namespace {
 
 constexpr int kProbeThreads = 256;
-constexpr int kProbeUnroll = 8;
+constexpr int kProbeDepth = 4;
+constexpr int kProbeBlocksPerCu = 2;
 
 __global__ void __launch_bounds__(kProbeThreads) k_read_probe(const u32x4* __restrict__ buf, int64_t pieces,
                                                               uint32_t* __restrict__ sink) {
-  const int64_t stride = (int64_t)gridDim.x * kProbeThreads;
+  constexpr int64_t kStep = (int64_t)kProbeThreads * kProbeDepth;     // pieces per workgroup step
+  const int64_t stride = (int64_t)gridDim.x * kStep;
   uint32_t acc = 0;
-  int64_t i = (int64_t)blockIdx.x * kProbeThreads + threadIdx.x;
-  for (; i + (kProbeUnroll - 1) * stride < pieces; i += kProbeUnroll * stride) {
-    u32x4 v[kProbeUnroll];
+  for (int64_t base = (int64_t)blockIdx.x * kStep + threadIdx.x; base < pieces; base += stride) {
+    u32x4 v[kProbeDepth];
 #pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) v[u] = buf[i + u * stride];
+    for (int d = 0; d < kProbeDepth; ++d) {
+      const int64_t i = base + (int64_t)kProbeThreads * d;
+      v[d] = i < pieces ? buf[i] : u32x4{0u, 0u, 0u, 0u};
+    }
 #pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
-  }
-  for (; i < pieces; i += stride) {
-    const u32x4 v = buf[i];
-    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    for (int d = 0; d < kProbeDepth; ++d) acc ^= v[d].x ^ v[d].y ^ v[d].z ^ v[d].w;
   }
   if (acc == 0x9E3779B9u) sink[0] = acc;
 }
@@ -38,8 +41,8 @@ __global__ void __launch_bounds__(kProbeThreads) k_read_probe(const u32x4* __res
 
 hipError_t launch_read_probe(const void* buf, int64_t bytes, uint32_t* sink, int cus, hipStream_t s) {
   const int64_t pieces = bytes / 16;
-  int64_t blocks = (int64_t)cus * 8;
-  const int64_t need = (pieces + kProbeThreads - 1) / kProbeThreads;
+  int64_t blocks = (int64_t)cus * kProbeBlocksPerCu;
+  const int64_t need = (pieces + (int64_t)kProbeThreads * kProbeDepth - 1) / ((int64_t)kProbeThreads * kProbeDepth);
   if (blocks > need) blocks = need;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_read_probe, dim3((unsigned)blocks), dim3(kProbeThreads), 0, s,

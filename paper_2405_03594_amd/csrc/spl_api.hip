@@ -8,16 +8,14 @@
 #include "spl.h"
 #include "spl_common.h"
 
-namespace spl {
-int decode_max_k();
-}
-
 namespace {
 
 constexpr int64_t kMaxDim = (int64_t)1 << 31;        // N, K, M < 2^31
 constexpr int64_t kMaxElems = (int64_t)1 << 40;      // N * K, M * K, M * N
 constexpr int64_t kDecodeMaxM = 32;
 constexpr int64_t kGatedDecodeMaxM = 16;           // the paired decode kernel holds one 16-row batch tile
+// The decode kernels address the activations [M][K] with 32-bit byte offsets.
+bool decode_fits(int64_t M, int64_t K) { return M <= kDecodeMaxM && 2 * M * K <= ((int64_t)1 << 31); }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -195,9 +193,8 @@ static spl_status check_sparse_task(const void* X, int64_t M, const spl_matrix* 
   const spl_status xy = check_xy(X, M, Wc->cols, Wc->rows, Y);
   if (xy != SPL_OK) return xy;
   if (Wc->cols % 8 != 0) return SPL_ERR_UNSUPPORTED;
-  if (*algo == SPL_ALGO_AUTO)
-    *algo = (M <= kDecodeMaxM && Wc->cols <= spl::decode_max_k()) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
-  if (*algo == SPL_ALGO_DECODE && (M > kDecodeMaxM || Wc->cols > spl::decode_max_k())) return SPL_ERR_UNSUPPORTED;
+  if (*algo == SPL_ALGO_AUTO) *algo = decode_fits(M, Wc->cols) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (*algo == SPL_ALGO_DECODE && !decode_fits(M, Wc->cols)) return SPL_ERR_UNSUPPORTED;
   return SPL_OK;
 }
 
@@ -207,8 +204,8 @@ static spl_status check_dense_task(const spl_dense_task* t, int64_t M, int32_t d
   const spl_status xy = check_xy(t->X, M, t->K, t->N, t->Y);
   if (xy != SPL_OK) return xy;
   if (t->K % 8 != 0) return SPL_ERR_UNSUPPORTED;
-  if (*algo == SPL_ALGO_AUTO) *algo = M <= kDecodeMaxM ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
-  if (*algo == SPL_ALGO_DECODE && M > kDecodeMaxM) return SPL_ERR_UNSUPPORTED;
+  if (*algo == SPL_ALGO_AUTO) *algo = decode_fits(M, t->K) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (*algo == SPL_ALGO_DECODE && !decode_fits(M, t->K)) return SPL_ERR_UNSUPPORTED;
   return SPL_OK;
 }
 
@@ -256,8 +253,9 @@ spl_status spl_sparse_linear_silu_mul(const void* X, int64_t M, const spl_matrix
   st = check_sparse_task(X, M, Wup, Y, &au);
   if (st != SPL_OK) return st;
   if (Wup->dtype != Wgate->dtype || Wup->rows != Wgate->rows || Wup->cols != Wgate->cols) return SPL_ERR_INVALID_ARG;
-  if (algo == SPL_ALGO_AUTO) ag = M <= kGatedDecodeMaxM ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
-  if (ag == SPL_ALGO_DECODE && M > kGatedDecodeMaxM) return SPL_ERR_UNSUPPORTED;
+  if (algo == SPL_ALGO_AUTO)
+    ag = M <= kGatedDecodeMaxM && decode_fits(M, Wgate->cols) ? SPL_ALGO_DECODE : SPL_ALGO_PREFILL;
+  if (ag == SPL_ALGO_DECODE && (M > kGatedDecodeMaxM || !decode_fits(M, Wgate->cols))) return SPL_ERR_UNSUPPORTED;
   if (2 * spl::tile_blocks(Wgate->rows) >= kMaxDim) return SPL_ERR_OVERFLOW;
   if (M == 0) return SPL_OK;
   (void)hipGetLastError();

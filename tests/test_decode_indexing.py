@@ -255,3 +255,101 @@ def test_pair_schedule_stays_in_bounds(orc, N, K, s):
                     for j in range(cn):
                         assert 2 * to[j + 1] - a0 + 12 <= alloc          # windows stay in the block's half
         assert (covered == 1).all(), p
+
+
+def _xl_shapes():
+    """(M, K) pairs whose activations the kernels stage in LDS: M * 32S * 2 <= 32 KB."""
+    out = []
+    for K in (8, 24, 64, 520, 1000, 4096, 8200, 11008, 16384):
+        S = -(-K // 32)
+        for M in (1, 2, 3, 5, 16, 31):
+            if M * 32 * S * 2 <= 32 * 1024:
+                out.append((M, K))
+    return out
+
+
+@pytest.mark.parametrize("W", [8, 16])
+def test_activation_staging_covers_each_piece_once(W):
+    """XStager: thread t, round i takes piece p = t + i * threads, i.e. row
+    p // per_row and piece p % per_row, from one division and a step per
+    round; every piece of the copy is written once, loads stay inside X and
+    stores inside the LDS rows."""
+    src = open(SRC).read()
+    for line in ("dm = kThreads / per_row;", "dq = kThreads - dm * per_row;",
+                 "if (q >= per_row) q -= per_row, ++m;",
+                 "if ((int)__umul24(m, per_row) > p) --m;", "if ((int)__umul24(m + 1, per_row) <= p) ++m;",
+                 "static constexpr int kXRounds = kXLdsMax / 16 / kThreads;",
+                 "if (p < total && q < kp)   // 32-bit byte offsets from the uniform base (SGPR-based loads)",
+                 "2u * (__umul24(m, (uint32_t)K) + 8u * (uint32_t)q));",
+                 "if (p < total) *reinterpret_cast<u32x4*>(xs + __umul24(m, stride) + 8 * q) = r[i];"):
+        assert line in src, f"staging changed: update this replay ({line})"
+    threads = 64 * W
+    rounds = 32 * 1024 // 16 // threads
+    for M, K in _xl_shapes():
+        S = -(-K // 32)
+        per_row, kp, total = 4 * S, K // 8, M * 4 * S
+        stride = 32 * S + 8
+        assert rounds * threads >= total
+        dm, dq = threads // per_row, threads - (threads // per_row) * per_row
+        seen = np.zeros(total, dtype=np.int64)
+        for t in range(threads):
+            m = int(np.float32(t) * (np.float32(1.0) / np.float32(per_row)))
+            if m * per_row > t:
+                m -= 1
+            if (m + 1) * per_row <= t:
+                m += 1
+            q = t - m * per_row
+            for i in range(rounds):
+                p = t + i * threads
+                if p < total:
+                    assert (m, q) == divmod(p, per_row), (M, K, t, i)
+                    assert m * K < 1 << 24 and m * stride < 1 << 24
+                    if q < kp:
+                        assert 2 * (m * K + 8 * q) + 16 <= 2 * M * K
+                    assert m * stride + 8 * q + 8 <= M * stride
+                    seen[p] += 1
+                m, q = m + dm, q + dq
+                if q >= per_row:
+                    q, m = q - per_row, m + 1
+        assert (seen == 1).all(), (M, K)
+
+
+@pytest.mark.parametrize("MT", [1, 2])
+@pytest.mark.parametrize("K", [8, 40, 520, 4096, 4104, 11008])
+def test_activation_buffer_offsets(MT, K):
+    """XGlobal: lane (fr, fg) of batch tile t loads 16 bytes at byte offset
+    2 (m K + 8 fg) + 64 s with m = 16t + fr; a row past M, or on the last
+    k-step of a ragged K a column past K, uses an offset beyond X so the
+    hardware returns zeros.  Every other load is inside X and brings exactly
+    X[m][32s + 8fg .. +8]."""
+    src = open(SRC).read()
+    for line in ("constexpr uint32_t kXOob = 0x80000000u;",
+                 "off[t] = m < M ? 2u * ((uint32_t)m * (uint32_t)K + 8u * (uint32_t)fg) : kXOob;",
+                 "if (ragged && (uint32_t)(32 * s + 8 * fg) >= (uint32_t)K) o = kXOob;",
+                 "xb[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, o, 64 * s, 0));",
+                 "if (j < cur.cn) xop.load(xb[j], c0 + j, c0 + j == S - 1 && (K & 31) != 0, fg, K);",
+                 "if (2 * M * kmax > kXBufMax) return hipErrorNotSupported;"):
+        assert line in src, f"activation loads changed: update this replay ({line})"
+    oob = 0x80000000
+    S = -(-K // 32)
+    for M in sorted({1, 2, 7, 16 * MT - 1, 16 * MT} - {0}):
+        nbytes = 2 * M * K
+        assert nbytes <= oob
+        X = np.arange(M * K, dtype=np.int64).reshape(M, K)
+        for s in range(S):
+            ragged = s == S - 1 and K % 32 != 0
+            for lane in range(64):
+                fr, fg = lane & 15, lane >> 4
+                for t in range(MT):
+                    m = 16 * t + fr
+                    o = 2 * (m * K + 8 * fg) if m < M else oob
+                    if ragged and 32 * s + 8 * fg >= K:
+                        o = oob
+                    live = m < M and 32 * s + 8 * fg < K
+                    if o == oob:
+                        assert not live, (M, s, lane, t)
+                        continue                      # the voffset alone is past X: zeros
+                    assert live and o + 64 * s + 16 <= nbytes, (M, s, lane, t)
+                    e = (o + 64 * s) // 2
+                    got = X.ravel()[e:e + 8]
+                    assert (got == X[m, 32 * s + 8 * fg:32 * s + 8 * fg + 8]).all()
