@@ -137,17 +137,15 @@ struct XGlobal {
 // Activations staged in LDS (MT == 1): rows of xs_stride(K) = 32*S + 8
 // elements, zero past K (so a ragged last tile reads zeros), the 16-byte pad
 // spreading rows over the LDS banks.  Lanes of padding batch rows (m >= M)
-// read a 64-byte zero area and do not advance with k.
+// read row 0: an MFMA output column depends only on its own B column, and
+// columns m >= M are never stored, so their operand may hold any data; every
+// lane then reads at a fixed stride of 64 bytes per k-step.
 __host__ __device__ __forceinline__ int64_t xs_stride(int64_t K) { return 32 * tile_steps(K) + 8; }
 
 struct XShared {
-  uint32_t addr;     // LDS byte address of k-step 0 of this lane's operand
-  uint32_t step;     // bytes per k-step: 64, or 0 for padding rows
-  __device__ __forceinline__ XShared(const uint16_t* xs, const u32x4* zero, int M, int64_t K, int fr, int fg) {
-    const bool live = fr < M;
-    const uint16_t* p = xs + (int64_t)fr * xs_stride(K) + 8 * fg;
-    addr = live ? lds_off(p) : lds_off(zero + fg);
-    step = live ? 64u : 0u;
+  uint32_t addr;     // LDS byte address of k-step 0 of this lane's operand (k-step s: + 64 s)
+  __device__ __forceinline__ XShared(const uint16_t* xs, int M, int64_t K, int fr, int fg) {
+    addr = lds_off(xs + (int64_t)(fr < M ? fr : 0) * xs_stride(K) + 8 * fg);
   }
 };
 
@@ -161,7 +159,10 @@ template <int W>
 struct XStager {
   static constexpr int kThreads = W * kWave;
   static constexpr int kXRounds = kXLdsMax / 16 / kThreads;   // staged pieces per thread (bounds M * 4S)
-  u32x4 r[kXRounds];
+  // pieces held in registers between load() and store(); store() copies any
+  // further rounds itself, in batches of kXHold
+  static constexpr int kXHold = kXRounds < 4 ? kXRounds : 4;
+  u32x4 r[kXHold];
   int per_row, total, kp, m0, q0, dm, dq;
   __device__ __forceinline__ void start(int M, int64_t K) {
     per_row = (int)(4 * tile_steps(K));          // 16-byte pieces per staged row (up to 32*S)
@@ -181,12 +182,11 @@ struct XStager {
     q += dq;
     if (q >= per_row) q -= per_row, ++m;
   }
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int M, int64_t K) {
-    start(M, K);
-    int m = m0, q = q0;
+  // rounds [i0, i0 + kXHold) into r, (m, q) the coordinates of round i0
+  __device__ __forceinline__ void load_batch(const uint16_t* __restrict__ X, int64_t K, int i0, int m, int q) {
 #pragma unroll
-    for (int i = 0; i < kXRounds; ++i) {
-      const int p = threadIdx.x + i * kThreads;
+    for (int i = 0; i < kXHold; ++i) {
+      const int p = threadIdx.x + (i0 + i) * kThreads;
       r[i] = u32x4{0u, 0u, 0u, 0u};
       if (p < total && q < kp)   // 32-bit byte offsets from the uniform base (SGPR-based loads)
         r[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const unsigned char*>(X) +
@@ -194,14 +194,27 @@ struct XStager {
       next(m, q);
     }
   }
-  __device__ __forceinline__ void store(uint16_t* xs, int64_t K) const {
-    const uint32_t stride = (uint32_t)xs_stride(K);
-    int m = m0, q = q0;
+  __device__ __forceinline__ void store_batch(uint16_t* xs, uint32_t stride, int i0, int& m, int& q) const {
 #pragma unroll
-    for (int i = 0; i < kXRounds; ++i) {
-      const int p = threadIdx.x + i * kThreads;
+    for (int i = 0; i < kXHold; ++i) {
+      const int p = threadIdx.x + (i0 + i) * kThreads;
       if (p < total) *reinterpret_cast<u32x4*>(xs + __umul24(m, stride) + 8 * q) = r[i];
       next(m, q);
+    }
+  }
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ X, int M, int64_t K) {
+    start(M, K);
+    load_batch(X, K, 0, m0, q0);
+  }
+  __device__ __forceinline__ void store(uint16_t* xs, const uint16_t* __restrict__ X, int64_t K) {
+    const uint32_t stride = (uint32_t)xs_stride(K);
+    int m = m0, q = q0;
+    store_batch(xs, stride, 0, m, q);
+    for (int i0 = kXHold; i0 < kXRounds && threadIdx.x + i0 * kThreads - (threadIdx.x & 63) < total; i0 += kXHold) {
+      load_batch(X, K, i0, m, q);
+      int ms = m, qs = q;
+      store_batch(xs, stride, i0, ms, qs);
+      m = ms, q = qs;
     }
   }
 };
@@ -307,7 +320,6 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   constexpr int C = MT == 1 ? kChunk : kChunk / 2;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
-  __shared__ u32x4 xzero[4];
   // per wave: [row][tile of the chunk]; the row stride C + 2 (even, for the 8-byte pair reads) puts
   // the 16 rows in distinct banks
   constexpr int WS = C + 2;
@@ -375,9 +387,8 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     }
   };
 
-  // prologue: activations, the range's offsets and the first chunk in flight, then the shared tables
-  XStager<W> xst;
-  if constexpr (XL) xst.load(tk.X, M, K);
+  // prologue: the range's offsets, then the first chunk and the activations in flight (offsets first:
+  // loads complete in issue order, and the chunk's addresses wait on them), then the shared tables
   int32_t orng = 0;
   Chunk ch{0, 0u, 0};
   if (kbeg < kend) {
@@ -385,19 +396,19 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     ch = shape(orng, kbeg);
     issue(ch, kbeg);
   }
+  XStager<W> xst;
+  if constexpr (XL) xst.load(tk.X, M, K);
   build_nibble_table(lut);
-  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
-  if constexpr (XL) xst.store(xs, K);
+  if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
 
   using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
   const XOp xop = [&]() {
-    if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
+    if constexpr (XL) return XShared(xs, M, K, fr, fg);
     else return XGlobal<MT>(tk.X, M, K, fr, fg);
   }();
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr = lds_off(vbuf);
-  u32x4 xlive = u32x4{0u, 0u, 0u, 0u};
 
   f32x4 acc[MT];
 #pragma unroll
@@ -435,17 +446,27 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     // 3. expand and multiply the current chunk, two tiles at a time
     const uint32_t vrel = vbuf_addr - cur.a0;          // LDS address of value byte 0 (a multiple of 4 apart)
     uint32_t xaddr = 0;
-    if constexpr (XL) xaddr = xop.addr + xop.step * (uint32_t)c0;
+    if constexpr (XL) xaddr = xop.addr + 64u * (uint32_t)c0;
+    // values stored before mine in each tile: a tile's values are ordered by
+    // column group (my fg), then row (my fr), so this is the exclusive wave scan
+    // of the lanes' kept counts, two tiles per scan in 16-bit halves (sums <=
+    // 512).  The chunk's scans are independent and run together, so their DPP
+    // steps interleave (tiles past the chunk scan staged words no one reads).
+    u32x2 wps[C / 2];
+    uint32_t exs[C / 2];
+#pragma unroll
+    for (int q = 0; q < C / 2; ++q) wps[q] = *reinterpret_cast<const u32x2*>(wl + fr * WS + 2 * q);
+#pragma unroll
+    for (int q = 0; q < C / 2; ++q) {
+      const uint32_t pc = __popc(__builtin_amdgcn_ubfe(wps[q].x, 8 * fg, 8)) |
+                          (__popc(__builtin_amdgcn_ubfe(wps[q].y, 8 * fg, 8)) << 16);
+      exs[q] = wave_inclusive_scan(pc) - pc;
+    }
 #pragma unroll
     for (int jp = 0; jp < C; jp += 2) {
       if (jp < cur.cn) {
-        const u32x2 wp = *reinterpret_cast<const u32x2*>(wl + fr * WS + jp);
-        // values stored before mine in both tiles: a tile's values are ordered by
-        // column group (my fg), then row (my fr), so this is the exclusive wave
-        // scan of the lanes' kept counts (16-bit halves, sums <= 512)
-        const uint32_t pc = __popc(__builtin_amdgcn_ubfe(wp.x, 8 * fg, 8)) |
-                            (__popc(__builtin_amdgcn_ubfe(wp.y, 8 * fg, 8)) << 16);
-        const uint32_t ex = wave_inclusive_scan(pc) - pc;
+        const u32x2 wp = wps[jp / 2];
+        const uint32_t ex = exs[jp / 2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int j = jp + h;
@@ -473,9 +494,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
             a.z = __builtin_amdgcn_perm(uhi, ulo, shi.x);
             a.w = __builtin_amdgcn_perm(uhi, ulo, shi.y);
             if constexpr (XL) {
-              if (xop.step) xlive = lds_load16(xaddr);   // padding rows keep their zero operand
-              acc[0] = Mfma16<T>::run(a, xlive, acc[0]);
-              xaddr += xop.step;
+              acc[0] = Mfma16<T>::run(a, lds_load16(xaddr + 64u * (uint32_t)j), acc[0]);
             } else {
 #pragma unroll
               for (int t = 0; t < MT; ++t) acc[t] = Mfma16<T>::run(a, xb[j][t], acc[t]);
@@ -522,7 +541,6 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   constexpr int C = kChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
-  __shared__ __align__(16) u32x4 xzero[4];
   constexpr int WS = C + 2;                          // word row stride (see k_sparse_decode)
   __shared__ __align__(16) uint32_t words[W][2][16 * WS];
   const int ti = kGated ? 0 : find_task(g.first, g.count);
@@ -593,23 +611,22 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   };
 
   uint16_t* xs = reinterpret_cast<uint16_t*>(dsm + sparse2_vbuf_bytes<W>());
-  XStager<W> xst;
-  if constexpr (XL) xst.load(tk.X, M, K);
   int32_t orng[2] = {0, 0};
   Chunk2 ch{0, {0u, 0u}, {0, 0}};
-  if (kbeg < kend) {
+  if (kbeg < kend) {                                 // offsets first (see k_sparse_decode)
     orng[0] = load_offsets(0, ob);
     orng[1] = load_offsets(1, ob);
     ch = shape(orng, kbeg);
     issue(ch, kbeg);
   }
+  XStager<W> xst;
+  if constexpr (XL) xst.load(tk.X, M, K);
   build_nibble_table(lut);
-  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
-  if constexpr (XL) xst.store(xs, K);
+  if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
 
   const XGlobal<1> xop(tk.X, M, K, fr, fg);
-  const XShared xsh(xs, xzero, M, K, fr, fg);        // (XL only)
+  const XShared xsh(xs, M, K, fr, fg);               // (XL only)
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr[2] = {lds_off(vbuf[0]), lds_off(vbuf[1])};
   f32x4 acc[2][1] = {{f32x4{0.f, 0.f, 0.f, 0.f}}, {f32x4{0.f, 0.f, 0.f, 0.f}}};
@@ -668,10 +685,7 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
         for (int h = 0; h < 2; ++h) {
           const int j = jp + h;
           if (j < cur.cn) {
-            if constexpr (XL) {                      // staged row: zeros past K; padding rows stay zero
-              xb[j][0] = u32x4{0u, 0u, 0u, 0u};
-              if (xsh.step) xb[j][0] = lds_load16(xsh.addr + xsh.step * (uint32_t)(c0 + j));
-            }
+            if constexpr (XL) xb[j][0] = lds_load16(xsh.addr + 64u * (uint32_t)(c0 + j));   // zeros past K
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
               const uint32_t wj = h ? wp[b].y : wp[b].x;
@@ -732,7 +746,6 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const De
   int kbeg, kend;
   wave_range<W>(S, wave, &kbeg, &kend);
   uint16_t* xs = reinterpret_cast<uint16_t*>(dsm);
-  __shared__ u32x4 xzero[4];
   const int64_t row = blk * kDecRows + fr < N ? blk * kDecRows + fr : N - 1;   // rows past N feed discarded outputs
   const uint16_t* wrow = tk.W + row * K + 8 * fg;
   auto load_a = [&](u32x4 (&dst)[C], int c0) {
@@ -748,12 +761,11 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const De
   if constexpr (XL) xst.load(tk.X, M, K);
   u32x4 a[C], an[C];
   if (kbeg < kend) load_a(a, kbeg);
-  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
-  if constexpr (XL) xst.store(xs, K);
+  if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
   using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
   const XOp xop = [&]() {
-    if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
+    if constexpr (XL) return XShared(xs, M, K, fr, fg);
     else return XGlobal<MT>(tk.X, M, K, fr, fg);
   }();
 
@@ -763,12 +775,10 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const De
   for (int c0 = kbeg; c0 < kend; c0 += C) {
     if constexpr (XL) {
       if (c0 + C < kend) load_a(an, c0 + C);
-      uint32_t xaddr = xop.addr + xop.step * (uint32_t)c0;
+      const uint32_t xaddr = xop.addr + 64u * (uint32_t)c0;
 #pragma unroll
-      for (int j = 0; j < C; ++j) {
-        if (c0 + j < kend) acc[0] = Mfma16<T>::run(a[j], lds_load16(xaddr), acc[0]);   // staged columns only
-        xaddr += xop.step;
-      }
+      for (int j = 0; j < C; ++j)
+        if (c0 + j < kend) acc[0] = Mfma16<T>::run(a[j], lds_load16(xaddr + 64u * (uint32_t)j), acc[0]);
     } else {
       u32x4 xb[C][MT];
 #pragma unroll
@@ -835,6 +845,7 @@ int variant(int64_t M, int64_t kmax, int64_t budget) {
 
 // 16 waves per workgroup when the launch has fewer than two row blocks per CU.
 bool small_grid(int64_t blocks) { return blocks < 2 * (int64_t)device_cus(); }
+bool large_grid(int64_t blocks) { return blocks >= 4 * (int64_t)device_cus(); }
 
 // Activation path of the sparse kernels.  One row: staged in LDS when it fits
 // (32 KB).  Two to 16 rows: staged only where the launch has two or more row
@@ -877,7 +888,9 @@ hipError_t sparse_group_t(const SparseGroupArg& g, int64_t kmax, hipStream_t s) 
   const int64_t blocks = g.first[g.count];
   // direct activations of up to 16 rows: pairs of row blocks when the pairs still fill the chip
   if (sparse_variant(g.M, kmax, blocks) == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);
-  return small_grid(blocks) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);
+  if (small_grid(blocks)) return sparse_group_w<T, 16>(g, kmax, s);
+  // four or more row blocks per CU: 4-wave workgroups, so that the whole grid is resident at once
+  return large_grid(blocks) && g.M <= 16 ? sparse_group_w<T, 4>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);
 }
 
 template <class T, int W>

@@ -31,9 +31,10 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
 
 def _constants():
     src = open(SRC).read()
-    assert "return small_grid(blocks) ? sparse_group_w<T, 16>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);" \
+    assert "if (small_grid(blocks)) return sparse_group_w<T, 16>(g, kmax, s);" in src and \
+        "return large_grid(blocks) && g.M <= 16 ? sparse_group_w<T, 4>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);" \
         in src, "waves per workgroup changed: update this replay"
-    waves = (8, 16)
+    waves = (4, 8, 16)
     chunk = int(re.search(r"constexpr int kChunk = (\d+);", src).group(1))
     assert "constexpr int C = MT == 1 ? kChunk : kChunk / 2;" in src, "chunk size formula changed: update this replay"
     vbuf = int(re.search(r"constexpr int kVBuf = (\d+);", src).group(1))
@@ -104,7 +105,7 @@ def _replay(T, N, K, MT, W):
         assert (covered == 1).all(), b
 
 
-@pytest.mark.parametrize("W", [8, 16])
+@pytest.mark.parametrize("W", [4, 8, 16])
 @pytest.mark.parametrize("MT", [1, 2])
 @pytest.mark.parametrize("N,K,s", [(16, 8, 0.5), (33, 40, 0.0), (20, 264, 0.7), (17, 520, 1.0), (48, 1064, 0.5),
                                    (16, 4096, 0.0), (32, 4104, 0.7), (16, 11008, 0.5), (16, 16384, 0.0),
@@ -268,7 +269,7 @@ def _xl_shapes():
     return out
 
 
-@pytest.mark.parametrize("W", [8, 16])
+@pytest.mark.parametrize("W", [4, 8, 16])
 def test_activation_staging_covers_each_piece_once(W):
     """XStager: thread t, round i takes piece p = t + i * threads, i.e. row
     p // per_row and piece p % per_row, from one division and a step per
