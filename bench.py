@@ -98,7 +98,7 @@ def make_activations(dtype: str, mmax: int):
     return xs
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sparse_decode_llama7b_layer_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sparse_decode_llama7b_stack_traffic.txt")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2405_03594_amd", "csrc", f) for f in ("k_decode.hip", "spl_common.h")]
 
 
