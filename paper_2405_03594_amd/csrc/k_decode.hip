@@ -137,15 +137,19 @@ struct XGlobal {
 // Activations staged in LDS (MT == 1): rows of xs_stride(K) = 32*S + 8
 // elements, zero past K (so a ragged last tile reads zeros), the 16-byte pad
 // spreading rows over the LDS banks.  Lanes of padding batch rows (m >= M)
-// read row 0: an MFMA output column depends only on its own B column, and
-// columns m >= M are never stored, so their operand may hold any data; every
-// lane then reads at a fixed stride of 64 bytes per k-step.
+// read a 64-byte zero area and do not advance with k; their reads are
+// masked off where the operand is kept in a register (one row at M = 1, so
+// the activation reads move 64 bytes per tile instead of 1 KB).
 __host__ __device__ __forceinline__ int64_t xs_stride(int64_t K) { return 32 * tile_steps(K) + 8; }
 
 struct XShared {
-  uint32_t addr;     // LDS byte address of k-step 0 of this lane's operand (k-step s: + 64 s)
-  __device__ __forceinline__ XShared(const uint16_t* xs, int M, int64_t K, int fr, int fg) {
-    addr = lds_off(xs + (int64_t)(fr < M ? fr : 0) * xs_stride(K) + 8 * fg);
+  uint32_t addr;     // LDS byte address of k-step 0 of this lane's operand
+  uint32_t step;     // bytes per k-step: 64, or 0 for padding rows
+  __device__ __forceinline__ XShared(const uint16_t* xs, const u32x4* zero, int M, int64_t K, int fr, int fg) {
+    const bool live = fr < M;
+    const uint16_t* p = xs + (int64_t)fr * xs_stride(K) + 8 * fg;
+    addr = live ? lds_off(p) : lds_off(zero + fg);
+    step = live ? 64u : 0u;
   }
 };
 
@@ -320,6 +324,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   constexpr int C = MT == 1 ? kChunk : kChunk / 2;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
+  __shared__ u32x4 xzero[4];
   // per wave: [row][tile of the chunk]; the row stride C + 2 (even, for the 8-byte pair reads) puts
   // the 16 rows in distinct banks
   constexpr int WS = C + 2;
@@ -399,16 +404,18 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   XStager<W> xst;
   if constexpr (XL) xst.load(tk.X, M, K);
   build_nibble_table(lut);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
   if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
 
   using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
   const XOp xop = [&]() {
-    if constexpr (XL) return XShared(xs, M, K, fr, fg);
+    if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
     else return XGlobal<MT>(tk.X, M, K, fr, fg);
   }();
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr = lds_off(vbuf);
+  u32x4 xlive = u32x4{0u, 0u, 0u, 0u};
 
   f32x4 acc[MT];
 #pragma unroll
@@ -446,7 +453,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     // 3. expand and multiply the current chunk, two tiles at a time
     const uint32_t vrel = vbuf_addr - cur.a0;          // LDS address of value byte 0 (a multiple of 4 apart)
     uint32_t xaddr = 0;
-    if constexpr (XL) xaddr = xop.addr + 64u * (uint32_t)c0;
+    if constexpr (XL) xaddr = xop.addr + xop.step * (uint32_t)c0;
     // values stored before mine in each tile: a tile's values are ordered by
     // column group (my fg), then row (my fr), so this is the exclusive wave scan
     // of the lanes' kept counts, two tiles per scan in 16-bit halves (sums <=
@@ -494,7 +501,9 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
             a.z = __builtin_amdgcn_perm(uhi, ulo, shi.x);
             a.w = __builtin_amdgcn_perm(uhi, ulo, shi.y);
             if constexpr (XL) {
-              acc[0] = Mfma16<T>::run(a, lds_load16(xaddr + 64u * (uint32_t)j), acc[0]);
+              if (xop.step) xlive = lds_load16(xaddr);   // padding rows keep their zero operand
+              acc[0] = Mfma16<T>::run(a, xlive, acc[0]);
+              xaddr += xop.step;
             } else {
 #pragma unroll
               for (int t = 0; t < MT; ++t) acc[t] = Mfma16<T>::run(a, xb[j][t], acc[t]);
@@ -541,6 +550,7 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   constexpr int C = kChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
+  __shared__ __align__(16) u32x4 xzero[4];
   constexpr int WS = C + 2;                          // word row stride (see k_sparse_decode)
   __shared__ __align__(16) uint32_t words[W][2][16 * WS];
   const int ti = kGated ? 0 : find_task(g.first, g.count);
@@ -622,11 +632,12 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   XStager<W> xst;
   if constexpr (XL) xst.load(tk.X, M, K);
   build_nibble_table(lut);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
   if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
 
   const XGlobal<1> xop(tk.X, M, K, fr, fg);
-  const XShared xsh(xs, M, K, fr, fg);               // (XL only)
+  const XShared xsh(xs, xzero, M, K, fr, fg);        // (XL only)
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr[2] = {lds_off(vbuf[0]), lds_off(vbuf[1])};
   f32x4 acc[2][1] = {{f32x4{0.f, 0.f, 0.f, 0.f}}, {f32x4{0.f, 0.f, 0.f, 0.f}}};
@@ -685,7 +696,10 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
         for (int h = 0; h < 2; ++h) {
           const int j = jp + h;
           if (j < cur.cn) {
-            if constexpr (XL) xb[j][0] = lds_load16(xsh.addr + 64u * (uint32_t)(c0 + j));   // zeros past K
+            if constexpr (XL) {                      // staged row: zeros past K; padding rows stay zero
+              xb[j][0] = u32x4{0u, 0u, 0u, 0u};
+              if (xsh.step) xb[j][0] = lds_load16(xsh.addr + xsh.step * (uint32_t)(c0 + j));
+            }
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
               const uint32_t wj = h ? wp[b].y : wp[b].x;
@@ -734,6 +748,7 @@ template <class T, int MT, bool XL, int W>
 __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const DenseGroupArg g) {
   constexpr int C = kDenseChunk;
   extern __shared__ __align__(16) unsigned char dsm[];
+  __shared__ u32x4 xzero[4];
   const int ti = find_task(g.first, g.count);
   const DenseTaskArg tk = g.t[ti];
   const int M = g.M;
@@ -761,11 +776,12 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const De
   if constexpr (XL) xst.load(tk.X, M, K);
   u32x4 a[C], an[C];
   if (kbeg < kend) load_a(a, kbeg);
+  if (threadIdx.x < 4) xzero[threadIdx.x] = u32x4{0u, 0u, 0u, 0u};
   if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
   using XOp = std::conditional_t<XL, XShared, XGlobal<MT>>;
   const XOp xop = [&]() {
-    if constexpr (XL) return XShared(xs, M, K, fr, fg);
+    if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
     else return XGlobal<MT>(tk.X, M, K, fr, fg);
   }();
 
@@ -775,10 +791,12 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_dense_decode(const De
   for (int c0 = kbeg; c0 < kend; c0 += C) {
     if constexpr (XL) {
       if (c0 + C < kend) load_a(an, c0 + C);
-      const uint32_t xaddr = xop.addr + 64u * (uint32_t)c0;
+      uint32_t xaddr = xop.addr + xop.step * (uint32_t)c0;
 #pragma unroll
-      for (int j = 0; j < C; ++j)
-        if (c0 + j < kend) acc[0] = Mfma16<T>::run(a[j], lds_load16(xaddr + 64u * (uint32_t)j), acc[0]);
+      for (int j = 0; j < C; ++j) {
+        if (c0 + j < kend) acc[0] = Mfma16<T>::run(a[j], lds_load16(xaddr), acc[0]);   // staged columns only
+        xaddr += xop.step;
+      }
     } else {
       u32x4 xb[C][MT];
 #pragma unroll
