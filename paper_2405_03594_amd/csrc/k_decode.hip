@@ -519,10 +519,10 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   reduce_store<T, MT, W>(reinterpret_cast<float*>(dsm), acc, M, blk * kDecRows, tk.N, tk.Y);
 }
 
-// Two row blocks per workgroup, for batches of up to 16 rows whose activations
-// are loaded directly: every wave walks the same k-range of both blocks, so
-// each activation load feeds two MFMAs (halving the activation loads, which
-// bound this case).  Each block keeps its own offsets window, half of the
+// Two row blocks per workgroup, for batches whose activations are loaded
+// directly (MT batch tiles of 16 rows): every wave walks the same k-range of
+// both blocks, so each activation load feeds two MFMAs per batch tile (halving
+// the activation loads, which bound this case).  Each block keeps its own offsets window, half of the
 // staging buffer, regrouped words and accumulator; a chunk is as many tiles as
 // fit both halves.  The second block of a pair past the last row block aliases
 // the first with zero words and is not stored.  Otherwise the same steps as
@@ -545,9 +545,11 @@ struct Chunk2 {
 // silu(gate) * up (silu(z) = z / (1 + e^-z), from the fp32 sums) into task 0's Y.
 // XL (one activation row): the row is staged in LDS after the value buffers,
 // as in k_sparse_decode, and both blocks' MFMAs read it from there.
-template <class T, int W, bool kGated, bool XL = false>
+template <class T, int W, bool kGated, bool XL = false, int MT = 1>
 __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGroupArg g) {
-  constexpr int C = kChunk;
+  static_assert(MT == 1 || (!kGated && !XL), "two batch tiles: plain products with direct activations");
+  static_assert((size_t)W * MT * 256 * sizeof(float) <= sparse2_vbuf_bytes<W>(), "one block's partial sums fit");
+  constexpr int C = MT == 1 ? kChunk : kChunk / 2;
   extern __shared__ __align__(16) unsigned char dsm[];
   __shared__ u32x2 lut[16];
   __shared__ __align__(16) u32x4 xzero[4];
@@ -636,11 +638,15 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
   if constexpr (XL) xst.store(xs, tk.X, K);
   __syncthreads();
 
-  const XGlobal<1> xop(tk.X, M, K, fr, fg);
+  const XGlobal<MT> xop(tk.X, M, K, fr, fg);
   const XShared xsh(xs, xzero, M, K, fr, fg);        // (XL only)
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr[2] = {lds_off(vbuf[0]), lds_off(vbuf[1])};
-  f32x4 acc[2][1] = {{f32x4{0.f, 0.f, 0.f, 0.f}}, {f32x4{0.f, 0.f, 0.f, 0.f}}};
+  f32x4 acc[2][MT];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[b][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int c0 = kbeg; c0 < kend;) {
     // 1. stage the current chunk of both blocks
@@ -661,7 +667,7 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
       for (int j = 0; j < C; ++j) tc[b][j] = __builtin_amdgcn_readlane(orng[b], c0 - ob + j);
 
     // 2. the chunk's activations, then the next chunk's loads
-    u32x4 xb[C][1];
+    u32x4 xb[C][MT];
     if constexpr (!XL) {
 #pragma unroll
       for (int j = 0; j < C; ++j)
@@ -722,7 +728,8 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
               a.y = __builtin_amdgcn_perm(vhi, vlo, slo.y);
               a.z = __builtin_amdgcn_perm(uhi, ulo, shi.x);
               a.w = __builtin_amdgcn_perm(uhi, ulo, shi.y);
-              acc[b][0] = Mfma16<T>::run(a, xb[j][0], acc[b][0]);
+#pragma unroll
+              for (int t = 0; t < MT; ++t) acc[b][t] = Mfma16<T>::run(a, xb[j][t], acc[b][t]);
             }
           }
         }
@@ -737,10 +744,10 @@ __global__ void __launch_bounds__(W * kWave, 4) k_sparse_decode2(const SparseGro
     reduce_store_gated<T, W>(red, acc[0][0], acc[1][0], M, blk0 * kDecRows, tk.N, tk.Y);
     return;
   }
-  reduce_store<T, 1, W>(red, acc[0], M, blk0 * kDecRows, tk.N, tk.Y);
+  reduce_store<T, MT, W>(red, acc[0], M, blk0 * kDecRows, tk.N, tk.Y);
   if (live1) {
     __syncthreads();                                   // the first block's sums are read before red is reused
-    reduce_store<T, 1, W>(red, acc[1], M, (blk0 + 1) * kDecRows, tk.N, tk.Y);
+    reduce_store<T, MT, W>(red, acc[1], M, (blk0 + 1) * kDecRows, tk.N, tk.Y);
   }
 }
 
@@ -886,14 +893,14 @@ hipError_t sparse_group_w(const SparseGroupArg& g, int64_t kmax, hipStream_t s) 
   }
 }
 
-// Two row blocks per workgroup (direct activations, M <= 16): the same group
-// with each task's workgroups counted in pairs of row blocks.
-template <class T, int W>
+// Two row blocks per workgroup (direct activations, MT batch tiles): the same
+// group with each task's workgroups counted in pairs of row blocks.
+template <class T, int W, int MT>
 hipError_t sparse_pair_launch(const SparseGroupArg& g1, hipStream_t s) {
   SparseGroupArg g = g1;
   for (int i = 0; i < g.count; ++i)
     g.first[i + 1] = g.first[i] + (int32_t)((tile_blocks(g1.t[i].N) + 1) / 2);
-  auto* kernel = k_sparse_decode2<T, W, false>;
+  auto* kernel = k_sparse_decode2<T, W, false, false, MT>;
   static PerDeviceFlag lds_set;
   const hipError_t attr = allow_lds_once(lds_set, kernel, sparse2_vbuf_bytes<W>());
   if (attr != hipSuccess) return attr;
@@ -904,8 +911,10 @@ hipError_t sparse_pair_launch(const SparseGroupArg& g1, hipStream_t s) {
 template <class T>
 hipError_t sparse_group_t(const SparseGroupArg& g, int64_t kmax, hipStream_t s) {
   const int64_t blocks = g.first[g.count];
-  // direct activations of up to 16 rows: pairs of row blocks when the pairs still fill the chip
-  if (sparse_variant(g.M, kmax, blocks) == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);
+  // direct activations of more than 4 rows: pairs of row blocks when the pairs still fill the chip
+  const int v = sparse_variant(g.M, kmax, blocks);
+  if (v == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8, 1>(g, s);
+  if (v == 2 && !small_grid(blocks)) return sparse_pair_launch<T, 8, 2>(g, s);
   if (small_grid(blocks)) return sparse_group_w<T, 16>(g, kmax, s);
   // four or more row blocks per CU: 4-wave workgroups, so that the whole grid is resident at once
   return large_grid(blocks) && g.M <= 16 ? sparse_group_w<T, 4>(g, kmax, s) : sparse_group_w<T, 8>(g, kmax, s);

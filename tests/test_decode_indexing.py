@@ -203,8 +203,10 @@ def _pair_constants():
     assert "constexpr int kHalfPieceRounds = (kHalfVBuf / 16 + kWave - 1) / kWave;" in src
     assert "const uint32_t lim = (ch.a0[b] + kHalfVBuf) >> 1;" in src and "cn = cb < cn ? cb : cn;" in src, \
         "pair chunk rule changed: update this replay"
-    assert "if (sparse_variant(g.M, kmax, blocks) == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8>(g, s);" \
-        in src, "pair launch rule changed: update this replay"
+    assert "if (v == 1 && g.M > 4 && !small_grid(blocks)) return sparse_pair_launch<T, 8, 1>(g, s);" in src and \
+        "if (v == 2 && !small_grid(blocks)) return sparse_pair_launch<T, 8, 2>(g, s);" in src, \
+        "pair launch rule changed: update this replay"
+    assert "constexpr int C = MT == 1 ? kChunk : kChunk / 2;" in src, "pair chunk length changed: update this replay"
     half = vbuf // 2
     return half, half + 16, -(-(half // 16) // 64)
 
@@ -235,9 +237,10 @@ def _pair_chunks(tobs, kbeg, kend, C, half):
 
 @pytest.mark.parametrize("N,K,s", [(16, 1056, 0.5), (48, 1056, 0.7), (40, 3296, 0.0), (17, 11008, 0.5),
                                    (33, 4096, 0.9), (16, 65552, 0.7)])
-def test_pair_schedule_stays_in_bounds(orc, N, K, s):
+@pytest.mark.parametrize("MT", [1, 2])
+def test_pair_schedule_stays_in_bounds(orc, N, K, s, MT):
     half, alloc, rounds = _pair_constants()
-    C = _constants()[1][1]
+    C = _constants()[1][1] // MT             # kChunk tiles per chunk, half of them with two batch tiles
     W, mask = synth.weight(61 + N, N, K, "bf16", s)
     T = orc.pack_tiled(W, "bf16", mask)
     S, B = -(-K // 32), -(-N // 16)

@@ -205,13 +205,15 @@ def test_decode_long_rows(orc, spl, s):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
-@pytest.mark.parametrize("N,K,M", [(8200, 1056, 16), (8200, 3296, 5), (8192, 2112, 9)])
+@pytest.mark.parametrize("N,K,M", [(8200, 1056, 16), (8200, 3296, 5), (8192, 2112, 9), (8200, 1056, 17),
+                                   (8200, 3296, 32), (8192, 4096, 31)])
 def test_decode_row_block_pairs(orc, spl, dtype, N, K, M):
     """Launches of at least 512 row blocks whose activations are loaded directly
-    (M x K too large to stage in LDS) run two row blocks per workgroup: an
-    odd row-block count (8200 rows = 512 blocks + a ragged 8-row block, the
-    last pair half empty) and an even one, compared in full with the oracle,
-    and as one task of a group with a smaller matrix."""
+    (M x K too large to stage in LDS) run two row blocks per workgroup, with
+    one batch tile up to 16 rows and two above: an odd row-block count (8200
+    rows = 512 blocks + a ragged 8-row block, the last pair half empty) and an
+    even one, compared in full with the oracle, and as one task of a group
+    with a smaller matrix."""
     W, mask = synth.weight(950 + M, N, K, dtype, 0.7)
     X = synth.activations(951, M, K, dtype)
     ref = orc.linear_f64(X, orc.pack(W, dtype, mask))
