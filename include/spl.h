@@ -223,8 +223,10 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
  *   type.  dY [M][N] and X [M][K] of Wc->dtype; Wc in the tile layout;
  *   grad_values out, nnz entries.  Requires M % 8 == 0 (M == 0:
  *   SPL_ERR_UNSUPPORTED), K % 8 == 0, M <= 4194240.  workspace: device
- *   scratch of spl_sparse_weight_grad_workspace_bytes(M, N, K) bytes,
- *   256-byte aligned, caller-owned (transposed dY and X and the dense product).
+ *   scratch of spl_sparse_weight_grad_workspace_bytes(M, N, K) bytes
+ *   (2 M (N + K) rounded up: the transposes of dY and X; no [N][K] buffer),
+ *   256-byte aligned, caller-owned.  The product's epilogue writes the kept
+ *   entries directly; nothing else of grad_values is touched.
  * spl_sparse_sgd_update: Wc->values[i] = RNE(v - lr * g) with v, g decoded
  *   from the payloads and each operation rounded to binary32; in place.
  * The input gradient dX = dY (W.Mask) is spl_sparse_linear(dY, Wt) with Wt the

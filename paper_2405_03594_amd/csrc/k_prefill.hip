@@ -297,7 +297,62 @@ struct PfArgs {
   const float* sx;               // int8: activation scales [M]
   const float* sw;               // int8: weight scales [N]
   int32_t* acc;                  // int8: optional exact sums [M][N]
+  const uint32_t* gbm;           // gather: tile pattern of the [M][N] product (bitmask words)
+  const int32_t* gtoff;          // gather: its tile offsets
+  uint16_t* gval;                // gather: out, the kept entries in the pattern's value order
 };
+
+// The gather epilogue (weight gradients): the product Y [M][N] is only wanted
+// at the kept positions of a tile pattern of tile_blocks(M) x tile_steps(N)
+// tiles, in its value order, so no dense Y is written.  A 16 x 32 tile is
+// fragments (j, 2p) and (j, 2p + 1) of a wave: in the D layout lane l holds
+// tile row l % 16 and tile columns 16 h + 4 (l / 16) + r (r < 4) of fragment
+// 2p + h.  A tile's values are ordered by 8-column group, then row, then
+// column (the decode kernels' lane order), so a kept entry's index is the
+// tile offset + the kept entries of the column groups left of its own (all
+// rows) + those of its group in the rows above + those left of it in its row
+// and group.  The per-group counts of the 16 rows are scanned in one 16-lane
+// DPP scan (four 8-bit fields; a field sums at most 16 x 8 = 128).  Values
+// are rounded once to the payload type.
+template <class T, int FN>
+__device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][4], const PfArgs& g, int64_t n0, int64_t m0,
+                                                int wn, int wm, int lane) {
+  const int64_t B = tile_blocks(g.M);
+  const int64_t S = tile_steps(g.N);
+  const int fr = lane & 15, q = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int64_t b = (m0 + wm * 64) / 16 + j;
+    if (b >= B) break;                                         // wave-uniform; later j lie further out
+#pragma unroll
+    for (int p = 0; p < FN / 2; ++p) {
+      const int64_t st = (n0 + wn * 16 * FN) / 32 + p;
+      if (st >= S) break;
+      const int64_t t = b * S + st;
+      const uint32_t w = g.gbm[t * 16 + fr];                   // my row's word
+      const uint32_t c = __popc(w & 0xffu) | (__popc((w >> 8) & 0xffu) << 8) | (__popc((w >> 16) & 0xffu) << 16) |
+                         (__popc(w >> 24) << 24);
+      const uint32_t incl = row16_inclusive_scan(c);
+      const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 15);   // every 16-lane row: the same tile
+      const uint32_t above = incl - c;                         // per group: rows above mine
+      const uint32_t base = (uint32_t)g.gtoff[t];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int col = 16 * h + 4 * q;                        // my first tile column in this fragment
+        const int f = col >> 3;                                // its 8-column group
+        uint32_t idx = base + __builtin_amdgcn_ubfe(above, 8 * f, 8);
+        if (f > 0) idx += tot & 0xffu;
+        if (f > 1) idx += (tot >> 8) & 0xffu;
+        if (f > 2) idx += (tot >> 16) & 0xffu;
+        if (col & 4) idx += __popc(__builtin_amdgcn_ubfe(w, 8 * f, 4));
+        const uint32_t nib = __builtin_amdgcn_ubfe(w, col, 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if ((nib >> r) & 1u) g.gval[idx++] = T::from_f32(acc[2 * p + h][j][r]);
+      }
+    }
+  }
+}
 
 // kGated: the workgroup's BN virtual rows are BN/32 row blocks of the gate and
 // of the up matrix, alternating (wave w expands virtual block w: matrix w % 2,
@@ -505,7 +560,9 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
   }
 }
 
-template <class T, int BN, int BM, int NW, int KS, bool kChecked>
+// kGather: only the kept entries of the product at a tile pattern are written
+// (pf_store_gather), for 16-bit payloads.
+template <class T, int BN, int BM, int NW, int KS, bool kChecked, bool kGather = false>
 __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(const PfArgs g) {
   extern __shared__ __align__(16) unsigned char dsm[];
   constexpr bool kI8 = std::is_same<T, I8P>::value;
@@ -578,9 +635,12 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(c
     step(st, x0, w0, x1, w1);                          // stage st + 2 -> set 0, stage st + 1 from set 1
     if (st + 1 < nh) step(st + 1, x1, w1, x0, w0);     // stage st + 3 -> set 1, stage st + 2 from set 0
   }
+  static_assert(!kGather || (!kI8 && FN % 2 == 0), "gather: 16-bit payloads, whole tiles per wave");
   if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) {
     if constexpr (kI8)
       pf_store_i8<FN>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+    else if constexpr (kGather)
+      pf_store_gather<T, FN>(acc, g, n0, m0, wn, wm, lane);
     else
       pf_store<T, FN>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
   }
@@ -644,9 +704,9 @@ hipError_t gated_prefill_t(const PfArgs& a, hipStream_t s) {
   return pf_split_k(Nv, a.M) ? gated_prefill_tile<T, 64, 128, 4, 2>(a, s) : gated_prefill_tile<T, 64, 128, 4, 1>(a, s);
 }
 
-template <class T, int BN, int BM, int NW, int KS, bool kChecked>
+template <class T, int BN, int BM, int NW, int KS, bool kChecked, bool kGather>
 hipError_t dense_prefill_launch(const PfArgs& a, hipStream_t s) {
-  auto* kernel = k_dense_prefill<T, BN, BM, NW, KS, kChecked>;
+  auto* kernel = k_dense_prefill<T, BN, BM, NW, KS, kChecked, kGather>;
   static PerDeviceFlag lds_set;
   const hipError_t attr = allow_lds_once(lds_set, kernel, KS * pf_lds(BN, BM));
   if (attr != hipSuccess) return attr;
@@ -655,17 +715,18 @@ hipError_t dense_prefill_launch(const PfArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <class T, int BN, int BM, int NW, int KS>
+template <class T, int BN, int BM, int NW, int KS, bool kGather>
 hipError_t dense_prefill_tile(const PfArgs& a, hipStream_t s) {
-  return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? dense_prefill_launch<T, BN, BM, NW, KS, false>(a, s)
-                                                       : dense_prefill_launch<T, BN, BM, NW, KS, true>(a, s);
+  return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM)
+             ? dense_prefill_launch<T, BN, BM, NW, KS, false, kGather>(a, s)
+             : dense_prefill_launch<T, BN, BM, NW, KS, true, kGather>(a, s);
 }
 
-template <class T>
+template <class T, bool kGather = false>
 hipError_t dense_prefill_t(const PfArgs& a, hipStream_t s) {
-  if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1>(a, s);
-  return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2>(a, s)
-                              : dense_prefill_tile<T, 64, 128, 4, 1>(a, s);
+  if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1, kGather>(a, s);
+  return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2, kGather>(a, s)
+                              : dense_prefill_tile<T, 64, 128, 4, 1, kGather>(a, s);
 }
 
 }  // namespace
@@ -690,6 +751,19 @@ hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t
   a.M = M, a.N = N, a.K = K;
   a.Y = static_cast<uint16_t*>(Y);
   return dtype == SPL_BF16 ? dense_prefill_t<Bf16>(a, s) : dense_prefill_t<F16>(a, s);
+}
+
+// The kept entries of X W^T at the tile pattern P ([M][N], P.rows == M,
+// P.cols == N), in P's value order; no dense product is written.
+hipError_t launch_dense_prefill_gather(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                                       const spl_matrix& P, void* values, hipStream_t s) {
+  if (P.rows != M || P.cols != N) return hipErrorInvalidValue;
+  PfArgs a{};
+  a.X = static_cast<const uint16_t*>(X);
+  a.W = static_cast<const uint16_t*>(W);
+  a.M = M, a.N = N, a.K = K;
+  a.gbm = P.bitmask, a.gtoff = P.tile_offsets, a.gval = static_cast<uint16_t*>(values);
+  return dtype == SPL_BF16 ? dense_prefill_t<Bf16, true>(a, s) : dense_prefill_t<F16, true>(a, s);
 }
 
 // Gated half of a Llama MLP: Y = silu(X Wg^T) * (X Wu^T) (same dtype and shape).

@@ -5,11 +5,14 @@
 // Weight gradient G = Mask . (dY^T X): both operands are [M][*] row-major and
 // the reduction runs over M, so dY and X are first transposed (LDS-tiled
 // copies) into [N][M] and [K][M]; the dense prefill kernel then computes
-// G = dY^T X as an M-deep product on the matrix cores ([N][K], payload type,
-// fp32 sums); finally the kept entries are gathered into the tile layout's
-// value order (the inverse of the decode kernels' expansion: lane (fr, fg) of
-// a tile's wave owns row fr, columns 8 fg .. 8 fg + 7, and its values start
-// at the exclusive wave scan of the lanes' kept counts).
+// dY^T X as an M-deep product on the matrix cores (fp32 sums) and its
+// epilogue writes only the kept entries, rounded once to the payload type,
+// straight into the tile layout's value order: no dense [N][K] gradient is
+// formed, and the workspace holds only the two transposes.
+//
+// k_gather_tiled (spl_gather_tiled) is the stand-alone form of that order:
+// lane (fr, fg) of a tile's wave owns row fr, columns 8 fg .. 8 fg + 7, and
+// its values start at the exclusive wave scan of the lanes' kept counts.
 #include "spl_common.h"
 
 namespace spl {
@@ -34,6 +37,37 @@ __global__ void __launch_bounds__(256) k_transpose16(const uint16_t* __restrict_
   for (int i = ty; i < kTT; i += 4) {
     const int64_t c = c0 + i, r = r0 + tx;
     if (c < C && r < R) dst[c * R + r] = tile[tx][i];
+  }
+}
+
+// The same transpose for R % 8 == 0 and C % 8 == 0 (16-byte aligned rows):
+// each thread moves one 8 x 8 block with eight 16-byte loads (rows r..r+7,
+// columns c..c+7), a register transpose (v_perm_b32 picks the 16-bit halves)
+// and eight 16-byte stores (rows c..c+7 of dst, columns r..r+7).  Lane
+// 8 y + x of a wave takes block (8 y, 8 x) of its 64 x 64 tile: per load the
+// eight lanes of one y read one 128-byte segment of a src row, and per store
+// the eight lanes of one x write one 128-byte segment of a dst row.  Four
+// waves per workgroup take four tiles along the columns.
+constexpr int kT8Tile = 64;
+__global__ void __launch_bounds__(256) k_transpose16_b8(const uint16_t* __restrict__ src, int64_t R, int64_t C,
+                                                        uint16_t* __restrict__ dst) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t r = (int64_t)blockIdx.y * kT8Tile + 8 * (lane >> 3);                 // block's first row
+  const int64_t c = ((int64_t)blockIdx.x * 4 + wave) * kT8Tile + 8 * (lane & 7);   // and first column
+  if (r >= R || c >= C) return;                      // whole blocks: R % 8 == C % 8 == 0
+  u32x4 v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = *reinterpret_cast<const u32x4*>(src + (r + i) * C + c);
+  // o[j] = column j of the block: its dword d holds rows 2d (low half) and 2d + 1 (high half)
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    u32x4 o;
+    o.x = __builtin_amdgcn_perm(v[1][j >> 1], v[0][j >> 1], sel);
+    o.y = __builtin_amdgcn_perm(v[3][j >> 1], v[2][j >> 1], sel);
+    o.z = __builtin_amdgcn_perm(v[5][j >> 1], v[4][j >> 1], sel);
+    o.w = __builtin_amdgcn_perm(v[7][j >> 1], v[6][j >> 1], sel);
+    *reinterpret_cast<u32x4*>(dst + (c + j) * R + r) = o;
   }
 }
 
@@ -116,6 +150,13 @@ constexpr int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
 }  // namespace
 
 hipError_t launch_transpose16(const void* src, int64_t R, int64_t C, void* dst, hipStream_t s) {
+  if (R % 8 == 0 && C % 8 == 0 && reinterpret_cast<uintptr_t>(src) % 16 == 0 &&
+      reinterpret_cast<uintptr_t>(dst) % 16 == 0) {
+    const dim3 grid((unsigned)((C + 4 * kT8Tile - 1) / (4 * kT8Tile)), (unsigned)((R + kT8Tile - 1) / kT8Tile));
+    hipLaunchKernelGGL(k_transpose16_b8, grid, dim3(256), 0, s, static_cast<const uint16_t*>(src), R, C,
+                       static_cast<uint16_t*>(dst));
+    return hipGetLastError();
+  }
   const dim3 grid((unsigned)((C + kTT - 1) / kTT), (unsigned)((R + kTT - 1) / kTT));
   hipLaunchKernelGGL(k_transpose16, grid, dim3(256), 0, s, static_cast<const uint16_t*>(src), R, C,
                      static_cast<uint16_t*>(dst));
@@ -131,7 +172,7 @@ hipError_t launch_gather_tiled(const void* dense, const spl_matrix& P, void* val
 }
 
 int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-  return align256(2 * N * M) + align256(2 * K * M) + align256(2 * N * K);
+  return align256(2 * N * M) + align256(2 * K * M);
 }
 
 hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
@@ -140,11 +181,10 @@ hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const sp
   unsigned char* base = static_cast<unsigned char*>(ws);
   void* dYt = base;                                  // [N][M]
   void* Xt = base + align256(2 * N * M);             // [K][M]
-  void* G = base + align256(2 * N * M) + align256(2 * K * M);   // [N][K]
   hipError_t e = launch_transpose16(dY, M, N, dYt, s);
   if (e == hipSuccess) e = launch_transpose16(X, M, K, Xt, s);
-  if (e == hipSuccess) e = launch_dense_prefill(dYt, N, Xt, Wc.dtype, K, M, G, s);   // G = dYt Xt^T
-  if (e == hipSuccess) e = launch_gather_tiled(G, Wc, grad_values, s);   // nnz > 0 (checked by the caller)
+  // the kept entries of dYt Xt^T ([N][K], Wc's pattern) in Wc's value order
+  if (e == hipSuccess) e = launch_dense_prefill_gather(dYt, N, Xt, Wc.dtype, K, M, Wc, grad_values, s);
   return e;
 }
 

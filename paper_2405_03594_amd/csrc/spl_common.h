@@ -206,6 +206,10 @@ hipError_t launch_dense_decode(const spl_dense_task* tasks, int count, int64_t M
 hipError_t launch_sparse_prefill(const void* X, int64_t M, const spl_matrix& Wc, void* Y, hipStream_t s);
 hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
                                 void* Y, hipStream_t s);
+// The same product written only at the kept positions of the tile pattern P
+// (P.rows == M, P.cols == N), in P's value order (fp16/bf16).
+hipError_t launch_dense_prefill_gather(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
+                                       const spl_matrix& P, void* values, hipStream_t s);
 // Sparse-quantized kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
 hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s);
 hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s);

@@ -343,7 +343,10 @@ def test_training_argument_checks(L):
     assert g(A, ctypes.byref(_mat()), G, None) == UNSUPPORTED                 # row layout
     assert g(A, ctypes.byref(_mat(dtype=3, layout=1, tile_offsets=0x40000)), G, None) == UNSUPPORTED
     w = L.spl_sparse_weight_grad
-    assert L.spl_sparse_weight_grad_workspace_bytes(16, 4, 64) >= 2 * (4 * 16 + 64 * 16 + 4 * 64)
+    a256 = lambda b: -(-b // 256) * 256
+    # the transposes of dY [16][4] and X [16][64] only: no dense [4][64] gradient
+    assert L.spl_sparse_weight_grad_workspace_bytes(16, 4, 64) == a256(2 * 4 * 16) + a256(2 * 64 * 16)
+    assert L.spl_sparse_weight_grad_workspace_bytes(2048, 11008, 4096) == 2 * 2048 * (11008 + 4096)
     assert L.spl_sparse_weight_grad_workspace_bytes(-1, 4, 64) < 0
     assert w(A, B, 0, ctypes.byref(m), G, ws, None) == UNSUPPORTED             # no tokens
     assert w(A, B, 12, ctypes.byref(m), G, ws, None) == UNSUPPORTED            # M % 8 != 0

@@ -27,8 +27,11 @@ def _with_values(spl, Wc, values):
     return spl.SparseMatrix(Wc.bitmask, values, None, Wc.tile_offsets, Wc.rows, Wc.cols, Wc.nnz, "tile16")
 
 
-@pytest.mark.parametrize("R,C", [(1, 1), (3, 70), (65, 129), (1000, 4096), (4096, 64)])
+@pytest.mark.parametrize("R,C", [(1, 1), (3, 70), (65, 129), (16, 12), (8, 8), (72, 520), (136, 24), (1000, 4096),
+                                 (4096, 64), (2048, 11008)])
 def test_transpose16(spl, R, C):
+    """Both kernels: 8 x 8 register blocks when R and C are multiples of 8
+    (whole and partial 64 x 256 workgroup tiles), LDS tiles otherwise."""
     A = np.random.default_rng(R * C).integers(0, 1 << 16, size=(R, C), dtype=np.uint16)
     got = from_dev_bits(spl.transpose16(to_dev(A, "bf16")))
     assert np.array_equal(got, A.T)
@@ -53,8 +56,11 @@ def test_gather_tiled_matches_oracle_encoder(orc, spl, dtype, N, K, s):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("N,K,M,s", [(24, 64, 16, 0.6), (100, 1000, 64, 0.7), (300, 264, 136, 0.5), (33, 512, 8, 0.9),
-                                     (130, 96, 520, 0.7)])
+                                     (130, 96, 520, 0.7), (2000, 4104, 72, 0.7)])
 def test_weight_grad(orc, spl, dtype, N, K, M, s):
+    """Small products (64 x 128 workgroups, split over M when they leave CUs
+    idle) and a ragged large one (128 x 256 workgroups, bounds-checked loads:
+    4104 columns, 2000 rows), compared with the oracle on every kept entry."""
     import torch
 
     W, mask = synth.weight(610 + N, N, K, dtype, s)

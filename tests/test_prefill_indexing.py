@@ -368,3 +368,88 @@ def test_gated_block_assignment(N, BN, NW):
             g, u = wn * FN + 2 * p, wn * FN + 2 * p + 1      # virtual blocks of the fragments (= expanding waves)
             assert g % 2 == 0 and u % 2 == 1 and g >> 1 == u >> 1
             assert (g >> 1) * 16 == wn * 8 * FN + 16 * p      # the real rows pf_store_gated writes
+
+
+# ---------------------------------------------------------------- the gather epilogue (weight gradients)
+
+def _gather_lines():
+    src = open(SRC).read()
+    for line in ("const int64_t b = (m0 + wm * 64) / 16 + j;",
+                 "if (b >= B) break;",
+                 "const int64_t st = (n0 + wn * 16 * FN) / 32 + p;",
+                 "if (st >= S) break;",
+                 "const uint32_t w = g.gbm[t * 16 + fr];",
+                 "const uint32_t incl = row16_inclusive_scan(c);",
+                 "const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 15);",
+                 "const uint32_t above = incl - c;",
+                 "const int col = 16 * h + 4 * q;",
+                 "uint32_t idx = base + __builtin_amdgcn_ubfe(above, 8 * f, 8);",
+                 "if (col & 4) idx += __popc(__builtin_amdgcn_ubfe(w, 8 * f, 4));",
+                 "const uint32_t nib = __builtin_amdgcn_ubfe(w, col, 4);",
+                 "if ((nib >> r) & 1u) g.gval[idx++] = T::from_f32(acc[2 * p + h][j][r]);",
+                 "if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1, kGather>(a, s);",
+                 "return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2, kGather>(a, s)"):
+        assert line in src, f"gather epilogue changed: update this replay ({line})"
+    return [(128, 256, 8), (64, 128, 4)]                # (BN, BM, NW)
+
+
+@pytest.mark.parametrize("R,C,s", [(24, 64, 0.6), (100, 1000, 0.7), (300, 264, 0.5), (33, 512, 0.9), (130, 96, 0.0),
+                                   (16, 32, 1.0), (257, 136, 0.5)])
+def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
+    """The product G [R][C] is written only at the kept positions of its tile
+    pattern: replaying every workgroup's waves (D layout: lane l holds tile
+    row l % 16, columns 16 h + 4 (l / 16) + r of fragment 2p + h) writes each
+    value index exactly once, and what lands there is the oracle's tile-layout
+    value of G at that index."""
+    W, mask = synth.weight(71 + R + C, R, C, "bf16", s)
+    T = orc.pack_tiled(W, "bf16", mask)
+    rng = np.random.default_rng(R * 1000 + C)
+    G = rng.integers(1, 60000, size=(R, C)).astype(np.uint16)        # distinct-enough payloads; position-tagged
+    want = orc.pack_tiled(G, "bf16", mask).values
+    B, S = -(-R // 16), -(-C // 32)
+    bm = T.bitmask.reshape(-1).astype(np.int64)
+    offs = T.tile_offsets.astype(np.int64)
+    for BN, BM, NW in _gather_lines():
+        FN = BN // 32
+        out = np.zeros(T.nnz, np.uint16)
+        hits = np.zeros(T.nnz, np.int64)
+        for gx in range(-(-C // BN)):                 # product columns = pattern columns
+            for gy in range(-(-R // BM)):             # product rows = pattern rows
+                n0, m0 = gx * BN, gy * BM
+                for wave in range(NW):
+                    wn, wm = wave & 1, wave >> 1
+                    for j in range(4):
+                        b = (m0 + wm * 64) // 16 + j
+                        if b >= B:
+                            break
+                        for p in range(FN // 2):
+                            st = (n0 + wn * 16 * FN) // 32 + p
+                            if st >= S:
+                                break
+                            t = b * S + st
+                            words = [int(bm[t * 16 + fr]) for fr in range(16)]
+                            c = [sum(_popc((w >> (8 * f)) & 0xFF) << (8 * f) for f in range(4)) for w in words]
+                            incl = np.cumsum(c)
+                            assert all(((int(x) >> (8 * f)) & 0xFF) <= 128 for x in incl for f in range(4))
+                            tot = int(incl[15])
+                            for lane in range(64):
+                                fr, q = lane & 15, lane >> 4
+                                w = words[fr]
+                                above = int(incl[fr]) - c[fr]
+                                for h in range(2):
+                                    col = 16 * h + 4 * q
+                                    f = col >> 3
+                                    idx = int(offs[t]) + ((above >> (8 * f)) & 0xFF)
+                                    idx += sum((tot >> (8 * g)) & 0xFF for g in range(f))
+                                    if col & 4:
+                                        idx += _popc((w >> (8 * f)) & 0xF)
+                                    nib = (w >> col) & 0xF
+                                    for r in range(4):
+                                        if (nib >> r) & 1:
+                                            row, k = 16 * b + fr, 32 * st + col + r
+                                            assert row < R and k < C
+                                            out[idx] = G[row, k]
+                                            hits[idx] += 1
+                                            idx += 1
+        assert (hits == 1).all(), (BN, "value index written other than once")
+        assert np.array_equal(out, want), BN
