@@ -163,7 +163,7 @@ def _inside_rule():
     rule = "return N % BN == 0 && M % BM == 0 && K % kPfBK == 0;"
     assert rule in src, "launch rule for the unchecked kernels changed: update this replay"
     for line in ("return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? sparse_prefill_launch<T, BN, BM, NW, KS, false>(a, s)",
-                 "return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM) ? dense_prefill_launch<T, BN, BM, NW, KS, false>(a, s)",
+                 "return pf_inside(a.N, a.M, pf_units<T>(a.K), BN, BM)\n             ? dense_prefill_launch<T, BN, BM, NW, KS, false, kGather>(a, s)",
                  "const int64_t t = b * S + s;",
                  "for (int i = 0; i < P; ++i) sl.v[i] = *reinterpret_cast<const u32x4*>(row0 + i * stride + k0);"):
         assert line in src, f"kernel changed: update this replay ({line})"
