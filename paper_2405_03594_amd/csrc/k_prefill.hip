@@ -19,7 +19,10 @@
 // stages all lie inside the matrix use loads without bounds branches.
 //
 //   * dense (comparator): W rows are copied into the A buffer exactly like
-//     X rows into the B buffer;
+//     X rows into the B buffer; launches whose 128 x 256 blocks and stages
+//     all lie inside the matrices move both operands straight from global
+//     memory into three rotating LDS stage buffers instead (see
+//     k_dense_prefill_dma);
 //   * sparse (paper section 2.4.2): the A buffer is filled by expanding the
 //     stage's compressed 16 x 32 tiles (BN/16 row blocks x 2 k-steps, shared
 //     out over the waves), each once per workgroup and one stage ahead, before
@@ -130,43 +133,43 @@ __device__ __forceinline__ void slab_store(const Slab<P>& sl, uint32_t buf, int 
 // fragments are read up front; the scheduling hints issue the first k-step's
 // reads, then put one second-k-step read after each of the first MFMAs, so
 // the LDS reads overlap the matrix cores instead of waiting ahead of them.
-template <class T, int FN>
-__device__ __forceinline__ void pf_mfma_stage(typename MfmaP<T>::acc_t (&acc)[FN][4], uint32_t abuf, uint32_t bbuf,
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_mfma_stage(typename MfmaP<T>::acc_t (&acc)[FN][FM], uint32_t abuf, uint32_t bbuf,
                                               int wn, int wm, int fr, int fg) {
   // fragment rows differ by multiples of 16, so every row a lane reads has row % 8 == fr % 8
-  u32x4 a[2][FN], b[2][4];
+  u32x4 a[2][FN], b[2][FM];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     const uint32_t a0 = abuf + pf_chunk(wn * 16 * FN + fr, 4 * ks + fg);
-    const uint32_t b0 = bbuf + pf_chunk(wm * 64 + fr, 4 * ks + fg);
+    const uint32_t b0 = bbuf + pf_chunk(wm * 16 * FM + fr, 4 * ks + fg);
 #pragma unroll
     for (int i = 0; i < FN; ++i) a[ks][i] = lds_load16(a0 + 16 * kPfRow * i);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[ks][j] = lds_load16(b0 + 16 * kPfRow * j);
+    for (int j = 0; j < FM; ++j) b[ks][j] = lds_load16(b0 + 16 * kPfRow * j);
   }
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
     for (int i = 0; i < FN; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = MfmaP<T>::run(a[ks][i], b[ks][j], acc[i][j]);
+      for (int j = 0; j < FM; ++j) acc[i][j] = MfmaP<T>::run(a[ks][i], b[ks][j], acc[i][j]);
   // masks: 0x100 LDS read, 0x008 MFMA
-  __builtin_amdgcn_sched_group_barrier(0x100, FN + 4, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, FN + FM, 0);
 #pragma unroll
-  for (int q = 0; q < FN + 4; ++q) {
+  for (int q = 0; q < FN + FM; ++q) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, 8 * FN - (FN + 4), 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 2 * FN * FM - (FN + FM), 0);
 }
 
 // D layout: lane l, register r -> row (n) 4 (l / 16) + r, column (m) l % 16.
-template <class T, int FN>
-__device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][4], uint16_t* __restrict__ Y, int64_t M, int64_t N,
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][FM], uint16_t* __restrict__ Y, int64_t M, int64_t N,
                                          int64_t n0, int64_t m0, int wn, int wm, int fr, int fg) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t m = m0 + wm * 64 + 16 * j + fr;
+  for (int j = 0; j < FM; ++j) {
+    const int64_t m = m0 + wm * 16 * FM + 16 * j + fr;
     if (m >= M) continue;
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
@@ -189,14 +192,14 @@ __device__ __forceinline__ void pf_store(const f32x4 (&acc)[FN][4], uint16_t* __
 // The int8 epilogue: Y = fp16_rne((float(acc) * sx[m]) * sw[n]), each product
 // rounded to binary32 (no fused multiply-add); acc_out (optional) gets the
 // exact int32 sums.
-template <int FN>
-__device__ __forceinline__ void pf_store_i8(const i32x4 (&acc)[FN][4], uint16_t* __restrict__ Y,
+template <int FN, int FM>
+__device__ __forceinline__ void pf_store_i8(const i32x4 (&acc)[FN][FM], uint16_t* __restrict__ Y,
                                             int32_t* __restrict__ acc_out, const float* __restrict__ sx,
                                             const float* __restrict__ sw, int64_t M, int64_t N, int64_t n0,
                                             int64_t m0, int wn, int wm, int fr, int fg) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t m = m0 + wm * 64 + 16 * j + fr;
+  for (int j = 0; j < FM; ++j) {
+    const int64_t m = m0 + wm * 16 * FM + 16 * j + fr;
     if (m >= M) continue;
     const float xs = sx[m];
 #pragma unroll
@@ -219,13 +222,13 @@ __device__ __forceinline__ void pf_store_i8(const i32x4 (&acc)[FN][4], uint16_t*
 // and 2p + 1 of a wave hold the gate and up sums of the same outputs, in the
 // same lanes.  Y[m][n] = silu(g) * u, silu(z) = z / (1 + e^-z), from the fp32
 // sums; n0 is the workgroup's first real row.
-template <class T, int FN>
-__device__ __forceinline__ void pf_store_gated(const f32x4 (&acc)[FN][4], uint16_t* __restrict__ Y, int64_t M,
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_store_gated(const f32x4 (&acc)[FN][FM], uint16_t* __restrict__ Y, int64_t M,
                                                int64_t N, int64_t n0, int64_t m0, int wn, int wm, int fr, int fg) {
   static_assert(FN % 2 == 0, "gate and up fragments pair up");
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t m = m0 + wm * 64 + 16 * j + fr;
+  for (int j = 0; j < FM; ++j) {
+    const int64_t m = m0 + wm * 16 * FM + 16 * j + fr;
     if (m >= M) continue;
 #pragma unroll
     for (int p = 0; p < FN / 2; ++p) {
@@ -243,26 +246,26 @@ __device__ __forceinline__ void pf_store_gated(const f32x4 (&acc)[FN][4], uint16
 // Split K: after every wave's last MFMA, k-group 1 hands its partial sums to
 // k-group 0 through the (then free) stage buffers; group 0 adds them (a fixed
 // order) and is the one that stores.  Returns whether this thread stores.
-template <int FN, int NT, int KS, class A>
-__device__ __forceinline__ bool pf_combine(A (&acc)[FN][4], unsigned char* dsm, int kh, int t) {
+template <int FN, int FM, int NT, int KS, class A>
+__device__ __forceinline__ bool pf_combine(A (&acc)[FN][FM], unsigned char* dsm, int kh, int t) {
   if constexpr (KS == 1) {
     return true;
   } else {
     static_assert(KS == 2, "two k-groups");
-    A* part = reinterpret_cast<A*>(dsm);             // [FN * 4][NT]
+    A* part = reinterpret_cast<A*>(dsm);             // [FN * FM][NT]
     __syncthreads();
     if (kh == 1) {
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) part[(i * 4 + j) * NT + t] = acc[i][j];
+        for (int j = 0; j < FM; ++j) part[(i * FM + j) * NT + t] = acc[i][j];
     }
     __syncthreads();
     if (kh == 0) {
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += part[(i * 4 + j) * NT + t];
+        for (int j = 0; j < FM; ++j) acc[i][j] += part[(i * FM + j) * NT + t];
     }
     return kh == 0;
   }
@@ -314,15 +317,15 @@ struct PfArgs {
 // and group.  The per-group counts of the 16 rows are scanned in one 16-lane
 // DPP scan (four 8-bit fields; a field sums at most 16 x 8 = 128).  Values
 // are rounded once to the payload type.
-template <class T, int FN>
-__device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][4], const PfArgs& g, int64_t n0, int64_t m0,
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], const PfArgs& g, int64_t n0, int64_t m0,
                                                 int wn, int wm, int lane) {
   const int64_t B = tile_blocks(g.M);
   const int64_t S = tile_steps(g.N);
   const int fr = lane & 15, q = lane >> 4;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int64_t b = (m0 + wm * 64) / 16 + j;
+  for (int j = 0; j < FM; ++j) {
+    const int64_t b = (m0 + wm * 16 * FM) / 16 + j;
     if (b >= B) break;                                         // wave-uniform; later j lie further out
 #pragma unroll
     for (int p = 0; p < FN / 2; ++p) {
@@ -382,8 +385,9 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
   constexpr int FN = BN / 32;                        // n-fragments per wave
   constexpr int TW = BN / 8 / NW;                    // operand units per wave per stage: tiles (int8: tile pairs)
   constexpr int RR = 8 * NW;                         // rows per staging round
-  static_assert(BM == 32 * NW && TW % 2 == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
-  static_assert(KS == 1 || FN * 4 * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
+  constexpr int FM = BM / (8 * NW);                  // m-fragments per wave
+  static_assert(BM % (8 * NW) == 0 && FM <= 8 && TW % 2 == 0, "wave layout: 2 x NW/2 waves of BN/2 x 16 FM");
+  static_assert(KS == 1 || FN * FM * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   static_assert(!kGated || (!kI8 && TW == 2), "gated: 16-bit payloads, one row block per wave");
@@ -494,11 +498,11 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
     }
   };
 
-  Acc acc[FN][4];
+  Acc acc[FN][FM];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = Acc{0, 0, 0, 0};
+    for (int j = 0; j < FM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
   // Pipeline: bitmask words three stages ahead, value windows and X slabs two
   // ahead (X in alternating register sets, the loop unrolled by two stages).
@@ -543,20 +547,20 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_sparse_prefill(
         xsrc.template fetch<kChecked>(xn, Kh, (int64_t)kPfBK * (sb + st + 2));
       }
     }
-    if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
+    if (st < nl) pf_mfma_stage<T, FN, FM>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (st + 1 < nh) __syncthreads();
   };
   for (int st = 0; st < nh; st += 2) {
     step(st, x0, x1);                                  // stage st + 1 from set 1, stage st + 2 -> set 0
     if (st + 1 < nh) step(st + 1, x1, x0);             // stage st + 2 from set 0, stage st + 3 -> set 1
   }
-  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) {
+  if (pf_combine<FN, FM, NT, KS>(acc, dsm, kh, tid)) {
     if constexpr (kI8)
-      pf_store_i8<FN>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+      pf_store_i8<FN, FM>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
     else if constexpr (kGated)
-      pf_store_gated<T, FN>(acc, g.Y, M, N, (int64_t)blockIdx.x * (BN / 2), m0, wn, wm, fr, fg);
+      pf_store_gated<T, FN, FM>(acc, g.Y, M, N, (int64_t)blockIdx.x * (BN / 2), m0, wn, wm, fr, fg);
     else
-      pf_store<T, FN>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
+      pf_store<T, FN, FM>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
   }
 }
 
@@ -582,19 +586,20 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(c
   const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;
   constexpr int FN = BN / 32;                         // n-fragments per wave
   constexpr int RR = 8 * NW;                          // rows per staging round
-  static_assert(BM == 32 * NW && BN % RR == 0, "wave layout: 2 x NW/2 waves of BN/2 x 64");
-  static_assert(KS == 1 || FN * 4 * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
+  constexpr int FM = BM / (8 * NW);                   // m-fragments per wave
+  static_assert(BM % (8 * NW) == 0 && FM <= 8 && BN % RR == 0, "wave layout: 2 x NW/2 waves of BN/2 x 16 FM");
+  static_assert(KS == 1 || FN * FM * NT * 16 <= KS * pf_lds(BN, BM), "partial sums fit the stage buffers");
   const int64_t n0 = (int64_t)blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
   unsigned char* gb = dsm + kh * pf_lds(BN, BM);
   const uint32_t abuf[2] = {lds_off(gb), lds_off(gb + BN * kPfRow)};
   const uint32_t bbuf[2] = {lds_off(gb + 2 * BN * kPfRow), lds_off(gb + (2 * BN + BM) * kPfRow)};
 
-  Acc acc[FN][4];
+  Acc acc[FN][FM];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = Acc{0, 0, 0, 0};
+    for (int j = 0; j < FM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
   // Global loads run two stages ahead of the multiplication: register sets
   // (x0, w0) and (x1, w1) alternate, the loop unrolled by two stages.  Stage
@@ -628,7 +633,7 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(c
       xsrc.template fetch<kChecked>(xn, Kh, (int64_t)kPfBK * (sb + st + 2));
       wsrc.template fetch<kChecked>(wn_, Kh, (int64_t)kPfBK * (sb + st + 2));
     }
-    if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
+    if (st < nl) pf_mfma_stage<T, FN, FM>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);
     if (st + 1 < nh) __syncthreads();
   };
   for (int st = 0; st < nh; st += 2) {
@@ -636,14 +641,104 @@ __global__ void __launch_bounds__(64 * NW * KS, 8 / (NW * KS)) k_dense_prefill(c
     if (st + 1 < nh) step(st + 1, x1, w1, x0, w0);     // stage st + 3 -> set 1, stage st + 2 from set 0
   }
   static_assert(!kGather || (!kI8 && FN % 2 == 0), "gather: 16-bit payloads, whole tiles per wave");
-  if (pf_combine<FN, NT, KS>(acc, dsm, kh, tid)) {
+  if (pf_combine<FN, FM, NT, KS>(acc, dsm, kh, tid)) {
     if constexpr (kI8)
-      pf_store_i8<FN>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+      pf_store_i8<FN, FM>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
     else if constexpr (kGather)
-      pf_store_gather<T, FN>(acc, g, n0, m0, wn, wm, lane);
+      pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);
     else
-      pf_store<T, FN>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
+      pf_store<T, FN, FM>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
   }
+}
+
+// Direct-to-LDS staging, for launches whose 128 x 256 blocks and 64-column
+// stages all lie inside the matrices (16-bit payloads; eight waves of 64 x 64
+// as above).  Operand rows go from global memory straight into LDS
+// (global_load_lds_dwordx4: lane i of a request fills the 16-byte slot i of a
+// 1 KB run, i.e. row i / 8 of an 8-row group at position i % 8, so the lane
+// fetches the chunk whose swizzled position that is), which takes no
+// registers and no LDS store instructions.  Three stage buffers per staged
+// operand: stage st + 2 is requested while stage st is multiplied, and one
+// barrier per stage both publishes stage st + 1 (each wave first waits for
+// its own requests of it) and retires the buffer that the next request
+// overwrites (last read by stage st).
+constexpr int kDmaBN = 128, kDmaBM = 256, kDmaStages = 3, kDmaWaves = 8;
+constexpr int kDmaStageBytes = (kDmaBN + kDmaBM) * kPfRow;     // 48 KB
+
+__device__ __forceinline__ void lds_dma16(const uint16_t* src, unsigned char* dst) {
+  __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                   (void __attribute__((address_space(3)))*)dst, 16, 0, 0);
+}
+
+// Wait until at most kOutstanding of this wave's vector memory requests remain
+// (they complete in order) and its LDS operations are done, then a bare
+// workgroup barrier: __syncthreads() would wait for every request.  The
+// compiler-only fences keep LDS accesses from moving across the barrier.
+template <int kOutstanding>
+__device__ __forceinline__ void dma_barrier() {
+  static_assert(kOutstanding >= 0 && kOutstanding < 16, "vmcnt's low field");
+  __builtin_amdgcn_s_waitcnt(0x0070 | kOutstanding);   // vmcnt(n) expcnt(7) lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// A wave's part of one stage's requests: `groups` 8-row groups of rows
+// [8 groups w, 8 groups (w + 1)) of a staged operand, from the lane's first
+// row `src` (row lane / 8 of the wave's first group, at its swizzled chunk).
+template <int kGroups>
+__device__ __forceinline__ void dma_rows(const uint16_t* src, int64_t K, int st, unsigned char* buf, int wave) {
+#pragma unroll
+  for (int i = 0; i < kGroups; ++i)
+    lds_dma16(src + 8 * K * i + kPfBK * st, buf + (8 * kGroups * wave + 8 * i) * kPfRow);
+}
+
+template <class T, bool kGather, int NW>
+__global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma(const PfArgs g) {
+  constexpr int FN = 4, FM = kDmaBM / (8 * NW);
+  constexpr int GA = kDmaBN / 8 / NW, GB = kDmaBM / 8 / NW;      // 8-row groups per wave: W, X
+  constexpr int kLoads = GA + GB;                                 // 1 KB requests per wave and stage
+  extern __shared__ __align__(16) unsigned char dsm[];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int64_t M = g.M, N = g.N, K = g.K;
+  const int nst = (int)(K / kPfBK);
+  const int64_t n0 = (int64_t)blockIdx.x * kDmaBN, m0 = (int64_t)blockIdx.y * kDmaBM;
+  // my slot in an 8-row group: row lane / 8, position lane % 8, holding chunk (lane % 8) ^ (lane / 8)
+  const int lr = lane >> 3, lc = (lane & 7) ^ lr;
+  // wave w requests W rows 8 GA w .. + 8 GA and X rows 8 GB w .. + 8 GB
+  const uint16_t* wsrc = g.W + (n0 + 8 * GA * wave + lr) * K + 8 * lc;
+  const uint16_t* xsrc = g.X + (m0 + 8 * GB * wave + lr) * K + 8 * lc;
+  auto request = [&](int st, int buf) {
+    unsigned char* a = dsm + buf * kDmaStageBytes;
+    dma_rows<GA>(wsrc, K, st, a, wave);
+    dma_rows<GB>(xsrc, K, st, a + kDmaBN * kPfRow, wave);
+  };
+
+  f32x4 acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  request(0, 0);
+  if (nst > 1) request(1, 1);
+  int cur = 0;
+  for (int st = 0; st < nst; ++st) {
+    // my requests of stage st are done once at most the next stage's remain
+    if (st + 1 < nst) dma_barrier<kLoads>();
+    else dma_barrier<0>();
+    if (st + 2 < nst) request(st + 2, cur == 0 ? 2 : cur - 1);
+    const uint32_t abuf = lds_off(dsm + cur * kDmaStageBytes);
+    pf_mfma_stage<T, FN, FM>(acc, abuf, abuf + kDmaBN * kPfRow, wn, wm, fr, fg);
+    cur = cur == kDmaStages - 1 ? 0 : cur + 1;
+  }
+  if constexpr (kGather)
+    pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);
+  else
+    pf_store<T, FN, FM>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
 int pf_cus() { return device_cus(); }
@@ -665,11 +760,12 @@ template <class T, int BN, int BM, int NW, int KS, bool kChecked, bool kGated = 
 hipError_t sparse_prefill_launch(const PfArgs& a, hipStream_t s) {
   auto* kernel = k_sparse_prefill<T, BN, BM, NW, KS, kChecked, kGated>;
   static PerDeviceFlag lds_set;
-  const hipError_t attr = allow_lds_once(lds_set, kernel, KS * pf_lds(BN, BM));
+  constexpr int lds = KS * pf_lds(BN, BM);
+  const hipError_t attr = allow_lds_once(lds_set, kernel, lds);
   if (attr != hipSuccess) return attr;
   constexpr int RN = kGated ? BN / 2 : BN;            // real rows per workgroup
   const dim3 grid((unsigned)((a.N + RN - 1) / RN), (unsigned)((a.M + BM - 1) / BM)), block(64 * NW * KS);
-  hipLaunchKernelGGL(kernel, grid, block, KS * pf_lds(BN, BM), s, a);
+  hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
   return hipGetLastError();
 }
 
@@ -722,8 +818,22 @@ hipError_t dense_prefill_tile(const PfArgs& a, hipStream_t s) {
              : dense_prefill_launch<T, BN, BM, NW, KS, true, kGather>(a, s);
 }
 
+template <class T, bool kGather>
+hipError_t dense_prefill_dma(const PfArgs& a, hipStream_t s) {
+  constexpr int NW = kDmaWaves;
+  auto* kernel = k_dense_prefill_dma<T, kGather, NW>;
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, kDmaStages * kDmaStageBytes);
+  if (attr != hipSuccess) return attr;
+  const dim3 grid((unsigned)(a.N / kDmaBN), (unsigned)(a.M / kDmaBM)), block(64 * NW);
+  hipLaunchKernelGGL(kernel, grid, block, kDmaStages * kDmaStageBytes, s, a);
+  return hipGetLastError();
+}
+
 template <class T, bool kGather = false>
 hipError_t dense_prefill_t(const PfArgs& a, hipStream_t s) {
+  if constexpr (!std::is_same<T, I8P>::value)
+    if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, a.K, kDmaBN, kDmaBM)) return dense_prefill_dma<T, kGather>(a, s);
   if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1, kGather>(a, s);
   return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2, kGather>(a, s)
                               : dense_prefill_tile<T, 64, 128, 4, 1, kGather>(a, s);

@@ -164,6 +164,20 @@ def test_dense_prefill_llama_sampled(orc, spl):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K", [(4096, 4096), (4096, 11008)])
+def test_dense_prefill_llama_rows(orc, spl, dtype, N, K):
+    """The dense comparator at M = 2048 on Llama-2-7B shapes (the direct-to-LDS
+    core: every block and stage inside, 64 or 172 stages through three
+    rotating buffers): 64 full rows against the oracle."""
+    M = 2048
+    W, _ = synth.weight(914 + K, N, K, dtype, 0.0)
+    X = synth.activations(915 + K, M, K, dtype)
+    Y = from_dev_f64(spl.dense_linear(to_dev(X, dtype), to_dev(W, dtype), algo="prefill"))
+    rows = _sample_rows(M, 17 + K)
+    assert_close(Y[rows], orc.dense_f64(X[rows], W, dtype), f"dense prefill {dtype} {N}x{K} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_prefill_large_grid_ragged(orc, spl, dtype):
     """A grid of at least one 128 x 256 block per CU (the large tiling) with
     ragged N, M and an odd number of 32-column steps, compared in full, sparse

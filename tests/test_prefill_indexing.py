@@ -198,10 +198,10 @@ def _split_rule():
     for line in ("const int nh = (nst + KS - 1) / KS;",
                  "const int sb = kh * nh;",
                  "const int nl = nst - sb < nh ? (nst > sb ? nst - sb : 0) : nh;",
-                 "if (st < nl) pf_mfma_stage<T, FN>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);",
+                 "if (st < nl) pf_mfma_stage<T, FN, FM>(acc, abuf[cur], bbuf[cur], wn, wm, fr, fg);",
                  "if (st + 1 < nh) __syncthreads();",
                  "unsigned char* gb = dsm + kh * pf_lds(BN, BM);",
-                 "A* part = reinterpret_cast<A*>(dsm);             // [FN * 4][NT]"):
+                 "A* part = reinterpret_cast<A*>(dsm);             // [FN * FM][NT]"):
         assert line in src, f"split-K schedule changed: update this replay ({line})"
 
 
@@ -374,7 +374,11 @@ def test_gated_block_assignment(N, BN, NW):
 
 def _gather_lines():
     src = open(SRC).read()
-    for line in ("const int64_t b = (m0 + wm * 64) / 16 + j;",
+    for line in ("const int64_t b = (m0 + wm * 16 * FM) / 16 + j;",
+                 "constexpr int FM = BM / (8 * NW);",
+                 "constexpr int FN = 4, FM = kDmaBM / (8 * NW);",
+                 "constexpr int kDmaBN = 128, kDmaBM = 256, kDmaStages = 3, kDmaWaves = 8;",
+                 "pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);",
                  "if (b >= B) break;",
                  "const int64_t st = (n0 + wn * 16 * FN) / 32 + p;",
                  "if (st >= S) break;",
@@ -390,7 +394,9 @@ def _gather_lines():
                  "if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1, kGather>(a, s);",
                  "return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2, kGather>(a, s)"):
         assert line in src, f"gather epilogue changed: update this replay ({line})"
-    return [(128, 256, 8), (64, 128, 4)]                # (BN, BM, NW)
+    # (BN, BM, NW): the 8-wave cores (register-staged and direct-to-LDS) and the 4-wave core;
+    # (128, 256, 4) checks the epilogue's general m-fragment count (FM = 8)
+    return [(128, 256, 8), (64, 128, 4), (128, 256, 4)]
 
 
 @pytest.mark.parametrize("R,C,s", [(24, 64, 0.6), (100, 1000, 0.7), (300, 264, 0.5), (33, 512, 0.9), (130, 96, 0.0),
@@ -410,7 +416,7 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
     bm = T.bitmask.reshape(-1).astype(np.int64)
     offs = T.tile_offsets.astype(np.int64)
     for BN, BM, NW in _gather_lines():
-        FN = BN // 32
+        FN, FM = BN // 32, BM // (8 * NW)
         out = np.zeros(T.nnz, np.uint16)
         hits = np.zeros(T.nnz, np.int64)
         for gx in range(-(-C // BN)):                 # product columns = pattern columns
@@ -418,8 +424,8 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
                 n0, m0 = gx * BN, gy * BM
                 for wave in range(NW):
                     wn, wm = wave & 1, wave >> 1
-                    for j in range(4):
-                        b = (m0 + wm * 64) // 16 + j
+                    for j in range(FM):
+                        b = (m0 + wm * 16 * FM) // 16 + j
                         if b >= B:
                             break
                         for p in range(FN // 2):
@@ -453,3 +459,59 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
                                             idx += 1
         assert (hits == 1).all(), (BN, "value index written other than once")
         assert np.array_equal(out, want), BN
+
+
+# ---------------------------------------------------------------- direct-to-LDS staging of the dense core
+
+def _dma_lines():
+    src = open(SRC).read()
+    for line in ("constexpr int kDmaBN = 128, kDmaBM = 256, kDmaStages = 3, kDmaWaves = 8;",
+                 "constexpr int GA = kDmaBN / 8 / NW, GB = kDmaBM / 8 / NW;",
+                 "const int lr = lane >> 3, lc = (lane & 7) ^ lr;",
+                 "const uint16_t* wsrc = g.W + (n0 + 8 * GA * wave + lr) * K + 8 * lc;",
+                 "const uint16_t* xsrc = g.X + (m0 + 8 * GB * wave + lr) * K + 8 * lc;",
+                 "lds_dma16(src + 8 * K * i + kPfBK * st, buf + (8 * kGroups * wave + 8 * i) * kPfRow);",
+                 "dma_rows<GA>(wsrc, K, st, a, wave);",
+                 "dma_rows<GB>(xsrc, K, st, a + kDmaBN * kPfRow, wave);",
+                 "if (st + 2 < nst) request(st + 2, cur == 0 ? 2 : cur - 1);",
+                 "if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, a.K, kDmaBN, kDmaBM)) return dense_prefill_dma<T, kGather>(a, s);"):
+        assert line in src, f"direct-to-LDS staging changed: update this replay ({line})"
+    return 128, 256, 8
+
+
+@pytest.mark.parametrize("N,M,K", [(4096, 2048, 4096), (11008, 512, 4096), (4096, 256, 11008), (128, 256, 64)])
+def test_dma_requests_fill_the_swizzled_stage(N, M, K):
+    """One stage's direct-to-LDS requests of a workgroup: lane i of a request
+    fills 16-byte slot i of a 1 KB run.  Every (row, chunk) of the W and X
+    stage lands exactly once, at the swizzled place the MFMA reads use
+    (pf_chunk: chunk c of row r at position c ^ (r % 8)), from inside the
+    matrices; the three stage buffers rotate so that a request never hits
+    the buffer being multiplied or the one published next."""
+    BN, BM, NW = _dma_lines()
+    bk, _ = _constants()
+    row_bytes = 2 * bk
+    GA, GB = BN // 8 // NW, BM // 8 // NW
+    assert N % BN == 0 and M % BM == 0 and K % bk == 0
+    nst = K // bk
+    for n0, m0 in ((0, 0), (N - BN, M - BM)):
+        for st in (0, nst - 1):
+            for rows0, R, groups, region, nrows in ((n0, N, GA, 0, BN), (m0, M, GB, BN * row_bytes, BM)):
+                seen = {}
+                for wave in range(NW):
+                    for i in range(groups):
+                        for lane in range(64):
+                            lr, lc = lane >> 3, (lane & 7) ^ (lane >> 3)
+                            row = rows0 + 8 * groups * wave + lr + 8 * i        # global row
+                            col = bk * st + 8 * lc                             # first element of the chunk
+                            assert row < R and col + 8 <= K
+                            slot = region + (8 * groups * wave + 8 * i) * row_bytes + 16 * lane
+                            r = row - rows0                                    # row within the stage buffer
+                            assert slot == region + _chunk(r, lc, row_bytes), (wave, i, lane)
+                            assert (r, lc) not in seen
+                            seen[(r, lc)] = True
+                assert len(seen) == nrows * 8
+    # buffer rotation: stage st + 2 goes to (st + 2) % 3, never st % 3 (being read) or (st + 1) % 3
+    for st in range(12):
+        cur = st % 3
+        target = 2 if cur == 0 else cur - 1
+        assert target == (st + 2) % 3 and target not in (st % 3, (st + 1) % 3)
