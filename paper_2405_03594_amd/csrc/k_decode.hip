@@ -33,7 +33,7 @@
 //     rather than registers bounds the workgroups per CU) when the copy is
 //     small enough to leave several workgroups per CU: a single row (up to
 //     32 KB; the dense comparator: any batch up to 32 KB), or a small batch
-//     in a large grid (up to 16 KB); otherwise each chunk's operands are
+//     in a large grid (up to 32 KB); otherwise each chunk's operands are
 //     loaded directly, which fetches only the live rows;
 //   * the waves' partial 16x16 results are summed in a fixed order
 //     (deterministic) and rounded once to the output type.
@@ -874,13 +874,14 @@ bool large_grid(int64_t blocks) { return blocks >= 4 * (int64_t)device_cus(); }
 
 // Activation path of the sparse kernels.  One row: staged in LDS when it fits
 // (32 KB).  Two to 16 rows: staged only where the launch has two or more row
-// blocks per CU and the copy fits 16 KB (so that three workgroups still share
-// a CU); otherwise loaded directly, which fetches only the live rows.  Two row
-// blocks per workgroup (direct path) pay off above four rows.
+// blocks per CU and the copy fits 32 KB (then at most ~57 KB of LDS per
+// workgroup: two still share a CU); otherwise loaded directly, which fetches
+// only the live rows.  Two row blocks per workgroup (direct path) pay off
+// above four rows.
 int sparse_variant(int64_t M, int64_t kmax, int64_t blocks) {
   const int64_t xbytes = M * 32 * tile_steps(kmax) * 2;
   if (M == 1 && xbytes <= kXLdsMaxSparse) return 0;
-  if (M > 1 && M <= 16 && xbytes <= kXLdsMaxSparse / 2 && !small_grid(blocks)) return 0;
+  if (M > 1 && M <= 16 && xbytes <= kXLdsMaxSparse && !small_grid(blocks)) return 0;
   return M <= 16 ? 1 : 2;
 }
 

@@ -227,11 +227,13 @@ def test_decode_row_block_pairs(orc, spl, dtype, N, K, M):
     assert_close(from_dev_f64(Y2), ref2, f"pairs group task 1 {dtype} N=40 K={K} M={M}")
 
 
-@pytest.mark.parametrize("N,K,M", [(8200, 1056, 2), (8192, 4096, 2), (8200, 3296, 3), (8192, 4096, 4)])
+@pytest.mark.parametrize("N,K,M", [(8200, 1056, 2), (8192, 4096, 2), (8200, 3296, 3), (8192, 4096, 4), (8200, 8192, 3),
+                                   (8200, 11008, 4)])
 def test_decode_large_grid_small_batches(orc, spl, N, K, M):
     """Launches of at least 512 row blocks at batches 2-4: activations staged in
-    LDS while the copy fits 16 KB (2 x 1056, 2 x 4096), loaded directly by the
-    single-block kernel otherwise (3 x 3296, 4 x 4096), compared in full."""
+    LDS while the copy fits 32 KB (2 x 1056, 2 x 4096, 3 x 3296, 4 x 4096),
+    loaded directly by the single-block kernel otherwise (3 x 8192,
+    4 x 11008), compared in full."""
     W, mask = synth.weight(960 + M + K, N, K, "bf16", 0.7)
     X = synth.activations(961, M, K, "bf16")
     ref = orc.linear_f64(X, orc.pack(W, "bf16", mask))
