@@ -31,6 +31,7 @@ from __future__ import annotations
 
 import argparse
 import concurrent.futures as cf
+import ctypes
 import json
 import os
 import sys
@@ -341,6 +342,13 @@ def run_prefill(args):
     def dense_fn(li, u):
         spl.dense_linear(xsl[u], layers[0][u[1]][1], out=ys[u], algo="prefill")
 
+    # the decoded-copy path: one workspace for the largest matrix, reused by every launch on the stream
+    ws = torch.empty((max(spl.lib().spl_sparse_linear_expanded_workspace_bytes(ctypes.byref(layers[0][j][0].view()))
+                          for j in range(len(shapes))),), dtype=torch.uint8, device="cuda")
+
+    def expanded_fn(li, u):
+        spl.sparse_linear_expanded(xsl[u], layers[0][u[1]][0], out=ys[u], workspace=ws)
+
     sp_wall, sp_gpu = _timed(units, sparse_fn, args.steps, args.warmup, [0])
     flops = sum(2.0 * M * N * K for M in Ms for (_, N, K) in shapes)
     launch_ms = sp_gpu / len(units)
@@ -351,10 +359,12 @@ def run_prefill(args):
         _, g = _timed(uM, sparse_fn, max(10, args.steps // 4), 2, [0])
         f = sum(2.0 * M * N * K for (_, N, K) in shapes)
         d = {"layer_us": round(g * 1e3, 2), "dense_equiv_tflops": round(f / (g * 1e-3) / 1e12, 1)}
+        _, ge = _timed(uM, expanded_fn, max(10, args.steps // 4), 2, [0])
+        d.update({"expanded_layer_us": round(ge * 1e3, 2), "expanded_tflops": round(f / (ge * 1e-3) / 1e12, 1)})
         if not args.no_dense:
             _, gd = _timed(uM, dense_fn, max(10, args.steps // 4), 2, [0])
             d.update({"dense_layer_us": round(gd * 1e3, 2), "dense_tflops": round(f / (gd * 1e-3) / 1e12, 1),
-                      "speedup_vs_dense": round(gd / g, 3)})
+                      "speedup_vs_dense": round(gd / g, 3), "expanded_speedup_vs_dense": round(gd / ge, 3)})
             gl = _library_linear_ms(torch, [(xsl[u], layers[0][u[1]][1]) for u in uM], max(10, args.steps // 4))
             d.update({"library_dense_layer_us": round(gl * 1e3, 2),
                       "library_dense_tflops": round(f / (gl * 1e-3) / 1e12, 1)})

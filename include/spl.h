@@ -213,6 +213,24 @@ spl_status spl_sparse_linear(const void* X, int64_t M, const spl_matrix* Wc, voi
 spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, void* Y, int32_t algo,
                                 hipStream_t stream);
 
+/* Sparse linear layer for large batches through a decoded copy (paper
+ * section 2.4.2 decompresses the stored submatrices before the matrix
+ * units consume them; at prefill batches the product is compute-bound, so
+ * decoding each tile once per call into device memory costs less than
+ * expanding it once per block of batch rows, as spl_sparse_linear's prefill
+ * kernel does).  Same arguments and result as spl_sparse_linear (fp16/bf16,
+ * tile layout, K % 8 == 0; M == 0 is a no-op), the sums those of the dense
+ * prefill kernel on the decoded matrix.  Two launches: spl_unpack into the
+ * workspace, then the dense product.
+ *   workspace  device scratch of spl_sparse_linear_expanded_workspace_bytes(Wc)
+ *              bytes (2 rows cols, rounded up to 256), 16-byte aligned, owned
+ *              by the caller, overwritten (one buffer can serve every matrix
+ *              of a layer in turn on one stream).
+ * The workspace-size function returns -1 for a view spl_check_matrix rejects. */
+int64_t spl_sparse_linear_expanded_workspace_bytes(const spl_matrix* Wc);
+spl_status spl_sparse_linear_expanded(const void* X, int64_t M, const spl_matrix* Wc, void* Y, void* workspace,
+                                      hipStream_t stream);
+
 /* Sparse training with the mask held fixed (paper Algorithm 1: the gradient is
  * masked and so are the weights after each step, i.e. only the kept values
  * change).  For Y = X (W.Mask)^T with an upstream gradient dY [M][N]:

@@ -104,6 +104,8 @@ def lib() -> ctypes.CDLL:
         "spl_unpack": (ctypes.c_int, [MP, P, P]),
         "spl_sparse_linear": (ctypes.c_int, [P, I64, MP, P, P]),
         "spl_sparse_linear_ex": (ctypes.c_int, [P, I64, MP, P, I32, P]),
+        "spl_sparse_linear_expanded_workspace_bytes": (I64, [MP]),
+        "spl_sparse_linear_expanded": (ctypes.c_int, [P, I64, MP, P, P, P]),
         "spl_sparse_linear_int8": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
         "spl_quantize_rows_i8": (ctypes.c_int, [P, ctypes.c_int32, I64, I64, P, P, P]),
         "spl_sparse_linear_silu_mul": (ctypes.c_int, [P, I64, MP, MP, P, I32, P]),
@@ -327,6 +329,31 @@ def sparse_linear(X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = 
     view = Wc.view()
     _check("spl_sparse_linear_ex", L.spl_sparse_linear_ex(_ptr(X), M, ctypes.byref(view), _ptr(out), ALGO[algo],
                                                           _stream(stream)))
+    return out
+
+
+def sparse_linear_expanded(X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = None,
+                           workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """sparse_linear through a decoded copy of W in `workspace` (see
+    spl_sparse_linear_expanded): for large batches."""
+    L = lib()
+    M = _rows_of(X, "X")
+    _arg(X, "X", shape=(M, Wc.cols), dtype=Wc.dtype, device=False)
+    if out is None:
+        out = torch.empty((M, Wc.rows), dtype=X.dtype, device=X.device)
+    _arg(out, "out", shape=(M, Wc.rows), dtype=Wc.dtype)
+    _dev_tensor(X, "X")
+    view = Wc.view()
+    need = L.spl_sparse_linear_expanded_workspace_bytes(ctypes.byref(view))
+    if need < 0:
+        raise ValueError("spl_sparse_linear_expanded: the matrix view is invalid")
+    if workspace is None:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=X.device)
+    _dev_tensor(workspace, "workspace")
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace holds {workspace.numel() * workspace.element_size()} bytes, needs {need}")
+    _check("spl_sparse_linear_expanded", L.spl_sparse_linear_expanded(_ptr(X), M, ctypes.byref(view), _ptr(out),
+                                                                      _ptr(workspace), _stream(stream)))
     return out
 
 

@@ -252,6 +252,46 @@ __global__ void __launch_bounds__(256) k_tile_scatter(const uint32_t* __restrict
   }
 }
 
+// The dense image of a 16-bit tile-layout matrix with K % 8 == 0: one wave
+// per tile (4 per workgroup), lane (fr, fg) writes row fr, columns
+// 8 fg .. 8 fg + 7 with one 16-byte store.  A tile's values are in lane order,
+// so the lane's first value is the tile offset + the exclusive wave scan of
+// the lanes' kept counts; two 8-byte windows from the first value of each of
+// its nibbles are expanded by a 16-entry selector table with v_perm_b32 (zero
+// where a bit is clear).  A window reads at most 3 values past the last kept
+// one: inside the 16 readable bytes that follow the payload.
+__global__ void __launch_bounds__(256) k_expand_tiles16(const uint32_t* __restrict__ bm_tiles,
+                                                        const uint16_t* __restrict__ values,
+                                                        const int32_t* __restrict__ tile_offsets, int64_t N,
+                                                        int64_t K, int64_t tiles, uint16_t* __restrict__ Wd) {
+  __shared__ u32x2 lut[16];
+  if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{nibble_selector16(threadIdx.x, 0), nibble_selector16(threadIdx.x, 1)};
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= tiles) return;                            // whole waves leave together
+  const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const int64_t S = tile_steps(K);
+  const int64_t n = (t / S) * 16 + fr;
+  const int64_t k0 = (t % S) * 32 + 8 * fg;
+  const uint32_t byte = (bm_tiles[t * 16 + fr] >> (8 * fg)) & 0xffu;   // pad rows and columns: zero bits
+  const uint32_t cnt = __popc(byte);
+  const uint32_t oa = (uint32_t)tile_offsets[t] + wave_inclusive_scan(cnt) - cnt;
+  if (n >= N || k0 >= K) return;                     // (after the scan: every lane took part)
+  u32x4 a = u32x4{0u, 0u, 0u, 0u};
+  if (byte != 0u) {
+    const uint32_t ob = oa + __popc(byte & 0xfu);
+    u32x2 v0, v1;
+    __builtin_memcpy(&v0, values + oa, 8);
+    __builtin_memcpy(&v1, values + ob, 8);
+    const u32x2 slo = lut[byte & 0xfu], shi = lut[byte >> 4];
+    a.x = __builtin_amdgcn_perm(v0.y, v0.x, slo.x);
+    a.y = __builtin_amdgcn_perm(v0.y, v0.x, slo.y);
+    a.z = __builtin_amdgcn_perm(v1.y, v1.x, shi.x);
+    a.w = __builtin_amdgcn_perm(v1.y, v1.x, shi.y);
+  }
+  *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;    // K % 8 == 0 and Wd 16-byte aligned
+}
+
 // Thread (tile t, row r): decode one tile row into the dense matrix.
 template <int EB>
 __global__ void __launch_bounds__(256) k_unpack_tiled(const uint32_t* __restrict__ bm_tiles,
@@ -491,6 +531,12 @@ hipError_t launch_validate(const spl_matrix& Wc, uint32_t* err, hipStream_t s) {
 hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s) {
   if (Wc.layout == SPL_LAYOUT_TILE16) {
     const int64_t T = tile_blocks(Wc.rows) * tile_steps(Wc.cols);
+    if (Wc.dtype != SPL_I8 && Wc.cols % 8 == 0) {   // W_dense is 16-byte aligned (checked by the caller)
+      hipLaunchKernelGGL(k_expand_tiles16, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, Wc.bitmask,
+                         static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows, Wc.cols, T,
+                         static_cast<uint16_t*>(W_dense));
+      return hipGetLastError();
+    }
     const dim3 grid((unsigned)((T + 15) / 16)), block(256);
     if (Wc.dtype == SPL_I8) {
       hipLaunchKernelGGL(k_unpack_tiled<1>, grid, block, 0, s, Wc.bitmask, Wc.values, Wc.tile_offsets, Wc.rows,

@@ -215,6 +215,25 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
   return spl_sparse_linear_group(&t, 1, M, algo, stream);
 }
 
+int64_t spl_sparse_linear_expanded_workspace_bytes(const spl_matrix* Wc) {
+  if (spl_check_matrix(Wc) != SPL_OK) return -1;
+  return (2 * Wc->rows * Wc->cols + 255) / 256 * 256;   // rows, cols < 2^31: far from 2^63
+}
+
+spl_status spl_sparse_linear_expanded(const void* X, int64_t M, const spl_matrix* Wc, void* Y, void* workspace,
+                                      hipStream_t stream) {
+  int32_t algo = SPL_ALGO_PREFILL;
+  const spl_status st = check_sparse_task(X, M, Wc, Y, &algo);
+  if (st != SPL_OK) return st;
+  if (!workspace || !aligned(workspace, 16)) return SPL_ERR_INVALID_ARG;
+  if (spl::tile_blocks(Wc->rows) >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
+  (void)hipGetLastError();
+  const spl_status e = launched(spl::launch_unpack(*Wc, workspace, stream));   // the decoded [N][K] matrix
+  if (e != SPL_OK) return e;
+  return launched(spl::launch_dense_prefill(X, M, workspace, Wc->dtype, Wc->rows, Wc->cols, Y, stream));
+}
+
 spl_status spl_sparse_linear_group(const spl_sparse_task* tasks, int32_t count, int64_t M, int32_t algo,
                                    hipStream_t stream) {
   if (!tasks || count < 1 || count > SPL_MAX_GROUP || M < 0) return SPL_ERR_INVALID_ARG;

@@ -67,6 +67,7 @@ int main() {
       }
     }
   EXPECT(spl_magnitude_mask_workspace_bytes() > 0);
+  EXPECT(spl_sparse_linear_expanded_workspace_bytes(nullptr) == -1);
   for (int s = -2; s < 8; ++s) EXPECT(spl_status_string(s) != nullptr);
   EXPECT(spl_version() > 0);
 
@@ -82,6 +83,9 @@ int main() {
                               nnz < (1ll << 31) && d >= SPL_F16 && d <= SPL_I8 &&
                               (layout == SPL_LAYOUT_ROWS || layout == SPL_LAYOUT_TILE16);
             if (!sane) EXPECT(st != SPL_OK);
+            const int64_t wsb = spl_sparse_linear_expanded_workspace_bytes(&m);
+            EXPECT((st == SPL_OK) == (wsb >= 0));
+            if (st == SPL_OK) EXPECT(wsb >= 2 * N * K && wsb % 256 == 0);
             m.values_bytes = -1;
             EXPECT(spl_check_matrix(&m) != SPL_OK);
           }
@@ -121,6 +125,8 @@ int main() {
     if (M != 0) REJECTS(spl_sparse_linear(odd, M, &rows, Y, nullptr));
     REJECTS(spl_sparse_linear(X, M, &bad, Y, nullptr));
     REJECTS(spl_sparse_linear_ex(X, M, &bad, Y, 77, nullptr));
+    REJECTS(spl_sparse_linear_expanded(X, M, &bad, Y, Y, nullptr));
+    REJECTS(spl_sparse_linear_expanded(X, M, &rows, Y, nullptr, nullptr));
     REJECTS(spl_sparse_linear_silu_mul(X, M, &bad, &bad, Y, SPL_ALGO_AUTO, nullptr));
     REJECTS(spl_sparse_linear_int8(q, sc, M, &i8bad, sc, Y, nullptr, nullptr));
     REJECTS(spl_sparse_linear_int4(q, sc, M, &rows, sc, Y, nullptr, nullptr));

@@ -112,6 +112,25 @@ def test_sparse_linear_argument_checks(L):
     assert f(X, 2, None, Y, 0, None) == INVALID
 
 
+def test_sparse_linear_expanded_argument_checks(L):
+    m = _mat(layout=1, tile_offsets=0x40000)
+    X, Y, ws = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x80000)
+    L.spl_sparse_linear_expanded_workspace_bytes.restype = ctypes.c_int64
+    need = L.spl_sparse_linear_expanded_workspace_bytes(ctypes.byref(m))
+    assert need >= 2 * m.rows * m.cols and need % 256 == 0
+    assert L.spl_sparse_linear_expanded_workspace_bytes(None) == -1
+    f = L.spl_sparse_linear_expanded
+    assert f(X, 2, ctypes.byref(m), Y, None, None) == INVALID              # no workspace
+    assert f(X, 2, ctypes.byref(m), Y, ctypes.c_void_p(0x80008), None) == INVALID   # misaligned workspace
+    assert f(None, 0, ctypes.byref(m), None, ws, None) == OK               # M = 0 is a no-op
+    assert f(X, -1, ctypes.byref(m), Y, ws, None) == INVALID
+    m8 = _mat(dtype=3, layout=1, tile_offsets=0x40000)
+    assert f(X, 2, ctypes.byref(m8), Y, ws, None) == UNSUPPORTED          # fp16/bf16 only
+    mk = _mat(cols=100, layout=1, tile_offsets=0x40000)
+    assert f(X, 2, ctypes.byref(mk), Y, ws, None) == UNSUPPORTED          # K % 8 != 0
+    assert f(X, 2, None, Y, ws, None) == INVALID
+
+
 def test_int8_argument_checks(L):
     m = _mat(dtype=3, layout=1, tile_offsets=0x40000)
     X, Y, s = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x60000)

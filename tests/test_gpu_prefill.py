@@ -178,6 +178,42 @@ def test_dense_prefill_llama_rows(orc, spl, dtype, N, K):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,M,s", [(100, 1000, 70, 0.7), (300, 264, 300, 0.5), (2000, 72, 4100, 0.7),
+                                     (33, 512, 1, 1.0)])
+def test_sparse_linear_expanded(orc, spl, dtype, N, K, M, s):
+    """The decoded-copy path against the oracle in full (ragged shapes, a
+    large grid, one row, an all-pruned matrix), and bit for bit the dense
+    prefill kernel on spl_unpack's output."""
+    import torch
+
+    W, mask = synth.weight(980 + N, N, K, dtype, s)
+    X = synth.activations(981 + K, M, K, dtype)
+    Wc = _pack(spl, W, mask, dtype)
+    Xd = to_dev(X, dtype)
+    Y = spl.sparse_linear_expanded(Xd, Wc)
+    assert_close(from_dev_f64(Y), orc.linear_f64(X, orc.pack(W, dtype, mask)), f"expanded {dtype} {N}x{K} M={M}")
+    Yd = spl.dense_linear(Xd, spl.unpack(Wc), algo="prefill")
+    assert torch.equal(Y.view(torch.int16), Yd.view(torch.int16))
+
+
+@pytest.mark.parametrize("name,j", [("gate", 4), ("down", 6)])
+def test_sparse_linear_expanded_llama_rows(orc, spl, name, j):
+    """Llama-2-7B gate and down at 70% and M = 2048 (the direct-to-LDS dense
+    core on the decoded copy, one workspace reused): 64 full rows."""
+    import torch
+
+    _, N, K = synth.LLAMA2_7B_LINEARS[j]
+    M = 2048
+    W, mask = synth.weight(synth.weight_seed(0, j), N, K, "bf16", 0.7)
+    X = synth.activations(synth.activation_seed(j), M, K, "bf16")
+    Wc = _pack(spl, W, mask, "bf16")
+    ws = torch.empty((2 * 11008 * 4096,), dtype=torch.uint8, device="cuda")
+    Y = from_dev_f64(spl.sparse_linear_expanded(to_dev(X, "bf16"), Wc, workspace=ws))
+    rows = _sample_rows(M, 23 + j)
+    assert_close(Y[rows], orc.linear_f64(X[rows], orc.pack(W, "bf16", mask)), f"expanded {name} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_prefill_large_grid_ragged(orc, spl, dtype):
     """A grid of at least one 128 x 256 block per CU (the large tiling) with
     ragged N, M and an odd number of 32-column steps, compared in full, sparse
