@@ -540,6 +540,16 @@ def run_int8_prefill(args):
         quantize(*u)
         linears(*u)
 
+    # the decoded-copy path: one workspace for the largest matrix, reused by every launch on the stream
+    ws = torch.empty((max(spl.lib().spl_sparse_linear_expanded_workspace_bytes(ctypes.byref(m[0].view()))
+                          for m in mats),), dtype=torch.uint8, device="cuda")
+
+    def linears_expanded(M, grp):
+        i = INPUT_OF_GROUP[grp]
+        for j in grp:
+            spl.sparse_linear_int8_expanded(xq[(M, i)], sx[(M, i)], mats[j][0], mats[j][2], out=ys[(M, j)],
+                                            workspace=ws)
+
     for u in units:                                     # quantized inputs in place before linears-only timing
         quantize(*u)
     torch.cuda.synchronize()
@@ -561,10 +571,12 @@ def run_int8_prefill(args):
         d = {"layer_us": round(g * 1e3, 2), "linears_us": round(gl * 1e3, 2),
              "linears_dense_equiv_tops": round(f / (gl * 1e-3) / 1e12, 1), "quantize_us": round(gq * 1e3, 2),
              "quantize_hbm_gbs": round(qbytes / (gq * 1e-3) / 1e9, 1)}
+        _, ge = _timed(uM, lambda li, u: linears_expanded(*u), reps, 2, [0])
+        d.update({"expanded_linears_us": round(ge * 1e3, 2), "expanded_tops": round(f / (ge * 1e-3) / 1e12, 1)})
         if not args.no_dense:
             _, gd = _timed(uM, lambda li, u: linears(*u, dense=True), reps, 2, [0])
             d.update({"dense_linears_us": round(gd * 1e3, 2), "dense_tops": round(f / (gd * 1e-3) / 1e12, 1),
-                      "speedup_vs_dense": round(gd / gl, 3)})
+                      "speedup_vs_dense": round(gd / gl, 3), "expanded_speedup_vs_dense": round(gd / ge, 3)})
         per_M[str(M)] = d
     cpu = None
     if not args.no_cpu_baseline:

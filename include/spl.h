@@ -223,9 +223,10 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
  * prefill kernel on the decoded matrix.  Two launches: spl_unpack into the
  * workspace, then the dense product.
  *   workspace  device scratch of spl_sparse_linear_expanded_workspace_bytes(Wc)
- *              bytes (2 rows cols, rounded up to 256), 16-byte aligned, owned
- *              by the caller, overwritten (one buffer can serve every matrix
- *              of a layer in turn on one stream).
+ *              bytes (2 rows cols for fp16/bf16, rows cols for int8, rounded
+ *              up to 256), 16-byte aligned, owned by the caller, overwritten
+ *              (one buffer can serve every matrix of a layer in turn on one
+ *              stream).
  * The workspace-size function returns -1 for a view spl_check_matrix rejects. */
 int64_t spl_sparse_linear_expanded_workspace_bytes(const spl_matrix* Wc);
 spl_status spl_sparse_linear_expanded(const void* X, int64_t M, const spl_matrix* Wc, void* Y, void* workspace,
@@ -330,6 +331,17 @@ spl_status spl_sparse_linear_silu_mul(const void* X, int64_t M, const spl_matrix
  *   Requires K % 16 == 0. */
 spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream);
+
+/* spl_sparse_linear_int8 for large batches through a decoded copy of the
+ * codes (as spl_sparse_linear_expanded for fp16/bf16; paper sections 2.4.2 and
+ * 3.4): spl_unpack writes the dense [N][K] int8 codes into the workspace, then
+ * the dense int8 prefill kernel multiplies.  Same arguments, checks and
+ * results (exact int32 sums, the same fp16 epilogue: bit-identical to
+ * spl_sparse_linear_int8); workspace: spl_sparse_linear_expanded_workspace_bytes(Wqc)
+ * bytes, 16-byte aligned, caller-owned, overwritten. */
+spl_status spl_sparse_linear_int8_expanded(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
+                                           const float* w_scales, void* Y, int32_t* acc_out, void* workspace,
+                                           hipStream_t stream);
 
 /* 4-bit sparse payloads (paper section 4 names INT4 as future work; the
  * reading taken: the int8 tile layout's pattern and value order, value i the

@@ -107,6 +107,7 @@ def lib() -> ctypes.CDLL:
         "spl_sparse_linear_expanded_workspace_bytes": (I64, [MP]),
         "spl_sparse_linear_expanded": (ctypes.c_int, [P, I64, MP, P, P, P]),
         "spl_sparse_linear_int8": (ctypes.c_int, [P, P, I64, MP, P, P, P, P]),
+        "spl_sparse_linear_int8_expanded": (ctypes.c_int, [P, P, I64, MP, P, P, P, P, P]),
         "spl_quantize_rows_i8": (ctypes.c_int, [P, ctypes.c_int32, I64, I64, P, P, P]),
         "spl_sparse_linear_silu_mul": (ctypes.c_int, [P, I64, MP, MP, P, I32, P]),
         "spl_magnitude_mask_workspace_bytes": (I64, []),
@@ -564,6 +565,33 @@ def sparse_linear_int8(Xq: torch.Tensor, x_scales: torch.Tensor, Wqc: SparseMatr
     _check("spl_sparse_linear_int8", L.spl_sparse_linear_int8(_ptr(Xq), _ptr(x_scales), M, ctypes.byref(view),
                                                               _ptr(w_scales), _ptr(out), _ptr(acc_out),
                                                               _stream(stream)))
+    return out
+
+
+def sparse_linear_int8_expanded(Xq: torch.Tensor, x_scales: torch.Tensor, Wqc: SparseMatrix, w_scales: torch.Tensor,
+                                out: torch.Tensor | None = None, acc_out: torch.Tensor | None = None,
+                                workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """sparse_linear_int8 through a decoded copy of the codes in `workspace`
+    (see spl_sparse_linear_int8_expanded): for large batches."""
+    L = lib()
+    M = _rows_of(Xq, "Xq")
+    _q_args(Xq, x_scales, Wqc.rows, Wqc.cols, w_scales, M, device=False)
+    if out is None:
+        out = torch.empty((M, Wqc.rows), dtype=torch.float16, device=Xq.device)
+    _q_outs(out, acc_out, M, Wqc.rows)
+    _q_args(Xq, x_scales, Wqc.rows, Wqc.cols, w_scales, M)
+    view = Wqc.view()
+    need = L.spl_sparse_linear_expanded_workspace_bytes(ctypes.byref(view))
+    if need < 0:
+        raise ValueError("spl_sparse_linear_int8_expanded: the matrix view is invalid")
+    if workspace is None:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=Xq.device)
+    _dev_tensor(workspace, "workspace")
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace holds {workspace.numel() * workspace.element_size()} bytes, needs {need}")
+    _check("spl_sparse_linear_int8_expanded",
+           L.spl_sparse_linear_int8_expanded(_ptr(Xq), _ptr(x_scales), M, ctypes.byref(view), _ptr(w_scales),
+                                             _ptr(out), _ptr(acc_out), _ptr(workspace), _stream(stream)))
     return out
 
 

@@ -292,6 +292,53 @@ __global__ void __launch_bounds__(256) k_expand_tiles16(const uint32_t* __restri
   *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;    // K % 8 == 0 and Wd 16-byte aligned
 }
 
+// The same for an int8 tile-layout matrix with K % 16 == 0: two tiles per
+// wave (lanes 0-31 the first, 32-63 the second), lane (r, g) of a tile
+// (r = lane % 16, g = lane / 16 % 2) writes row r, columns 16 g .. 16 g + 15
+// with one 16-byte store.  A tile's int8 values are ordered by 16-column
+// group, then row (the order of its 32 lanes), so the lane's first value is
+// the tile offset + the exclusive scan over its half-wave of the lanes' kept
+// counts; the 8-byte windows from the first value of columns 0-7 and of
+// columns 8-15 of its group are expanded per nibble by a selector table
+// indexed by the nibble and the place of its first value in the window.  A
+// window reads at most 7 bytes past the last kept value: inside the 16
+// readable bytes that follow the payload.
+__global__ void __launch_bounds__(256) k_expand_tiles8(const uint32_t* __restrict__ bm_tiles,
+                                                       const uint8_t* __restrict__ values,
+                                                       const int32_t* __restrict__ tile_offsets, int64_t N,
+                                                       int64_t K, int64_t tiles, uint8_t* __restrict__ Wd) {
+  __shared__ uint32_t lut[80];
+  if (threadIdx.x < 80) lut[threadIdx.x] = nibble_selector8(threadIdx.x / 5, threadIdx.x % 5);
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 2;   // the wave's first tile
+  if (t0 >= tiles) return;                           // whole waves leave together
+  const int64_t t = t0 + (lane >> 5);
+  const bool live = t < tiles;
+  const int r = lane & 15, gq = (lane >> 4) & 1;
+  const uint32_t hw = live ? (bm_tiles[t * 16 + r] >> (16 * gq)) & 0xffffu : 0u;   // pad rows, columns: 0
+  const uint32_t cnt = __popc(hw);
+  const uint32_t oa = (live ? (uint32_t)tile_offsets[t] : 0u) + half_inclusive_scan(cnt) - cnt;
+  if (!live) return;                                 // (after the scan: every lane took part)
+  const int64_t S = tile_steps(K);
+  const int64_t n = (t / S) * 16 + r;
+  const int64_t k0 = (t % S) * 32 + 16 * gq;
+  if (n >= N || k0 >= K) return;
+  u32x4 a = u32x4{0u, 0u, 0u, 0u};
+  if (hw != 0u) {
+    const uint32_t q0 = hw & 15u, q1 = (hw >> 4) & 15u, q2 = (hw >> 8) & 15u, q3 = hw >> 12;
+    const uint32_t ob = oa + __popc(hw & 0xffu);    // columns 8-15 start after the kept ones of 0-7
+    u32x2 v0, v1;
+    __builtin_memcpy(&v0, values + oa, 8);
+    __builtin_memcpy(&v1, values + ob, 8);
+    a.x = __builtin_amdgcn_perm(v0.y, v0.x, lut[5 * q0]);
+    a.y = __builtin_amdgcn_perm(v0.y, v0.x, lut[5 * q1 + __popc(q0)]);
+    a.z = __builtin_amdgcn_perm(v1.y, v1.x, lut[5 * q2]);
+    a.w = __builtin_amdgcn_perm(v1.y, v1.x, lut[5 * q3 + __popc(q2)]);
+  }
+  *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;    // K % 16 == 0 and Wd 16-byte aligned
+}
+
 // Thread (tile t, row r): decode one tile row into the dense matrix.
 template <int EB>
 __global__ void __launch_bounds__(256) k_unpack_tiled(const uint32_t* __restrict__ bm_tiles,
@@ -535,6 +582,12 @@ hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s) {
       hipLaunchKernelGGL(k_expand_tiles16, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, Wc.bitmask,
                          static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows, Wc.cols, T,
                          static_cast<uint16_t*>(W_dense));
+      return hipGetLastError();
+    }
+    if (Wc.dtype == SPL_I8 && Wc.cols % 16 == 0) {
+      hipLaunchKernelGGL(k_expand_tiles8, dim3((unsigned)((T + 7) / 8)), dim3(256), 0, s, Wc.bitmask,
+                         static_cast<const uint8_t*>(Wc.values), Wc.tile_offsets, Wc.rows, Wc.cols, T,
+                         static_cast<uint8_t*>(W_dense));
       return hipGetLastError();
     }
     const dim3 grid((unsigned)((T + 15) / 16)), block(256);

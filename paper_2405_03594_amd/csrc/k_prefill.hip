@@ -693,8 +693,12 @@ __device__ __forceinline__ void dma_rows(const uint16_t* src, int64_t K, int st,
     lds_dma16(src + 8 * K * i + kPfBK * st, buf + (8 * kGroups * wave + 8 * i) * kPfRow);
 }
 
+// (int8 payloads, I8P: rows of K bytes staged as K/2 16-bit units, exact int32 sums, the int8 epilogue)
 template <class T, bool kGather, int NW>
 __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma(const PfArgs g) {
+  constexpr bool kI8 = std::is_same<T, I8P>::value;
+  static_assert(!(kI8 && kGather), "gather: 16-bit payloads");
+  using Acc = typename MfmaP<T>::acc_t;
   constexpr int FN = 4, FM = kDmaBM / (8 * NW);
   constexpr int GA = kDmaBN / 8 / NW, GB = kDmaBM / 8 / NW;      // 8-row groups per wave: W, X
   constexpr int kLoads = GA + GB;                                 // 1 KB requests per wave and stage
@@ -704,24 +708,25 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma(const PfArgs g
   const int wn = wave & 1, wm = wave >> 1;
   const int fr = lane & 15, fg = lane >> 4;
   const int64_t M = g.M, N = g.N, K = g.K;
-  const int nst = (int)(K / kPfBK);
+  const int64_t Kh = kI8 ? K / 2 : K;                 // row length in 16-bit units
+  const int nst = (int)(Kh / kPfBK);
   const int64_t n0 = (int64_t)blockIdx.x * kDmaBN, m0 = (int64_t)blockIdx.y * kDmaBM;
   // my slot in an 8-row group: row lane / 8, position lane % 8, holding chunk (lane % 8) ^ (lane / 8)
   const int lr = lane >> 3, lc = (lane & 7) ^ lr;
   // wave w requests W rows 8 GA w .. + 8 GA and X rows 8 GB w .. + 8 GB
-  const uint16_t* wsrc = g.W + (n0 + 8 * GA * wave + lr) * K + 8 * lc;
-  const uint16_t* xsrc = g.X + (m0 + 8 * GB * wave + lr) * K + 8 * lc;
+  const uint16_t* wsrc = g.W + (n0 + 8 * GA * wave + lr) * Kh + 8 * lc;
+  const uint16_t* xsrc = g.X + (m0 + 8 * GB * wave + lr) * Kh + 8 * lc;
   auto request = [&](int st, int buf) {
     unsigned char* a = dsm + buf * kDmaStageBytes;
-    dma_rows<GA>(wsrc, K, st, a, wave);
-    dma_rows<GB>(xsrc, K, st, a + kDmaBN * kPfRow, wave);
+    dma_rows<GA>(wsrc, Kh, st, a, wave);
+    dma_rows<GB>(xsrc, Kh, st, a + kDmaBN * kPfRow, wave);
   };
 
-  f32x4 acc[FN][FM];
+  Acc acc[FN][FM];
 #pragma unroll
   for (int i = 0; i < FN; ++i)
 #pragma unroll
-    for (int j = 0; j < FM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
   request(0, 0);
   if (nst > 1) request(1, 1);
@@ -735,7 +740,9 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma(const PfArgs g
     pf_mfma_stage<T, FN, FM>(acc, abuf, abuf + kDmaBN * kPfRow, wn, wm, fr, fg);
     cur = cur == kDmaStages - 1 ? 0 : cur + 1;
   }
-  if constexpr (kGather)
+  if constexpr (kI8)
+    pf_store_i8<FN, FM>(acc, g.Y, g.acc, g.sx, g.sw, M, N, n0, m0, wn, wm, fr, fg);
+  else if constexpr (kGather)
     pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);
   else
     pf_store<T, FN, FM>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
@@ -832,8 +839,8 @@ hipError_t dense_prefill_dma(const PfArgs& a, hipStream_t s) {
 
 template <class T, bool kGather = false>
 hipError_t dense_prefill_t(const PfArgs& a, hipStream_t s) {
-  if constexpr (!std::is_same<T, I8P>::value)
-    if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, a.K, kDmaBN, kDmaBM)) return dense_prefill_dma<T, kGather>(a, s);
+  if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, pf_units<T>(a.K), kDmaBN, kDmaBM))
+    return dense_prefill_dma<T, kGather>(a, s);
   if (pf_large_tile(a.N, a.M)) return dense_prefill_tile<T, 128, 256, 8, 1, kGather>(a, s);
   return pf_split_k(a.N, a.M) ? dense_prefill_tile<T, 64, 128, 4, 2, kGather>(a, s)
                               : dense_prefill_tile<T, 64, 128, 4, 1, kGather>(a, s);

@@ -217,7 +217,8 @@ spl_status spl_sparse_linear_ex(const void* X, int64_t M, const spl_matrix* Wc, 
 
 int64_t spl_sparse_linear_expanded_workspace_bytes(const spl_matrix* Wc) {
   if (spl_check_matrix(Wc) != SPL_OK) return -1;
-  return (2 * Wc->rows * Wc->cols + 255) / 256 * 256;   // rows, cols < 2^31: far from 2^63
+  const int64_t eb = Wc->dtype == SPL_I8 ? 1 : 2;
+  return (eb * Wc->rows * Wc->cols + 255) / 256 * 256;   // rows, cols < 2^31: far from 2^63
 }
 
 spl_status spl_sparse_linear_expanded(const void* X, int64_t M, const spl_matrix* Wc, void* Y, void* workspace,
@@ -471,6 +472,24 @@ spl_status spl_sparse_linear_int8(const int8_t* Xq, const float* x_scales, int64
                                   const float* w_scales, void* Y, int32_t* acc_out, hipStream_t stream) {
   const spl_int8_task t{Xq, x_scales, Wqc, w_scales, Y, acc_out};
   return spl_sparse_linear_int8_group(&t, 1, M, stream);
+}
+
+spl_status spl_sparse_linear_int8_expanded(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* Wqc,
+                                           const float* w_scales, void* Y, int32_t* acc_out, void* workspace,
+                                           hipStream_t stream) {
+  const spl_int8_task t{Xq, x_scales, Wqc, w_scales, Y, acc_out};
+  if (!Wqc) return SPL_ERR_INVALID_ARG;
+  const spl_status st = check_int8_task(&t, M);
+  if (st != SPL_OK) return st;
+  if (!workspace || !aligned(workspace, 16)) return SPL_ERR_INVALID_ARG;
+  if (spl::tile_blocks(Wqc->rows) >= kMaxDim || M >= kMaxDim) return SPL_ERR_OVERFLOW;
+  if (M == 0) return SPL_OK;
+  (void)hipGetLastError();
+  const spl_status e = launched(spl::launch_unpack(*Wqc, workspace, stream));   // the decoded [N][K] codes
+  if (e != SPL_OK) return e;
+  const spl_dense_int8_task d{Xq, x_scales, static_cast<const int8_t*>(workspace), w_scales, Wqc->rows, Wqc->cols,
+                              Y, acc_out};
+  return launched(spl::launch_dense_prefill_i8(d, M, stream));
 }
 
 spl_status spl_sparse_linear_int8_group(const spl_int8_task* tasks, int32_t count, int64_t M, hipStream_t stream) {

@@ -85,7 +85,7 @@ int main() {
             if (!sane) EXPECT(st != SPL_OK);
             const int64_t wsb = spl_sparse_linear_expanded_workspace_bytes(&m);
             EXPECT((st == SPL_OK) == (wsb >= 0));
-            if (st == SPL_OK) EXPECT(wsb >= 2 * N * K && wsb % 256 == 0);
+            if (st == SPL_OK) EXPECT(wsb >= (d == SPL_I8 ? 1 : 2) * N * K && wsb % 256 == 0);
             m.values_bytes = -1;
             EXPECT(spl_check_matrix(&m) != SPL_OK);
           }
@@ -127,6 +127,8 @@ int main() {
     REJECTS(spl_sparse_linear_ex(X, M, &bad, Y, 77, nullptr));
     REJECTS(spl_sparse_linear_expanded(X, M, &bad, Y, Y, nullptr));
     REJECTS(spl_sparse_linear_expanded(X, M, &rows, Y, nullptr, nullptr));
+    REJECTS(spl_sparse_linear_int8_expanded(q, sc, M, &i8bad, sc, Y, nullptr, Y, nullptr));
+    REJECTS(spl_sparse_linear_int8_expanded(q, sc, M, &rows, sc, Y, nullptr, nullptr, nullptr));
     REJECTS(spl_sparse_linear_silu_mul(X, M, &bad, &bad, Y, SPL_ALGO_AUTO, nullptr));
     REJECTS(spl_sparse_linear_int8(q, sc, M, &i8bad, sc, Y, nullptr, nullptr));
     REJECTS(spl_sparse_linear_int4(q, sc, M, &rows, sc, Y, nullptr, nullptr));

@@ -131,6 +131,21 @@ def test_sparse_linear_expanded_argument_checks(L):
     assert f(X, 2, None, Y, ws, None) == INVALID
 
 
+def test_int8_expanded_argument_checks(L):
+    m = _mat(dtype=3, layout=1, tile_offsets=0x40000)
+    X, Y, s, ws = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x60000), ctypes.c_void_p(0x80000)
+    L.spl_sparse_linear_expanded_workspace_bytes.restype = ctypes.c_int64
+    assert L.spl_sparse_linear_expanded_workspace_bytes(ctypes.byref(m)) >= m.rows * m.cols   # one byte per code
+    f = L.spl_sparse_linear_int8_expanded
+    assert f(X, s, 2, ctypes.byref(m), s, Y, None, None, None) == INVALID          # no workspace
+    assert f(X, s, 2, ctypes.byref(m), s, Y, None, ctypes.c_void_p(0x80004), None) == INVALID
+    assert f(X, None, 2, ctypes.byref(m), s, Y, None, ws, None) == INVALID         # no activation scales
+    assert f(None, None, 0, ctypes.byref(m), None, None, None, ws, None) == OK     # M = 0 is a no-op
+    mb = _mat(layout=1, tile_offsets=0x40000)
+    assert f(X, s, 2, ctypes.byref(mb), s, Y, None, ws, None) == UNSUPPORTED      # a bf16 view
+    assert f(X, s, 2, None, s, Y, None, ws, None) == INVALID
+
+
 def test_int8_argument_checks(L):
     m = _mat(dtype=3, layout=1, tile_offsets=0x40000)
     X, Y, s = ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000), ctypes.c_void_p(0x60000)

@@ -276,6 +276,53 @@ def test_dense_int8_prefill(orc, spl):
     _assert_equal(y[rows], y_ref, "dense gate Y M=512")
 
 
+@pytest.mark.parametrize("N,K,M,s", [(100, 1008, 70, 0.7), (130, 272, 300, 0.5), (2000, 144, 4100, 0.7),
+                                     (33, 512, 1, 1.0)])
+def test_int8_expanded(orc, spl, N, K, M, s):
+    """The decoded-copy int8 path: int32 sums and fp16 outputs bit for bit the
+    oracle's in full (ragged shapes, a large ragged grid, one row, an
+    all-pruned matrix) and bit for bit spl_sparse_linear_int8's."""
+    import torch
+
+    Wq, mask, sw = synth.int8_weight(990 + N, N, K, s)
+    Xq, sx = synth.int8_activations(991 + K, M, K)
+    acc_ref, y_ref = orc.linear_i8(Xq, sx, orc.pack(Wq, "i8", mask), sw)
+    Wqc = spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda())
+    acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    Xd, sxd, swd = to_dev(Xq, "i8"), torch.from_numpy(sx).cuda(), torch.from_numpy(sw).cuda()
+    Y = spl.sparse_linear_int8_expanded(Xd, sxd, Wqc, swd, acc_out=acc)
+    _assert_equal(acc.cpu().numpy(), acc_ref, f"expanded acc N={N} K={K} M={M}")
+    _assert_equal(Y.cpu().view(torch.int16).numpy().view(np.uint16), y_ref, f"expanded Y N={N} K={K} M={M}")
+    Y2 = spl.sparse_linear_int8(Xd, sxd, Wqc, swd)
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ["gate", "down"])
+def test_int8_expanded_and_dense_llama_rows(orc, spl, name):
+    """Llama-2-7B gate and down at 70% and M = 2048 (the direct-to-LDS dense
+    int8 core on the decoded codes, and on the dense codes for the comparator):
+    64 full rows bit for bit."""
+    import torch
+
+    j = [n for n, _, _ in synth.LLAMA2_7B_LINEARS].index(name)
+    _, N, K = synth.LLAMA2_7B_LINEARS[j]
+    M = 2048
+    Wq, mask, sw = synth.int8_weight(synth.weight_seed(0, j), N, K, 0.7)
+    Xq, sx = synth.int8_activations(synth.activation_seed(j), M, K)
+    rows = _sample_rows(M, 31 + j)
+    acc_ref, y_ref = orc.linear_i8(Xq[rows], sx[rows], orc.pack(Wq, "i8", mask), sw)
+    Wqc = spl.pack_sparse(to_dev(Wq, "i8"), torch.from_numpy(mask).cuda())
+    acc = torch.empty((M, N), dtype=torch.int32, device="cuda")
+    Y = spl.sparse_linear_int8_expanded(to_dev(Xq, "i8"), torch.from_numpy(sx).cuda(), Wqc,
+                                        torch.from_numpy(sw).cuda(), acc_out=acc)
+    _assert_equal(acc.cpu().numpy()[rows], acc_ref, f"{name} expanded acc")
+    _assert_equal(Y.cpu().view(torch.int16).numpy().view(np.uint16)[rows], y_ref, f"{name} expanded Y")
+    Wm = np.where(mask.astype(bool), Wq, np.zeros_like(Wq))
+    dacc, dy = _run_dense(spl, Xq, sx, Wm, sw)
+    _assert_equal(dacc[rows], acc_ref, f"{name} dense acc")
+    _assert_equal(dy[rows], y_ref, f"{name} dense Y")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("M,K", [(1, 8), (3, 520), (5, 6000), (3, 20000), (300, 4096), (17, 11008), (2048, 11008)])
 def test_quantize_rows_matches_oracle(orc, spl, dtype, M, K):

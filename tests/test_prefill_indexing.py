@@ -468,25 +468,28 @@ def _dma_lines():
     for line in ("constexpr int kDmaBN = 128, kDmaBM = 256, kDmaStages = 3, kDmaWaves = 8;",
                  "constexpr int GA = kDmaBN / 8 / NW, GB = kDmaBM / 8 / NW;",
                  "const int lr = lane >> 3, lc = (lane & 7) ^ lr;",
-                 "const uint16_t* wsrc = g.W + (n0 + 8 * GA * wave + lr) * K + 8 * lc;",
-                 "const uint16_t* xsrc = g.X + (m0 + 8 * GB * wave + lr) * K + 8 * lc;",
+                 "const uint16_t* wsrc = g.W + (n0 + 8 * GA * wave + lr) * Kh + 8 * lc;",
+                 "const uint16_t* xsrc = g.X + (m0 + 8 * GB * wave + lr) * Kh + 8 * lc;",
                  "lds_dma16(src + 8 * K * i + kPfBK * st, buf + (8 * kGroups * wave + 8 * i) * kPfRow);",
-                 "dma_rows<GA>(wsrc, K, st, a, wave);",
-                 "dma_rows<GB>(xsrc, K, st, a + kDmaBN * kPfRow, wave);",
+                 "dma_rows<GA>(wsrc, Kh, st, a, wave);",
+                 "dma_rows<GB>(xsrc, Kh, st, a + kDmaBN * kPfRow, wave);",
+                 "const int64_t Kh = kI8 ? K / 2 : K;",
                  "if (st + 2 < nst) request(st + 2, cur == 0 ? 2 : cur - 1);",
-                 "if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, a.K, kDmaBN, kDmaBM)) return dense_prefill_dma<T, kGather>(a, s);"):
+                 "if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, pf_units<T>(a.K), kDmaBN, kDmaBM))"):
         assert line in src, f"direct-to-LDS staging changed: update this replay ({line})"
     return 128, 256, 8
 
 
-@pytest.mark.parametrize("N,M,K", [(4096, 2048, 4096), (11008, 512, 4096), (4096, 256, 11008), (128, 256, 64)])
+@pytest.mark.parametrize("N,M,K", [(4096, 2048, 4096), (11008, 512, 4096), (4096, 256, 11008), (128, 256, 64),
+                                   (4096, 2048, 5504)])
 def test_dma_requests_fill_the_swizzled_stage(N, M, K):
     """One stage's direct-to-LDS requests of a workgroup: lane i of a request
     fills 16-byte slot i of a 1 KB run.  Every (row, chunk) of the W and X
     stage lands exactly once, at the swizzled place the MFMA reads use
     (pf_chunk: chunk c of row r at position c ^ (r % 8)), from inside the
     matrices; the three stage buffers rotate so that a request never hits
-    the buffer being multiplied or the one published next."""
+    the buffer being multiplied or the one published next.  K counts 16-bit
+    units (an int8 row of K codes is K / 2 of them: 5504 for the down shape)."""
     BN, BM, NW = _dma_lines()
     bk, _ = _constants()
     row_bytes = 2 * bk
@@ -515,3 +518,87 @@ def test_dma_requests_fill_the_swizzled_stage(N, M, K):
         cur = st % 3
         target = 2 if cur == 0 else cur - 1
         assert target == (st + 2) % 3 and target not in (st % 3, (st + 1) % 3)
+
+
+# ---------------------------------------------------------------- tile-layout expansion (spl_unpack's fast kernels)
+
+PACK_SRC = os.path.join(os.path.dirname(SRC), "k_pack.hip")
+
+
+def _expand_lines():
+    src = open(PACK_SRC).read()
+    for line in ("const uint32_t byte = (bm_tiles[t * 16 + fr] >> (8 * fg)) & 0xffu;",
+                 "const uint32_t oa = (uint32_t)tile_offsets[t] + wave_inclusive_scan(cnt) - cnt;",
+                 "const uint32_t ob = oa + __popc(byte & 0xfu);",
+                 "*reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;",
+                 "const int64_t t = t0 + (lane >> 5);",
+                 "const uint32_t hw = live ? (bm_tiles[t * 16 + r] >> (16 * gq)) & 0xffffu : 0u;",
+                 "const uint32_t oa = (live ? (uint32_t)tile_offsets[t] : 0u) + half_inclusive_scan(cnt) - cnt;",
+                 "const int64_t k0 = (t % S) * 32 + 16 * gq;",
+                 "const uint32_t ob = oa + __popc(hw & 0xffu);",
+                 "a.y = __builtin_amdgcn_perm(v0.y, v0.x, lut[5 * q1 + __popc(q0)]);",
+                 "a.w = __builtin_amdgcn_perm(v1.y, v1.x, lut[5 * q3 + __popc(q2)]);",
+                 "if (Wc.dtype == SPL_I8 && Wc.cols % 16 == 0) {"):
+        assert line in src, f"expansion changed: update this replay ({line})"
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "i8"])
+@pytest.mark.parametrize("N,K,s", [(16, 32, 0.5), (33, 64, 0.7), (100, 1008, 0.0), (17, 96, 1.0), (48, 4096, 0.9)])
+def test_expand_tiles_rebuild_the_dense_matrix(orc, dtype, N, K, s):
+    """Every lane of the expansion kernels, replayed: its windows stay inside
+    the payload + 16 readable bytes, and the 16-byte pieces it stores are the
+    oracle's dense masked matrix (16-bit: 8 columns per lane of a 64-lane tile;
+    int8: 16 columns per lane of a 32-lane half-wave tile)."""
+    _expand_lines()
+    if dtype == "i8":
+        W, mask, _ = synth.int8_weight(77 + N + K, N, K, s)
+        eb, width = 1, 16
+    else:
+        W, mask = synth.weight(77 + N + K, N, K, dtype, s)
+        eb, width = 2, 8
+    T = orc.pack_tiled(W, dtype, mask)
+    vbytes = np.concatenate([T.values.view(np.uint8), np.zeros(16, np.uint8)])
+    dense = np.where(mask.astype(bool), W, np.zeros_like(W)).view(np.uint8).reshape(N, K * eb)
+    S, B = -(-K // 32), -(-N // 16)
+    bm = T.bitmask.reshape(-1).astype(np.int64)
+    offs = T.tile_offsets.astype(np.int64)
+    got = np.zeros((N, K * eb), np.uint8)
+    lanes = 64 if eb == 2 else 32
+    for t in range(B * S):
+        cnt = []
+        for l in range(lanes):
+            r, g = l & 15, l >> 4
+            bits = (int(bm[t * 16 + r]) >> (width * g)) & ((1 << width) - 1)
+            cnt.append(_popc(bits))
+        ex = np.cumsum(cnt) - np.array(cnt)
+        for l in range(lanes):
+            r, g = l & 15, l >> 4
+            n, k0 = (t // S) * 16 + r, (t % S) * 32 + width * g
+            bits = (int(bm[t * 16 + r]) >> (width * g)) & ((1 << width) - 1)
+            if n >= N or k0 >= K:
+                assert bits == 0
+                continue
+            oa = int(offs[t]) + int(ex[l])
+            if eb == 2:
+                ob = oa + _popc(bits & 0xF)
+                assert 2 * ob + 8 <= 2 * T.nnz + 16
+                v0 = vbytes[2 * oa:2 * oa + 8].view(np.uint32)
+                v1 = vbytes[2 * ob:2 * ob + 8].view(np.uint32)
+                words = [_perm(v0[1], v0[0], _nibble_selector(bits & 0xF, 0)),
+                         _perm(v0[1], v0[0], _nibble_selector(bits & 0xF, 1)),
+                         _perm(v1[1], v1[0], _nibble_selector(bits >> 4, 0)),
+                         _perm(v1[1], v1[0], _nibble_selector(bits >> 4, 1))]
+            else:
+                q = [(bits >> (4 * i)) & 0xF for i in range(4)]
+                ob = oa + _popc(bits & 0xFF)
+                assert ob + 8 <= T.nnz + 16
+                v0 = vbytes[oa:oa + 8].view(np.uint32)
+                v1 = vbytes[ob:ob + 8].view(np.uint32)
+                words = [_perm(v0[1], v0[0], _i8_selector(q[0], 0)),
+                         _perm(v0[1], v0[0], _i8_selector(q[1], _popc(q[0]))),
+                         _perm(v1[1], v1[0], _i8_selector(q[2], 0)),
+                         _perm(v1[1], v1[0], _i8_selector(q[3], _popc(q[2])))]
+            piece = np.array(words, np.uint32).view(np.uint8)
+            assert k0 * eb + 16 <= K * eb
+            got[n, k0 * eb:k0 * eb + 16] = piece
+    assert np.array_equal(got, dense)
