@@ -252,14 +252,17 @@ __global__ void __launch_bounds__(256) k_tile_scatter(const uint32_t* __restrict
   }
 }
 
-// The dense image of a 16-bit tile-layout matrix with K % 8 == 0: one wave
-// per tile (4 per workgroup), lane (fr, fg) writes row fr, columns
-// 8 fg .. 8 fg + 7 with one 16-byte store.  A tile's values are in lane order,
-// so the lane's first value is the tile offset + the exclusive wave scan of
-// the lanes' kept counts; two 8-byte windows from the first value of each of
-// its nibbles are expanded by a 16-entry selector table with v_perm_b32 (zero
-// where a bit is clear).  A window reads at most 3 values past the last kept
-// one: inside the 16 readable bytes that follow the payload.
+// The dense image of a 16-bit tile-layout matrix with K % 8 == 0.  A wave
+// expands kExpandTiles consecutive tiles (4 per workgroup of 4 waves), with
+// every tile's loads in flight together: lane (fr, fg) writes row fr, columns
+// 8 fg .. 8 fg + 7 of each with one 16-byte store.  A tile's values are in
+// lane order, so the lane's first value is the tile offset + the exclusive
+// wave scan of the lanes' kept counts (two tiles per scan, in 16-bit halves);
+// two 8-byte windows from the first value of each of its nibbles are expanded
+// by a 16-entry selector table with v_perm_b32 (zero where a bit is clear).
+// A window reads at most 3 values past the last kept one: inside the 16
+// readable bytes that follow the payload.
+constexpr int kExpandTiles = 4;
 __global__ void __launch_bounds__(256) k_expand_tiles16(const uint32_t* __restrict__ bm_tiles,
                                                         const uint16_t* __restrict__ values,
                                                         const int32_t* __restrict__ tile_offsets, int64_t N,
@@ -267,42 +270,61 @@ __global__ void __launch_bounds__(256) k_expand_tiles16(const uint32_t* __restri
   __shared__ u32x2 lut[16];
   if (threadIdx.x < 16) lut[threadIdx.x] = u32x2{nibble_selector16(threadIdx.x, 0), nibble_selector16(threadIdx.x, 1)};
   __syncthreads();
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= tiles) return;                            // whole waves leave together
+  const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kExpandTiles;
+  if (t0 >= tiles) return;                           // whole waves leave together
   const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
   const int64_t S = tile_steps(K);
-  const int64_t n = (t / S) * 16 + fr;
-  const int64_t k0 = (t % S) * 32 + 8 * fg;
-  const uint32_t byte = (bm_tiles[t * 16 + fr] >> (8 * fg)) & 0xffu;   // pad rows and columns: zero bits
-  const uint32_t cnt = __popc(byte);
-  const uint32_t oa = (uint32_t)tile_offsets[t] + wave_inclusive_scan(cnt) - cnt;
-  if (n >= N || k0 >= K) return;                     // (after the scan: every lane took part)
-  u32x4 a = u32x4{0u, 0u, 0u, 0u};
-  if (byte != 0u) {
-    const uint32_t ob = oa + __popc(byte & 0xfu);
-    u32x2 v0, v1;
-    __builtin_memcpy(&v0, values + oa, 8);
-    __builtin_memcpy(&v1, values + ob, 8);
-    const u32x2 slo = lut[byte & 0xfu], shi = lut[byte >> 4];
-    a.x = __builtin_amdgcn_perm(v0.y, v0.x, slo.x);
-    a.y = __builtin_amdgcn_perm(v0.y, v0.x, slo.y);
-    a.z = __builtin_amdgcn_perm(v1.y, v1.x, shi.x);
-    a.w = __builtin_amdgcn_perm(v1.y, v1.x, shi.y);
+  uint32_t byte[kExpandTiles], oa[kExpandTiles];
+#pragma unroll
+  for (int i = 0; i < kExpandTiles; ++i) {          // tiles past the end: no kept bits, no store
+    const bool live = t0 + i < tiles;
+    byte[i] = live ? (bm_tiles[(t0 + i) * 16 + fr] >> (8 * fg)) & 0xffu : 0u;   // pad rows, columns: 0
+    oa[i] = live ? (uint32_t)tile_offsets[t0 + i] : 0u;
   }
-  *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;    // K % 8 == 0 and Wd 16-byte aligned
+#pragma unroll
+  for (int i = 0; i < kExpandTiles; i += 2) {
+    const uint32_t pc = __popc(byte[i]) | (__popc(byte[i + 1]) << 16);
+    const uint32_t ex = wave_inclusive_scan(pc) - pc;
+    oa[i] += ex & 0xffffu;
+    oa[i + 1] += ex >> 16;
+  }
+  u32x2 v0[kExpandTiles], v1[kExpandTiles];
+#pragma unroll
+  for (int i = 0; i < kExpandTiles; ++i) {
+    if (byte[i] != 0u) {
+      __builtin_memcpy(&v0[i], values + oa[i], 8);
+      __builtin_memcpy(&v1[i], values + oa[i] + __popc(byte[i] & 0xfu), 8);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kExpandTiles; ++i) {
+    const int64_t t = t0 + i;
+    const int64_t n = (t / S) * 16 + fr;
+    const int64_t k0 = (t % S) * 32 + 8 * fg;
+    if (t >= tiles || n >= N || k0 >= K) continue;
+    u32x4 a = u32x4{0u, 0u, 0u, 0u};
+    if (byte[i] != 0u) {
+      const u32x2 slo = lut[byte[i] & 0xfu], shi = lut[byte[i] >> 4];
+      a.x = __builtin_amdgcn_perm(v0[i].y, v0[i].x, slo.x);
+      a.y = __builtin_amdgcn_perm(v0[i].y, v0[i].x, slo.y);
+      a.z = __builtin_amdgcn_perm(v1[i].y, v1[i].x, shi.x);
+      a.w = __builtin_amdgcn_perm(v1[i].y, v1[i].x, shi.y);
+    }
+    *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;  // K % 8 == 0 and Wd 16-byte aligned
+  }
 }
 
-// The same for an int8 tile-layout matrix with K % 16 == 0: two tiles per
-// wave (lanes 0-31 the first, 32-63 the second), lane (r, g) of a tile
-// (r = lane % 16, g = lane / 16 % 2) writes row r, columns 16 g .. 16 g + 15
-// with one 16-byte store.  A tile's int8 values are ordered by 16-column
-// group, then row (the order of its 32 lanes), so the lane's first value is
-// the tile offset + the exclusive scan over its half-wave of the lanes' kept
-// counts; the 8-byte windows from the first value of columns 0-7 and of
-// columns 8-15 of its group are expanded per nibble by a selector table
-// indexed by the nibble and the place of its first value in the window.  A
-// window reads at most 7 bytes past the last kept value: inside the 16
-// readable bytes that follow the payload.
+// The same for an int8 tile-layout matrix with K % 16 == 0: a wave expands
+// 2 kExpandTiles consecutive tiles, tile pair p being tiles 2p (lanes 0-31)
+// and 2p + 1 (lanes 32-63); lane (r, g) of a tile (r = lane % 16, g = lane /
+// 16 % 2) writes row r, columns 16 g .. 16 g + 15 with one 16-byte store.  A
+// tile's int8 values are ordered by 16-column group, then row (the order of
+// its 32 lanes), so the lane's first value is the tile offset + the exclusive
+// scan over its half-wave of the lanes' kept counts; the 8-byte windows from
+// the first value of columns 0-7 and of columns 8-15 of its group are
+// expanded per nibble by a selector table indexed by the nibble and the place
+// of its first value in the window.  A window reads at most 7 bytes past the
+// last kept value: inside the 16 readable bytes that follow the payload.
 __global__ void __launch_bounds__(256) k_expand_tiles8(const uint32_t* __restrict__ bm_tiles,
                                                        const uint8_t* __restrict__ values,
                                                        const int32_t* __restrict__ tile_offsets, int64_t N,
@@ -311,32 +333,49 @@ __global__ void __launch_bounds__(256) k_expand_tiles8(const uint32_t* __restric
   if (threadIdx.x < 80) lut[threadIdx.x] = nibble_selector8(threadIdx.x / 5, threadIdx.x % 5);
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 2;   // the wave's first tile
+  const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 2 * kExpandTiles;
   if (t0 >= tiles) return;                           // whole waves leave together
-  const int64_t t = t0 + (lane >> 5);
-  const bool live = t < tiles;
   const int r = lane & 15, gq = (lane >> 4) & 1;
-  const uint32_t hw = live ? (bm_tiles[t * 16 + r] >> (16 * gq)) & 0xffffu : 0u;   // pad rows, columns: 0
-  const uint32_t cnt = __popc(hw);
-  const uint32_t oa = (live ? (uint32_t)tile_offsets[t] : 0u) + half_inclusive_scan(cnt) - cnt;
-  if (!live) return;                                 // (after the scan: every lane took part)
   const int64_t S = tile_steps(K);
-  const int64_t n = (t / S) * 16 + r;
-  const int64_t k0 = (t % S) * 32 + 16 * gq;
-  if (n >= N || k0 >= K) return;
-  u32x4 a = u32x4{0u, 0u, 0u, 0u};
-  if (hw != 0u) {
-    const uint32_t q0 = hw & 15u, q1 = (hw >> 4) & 15u, q2 = (hw >> 8) & 15u, q3 = hw >> 12;
-    const uint32_t ob = oa + __popc(hw & 0xffu);    // columns 8-15 start after the kept ones of 0-7
-    u32x2 v0, v1;
-    __builtin_memcpy(&v0, values + oa, 8);
-    __builtin_memcpy(&v1, values + ob, 8);
-    a.x = __builtin_amdgcn_perm(v0.y, v0.x, lut[5 * q0]);
-    a.y = __builtin_amdgcn_perm(v0.y, v0.x, lut[5 * q1 + __popc(q0)]);
-    a.z = __builtin_amdgcn_perm(v1.y, v1.x, lut[5 * q2]);
-    a.w = __builtin_amdgcn_perm(v1.y, v1.x, lut[5 * q3 + __popc(q2)]);
+  uint32_t hw[kExpandTiles], oa[kExpandTiles];
+#pragma unroll
+  for (int p = 0; p < kExpandTiles; ++p) {
+    const int64_t t = t0 + 2 * p + (lane >> 5);
+    const bool live = t < tiles;
+    hw[p] = live ? (bm_tiles[t * 16 + r] >> (16 * gq)) & 0xffffu : 0u;   // pad rows, columns: 0
+    oa[p] = live ? (uint32_t)tile_offsets[t] : 0u;
   }
-  *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;    // K % 16 == 0 and Wd 16-byte aligned
+#pragma unroll
+  for (int p = 0; p < kExpandTiles; p += 2) {
+    const uint32_t pc = __popc(hw[p]) | (__popc(hw[p + 1]) << 16);
+    const uint32_t ex = half_inclusive_scan(pc) - pc;
+    oa[p] += ex & 0xffffu;
+    oa[p + 1] += ex >> 16;
+  }
+  u32x2 v0[kExpandTiles], v1[kExpandTiles];
+#pragma unroll
+  for (int p = 0; p < kExpandTiles; ++p) {
+    if (hw[p] != 0u) {
+      __builtin_memcpy(&v0[p], values + oa[p], 8);
+      __builtin_memcpy(&v1[p], values + oa[p] + __popc(hw[p] & 0xffu), 8);   // columns 8-15 after 0-7
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < kExpandTiles; ++p) {
+    const int64_t t = t0 + 2 * p + (lane >> 5);
+    const int64_t n = (t / S) * 16 + r;
+    const int64_t k0 = (t % S) * 32 + 16 * gq;
+    if (t >= tiles || n >= N || k0 >= K) continue;
+    u32x4 a = u32x4{0u, 0u, 0u, 0u};
+    if (hw[p] != 0u) {
+      const uint32_t q0 = hw[p] & 15u, q1 = (hw[p] >> 4) & 15u, q2 = (hw[p] >> 8) & 15u, q3 = hw[p] >> 12;
+      a.x = __builtin_amdgcn_perm(v0[p].y, v0[p].x, lut[5 * q0]);
+      a.y = __builtin_amdgcn_perm(v0[p].y, v0[p].x, lut[5 * q1 + __popc(q0)]);
+      a.z = __builtin_amdgcn_perm(v1[p].y, v1[p].x, lut[5 * q2]);
+      a.w = __builtin_amdgcn_perm(v1[p].y, v1[p].x, lut[5 * q3 + __popc(q2)]);
+    }
+    *reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;  // K % 16 == 0 and Wd 16-byte aligned
+  }
 }
 
 // Thread (tile t, row r): decode one tile row into the dense matrix.
@@ -579,13 +618,15 @@ hipError_t launch_unpack(const spl_matrix& Wc, void* W_dense, hipStream_t s) {
   if (Wc.layout == SPL_LAYOUT_TILE16) {
     const int64_t T = tile_blocks(Wc.rows) * tile_steps(Wc.cols);
     if (Wc.dtype != SPL_I8 && Wc.cols % 8 == 0) {   // W_dense is 16-byte aligned (checked by the caller)
-      hipLaunchKernelGGL(k_expand_tiles16, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, Wc.bitmask,
+      hipLaunchKernelGGL(k_expand_tiles16, dim3((unsigned)((T + 4 * kExpandTiles - 1) / (4 * kExpandTiles))),
+                         dim3(256), 0, s, Wc.bitmask,
                          static_cast<const uint16_t*>(Wc.values), Wc.tile_offsets, Wc.rows, Wc.cols, T,
                          static_cast<uint16_t*>(W_dense));
       return hipGetLastError();
     }
     if (Wc.dtype == SPL_I8 && Wc.cols % 16 == 0) {
-      hipLaunchKernelGGL(k_expand_tiles8, dim3((unsigned)((T + 7) / 8)), dim3(256), 0, s, Wc.bitmask,
+      hipLaunchKernelGGL(k_expand_tiles8, dim3((unsigned)((T + 8 * kExpandTiles - 1) / (8 * kExpandTiles))),
+                         dim3(256), 0, s, Wc.bitmask,
                          static_cast<const uint8_t*>(Wc.values), Wc.tile_offsets, Wc.rows, Wc.cols, T,
                          static_cast<uint8_t*>(W_dense));
       return hipGetLastError();

@@ -527,19 +527,26 @@ PACK_SRC = os.path.join(os.path.dirname(SRC), "k_pack.hip")
 
 def _expand_lines():
     src = open(PACK_SRC).read()
-    for line in ("const uint32_t byte = (bm_tiles[t * 16 + fr] >> (8 * fg)) & 0xffu;",
-                 "const uint32_t oa = (uint32_t)tile_offsets[t] + wave_inclusive_scan(cnt) - cnt;",
-                 "const uint32_t ob = oa + __popc(byte & 0xfu);",
+    for line in ("constexpr int kExpandTiles = 4;",
+                 "const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kExpandTiles;",
+                 "byte[i] = live ? (bm_tiles[(t0 + i) * 16 + fr] >> (8 * fg)) & 0xffu : 0u;",
+                 "const uint32_t pc = __popc(byte[i]) | (__popc(byte[i + 1]) << 16);",
+                 "const uint32_t ex = wave_inclusive_scan(pc) - pc;",
+                 "__builtin_memcpy(&v1[i], values + oa[i] + __popc(byte[i] & 0xfu), 8);",
+                 "const int64_t k0 = (t % S) * 32 + 8 * fg;",
                  "*reinterpret_cast<u32x4*>(Wd + n * K + k0) = a;",
-                 "const int64_t t = t0 + (lane >> 5);",
-                 "const uint32_t hw = live ? (bm_tiles[t * 16 + r] >> (16 * gq)) & 0xffffu : 0u;",
-                 "const uint32_t oa = (live ? (uint32_t)tile_offsets[t] : 0u) + half_inclusive_scan(cnt) - cnt;",
+                 "const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 2 * kExpandTiles;",
+                 "const int64_t t = t0 + 2 * p + (lane >> 5);",
+                 "hw[p] = live ? (bm_tiles[t * 16 + r] >> (16 * gq)) & 0xffffu : 0u;",
+                 "const uint32_t ex = half_inclusive_scan(pc) - pc;",
                  "const int64_t k0 = (t % S) * 32 + 16 * gq;",
-                 "const uint32_t ob = oa + __popc(hw & 0xffu);",
-                 "a.y = __builtin_amdgcn_perm(v0.y, v0.x, lut[5 * q1 + __popc(q0)]);",
-                 "a.w = __builtin_amdgcn_perm(v1.y, v1.x, lut[5 * q3 + __popc(q2)]);",
+                 "__builtin_memcpy(&v1[p], values + oa[p] + __popc(hw[p] & 0xffu), 8);",
+                 "a.y = __builtin_amdgcn_perm(v0[p].y, v0[p].x, lut[5 * q1 + __popc(q0)]);",
+                 "a.w = __builtin_amdgcn_perm(v1[p].y, v1[p].x, lut[5 * q3 + __popc(q2)]);",
                  "if (Wc.dtype == SPL_I8 && Wc.cols % 16 == 0) {"):
         assert line in src, f"expansion changed: update this replay ({line})"
+    # every tile is one wave's (16-bit) or half-wave's (int8) unit; the scans of a wave's tiles,
+    # two per scan in 16-bit halves, are each tile's own (sums <= 512)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "i8"])
