@@ -244,8 +244,11 @@ spl_status spl_sparse_linear_expanded(const void* X, int64_t M, const spl_matrix
  *   SPL_ERR_UNSUPPORTED), K % 8 == 0, M <= 4194240.  workspace: device
  *   scratch of spl_sparse_weight_grad_workspace_bytes(M, N, K) bytes
  *   (2 M (N + K) rounded up: the transposes of dY and X; no [N][K] buffer),
- *   256-byte aligned, caller-owned.  The product's epilogue writes the kept
- *   entries directly; nothing else of grad_values is touched.
+ *   256-byte aligned, caller-owned; left untouched where the product reads
+ *   dY and X as they are stored (N % 256 == 0, K % 128 == 0, M % 64 == 0,
+ *   16-byte aligned dY and X, and at least one 128 x 256 output block per
+ *   compute unit).  The product's epilogue writes the kept entries directly;
+ *   nothing else of grad_values is touched.
  * spl_sparse_sgd_update: Wc->values[i] = RNE(v - lr * g) with v, g decoded
  *   from the payloads and each operation rounded to binary32; in place.
  * The input gradient dX = dY (W.Mask) is spl_sparse_linear(dY, Wt) with Wt the

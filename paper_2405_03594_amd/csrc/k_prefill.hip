@@ -748,6 +748,149 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma(const PfArgs g
     pf_store<T, FN, FM>(acc, g.Y, M, N, n0, m0, wn, wm, fr, fg);
 }
 
+// Contraction-major factors (the weight gradient dY^T X, both factors stored
+// with the token as the row): the same 128 x 256 blocks and eight waves, the
+// operands again moved straight from global memory into three rotating LDS
+// stage buffers, now as kPfBK contraction rows of the block's 128 W columns
+// (256-byte rows) and 256 X columns (512-byte rows), so that no transposed
+// copy of either factor is written first.  The fragments are read with
+// ds_read_b64_tr_b16: within each 16-lane quarter of the wave, lane s reads 8
+// bytes at its own address and lane t receives, as its element e, element
+// t % 4 of the 8 bytes of lane 4 e + t / 4.  Lane s points at contraction row
+// k0 + s / 4, columns c0 + 4 (s % 4) .. + 3, so lane t receives column c0 + t
+// at rows k0 .. k0 + 3: the MFMA operand layout (fragment row lane % 16,
+// contraction index 8 (lane / 16) + j), in two reads per 16 x 32 fragment.
+// Swizzle: the 16-byte chunk c of staged row r sits at chunk c ^ 2 h(r),
+// h(r) = r % 4 + 4 ((r / 8) % 2).  A read of half a wave covers rows
+// r0 .. r0 + 3 and r0 + 8 .. r0 + 11 (r0 % 16 = 0 or 4), 32 bytes each, and
+// h places those 8 pieces in 8 distinct 32-byte bank groups; h is the same
+// for rows 4 and 32 apart, so a fragment's four reads share one address
+// register and differ in the instruction's offset.
+constexpr int kTrRowA = 2 * kDmaBN, kTrRowB = 2 * kDmaBM;      // bytes per staged contraction row: W, X
+constexpr int kTrOffB = kPfBK * kTrRowA;                        // X part of a stage buffer
+
+// The same 16-byte direct-to-LDS request as lds_dma16, issued from inline
+// assembly: the compiler then does not count it, and so does not wait for
+// every outstanding request before each ds_read_b64_tr_b16 (which it cannot
+// tell apart from reads of the buffer being filled).  dma_barrier's explicit
+// wait is what orders the requests before the reads.  M0 (the request's LDS
+// base) is declared clobbered; the kernel that uses this issues no other
+// instruction that reads M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16_opaque(const uint16_t* src, unsigned char* dst) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_off(dst))
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ u32x2 lds_load_tr8(uint32_t addr) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(uintptr_t)addr);
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// One stage of MFMA work from contraction-major buffers: ao / bo are the
+// lane's byte offsets of its A and B fragments' first read in a stage buffer.
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_mfma_stage_tr(typename MfmaP<T>::acc_t (&acc)[FN][FM], uint32_t buf,
+                                                 const uint32_t (&ao)[FN], const uint32_t (&bo)[FM]) {
+  u32x4 a[2][FN], b[2][FM];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+      const uint32_t p = buf + ao[i] + 32 * kTrRowA * ks;
+      const u32x2 lo = lds_load_tr8(p), hi = lds_load_tr8(p + 4 * kTrRowA);
+      a[ks][i] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const uint32_t p = buf + bo[j] + 32 * kTrRowB * ks;
+      const u32x2 lo = lds_load_tr8(p), hi = lds_load_tr8(p + 4 * kTrRowB);
+      b[ks][j] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+  }
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int j = 0; j < FM; ++j) acc[i][j] = MfmaP<T>::run(a[ks][i], b[ks][j], acc[i][j]);
+  // masks: 0x100 LDS read, 0x008 MFMA; two reads per fragment
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * (FN + FM), 0);
+#pragma unroll
+  for (int q = 0; q < FN + FM; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2 * FN * FM - (FN + FM), 0);
+}
+
+// Y = Xc^T Wc for Xc [K][M] and Wc [K][N] (g.X, g.W), kept entries only
+// (pf_store_gather); M % 256 == 0, N % 128 == 0, K % kPfBK == 0.
+template <class T, int NW>
+__global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const PfArgs g) {
+  static_assert(!std::is_same<T, I8P>::value && NW == 8, "16-bit payloads, eight waves");
+  using Acc = typename MfmaP<T>::acc_t;
+  constexpr int FN = 4, FM = kDmaBM / (8 * NW);
+  constexpr int RA = kPfBK * kTrRowA / 1024 / NW, RB = kPfBK * kTrRowB / 1024 / NW;   // 1 KB runs per wave: 2, 4
+  constexpr int kLoads = RA + RB;
+  extern __shared__ __align__(16) unsigned char dsm[];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int64_t M = g.M, N = g.N, K = g.K;
+  const int nst = (int)(K / kPfBK);
+  const int64_t n0 = (int64_t)blockIdx.x * kDmaBN, m0 = (int64_t)blockIdx.y * kDmaBM;
+  // wave w requests rows 8 w .. 8 w + 7 of each operand's stage (bit 3 of the row: w % 2).
+  // W run u: rows 8 w + 4 u + lane / 16, the lane's slot lane % 16 of the row;
+  // X run u: rows 8 w + 2 u + lane / 32, slot lane % 32 (h depends on u % 2).
+  const int hw = (wave & 1) << 2;
+  const uint16_t* wsrc = g.W + (int64_t)(8 * wave + (lane >> 4)) * N + n0 + 8 * ((lane & 15) ^ (2 * ((lane >> 4) | hw)));
+  const uint16_t* xsrc[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+    xsrc[p] = g.X + (int64_t)(8 * wave + 2 * p + (lane >> 5)) * M + m0 + 8 * ((lane & 31) ^ (2 * ((2 * p + (lane >> 5)) | hw)));
+  auto request = [&](int st, int buf) {
+    unsigned char* a = dsm + buf * kDmaStageBytes;
+    const int64_t k0 = (int64_t)kPfBK * st;
+#pragma unroll
+    for (int u = 0; u < RA; ++u) lds_dma16_opaque(wsrc + (k0 + 4 * u) * N, a + (RA * wave + u) * 1024);
+#pragma unroll
+    for (int u = 0; u < RB; ++u)
+      lds_dma16_opaque(xsrc[u & 1] + (k0 + 4 * (u >> 1)) * M, a + kTrOffB + (RB * wave + u) * 1024);
+  };
+  // my fragments' first reads: row r0 = 8 (lane / 16) + t / 4 (t = lane % 16), columns 16 i + 4 (t % 4) of the wave's
+  const int t = lane & 15, r0 = 8 * (lane >> 4) + (t >> 2);
+  const int h = (t >> 2) | (((lane >> 4) & 1) << 2);
+  uint32_t ao[FN], bo[FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+    ao[i] = (uint32_t)(r0 * kTrRowA + 16 * ((8 * wn + 2 * i + ((t & 3) >> 1)) ^ (2 * h)) + 8 * (t & 1));
+#pragma unroll
+  for (int j = 0; j < FM; ++j)
+    bo[j] = (uint32_t)(kTrOffB + r0 * kTrRowB + 16 * ((8 * wm + 2 * j + ((t & 3) >> 1)) ^ (2 * h)) + 8 * (t & 1));
+
+  Acc acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
+
+  request(0, 0);
+  if (nst > 1) request(1, 1);
+  int cur = 0;
+  for (int st = 0; st < nst; ++st) {
+    if (st + 1 < nst) dma_barrier<kLoads>();
+    else dma_barrier<0>();
+    if (st + 2 < nst) request(st + 2, cur == 0 ? 2 : cur - 1);
+    pf_mfma_stage_tr<T, FN, FM>(acc, lds_off(dsm + cur * kDmaStageBytes), ao, bo);
+    cur = cur == kDmaStages - 1 ? 0 : cur + 1;
+  }
+  pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);
+}
+
 int pf_cus() { return device_cus(); }
 
 // Workgroup tile of a launch: 128 x 256 (8 waves) when that still gives every
@@ -837,6 +980,18 @@ hipError_t dense_prefill_dma(const PfArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <class T>
+hipError_t dense_prefill_tr(const PfArgs& a, hipStream_t s) {
+  constexpr int NW = kDmaWaves;
+  auto* kernel = k_dense_prefill_dma_tr<T, NW>;
+  static PerDeviceFlag lds_set;
+  const hipError_t attr = allow_lds_once(lds_set, kernel, kDmaStages * kDmaStageBytes);
+  if (attr != hipSuccess) return attr;
+  const dim3 grid((unsigned)(a.N / kDmaBN), (unsigned)(a.M / kDmaBM)), block(64 * NW);
+  hipLaunchKernelGGL(kernel, grid, block, kDmaStages * kDmaStageBytes, s, a);
+  return hipGetLastError();
+}
+
 template <class T, bool kGather = false>
 hipError_t dense_prefill_t(const PfArgs& a, hipStream_t s) {
   if (pf_large_tile(a.N, a.M) && pf_inside(a.N, a.M, pf_units<T>(a.K), kDmaBN, kDmaBM))
@@ -881,6 +1036,25 @@ hipError_t launch_dense_prefill_gather(const void* X, int64_t M, const void* W, 
   a.M = M, a.N = N, a.K = K;
   a.gbm = P.bitmask, a.gtoff = P.tile_offsets, a.gval = static_cast<uint16_t*>(values);
   return dtype == SPL_BF16 ? dense_prefill_t<Bf16, true>(a, s) : dense_prefill_t<F16, true>(a, s);
+}
+
+// The kept entries of Xc^T Wc (Xc [K][M], Wc [K][N]) at the tile pattern P
+// ([M][N]), in P's value order, read from the contraction-major factors
+// directly.
+bool dense_prefill_tr_applies(int64_t M, int64_t N, int64_t K, const void* Xc, const void* Wc) {
+  return pf_large_tile(N, M) && pf_inside(N, M, K, kDmaBN, kDmaBM) &&
+         (((uintptr_t)Xc | (uintptr_t)Wc) & 15) == 0;
+}
+
+hipError_t launch_dense_prefill_gather_tr(const void* Xc, int64_t M, const void* Wc, int32_t dtype, int64_t N,
+                                          int64_t K, const spl_matrix& P, void* values, hipStream_t s) {
+  if (P.rows != M || P.cols != N || !dense_prefill_tr_applies(M, N, K, Xc, Wc)) return hipErrorInvalidValue;
+  PfArgs a{};
+  a.X = static_cast<const uint16_t*>(Xc);
+  a.W = static_cast<const uint16_t*>(Wc);
+  a.M = M, a.N = N, a.K = K;
+  a.gbm = P.bitmask, a.gtoff = P.tile_offsets, a.gval = static_cast<uint16_t*>(values);
+  return dtype == SPL_BF16 ? dense_prefill_tr<Bf16>(a, s) : dense_prefill_tr<F16>(a, s);
 }
 
 // Gated half of a Llama MLP: Y = silu(X Wg^T) * (X Wu^T) (same dtype and shape).

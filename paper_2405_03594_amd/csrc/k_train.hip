@@ -178,6 +178,9 @@ int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K) {
 hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
                               void* ws, hipStream_t s) {
   const int64_t N = Wc.rows, K = Wc.cols;
+  // dY [M][N] and X [M][K] are the contraction-major factors of dY^T X
+  if (dense_prefill_tr_applies(N, K, M, dY, X))
+    return launch_dense_prefill_gather_tr(dY, N, X, Wc.dtype, K, M, Wc, grad_values, s);
   unsigned char* base = static_cast<unsigned char*>(ws);
   void* dYt = base;                                  // [N][M]
   void* Xt = base + align256(2 * N * M);             // [K][M]

@@ -210,6 +210,12 @@ hipError_t launch_dense_prefill(const void* X, int64_t M, const void* W, int32_t
 // (P.rows == M, P.cols == N), in P's value order (fp16/bf16).
 hipError_t launch_dense_prefill_gather(const void* X, int64_t M, const void* W, int32_t dtype, int64_t N, int64_t K,
                                        const spl_matrix& P, void* values, hipStream_t s);
+// The same from contraction-major factors, Y = Xc^T Wc (Xc [K][M], Wc [K][N]),
+// where dense_prefill_tr_applies (M % 256, N % 128 and K % 64 all zero, a
+// launch of at least one 128 x 256 block per CU, 16-byte aligned factors).
+bool dense_prefill_tr_applies(int64_t M, int64_t N, int64_t K, const void* Xc, const void* Wc);
+hipError_t launch_dense_prefill_gather_tr(const void* Xc, int64_t M, const void* Wc, int32_t dtype, int64_t N,
+                                          int64_t K, const spl_matrix& P, void* values, hipStream_t s);
 // Sparse-quantized kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
 hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s);
 hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s);

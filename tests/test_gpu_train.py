@@ -74,6 +74,27 @@ def test_weight_grad(orc, spl, dtype, N, K, M, s):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,M,s", [(1024, 8192, 64, 0.7), (1024, 8192, 192, 0.5), (2048, 4096, 128, 0.9),
+                                     (2048, 4096, 320, 0.7)])
+def test_weight_grad_contraction_major(orc, spl, dtype, N, K, M, s):
+    """Shapes whose weight gradient is read straight from dY and X (the
+    token as the row of both; no transposed copies): N % 256, K % 128 and
+    M % 64 zero and one 128 x 256 block per CU, over one, two, three and five
+    64-token stages (the three stage buffers used once, and rotated), every
+    kept entry compared with the oracle."""
+    import torch
+
+    W, mask = synth.weight(620 + N, N, K, dtype, s)
+    X = synth.activations(621 + M, M, K, dtype)
+    dY = synth.activations(622 + M, M, N, dtype)
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    g = spl.sparse_weight_grad(to_dev(dY, dtype), to_dev(X, dtype), Wc)
+    G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
+    ref = orc.weight_grad_f64(dY, X, dtype, orc.pack(W, dtype, mask))
+    assert_close(G, ref, f"weight grad {dtype} N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_sgd_update(orc, spl, dtype):
     import torch
 

@@ -609,3 +609,127 @@ def test_expand_tiles_rebuild_the_dense_matrix(orc, dtype, N, K, s):
             assert k0 * eb + 16 <= K * eb
             got[n, k0 * eb:k0 * eb + 16] = piece
     assert np.array_equal(got, dense)
+
+
+# ---------------------------------------------------------------- contraction-major factors (the weight gradient)
+
+TRAIN_SRC = os.path.join(os.path.dirname(SRC), "k_train.hip")
+
+
+def _tr_lines():
+    src = open(SRC).read()
+    for line in ("constexpr int kTrRowA = 2 * kDmaBN, kTrRowB = 2 * kDmaBM;",
+                 "constexpr int kTrOffB = kPfBK * kTrRowA;",
+                 "constexpr int RA = kPfBK * kTrRowA / 1024 / NW, RB = kPfBK * kTrRowB / 1024 / NW;",
+                 "const int hw = (wave & 1) << 2;",
+                 "const uint16_t* wsrc = g.W + (int64_t)(8 * wave + (lane >> 4)) * N + n0 + 8 * ((lane & 15) ^ "
+                 "(2 * ((lane >> 4) | hw)));",
+                 "xsrc[p] = g.X + (int64_t)(8 * wave + 2 * p + (lane >> 5)) * M + m0 + 8 * ((lane & 31) ^ "
+                 "(2 * ((2 * p + (lane >> 5)) | hw)));",
+                 "for (int u = 0; u < RA; ++u) lds_dma16_opaque(wsrc + (k0 + 4 * u) * N, a + (RA * wave + u) * 1024);",
+                 "lds_dma16_opaque(xsrc[u & 1] + (k0 + 4 * (u >> 1)) * M, a + kTrOffB + (RB * wave + u) * 1024);",
+                 "const int t = lane & 15, r0 = 8 * (lane >> 4) + (t >> 2);",
+                 "const int h = (t >> 2) | (((lane >> 4) & 1) << 2);",
+                 "ao[i] = (uint32_t)(r0 * kTrRowA + 16 * ((8 * wn + 2 * i + ((t & 3) >> 1)) ^ (2 * h)) + 8 * (t & 1));",
+                 "bo[j] = (uint32_t)(kTrOffB + r0 * kTrRowB + 16 * ((8 * wm + 2 * j + ((t & 3) >> 1)) ^ (2 * h)) + "
+                 "8 * (t & 1));",
+                 "const uint32_t p = buf + ao[i] + 32 * kTrRowA * ks;",
+                 "const u32x2 lo = lds_load_tr8(p), hi = lds_load_tr8(p + 4 * kTrRowA);",
+                 "const uint32_t p = buf + bo[j] + 32 * kTrRowB * ks;",
+                 "const u32x2 lo = lds_load_tr8(p), hi = lds_load_tr8(p + 4 * kTrRowB);",
+                 "a[ks][i] = u32x4{lo.x, lo.y, hi.x, hi.y};",
+                 "if (st + 2 < nst) request(st + 2, cur == 0 ? 2 : cur - 1);",
+                 "return pf_large_tile(N, M) && pf_inside(N, M, K, kDmaBN, kDmaBM) &&"):
+        assert line in src, f"contraction-major core changed: update this replay ({line})"
+    train = open(TRAIN_SRC).read()
+    for line in ("if (dense_prefill_tr_applies(N, K, M, dY, X))",
+                 "return launch_dense_prefill_gather_tr(dY, N, X, Wc.dtype, K, M, Wc, grad_values, s);"):
+        assert line in train, f"weight gradient launch changed: update this replay ({line})"
+    # (BN, BM, NW, FN, FM)
+    return 128, 256, 8, 4, 4
+
+
+def _tr_read(addrs, lane):
+    """ds_read_b64_tr_b16 (CDNA4 LDS transpose load, 16-bit elements): in each
+    16-lane quarter, lane t receives as element e the (t % 4)-th 16-bit
+    element of the 8 bytes addressed by lane 4 e + t / 4 of its quarter.
+    Returns the 4 byte addresses lane `lane` receives."""
+    q, t = lane >> 4, lane & 15
+    return [addrs[16 * q + 4 * e + (t >> 2)] + 2 * (t & 3) for e in range(4)]
+
+
+@pytest.mark.parametrize("M,N,K", [(4096, 4096, 2048), (11008, 4096, 2048), (4096, 11008, 2048), (256, 128, 64),
+                                   (1024, 8192, 192)])
+def test_contraction_major_stage_and_transposed_reads(M, N, K):
+    """The weight gradient's core (Y = Xc^T Wc from Xc [K][M] = dY and
+    Wc [K][N] = X, the token as the row of both): one stage of a corner
+    workgroup, replayed.  The direct-to-LDS requests fill every (contraction
+    row, 16-byte chunk) of the stage exactly once, from inside the matrices,
+    at the swizzled place (chunk c of row r at chunk c ^ 2 h(r),
+    h(r) = r % 4 + 4 ((r / 8) % 2)); through the instruction's lane mapping,
+    each lane's two transpose reads per fragment and k-step return exactly
+    its MFMA operand (fragment row lane % 16, contraction rows
+    8 (lane / 16) + 0..7); and each read is free of bank conflicts (64 banks
+    of 4 bytes over half a wave, 32 over a quarter)."""
+    BN, BM, NW, FN, FM = _tr_lines()
+    bk, _ = _constants()
+    rowA, rowB = 2 * BN, 2 * BM
+    offB = bk * rowA
+    RA, RB = bk * rowA // 1024 // NW, bk * rowB // 1024 // NW
+    assert (RA, RB) == (2, 4) and offB + bk * rowB == (BN + BM) * 2 * bk
+    assert M % BM == 0 and N % BN == 0 and K % bk == 0
+
+    def h(r):
+        return (r & 3) | (((r >> 3) & 1) << 2)
+
+    for n0, m0 in ((0, 0), (N - BN, M - BM)):
+        for st in sorted({0, K // bk - 1}):
+            k0 = bk * st
+            lds = {}                                   # byte -> (operand, contraction row, column)
+            for wave in range(NW):
+                hw = (wave & 1) << 2
+                for lane in range(64):
+                    for u in range(RA):
+                        row = 8 * wave + (lane >> 4) + 4 * u          # stage row
+                        col = n0 + 8 * ((lane & 15) ^ (2 * ((lane >> 4) | hw)))
+                        slot = (RA * wave + u) * 1024 + 16 * lane
+                        assert k0 + row < K and n0 <= col and col + 8 <= min(N, n0 + BN)
+                        assert slot == row * rowA + 16 * (((col - n0) // 8) ^ (2 * h(row)))
+                        for e in range(8):
+                            assert slot + 2 * e not in lds
+                            lds[slot + 2 * e] = ("W", k0 + row, col + e)
+                    for u in range(RB):
+                        p = u & 1
+                        row = 8 * wave + 2 * p + (lane >> 5) + 4 * (u >> 1)
+                        col = m0 + 8 * ((lane & 31) ^ (2 * ((2 * p + (lane >> 5)) | hw)))
+                        slot = offB + (RB * wave + u) * 1024 + 16 * lane
+                        assert k0 + row < K and m0 <= col and col + 8 <= min(M, m0 + BM)
+                        assert slot == offB + row * rowB + 16 * (((col - m0) // 8) ^ (2 * h(row)))
+                        for e in range(8):
+                            assert slot + 2 * e not in lds
+                            lds[slot + 2 * e] = ("X", k0 + row, col + e)
+            assert len(lds) == (BN + BM) * bk
+            for wave in range(NW):
+                wn, wm = wave & 1, wave >> 1
+                for op, frags, rowb, base, first, c0 in (("W", FN, rowA, 0, n0, 64 * wn),
+                                                        ("X", FM, rowB, offB, m0, 64 * wm)):
+                    for f in range(frags):
+                        off = []
+                        for lane in range(64):
+                            t, r0 = lane & 15, 8 * (lane >> 4) + ((lane & 15) >> 2)
+                            hh = (t >> 2) | (((lane >> 4) & 1) << 2)
+                            assert hh == h(r0)
+                            off.append(base + r0 * rowb + 16 * (((c0 // 8) + 2 * f + ((t & 3) >> 1)) ^ (2 * hh))
+                                       + 8 * (t & 1))
+                        for ks in range(2):
+                            for half in range(2):
+                                addrs = [o + 32 * rowb * ks + 4 * rowb * half for o in off]
+                                for part, nb in ((32, 64), (16, 32)):
+                                    for l0 in range(0, 64, part):
+                                        banks = {(a // 4 + d) % nb for a in addrs[l0:l0 + part] for d in (0, 1)}
+                                        assert len(banks) == 2 * part, (op, f, ks, half, part, l0)
+                                for lane in range(64):
+                                    got = [lds[b] for b in _tr_read(addrs, lane)]
+                                    want = [(op, k0 + 32 * ks + 8 * (lane >> 4) + 4 * half + e,
+                                             first + c0 + 16 * f + (lane & 15)) for e in range(4)]
+                                    assert got == want, (op, wave, f, ks, half, lane)
