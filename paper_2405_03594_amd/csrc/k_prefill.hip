@@ -317,28 +317,52 @@ struct PfArgs {
 // and group.  The per-group counts of the 16 rows are scanned in one 16-lane
 // DPP scan (four 8-bit fields; a field sums at most 16 x 8 = 128).  Values
 // are rounded once to the payload type.
-template <class T, int FN, int FM>
-__device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], const PfArgs& g, int64_t n0, int64_t m0,
-                                                int wn, int wm, int lane) {
+// A wave's part of the pattern: its row's bitmask word of each of its
+// FM x FN/2 tiles (zero past the pattern), and the tiles' offsets, tile i's in
+// lane i (vector loads: a scalar load here would be waited for at once),
+// loaded apart from the epilogue so that a kernel can issue the loads early.
+template <int FN, int FM>
+struct GatherMeta {
+  uint32_t w[FM][FN / 2];
+  uint32_t off;
+};
+
+template <int FN, int FM>
+__device__ __forceinline__ void pf_gather_meta(GatherMeta<FN, FM>& gm, const PfArgs& g, int64_t n0, int64_t m0, int wn,
+                                               int wm, int lane) {
+  static_assert(FM * FN / 2 <= 64, "one tile offset per lane");
   const int64_t B = tile_blocks(g.M);
   const int64_t S = tile_steps(g.N);
-  const int fr = lane & 15, q = lane >> 4;
+  const int fr = lane & 15;
+  const int64_t b0 = (m0 + wm * 16 * FM) / 16, s0 = (n0 + wn * 16 * FN) / 32;
 #pragma unroll
   for (int j = 0; j < FM; ++j) {
-    const int64_t b = (m0 + wm * 16 * FM) / 16 + j;
-    if (b >= B) break;                                         // wave-uniform; later j lie further out
 #pragma unroll
     for (int p = 0; p < FN / 2; ++p) {
-      const int64_t st = (n0 + wn * 16 * FN) / 32 + p;
-      if (st >= S) break;
-      const int64_t t = b * S + st;
-      const uint32_t w = g.gbm[t * 16 + fr];                   // my row's word
+      const bool ok = b0 + j < B && s0 + p < S;                // wave-uniform
+      gm.w[j][p] = ok ? g.gbm[((b0 + j) * S + s0 + p) * 16 + fr] : 0u;   // my row's word
+    }
+  }
+  const int jl = lane / (FN / 2), pl = lane % (FN / 2);        // lane i: tile i = (j, p) = (i / (FN/2), i % (FN/2))
+  const bool okl = lane < FM * FN / 2 && b0 + jl < B && s0 + pl < S;
+  gm.off = okl ? (uint32_t)g.gtoff[(b0 + jl) * S + s0 + pl] : 0u;
+}
+
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], const GatherMeta<FN, FM>& gm,
+                                                const PfArgs& g, int lane) {
+  const int q = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < FM; ++j) {
+#pragma unroll
+    for (int p = 0; p < FN / 2; ++p) {
+      const uint32_t w = gm.w[j][p];
       const uint32_t c = __popc(w & 0xffu) | (__popc((w >> 8) & 0xffu) << 8) | (__popc((w >> 16) & 0xffu) << 16) |
                          (__popc(w >> 24) << 24);
       const uint32_t incl = row16_inclusive_scan(c);
       const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 15);   // every 16-lane row: the same tile
       const uint32_t above = incl - c;                         // per group: rows above mine
-      const uint32_t base = (uint32_t)g.gtoff[t];
+      const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)gm.off, j * (FN / 2) + p);
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int col = 16 * h + 4 * q;                        // my first tile column in this fragment
@@ -355,6 +379,14 @@ __device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], cons
       }
     }
   }
+}
+
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], const PfArgs& g, int64_t n0, int64_t m0,
+                                                int wn, int wm, int lane) {
+  GatherMeta<FN, FM> gm;
+  pf_gather_meta<FN, FM>(gm, g, n0, m0, wn, wm, lane);
+  pf_store_gather<T, FN, FM>(acc, gm, g, lane);
 }
 
 // kGated: the workgroup's BN virtual rows are BN/32 row blocks of the gate and
@@ -878,6 +910,10 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const PfArg
 #pragma unroll
     for (int j = 0; j < FM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
 
+  // the epilogue's pattern loads go first: the stage waits complete them, so the
+  // epilogue does not wait for their latency after the last MFMAs
+  GatherMeta<FN, FM> gm;
+  pf_gather_meta<FN, FM>(gm, g, n0, m0, wn, wm, lane);
   request(0, 0);
   if (nst > 1) request(1, 1);
   int cur = 0;
@@ -888,7 +924,7 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const PfArg
     pf_mfma_stage_tr<T, FN, FM>(acc, lds_off(dsm + cur * kDmaStageBytes), ao, bo);
     cur = cur == kDmaStages - 1 ? 0 : cur + 1;
   }
-  pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);
+  pf_store_gather<T, FN, FM>(acc, gm, g, lane);
 }
 
 int pf_cus() { return device_cus(); }

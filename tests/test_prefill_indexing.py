@@ -374,15 +374,20 @@ def test_gated_block_assignment(N, BN, NW):
 
 def _gather_lines():
     src = open(SRC).read()
-    for line in ("const int64_t b = (m0 + wm * 16 * FM) / 16 + j;",
+    for line in ("const int64_t b0 = (m0 + wm * 16 * FM) / 16, s0 = (n0 + wn * 16 * FN) / 32;",
                  "constexpr int FM = BM / (8 * NW);",
                  "constexpr int FN = 4, FM = kDmaBM / (8 * NW);",
                  "constexpr int kDmaBN = 128, kDmaBM = 256, kDmaStages = 3, kDmaWaves = 8;",
                  "pf_store_gather<T, FN, FM>(acc, g, n0, m0, wn, wm, lane);",
-                 "if (b >= B) break;",
-                 "const int64_t st = (n0 + wn * 16 * FN) / 32 + p;",
-                 "if (st >= S) break;",
-                 "const uint32_t w = g.gbm[t * 16 + fr];",
+                 "pf_gather_meta<FN, FM>(gm, g, n0, m0, wn, wm, lane);",
+                 "pf_store_gather<T, FN, FM>(acc, gm, g, lane);",
+                 "const bool ok = b0 + j < B && s0 + p < S;",
+                 "gm.w[j][p] = ok ? g.gbm[((b0 + j) * S + s0 + p) * 16 + fr] : 0u;",
+                 "const int jl = lane / (FN / 2), pl = lane % (FN / 2);",
+                 "const bool okl = lane < FM * FN / 2 && b0 + jl < B && s0 + pl < S;",
+                 "gm.off = okl ? (uint32_t)g.gtoff[(b0 + jl) * S + s0 + pl] : 0u;",
+                 "const uint32_t w = gm.w[j][p];",
+                 "const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)gm.off, j * (FN / 2) + p);",
                  "const uint32_t incl = row16_inclusive_scan(c);",
                  "const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 15);",
                  "const uint32_t above = incl - c;",
@@ -424,16 +429,22 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
                 n0, m0 = gx * BN, gy * BM
                 for wave in range(NW):
                     wn, wm = wave & 1, wave >> 1
+                    b0, s0 = (m0 + wm * 16 * FM) // 16, (n0 + wn * 16 * FN) // 32
+                    # the pattern loads: words per tile (zero past the pattern), tile i's offset in lane i
+                    off = []
+                    for lane in range(64):
+                        jl, pl = lane // (FN // 2), lane % (FN // 2)
+                        okl = lane < FM * FN // 2 and b0 + jl < B and s0 + pl < S
+                        off.append(int(offs[(b0 + jl) * S + s0 + pl]) if okl else 0)
                     for j in range(FM):
-                        b = (m0 + wm * 16 * FM) // 16 + j
-                        if b >= B:
-                            break
                         for p in range(FN // 2):
-                            st = (n0 + wn * 16 * FN) // 32 + p
-                            if st >= S:
-                                break
+                            b, st = b0 + j, s0 + p
+                            ok = b < B and st < S
                             t = b * S + st
-                            words = [int(bm[t * 16 + fr]) for fr in range(16)]
+                            words = [int(bm[t * 16 + fr]) if ok else 0 for fr in range(16)]
+                            assert j * (FN // 2) + p < 64
+                            base = off[j * (FN // 2) + p]
+                            assert not ok or base == int(offs[t])
                             c = [sum(_popc((w >> (8 * f)) & 0xFF) << (8 * f) for f in range(4)) for w in words]
                             incl = np.cumsum(c)
                             assert all(((int(x) >> (8 * f)) & 0xFF) <= 128 for x in incl for f in range(4))
@@ -445,7 +456,7 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
                                 for h in range(2):
                                     col = 16 * h + 4 * q
                                     f = col >> 3
-                                    idx = int(offs[t]) + ((above >> (8 * f)) & 0xFF)
+                                    idx = base + ((above >> (8 * f)) & 0xFF)
                                     idx += sum((tot >> (8 * g)) & 0xFF for g in range(f))
                                     if col & 4:
                                         idx += _popc((w >> (8 * f)) & 0xF)
