@@ -251,9 +251,22 @@ spl_status spl_sparse_linear_expanded(const void* X, int64_t M, const spl_matrix
  *   nothing else of grad_values is touched.
  * spl_sparse_sgd_update: Wc->values[i] = RNE(v - lr * g) with v, g decoded
  *   from the payloads and each operation rounded to binary32; in place.
- * The input gradient dX = dY (W.Mask) is spl_sparse_linear(dY, Wt) with Wt the
- * packed transpose: spl_unpack, spl_transpose16, then pack (the same kept
- * products; kept zeros may be dropped).
+ * spl_sparse_input_grad: dX [M][K] = dY [M][N] (W.Mask), the gradient with
+ *   respect to the activations, fp32 sums over n, one rounding to the payload
+ *   type; dY and dX of Wc->dtype, row-major, 16-byte aligned; Wc in the tile
+ *   layout (W itself, not its transpose).  Where M % 256 == 0, N % 64 == 0,
+ *   K % 128 == 0 and the launch has at least one 128 x 256 output block per
+ *   compute unit of the current device, W's tiles are expanded inside the
+ *   product and the workspace is not used
+ *   (spl_sparse_input_grad_workspace_bytes returns 0; NULL is accepted);
+ *   otherwise W is decoded and transposed into the workspace (4 N K bytes
+ *   rounded up, 256-byte aligned, caller-owned; N % 8 == 0 or
+ *   SPL_ERR_UNSUPPORTED) and multiplied densely.  M == 0: nothing to do;
+ *   nnz == 0: dX = 0.  The workspace-size function returns -1 for a view
+ *   spl_check_matrix rejects or an M outside the dimension limits.
+ * Alternatively dX is spl_sparse_linear(dY, Wt) with Wt the packed transpose
+ * (spl_unpack, spl_transpose16, then pack; the same kept products, kept zeros
+ * may be dropped), kept in step by the permutation below.
  * spl_transpose16: dst [C][R] = src [R][C]^T for 16-bit payloads (R <= 4194240).
  * spl_gather_tiled: the entries of a dense [N][K] matrix (16-byte aligned,
  *   K % 8 == 0) at the kept positions of a tile pattern, in its value order. */
@@ -277,6 +290,9 @@ spl_status spl_gather_tiled(const void* W_dense, const spl_matrix* pattern, void
 int64_t spl_sparse_weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
 spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix* Wc, void* grad_values,
                                   void* workspace, hipStream_t stream);
+int64_t spl_sparse_input_grad_workspace_bytes(int64_t M, const spl_matrix* Wc);
+spl_status spl_sparse_input_grad(const void* dY, int64_t M, const spl_matrix* Wc, void* dX, void* workspace,
+                                 hipStream_t stream);
 spl_status spl_sparse_sgd_update(const spl_matrix* Wc, const void* grad_values, float lr, hipStream_t stream);
 
 /* One-shot magnitude pruning on the GPU (paper section 2 removes the weights

@@ -120,6 +120,8 @@ def lib() -> ctypes.CDLL:
         "spl_gather_tiled": (ctypes.c_int, [P, MP, P, P]),
         "spl_sparse_weight_grad_workspace_bytes": (I64, [I64, I64, I64]),
         "spl_sparse_weight_grad": (ctypes.c_int, [P, P, I64, MP, P, P, P]),
+        "spl_sparse_input_grad_workspace_bytes": (I64, [I64, MP]),
+        "spl_sparse_input_grad": (ctypes.c_int, [P, I64, MP, P, P, P]),
         "spl_sparse_sgd_update": (ctypes.c_int, [MP, P, ctypes.c_float, P]),
         "spl_transpose_perm_workspace_bytes": (I64, [I64, I64, I64]),
         "spl_transpose_perm": (ctypes.c_int, [MP, MP, P, P, P]),
@@ -459,6 +461,27 @@ def sparse_weight_grad(dY: torch.Tensor, X: torch.Tensor, Wc: SparseMatrix, out:
     view = Wc.view()
     _check("spl_sparse_weight_grad", L.spl_sparse_weight_grad(_ptr(dY), _ptr(X), M, ctypes.byref(view), _ptr(out),
                                                               _ptr(workspace), _stream(stream)))
+    return out
+
+
+def sparse_input_grad(dY: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = None,
+                      workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """dX [M][K] = dY [M][N] (W . Mask) from W's packed tiles (see spl_sparse_input_grad)."""
+    L = lib()
+    M = _rows_of(dY, "dY")
+    _arg(dY, "dY", shape=(M, Wc.rows), dtype=Wc.dtype, device=False)
+    _dev_tensor(dY, "dY")
+    if out is None:
+        out = torch.empty((M, Wc.cols), dtype=dY.dtype, device=dY.device)
+    _arg(out, "out", shape=(M, Wc.cols), dtype=Wc.dtype)
+    view = Wc.view()
+    if workspace is None:
+        n = L.spl_sparse_input_grad_workspace_bytes(M, ctypes.byref(view))
+        if n < 0:
+            raise ValueError("spl_sparse_input_grad_workspace_bytes rejected the shape")
+        workspace = torch.empty((n,), dtype=torch.uint8, device=dY.device) if n > 0 else None
+    _check("spl_sparse_input_grad", L.spl_sparse_input_grad(_ptr(dY), M, ctypes.byref(view), _ptr(out),
+                                                            _ptr(workspace), _stream(stream)))
     return out
 
 

@@ -927,6 +927,184 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const PfArg
   pf_store_gather<T, FN, FM>(acc, gm, g, lane);
 }
 
+// One stage of MFMA work with the A operand read by LDS transpose reads from
+// a contraction-major buffer (ao: the lane's first-read offsets) and the B
+// operand from a staged X buffer as in pf_mfma_stage.
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_mfma_stage_trA(typename MfmaP<T>::acc_t (&acc)[FN][FM], uint32_t abuf,
+                                                  const uint32_t (&ao)[FN], uint32_t bbuf, int wm, int fr, int fg) {
+  u32x4 a[2][FN], b[2][FM];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+    for (int i = 0; i < FN; ++i) {
+      const uint32_t p = abuf + ao[i] + 32 * kTrRowA * ks;
+      const u32x2 lo = lds_load_tr8(p), hi = lds_load_tr8(p + 4 * kTrRowA);
+      a[ks][i] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+    const uint32_t b0 = bbuf + pf_chunk(wm * 16 * FM + fr, 4 * ks + fg);
+#pragma unroll
+    for (int j = 0; j < FM; ++j) b[ks][j] = lds_load16(b0 + 16 * kPfRow * j);
+  }
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int j = 0; j < FM; ++j) acc[i][j] = MfmaP<T>::run(a[ks][i], b[ks][j], acc[i][j]);
+  // masks: 0x100 LDS read, 0x008 MFMA
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * FN + FM, 0);
+#pragma unroll
+  for (int q = 0; q < 2 * FN + FM; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2 * FN * FM - (2 * FN + FM), 0);
+}
+
+// The input gradient through a sparse layer (Algorithm 1's backward pass):
+// dX [M][K] = dY [M][N] (W.Mask) straight from W's packed tiles, with no
+// packed transpose.  The contraction runs over W's rows, so a stage takes 64
+// of them (four row blocks) across the workgroup's 128 columns: wave w
+// expands the stage's tiles (row block 4 st + w / 2, k-steps 2 (w % 2) + {0, 1}
+// of the block's four; a consecutive pair, one scan) exactly as
+// k_sparse_prefill does, but stores each lane's 8 columns of row r into a
+// contraction-major buffer of 256-byte rows (chunk c of row r at c ^ 2 h(r),
+// h(r) = r % 4 + 4 ((r / 8) % 2)), from which the A fragments (fragment row =
+// column of W, contraction = row of W) come with LDS transpose reads as in
+// k_dense_prefill_dma_tr; dY rows are staged and read as X is.  The same
+// pipeline as k_sparse_prefill: words three stages ahead, windows and dY
+// slabs two ahead, the next stage expanded before this stage's MFMAs, one
+// barrier per stage.  M % 256 == 0, N % 64 == 0, K % 128 == 0 (every tile
+// and slab inside the matrices).
+template <class T>
+__global__ void __launch_bounds__(512, 1) k_sparse_prefill_t(const PfArgs g) {
+  static_assert(!std::is_same<T, I8P>::value, "16-bit payloads");
+  extern __shared__ __align__(16) unsigned char dsm[];
+  __shared__ __align__(16) uint32_t lut[32];
+  using Acc = typename MfmaP<T>::acc_t;
+  constexpr int NW = 8, BN = 128, BM = 256, FN = 4, FM = 4, TW = 2, RR = 8 * NW;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int64_t M = g.M, N = g.N, K = g.K;              // dY [M][N], W [N][K], dX [M][K]
+  const int64_t S = tile_steps(K);
+  const int nst = (int)(N / kPfBK);
+  const int64_t k0 = (int64_t)blockIdx.x * BN, m0 = (int64_t)blockIdx.y * BM;
+  const int64_t s0 = k0 / 32 + 2 * (wave & 1);          // my tiles' k-steps: s0, s0 + 1
+  const int rbw = wave >> 1;                             // my row block within a stage
+  const uint32_t abuf[2] = {lds_off(dsm), lds_off(dsm + kPfBK * kTrRowA)};
+  const uint32_t bbuf[2] = {lds_off(dsm + 2 * kPfBK * kTrRowA), lds_off(dsm + 2 * kPfBK * kTrRowA + BM * kPfRow)};
+  const uint32_t lut_addr = lds_off(lut);
+  if (tid < 16) {
+    lut[2 * tid] = nibble_selector16(tid, 0);
+    lut[2 * tid + 1] = nibble_selector16(tid, 1);
+  }
+  // where my expanded 8 columns go: row r = 16 rbw + fr of the stage, chunk 4 (2 (w % 2) + i) + fg
+  const int er = 16 * rbw + fr;
+  const int eh = (er & 3) | (((er >> 3) & 1) << 2);
+  uint32_t eo[TW];
+#pragma unroll
+  for (int i = 0; i < TW; ++i) eo[i] = (uint32_t)(er * kTrRowA + 16 * ((4 * (2 * (wave & 1) + i) + fg) ^ (2 * eh)));
+  // my A fragments' first reads (as in k_dense_prefill_dma_tr)
+  const int t = lane & 15, r0 = 8 * (lane >> 4) + (t >> 2);
+  const int h = (t >> 2) | (((lane >> 4) & 1) << 2);
+  uint32_t ao[FN];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+    ao[i] = (uint32_t)(r0 * kTrRowA + 16 * ((8 * wn + 2 * i + ((t & 3) >> 1)) ^ (2 * h)) + 8 * (t & 1));
+
+  auto fetch_words = [&](TileWords<TW>& tw, int st) {
+#pragma unroll
+    for (int i = 0; i < TW; ++i) {
+      const int64_t tt = (int64_t)(4 * st + rbw) * S + s0 + i;
+      tw.w[i] = g.bm[tt * 16 + fr];
+      tw.off[i] = g.toff[tt];
+    }
+  };
+  auto fetch_windows = [&](TileWindows<TW>& tv, const TileWords<TW>& tw) {
+    // the pair's values before mine: the exclusive wave scan of the lanes' kept counts (16-bit halves)
+    const uint32_t b0 = __builtin_amdgcn_ubfe(tw.w[0], 8 * fg, 8);
+    const uint32_t b1 = __builtin_amdgcn_ubfe(tw.w[1], 8 * fg, 8);
+    const uint32_t pc = __popc(b0) | (__popc(b1) << 16);
+    const uint32_t ex = wave_inclusive_scan(pc) - pc;
+#pragma unroll
+    for (int i = 0; i < TW; ++i) {
+      const uint32_t byte = i ? b1 : b0;
+      const uint32_t oa = (uint32_t)tw.off[i] + (i ? ex >> 16 : ex & 0xffffu);
+      const uint32_t ob = oa + __popc(byte & 0xfu);
+      tv.byte[i] = byte;
+      __builtin_memcpy(&tv.v0[i], g.values + 2u * oa, 8);
+      __builtin_memcpy(&tv.v1[i], g.values + 2u * ob, 8);
+    }
+  };
+  auto expand_store = [&](const TileWindows<TW>& tv, uint32_t buf) {
+#pragma unroll
+    for (int i = 0; i < TW; ++i) {
+      const u32x2 slo = lds_load8(lut_addr + 8u * (tv.byte[i] & 0xfu));
+      const u32x2 shi = lds_load8(lut_addr + 8u * (tv.byte[i] >> 4));
+      u32x4 a;
+      a.x = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.x);
+      a.y = __builtin_amdgcn_perm(tv.v0[i].y, tv.v0[i].x, slo.y);
+      a.z = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.x);
+      a.w = __builtin_amdgcn_perm(tv.v1[i].y, tv.v1[i].x, shi.y);
+      *reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(buf + eo[i])) = a;
+    }
+  };
+
+  Acc acc[FN][FM];
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j) acc[i][j] = Acc{0, 0, 0, 0};
+
+  const SlabSrc<RR> xsrc(g.X, M, N, m0, tid);
+  Slab<BM / RR> x0, x1;
+  TileWords<TW> tw;
+  TileWindows<TW> tv;
+  if (nst > 0) {
+    fetch_words(tw, 0);
+    xsrc.template fetch<false>(x0, N, 0);
+    fetch_windows(tv, tw);                               // stage 0
+    if (nst > 1) {
+      fetch_words(tw, 1);
+      xsrc.template fetch<false>(x1, N, kPfBK);
+    }
+  }
+  __syncthreads();                                       // the selector table
+  if (nst > 0) {
+    expand_store(tv, abuf[0]);
+    slab_store<RR>(x0, bbuf[0], tid);
+    if (nst > 1) {
+      fetch_windows(tv, tw);                             // stage 1
+      if (nst > 2) fetch_words(tw, 2);
+    }
+  }
+  __syncthreads();
+  // (xl holds stage st + 1; xn receives stage st + 2)
+  auto step = [&](int st, Slab<BM / RR>& xn, Slab<BM / RR>& xl) {
+    const int cur = st & 1;
+    if (st + 1 < nst) {
+      expand_store(tv, abuf[cur ^ 1]);                   // stage st + 1
+      slab_store<RR>(xl, bbuf[cur ^ 1], tid);
+      if (st + 2 < nst) {
+        fetch_windows(tv, tw);                           // stage st + 2 (its words were fetched a stage ago)
+        if (st + 3 < nst) fetch_words(tw, st + 3);
+        xsrc.template fetch<false>(xn, N, (int64_t)kPfBK * (st + 2));
+      }
+    }
+    pf_mfma_stage_trA<T, FN, FM>(acc, abuf[cur], ao, bbuf[cur], wm, fr, fg);
+    if (st + 1 < nst) __syncthreads();
+  };
+  for (int st = 0; st < nst; st += 2) {
+    step(st, x0, x1);
+    if (st + 1 < nst) step(st + 1, x1, x0);
+  }
+  pf_store<T, FN, FM>(acc, g.Y, M, K, k0, m0, wn, wm, fr, fg);
+}
+
 int pf_cus() { return device_cus(); }
 
 // Workgroup tile of a launch: 128 x 256 (8 waves) when that still gives every
@@ -1091,6 +1269,29 @@ hipError_t launch_dense_prefill_gather_tr(const void* Xc, int64_t M, const void*
   a.M = M, a.N = N, a.K = K;
   a.gbm = P.bitmask, a.gtoff = P.tile_offsets, a.gval = static_cast<uint16_t*>(values);
   return dtype == SPL_BF16 ? dense_prefill_tr<Bf16>(a, s) : dense_prefill_tr<F16>(a, s);
+}
+
+// dX [M][K] = dY [M][N] (W.Mask) from W's packed tiles (W [N][K], tile layout).
+bool sparse_input_grad_applies(int64_t M, const spl_matrix& W) {
+  return M % 256 == 0 && W.rows % 64 == 0 && W.cols % 128 == 0 && pf_large_tile(W.cols, M);
+}
+
+hipError_t launch_sparse_input_grad(const void* dY, int64_t M, const spl_matrix& W, void* dX, hipStream_t s) {
+  if (!sparse_input_grad_applies(M, W)) return hipErrorInvalidValue;
+  PfArgs a{};
+  a.X = static_cast<const uint16_t*>(dY);
+  a.bm = W.bitmask;
+  a.values = static_cast<const unsigned char*>(W.values);
+  a.toff = W.tile_offsets;
+  a.M = M, a.N = W.rows, a.K = W.cols;
+  a.Y = static_cast<uint16_t*>(dX);
+  auto* kernel = W.dtype == SPL_BF16 ? k_sparse_prefill_t<Bf16> : k_sparse_prefill_t<F16>;
+  static PerDeviceFlag lds_set[2];
+  const int lds = pf_lds(128, 256);
+  const hipError_t attr = allow_lds_once(lds_set[W.dtype == SPL_BF16 ? 0 : 1], kernel, lds);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)(W.cols / 128), (unsigned)(M / 256)), dim3(512), lds, s, a);
+  return hipGetLastError();
 }
 
 // Gated half of a Llama MLP: Y = silu(X Wg^T) * (X Wu^T) (same dtype and shape).

@@ -191,6 +191,27 @@ hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const sp
   return e;
 }
 
+// The input gradient dX [M][K] = dY [M][N] (W.Mask): straight from W's packed
+// tiles where the direct kernel applies (no workspace); otherwise W is decoded
+// and transposed into the workspace ([N][K], then [K][N]) and multiplied by
+// the dense prefill kernels.
+int64_t input_grad_workspace_bytes(int64_t M, const spl_matrix& W) {
+  return sparse_input_grad_applies(M, W) ? 0 : 2 * align256(2 * W.rows * W.cols);
+}
+
+hipError_t launch_input_grad(const void* dY, int64_t M, const spl_matrix& W, void* dX, void* ws, hipStream_t s) {
+  if (W.nnz == 0) return launch_zero_fill(dX, M * W.cols, s);
+  if (sparse_input_grad_applies(M, W)) return launch_sparse_input_grad(dY, M, W, dX, s);
+  const int64_t N = W.rows, K = W.cols;
+  unsigned char* base = static_cast<unsigned char*>(ws);
+  void* Wd = base;                                   // [N][K]
+  void* Wt = base + align256(2 * N * K);             // [K][N]
+  hipError_t e = launch_unpack(W, Wd, s);
+  if (e == hipSuccess) e = launch_transpose16(Wd, N, K, Wt, s);
+  if (e == hipSuccess) e = launch_dense_prefill(dY, M, Wt, W.dtype, K, N, dX, s);   // dY Wt^T
+  return e;
+}
+
 int64_t transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz) {
   return 4 * align256(2 * N * K) + 2 * align256(2 * nnz);
 }

@@ -378,6 +378,26 @@ spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, cons
   return launched(spl::launch_weight_grad(dY, X, M, *Wc, grad_values, workspace, stream));
 }
 
+int64_t spl_sparse_input_grad_workspace_bytes(int64_t M, const spl_matrix* Wc) {
+  if (check_tiled_fp(Wc) != SPL_OK || M < 0) return -1;
+  if (M > 0 && (!dims_ok(M, Wc->rows) || !dims_ok(M, Wc->cols))) return -1;
+  return spl::input_grad_workspace_bytes(M, *Wc);
+}
+
+spl_status spl_sparse_input_grad(const void* dY, int64_t M, const spl_matrix* Wc, void* dX, void* workspace,
+                                 hipStream_t stream) {
+  const spl_status st = check_tiled_fp(Wc);
+  if (st != SPL_OK) return st;
+  const spl_status xy = check_xy(dY, M, Wc->rows, Wc->cols, dX);   // dY [M][N], dX [M][K]
+  if (xy != SPL_OK || M == 0) return xy;
+  if (!spl::sparse_input_grad_applies(M, *Wc)) {
+    if (Wc->rows % 8 != 0) return SPL_ERR_UNSUPPORTED;             // the dense product's 16-byte rows of dY
+    if (!workspace || !aligned(workspace, 256)) return SPL_ERR_INVALID_ARG;
+  }
+  (void)hipGetLastError();
+  return launched(spl::launch_input_grad(dY, M, *Wc, dX, workspace, stream));
+}
+
 spl_status spl_sparse_sgd_update(const spl_matrix* Wc, const void* grad_values, float lr, hipStream_t stream) {
   const spl_status st = check_tiled_fp(Wc);
   if (st != SPL_OK) return st;

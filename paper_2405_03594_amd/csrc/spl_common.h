@@ -214,6 +214,11 @@ hipError_t launch_dense_prefill_gather(const void* X, int64_t M, const void* W, 
 // where dense_prefill_tr_applies (M % 256, N % 128 and K % 64 all zero, a
 // launch of at least one 128 x 256 block per CU, 16-byte aligned factors).
 bool dense_prefill_tr_applies(int64_t M, int64_t N, int64_t K, const void* Xc, const void* Wc);
+// The input gradient dX [M][K] = dY [M][N] (W.Mask) from W's packed tiles
+// where sparse_input_grad_applies (M % 256, N % 64 and K % 128 all zero, a
+// launch of at least one 128 x 256 block per CU; W in the tile layout, 16-bit).
+bool sparse_input_grad_applies(int64_t M, const spl_matrix& W);
+hipError_t launch_sparse_input_grad(const void* dY, int64_t M, const spl_matrix& W, void* dX, hipStream_t s);
 hipError_t launch_dense_prefill_gather_tr(const void* Xc, int64_t M, const void* Wc, int32_t dtype, int64_t N,
                                           int64_t K, const spl_matrix& P, void* values, hipStream_t s);
 // Sparse-quantized kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
@@ -239,6 +244,8 @@ int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
                               void* ws, hipStream_t s);
 hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, hipStream_t s);
+int64_t input_grad_workspace_bytes(int64_t M, const spl_matrix& W);
+hipError_t launch_input_grad(const void* dY, int64_t M, const spl_matrix& W, void* dX, void* ws, hipStream_t s);
 int64_t transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz);
 hipError_t launch_transpose_perm(const spl_matrix& W, const spl_matrix& Wt, int32_t* perm, void* ws, hipStream_t s);
 hipError_t launch_permute_values(const void* src, const int32_t* perm, int64_t nnz, void* dst, hipStream_t s);

@@ -134,6 +134,9 @@ int main() {
     REJECTS(spl_sparse_linear_int4(q, sc, M, &rows, sc, Y, nullptr, nullptr));
     REJECTS(spl_quantize_rows_i8(X, 42, M, 64, const_cast<int8_t*>(q), const_cast<float*>(sc), nullptr));
     REJECTS(spl_sparse_weight_grad(X, X, M, &bad, Y, Y, nullptr));
+    REJECTS(spl_sparse_input_grad(X, M, &bad, Y, Y, nullptr));
+    if (M != 0) REJECTS(spl_sparse_input_grad(X, M, &rows, Y, Y, nullptr));
+    EXPECT(spl_sparse_input_grad_workspace_bytes(M, &bad) == -1);
     REJECTS(spl_dense_linear_ex(X, M, X, SPL_BF16, 64, 64, Y, 77, nullptr));
   }
   REJECTS(spl_pack_int4(&i4, static_cast<uint8_t*>(Y), nullptr, nullptr));

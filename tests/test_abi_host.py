@@ -387,6 +387,22 @@ def test_training_argument_checks(L):
     assert w(A, B, 16, ctypes.byref(m), G, ws + 16, None) == INVALID           # workspace alignment
     assert w(None, B, 16, ctypes.byref(m), G, ws, None) == INVALID
     assert w(A, B, 16, ctypes.byref(m), None, ws, None) == INVALID
+    ig, wb = L.spl_sparse_input_grad, L.spl_sparse_input_grad_workspace_bytes
+    big = _mat(rows=4096, cols=4096, layout=1, tile_offsets=0x40000)
+    assert wb(2048, ctypes.byref(big)) == 0                                    # W's tiles read in the product
+    assert wb(2000, ctypes.byref(big)) == 2 * a256(2 * 4096 * 4096)            # decoded, transposed copies
+    assert wb(256, ctypes.byref(big)) == 2 * a256(2 * 4096 * 4096)            # 16 x 1 blocks: fewer than CUs
+    assert wb(-1, ctypes.byref(big)) < 0 and wb(16, ctypes.byref(_mat())) < 0  # row layout
+    m8 = _mat(rows=8, cols=64, layout=1, tile_offsets=0x40000)
+    assert ig(A, 0, ctypes.byref(m8), G, None, None) == OK                     # no tokens
+    assert ig(A, -1, ctypes.byref(m8), G, ws, None) == INVALID
+    assert ig(None, 16, ctypes.byref(m8), G, ws, None) == INVALID
+    assert ig(A, 16, ctypes.byref(m8), None, ws, None) == INVALID
+    assert ig(A + 8, 16, ctypes.byref(m8), G, ws, None) == INVALID             # misaligned dY rows
+    assert ig(A, 16, ctypes.byref(m8), G, None, None) == INVALID               # the fallback needs a workspace
+    assert ig(A, 16, ctypes.byref(m8), G, ws + 16, None) == INVALID            # workspace alignment
+    assert ig(A, 16, ctypes.byref(m), G, ws, None) == UNSUPPORTED              # N % 8 != 0 (dense fallback)
+    assert ig(A, 16, ctypes.byref(_mat(rows=8)), G, ws, None) == UNSUPPORTED   # row layout
     s = L.spl_sparse_sgd_update
     assert s(ctypes.byref(m), None, 0.1, None) == INVALID                      # nnz > 0 needs a gradient
     assert s(ctypes.byref(_mat()), G, 0.1, None) == UNSUPPORTED                # row layout

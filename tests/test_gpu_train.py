@@ -6,6 +6,8 @@ with |y - y64| <= max(2e-2, 1e-2 |y64|); one SGD step (binary32 product and
 difference, one rounding) within 2^-8 |y64| (bf16) / 2^-11 |y64| (fp16), plus
 2^-22 (|w| + lr |g|) for the binary32 steps and the smallest normal of the
 payload type."""
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -94,6 +96,41 @@ def test_weight_grad_contraction_major(orc, spl, dtype, N, K, M, s):
     assert_close(G, ref, f"weight grad {dtype} N={N} K={K} M={M}")
 
 
+def test_weight_grad_direct_path_and_fallback_agree(orc, spl):
+    """The same product through both paths: with 16-byte aligned dY and X the
+    weight gradient reads them as stored and leaves the workspace untouched;
+    with X 8 bytes off that alignment (a view into a larger buffer) it
+    transposes both into the workspace first.  Both match the oracle on every
+    kept entry, and they agree bit for bit (the same 128 x 256 blocks, the
+    same MFMA operands in the same token order)."""
+    import torch
+
+    N, K, M = 2048, 4096, 128
+    W, mask = synth.weight(630, N, K, "bf16", 0.7)
+    X = synth.activations(631, M, K, "bf16")
+    dY = synth.activations(632, M, N, "bf16")
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), torch.from_numpy(mask).cuda())
+    dYd, Xd = to_dev(dY, "bf16"), to_dev(X, "bf16")
+    nws = spl.lib().spl_sparse_weight_grad_workspace_bytes(M, N, K)
+    ws = torch.full((nws,), 0xA5, dtype=torch.uint8, device="cuda")
+    g_direct = spl.sparse_weight_grad(dYd, Xd, Wc, workspace=ws)
+    torch.cuda.synchronize()
+    assert bool((ws == 0xA5).all()), "the direct path wrote to the workspace"
+    flat = torch.empty((M * K + 4,), dtype=Xd.dtype, device="cuda")
+    Xu = flat[4:].view(M, K)
+    Xu.copy_(Xd)
+    assert Xu.data_ptr() % 16 == 8
+    g_fallback = spl.sparse_weight_grad(dYd, Xu, Wc, workspace=ws)
+    torch.cuda.synchronize()
+    assert not bool((ws == 0xA5).all()), "the fallback path did not use the workspace"
+    ref = orc.weight_grad_f64(dY, X, "bf16", orc.pack(W, "bf16", mask))
+    for g, name in ((g_direct, "direct"), (g_fallback, "fallback")):
+        G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
+        assert_close(G, ref, f"weight grad ({name} path)")
+    n = Wc.nnz                                         # the buffers' tails past nnz are never written
+    assert torch.equal(g_direct[:n].view(torch.int16), g_fallback[:n].view(torch.int16))
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_sgd_update(orc, spl, dtype):
     import torch
@@ -144,6 +181,84 @@ def test_weight_grad_llama_shapes(orc, spl, name, j, M):
     G = from_dev_f64(spl.unpack(_with_values(spl, Wc, g)))
     ref = orc.to_f64(dY, "bf16").T @ orc.to_f64(X, "bf16") * mask
     assert_close(G, ref, f"{name} weight grad M={M}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("N,K,M,s", [(64, 8192, 1024, 0.7), (192, 16384, 512, 0.5), (320, 4096, 2048, 0.9),
+                                     (128, 4096, 2048, 0.0)])
+def test_input_grad_from_packed_tiles(orc, spl, dtype, N, K, M, s):
+    """dX = dY (W.Mask) straight from W's tiles (no packed transpose, no
+    workspace): shapes of one 128 x 256 block per CU over one, three, five
+    (an odd count: the two-stage loop's tail) and two 64-row stages of W,
+    every output compared with the oracle."""
+    import torch
+
+    W, mask = synth.weight(650 + N, N, K, dtype, s)
+    dY = synth.activations(651 + M, M, N, dtype)
+    Wc = spl.pack_sparse(to_dev(W, dtype), torch.from_numpy(mask).cuda())
+    assert spl.lib().spl_sparse_input_grad_workspace_bytes(M, ctypes.byref(Wc.view())) == 0
+    dX = from_dev_f64(spl.sparse_input_grad(to_dev(dY, dtype), Wc))
+    assert_close(dX, orc.input_grad_f64(dY, dtype, orc.pack(W, dtype, mask)), f"dX {dtype} N={N} K={K} M={M}")
+
+
+@pytest.mark.parametrize("N,K,M,s", [(104, 1000, 64, 0.7), (296, 264, 136, 0.5), (48, 520, 3, 0.9),
+                                     (4096, 4096, 2000, 0.7)])
+def test_input_grad_decoded_fallback(orc, spl, N, K, M, s):
+    """Shapes the direct kernel does not take: W decoded and transposed into
+    the workspace, then the dense product; compared with the oracle (every
+    output, or 64 full rows at 4096 x 4096, M = 2000)."""
+    import torch
+
+    W, mask = synth.weight(660 + N, N, K, "bf16", s)
+    dY = synth.activations(661 + M, M, N, "bf16")
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), torch.from_numpy(mask).cuda())
+    assert spl.lib().spl_sparse_input_grad_workspace_bytes(M, ctypes.byref(Wc.view())) > 0
+    dX = from_dev_f64(spl.sparse_input_grad(to_dev(dY, "bf16"), Wc))
+    rows = np.arange(M) if M * K <= 1 << 22 else np.sort(np.concatenate(
+        [[0, M - 1], np.random.default_rng(N).choice(np.arange(1, M - 1), 62, replace=False)]))
+    ref = orc.input_grad_f64(dY[rows], "bf16", orc.pack(W, "bf16", mask))
+    assert_close(dX[rows], ref, f"dX fallback N={N} K={K} M={M}")
+
+
+def test_input_grad_edge_cases(spl):
+    """No kept entry: dX = 0 on both paths; no tokens: nothing to do."""
+    import torch
+
+    for N, K, M in ((64, 8192, 1024), (40, 72, 24)):
+        Wc = spl.pack_sparse(torch.zeros((N, K), dtype=torch.bfloat16, device="cuda"))
+        assert Wc.nnz == 0
+        dX = spl.sparse_input_grad(torch.ones((M, N), dtype=torch.bfloat16, device="cuda"), Wc,
+                                   out=torch.full((M, K), 7.0, dtype=torch.bfloat16, device="cuda"))
+        assert not bool(dX.any())
+    W, mask = synth.weight(670, 64, 128, "bf16", 0.5)
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), torch.from_numpy(mask).cuda())
+    out = spl.sparse_input_grad(torch.empty((0, 64), dtype=torch.bfloat16, device="cuda"), Wc)
+    assert out.shape == (0, 128)
+
+
+@pytest.mark.parametrize("name,j", [("q", 0), ("gate", 4), ("down", 6)])
+def test_input_grad_llama_shapes(orc, spl, name, j):
+    """The bench's training shapes at M = 2048 (the direct kernel): 64 full
+    rows (0, M - 1 and 62 seeded) of dX against the oracle, and the same rows
+    through the packed transpose (spl_sparse_linear on Wt) within the same
+    tolerance."""
+    import torch
+
+    _, N, K = synth.LLAMA2_7B_LINEARS[j]
+    M = 2048
+    W, mask = synth.weight(synth.weight_seed(0, j), N, K, "bf16", 0.7)
+    dY = synth.activations(680 + j, M, N, "bf16")
+    md = torch.from_numpy(mask).cuda()
+    Wc = spl.pack_sparse(to_dev(W, "bf16"), md)
+    dYd = to_dev(dY, "bf16")
+    dX = from_dev_f64(spl.sparse_input_grad(dYd, Wc))
+    rng = np.random.default_rng(j)
+    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(np.arange(1, M - 1), 62, replace=False)]))
+    ref = orc.input_grad_f64(dY[rows], "bf16", orc.pack(W, "bf16", mask))
+    assert_close(dX[rows], ref, f"{name} dX M={M}")
+    Wt = spl.pack_sparse(spl.transpose16(spl.unpack(Wc)), md.t().contiguous())
+    dXt = from_dev_f64(spl.sparse_linear(dYd, Wt))
+    assert_close(dXt[rows], ref, f"{name} dX via the packed transpose M={M}")
 
 
 @pytest.mark.parametrize("N,K,s", [(8, 8, 0.5), (104, 1000, 0.7), (296, 264, 0.0), (64, 520, 0.9)])

@@ -744,3 +744,116 @@ def test_contraction_major_stage_and_transposed_reads(M, N, K):
                                     want = [(op, k0 + 32 * ks + 8 * (lane >> 4) + 4 * half + e,
                                              first + c0 + 16 * f + (lane & 15)) for e in range(4)]
                                     assert got == want, (op, wave, f, ks, half, lane)
+
+
+# ---------------------------------------------------------------- the input gradient from W's packed tiles
+
+def _input_grad_lines():
+    src = open(SRC).read()
+    for line in ("constexpr int NW = 8, BN = 128, BM = 256, FN = 4, FM = 4, TW = 2, RR = 8 * NW;",
+                 "const int nst = (int)(N / kPfBK);",
+                 "const int64_t s0 = k0 / 32 + 2 * (wave & 1);",
+                 "const int rbw = wave >> 1;",
+                 "const int er = 16 * rbw + fr;",
+                 "const int eh = (er & 3) | (((er >> 3) & 1) << 2);",
+                 "for (int i = 0; i < TW; ++i) eo[i] = (uint32_t)(er * kTrRowA + 16 * ((4 * (2 * (wave & 1) + i) + "
+                 "fg) ^ (2 * eh)));",
+                 "ao[i] = (uint32_t)(r0 * kTrRowA + 16 * ((8 * wn + 2 * i + ((t & 3) >> 1)) ^ (2 * h)) + 8 * (t & 1));",
+                 "const int64_t tt = (int64_t)(4 * st + rbw) * S + s0 + i;",
+                 "tw.w[i] = g.bm[tt * 16 + fr];",
+                 "const uint32_t ex = wave_inclusive_scan(pc) - pc;",
+                 "const uint32_t oa = (uint32_t)tw.off[i] + (i ? ex >> 16 : ex & 0xffffu);",
+                 "__builtin_memcpy(&tv.v1[i], g.values + 2u * ob, 8);",
+                 "*reinterpret_cast<__attribute__((address_space(3))) u32x4*>((uintptr_t)(buf + eo[i])) = a;",
+                 "const uint32_t p = abuf + ao[i] + 32 * kTrRowA * ks;",
+                 "const uint32_t b0 = bbuf + pf_chunk(wm * 16 * FM + fr, 4 * ks + fg);",
+                 "if (st + 3 < nst) fetch_words(tw, st + 3);",
+                 "pf_store<T, FN, FM>(acc, g.Y, M, K, k0, m0, wn, wm, fr, fg);",
+                 "return M % 256 == 0 && W.rows % 64 == 0 && W.cols % 128 == 0 && pf_large_tile(W.cols, M);",
+                 "hipLaunchKernelGGL(kernel, dim3((unsigned)(W.cols / 128), (unsigned)(M / 256)), dim3(512), lds, s, a);"):
+        assert line in src, f"input-gradient kernel changed: update this replay ({line})"
+
+
+@pytest.mark.parametrize("N,K,s", [(64, 128, 0.5), (128, 256, 0.7), (192, 384, 0.0), (64, 128, 1.0), (256, 512, 0.9)])
+def test_input_grad_expansion_and_transposed_reads(orc, N, K, s):
+    """dX = dY (W.Mask) from W's packed tiles: every workgroup column's
+    stages, replayed.  Each stage's 16 tiles (four row blocks of W x the
+    block's four k-steps) are expanded once, by wave w the pair (row block
+    4 st + w / 2, k-steps 2 (w % 2) + {0, 1}), with windows inside the payload
+    + 16 readable bytes; the expanded 8 columns of each lane equal the dense
+    masked W and land once each in the contraction-major stage buffer (row
+    of W r at 256 r, chunk c at c ^ 2 h(r)); and through the transpose read's
+    lane mapping every lane of every A fragment receives W[64 st + 32 ks +
+    8 (lane / 16) + 4 half + e][k0 + 64 wn + 16 i + lane % 16], its operand."""
+    _input_grad_lines()
+    bk, _ = _constants()
+    BN, NW, FN = 128, 8, 4
+    rowA = 2 * BN
+    W, mask = synth.weight(83 + N + K, N, K, "bf16", s)
+    T = orc.pack_tiled(W, "bf16", mask)
+    vbytes = np.concatenate([T.values.view(np.uint8), np.zeros(16, np.uint8)])
+    limit = 2 * T.nnz + 16
+    dense = np.where(mask.astype(bool), W.view(np.uint16), 0).astype(np.uint16)
+    S = K // 32
+    bm = T.bitmask.reshape(-1).astype(np.uint64)
+    offs = T.tile_offsets.astype(np.int64)
+    assert N % bk == 0 and K % BN == 0
+    for kb in range(K // BN):
+        k0 = kb * BN
+        for st in range(N // bk):
+            lds = {}                                     # byte -> W element (row, col) it holds
+            seen = set()
+            for wave in range(NW):
+                rbw, s0 = wave >> 1, k0 // 32 + 2 * (wave & 1)
+                tiles = []
+                for i in range(2):
+                    t = (4 * st + rbw) * S + s0 + i
+                    assert (4 * st + rbw, s0 + i) not in seen
+                    seen.add((4 * st + rbw, s0 + i))
+                    tiles.append((t, [int(bm[t * 16 + r]) for r in range(16)]))
+                cnt = np.array([[_popc((tiles[i][1][l & 15] >> (8 * (l >> 4))) & 0xFF) for l in range(64)]
+                                for i in range(2)])
+                packed = cnt[0] | (cnt[1] << 16)
+                ex = np.cumsum(packed) - packed
+                for i in range(2):
+                    t, words = tiles[i]
+                    for lane in range(64):
+                        fr, fg = lane & 15, lane >> 4
+                        byte = (words[fr] >> (8 * fg)) & 0xFF
+                        oa = int(offs[t]) + (int(ex[lane] >> 16) if i else int(ex[lane] & 0xFFFF))
+                        ob = oa + _popc(byte & 0xF)
+                        for o in (oa, ob):
+                            assert 2 * o + 8 <= limit
+                        v0 = vbytes[2 * oa:2 * oa + 8].view(np.uint32)
+                        v1 = vbytes[2 * ob:2 * ob + 8].view(np.uint32)
+                        lo, hi = byte & 0xF, byte >> 4
+                        got = np.array([_perm(v0[1], v0[0], _nibble_selector(lo, 0)),
+                                        _perm(v0[1], v0[0], _nibble_selector(lo, 1)),
+                                        _perm(v1[1], v1[0], _nibble_selector(hi, 0)),
+                                        _perm(v1[1], v1[0], _nibble_selector(hi, 1))], dtype=np.uint32).view(np.uint16)
+                        n, kk = 16 * (4 * st + rbw) + fr, 32 * (s0 + i) + 8 * fg
+                        assert np.array_equal(got, dense[n, kk:kk + 8]), (kb, st, wave, i, lane)
+                        er = 16 * rbw + fr
+                        eh = (er & 3) | (((er >> 3) & 1) << 2)
+                        eo = er * rowA + 16 * ((4 * (2 * (wave & 1) + i) + fg) ^ (2 * eh))
+                        assert 0 <= eo and eo + 16 <= bk * rowA
+                        for e in range(8):
+                            assert eo + 2 * e not in lds
+                            lds[eo + 2 * e] = (n, kk + e)
+            assert len(lds) == bk * BN
+            for wave in range(NW):
+                wn = wave & 1
+                for i in range(FN):
+                    off = []
+                    for lane in range(64):
+                        t, r0 = lane & 15, 8 * (lane >> 4) + ((lane & 15) >> 2)
+                        h = (t >> 2) | (((lane >> 4) & 1) << 2)
+                        off.append(r0 * rowA + 16 * ((8 * wn + 2 * i + ((t & 3) >> 1)) ^ (2 * h)) + 8 * (t & 1))
+                    for ks in range(2):
+                        for half in range(2):
+                            addrs = [o + 32 * rowA * ks + 4 * rowA * half for o in off]
+                            for lane in range(64):
+                                got = [lds[b] for b in _tr_read(addrs, lane)]
+                                want = [(bk * st + 32 * ks + 8 * (lane >> 4) + 4 * half + e,
+                                         k0 + 64 * wn + 16 * i + (lane & 15)) for e in range(4)]
+                                assert got == want, (kb, st, wave, i, ks, half, lane)
