@@ -290,6 +290,23 @@ spl_status spl_gather_tiled(const void* W_dense, const spl_matrix* pattern, void
 int64_t spl_sparse_weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
 spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix* Wc, void* grad_values,
                                   void* workspace, hipStream_t stream);
+/* spl_sparse_weight_grad_group: the weight gradients of up to SPL_MAX_GROUP
+ *   layers that share the batch M and the dtype (for example q, k and v, which
+ *   share X), each task's output identical to spl_sparse_weight_grad's on the
+ *   same arguments.  When every task takes the path that reads dY and X as
+ *   stored, they run in one launch (so the blocks of all tasks share the
+ *   chip's last partial round); otherwise one call per task, the workspace
+ *   (the largest spl_sparse_weight_grad_workspace_bytes of the tasks, 256-byte
+ *   aligned) serving them in turn.  Tasks must not write overlapping outputs;
+ *   the task array is read during the call only. */
+typedef struct {
+  const void* dY;                /* [M][N] of W->dtype */
+  const void* X;                 /* [M][K] of W->dtype */
+  const spl_matrix* W;           /* tile layout, fp16 or bf16: the pattern and value order of the gradient */
+  void* grad_values;             /* out: W->nnz payloads in W's value order */
+} spl_weight_grad_task;
+spl_status spl_sparse_weight_grad_group(const spl_weight_grad_task* tasks, int32_t count, int64_t M,
+                                        void* workspace, hipStream_t stream);
 int64_t spl_sparse_input_grad_workspace_bytes(int64_t M, const spl_matrix* Wc);
 spl_status spl_sparse_input_grad(const void* dY, int64_t M, const spl_matrix* Wc, void* dX, void* workspace,
                                  hipStream_t stream);

@@ -70,6 +70,11 @@ class _Int8Task(ctypes.Structure):
                 ("w_scales", ctypes.c_void_p), ("Y", ctypes.c_void_p), ("acc_out", ctypes.c_void_p)]
 
 
+class _WeightGradTask(ctypes.Structure):
+    _fields_ = [("dY", ctypes.c_void_p), ("X", ctypes.c_void_p), ("W", ctypes.POINTER(_Matrix)),
+                ("grad_values", ctypes.c_void_p)]
+
+
 class _DenseInt8Task(ctypes.Structure):
     _fields_ = [("Xq", ctypes.c_void_p), ("x_scales", ctypes.c_void_p), ("Wq", ctypes.c_void_p),
                 ("w_scales", ctypes.c_void_p), ("N", ctypes.c_int64), ("K", ctypes.c_int64), ("Y", ctypes.c_void_p),
@@ -120,6 +125,7 @@ def lib() -> ctypes.CDLL:
         "spl_gather_tiled": (ctypes.c_int, [P, MP, P, P]),
         "spl_sparse_weight_grad_workspace_bytes": (I64, [I64, I64, I64]),
         "spl_sparse_weight_grad": (ctypes.c_int, [P, P, I64, MP, P, P, P]),
+        "spl_sparse_weight_grad_group": (ctypes.c_int, [ctypes.POINTER(_WeightGradTask), I32, I64, P, P]),
         "spl_sparse_input_grad_workspace_bytes": (I64, [I64, MP]),
         "spl_sparse_input_grad": (ctypes.c_int, [P, I64, MP, P, P, P]),
         "spl_sparse_sgd_update": (ctypes.c_int, [MP, P, ctypes.c_float, P]),
@@ -462,6 +468,33 @@ def sparse_weight_grad(dY: torch.Tensor, X: torch.Tensor, Wc: SparseMatrix, out:
     _check("spl_sparse_weight_grad", L.spl_sparse_weight_grad(_ptr(dY), _ptr(X), M, ctypes.byref(view), _ptr(out),
                                                               _ptr(workspace), _stream(stream)))
     return out
+
+
+def sparse_weight_grad_group(dYs, Xs, mats, outs=None, workspace: torch.Tensor | None = None,
+                             stream=None) -> list:
+    """Weight gradients of several layers of one batch in one call (see
+    spl_sparse_weight_grad_group); outs[i] gets mats[i]'s kept entries."""
+    L = lib()
+    if not (len(dYs) == len(Xs) == len(mats)) or not 1 <= len(mats) <= MAX_GROUP:
+        raise ValueError("dYs, Xs and mats: one entry per task, 1..MAX_GROUP tasks")
+    M = Xs[0].shape[0]
+    for dY, X in zip(dYs, Xs):
+        _dev_tensor(dY, "dY")
+        _dev_tensor(X, "X")
+        if dY.shape[0] != M or X.shape[0] != M:
+            raise ValueError("every task has the same batch M")
+    if outs is None:
+        outs = [torch.empty_like(Wc.values) for Wc in mats]
+    if workspace is None:
+        need = max(L.spl_sparse_weight_grad_workspace_bytes(M, Wc.rows, Wc.cols) for Wc in mats)
+        workspace = torch.empty((need,), dtype=torch.uint8, device=Xs[0].device)
+    views = [Wc.view() for Wc in mats]
+    tasks = (_WeightGradTask * len(mats))(*[
+        _WeightGradTask(dY.data_ptr(), X.data_ptr(), ctypes.pointer(v), o.data_ptr())
+        for dY, X, v, o in zip(dYs, Xs, views, outs)])
+    _check("spl_sparse_weight_grad_group", L.spl_sparse_weight_grad_group(tasks, len(mats), M, _ptr(workspace),
+                                                                          _stream(stream)))
+    return outs
 
 
 def sparse_input_grad(dY: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = None,

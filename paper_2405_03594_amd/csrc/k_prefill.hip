@@ -859,10 +859,22 @@ __device__ __forceinline__ void pf_mfma_stage_tr(typename MfmaP<T>::acc_t (&acc)
   __builtin_amdgcn_sched_group_barrier(0x008, 2 * FN * FM - (FN + FM), 0);
 }
 
+// A grouped launch of the contraction-major core: task i (its own factors,
+// shapes and pattern, one dtype) owns workgroups [first[i], first[i + 1]),
+// block b of it at n-block b % (N / 128), m-block b / (N / 128).
+constexpr int kTrGroupMax = 4;
+struct TrGroupArg {
+  PfArgs t[kTrGroupMax];
+  int32_t first[kTrGroupMax + 1];
+  int32_t count;
+};
+
 // Y = Xc^T Wc for Xc [K][M] and Wc [K][N] (g.X, g.W), kept entries only
 // (pf_store_gather); M % 256 == 0, N % 128 == 0, K % kPfBK == 0.
 template <class T, int NW>
-__global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const PfArgs g) {
+__global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const TrGroupArg ga) {
+  const int ti = find_task(ga.first, ga.count);
+  const PfArgs& g = ga.t[ti];
   static_assert(!std::is_same<T, I8P>::value && NW == 8, "16-bit payloads, eight waves");
   using Acc = typename MfmaP<T>::acc_t;
   constexpr int FN = 4, FM = kDmaBM / (8 * NW);
@@ -874,7 +886,8 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const PfArg
   const int wn = wave & 1, wm = wave >> 1;
   const int64_t M = g.M, N = g.N, K = g.K;
   const int nst = (int)(K / kPfBK);
-  const int64_t n0 = (int64_t)blockIdx.x * kDmaBN, m0 = (int64_t)blockIdx.y * kDmaBM;
+  const int64_t b = (int64_t)blockIdx.x - ga.first[ti], tn = N / kDmaBN;
+  const int64_t n0 = (b % tn) * kDmaBN, m0 = (b / tn) * kDmaBM;
   // wave w requests rows 8 w .. 8 w + 7 of each operand's stage (bit 3 of the row: w % 2).
   // W run u: rows 8 w + 4 u + lane / 16, the lane's slot lane % 16 of the row;
   // X run u: rows 8 w + 2 u + lane / 32, slot lane % 32 (h depends on u % 2).
@@ -1195,15 +1208,25 @@ hipError_t dense_prefill_dma(const PfArgs& a, hipStream_t s) {
 }
 
 template <class T>
-hipError_t dense_prefill_tr(const PfArgs& a, hipStream_t s) {
+hipError_t dense_prefill_tr(const PfArgs* a, int count, hipStream_t s) {
   constexpr int NW = kDmaWaves;
   auto* kernel = k_dense_prefill_dma_tr<T, NW>;
   static PerDeviceFlag lds_set;
   const hipError_t attr = allow_lds_once(lds_set, kernel, kDmaStages * kDmaStageBytes);
   if (attr != hipSuccess) return attr;
-  const dim3 grid((unsigned)(a.N / kDmaBN), (unsigned)(a.M / kDmaBM)), block(64 * NW);
-  hipLaunchKernelGGL(kernel, grid, block, kDmaStages * kDmaStageBytes, s, a);
-  return hipGetLastError();
+  for (int c0 = 0; c0 < count; c0 += kTrGroupMax) {          // kTrGroupMax tasks per launch
+    TrGroupArg ga{};
+    ga.count = count - c0 < kTrGroupMax ? count - c0 : kTrGroupMax;
+    ga.first[0] = 0;
+    for (int i = 0; i < ga.count; ++i) {
+      ga.t[i] = a[c0 + i];
+      ga.first[i + 1] = ga.first[i] + (int32_t)((a[c0 + i].N / kDmaBN) * (a[c0 + i].M / kDmaBM));
+    }
+    hipLaunchKernelGGL(kernel, dim3((unsigned)ga.first[ga.count]), dim3(64 * NW), kDmaStages * kDmaStageBytes, s, ga);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <class T, bool kGather = false>
@@ -1260,15 +1283,20 @@ bool dense_prefill_tr_applies(int64_t M, int64_t N, int64_t K, const void* Xc, c
          (((uintptr_t)Xc | (uintptr_t)Wc) & 15) == 0;
 }
 
-hipError_t launch_dense_prefill_gather_tr(const void* Xc, int64_t M, const void* Wc, int32_t dtype, int64_t N,
-                                          int64_t K, const spl_matrix& P, void* values, hipStream_t s) {
-  if (P.rows != M || P.cols != N || !dense_prefill_tr_applies(M, N, K, Xc, Wc)) return hipErrorInvalidValue;
-  PfArgs a{};
-  a.X = static_cast<const uint16_t*>(Xc);
-  a.W = static_cast<const uint16_t*>(Wc);
-  a.M = M, a.N = N, a.K = K;
-  a.gbm = P.bitmask, a.gtoff = P.tile_offsets, a.gval = static_cast<uint16_t*>(values);
-  return dtype == SPL_BF16 ? dense_prefill_tr<Bf16>(a, s) : dense_prefill_tr<F16>(a, s);
+hipError_t launch_dense_prefill_gather_tr(const TrTask* tasks, int count, int32_t dtype, hipStream_t s) {
+  PfArgs a[SPL_MAX_GROUP];
+  if (count < 1 || count > SPL_MAX_GROUP) return hipErrorInvalidValue;
+  for (int i = 0; i < count; ++i) {
+    const TrTask& t = tasks[i];
+    if (t.P->rows != t.M || t.P->cols != t.N || !dense_prefill_tr_applies(t.M, t.N, t.K, t.Xc, t.Wc))
+      return hipErrorInvalidValue;
+    a[i] = PfArgs{};
+    a[i].X = static_cast<const uint16_t*>(t.Xc);
+    a[i].W = static_cast<const uint16_t*>(t.Wc);
+    a[i].M = t.M, a[i].N = t.N, a[i].K = t.K;
+    a[i].gbm = t.P->bitmask, a[i].gtoff = t.P->tile_offsets, a[i].gval = static_cast<uint16_t*>(t.values);
+  }
+  return dtype == SPL_BF16 ? dense_prefill_tr<Bf16>(a, count, s) : dense_prefill_tr<F16>(a, count, s);
 }
 
 // dX [M][K] = dY [M][N] (W.Mask) from W's packed tiles (W [N][K], tile layout).

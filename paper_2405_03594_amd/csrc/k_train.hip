@@ -3,12 +3,14 @@
 // update of the stored values.
 //
 // Weight gradient G = Mask . (dY^T X): both operands are [M][*] row-major and
-// the reduction runs over M, so dY and X are first transposed (LDS-tiled
-// copies) into [N][M] and [K][M]; the dense prefill kernel then computes
-// dY^T X as an M-deep product on the matrix cores (fp32 sums) and its
+// the reduction runs over M.  Where the shapes allow, the contraction-major
+// core of the prefill kernels reads dY and X as stored (LDS transpose reads);
+// otherwise they are first transposed into [N][M] and [K][M] (the workspace)
+// and a dense prefill kernel multiplies those.  Either way the product's
 // epilogue writes only the kept entries, rounded once to the payload type,
 // straight into the tile layout's value order: no dense [N][K] gradient is
-// formed, and the workspace holds only the two transposes.
+// formed.  The input gradient dX = dY (W.Mask) is read from W's own packed
+// tiles where the shapes allow, else from a decoded, transposed copy.
 //
 // k_gather_tiled (spl_gather_tiled) is the stand-alone form of that order:
 // lane (fr, fg) of a tile's wave owns row fr, columns 8 fg .. 8 fg + 7, and
@@ -135,7 +137,7 @@ __global__ void __launch_bounds__(256) k_permute_values(const uint16_t* __restri
   }
 }
 
-// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.
+// values[i] = RNE(values[i] - lr * grad[i]), each operation rounded to binary32.
 template <class T>
 __global__ void __launch_bounds__(256) k_sgd(uint16_t* __restrict__ values, const uint16_t* __restrict__ grad,
                                              int64_t nnz, float lr) {
@@ -179,8 +181,10 @@ hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const sp
                               void* ws, hipStream_t s) {
   const int64_t N = Wc.rows, K = Wc.cols;
   // dY [M][N] and X [M][K] are the contraction-major factors of dY^T X
-  if (dense_prefill_tr_applies(N, K, M, dY, X))
-    return launch_dense_prefill_gather_tr(dY, N, X, Wc.dtype, K, M, Wc, grad_values, s);
+  if (dense_prefill_tr_applies(N, K, M, dY, X)) {
+    const TrTask t{dY, X, N, K, M, &Wc, grad_values};
+    return launch_dense_prefill_gather_tr(&t, 1, Wc.dtype, s);
+  }
   unsigned char* base = static_cast<unsigned char*>(ws);
   void* dYt = base;                                  // [N][M]
   void* Xt = base + align256(2 * N * M);             // [K][M]
@@ -210,6 +214,30 @@ hipError_t launch_input_grad(const void* dY, int64_t M, const spl_matrix& W, voi
   if (e == hipSuccess) e = launch_transpose16(Wd, N, K, Wt, s);
   if (e == hipSuccess) e = launch_dense_prefill(dY, M, Wt, W.dtype, K, N, dX, s);   // dY Wt^T
   return e;
+}
+
+// Several weight gradients of one batch (one dtype): one grouped launch when
+// every task reads its factors as stored, else one call per task (the
+// workspace serving them in turn).
+hipError_t launch_weight_grad_group(const spl_weight_grad_task* tasks, int count, int64_t M, void* ws,
+                                    hipStream_t s) {
+  TrTask tr[SPL_MAX_GROUP];
+  int n = 0;
+  bool direct = true;
+  for (int i = 0; i < count; ++i) {
+    const spl_matrix& W = *tasks[i].W;
+    if (W.nnz == 0) continue;                        // no kept entry: nothing to write
+    if (!dense_prefill_tr_applies(W.rows, W.cols, M, tasks[i].dY, tasks[i].X)) direct = false;
+    tr[n++] = TrTask{tasks[i].dY, tasks[i].X, W.rows, W.cols, M, &W, tasks[i].grad_values};
+  }
+  if (n == 0) return hipSuccess;
+  if (direct) return launch_dense_prefill_gather_tr(tr, n, tasks[0].W->dtype, s);
+  for (int i = 0; i < count; ++i) {
+    if (tasks[i].W->nnz == 0) continue;
+    const hipError_t e = launch_weight_grad(tasks[i].dY, tasks[i].X, M, *tasks[i].W, tasks[i].grad_values, ws, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 int64_t transpose_perm_workspace_bytes(int64_t N, int64_t K, int64_t nnz) {

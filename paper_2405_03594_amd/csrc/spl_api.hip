@@ -378,6 +378,24 @@ spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, cons
   return launched(spl::launch_weight_grad(dY, X, M, *Wc, grad_values, workspace, stream));
 }
 
+spl_status spl_sparse_weight_grad_group(const spl_weight_grad_task* tasks, int32_t count, int64_t M,
+                                        void* workspace, hipStream_t stream) {
+  if (!tasks || count < 1 || count > SPL_MAX_GROUP) return SPL_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < count; ++i) {
+    const spl_weight_grad_task& t = tasks[i];
+    const spl_status st = check_tiled_fp(t.W);
+    if (st != SPL_OK) return st;
+    if (t.W->dtype != tasks[0].W->dtype) return SPL_ERR_INVALID_ARG;
+    if (M < 0 || !t.grad_values || !aligned(t.grad_values, 2)) return SPL_ERR_INVALID_ARG;
+    if (M == 0) return SPL_ERR_UNSUPPORTED;
+    if (!t.dY || !t.X || !workspace || !dims_ok(M, t.W->rows) || !dims_ok(M, t.W->cols)) return SPL_ERR_INVALID_ARG;
+    if (!aligned(t.dY, 2) || !aligned(t.X, 2) || !aligned(workspace, 256)) return SPL_ERR_INVALID_ARG;
+    if (M % 8 != 0 || t.W->cols % 8 != 0 || (M + 63) / 64 > 65535) return SPL_ERR_UNSUPPORTED;
+  }
+  (void)hipGetLastError();
+  return launched(spl::launch_weight_grad_group(tasks, count, M, workspace, stream));
+}
+
 int64_t spl_sparse_input_grad_workspace_bytes(int64_t M, const spl_matrix* Wc) {
   if (check_tiled_fp(Wc) != SPL_OK || M < 0) return -1;
   if (M > 0 && (!dims_ok(M, Wc->rows) || !dims_ok(M, Wc->cols))) return -1;

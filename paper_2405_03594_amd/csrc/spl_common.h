@@ -219,8 +219,16 @@ bool dense_prefill_tr_applies(int64_t M, int64_t N, int64_t K, const void* Xc, c
 // launch of at least one 128 x 256 block per CU; W in the tile layout, 16-bit).
 bool sparse_input_grad_applies(int64_t M, const spl_matrix& W);
 hipError_t launch_sparse_input_grad(const void* dY, int64_t M, const spl_matrix& W, void* dX, hipStream_t s);
-hipError_t launch_dense_prefill_gather_tr(const void* Xc, int64_t M, const void* Wc, int32_t dtype, int64_t N,
-                                          int64_t K, const spl_matrix& P, void* values, hipStream_t s);
+// A group of such products (one dtype; each where dense_prefill_tr_applies)
+// in as few launches as possible.
+struct TrTask {
+  const void* Xc;
+  const void* Wc;
+  int64_t M, N, K;
+  const spl_matrix* P;
+  void* values;
+};
+hipError_t launch_dense_prefill_gather_tr(const TrTask* tasks, int count, int32_t dtype, hipStream_t s);
 // Sparse-quantized kernels over a group of 1..SPL_MAX_GROUP validated tasks (one launch).
 hipError_t launch_sparse_int8(const spl_int8_task* tasks, int count, int64_t M, hipStream_t s);
 hipError_t launch_dense_int8(const spl_dense_int8_task* tasks, int count, int64_t M, hipStream_t s);
@@ -243,6 +251,8 @@ hipError_t launch_gather_tiled(const void* dense, const spl_matrix& P, void* val
 int64_t weight_grad_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_weight_grad(const void* dY, const void* X, int64_t M, const spl_matrix& Wc, void* grad_values,
                               void* ws, hipStream_t s);
+hipError_t launch_weight_grad_group(const spl_weight_grad_task* tasks, int count, int64_t M, void* ws,
+                                    hipStream_t s);
 hipError_t launch_sgd(const spl_matrix& Wc, const void* grad_values, float lr, hipStream_t s);
 int64_t input_grad_workspace_bytes(int64_t M, const spl_matrix& W);
 hipError_t launch_input_grad(const void* dY, int64_t M, const spl_matrix& W, void* dX, void* ws, hipStream_t s);

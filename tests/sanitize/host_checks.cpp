@@ -135,6 +135,11 @@ int main() {
     REJECTS(spl_quantize_rows_i8(X, 42, M, 64, const_cast<int8_t*>(q), const_cast<float*>(sc), nullptr));
     REJECTS(spl_sparse_weight_grad(X, X, M, &bad, Y, Y, nullptr));
     REJECTS(spl_sparse_input_grad(X, M, &bad, Y, Y, nullptr));
+    {
+      const spl_weight_grad_task wt[2] = {{X, X, &bad, Y}, {X, X, &rows, Y}};
+      REJECTS(spl_sparse_weight_grad_group(wt, 2, M, Y, nullptr));
+      REJECTS(spl_sparse_weight_grad_group(wt, 0, M, Y, nullptr));
+    }
     if (M != 0) REJECTS(spl_sparse_input_grad(X, M, &rows, Y, Y, nullptr));
     EXPECT(spl_sparse_input_grad_workspace_bytes(M, &bad) == -1);
     REJECTS(spl_dense_linear_ex(X, M, X, SPL_BF16, 64, 64, Y, 77, nullptr));

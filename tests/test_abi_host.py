@@ -387,6 +387,19 @@ def test_training_argument_checks(L):
     assert w(A, B, 16, ctypes.byref(m), G, ws + 16, None) == INVALID           # workspace alignment
     assert w(None, B, 16, ctypes.byref(m), G, ws, None) == INVALID
     assert w(A, B, 16, ctypes.byref(m), None, ws, None) == INVALID
+    from paper_2405_03594_amd import _WeightGradTask
+    gg = L.spl_sparse_weight_grad_group
+    task = lambda mm, dY=A, X=B, out=G: _WeightGradTask(dY, X, ctypes.pointer(mm), out)
+    two = (_WeightGradTask * 2)(task(m), task(m))
+    assert gg(two, 0, 16, ws, None) == INVALID and gg(None, 1, 16, ws, None) == INVALID
+    assert gg(two, 17, 16, ws, None) == INVALID                                # past SPL_MAX_GROUP
+    assert gg(two, 2, 0, ws, None) == UNSUPPORTED                              # no tokens
+    assert gg(two, 2, 12, ws, None) == UNSUPPORTED                             # M % 8 != 0
+    assert gg(two, 2, 16, ws + 16, None) == INVALID                            # workspace alignment
+    f16 = _mat(dtype=1, layout=1, tile_offsets=0x40000)
+    assert gg((_WeightGradTask * 2)(task(m), task(f16)), 2, 16, ws, None) == INVALID   # mixed dtypes
+    assert gg((_WeightGradTask * 2)(task(m), task(m, out=None)), 2, 16, ws, None) == INVALID
+    assert gg((_WeightGradTask * 1)(task(_mat())), 1, 16, ws, None) == UNSUPPORTED     # row layout
     ig, wb = L.spl_sparse_input_grad, L.spl_sparse_input_grad_workspace_bytes
     big = _mat(rows=4096, cols=4096, layout=1, tile_offsets=0x40000)
     assert wb(2048, ctypes.byref(big)) == 0                                    # W's tiles read in the product

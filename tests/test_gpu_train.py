@@ -131,6 +131,38 @@ def test_weight_grad_direct_path_and_fallback_agree(orc, spl):
     assert torch.equal(g_direct[:n].view(torch.int16), g_fallback[:n].view(torch.int16))
 
 
+def test_weight_grad_group_matches_single_calls(orc, spl):
+    """q, k, v (one X, three dY) at M = 256 and gate, up at M = 128, each
+    group in one call (one launch: every task reads its factors as stored):
+    the kept entries equal the single calls' bit for bit, and q's and gate's
+    equal the oracle within tolerance.  A group with a task the direct path
+    does not take (2000 x 4104) runs task by task and equals the single calls
+    too."""
+    import torch
+
+    def task(j, N, K, M, seed):
+        W, mask = synth.weight(seed, N, K, "bf16", 0.7)
+        Wc = spl.pack_sparse(to_dev(W, "bf16"), torch.from_numpy(mask).cuda())
+        dY = synth.activations(seed + 1, M, N, "bf16")
+        return W, mask, Wc, dY
+
+    for shapes, M in (([(4096, 4096)] * 3, 256), ([(11008, 4096)] * 2, 128), ([(2048, 4096), (2000, 4104)], 128)):
+        Ks = {K for _, K in shapes}
+        Xh = {K: synth.activations(690 + K, M, K, "bf16") for K in Ks}
+        Xd = {K: to_dev(Xh[K], "bf16") for K in Ks}
+        ts = [task(j, N, K, M, 700 + 10 * j + N) for j, (N, K) in enumerate(shapes)]
+        dYd = [to_dev(t[3], "bf16") for t in ts]
+        outs = spl.sparse_weight_grad_group(dYd, [Xd[K] for _, K in shapes], [t[2] for t in ts])
+        for i, ((N, K), t) in enumerate(zip(shapes, ts)):
+            single = spl.sparse_weight_grad(dYd[i], Xd[K], t[2])
+            n = t[2].nnz
+            assert torch.equal(outs[i][:n].view(torch.int16), single[:n].view(torch.int16)), (shapes, i)
+        W, mask, Wc, dY = ts[0]
+        G = from_dev_f64(spl.unpack(_with_values(spl, Wc, outs[0])))
+        ref = orc.weight_grad_f64(dY, Xh[shapes[0][1]], "bf16", orc.pack(W, "bf16", mask))
+        assert_close(G, ref, f"grouped weight grad {shapes[0]} M={M}")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_sgd_update(orc, spl, dtype):
     import torch

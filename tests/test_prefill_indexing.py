@@ -650,11 +650,21 @@ def _tr_lines():
                  "const u32x2 lo = lds_load_tr8(p), hi = lds_load_tr8(p + 4 * kTrRowB);",
                  "a[ks][i] = u32x4{lo.x, lo.y, hi.x, hi.y};",
                  "if (st + 2 < nst) request(st + 2, cur == 0 ? 2 : cur - 1);",
-                 "return pf_large_tile(N, M) && pf_inside(N, M, K, kDmaBN, kDmaBM) &&"):
+                 "return pf_large_tile(N, M) && pf_inside(N, M, K, kDmaBN, kDmaBM) &&",
+                 "const int ti = find_task(ga.first, ga.count);",
+                 "const int64_t b = (int64_t)blockIdx.x - ga.first[ti], tn = N / kDmaBN;",
+                 "const int64_t n0 = (b % tn) * kDmaBN, m0 = (b / tn) * kDmaBM;",
+                 "constexpr int kTrGroupMax = 4;",
+                 "ga.count = count - c0 < kTrGroupMax ? count - c0 : kTrGroupMax;",
+                 "ga.first[i + 1] = ga.first[i] + (int32_t)((a[c0 + i].N / kDmaBN) * (a[c0 + i].M / kDmaBM));",
+                 "hipLaunchKernelGGL(kernel, dim3((unsigned)ga.first[ga.count]), dim3(64 * NW), kDmaStages * "
+                 "kDmaStageBytes, s, ga);"):
         assert line in src, f"contraction-major core changed: update this replay ({line})"
     train = open(TRAIN_SRC).read()
-    for line in ("if (dense_prefill_tr_applies(N, K, M, dY, X))",
-                 "return launch_dense_prefill_gather_tr(dY, N, X, Wc.dtype, K, M, Wc, grad_values, s);"):
+    for line in ("if (dense_prefill_tr_applies(N, K, M, dY, X)) {",
+                 "const TrTask t{dY, X, N, K, M, &Wc, grad_values};",
+                 "if (!dense_prefill_tr_applies(W.rows, W.cols, M, tasks[i].dY, tasks[i].X)) direct = false;",
+                 "tr[n++] = TrTask{tasks[i].dY, tasks[i].X, W.rows, W.cols, M, &W, tasks[i].grad_values};"):
         assert line in train, f"weight gradient launch changed: update this replay ({line})"
     # (BN, BM, NW, FN, FM)
     return 128, 256, 8, 4, 4
@@ -857,3 +867,32 @@ def test_input_grad_expansion_and_transposed_reads(orc, N, K, s):
                                 want = [(bk * st + 32 * ks + 8 * (lane >> 4) + 4 * half + e,
                                          k0 + 64 * wn + 16 * i + (lane & 15)) for e in range(4)]
                                 assert got == want, (kb, st, wave, i, ks, half, lane)
+
+
+@pytest.mark.parametrize("shapes", [[(4096, 4096)] * 3, [(11008, 4096)] * 2, [(4096, 11008)], [(4096, 4096)] * 7,
+                                    [(256, 128), (512, 256), (2048, 384)]])
+def test_contraction_major_group_covers_every_block(shapes):
+    """A grouped launch of the weight gradient's core (task i: M_i x N_i
+    output in 256 x 128 blocks): launches of at most four tasks, workgroup x
+    finds its task as the last i with first[i] <= x (find_task) and its block
+    b = x - first[i] at n-block b % (N_i / 128), m-block b / (N_i / 128); every
+    block of every task is computed exactly once."""
+    _tr_lines()
+    seen = set()
+    for c0 in range(0, len(shapes), 4):
+        grp = shapes[c0:c0 + 4]
+        first = [0]
+        for (M, N) in grp:
+            first.append(first[-1] + (N // 128) * (M // 256))
+        for x in range(first[-1]):
+            ti = 0
+            for i in range(1, len(grp)):
+                ti = i if x >= first[i] else ti
+            M, N = grp[ti]
+            b, tn = x - first[ti], N // 128
+            n0, m0 = (b % tn) * 128, (b // tn) * 256
+            assert n0 + 128 <= N and m0 + 256 <= M
+            key = (c0 + ti, n0, m0)
+            assert key not in seen
+            seen.add(key)
+    assert len(seen) == sum((N // 128) * (M // 256) for (M, N) in shapes)
