@@ -452,18 +452,36 @@ def gather_tiled(W: torch.Tensor, pattern: SparseMatrix, out: torch.Tensor | Non
     return out
 
 
+def _wgrad_args(dY, X, Wc: SparseMatrix, out, M: int, name: str = "") -> None:
+    _arg(dY, "dY" + name, shape=(M, Wc.rows), dtype=Wc.dtype, device=False)
+    _arg(X, "X" + name, shape=(M, Wc.cols), dtype=Wc.dtype, device=False)
+    if out is not None:
+        _arg(out, "out" + name, dtype=Wc.dtype, min_numel=Wc.nnz, device=False)
+
+
+def _workspace(L, workspace, need: int, device) -> torch.Tensor:
+    if need < 0:
+        raise ValueError("the workspace-size function rejected the shape")
+    if workspace is None:
+        return torch.empty((max(need, 1),), dtype=torch.uint8, device=device)
+    _dev_tensor(workspace, "workspace")
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace holds {workspace.numel() * workspace.element_size()} bytes, needs {need}")
+    return workspace
+
+
 def sparse_weight_grad(dY: torch.Tensor, X: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | None = None,
                        workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Kept entries of dY^T X in Wc's value order (see spl_sparse_weight_grad)."""
     L = lib()
+    M = _rows_of(X, "X")
+    _wgrad_args(dY, X, Wc, out, M)
     _dev_tensor(dY, "dY")
     _dev_tensor(X, "X")
-    M = X.shape[0]
     if out is None:
         out = torch.empty_like(Wc.values)
-    if workspace is None:
-        workspace = torch.empty((L.spl_sparse_weight_grad_workspace_bytes(M, Wc.rows, Wc.cols),), dtype=torch.uint8,
-                                device=X.device)
+    _dev_tensor(out, "out")
+    workspace = _workspace(L, workspace, L.spl_sparse_weight_grad_workspace_bytes(M, Wc.rows, Wc.cols), X.device)
     view = Wc.view()
     _check("spl_sparse_weight_grad", L.spl_sparse_weight_grad(_ptr(dY), _ptr(X), M, ctypes.byref(view), _ptr(out),
                                                               _ptr(workspace), _stream(stream)))
@@ -477,17 +495,20 @@ def sparse_weight_grad_group(dYs, Xs, mats, outs=None, workspace: torch.Tensor |
     L = lib()
     if not (len(dYs) == len(Xs) == len(mats)) or not 1 <= len(mats) <= MAX_GROUP:
         raise ValueError("dYs, Xs and mats: one entry per task, 1..MAX_GROUP tasks")
-    M = Xs[0].shape[0]
-    for dY, X in zip(dYs, Xs):
-        _dev_tensor(dY, "dY")
-        _dev_tensor(X, "X")
-        if dY.shape[0] != M or X.shape[0] != M:
-            raise ValueError("every task has the same batch M")
+    if outs is not None and len(outs) != len(mats):
+        raise ValueError("outs: one entry per task")
+    M = _rows_of(Xs[0], "X")
+    for i, (dY, X, Wc) in enumerate(zip(dYs, Xs, mats)):
+        _wgrad_args(dY, X, Wc, outs[i] if outs is not None else None, M, f"[{i}]")
+    for i, (dY, X) in enumerate(zip(dYs, Xs)):
+        _dev_tensor(dY, f"dY[{i}]")
+        _dev_tensor(X, f"X[{i}]")
     if outs is None:
         outs = [torch.empty_like(Wc.values) for Wc in mats]
-    if workspace is None:
-        need = max(L.spl_sparse_weight_grad_workspace_bytes(M, Wc.rows, Wc.cols) for Wc in mats)
-        workspace = torch.empty((need,), dtype=torch.uint8, device=Xs[0].device)
+    for i, o in enumerate(outs):
+        _dev_tensor(o, f"out[{i}]")
+    need = max(L.spl_sparse_weight_grad_workspace_bytes(M, Wc.rows, Wc.cols) for Wc in mats)
+    workspace = _workspace(L, workspace, need, Xs[0].device)
     views = [Wc.view() for Wc in mats]
     tasks = (_WeightGradTask * len(mats))(*[
         _WeightGradTask(dY.data_ptr(), X.data_ptr(), ctypes.pointer(v), o.data_ptr())
@@ -503,16 +524,18 @@ def sparse_input_grad(dY: torch.Tensor, Wc: SparseMatrix, out: torch.Tensor | No
     L = lib()
     M = _rows_of(dY, "dY")
     _arg(dY, "dY", shape=(M, Wc.rows), dtype=Wc.dtype, device=False)
+    if out is not None:
+        _arg(out, "out", shape=(M, Wc.cols), dtype=Wc.dtype, device=False)
     _dev_tensor(dY, "dY")
     if out is None:
         out = torch.empty((M, Wc.cols), dtype=dY.dtype, device=dY.device)
-    _arg(out, "out", shape=(M, Wc.cols), dtype=Wc.dtype)
+    _dev_tensor(out, "out")
     view = Wc.view()
-    if workspace is None:
-        n = L.spl_sparse_input_grad_workspace_bytes(M, ctypes.byref(view))
-        if n < 0:
-            raise ValueError("spl_sparse_input_grad_workspace_bytes rejected the shape")
-        workspace = torch.empty((n,), dtype=torch.uint8, device=dY.device) if n > 0 else None
+    need = L.spl_sparse_input_grad_workspace_bytes(M, ctypes.byref(view))
+    if need < 0:
+        raise ValueError("spl_sparse_input_grad_workspace_bytes rejected the shape")
+    if need > 0 or workspace is not None:
+        workspace = _workspace(L, workspace, need, dY.device)
     _check("spl_sparse_input_grad", L.spl_sparse_input_grad(_ptr(dY), M, ctypes.byref(view), _ptr(out),
                                                             _ptr(workspace), _stream(stream)))
     return out

@@ -510,6 +510,22 @@ def test_wrappers_reject_mismatched_tensors_before_any_launch():
         (lambda: spl.dense_linear_int8(Xq, sx, torch.zeros((8, 64), dtype=torch.int8), sw[:4]), "w_scales"),
         (lambda: spl.quantize_rows_i8(X, scales=torch.zeros(1, dtype=torch.float32)), "scales"),
     ]
+    dY = torch.zeros((2, 8), dtype=torch.bfloat16)                      # Wc is [8][64]
+    Wn = _cpu_matrix()
+    Wn.nnz = 40
+    cases += [
+        (lambda: spl.sparse_weight_grad(torch.zeros((2, 9), dtype=torch.bfloat16), X, Wc), "shape"),
+        (lambda: spl.sparse_weight_grad(dY, torch.zeros((3, 64), dtype=torch.bfloat16), Wc), "shape"),
+        (lambda: spl.sparse_weight_grad(dY, X.half(), Wc), "dtype"),
+        (lambda: spl.sparse_weight_grad(dY, X, Wn, out=torch.zeros(39, dtype=torch.bfloat16)), "at least 40"),
+        (lambda: spl.sparse_weight_grad_group([dY, dY], [X, X], [Wc]), "one entry per task"),
+        (lambda: spl.sparse_weight_grad_group([dY], [torch.zeros((2, 63), dtype=torch.bfloat16)], [Wc]), "shape"),
+        (lambda: spl.sparse_weight_grad_group([dY], [X], [Wn], outs=[torch.zeros(8, dtype=torch.bfloat16)]),
+         "at least 40"),
+        (lambda: spl.sparse_input_grad(torch.zeros((2, 7), dtype=torch.bfloat16), Wc), "shape"),
+        (lambda: spl.sparse_input_grad(dY.half(), Wc), "dtype"),
+        (lambda: spl.sparse_input_grad(dY, Wc, out=torch.zeros((2, 63), dtype=torch.bfloat16)), "shape"),
+    ]
     for fn, what in cases:
         with pytest.raises(ValueError, match=what):
             fn()
