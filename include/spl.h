@@ -294,8 +294,9 @@ spl_status spl_sparse_weight_grad(const void* dY, const void* X, int64_t M, cons
  *   layers that share the batch M and the dtype (for example q, k and v, which
  *   share X), each task's output identical to spl_sparse_weight_grad's on the
  *   same arguments.  When every task takes the path that reads dY and X as
- *   stored, they run in one launch (so the blocks of all tasks share the
- *   chip's last partial round); otherwise one call per task, the workspace
+ *   stored, they run in one launch per four tasks (so the blocks of those
+ *   tasks share the chip's last partial round); otherwise one call per task,
+ *   the workspace
  *   (the largest spl_sparse_weight_grad_workspace_bytes of the tasks, 256-byte
  *   aligned) serving them in turn.  Tasks must not write overlapping outputs;
  *   the task array is read during the call only. */
