@@ -137,7 +137,7 @@ def test_weight_grad_group_matches_single_calls(orc, spl):
     the kept entries equal the single calls' bit for bit, and q's and gate's
     equal the oracle within tolerance.  A group with a task the direct path
     does not take (2000 x 4104) runs task by task and equals the single calls
-    too."""
+    too, and so does a group of five (two launches of the grouped core)."""
     import torch
 
     def task(j, N, K, M, seed):
@@ -146,7 +146,8 @@ def test_weight_grad_group_matches_single_calls(orc, spl):
         dY = synth.activations(seed + 1, M, N, "bf16")
         return W, mask, Wc, dY
 
-    for shapes, M in (([(4096, 4096)] * 3, 256), ([(11008, 4096)] * 2, 128), ([(2048, 4096), (2000, 4104)], 128)):
+    for shapes, M in (([(4096, 4096)] * 3, 256), ([(11008, 4096)] * 2, 128), ([(2048, 4096), (2000, 4104)], 128),
+                      ([(2048, 4096)] * 5, 64)):                     # five tasks: two launches (four, then one)
         Ks = {K for _, K in shapes}
         Xh = {K: synth.activations(690 + K, M, K, "bf16") for K in Ks}
         Xd = {K: to_dev(Xh[K], "bf16") for K in Ks}
