@@ -13,7 +13,9 @@ Names follow the C ABI without its ``spl_`` prefix:
 * ``sparse_linear_int8(Xq, x_scales, Wqc, w_scales)`` -> fp16 ``Y`` (section 3.4);
 * ``sparse_linear_group`` / ``dense_linear_group``: several independent
   linears (e.g. q, k, v) of one batch size in one launch;
-* ``unpack``, ``dense_linear``, ``dense_linear_int8``: decoder and dense comparators.
+* ``unpack``, ``dense_linear``, ``dense_linear_int8``: decoder and dense comparators;
+* ``sparse_weight_grad[_group]``, ``sparse_input_grad``, ``sparse_sgd_update``:
+  the training step with the mask held fixed (Algorithm 1).
 """
 from __future__ import annotations
 
