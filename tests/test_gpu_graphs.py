@@ -7,6 +7,8 @@ replayed three times; between replays the test fills every output with NaN
 replay must reproduce the eager results bit for bit (the same kernels on the
 same inputs are deterministic).  The library records no memset or copy nodes:
 zero fills are kernels."""
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -128,6 +130,73 @@ def test_graph_replays_new_ops_match_eager():
         mask.fill_(7)
         ws_m.fill_(0xAB)                               # the histogram must be cleared inside the graph
         ws_g.fill_(0xCD)
+
+    run()
+    torch.cuda.synchronize()
+    eager = snapshot()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    torch.cuda.synchronize()
+    scratch = torch.randn(1 << 20, device="cuda")
+    for rep in range(3):
+        poison()
+        scratch.mul_(1.0001).add_(0.5)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(snapshot(), eager)):
+            assert np.array_equal(a, b), f"replay {rep}, output {i} differs from the eager run"
+
+
+def test_graph_replays_training_kernels_match_eager():
+    """The training step's direct kernels in one captured graph - the grouped
+    weight gradient read straight from dY and X (two tasks, one launch) and
+    the input gradient from W's packed tiles - plus the input gradient's
+    decoded fallback: three replays with poisoned outputs and eager work in
+    between reproduce the eager results bit for bit."""
+    import torch
+
+    import paper_2405_03594_amd as spl
+
+    spl.lib()
+    M, N, K = 256, 2048, 8192                          # 64 x 8 and 64 x 8 blocks: each at least one per CU
+    Wa, ma = synth.weight(990, N, K, "bf16", 0.7)
+    Wb, mb = synth.weight(991, N, K, "bf16", 0.5)
+    A = spl.pack_sparse(to_dev(Wa, "bf16"), torch.from_numpy(ma).cuda())
+    Bm = spl.pack_sparse(to_dev(Wb, "bf16"), torch.from_numpy(mb).cuda())
+    X = to_dev(synth.activations(992, M, K, "bf16"), "bf16")
+    dYa = to_dev(synth.activations(993, M, N, "bf16"), "bf16")
+    dYb = to_dev(synth.activations(994, M, N, "bf16"), "bf16")
+    Ws, ms = synth.weight(995, 96, 200, "bf16", 0.6)   # the input gradient's fallback shape
+    S = spl.pack_sparse(to_dev(Ws, "bf16"), torch.from_numpy(ms).cuda())
+    dYs = to_dev(synth.activations(996, 40, 96, "bf16"), "bf16")
+    dYd = to_dev(synth.activations(997, 1024, N, "bf16"), "bf16")       # the input gradient: 64 x 4 blocks
+    assert spl.lib().spl_sparse_input_grad_workspace_bytes(1024, ctypes.byref(A.view())) == 0
+    ws_s = torch.empty((spl.lib().spl_sparse_input_grad_workspace_bytes(40, ctypes.byref(S.view())),),
+                       dtype=torch.uint8, device="cuda")
+    ga, gb = torch.empty_like(A.values), torch.empty_like(Bm.values)
+    dx = torch.empty((1024, K), dtype=torch.bfloat16, device="cuda")
+    dxs = torch.empty((40, 200), dtype=torch.bfloat16, device="cuda")
+
+    def run():
+        spl.sparse_weight_grad_group([dYa, dYb], [X, X], [A, Bm], outs=[ga, gb])
+        spl.sparse_input_grad(dYd, A, out=dx)
+        spl.sparse_input_grad(dYs, S, out=dxs, workspace=ws_s)
+
+    def snapshot():
+        return [from_dev_bits(ga)[:A.nnz], from_dev_bits(gb)[:Bm.nnz], from_dev_bits(dx), from_dev_bits(dxs)]
+
+    def poison():
+        for o in (ga, gb, dx, dxs):
+            o.fill_(float("nan"))
+        ws_s.fill_(0xCD)
 
     run()
     torch.cuda.synchronize()
