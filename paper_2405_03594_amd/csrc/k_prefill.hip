@@ -381,6 +381,65 @@ __device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], cons
   }
 }
 
+// The same epilogue through LDS, for a kernel whose LDS is free at its end:
+// the wave writes its tiles' kept entries into its own region (FM runs of
+// 1024 16-bit slots) in value order - the two tiles (j, 0) and (j, 1) are
+// consecutive in the pattern, so their values are one run - then stores each
+// run with coalesced 2-byte stores (64 consecutive entries per store) instead
+// of one predicated scattered store per entry.  bf16 values are rounded by
+// the hardware conversion (round to nearest even, as T::from_f32 for finite
+// values).
+template <class T, int FN, int FM>
+__device__ __forceinline__ void pf_store_gather_lds(const f32x4 (&acc)[FN][FM], const GatherMeta<FN, FM>& gm,
+                                                    const PfArgs& g, int lane, uint16_t* __restrict__ run) {
+  static_assert(FN == 4, "two tiles per m-fragment: one run of at most 1024 entries");
+  const int q = lane >> 4;
+  uint32_t len[FM];
+#pragma unroll
+  for (int j = 0; j < FM; ++j) {
+    uint32_t n = 0;                                            // entries of the run so far (wave-uniform)
+#pragma unroll
+    for (int p = 0; p < FN / 2; ++p) {
+      const uint32_t w = gm.w[j][p];
+      const uint32_t c = __popc(w & 0xffu) | (__popc((w >> 8) & 0xffu) << 8) | (__popc((w >> 16) & 0xffu) << 16) |
+                         (__popc(w >> 24) << 24);
+      const uint32_t incl = row16_inclusive_scan(c);
+      const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 15);
+      const uint32_t above = incl - c;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int col = 16 * h + 4 * q;
+        const int f = col >> 3;
+        uint32_t idx = n + __builtin_amdgcn_ubfe(above, 8 * f, 8);   // within the run
+        if (f > 0) idx += tot & 0xffu;
+        if (f > 1) idx += (tot >> 8) & 0xffu;
+        if (f > 2) idx += (tot >> 16) & 0xffu;
+        if (col & 4) idx += __popc(__builtin_amdgcn_ubfe(w, 8 * f, 4));
+        const uint32_t nib = __builtin_amdgcn_ubfe(w, col, 4);
+        uint16_t v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if constexpr (std::is_same<T, Bf16>::value)
+            v[r] = __builtin_bit_cast(uint16_t, (__bf16)acc[2 * p + h][j][r]);
+          else
+            v[r] = T::from_f32(acc[2 * p + h][j][r]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if ((nib >> r) & 1u) run[1024 * j + idx++] = v[r];
+      }
+      n += (tot & 0xffu) + ((tot >> 8) & 0xffu) + ((tot >> 16) & 0xffu) + (tot >> 24);
+    }
+    len[j] = n;
+  }
+  // the wave's LDS operations complete in order: its stores above precede these reads
+#pragma unroll
+  for (int j = 0; j < FM; ++j) {
+    const uint32_t base0 = (uint32_t)__builtin_amdgcn_readlane((int)gm.off, j * (FN / 2));
+    for (uint32_t i = (uint32_t)lane; i < len[j]; i += 64) g.gval[base0 + i] = run[1024 * j + i];
+  }
+}
+
 template <class T, int FN, int FM>
 __device__ __forceinline__ void pf_store_gather(const f32x4 (&acc)[FN][FM], const PfArgs& g, int64_t n0, int64_t m0,
                                                 int wn, int wm, int lane) {
@@ -937,7 +996,9 @@ __global__ void __launch_bounds__(64 * NW, 1) k_dense_prefill_dma_tr(const TrGro
     pf_mfma_stage_tr<T, FN, FM>(acc, lds_off(dsm + cur * kDmaStageBytes), ao, bo);
     cur = cur == kDmaStages - 1 ? 0 : cur + 1;
   }
-  pf_store_gather<T, FN, FM>(acc, gm, g, lane);
+  static_assert(2 * 1024 * FM * NW <= kDmaStages * kDmaStageBytes, "the waves' value runs fit the stage buffers");
+  __syncthreads();                                   // every wave is done reading the stage buffers
+  pf_store_gather_lds<T, FN, FM>(acc, gm, g, lane, reinterpret_cast<uint16_t*>(dsm) + 1024 * FM * wave);
 }
 
 // One stage of MFMA work with the A operand read by LDS transpose reads from

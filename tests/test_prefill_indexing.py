@@ -388,6 +388,12 @@ def _gather_lines():
                  "gm.off = okl ? (uint32_t)g.gtoff[(b0 + jl) * S + s0 + pl] : 0u;",
                  "const uint32_t w = gm.w[j][p];",
                  "const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)gm.off, j * (FN / 2) + p);",
+                 "uint32_t idx = n + __builtin_amdgcn_ubfe(above, 8 * f, 8);   // within the run",
+                 "if ((nib >> r) & 1u) run[1024 * j + idx++] = v[r];",
+                 "n += (tot & 0xffu) + ((tot >> 8) & 0xffu) + ((tot >> 16) & 0xffu) + (tot >> 24);",
+                 "const uint32_t base0 = (uint32_t)__builtin_amdgcn_readlane((int)gm.off, j * (FN / 2));",
+                 "for (uint32_t i = (uint32_t)lane; i < len[j]; i += 64) g.gval[base0 + i] = run[1024 * j + i];",
+                 "pf_store_gather_lds<T, FN, FM>(acc, gm, g, lane, reinterpret_cast<uint16_t*>(dsm) + 1024 * FM * wave);",
                  "const uint32_t incl = row16_inclusive_scan(c);",
                  "const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 15);",
                  "const uint32_t above = incl - c;",
@@ -424,6 +430,7 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
         FN, FM = BN // 32, BM // (8 * NW)
         out = np.zeros(T.nnz, np.uint16)
         hits = np.zeros(T.nnz, np.int64)
+        runs, run_info = {}, {}
         for gx in range(-(-C // BN)):                 # product columns = pattern columns
             for gy in range(-(-R // BM)):             # product rows = pattern rows
                 n0, m0 = gx * BN, gy * BM
@@ -445,6 +452,10 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
                             assert j * (FN // 2) + p < 64
                             base = off[j * (FN // 2) + p]
                             assert not ok or base == int(offs[t])
+                            key = (gx, gy, wave, j)
+                            runs.setdefault(key, [])
+                            rb0, ln = run_info.get(key, (off[j * (FN // 2)], 0))
+                            run_info[key] = (rb0, ln + sum(_popc(wd) for wd in words))
                             c = [sum(_popc((w >> (8 * f)) & 0xFF) << (8 * f) for f in range(4)) for w in words]
                             incl = np.cumsum(c)
                             assert all(((int(x) >> (8 * f)) & 0xFF) <= 128 for x in incl for f in range(4))
@@ -467,9 +478,17 @@ def test_gather_epilogue_writes_the_value_order(orc, R, C, s):
                                             assert row < R and k < C
                                             out[idx] = G[row, k]
                                             hits[idx] += 1
+                                            runs[key].append(idx)
                                             idx += 1
         assert (hits == 1).all(), (BN, "value index written other than once")
         assert np.array_equal(out, want), BN
+        if (BN, BM, NW) == (128, 256, 8):
+            # the LDS-staged form (the weight gradient's core): tiles (j, 0) and (j, 1) of a wave are one run
+            # of nnz(j, 0) + nnz(j, 1) entries from tile (j, 0)'s offset, each slot < 1024 written once
+            for key, idxs in runs.items():
+                base0, length = run_info[key]
+                assert length <= 1024
+                assert sorted(i - base0 for i in idxs) == list(range(length)), key
 
 
 # ---------------------------------------------------------------- direct-to-LDS staging of the dense core
