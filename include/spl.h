@@ -392,7 +392,8 @@ spl_status spl_sparse_linear_int8_expanded(const int8_t* Xq, const float* x_scal
  *   The view of the result is W8's with dtype SPL_I4 and values = values4.
  * spl_sparse_linear_int4: as spl_sparse_linear_int8 (exact int32 sums, the
  *   same fp16 epilogue) for a SPL_I4 tile-layout view, decode batches
- *   0 <= M <= 16 (SPL_ERR_UNSUPPORTED above), K % 16 == 0. */
+ *   0 <= M <= 16 (SPL_ERR_UNSUPPORTED above), K % 16 == 0; M * K < 2^31
+ *   and ceil(K / 32) < 2^25 (SPL_ERR_UNSUPPORTED otherwise). */
 int64_t spl_int4_values_bytes(int64_t nnz);
 spl_status spl_pack_int4(const spl_matrix* W8, uint8_t* values4, int32_t* bad_codes, hipStream_t stream);
 spl_status spl_sparse_linear_int4(const int8_t* Xq, const float* x_scales, int64_t M, const spl_matrix* W4,

@@ -19,6 +19,9 @@
 // a 16-entry selector table (v_perm_b32) places them, zeros where the bitmask
 // is clear.  Activation rows
 // are read directly (16 bytes per lane), int32 partial sums added in LDS.
+// Each wave pipelines its pairs so that no global load is waited for in the
+// pair that issues it: pattern words and tile offsets two pairs ahead, nibble
+// dwords and activations one pair ahead.
 #include "spl_common.h"
 
 namespace spl {
@@ -69,7 +72,8 @@ template <int W>
 __global__ void __launch_bounds__(W * 64) k_sparse_i4(const I4Args g) {
   __shared__ i32x4 part[W][64];
   __shared__ uint32_t sel4[16];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, fr = lane & 15, fg = lane >> 4;
   if (threadIdx.x < 16) sel4[threadIdx.x] = nibble_selector8(threadIdx.x);
   __syncthreads();
   const int64_t b = blockIdx.x;
@@ -79,40 +83,92 @@ __global__ void __launch_bounds__(W * 64) k_sparse_i4(const I4Args g) {
   const int pb = wave * L < P ? wave * L : P;
   const int pe = pb + L < P ? pb + L : P;
   const bool xlive = fr < g.M;
-  const int8_t* xrow = g.Xq + (int64_t)(xlive ? fr : 0) * g.K;
-  i32x4 acc = i32x4{0, 0, 0, 0};
-  for (int p = pb; p < pe; ++p) {
-    const int s = 2 * p + (fg >> 1), h = fg & 1;
-    uint32_t hw = 0u, base = 0u;
-    if (s < S) {
-      const int64_t t = b * S + s;
-      hw = (g.bm[t * 16 + fr] >> (16 * h)) & 0xffffu;
-      base = (uint32_t)g.toff[t];
-    }
-    const uint32_t cnt = __popc(hw);
-    const uint32_t off = base + half_inclusive_scan(cnt) - cnt;   // nibble index of my first value
+  // Software pipeline over tile pairs: the pattern word and tile offset of
+  // pair p + 2, the nibble dwords and activation row of pair p + 1 are in
+  // flight while pair p is expanded and multiplied (the nibble addresses need
+  // the scan of that pair's counts, so they are issued one pair behind the
+  // pattern loads).
+  // Every load is issued unconditionally (raw buffer loads: an offset past a
+  // buffer's size returns zeros), so each pair issues the same loads and the
+  // waits before its MFMA cover only the loads of earlier pairs.
+  struct Meta {
+    uint32_t w, base;   // my tile row's bitmask word (both halves), the tile's first value
+  };
+  struct Vals {
+    uint32_t hw, d0, d1, d2, sh;
+  };
+  const int h = fg & 1;
+  // this row block's words and tile offsets; tiles past S (odd S) and pairs past the range read zeros
+  const __amdgpu_buffer_rsrc_t bm_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(g.bm + b * S * 16), (short)0, 64 * S, 0x00020000);
+  const __amdgpu_buffer_rsrc_t to_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(g.toff + b * S), (short)0, 4 * S, 0x00020000);
+  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int8_t*>(g.Xq), (short)0, (int)(g.M * g.K), 0x00020000);
+  constexpr uint32_t kOob = 0x80000000u;             // past every buffer above (the host bounds them)
+  auto load_meta = [&](int p) {
+    const uint32_t s = (uint32_t)(2 * p + (fg >> 1));
+    const bool ok = p < pe;
+    Meta m;
+    m.w = __builtin_amdgcn_raw_buffer_load_b32(bm_rsrc, ok ? 4u * (16u * s + (uint32_t)fr) : kOob, 0, 0);
+    m.base = __builtin_amdgcn_raw_buffer_load_b32(to_rsrc, ok ? 4u * s : kOob, 0, 0);
+    return m;
+  };
+  // needs every lane (the half-wave scan); the loads are unconditional: a lane
+  // with no kept value reads the dwords at its offset, which lie inside the
+  // values buffer (off <= nnz, and nnz / 2 + 16 bytes are readable)
+  auto load_vals = [&](const Meta& m) {
+    Vals v;
+    v.hw = (m.w >> (16 * h)) & 0xffffu;
+    const uint32_t cnt = __popc(v.hw);
+    const uint32_t off = m.base + half_inclusive_scan(cnt) - cnt;   // nibble index of my first value
+    const uint32_t byte0 = off >> 1;
+    const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));
+    v.d0 = d[0];
+    v.d1 = d[1];
+    v.d2 = d[2];
+    v.sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;       // 0 .. 28
+    return v;
+  };
+  auto load_x = [&](int p) {
+    const uint32_t k0 = 64u * (uint32_t)p + 16u * (uint32_t)fg;
+    const bool ok = p < pe && xlive && (int64_t)k0 < g.K;                             // K % 16 == 0
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                         x_rsrc, ok ? (uint32_t)fr * (uint32_t)g.K + k0 : kOob, 0, 0));
+  };
+  auto mul = [&](const Vals& v, const u32x4& x, i32x4& acc) {
     u32x4 a = u32x4{0u, 0u, 0u, 0u};
-    if (hw != 0u) {                                  // off + cnt <= nnz: bytes read < nnz / 2 + 12
-      const uint32_t byte0 = off >> 1;
-      const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));
-      const uint32_t d0 = d[0], d1 = d[1], d2 = d[2];
-      const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;   // 0 .. 28
-      const uint32_t lo = __builtin_amdgcn_alignbit(d1, d0, sh);    // nibbles off .. off + 7
-      const uint32_t hi = __builtin_amdgcn_alignbit(d2, d1, sh);    // nibbles off + 8 .. off + 15
+    if (v.hw != 0u) {
+      const uint32_t lo = __builtin_amdgcn_alignbit(v.d1, v.d0, v.sh);   // nibbles off .. off + 7
+      const uint32_t hi = __builtin_amdgcn_alignbit(v.d2, v.d1, v.sh);   // nibbles off + 8 .. off + 15
       const uint64_t nibs = ((uint64_t)hi << 32) | lo;
       uint32_t rank = 0u;                            // values before this 4-column nibble
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t m4 = (hw >> (4 * q)) & 0xFu;
+        const uint32_t m4 = (v.hw >> (4 * q)) & 0xFu;
         const uint32_t y = i4_widen((uint32_t)(nibs >> (4u * rank)) & 0xFFFFu);   // ranks rank .. rank + 3
         a[q] = __builtin_amdgcn_perm(0u, y, sel4[m4]);
         rank += __popc(m4);
       }
     }
-    u32x4 xb = u32x4{0u, 0u, 0u, 0u};
-    const int64_t k0 = 64 * (int64_t)p + 16 * fg;
-    if (xlive && k0 < g.K) xb = *reinterpret_cast<const u32x4*>(xrow + k0);   // K % 16 == 0
-    acc = mfma_i8_i4(a, xb, acc);
+    acc = mfma_i8_i4(a, x, acc);
+  };
+  // two pairs per iteration with the roles of the register sets swapped, so
+  // that no loaded register is copied (a copy would wait for its load); a pair
+  // past the range has zero words and activations and adds nothing
+  i32x4 acc = i32x4{0, 0, 0, 0};
+  Meta m1 = load_meta(pb + 1);
+  Vals v0 = load_vals(load_meta(pb));
+  u32x4 x0 = load_x(pb);
+  for (int p = pb; p < pe; p += 2) {
+    const Meta m2 = load_meta(p + 2);
+    const Vals v1 = load_vals(m1);
+    const u32x4 x1 = load_x(p + 1);
+    mul(v0, x0, acc);
+    m1 = load_meta(p + 3);
+    v0 = load_vals(m2);
+    x0 = load_x(p + 2);
+    mul(v1, x1, acc);
   }
   part[wave][lane] = acc;
   __syncthreads();
@@ -148,6 +204,8 @@ hipError_t launch_pack_nibbles(const int8_t* v8, int64_t nnz, uint8_t* v4, int32
 
 hipError_t launch_sparse_int4(const int8_t* Xq, const float* sx, int64_t M, const spl_matrix& W4, const float* sw,
                               void* Y, int32_t* acc_out, hipStream_t s) {
+  // the kernel addresses X, a row block's words and its tile offsets with 32-bit buffer offsets
+  if (M * W4.cols >= (int64_t)1 << 31 || tile_steps(W4.cols) >= (int64_t)1 << 25) return hipErrorNotSupported;
   I4Args g{Xq, sx, W4.bitmask, static_cast<const uint8_t*>(W4.values), W4.tile_offsets, sw,
            static_cast<uint16_t*>(Y), acc_out, W4.rows, W4.cols, (int32_t)M};
   const int64_t blocks = tile_blocks(W4.rows);

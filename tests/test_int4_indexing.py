@@ -48,11 +48,22 @@ def _values_bytes(nnz):
 @pytest.mark.parametrize("N,K,s", [(1, 16, 0.5), (17, 48, 0.7), (40, 96, 0.0), (33, 208, 0.9), (16, 64, 1.0)])
 def test_int4_schedule_reads_and_operands(orc, N, K, s, waves, gen):
     src = open(SRC).read()
-    for line in ("const int s = 2 * p + (fg >> 1), h = fg & 1;",
-                 "hw = (g.bm[t * 16 + fr] >> (16 * h)) & 0xffffu;",
-                 "const uint32_t off = base + half_inclusive_scan(cnt) - cnt;",
+    for line in ("const uint32_t s = (uint32_t)(2 * p + (fg >> 1));",
+                 "const bool ok = p < pe;",
+                 "const_cast<uint32_t*>(g.bm + b * S * 16), (short)0, 64 * S, 0x00020000);",
+                 "const_cast<int32_t*>(g.toff + b * S), (short)0, 4 * S, 0x00020000);",
+                 "m.w = __builtin_amdgcn_raw_buffer_load_b32(bm_rsrc, ok ? 4u * (16u * s + (uint32_t)fr) : kOob, 0, 0);",
+                 "m.base = __builtin_amdgcn_raw_buffer_load_b32(to_rsrc, ok ? 4u * s : kOob, 0, 0);",
+                 "v.hw = (m.w >> (16 * h)) & 0xffffu;",
+                 "const uint32_t off = m.base + half_inclusive_scan(cnt) - cnt;   // nibble index of my first value",
                  "const uint32_t* d = reinterpret_cast<const uint32_t*>(g.v4 + (byte0 & ~3u));",
-                 "const uint32_t sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;",
+                 "v.sh = (byte0 & 3u) * 8u + (off & 1u) * 4u;",
+                 "const bool ok = p < pe && xlive && (int64_t)k0 < g.K;",
+                 "x_rsrc, ok ? (uint32_t)fr * (uint32_t)g.K + k0 : kOob, 0, 0));",
+                 "Meta m1 = load_meta(pb + 1);",
+                 "const Meta m2 = load_meta(p + 2);",
+                 "m1 = load_meta(p + 3);",
+                 "for (int p = pb; p < pe; p += 2) {",
                  "const int L = (P + W - 1) / W;",
                  "const uint32_t y = i4_widen((uint32_t)(nibs >> (4u * rank)) & 0xFFFFu);   // ranks rank .. rank + 3",
                  "a[q] = __builtin_amdgcn_perm(0u, y, sel4[m4]);",
@@ -74,13 +85,19 @@ def test_int4_schedule_reads_and_operands(orc, N, K, s, waves, gen):
         for w in range(waves):
             pb = min(w * L, P)
             pe = min(pb + L, P)
-            for p in range(pb, pe):
+            # every pair whose pattern the pipeline loads: two pairs per
+            # iteration, pattern loads up to p + 3; a pair past the range
+            # (or a tile past S) reads zeros through the buffer bounds
+            last = pb + 2 * ((pe - pb + 1) // 2) + 1 if pe > pb else pb + 1
+            for p in range(pb, last + 1):
+                ok = p < pe
                 hw = np.zeros(64, np.int64)
                 base = np.zeros(64, np.int64)
                 for lane in range(64):
                     fr, fg = lane & 15, lane >> 4
                     sk, h = 2 * p + (fg >> 1), fg & 1
-                    if sk < S:
+                    if ok and 4 * (16 * sk + fr) < 64 * S:
+                        assert 4 * sk < 4 * S
                         t = b * S + sk
                         hw[lane] = (int(T.bitmask[t * 16 + fr]) >> (16 * h)) & 0xFFFF
                         base[lane] = int(T.tile_offsets[t])
@@ -89,13 +106,15 @@ def test_int4_schedule_reads_and_operands(orc, N, K, s, waves, gen):
                     seg = slice(32 * half, 32 * half + 32)
                     excl = np.cumsum(cnt[seg]) - cnt[seg]
                     for i, lane in enumerate(range(32 * half, 32 * half + 32)):
-                        if hw[lane] == 0:
-                            continue
+                        # every lane reads its three dwords, kept values or not
                         off = int(base[lane] + excl[i])
                         assert off + cnt[lane] <= nnz
                         byte0 = off >> 1
                         first = (byte0 & ~3) // 4
                         assert 0 <= first and (first + 3) * 4 <= packed.size, (b, w, p, lane)
+                        if hw[lane] == 0:
+                            continue
+                        assert ok
                         d0, d1, d2 = (int(x) for x in words[first:first + 3])
                         sh = (byte0 & 3) * 8 + (off & 1) * 4
                         lo = ((d1 << 32 | d0) >> sh) & 0xFFFFFFFF
