@@ -396,10 +396,23 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
   // loads complete in issue order, and the chunk's addresses wait on them), then the shared tables
   int32_t orng = 0;
   Chunk ch{0, 0u, 0};
+  // direct path: a chunk's activations are loaded with its values (every
+  // tile of the chunk unconditionally: a k-step past the chunk reads in-range
+  // X or, past the buffer, zeros, and is not used), so that their latency
+  // overlaps the previous chunk's products
+  u32x4 xn[XL ? 1 : C][MT];
+  auto load_x_chunk = [&](int c) {
+    if constexpr (!XL) {
+      const XGlobal<MT> xg(tk.X, M, K, fr, fg);
+#pragma unroll
+      for (int j = 0; j < C; ++j) xg.load(xn[j], c + j, c + j == S - 1 && (K & 31) != 0, fg, K);
+    }
+  };
   if (kbeg < kend) {
     orng = load_offsets(ob);
     ch = shape(orng, kbeg);
     issue(ch, kbeg);
+    load_x_chunk(kbeg);
   }
   XStager<W> xst;
   if constexpr (XL) xst.load(tk.X, M, K);
@@ -413,6 +426,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
     if constexpr (XL) return XShared(xs, xzero, M, K, fr, fg);
     else return XGlobal<MT>(tk.X, M, K, fr, fg);
   }();
+
   const uint32_t lut_addr = lds_off(lut);
   const uint32_t vbuf_addr = lds_off(vbuf);
   u32x4 xlive = u32x4{0u, 0u, 0u, 0u};
@@ -433,12 +447,13 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
 #pragma unroll
     for (int j = 0; j < C; ++j) tc[j] = __builtin_amdgcn_readlane(orng, c0 - ob + j);
 
-    // 2. the current chunk's activations (direct path), then the next chunk's loads
+    // 2. the current chunk's activations (direct path), then the next chunk's loads and activations
     u32x4 xb[XL ? 1 : C][MT];
     if constexpr (!XL) {
 #pragma unroll
       for (int j = 0; j < C; ++j)
-        if (j < cur.cn) xop.load(xb[j], c0 + j, c0 + j == S - 1 && (K & 31) != 0, fg, K);
+#pragma unroll
+        for (int t = 0; t < MT; ++t) xb[j][t] = xn[j][t];
     }
     const int c1 = c0 + cur.cn;
     if (c1 < kend) {
@@ -448,6 +463,7 @@ __global__ void __launch_bounds__(W * kWave, XL ? 8 : 4) k_sparse_decode(const S
       }
       ch = shape(orng, c1);
       issue(ch, c1);
+      load_x_chunk(c1);
     }
 
     // 3. expand and multiply the current chunk, two tiles at a time
